@@ -1,0 +1,529 @@
+/*
+ * oracle.c -- plain CPU oracle for budgeted weight-space merging.
+ *
+ * TEST INFRASTRUCTURE ONLY: loaded by the tests, the smoke check and the
+ * benchmark's CPU-baseline leg, never by the product path.  It shares no
+ * code with the GPU library.  Each function follows the paper's definition
+ * in the paper's order, plainly; readings of points the paper leaves open
+ * are stated where they are used.
+ *
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fopenmp -shared -fPIC
+ * (no fast-math: every rounding below is the IEEE-754 one written).
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------ */
+/* element access                                                      */
+/* ------------------------------------------------------------------ */
+
+static int elem_bytes(int32_t dtype) { return dtype == 0 ? 4 : (dtype == 1 ? 2 : 0); }
+
+static float bf16_to_f32(uint16_t h)
+{
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+/* Round-to-nearest-even from fp32 to bfloat16 (inputs are finite). */
+static uint16_t f32_to_bf16(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u) /* inf / nan: keep, quiet nan */
+        return (uint16_t)((u >> 16) | ((u & 0x007fffffu) ? 0x40u : 0u));
+    uint32_t lsb = (u >> 16) & 1u;
+    u += 0x7fffu + lsb;
+    return (uint16_t)(u >> 16);
+}
+
+static float load(const void* p, int32_t dtype, int64_t j)
+{
+    if (dtype == 0)
+        return ((const float*)p)[j];
+    return bf16_to_f32(((const uint16_t*)p)[j]);
+}
+
+static void store(void* p, int32_t dtype, int64_t j, float v)
+{
+    if (dtype == 0)
+        ((float*)p)[j] = v;
+    else
+        ((uint16_t*)p)[j] = f32_to_bf16(v);
+}
+
+void orc_round_bf16(const float* x, uint16_t* y, int64_t n)
+{
+    for (int64_t j = 0; j < n; ++j)
+        y[j] = f32_to_bf16(x[j]);
+}
+
+int orc_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------ */
+/* Section 2: the tensor set and its deterministic blocks.             */
+/* Reading: each tensor is flattened row-major and cut into            */
+/* consecutive blocks of block_elems elements; the last block of a     */
+/* tensor may be shorter; blocks never cross tensors; blocks are       */
+/* numbered in tensor order.  (Prop. 2 assumes such a disjoint          */
+/* partition of the parameter vector.)                                 */
+/* ------------------------------------------------------------------ */
+
+int64_t orc_num_blocks(int32_t n_tensors, const int64_t* numel, int64_t block_elems)
+{
+    if (n_tensors < 0 || block_elems <= 0)
+        return -1;
+    int64_t G = 0;
+    for (int32_t t = 0; t < n_tensors; ++t) {
+        if (numel[t] < 0)
+            return -1;
+        G += (numel[t] + block_elems - 1) / block_elems;
+    }
+    return G;
+}
+
+int orc_blocks(int32_t n_tensors, const int64_t* numel, int64_t block_elems,
+               int64_t* off, int64_t* len, int32_t* tensor, int64_t* elem0)
+{
+    if (orc_num_blocks(n_tensors, numel, block_elems) < 0)
+        return -1;
+    int64_t g = 0, start = 0;
+    for (int32_t t = 0; t < n_tensors; ++t) {
+        for (int64_t e = 0; e < numel[t]; e += block_elems) {
+            int64_t n = numel[t] - e;
+            if (n > block_elems)
+                n = block_elems;
+            off[g] = start + e;
+            len[g] = n;
+            tensor[g] = t;
+            elem0[g] = e;
+            ++g;
+        }
+        start += numel[t];
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Catalog statistic (Section 2 and Section 3 "Catalog"): the squared   */
+/* L2 norm of each expert delta block, Delta = M_i - M_0.              */
+/* Reading of the summation order (the paper leaves it open; a fixed   */
+/* order is what makes plans reproducible bit for bit): with V = 16 /   */
+/* (bytes per element) elements per 16-byte chunk, 64 partial sums p_l; */
+/* partial l takes chunks l, l+64, l+128, ... in turn, elements of a    */
+/* chunk in order, p_l = fma(d, d, p_l) from +0; then for              */
+/* s = 32,16,8,4,2,1 every p_l becomes p_l + p_(l xor s); the result   */
+/* is p_0.  Deltas are fp32: d = float(x_i) - float(x_0).              */
+/* ------------------------------------------------------------------ */
+
+static float block_sumsq(const void* base, const void* ex, int32_t dtype, int64_t doff, int64_t n)
+{
+    const int V = 16 / elem_bytes(dtype);
+    float p[64], q[64];
+    for (int l = 0; l < 64; ++l)
+        p[l] = 0.0f;
+    int64_t R = (n + 64 * V - 1) / (64 * V);
+    for (int l = 0; l < 64; ++l) {
+        for (int64_t r = 0; r < R; ++r) {
+            for (int e = 0; e < V; ++e) {
+                int64_t j = (r * 64 + l) * V + e;
+                if (j >= n)
+                    continue;
+                float d = load(ex, dtype, doff + j) - load(base, dtype, doff + j);
+                p[l] = fmaf(d, d, p[l]);
+            }
+        }
+    }
+    for (int s = 32; s >= 1; s >>= 1) {
+        for (int l = 0; l < 64; ++l)
+            q[l] = p[l] + p[l ^ s];
+        for (int l = 0; l < 64; ++l)
+            p[l] = q[l];
+    }
+    return p[0];
+}
+
+int orc_index(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+              const void* base, const void* const* experts, int32_t K, float* sumsq)
+{
+    if (elem_bytes(dtype) == 0 || K < 1 || K > 32 || nb < 0)
+        return -1;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int64_t b = 0; b < nb; ++b)
+        for (int32_t i = 0; i < K; ++i)
+            sumsq[b * K + i] = block_sumsq(base, experts[i], dtype, doff[b], len[b]);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Algorithm 1 (PlanGen).                                              */
+/*  candidates: every unit u = (g, i), uid = g*K + i;                  */
+/*  score (Eq. 6 with Section 2's retained utility u = |alpha| ||D||):  */
+/*      s = float(float(w_i * w_i) * S_u), ranking as |w_i| * ||D||;    */
+/*  cost (Appendix A.1: stored byte length of the block):              */
+/*      c = len(g) * bytes per element;                                */
+/*  sort by decreasing score, ties by increasing uid (earlier          */
+/*  tensor/block first, then lower expert);                            */
+/*  greedy: take a candidate iff C + c <= B, and keep scanning.         */
+/* Digest (the "selected-block digest"; the hash is this reading):     */
+/*  D = sum over blocks g of mix64((g << 32) | mask[g]) mod 2^64,       */
+/*  digest = mix64(D xor C).                                           */
+/* ------------------------------------------------------------------ */
+
+uint64_t orc_mix64(uint64_t x)
+{
+    /* SplitMix64 output function (Steele, Lea, Flood 2014; Vigna): the  */
+    /* value SplitMix64 returns when its state before the step is x.     */
+    uint64_t z = x + 0x9e3779b97f4a7c15ull;
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+}
+
+typedef struct {
+    float score;
+    uint32_t uid;
+} cand_t;
+
+static int cand_cmp(const void* pa, const void* pb)
+{
+    const cand_t* a = (const cand_t*)pa;
+    const cand_t* b = (const cand_t*)pb;
+    if (a->score > b->score)
+        return -1;
+    if (a->score < b->score)
+        return 1;
+    return (a->uid < b->uid) ? -1 : (a->uid > b->uid ? 1 : 0);
+}
+
+int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
+             const float* sumsq, const float* w, uint64_t budget, uint32_t flags,
+             uint32_t* mask, uint64_t* stats)
+{
+    int s = elem_bytes(dtype);
+    if (s == 0 || K < 1 || K > 32 || G < 0 || flags != 0)
+        return -1;
+    if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
+        return -1;
+    int64_t nu = G * K;
+    cand_t* q = (cand_t*)malloc(sizeof(cand_t) * (size_t)(nu > 0 ? nu : 1));
+    if (!q)
+        return -2;
+    uint64_t full = 0;
+    for (int64_t u = 0; u < nu; ++u) {
+        int32_t i = (int32_t)(u % K);
+        float w2 = w[i] * w[i];
+        q[u].score = w2 * sumsq[u];
+        q[u].uid = (uint32_t)u;
+        full += (uint64_t)len[u / K] * (uint64_t)s;
+    }
+    qsort(q, (size_t)nu, sizeof(cand_t), cand_cmp);
+
+    for (int64_t g = 0; g < G; ++g)
+        mask[g] = 0;
+    uint64_t C = 0, nsel = 0;
+    for (int64_t r = 0; r < nu; ++r) {
+        uint32_t u = q[r].uid;
+        uint64_t c = (uint64_t)len[u / K] * (uint64_t)s;
+        if (C + c <= budget) {
+            mask[u / K] |= 1u << (u % K);
+            C += c;
+            ++nsel;
+        }
+    }
+    free(q);
+
+    uint64_t D = 0;
+    for (int64_t g = 0; g < G; ++g)
+        D += orc_mix64(((uint64_t)g << 32) | (uint64_t)mask[g]);
+    stats[0] = C;
+    stats[1] = nsel;
+    stats[2] = full;
+    stats[3] = orc_mix64(D ^ C);
+    stats[4] = (uint64_t)nu;
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* AVG (Appendix A.1): Psi = sum_i alpha_i * A_i * Delta_i with fixed   */
+/* alpha (no renormalisation over the selected experts); output        */
+/* M_A = M_0 + Psi (Eq. 4).  Omitted experts contribute nothing and     */
+/* are never read.  Accumulation: acc = +0, then for selected i in     */
+/* increasing order acc = fma(alpha_i, d_i, acc); y = x_0 + acc;        */
+/* round once to the checkpoint dtype.                                 */
+/* ------------------------------------------------------------------ */
+
+static int check_common(int32_t dtype, int32_t K, int64_t nb)
+{
+    return (elem_bytes(dtype) == 0 || K < 1 || K > 32 || nb < 0) ? -1 : 0;
+}
+
+int orc_merge_avg(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                  const void* base, const void* const* experts, int32_t K,
+                  const uint32_t* mask, const float* alpha, void* out)
+{
+    if (check_common(dtype, K, nb))
+        return -1;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int64_t b = 0; b < nb; ++b) {
+        for (int64_t j = doff[b]; j < doff[b] + len[b]; ++j) {
+            float x0 = load(base, dtype, j);
+            float acc = 0.0f;
+            for (int32_t i = 0; i < K; ++i) {
+                if (!((mask[b] >> i) & 1u))
+                    continue;
+                float d = load(experts[i], dtype, j) - x0;
+                acc = fmaf(alpha[i], d, acc);
+            }
+            store(out, dtype, j, x0 + acc);
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Sign election and disjoint mean (TIES: "elects signs, and averages   */
+/* sign-consistent entries"), shared by TIES and DARE's sign-elect      */
+/* combine.  t[r*n + j] holds the (trimmed or dropped) delta of the    */
+/* r-th selected expert, experts in increasing index order.            */
+/*   sigma_j = sum_r t_rj (fp32 adds from +0, increasing r);            */
+/*   gamma_j = sign(sigma_j) in {-1, 0, +1};                           */
+/*   agreeing set = { r : t_rj != 0 and sign(t_rj) == gamma_j };        */
+/*   mean_j = (sum over the agreeing set, fp32 adds from +0) / count,   */
+/*            0 when the set is empty;                                 */
+/*   out_j = round(fma(lambda, mean_j, x0_j)).                          */
+/* ------------------------------------------------------------------ */
+
+static float sign_elect_mean(const float* t, int nsel, int64_t n, int64_t j)
+{
+    float sigma = 0.0f;
+    for (int r = 0; r < nsel; ++r)
+        sigma = sigma + t[(int64_t)r * n + j];
+    int gamma = (sigma > 0.0f) ? 1 : ((sigma < 0.0f) ? -1 : 0);
+    float num = 0.0f;
+    int cnt = 0;
+    for (int r = 0; r < nsel; ++r) {
+        float v = t[(int64_t)r * n + j];
+        int sv = (v > 0.0f) ? 1 : ((v < 0.0f) ? -1 : 0);
+        if (v != 0.0f && sv == gamma) {
+            num = num + v;
+            ++cnt;
+        }
+    }
+    return cnt > 0 ? num / (float)cnt : 0.0f;
+}
+
+/* ------------------------------------------------------------------ */
+/* TIES (Appendix A.1: "trims, elects signs, and averages               */
+/* sign-consistent entries after masking").                            */
+/* Reading: trim is per (selected expert, block) -- Eq. 1 and Eq. 4     */
+/* make the operator a function of that block's deltas only.  Keep     */
+/* density rho: k = min(n, ceil(rho * n)) computed in fp64; tau = the   */
+/* k-th largest |d| of the block (multiplicity counted); keep d_j iff   */
+/* |d_j| >= tau and |d_j| > 0 (ties at tau are all kept, k = 0 keeps     */
+/* nothing).  Then sign election and disjoint mean as above.           */
+/* ------------------------------------------------------------------ */
+
+int64_t orc_ties_k(int64_t n, double density)
+{
+    double kk = ceil(density * (double)n);
+    int64_t k = (int64_t)kk;
+    if (k > n)
+        k = n;
+    if (k < 0)
+        k = 0;
+    return k;
+}
+
+static int desc_float(const void* pa, const void* pb)
+{
+    float a = *(const float*)pa, b = *(const float*)pb;
+    return (a > b) ? -1 : ((a < b) ? 1 : 0);
+}
+
+int orc_merge_ties(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                   const void* base, const void* const* experts, int32_t K,
+                   const uint32_t* mask, double density, float lambda, void* out)
+{
+    if (check_common(dtype, K, nb) || !(density >= 0.0 && density <= 1.0))
+        return -1;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t b = 0; b < nb; ++b) {
+        int64_t n = len[b], o = doff[b];
+        int nsel = 0;
+        for (int32_t i = 0; i < K; ++i)
+            nsel += (mask[b] >> i) & 1u;
+        float* t = (float*)malloc(sizeof(float) * (size_t)((nsel > 0 ? nsel : 1) * n + 1));
+        float* m = (float*)malloc(sizeof(float) * (size_t)(n + 1));
+        if (!t || !m) {
+            free(t);
+            free(m);
+#pragma omp atomic write
+            bad = 1;
+            continue;
+        }
+        int64_t k = orc_ties_k(n, density);
+        int r = 0;
+        for (int32_t i = 0; i < K; ++i) {
+            if (!((mask[b] >> i) & 1u))
+                continue;
+            float* ti = t + (int64_t)r * n;
+            for (int64_t j = 0; j < n; ++j) {
+                ti[j] = load(experts[i], dtype, o + j) - load(base, dtype, o + j);
+                m[j] = fabsf(ti[j]);
+            }
+            if (k == 0) {
+                for (int64_t j = 0; j < n; ++j)
+                    ti[j] = 0.0f;
+            } else {
+                qsort(m, (size_t)n, sizeof(float), desc_float);
+                float tau = m[k - 1];
+                for (int64_t j = 0; j < n; ++j) {
+                    float a = fabsf(ti[j]);
+                    if (!(a >= tau && a > 0.0f))
+                        ti[j] = 0.0f;
+                }
+            }
+            ++r;
+        }
+        for (int64_t j = 0; j < n; ++j) {
+            float x0 = load(base, dtype, o + j);
+            float mean = sign_elect_mean(t, nsel, n, j);
+            store(out, dtype, o + j, fmaf(lambda, mean, x0));
+        }
+        free(t);
+        free(m);
+    }
+    return bad ? -2 : 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: */
+/* As Easy as 1, 2, 3", SC 2011): ten rounds of                        */
+/*   (hi0,lo0) = M0 * c0, (hi1,lo1) = M1 * c2 (32x32 -> 64 products),  */
+/*   c = (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0),                      */
+/* with the key bumped by the Weyl constants between rounds.           */
+/* ------------------------------------------------------------------ */
+
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) {
+            k0 += W0;
+            k1 += W1;
+        }
+        uint64_t p0 = (uint64_t)M0 * (uint64_t)c0;
+        uint64_t p1 = (uint64_t)M1 * (uint64_t)c2;
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t n0 = hi1 ^ c1 ^ k0;
+        uint32_t n1 = lo1;
+        uint32_t n2 = hi0 ^ c3 ^ k1;
+        uint32_t n3 = lo0;
+        c0 = n0;
+        c1 = n1;
+        c2 = n2;
+        c3 = n3;
+    }
+    out[0] = c0;
+    out[1] = c1;
+    out[2] = c2;
+    out[3] = c3;
+}
+
+/* ------------------------------------------------------------------ */
+/* DARE (Appendix A.1: "applies the same idea before random            */
+/* drop/rescale, using a fixed seed or mask omega").                   */
+/* Reading: the drop decision for expert i, tensor t, element e of     */
+/* that tensor comes from Philox4x32-10 with key (seed, i) and counter  */
+/* (low32(e/4), high32(e/4), t, 0); output word e mod 4 is u; the       */
+/* element is dropped iff u < T with T = floor(p * 2^32) (fp64).  It    */
+/* depends only on (seed, i, t, e), never on the access mask.  Kept    */
+/* deltas are rescaled: t = float(d * s) with s = float(1 / (1 - p))    */
+/* (fp64 quotient).  Combine: linear -- acc = fma(alpha_i, t_i, acc)    */
+/* over selected i increasing, out = round(fma(lambda, acc, x0)); or    */
+/* sign-elect -- the TIES election and disjoint mean without a trim.   */
+/* ------------------------------------------------------------------ */
+
+int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
+                   const int32_t* tensor, const int64_t* elem0, int32_t dtype,
+                   const void* base, const void* const* experts, int32_t K,
+                   const uint32_t* mask, double p, uint32_t seed, int32_t combine,
+                   const float* alpha, float lambda, void* out)
+{
+    if (check_common(dtype, K, nb) || !(p >= 0.0 && p < 1.0) || (combine != 0 && combine != 1))
+        return -1;
+    const uint32_t T = (uint32_t)floor(p * 4294967296.0);
+    const float scale = (float)(1.0 / (1.0 - p));
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t b = 0; b < nb; ++b) {
+        int64_t n = len[b], o = doff[b];
+        int nsel = 0;
+        for (int32_t i = 0; i < K; ++i)
+            nsel += (mask[b] >> i) & 1u;
+        float* t = (float*)malloc(sizeof(float) * (size_t)((nsel > 0 ? nsel : 1) * n + 1));
+        if (!t) {
+#pragma omp atomic write
+            bad = 1;
+            continue;
+        }
+        int r = 0;
+        for (int32_t i = 0; i < K; ++i) {
+            if (!((mask[b] >> i) & 1u))
+                continue;
+            for (int64_t j = 0; j < n; ++j) {
+                uint64_t e = (uint64_t)elem0[b] + (uint64_t)j;
+                uint64_t q = e >> 2;
+                uint32_t ctr[4] = {(uint32_t)q, (uint32_t)(q >> 32), (uint32_t)tensor[b], 0u};
+                uint32_t key[2] = {seed, (uint32_t)i};
+                uint32_t word[4];
+                orc_philox4x32_10(ctr, key, word);
+                uint32_t u = word[e & 3u];
+                float d = load(experts[i], dtype, o + j) - load(base, dtype, o + j);
+                t[(int64_t)r * n + j] = (u < T) ? 0.0f : d * scale;
+            }
+            ++r;
+        }
+        for (int64_t j = 0; j < n; ++j) {
+            float x0 = load(base, dtype, o + j);
+            float y;
+            if (combine == 0) {
+                float acc = 0.0f;
+                int rr = 0;
+                for (int32_t i = 0; i < K; ++i) {
+                    if (!((mask[b] >> i) & 1u))
+                        continue;
+                    acc = fmaf(alpha[i], t[(int64_t)rr * n + j], acc);
+                    ++rr;
+                }
+                y = fmaf(lambda, acc, x0);
+            } else {
+                y = fmaf(lambda, sign_elect_mean(t, nsel, n, j), x0);
+            }
+            store(out, dtype, o + j, y);
+        }
+        free(t);
+    }
+    return bad ? -2 : 0;
+}

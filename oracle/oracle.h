@@ -1,0 +1,70 @@
+/*
+ * oracle.h -- plain CPU oracle for budgeted weight-space merging
+ * ("Access Sets Matter: Budgeting Expert Reads for Scalable Weight-Space
+ * Model Merging").
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no source
+ * with the GPU library and is written to be read against the paper, not to
+ * be fast.
+ *
+ * Conventions (the readings of the paper this oracle takes):
+ *  - dtype 0 = IEEE fp32, dtype 1 = bfloat16 (raw 16-bit patterns).
+ *  - A "block list" describes the blocks to process: for block b, its data
+ *    starts at element doff[b] of every checkpoint buffer passed and holds
+ *    len[b] elements; tensor[b] / elem0[b] give its tensor id and the index,
+ *    inside that tensor, of its first element (only the DARE drop mask needs
+ *    them).  Full-checkpoint calls pass doff = the block's checkpoint offset.
+ *  - Masks are one uint32 word per block, bit i = expert i selected.
+ *  - Return value 0 = ok, negative = invalid argument.
+ */
+#ifndef MERGEPIPE_ORACLE_H
+#define MERGEPIPE_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Block partition (Section 2: deterministic blocks of each tensor). */
+int64_t orc_num_blocks(int32_t n_tensors, const int64_t* numel, int64_t block_elems);
+int orc_blocks(int32_t n_tensors, const int64_t* numel, int64_t block_elems,
+               int64_t* off, int64_t* len, int32_t* tensor, int64_t* elem0);
+
+/* Per-(block, expert) sum of squared deltas, canonical fp32 order.
+ * sumsq[b*K + i]. */
+int orc_index(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+              const void* base, const void* const* experts, int32_t K, float* sumsq);
+
+/* Algorithm 1 (PlanGen), literal: score, sort, skip-and-continue greedy.
+ * stats[0]=selected cost, [1]=selected units, [2]=full cost, [3]=digest,
+ * [4]=number of units. */
+int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
+             const float* sumsq, const float* w, uint64_t budget, uint32_t flags,
+             uint32_t* mask, uint64_t* stats);
+
+/* Mask-aware merge operators (Eq. 4 with Appendix A.1's operators). */
+int orc_merge_avg(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                  const void* base, const void* const* experts, int32_t K,
+                  const uint32_t* mask, const float* alpha, void* out);
+int orc_merge_ties(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                   const void* base, const void* const* experts, int32_t K,
+                   const uint32_t* mask, double density, float lambda, void* out);
+int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
+                   const int32_t* tensor, const int64_t* elem0, int32_t dtype,
+                   const void* base, const void* const* experts, int32_t K,
+                   const uint32_t* mask, double p, uint32_t seed, int32_t combine,
+                   const float* alpha, float lambda, void* out);
+
+/* Building blocks exposed so the tests can pin them. */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+uint64_t orc_mix64(uint64_t x);
+void orc_round_bf16(const float* x, uint16_t* y, int64_t n);
+int64_t orc_ties_k(int64_t n, double density);
+int orc_num_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

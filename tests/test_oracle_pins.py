@@ -1,0 +1,638 @@
+"""Pins for the CPU oracle: published values, closed forms, invariants the
+paper proves, special cases and brute force on tiny inputs.
+
+None of these compares the oracle with a re-typed copy of itself; each fails
+for a plausible mistake (a dropped term, a wrong sign or index, a transposed
+operand, the wrong greedy semantics, a wrong tie-break).
+"""
+
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bits_bf16(x):
+    return oracle.round_bf16(np.asarray(x, np.float32))
+
+
+def _f32_of_bf16(u16):
+    return (np.asarray(u16, np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+# --------------------------------------------------------------------------
+# building blocks: published known answers
+# --------------------------------------------------------------------------
+
+def test_philox_known_answers():
+    rows = [l.split() for l in open(os.path.join(GOLD, "philox4x32_10_kat.txt")) if l.strip() and l[0] != "#"]
+    assert len(rows) == 3
+    for r in rows:
+        v = [int(x, 16) for x in r]
+        got = oracle.philox4x32_10(v[0:4], v[4:6])
+        assert [int(x) for x in got] == v[6:10]
+
+
+def test_splitmix64_published_outputs():
+    want = [int(l, 16) for l in open(os.path.join(GOLD, "splitmix64_seed0.txt")) if l.strip() and l[0] != "#"]
+    gamma = 0x9E3779B97F4A7C15
+    got = [oracle.mix64((n * gamma) & (2**64 - 1)) for n in range(len(want))]
+    assert got == want
+
+
+def test_bf16_rounding_matches_torch():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(1)
+    x = np.concatenate([
+        rng.standard_normal(200000).astype(np.float32) * np.float32(0.02),
+        rng.standard_normal(1000).astype(np.float32) * np.float32(1e30),
+        rng.standard_normal(1000).astype(np.float32) * np.float32(1e-38),  # subnormal range
+        np.array([0.0, -0.0, 1.0, 1.00390625, 1.0078125, 1.01171875, -1.00390625, 3.0e38], np.float32),
+    ])
+    # exact halfway cases: mantissa low 16 bits == 0x8000
+    u = rng.integers(0, 2**32, 5000, dtype=np.uint64).astype(np.uint32)
+    u = (u & np.uint32(0xFFFF0000)) | np.uint32(0x8000)
+    u = u[(u & np.uint32(0x7F800000)) != np.uint32(0x7F800000)]
+    x = np.concatenate([x, u.view(np.float32)])
+    want = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = oracle.round_bf16(x)
+    assert np.array_equal(got, want)
+
+
+def test_ties_k_rounding():
+    assert oracle.ties_k(4096, 0.2) == 820  # 819.2 -> 820
+    assert oracle.ties_k(4096, 0.1) == 410  # 409.6 -> 410
+    assert oracle.ties_k(4096, 0.25) == 1024  # exact, no ceil bump
+    assert oracle.ties_k(4096, 1.0) == 4096
+    assert oracle.ties_k(4096, 0.0) == 0
+    assert oracle.ties_k(256, 0.2) == 52  # 51.2
+    assert oracle.ties_k(1536, 0.2) == 308  # 307.2
+
+
+# --------------------------------------------------------------------------
+# Section 2: block partition
+# --------------------------------------------------------------------------
+
+def test_block_partition_is_disjoint_and_tensor_local():
+    numel = [8192, 1536, 256, 4096 * 3 + 8, 8, 4096]
+    b = oracle.Blocks(numel, 4096)
+    # closed-form count: sum of ceilings
+    assert b.G == sum(-(-n // 4096) for n in numel) == 2 + 1 + 1 + 4 + 1 + 1
+    # blocks tile [0, P) in order with no gap/overlap
+    assert b.off[0] == 0
+    assert np.array_equal(b.off[1:], b.off[:-1] + b.len[:-1])
+    assert b.off[-1] + b.len[-1] == sum(numel)
+    starts = np.concatenate([[0], np.cumsum(numel)[:-1]])
+    for g in range(b.G):
+        t = b.tensor[g]
+        assert starts[t] <= b.off[g] and b.off[g] + b.len[g] <= starts[t] + numel[t]
+        assert b.elem0[g] == b.off[g] - starts[t]
+        assert b.elem0[g] % 4096 == 0
+        # only the last block of a tensor may be short
+        if b.len[g] < 4096:
+            assert b.off[g] + b.len[g] == starts[t] + numel[t]
+
+
+@pytest.mark.parametrize("name,G,short", [
+    ("qwen2.5-1.5b", 376989, 141), ("llama3-8b", 1960513, 0), ("qwen2.5-7b", 1859341, 141), ("toy", 1024, 0)])
+def test_block_counts_of_the_workload_shapes(name, G, short):
+    from workloads import family_spec
+    lay = family_spec(name).layout
+    b = oracle.Blocks(lay.numel, lay.block_elems)
+    assert b.G == G
+    assert int((b.len < lay.block_elems).sum()) == short
+
+
+# --------------------------------------------------------------------------
+# index: canonical fp32 sum of squares
+# --------------------------------------------------------------------------
+
+def _blocks_for(numel, be=4096):
+    return oracle.Blocks(numel, be)
+
+
+def test_index_closed_form_constant_delta():
+    # bf16: base 0.5, expert 0.5 + 2^-8 -> d = 2^-8 exactly, S = n * 2^-16 exactly
+    numel = [4096, 1536, 256, 4096]
+    b = _blocks_for(numel)
+    P = sum(numel)
+    base = _bits_bf16(np.full(P, 0.5))
+    ex = _bits_bf16(np.full(P, 0.5 + 2**-8))
+    S = oracle.index(b, "bf16", base, [ex, base])
+    assert np.array_equal(S[:, 0], (b.len * 2.0**-16).astype(np.float32))
+    assert np.all(S[:, 1] == 0.0)
+    # fp32: d = 2^-10 -> S = n * 2^-20
+    base32 = np.full(P, 0.25, np.float32)
+    S32 = oracle.index(b, "f32", base32, [base32 + np.float32(2**-10), base32 - np.float32(2**-10)])
+    assert np.array_equal(S32[:, 0], (b.len * 2.0**-20).astype(np.float32))
+    assert np.array_equal(S32[:, 1], S32[:, 0])  # sign of the delta does not matter
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_index_counts_every_position_once(dtype):
+    # 128 blocks x 32 experts: expert k of block g carries one nonzero delta at
+    # position (g*32 + k) of its block, so all 4096 positions are hit once.
+    nblk, K = 128, 32
+    b = _blocks_for([4096] * nblk)
+    P = 4096 * nblk
+    base = np.zeros(P, np.float32)
+    exps = []
+    vals = np.zeros((nblk, K), np.float64)
+    for k in range(K):
+        e = np.zeros(P, np.float32)
+        for g in range(nblk):
+            pos = g * K + k
+            v = np.float32(1.0 + (pos % 7) / 8.0) * np.float32(2.0 ** -(pos % 5))
+            e[g * 4096 + pos] = v
+            vals[g, k] = float(v) ** 2
+        exps.append(e)
+    if dtype == "bf16":
+        base = _bits_bf16(base)
+        exps = [_bits_bf16(e) for e in exps]
+    S = oracle.index(b, dtype, base, exps)
+    assert np.array_equal(S.astype(np.float64), vals)
+
+
+def test_index_short_block_tail_positions():
+    # short blocks (1536, 256 elements): a nonzero at each tail position is counted
+    for n in (1536, 256, 8, 24):
+        b = _blocks_for([n], 4096)
+        for pos in sorted({0, n - 1, n // 2, max(0, n - 8)}):
+            base = np.zeros(n, np.float32)
+            e = base.copy()
+            e[pos] = 3.0
+            S = oracle.index(b, "f32", base, [e])
+            assert S[0, 0] == 9.0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_index_within_rounding_bound_of_exact(dtype):
+    from workloads import family_spec, make_family
+    spec = family_spec("qwen2.5-1.5b", n_layers=1, vocab=64)
+    lay = spec.layout
+    base, exps = make_family(spec, K=3, seed=5)
+    if dtype == "f32":
+        base = _f32_of_bf16(base)
+        exps = [_f32_of_bf16(e) for e in exps]
+    b = oracle.Blocks(lay.numel, lay.block_elems)
+    S = oracle.index(b, dtype, base, exps).astype(np.float64)
+    b32 = base.astype(np.float32) if dtype == "f32" else _f32_of_bf16(base)
+    u = 2.0**-24
+    for i, e in enumerate(exps):
+        e32 = e if dtype == "f32" else _f32_of_bf16(e)
+        d = (e32 - b32).astype(np.float64)  # the fp32 subtraction is exact here? use fp32 result
+        d = (e32 - b32).astype(np.float32).astype(np.float64)
+        for g in range(b.G):
+            o, n = b.off[g], b.len[g]
+            exact = float(np.sum(d[o:o + n] ** 2))
+            V = 4 if dtype == "f32" else 8
+            chain = -(-n // (64 * V)) * V + 6
+            gam = chain * u / (1 - chain * u)
+            assert abs(S[g, i] - exact) <= gam * exact + 1e-45
+
+
+def test_index_power_of_two_scaling_is_exact():
+    rng = np.random.default_rng(3)
+    b = _blocks_for([4096, 4096, 520])
+    P = 4096 * 2 + 520
+    base = rng.standard_normal(P).astype(np.float32)
+    d = (rng.standard_normal(P) * 1e-3).astype(np.float32)
+    S1 = oracle.index(b, "f32", np.zeros(P, np.float32), [d])
+    S2 = oracle.index(b, "f32", np.zeros(P, np.float32), [d * np.float32(2.0)])
+    assert np.array_equal(S2, S1 * np.float32(4.0))
+
+
+# --------------------------------------------------------------------------
+# Algorithm 1 (PlanGen)
+# --------------------------------------------------------------------------
+
+def test_plan_worked_example():
+    ex = json.load(open(os.path.join(GOLD, "plan_worked_example.json")))
+    b = oracle.Blocks(ex["numel"], ex["block_elems"])
+    assert list(b.len * 4) == ex["block_cost_bytes"]
+    K = ex["K"]
+    S = np.array(ex["sumsq"], np.float32)
+    for c in ex["cases"]:
+        mask, st = oracle.plan(b, ex["dtype"], K, S, c["w"], c["budget"])
+        assert list(mask) == c["mask"], c["notes"]
+        assert st["cost"] == c["cost"] and st["n_selected"] == c["n_selected"]
+        assert st["full_bytes"] == 160 and st["n_units"] == 6
+        # digest definition: mix64(sum_g mix64(g<<32 | mask_g) xor cost)
+        D = sum(oracle.mix64((g << 32) | int(m)) for g, m in enumerate(mask)) & (2**64 - 1)
+        assert st["digest"] == oracle.mix64(D ^ st["cost"])
+
+
+def _random_plan_case(rng, G, K, uniform, ties=False):
+    if uniform:
+        numel = [16] * G
+    else:
+        numel = list(rng.choice([16, 8, 4, 12], size=G))
+    b = oracle.Blocks(numel, 16)
+    if ties:
+        S = rng.integers(0, 3, size=G * K).astype(np.float32)
+    else:
+        S = (rng.random(G * K) * 10).astype(np.float32)
+        S[rng.random(G * K) < 0.2] = 0.0
+    w = (rng.random(K) + 0.5).astype(np.float32)
+    return b, S, w
+
+
+def test_plan_budget_soundness_and_maximality():
+    # Prop. 1: C(A) <= B.  Skip-and-continue greedy: every unselected unit
+    # overflows the final cost.
+    rng = np.random.default_rng(7)
+    for trial in range(300):
+        G, K = int(rng.integers(1, 12)), int(rng.integers(1, 5))
+        b, S, w = _random_plan_case(rng, G, K, uniform=bool(trial % 2), ties=bool(trial % 3 == 0))
+        full = int(b.len.sum()) * 4 * K
+        B = int(rng.integers(0, full + 20))
+        mask, st = oracle.plan(b, "f32", K, S, w, B)
+        cost = sum(int(b.len[g]) * 4 for g in range(b.G) for i in range(K) if (mask[g] >> i) & 1)
+        assert cost == st["cost"] <= B
+        assert st["full_bytes"] == full
+        for g in range(b.G):
+            for i in range(K):
+                if not (mask[g] >> i) & 1:
+                    assert st["cost"] + int(b.len[g]) * 4 > B
+        if B >= full:
+            assert np.all(mask == (1 << K) - 1)
+
+
+def test_plan_uniform_costs_brute_force_optimal():
+    # Eq. 6 with equal costs: the greedy maximises the retained score, the
+    # cost is floor(B/c)*c, and the selected set is the top of the
+    # (score desc, uid asc) order.
+    rng = np.random.default_rng(11)
+    for trial in range(120):
+        G, K = int(rng.integers(1, 5)), int(rng.integers(1, 4))
+        nu = G * K
+        if nu > 12:
+            continue
+        b, S, w = _random_plan_case(rng, G, K, uniform=True, ties=bool(trial % 2))
+        c = 64
+        B = int(rng.integers(0, nu * c + 1))
+        mask, st = oracle.plan(b, "f32", K, S, w, B)
+        m = min(B // c, nu)
+        assert st["cost"] == m * c and st["n_selected"] == m
+        score = [float(np.float32(np.float32(w[u % K] * w[u % K]) * S[u])) for u in range(nu)]
+        best = 0.0
+        for r in range(m + 1):
+            for comb in itertools.combinations(range(nu), r):
+                best = max(best, sum(score[u] for u in comb))
+        got = sum(score[u] for u in range(nu) if (mask[u // K] >> (u % K)) & 1)
+        assert math.isclose(got, best, rel_tol=1e-12, abs_tol=1e-12)
+        order = sorted(range(nu), key=lambda u: (-score[u], u))
+        sel = {u for u in range(nu) if (mask[u // K] >> (u % K)) & 1}
+        assert sel == set(order[:m])
+
+
+def test_plan_ties_prefer_lower_uid():
+    b = oracle.Blocks([16] * 3, 16)
+    S = np.ones(6, np.float32)
+    for m in range(7):
+        mask, st = oracle.plan(b, "f32", 2, S, [1.0, 1.0], m * 64)
+        sel = [u for u in range(6) if (mask[u // 2] >> (u % 2)) & 1]
+        assert sel == list(range(m))
+
+
+def test_plan_digest_sensitive_to_every_bit():
+    b = oracle.Blocks([16] * 5, 16)
+    rng = np.random.default_rng(2)
+    S = rng.random(20).astype(np.float32)
+    _, st0 = oracle.plan(b, "f32", 4, S, [1, 1, 1, 1], 5 * 64)
+    digests = {st0["digest"]}
+    for u in range(20):
+        S2 = S.copy()
+        S2[u] = 100.0  # forces u into the selection, changing the mask
+        m2, st2 = oracle.plan(b, "f32", 4, S2, [1, 1, 1, 1], 5 * 64)
+        digests.add(st2["digest"])
+    assert len(digests) > 15
+
+
+# --------------------------------------------------------------------------
+# AVG
+# --------------------------------------------------------------------------
+
+def _tiny_family(rng, numel, K, dtype="f32", scale=1e-2):
+    P = sum(numel)
+    base = rng.standard_normal(P).astype(np.float32) * np.float32(0.02)
+    exps = [base + (rng.standard_normal(P) * scale).astype(np.float32) for _ in range(K)]
+    if dtype == "bf16":
+        base = _bits_bf16(base)
+        exps = [_bits_bf16(e) for e in exps]
+    return base, exps
+
+
+def test_avg_empty_mask_is_base_bitwise():
+    rng = np.random.default_rng(0)
+    for dtype in ("f32", "bf16"):
+        numel = [4096, 1536, 256]
+        b = oracle.Blocks(numel, 4096)
+        base, exps = _tiny_family(rng, numel, 3, dtype)
+        out = oracle.merge_avg(b, dtype, base, exps, np.zeros(b.G, np.uint32), [1 / 3] * 3)
+        assert np.array_equal(out, base)
+
+
+def test_avg_one_hot_alpha_reproduces_that_expert():
+    rng = np.random.default_rng(1)
+    numel = [4096, 1536, 256, 4096]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 4, "bf16", scale=1e-3)
+    full = np.full(b.G, 15, np.uint32)
+    for i in range(4):
+        a = np.zeros(4, np.float32)
+        a[i] = 1.0
+        out = oracle.merge_avg(b, "bf16", base, exps, full, a)
+        assert np.array_equal(out, exps[i]), i
+
+
+def test_avg_closed_form_two_experts():
+    rng = np.random.default_rng(2)
+    numel = [4096, 520]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 2, "f32")
+    out = oracle.merge_avg(b, "f32", base, exps, np.full(b.G, 3, np.uint32), [0.5, 0.5])
+    want = base.astype(np.float64) + 0.5 * ((exps[0].astype(np.float64) - base) + (exps[1].astype(np.float64) - base))
+    err = np.abs(out.astype(np.float64) - want)
+    # each fp32 rounding is relative to the operand it rounds: x0, d_i, acc, y
+    mag = np.maximum.reduce([np.abs(base), np.abs(exps[0] - base), np.abs(exps[1] - base),
+                             np.abs(want).astype(np.float32)])
+    assert np.all(err <= 4 * np.spacing(mag).astype(np.float64))
+
+
+def test_avg_additive_identity_and_omission_bound_all_masks():
+    # Prop. 2: M_full - M_A = sum_i (1-A_i) alpha_i Delta_i and
+    # ||M_full - M_A|| <= sqrt(sum q^2) <= sum q, for every mask of a tiny
+    # family.  Values are dyadic so every fp32 operation is exact and the
+    # identity must hold with equality.
+    rng = np.random.default_rng(3)
+    numel = [8, 8, 4]
+    b = oracle.Blocks(numel, 8)
+    K = 3
+    P = sum(numel)
+    base = (rng.integers(-64, 64, P) / 1024.0).astype(np.float32)
+    deltas = [(rng.integers(-16, 16, P) / 4096.0).astype(np.float32) for _ in range(K)]
+    exps = [base + d for d in deltas]
+    alpha = np.array([0.25, 0.5, 0.25], np.float32)
+    full_mask = np.full(b.G, 7, np.uint32)
+    Mf = oracle.merge_avg(b, "f32", base, exps, full_mask, alpha).astype(np.float64)
+    nu = b.G * K
+    for bits in range(1 << nu):
+        A = np.array([[(bits >> (g * K + i)) & 1 for i in range(K)] for g in range(b.G)])
+        mask = np.array([sum(int(A[g, i]) << i for i in range(K)) for g in range(b.G)], np.uint32)
+        MA = oracle.merge_avg(b, "f32", base, exps, mask, alpha).astype(np.float64)
+        diff = Mf - MA
+        ident = np.zeros(P)
+        q = np.zeros(b.G)
+        for g in range(b.G):
+            o, n = b.off[g], b.len[g]
+            for i in range(K):
+                if not A[g, i]:
+                    ident[o:o + n] += float(alpha[i]) * deltas[i][o:o + n].astype(np.float64)
+                    q[g] += abs(float(alpha[i])) * np.linalg.norm(deltas[i][o:o + n].astype(np.float64))
+        assert np.array_equal(diff, ident)
+        lhs = np.linalg.norm(diff)
+        assert lhs <= math.sqrt(np.sum(q**2)) * (1 + 1e-12) + 1e-15
+        assert math.sqrt(np.sum(q**2)) <= np.sum(q) * (1 + 1e-12) + 1e-15
+
+
+def test_avg_non_anticipatory():
+    # Section 2: the output depends only on the selected entries.
+    rng = np.random.default_rng(4)
+    numel = [4096, 1536, 256, 4096]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 4, "bf16")
+    mask = rng.integers(0, 16, b.G).astype(np.uint32)
+    out1 = oracle.merge_avg(b, "bf16", base, exps, mask, [0.25] * 4)
+    junk = [e.copy() for e in exps]
+    for g in range(b.G):
+        for i in range(4):
+            if not (mask[g] >> i) & 1:
+                junk[i][b.off[g]:b.off[g] + b.len[g]] = rng.integers(0, 2**15, b.len[g]).astype(np.uint16)
+    out2 = oracle.merge_avg(b, "bf16", base, junk, mask, [0.25] * 4)
+    assert np.array_equal(out1, out2)
+
+
+# --------------------------------------------------------------------------
+# TIES
+# --------------------------------------------------------------------------
+
+def test_ties_worked_example():
+    ex = json.load(open(os.path.join(GOLD, "ties_worked_example.json")))
+    b = oracle.Blocks(ex["numel"], ex["block_elems"])
+    for case in ex["cases"]:
+        deltas = [np.array(d, np.float32) for d in case["deltas"]]
+        for run in case["runs"]:
+            base = np.full(8, run["base"], np.float32)
+            exps = [base + d for d in deltas]
+            out = oracle.merge_ties(b, "f32", base, exps, np.array(case["mask"], np.uint32),
+                                    case["density"], run["lambda"])
+            assert np.array_equal(out, np.array(run["out"], np.float32)), case["name"]
+
+
+def test_ties_trim_keeps_exactly_top_k():
+    # K=1, lambda=1, base 0, continuous deltas (all magnitudes distinct): the
+    # output is nonzero exactly on the k largest-|d| positions of each block.
+    rng = np.random.default_rng(5)
+    numel = [4096, 4096, 1536, 256, 24]
+    b = oracle.Blocks(numel, 4096)
+    P = sum(numel)
+    base = np.zeros(P, np.float32)
+    d = rng.standard_normal(P).astype(np.float32)
+    for rho in (0.2, 0.1, 0.5, 0.013):
+        out = oracle.merge_ties(b, "f32", base, [d], np.ones(b.G, np.uint32), rho, 1.0)
+        for g in range(b.G):
+            o, n = b.off[g], b.len[g]
+            k = min(n, math.ceil(rho * n))
+            top = set(np.argsort(-np.abs(d[o:o + n]), kind="stable")[:k].tolist())
+            nz = set(np.nonzero(out[o:o + n])[0].tolist())
+            assert nz == top
+            assert np.array_equal(out[o:o + n][list(top)], d[o:o + n][list(top)])
+
+
+def test_ties_threshold_ties_all_kept_and_zeros_never():
+    b = oracle.Blocks([16], 16)
+    d = np.array([3, 3, 3, 3, 2, 2, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0], np.float32)
+    base = np.zeros(16, np.float32)
+    # k = ceil(0.125*16) = 2 -> tau = 3 -> all four 3s kept
+    out = oracle.merge_ties(b, "f32", base, [d], np.ones(1, np.uint32), 0.125, 1.0)
+    assert np.array_equal(out, np.where(d == 3, d, 0))
+    # k = 16 > nnz: tau = 0, zeros never kept -> all nonzeros
+    out = oracle.merge_ties(b, "f32", base, [d], np.ones(1, np.uint32), 1.0, 1.0)
+    assert np.array_equal(out, d)
+    # density 0 keeps nothing
+    out = oracle.merge_ties(b, "f32", base, [d], np.ones(1, np.uint32), 0.0, 1.0)
+    assert np.array_equal(out, base)
+
+
+def test_ties_single_expert_full_density_is_that_expert():
+    rng = np.random.default_rng(6)
+    numel = [4096, 1536, 256]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 1, "bf16", scale=1e-3)
+    out = oracle.merge_ties(b, "bf16", base, exps, np.ones(b.G, np.uint32), 1.0, 1.0)
+    assert np.array_equal(out, exps[0])
+    # two identical experts: disjoint mean of equal entries is that entry
+    out = oracle.merge_ties(b, "bf16", base, [exps[0], exps[0]], np.full(b.G, 3, np.uint32), 1.0, 1.0)
+    assert np.array_equal(out, exps[0])
+
+
+def test_ties_negation_symmetry():
+    rng = np.random.default_rng(7)
+    numel = [4096, 1536]
+    b = oracle.Blocks(numel, 4096)
+    P = sum(numel)
+    base = np.zeros(P, np.float32)
+    ds = [(rng.standard_normal(P) * 1e-3).astype(np.float32) for _ in range(4)]
+    mask = rng.integers(0, 16, b.G).astype(np.uint32)
+    o1 = oracle.merge_ties(b, "f32", base, ds, mask, 0.2, 1.0)
+    o2 = oracle.merge_ties(b, "f32", base, [-d for d in ds], mask, 0.2, 1.0)
+    assert np.array_equal(o2, -o1)
+
+
+def test_ties_elected_sign_and_mean_bounds():
+    # the merged delta has the sign of the (trimmed) sum and lies within the
+    # range of the agreeing entries.
+    rng = np.random.default_rng(8)
+    numel = [4096]
+    b = oracle.Blocks(numel, 4096)
+    base = np.zeros(4096, np.float32)
+    ds = [(rng.standard_normal(4096) * 1e-3).astype(np.float32) for _ in range(5)]
+    out = oracle.merge_ties(b, "f32", base, ds, np.full(1, 31, np.uint32), 1.0, 1.0).astype(np.float64)
+    D = np.stack(ds).astype(np.float64)
+    s = D.sum(0)
+    assert np.all(np.sign(out) == np.sign(s))
+    pos = np.where(D > 0, D, np.nan)
+    neg = np.where(D < 0, D, np.nan)
+    with np.errstate(all="ignore"):
+        lo = np.where(s > 0, np.nanmin(pos, 0), np.nanmin(neg, 0))
+        hi = np.where(s > 0, np.nanmax(pos, 0), np.nanmax(neg, 0))
+    sel = s != 0
+    assert np.all((out[sel] >= np.minimum(lo, hi)[sel] - 1e-9) & (out[sel] <= np.maximum(lo, hi)[sel] + 1e-9))
+
+
+def test_ties_lambda_zero_is_base_and_non_anticipatory():
+    rng = np.random.default_rng(9)
+    numel = [4096, 256]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 3, "bf16")
+    mask = np.array([5, 2], np.uint32)
+    assert np.array_equal(oracle.merge_ties(b, "bf16", base, exps, mask, 0.2, 0.0), base)
+    o1 = oracle.merge_ties(b, "bf16", base, exps, mask, 0.2, 1.0)
+    junk = [e.copy() for e in exps]
+    junk[1][:4096] = 0x3F80  # expert 1 not selected in block 0
+    junk[0][4096:] = 0x4000  # expert 0 not selected in block 1
+    junk[2][4096:] = 0x4000
+    o2 = oracle.merge_ties(b, "bf16", base, junk, mask, 0.2, 1.0)
+    assert np.array_equal(o1, o2)
+
+
+# --------------------------------------------------------------------------
+# DARE
+# --------------------------------------------------------------------------
+
+def test_dare_p0_linear_equals_avg_bitwise():
+    rng = np.random.default_rng(10)
+    numel = [4096, 1536, 256, 4096]
+    b = oracle.Blocks(numel, 4096)
+    for dtype in ("bf16", "f32"):
+        base, exps = _tiny_family(rng, numel, 4, dtype)
+        mask = rng.integers(0, 16, b.G).astype(np.uint32)
+        alpha = np.array([0.25, 0.125, 0.5, 0.3], np.float32)
+        a = oracle.merge_avg(b, dtype, base, exps, mask, alpha)
+        d = oracle.merge_dare(b, dtype, base, exps, mask, 0.0, 123, 0, alpha, 1.0)
+        assert np.array_equal(a, d)
+
+
+def test_dare_p0_sign_elect_equals_ties_full_density():
+    rng = np.random.default_rng(11)
+    numel = [4096, 1536, 256]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 5, "bf16")
+    mask = rng.integers(0, 32, b.G).astype(np.uint32)
+    t = oracle.merge_ties(b, "bf16", base, exps, mask, 1.0, 0.7)
+    d = oracle.merge_dare(b, "bf16", base, exps, mask, 0.0, 9, 1, np.ones(5, np.float32), 0.7)
+    assert np.array_equal(t, d)
+
+
+def _const_delta_family(numel, K, c=1.0):
+    P = sum(numel)
+    base = np.zeros(P, np.float32)
+    return base, [base + np.float32(c) for _ in range(K)]
+
+
+def test_dare_keep_rate_and_rescale():
+    numel = [1 << 20]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _const_delta_family(numel, 1)
+    for p in (0.9, 0.5, 0.1):
+        out = oracle.merge_dare(b, "f32", base, exps, np.ones(b.G, np.uint32), p, 7, 0, [1.0], 1.0)
+        s = np.float32(1.0 / (1.0 - p))
+        kept = out != 0
+        assert np.all(out[kept] == s)  # kept entries rescaled by 1/(1-p)
+        n = out.size
+        frac = kept.mean()
+        assert abs(frac - (1 - p)) < 6 * math.sqrt(p * (1 - p) / n)
+        # unbiased: the mean rescaled delta estimates the delta (1.0)
+        assert abs(out.astype(np.float64).mean() - 1.0) < 6 * float(s) * math.sqrt(p * (1 - p) / n)
+
+
+def test_dare_masks_independent_across_experts_tensors_and_lanes():
+    numel = [1 << 18, 1 << 18]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _const_delta_family(numel, 2)
+    p = 0.5
+    # expert 0 alone and expert 1 alone
+    k0 = oracle.merge_dare(b, "f32", base, exps, np.full(b.G, 1, np.uint32), p, 3, 0, [1.0, 1.0], 1.0) != 0
+    k1 = oracle.merge_dare(b, "f32", base, exps, np.full(b.G, 2, np.uint32), p, 3, 0, [1.0, 1.0], 1.0) != 0
+    n = k0.size
+    sd = math.sqrt(0.25 * 0.75 / n)
+    assert abs((k0 & k1).mean() - 0.25) < 6 * sd  # experts draw independent masks
+    half = numel[0]
+    assert abs((k0[:half] == k0[half:]).mean() - 0.5) < 6 * math.sqrt(0.25 / half)  # tensors differ
+    g4 = k0.reshape(-1, 4)
+    all_eq = (g4.all(1) | (~g4).all(1)).mean()
+    assert abs(all_eq - 0.125) < 6 * math.sqrt(0.125 * 0.875 / g4.shape[0])  # the 4 words of a draw differ
+    # a different seed gives a different mask
+    k0b = oracle.merge_dare(b, "f32", base, exps, np.full(b.G, 1, np.uint32), p, 4, 0, [1.0, 1.0], 1.0) != 0
+    assert abs((k0 == k0b).mean() - 0.5) < 6 * math.sqrt(0.25 / n)
+
+
+def test_dare_drop_decision_follows_counter_mapping():
+    # element e of tensor t of expert i uses Philox word e%4 of counter
+    # (e//4, 0, t, 0) under key (seed, i); dropped iff word < floor(p*2^32).
+    numel = [64, 4096 + 64]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _const_delta_family(numel, 3)
+    p, seed = 0.5, 0xDEADBEEF
+    out = oracle.merge_dare(b, "f32", base, exps, np.full(b.G, 4, np.uint32), p, seed, 0,
+                            [0.0, 0.0, 1.0], 1.0)
+    T = math.floor(p * 2**32)
+    starts = [0, 64]
+    for t, n in enumerate(numel):
+        for e in list(range(0, 12)) + [n - 1, n - 5, 4096 + 3] if n > 4096 else range(n):
+            if e >= n:
+                continue
+            w = oracle.philox4x32_10([e // 4, 0, t, 0], [seed, 2])[e % 4]
+            assert (out[starts[t] + e] == 0) == (int(w) < T)
+
+
+def test_dare_non_anticipatory_drop_mask():
+    # the drop mask of a selected expert does not depend on which other
+    # experts are selected (omega is fixed by (seed, expert, element)).
+    numel = [4096, 1536]
+    rng = np.random.default_rng(12)
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 3, "f32")
+    alpha = np.array([0.5, 0.25, 0.25], np.float32)
+    only2 = oracle.merge_dare(b, "f32", base, exps, np.full(b.G, 4, np.uint32), 0.9, 7, 0, alpha, 1.0)
+    zeroed = [base.copy(), base.copy(), exps[2]]  # experts 0,1 have zero delta
+    all3 = oracle.merge_dare(b, "f32", base, zeroed, np.full(b.G, 7, np.uint32), 0.9, 7, 0, alpha, 1.0)
+    assert np.array_equal(only2, all3)

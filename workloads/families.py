@@ -1,0 +1,305 @@
+"""Shape tables and the seeded value recipe for synthetic checkpoint families.
+
+A checkpoint is one flat buffer holding its tensors back to back, each tensor
+flattened row-major, in the order listed by the shape table.  The paper's
+checkpoints are homologous families fine-tuned from a shared base (Section 1,
+Section 2); the recipe below imitates that structure:
+
+* base weights ~ N(0, 0.02^2); normalisation weights 1 + N(0, 0.02^2);
+  generated in fp32, then rounded to the family dtype;
+* expert i, per consecutive run of ``block_elems`` elements of a tensor
+  ("data block"): with probability-free exact count, ``round(zeta_i * G)``
+  data blocks (chosen by a seeded permutation) are left untouched, the rest
+  get a delta d ~ N(0, s^2) with s = exp(ln 1e-3 + xi), xi ~ N(0, 1)
+  (log-normal per block);
+* W_i = round_to_dtype(float32(W_0 + d)); untouched blocks copy W_0 bitwise.
+
+The data blocks here are only a property of the *input distribution* (the
+per-block scale of the synthetic fine-tune); how the merge method partitions
+a checkpoint is computed independently by each implementation.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+DTYPE_CODES = {"f32": 0, "bf16": 1}
+DTYPE_BYTES = {"f32": 4, "bf16": 2}
+
+
+@dataclass(frozen=True)
+class Layout:
+    """Tensor numels of a flat checkpoint plus block size and dtype."""
+
+    numel: Tuple[int, ...]
+    block_elems: int
+    dtype: str  # "f32" or "bf16"
+
+    @property
+    def n_params(self) -> int:
+        return int(sum(self.numel))
+
+    @property
+    def elem_bytes(self) -> int:
+        return DTYPE_BYTES[self.dtype]
+
+    @property
+    def dtype_code(self) -> int:
+        return DTYPE_CODES[self.dtype]
+
+    @property
+    def ckpt_bytes(self) -> int:
+        return self.n_params * self.elem_bytes
+
+
+@dataclass(frozen=True)
+class FamilySpec:
+    name: str
+    tensors: Tuple[Tuple[str, Tuple[int, ...]], ...]
+    dtype: str
+    block_elems: int = 4096
+    K: int = 4
+    zero_frac: Tuple[float, ...] = ()
+    description: str = ""
+
+    @property
+    def layout(self) -> Layout:
+        numel = tuple(int(np.prod(s)) for _, s in self.tensors)
+        return Layout(numel=numel, block_elems=self.block_elems, dtype=self.dtype)
+
+    def zeta(self, i: int) -> float:
+        if self.zero_frac:
+            return float(self.zero_frac[i])
+        return 0.2
+
+
+def _qwen_like(n_layers, hidden, ffn, n_q, n_kv, head_dim, vocab, tied):
+    q = n_q * head_dim
+    kv = n_kv * head_dim
+    t: List[Tuple[str, Tuple[int, ...]]] = [("embed_tokens.weight", (vocab, hidden))]
+    for l in range(n_layers):
+        p = f"layers.{l}."
+        t += [
+            (p + "self_attn.q_proj.weight", (q, hidden)),
+            (p + "self_attn.q_proj.bias", (q,)),
+            (p + "self_attn.k_proj.weight", (kv, hidden)),
+            (p + "self_attn.k_proj.bias", (kv,)),
+            (p + "self_attn.v_proj.weight", (kv, hidden)),
+            (p + "self_attn.v_proj.bias", (kv,)),
+            (p + "self_attn.o_proj.weight", (hidden, q)),
+            (p + "mlp.gate_proj.weight", (ffn, hidden)),
+            (p + "mlp.up_proj.weight", (ffn, hidden)),
+            (p + "mlp.down_proj.weight", (hidden, ffn)),
+            (p + "input_layernorm.weight", (hidden,)),
+            (p + "post_attention_layernorm.weight", (hidden,)),
+        ]
+    t.append(("norm.weight", (hidden,)))
+    if not tied:
+        t.append(("lm_head.weight", (vocab, hidden)))
+    return tuple(t)
+
+
+def _llama_like(n_layers, hidden, ffn, n_q, n_kv, head_dim, vocab, tied):
+    q = n_q * head_dim
+    kv = n_kv * head_dim
+    t: List[Tuple[str, Tuple[int, ...]]] = [("embed_tokens.weight", (vocab, hidden))]
+    for l in range(n_layers):
+        p = f"layers.{l}."
+        t += [
+            (p + "self_attn.q_proj.weight", (q, hidden)),
+            (p + "self_attn.k_proj.weight", (kv, hidden)),
+            (p + "self_attn.v_proj.weight", (kv, hidden)),
+            (p + "self_attn.o_proj.weight", (hidden, q)),
+            (p + "mlp.gate_proj.weight", (ffn, hidden)),
+            (p + "mlp.up_proj.weight", (ffn, hidden)),
+            (p + "mlp.down_proj.weight", (hidden, ffn)),
+            (p + "input_layernorm.weight", (hidden,)),
+            (p + "post_attention_layernorm.weight", (hidden,)),
+        ]
+    t.append(("norm.weight", (hidden,)))
+    if not tied:
+        t.append(("lm_head.weight", (vocab, hidden)))
+    return tuple(t)
+
+
+def _toy():
+    return tuple((f"w{j}", (512, 1024)) for j in range(8))
+
+
+def family_spec(name: str, n_layers: Optional[int] = None, vocab: Optional[int] = None) -> FamilySpec:
+    """Return the family spec ``name``; ``n_layers``/``vocab`` truncate the
+    shape for small parity cases (same tensor shapes, fewer of them)."""
+    if name == "toy":
+        return FamilySpec("toy", _toy(), "f32", 4096, 4, (),
+                          "fp32 toy: 8 x (512x1024), K=4")
+    if name == "qwen2.5-1.5b":
+        L = 28 if n_layers is None else n_layers
+        V = 151936 if vocab is None else vocab
+        return FamilySpec(name, _qwen_like(L, 1536, 8960, 12, 2, 128, V, True), "bf16", 4096, 4, (),
+                          f"Qwen2.5-1.5B-shaped bf16, {L} layers, vocab {V}, tied, K=4")
+    if name == "llama3-8b":
+        L = 32 if n_layers is None else n_layers
+        V = 128256 if vocab is None else vocab
+        return FamilySpec(name, _llama_like(L, 4096, 14336, 32, 8, 128, V, False), "bf16", 4096, 8, (),
+                          f"Llama-3-8B-shaped bf16, {L} layers, vocab {V}, untied, K=8")
+    if name == "qwen2.5-7b":
+        L = 28 if n_layers is None else n_layers
+        V = 152064 if vocab is None else vocab
+        return FamilySpec(name, _qwen_like(L, 3584, 18944, 28, 4, 128, V, False), "bf16", 4096, 8, (),
+                          f"Qwen2.5-7B-shaped bf16, {L} layers, vocab {V}, untied, K=8")
+    if name == "llama3-8b-k16":
+        L = 32 if n_layers is None else n_layers
+        V = 128256 if vocab is None else vocab
+        z = tuple(0.8 * i / 15.0 for i in range(16))
+        return FamilySpec(name, _llama_like(L, 4096, 14336, 32, 8, 128, V, False), "bf16", 4096, 16, z,
+                          f"Llama-3-8B-shaped bf16, {L} layers, K=16, 0-80% zero blocks")
+    raise KeyError(name)
+
+
+# The five workloads and the operator settings each is quoted with.
+CONFIGS = {
+    "toy": dict(family="toy", op="avg", budgets=(0.5,), residency="device"),
+    "qwen2.5-1.5b": dict(family="qwen2.5-1.5b", op="ties", density=0.2, lam=1.0,
+                         budgets=(0.25, 0.5, 1.0), residency="device"),
+    "llama3-8b": dict(family="llama3-8b", op="avg", budgets=tuple(x / 10 for x in range(1, 11)),
+                      residency="host_pinned"),
+    "qwen2.5-7b": dict(family="qwen2.5-7b", op="dare", p=0.9, seed=7, combine="sign_elect", lam=1.0,
+                       budgets=(0.3,), residency="device"),
+    "llama3-8b-k16": dict(family="llama3-8b-k16", op="ties", density=0.1, lam=1.0,
+                          budgets=(1 / 16, 0.1, 0.25, 0.5, 0.75, 1.0), residency="host_pinned"),
+}
+
+
+def _is_norm(name: str) -> bool:
+    return "layernorm" in name or name.startswith("norm.")
+
+
+def _data_blocks(n: int, be: int) -> int:
+    return (n + be - 1) // be
+
+
+def _expert_block_scales(torch, spec: FamilySpec, i: int, seed: int, device):
+    """Per data-block delta scale for expert i (0 for untouched blocks)."""
+    lay = spec.layout
+    nblk = sum(_data_blocks(n, lay.block_elems) for n in lay.numel)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(1_000_003 * (seed + 1) + 7919 * (i + 1))
+    xi = torch.randn(nblk, generator=g, dtype=torch.float64)
+    sig = torch.exp(math.log(1e-3) + xi).to(torch.float32)
+    nz = int(round(spec.zeta(i) * nblk))
+    if nz > 0:
+        perm = torch.randperm(nblk, generator=g)
+        sig[perm[:nz]] = 0.0
+    return sig.to(device)
+
+
+def _fill(torch, spec: FamilySpec, K: int, seed: int, device, out_base, out_experts, tensor_filter=None):
+    lay = spec.layout
+    tdt = torch.float32 if lay.dtype == "f32" else torch.bfloat16
+    be = lay.block_elems
+    gb = torch.Generator(device=device)
+    scales = [_expert_block_scales(torch, spec, i, seed, device) for i in range(K)]
+    gens = []
+    for i in range(K):
+        ge = torch.Generator(device=device)
+        ge.manual_seed(97 * (seed + 1) + 131 * (i + 1) + 17)
+        gens.append(ge)
+    gb.manual_seed(seed * 7 + 3)
+    off = 0
+    blk = 0
+    for (name, shape), n in zip(spec.tensors, lay.numel):
+        nb = _data_blocks(n, be)
+        w0 = torch.randn(n, generator=gb, device=device, dtype=torch.float32) * 0.02
+        if _is_norm(name):
+            w0 = w0 + 1.0
+        w0q = w0.to(tdt)
+        out_base[off:off + n].copy_(w0q)
+        w0f = w0q.to(torch.float32)
+        for i in range(K):
+            s = scales[i][blk:blk + nb]
+            s_el = torch.repeat_interleave(s, be)[:n]
+            d = torch.randn(n, generator=gens[i], device=device, dtype=torch.float32) * s_el
+            wi = (w0f + d).to(tdt)
+            out_experts[i][off:off + n].copy_(wi)
+        off += n
+        blk += nb
+    return out_base, out_experts
+
+
+def make_family(spec: FamilySpec, K: Optional[int] = None, seed: int = 0):
+    """Generate base + K experts on the CPU; returns numpy arrays.
+
+    fp32 families come back as float32 arrays, bf16 families as uint16 arrays
+    holding the raw bfloat16 bit patterns.
+    """
+    import torch
+
+    K = spec.K if K is None else K
+    lay = spec.layout
+    tdt = torch.float32 if lay.dtype == "f32" else torch.bfloat16
+    P = lay.n_params
+    base = torch.empty(P, dtype=tdt)
+    experts = [torch.empty(P, dtype=tdt) for _ in range(K)]
+    _fill(torch, spec, K, seed, "cpu", base, experts)
+    if lay.dtype == "f32":
+        return base.numpy(), [e.numpy() for e in experts]
+    return base.view(torch.int16).numpy().view(np.uint16), [e.view(torch.int16).numpy().view(np.uint16) for e in experts]
+
+
+def make_family_device(spec: FamilySpec, K: Optional[int] = None, seed: int = 0, device="cuda",
+                       experts_on_host_pinned: bool = False):
+    """Generate base + K experts as torch tensors on ``device``.
+
+    With ``experts_on_host_pinned`` the experts are generated on the device one
+    at a time and copied into pinned host tensors (the base stays on device).
+    The values depend on the device's RNG, so families generated on different
+    devices differ; consumers that need the same bytes copy them.
+    """
+    import torch
+
+    K = spec.K if K is None else K
+    lay = spec.layout
+    tdt = torch.float32 if lay.dtype == "f32" else torch.bfloat16
+    P = lay.n_params
+    base = torch.empty(P, dtype=tdt, device=device)
+    if not experts_on_host_pinned:
+        experts = [torch.empty(P, dtype=tdt, device=device) for _ in range(K)]
+        _fill(torch, spec, K, seed, device, base, experts)
+        return base, experts
+    # one device scratch expert at a time, then copy to pinned host memory
+    experts = []
+    scratch = torch.empty(P, dtype=tdt, device=device)
+    # generate base once with K=0 then each expert with the same per-expert streams
+    _fill(torch, spec, 0, seed, device, base, [])
+    for i in range(K):
+        _fill_one_expert(torch, spec, i, seed, device, base, scratch)
+        h = torch.empty(P, dtype=tdt, pin_memory=True)
+        h.copy_(scratch)
+        experts.append(h)
+    del scratch
+    return base, experts
+
+
+def _fill_one_expert(torch, spec: FamilySpec, i: int, seed: int, device, base, out):
+    """Regenerate expert i exactly as ``_fill`` would (same RNG streams)."""
+    lay = spec.layout
+    tdt = torch.float32 if lay.dtype == "f32" else torch.bfloat16
+    be = lay.block_elems
+    s_all = _expert_block_scales(torch, spec, i, seed, device)
+    ge = torch.Generator(device=device)
+    ge.manual_seed(97 * (seed + 1) + 131 * (i + 1) + 17)
+    off = 0
+    blk = 0
+    for n in lay.numel:
+        nb = _data_blocks(n, be)
+        w0f = base[off:off + n].to(torch.float32)
+        s_el = torch.repeat_interleave(s_all[blk:blk + nb], be)[:n]
+        d = torch.randn(n, generator=ge, device=device, dtype=torch.float32) * s_el
+        out[off:off + n].copy_((w0f + d).to(tdt))
+        off += n
+        blk += nb
+    return out
