@@ -1,0 +1,181 @@
+/*
+ * mergepipe.h -- C ABI of the MI355X budgeted-merge library (libmergepipe.so).
+ *
+ * Budgeted weight-space merging after "Access Sets Matter: Budgeting Expert
+ * Reads for Scalable Weight-Space Model Merging": index the per-block expert
+ * deltas, build a deterministic access plan A with C_expert(A) <= B, and run
+ * the mask-aware merge operator Psi_op over only the selected delta blocks.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Checkpoints.  A checkpoint is ONE flat, contiguous buffer holding the
+ *   tensors of an mp_layout back to back, each flattened row-major, in
+ *   layout order.  Elements are IEEE fp32 (MP_F32) or bfloat16 (MP_BF16).
+ *   The base, the output and every expert share the layout.
+ * Blocks (Section 2, the deterministic blocks of each tensor).  Each tensor
+ *   is cut into consecutive blocks of layout.block_elems elements; the last
+ *   block of a tensor may be shorter; blocks never cross tensors.  Blocks
+ *   are numbered g = 0..G-1 in layout order.  They partition the parameter
+ *   vector, as Prop. 2 assumes.
+ * Units.  An access unit is (expert i, block g), uid = g*K + i (Eq. 2).  Its
+ *   read cost c is the stored byte length of the block (Appendix A.1).
+ * Masks.  One uint32 word per block, bit i set iff expert i is read for the
+ *   block (the access mask A of Eq. 2).  K <= 32.
+ * Memory.  Unless stated otherwise pointers are device pointers (memory of
+ *   the current HIP device).  `experts` is a HOST array of K pointers; with
+ *   residency MP_HOST_PINNED those K pointers are pinned host memory
+ *   (hipHostMalloc / pinned torch tensors), otherwise device memory.  The
+ *   caller owns every buffer; the library only reads inputs and writes the
+ *   named outputs.  The library keeps a per-device workspace (block tables,
+ *   plan scratch, staging buffers, a side stream) that mp_release() frees.
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Work is
+ *   enqueued on it; calls return once enqueued unless stated otherwise.
+ *   Calls that fill a host-side stats struct synchronise the stream first.
+ * Errors.  Every call returns MP_OK (0) or a negative MP_E_* code;
+ *   mp_last_error() gives a message (thread-local).  On an argument error
+ *   nothing is enqueued and no output is written.  Asynchronous device
+ *   errors surface at the next synchronising call.  No C++ exception crosses
+ *   the ABI.
+ * Validation (all calls): 1 <= K <= 32; block_elems > 0 and a multiple of
+ *   16 / (bytes per element); every tensor numel >= 0 and a multiple of
+ *   16 / (bytes per element) (each tensor starts 16-byte aligned);
+ *   K * G < 2^32; non-NULL pointers; device buffers must be device memory
+ *   large enough for the layout; pinned buffers must be pinned host memory.
+ *   `out` must not overlap the base or any expert.
+ */
+#ifndef MERGEPIPE_H
+#define MERGEPIPE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MP_OK 0
+#define MP_E_ARG (-1)         /* invalid argument; nothing was done */
+#define MP_E_UNSUPPORTED (-2) /* valid request this build does not handle */
+#define MP_E_NOMEM (-3)       /* workspace allocation failed */
+#define MP_E_HIP (-4)         /* a HIP runtime call failed */
+#define MP_E_IO (-5)          /* host-to-device streaming failed */
+
+typedef enum { MP_F32 = 0, MP_BF16 = 1 } mp_dtype;
+typedef enum { MP_DEVICE = 0, MP_HOST_PINNED = 1 } mp_residency;
+typedef enum { MP_COMBINE_LINEAR = 0, MP_COMBINE_SIGN_ELECT = 1 } mp_combine;
+
+typedef struct mp_layout {
+    int32_t n_tensors;     /* number of tensors (>= 0) */
+    int32_t dtype;         /* mp_dtype of every checkpoint */
+    const int64_t* numel;  /* HOST array [n_tensors]: elements per tensor */
+    int64_t block_elems;   /* block size in elements */
+} mp_layout;
+
+typedef struct mp_plan_stats {
+    uint64_t budget_bytes; /* B as passed */
+    uint64_t cost_bytes;   /* C_expert(A) of the returned mask (<= B) */
+    uint64_t full_bytes;   /* C_expert(1) = K * P * bytes per element */
+    uint64_t n_selected;   /* units with A = 1 */
+    uint64_t n_units;      /* K * G */
+    uint64_t digest;       /* selected-block digest of (mask, cost) */
+} mp_plan_stats;
+
+typedef struct mp_io_stats {
+    uint64_t expert_bytes; /* expert bytes the merge kernels loaded */
+    uint64_t base_bytes;   /* base bytes read */
+    uint64_t out_bytes;    /* output bytes written */
+    uint64_t h2d_bytes;    /* bytes copied host -> device (MP_HOST_PINNED) */
+    uint64_t h2d_copies;   /* number of host -> device copies issued */
+    uint64_t n_stages;     /* pipeline stages (MP_HOST_PINNED) */
+} mp_io_stats;
+
+/* Number of blocks G of a layout (Section 2's block partition).
+ * Host only; enqueues nothing.  Returns MP_E_ARG for an invalid layout. */
+int mp_layout_blocks(const mp_layout* layout, int64_t* n_blocks);
+
+/* Catalog statistic (Section 2 "Offline Analyze", Section 3 "Catalog"):
+ * for every unit, S = sum over the block of d*d with d = float(x_i) -
+ * float(x_0) the fp32 delta, summed in this fixed order: with V = 16 /
+ * (bytes per element), 64 partial sums p_l, p_l takes 16-byte chunks
+ * l, l+64, l+128, ... of the block in turn and their elements in order,
+ * p_l = fma(d, d, p_l) from +0; then for s = 32,16,8,4,2,1 each p_l
+ * becomes p_l + p_(l xor s); S = p_0.  (The paper fixes no order; a fixed
+ * one makes plans reproducible bit for bit.)
+ *   sumsq: device float[G*K], written at uid = g*K + i.
+ * MP_DEVICE: asynchronous on `stream`.  MP_HOST_PINNED: every expert byte
+ * crosses PCIe once (amortised catalog construction); the call returns
+ * after the work is enqueued and the staging buffers are released, i.e.
+ * it synchronises `stream`. */
+int mp_index_blocks(const mp_layout* layout, const void* base,
+                    const void* const* experts, int32_t K, int32_t residency,
+                    float* sumsq, void* stream);
+
+/* Algorithm 1 (PlanGen) over all units, budget-feasible by construction
+ * (Prop. 1: C_expert(A) <= B):
+ *   score  s_u = float(float(w_i * w_i) * S_u), which ranks units as
+ *          |w_i| * ||Delta||_2, the retained utility of Section 2;
+ *   cost   c_u = block length * bytes per element;
+ *   order  decreasing score, ties by increasing uid;
+ *   greedy take u iff Chat + c_u <= B, and continue past candidates that
+ *          do not fit (skip-and-continue).
+ *   sumsq: device float[G*K] from mp_index_blocks.  w: HOST float[K]
+ *   (alpha for AVG and DARE-linear, 1 for TIES and sign-elect).  flags: 0.
+ *   mask: device uint32[G], written for every block.
+ *   stats: HOST, filled; digest = mix64(D xor Chat) with D = sum over g of
+ *   mix64((g << 32) | mask[g]) mod 2^64 and mix64 the SplitMix64 output
+ *   function.  B >= full_bytes yields the all-ones mask.
+ * Synchronises `stream` before returning (the one blocking point). */
+int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq,
+            const float* w, uint64_t budget_bytes, uint32_t flags,
+            uint32_t* mask, mp_plan_stats* stats, void* stream);
+
+/* Budgeted AVG (Eq. 4 with Appendix A.1's Psi_AVG): per element
+ * acc = +0; for selected i in increasing order acc = fma(alpha_i, d_i, acc);
+ * out = round(x_0 + acc) (round-to-nearest-even into the checkpoint dtype).
+ * alpha: HOST float[K], fixed (no renormalisation over the selected
+ * experts).  Unselected experts are never read.  mask: device uint32[G].
+ * io: optional (NULL = none); when given the call synchronises `stream`
+ * and reports the bytes the kernels loaded and stored. */
+int mp_merge_avg(const mp_layout* layout, const void* base,
+                 const void* const* experts, int32_t K, int32_t residency,
+                 const uint32_t* mask, const float* alpha, void* out,
+                 mp_io_stats* io, void* stream);
+
+/* Budgeted TIES (Appendix A.1: trim, elect signs, disjoint mean after
+ * masking).  Trim is per selected (expert, block): k = min(n, ceil(density
+ * * n)) in fp64, tau = the k-th largest |d| of the block; d is kept iff
+ * |d| >= tau and |d| > 0.  Per element: sigma = sum of kept d over selected
+ * experts (fp32 adds from +0, increasing i); gamma = sign(sigma); mean =
+ * (sum of kept d with sign gamma) / (their count), 0 if none;
+ * out = round(fma(lambda, mean, x_0)).  0 <= density <= 1.
+ * block_elems must be <= 4096 (MP_E_UNSUPPORTED otherwise). */
+int mp_merge_ties(const mp_layout* layout, const void* base,
+                  const void* const* experts, int32_t K, int32_t residency,
+                  const uint32_t* mask, double density, float lambda, void* out,
+                  mp_io_stats* io, void* stream);
+
+/* Budgeted DARE (Appendix A.1: random drop and rescale with a fixed seed).
+ * Element e of tensor t of expert i is dropped iff u < floor(p * 2^32),
+ * u = word (e mod 4) of Philox4x32-10 (Salmon et al., SC 2011) with key
+ * (seed, i) and counter (low32(e/4), high32(e/4), t, 0); the decision never
+ * depends on the mask.  Kept deltas become float(d * s), s = float(1/(1-p)).
+ * combine MP_COMBINE_LINEAR: acc = fma(alpha_i, t_i, acc) over selected i
+ * increasing, out = round(fma(lambda, acc, x_0)).  MP_COMBINE_SIGN_ELECT:
+ * TIES's sign election and disjoint mean (no trim); alpha is ignored and
+ * may be NULL.  0 <= p < 1. */
+int mp_merge_dare(const mp_layout* layout, const void* base,
+                  const void* const* experts, int32_t K, int32_t residency,
+                  const uint32_t* mask, double p, uint32_t seed, int32_t combine,
+                  const float* alpha, float lambda, void* out, mp_io_stats* io,
+                  void* stream);
+
+/* Message for the last failing call on this thread ("" if none). */
+const char* mp_last_error(void);
+
+/* Free the library's cached per-device workspaces.  No call may be in
+ * flight on any stream. */
+void mp_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MERGEPIPE_H */

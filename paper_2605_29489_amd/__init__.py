@@ -1,0 +1,202 @@
+"""Python binding of libmergepipe.so (budgeted weight-space merging on MI355X).
+
+Argument marshalling only: every step of the path (index, plan, merge) runs
+in the library's HIP kernels.  PyTorch is used for device/pinned memory and
+streams.  The functions have the names of the C entry points declared in
+``include/mergepipe.h``; they take torch tensors and raise ``MPError`` on a
+non-zero status.
+
+The library must have been built (``python -m paper_2605_29489_amd.build``
+or ``__graft_entry__.build()``); importing this package without it raises
+ImportError -- there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmergepipe.so")
+
+MP_OK = 0
+MP_E_ARG = -1
+MP_E_UNSUPPORTED = -2
+MP_E_NOMEM = -3
+MP_E_HIP = -4
+MP_E_IO = -5
+MP_F32, MP_BF16 = 0, 1
+MP_DEVICE, MP_HOST_PINNED = 0, 1
+MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
+
+EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+           "mp_merge_dare", "mp_last_error", "mp_release")
+
+
+class mp_layout(C.Structure):
+    _fields_ = [("n_tensors", C.c_int32), ("dtype", C.c_int32),
+                ("numel", C.POINTER(C.c_int64)), ("block_elems", C.c_int64)]
+
+
+class mp_plan_stats(C.Structure):
+    _fields_ = [("budget_bytes", C.c_uint64), ("cost_bytes", C.c_uint64), ("full_bytes", C.c_uint64),
+                ("n_selected", C.c_uint64), ("n_units", C.c_uint64), ("digest", C.c_uint64)]
+
+    def as_dict(self):
+        return {f: int(getattr(self, f)) for f, _ in self._fields_}
+
+
+class mp_io_stats(C.Structure):
+    _fields_ = [("expert_bytes", C.c_uint64), ("base_bytes", C.c_uint64), ("out_bytes", C.c_uint64),
+                ("h2d_bytes", C.c_uint64), ("h2d_copies", C.c_uint64), ("n_stages", C.c_uint64)]
+
+    def as_dict(self):
+        return {f: int(getattr(self, f)) for f, _ in self._fields_}
+
+
+class MPError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"mergepipe error {code}: {msg}")
+        self.code = code
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, u32, u64 = C.c_void_p, C.c_int32, C.c_uint32, C.c_uint64
+    lp = C.POINTER(mp_layout)
+    L.mp_layout_blocks.argtypes = [lp, C.POINTER(C.c_int64)]
+    L.mp_index_blocks.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, vp]
+    L.mp_plan.argtypes = [lp, i32, vp, C.POINTER(C.c_float), u64, u32, vp, C.POINTER(mp_plan_stats), vp]
+    L.mp_merge_avg.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.POINTER(C.c_float), vp,
+                               C.POINTER(mp_io_stats), vp]
+    L.mp_merge_ties.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, C.c_float, vp,
+                                C.POINTER(mp_io_stats), vp]
+    L.mp_merge_dare.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, u32, i32,
+                                C.POINTER(C.c_float), C.c_float, vp, C.POINTER(mp_io_stats), vp]
+    L.mp_last_error.restype = C.c_char_p
+    L.mp_last_error.argtypes = []
+    L.mp_release.argtypes = []
+    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+                 "mp_merge_dare"):
+        getattr(L, name).restype = C.c_int
+    return L
+
+
+lib = _load()
+
+
+@dataclass
+class Layout:
+    """Host-side mp_layout: tensor numels, block size and dtype code."""
+
+    numel: Sequence[int]
+    block_elems: int
+    dtype: int  # MP_F32 or MP_BF16
+
+    def __post_init__(self):
+        self._numel = (C.c_int64 * max(len(self.numel), 1))(*[int(n) for n in self.numel])
+        self._s = mp_layout(len(self.numel), int(self.dtype), C.cast(self._numel, C.POINTER(C.c_int64)),
+                            int(self.block_elems))
+
+    @property
+    def ref(self):
+        return C.byref(self._s)
+
+    @property
+    def elem_bytes(self) -> int:
+        return 4 if self.dtype == MP_F32 else 2
+
+    @property
+    def n_params(self) -> int:
+        return int(sum(int(n) for n in self.numel))
+
+
+def _check(rc: int):
+    if rc != MP_OK:
+        raise MPError(rc, lib.mp_last_error().decode())
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _ptrs(ts):
+    return (C.c_void_p * max(len(ts), 1))(*[_ptr(t) for t in ts])
+
+
+def _floats(xs, K):
+    if xs is None:
+        return None
+    xs = [float(x) for x in xs]
+    if len(xs) != K:
+        raise ValueError(f"expected {K} coefficients, got {len(xs)}")
+    return (C.c_float * K)(*xs)
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return C.c_void_p(stream)
+    return C.c_void_p(stream.cuda_stream)
+
+
+def mp_layout_blocks(layout: Layout) -> int:
+    g = C.c_int64(0)
+    _check(lib.mp_layout_blocks(layout.ref, C.byref(g)))
+    return int(g.value)
+
+
+def mp_index_blocks(layout: Layout, base, experts, sumsq, residency: int = MP_DEVICE, stream=None):
+    _check(lib.mp_index_blocks(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency,
+                               _ptr(sumsq), _stream(stream)))
+
+
+def mp_plan(layout: Layout, K: int, sumsq, w, budget_bytes: int, mask, flags: int = 0, stream=None) -> dict:
+    st = mp_plan_stats()
+    _check(lib.mp_plan(layout.ref, K, _ptr(sumsq), _floats(w, K), int(budget_bytes), flags, _ptr(mask),
+                       C.byref(st), _stream(stream)))
+    return st.as_dict()
+
+
+def _io(io):
+    return C.byref(io) if io is not None else None
+
+
+def mp_merge_avg(layout: Layout, base, experts, mask, alpha, out, residency: int = MP_DEVICE,
+                 io: bool = False, stream=None) -> Optional[dict]:
+    st = mp_io_stats() if io else None
+    _check(lib.mp_merge_avg(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+                            _floats(alpha, len(experts)), _ptr(out), _io(st), _stream(stream)))
+    return st.as_dict() if io else None
+
+
+def mp_merge_ties(layout: Layout, base, experts, mask, density: float, lam: float, out,
+                  residency: int = MP_DEVICE, io: bool = False, stream=None) -> Optional[dict]:
+    st = mp_io_stats() if io else None
+    _check(lib.mp_merge_ties(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+                             float(density), float(lam), _ptr(out), _io(st), _stream(stream)))
+    return st.as_dict() if io else None
+
+
+def mp_merge_dare(layout: Layout, base, experts, mask, p: float, seed: int, combine: int, alpha, lam: float,
+                  out, residency: int = MP_DEVICE, io: bool = False, stream=None) -> Optional[dict]:
+    st = mp_io_stats() if io else None
+    a = _floats(alpha, len(experts)) if alpha is not None else None
+    _check(lib.mp_merge_dare(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+                             float(p), int(seed) & 0xFFFFFFFF, int(combine), a, float(lam), _ptr(out), _io(st),
+                             _stream(stream)))
+    return st.as_dict() if io else None
+
+
+def mp_last_error() -> str:
+    return lib.mp_last_error().decode()
+
+
+def mp_release():
+    lib.mp_release()

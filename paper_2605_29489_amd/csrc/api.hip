@@ -1,0 +1,599 @@
+// Host runtime behind include/mergepipe.h: argument validation, the cached
+// per-(device, layout) block tables, per-device workspaces and dispatch to
+// the kernel launchers.  Everything the paper's path computes runs in the
+// kernels; this file only checks, allocates, copies tables and enqueues.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "mp_internal.h"
+#include "pipeline.h"
+
+namespace mp {
+
+hipError_t plan_ctl_alloc(PlanCtl** ctl);
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what)
+{
+    return fail(MP_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ------------------------------------------------------------ workspaces
+struct DeviceWs {
+    PlanScratch plan;
+    unsigned long long* counters = nullptr;  // [256]
+    unsigned long long* h_counters = nullptr;  // pinned [256]
+    std::unique_ptr<Pipeline> pipe;
+};
+
+std::mutex g_mu;
+std::map<std::string, std::unique_ptr<BlockTable>> g_tables;
+std::map<int, std::unique_ptr<DeviceWs>> g_ws;
+
+void free_table(BlockTable& bt)
+{
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(bt.device);
+    (void)hipFree(bt.d_off);
+    (void)hipFree(bt.d_len);
+    (void)hipFree(bt.d_tensor);
+    (void)hipFree(bt.d_elem0);
+    (void)hipSetDevice(cur);
+}
+
+void free_ws(int dev, DeviceWs& w)
+{
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(dev);
+    w.pipe.reset();
+    (void)hipFree(w.plan.ctl);
+    (void)hipFree(w.plan.list[0]);
+    (void)hipFree(w.plan.list[1]);
+    (void)hipHostFree(w.plan.h_stats);
+    (void)hipFree(w.counters);
+    (void)hipHostFree(w.h_counters);
+    (void)hipSetDevice(cur);
+}
+
+// ------------------------------------------------------------ layout
+int validate_layout(const mp_layout* L, int* esize)
+{
+    if (L == nullptr)
+        return fail(MP_E_ARG, "layout is NULL");
+    if (L->dtype != MP_F32 && L->dtype != MP_BF16)
+        return fail(MP_E_ARG, "layout.dtype %d is not MP_F32 or MP_BF16", L->dtype);
+    if (L->n_tensors < 0)
+        return fail(MP_E_ARG, "layout.n_tensors %d < 0", L->n_tensors);
+    if (L->n_tensors > 0 && L->numel == nullptr)
+        return fail(MP_E_ARG, "layout.numel is NULL");
+    *esize = L->dtype == MP_F32 ? 4 : 2;
+    const int64_t V = 16 / *esize;
+    if (L->block_elems <= 0 || L->block_elems % V != 0)
+        return fail(MP_E_ARG, "layout.block_elems %lld must be a positive multiple of %lld",
+                    (long long)L->block_elems, (long long)V);
+    if (L->block_elems > (int64_t)1 << 30)
+        return fail(MP_E_ARG, "layout.block_elems %lld too large", (long long)L->block_elems);
+    for (int32_t t = 0; t < L->n_tensors; ++t) {
+        if (L->numel[t] < 0 || L->numel[t] % V != 0)
+            return fail(MP_E_ARG, "layout.numel[%d] = %lld must be >= 0 and a multiple of %lld", t,
+                        (long long)L->numel[t], (long long)V);
+    }
+    return MP_OK;
+}
+
+int64_t count_blocks(const mp_layout* L)
+{
+    int64_t G = 0;
+    for (int32_t t = 0; t < L->n_tensors; ++t)
+        G += (L->numel[t] + L->block_elems - 1) / L->block_elems;
+    return G;
+}
+
+std::string layout_key(int dev, const mp_layout* L)
+{
+    std::string k;
+    k.reserve(32 + 8 * (size_t)L->n_tensors);
+    k.append(reinterpret_cast<const char*>(&dev), sizeof dev);
+    k.append(reinterpret_cast<const char*>(&L->dtype), sizeof L->dtype);
+    k.append(reinterpret_cast<const char*>(&L->block_elems), sizeof L->block_elems);
+    if (L->n_tensors > 0)
+        k.append(reinterpret_cast<const char*>(L->numel), sizeof(int64_t) * (size_t)L->n_tensors);
+    return k;
+}
+
+// Looks up or builds the device block table of a validated layout.
+int get_table(const mp_layout* L, int esize, BlockTable** out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    const std::string key = layout_key(dev, L);
+    auto it = g_tables.find(key);
+    if (it != g_tables.end()) {
+        *out = it->second.get();
+        return MP_OK;
+    }
+    auto bt = std::make_unique<BlockTable>();
+    bt->device = dev;
+    bt->dtype = L->dtype;
+    bt->esize = esize;
+    bt->block_elems = L->block_elems;
+    bt->n_tensors = L->n_tensors;
+    bt->numel.assign(L->numel, L->numel + L->n_tensors);
+    const int64_t G = count_blocks(L);
+    bt->G = G;
+    std::vector<uint32_t> tens((size_t)G);
+    std::vector<uint64_t> e0((size_t)G);
+    bt->h_off.resize((size_t)G);
+    bt->h_len.resize((size_t)G);
+    std::set<uint32_t> lens;
+    int64_t g = 0, start = 0;
+    for (int32_t t = 0; t < L->n_tensors; ++t) {
+        for (int64_t x = 0; x < L->numel[t]; x += L->block_elems) {
+            const int64_t n = std::min<int64_t>(L->block_elems, L->numel[t] - x);
+            bt->h_off[(size_t)g] = (uint64_t)(start + x);
+            bt->h_len[(size_t)g] = (uint32_t)n;
+            tens[(size_t)g] = (uint32_t)t;
+            e0[(size_t)g] = (uint64_t)x;
+            lens.insert((uint32_t)n);
+            bt->max_len = std::max<uint32_t>(bt->max_len, (uint32_t)n);
+            if (n < L->block_elems)
+                ++bt->n_short;
+            ++g;
+        }
+        start += L->numel[t];
+    }
+    bt->P = start;
+    bt->n_distinct_len = (int)lens.size();
+    if (G > 0) {
+        if ((e = hipMalloc((void**)&bt->d_off, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
+            (e = hipMalloc((void**)&bt->d_len, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
+            (e = hipMalloc((void**)&bt->d_tensor, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
+            (e = hipMalloc((void**)&bt->d_elem0, sizeof(uint64_t) * (size_t)G)) != hipSuccess) {
+            free_table(*bt);
+            return fail(MP_E_NOMEM, "block table allocation failed: %s", hipGetErrorString(e));
+        }
+        if ((e = hipMemcpy(bt->d_off, bt->h_off.data(), sizeof(uint64_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
+            (e = hipMemcpy(bt->d_len, bt->h_len.data(), sizeof(uint32_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
+            (e = hipMemcpy(bt->d_tensor, tens.data(), sizeof(uint32_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
+            (e = hipMemcpy(bt->d_elem0, e0.data(), sizeof(uint64_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess) {
+            free_table(*bt);
+            return hip_fail(e, "block table upload");
+        }
+    }
+    *out = bt.get();
+    g_tables.emplace(key, std::move(bt));
+    return MP_OK;
+}
+
+int get_ws(DeviceWs** out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    auto it = g_ws.find(dev);
+    if (it != g_ws.end()) {
+        *out = it->second.get();
+        return MP_OK;
+    }
+    auto w = std::make_unique<DeviceWs>();
+    if ((e = plan_ctl_alloc(&w->plan.ctl)) != hipSuccess ||
+        (e = hipHostMalloc((void**)&w->plan.h_stats, sizeof(uint64_t) * 8, hipHostMallocDefault)) != hipSuccess ||
+        (e = hipMalloc((void**)&w->counters, sizeof(unsigned long long) * 256)) != hipSuccess ||
+        (e = hipHostMalloc((void**)&w->h_counters, sizeof(unsigned long long) * 256, hipHostMallocDefault)) != hipSuccess) {
+        free_ws(dev, *w);
+        return fail(MP_E_NOMEM, "workspace allocation failed: %s", hipGetErrorString(e));
+    }
+    *out = w.get();
+    g_ws.emplace(dev, std::move(w));
+    return MP_OK;
+}
+
+// Plan candidate lists hold at most K * (number of short blocks) entries
+// after the first round: every later candidate is cheaper than a cut unit,
+// hence shorter than block_elems, and each tensor has at most one short block.
+int ensure_lists(PlanScratch& ps, int64_t need)
+{
+    if (ps.list_cap >= need)
+        return MP_OK;
+    (void)hipFree(ps.list[0]);
+    (void)hipFree(ps.list[1]);
+    ps.list[0] = ps.list[1] = nullptr;
+    ps.list_cap = 0;
+    const size_t bytes = sizeof(uint32_t) * (size_t)std::max<int64_t>(need, 1);
+    hipError_t e;
+    if ((e = hipMalloc((void**)&ps.list[0], bytes)) != hipSuccess ||
+        (e = hipMalloc((void**)&ps.list[1], bytes)) != hipSuccess)
+        return fail(MP_E_NOMEM, "plan list allocation failed: %s", hipGetErrorString(e));
+    ps.list_cap = std::max<int64_t>(need, 1);
+    return MP_OK;
+}
+
+// ------------------------------------------------------------ pointer checks
+struct Range {
+    const char* p;
+    size_t n;
+    const char* name;
+};
+
+int check_device_buffer(const void* p, size_t bytes, const char* name)
+{
+    if (p == nullptr)
+        return fail(MP_E_ARG, "%s is NULL", name);
+    if (bytes == 0)
+        return MP_OK;
+    int dev = 0;
+    (void)hipGetDevice(&dev);
+    hipPointerAttribute_t a;
+    std::memset(&a, 0, sizeof a);
+    hipError_t e = hipPointerGetAttributes(&a, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(MP_E_ARG, "%s is not a HIP allocation", name);
+    }
+    if (a.type != hipMemoryTypeDevice && !a.isManaged)
+        return fail(MP_E_ARG, "%s is not device memory", name);
+    if (a.type == hipMemoryTypeDevice && a.device != dev)
+        return fail(MP_E_ARG, "%s lives on device %d, current device is %d", name, a.device, dev);
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    e = hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)p);
+    if (e == hipSuccess) {
+        const char* b = static_cast<const char*>(base);
+        const char* q = static_cast<const char*>(p);
+        if (q < b || (size_t)(q - b) + bytes > size)
+            return fail(MP_E_ARG, "%s: %zu bytes needed, allocation too small", name, bytes);
+    } else {
+        (void)hipGetLastError();
+    }
+    return MP_OK;
+}
+
+int check_pinned_buffer(const void* p, size_t bytes, const char* name)
+{
+    if (p == nullptr)
+        return fail(MP_E_ARG, "%s is NULL", name);
+    if (bytes == 0)
+        return MP_OK;
+    hipPointerAttribute_t a;
+    std::memset(&a, 0, sizeof a);
+    hipError_t e = hipPointerGetAttributes(&a, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(MP_E_ARG, "%s is not pinned host memory", name);
+    }
+    if (a.type != hipMemoryTypeHost)
+        return fail(MP_E_ARG, "%s is not pinned host memory", name);
+    return MP_OK;
+}
+
+bool overlaps(const Range& a, const Range& b)
+{
+    return a.n && b.n && a.p < b.p + b.n && b.p < a.p + a.n;
+}
+
+struct Common {
+    int esize = 0;
+    BlockTable* bt = nullptr;
+    DeviceWs* ws = nullptr;
+    ExpertPtrs ex{};
+    size_t ckpt_bytes = 0;
+};
+
+// Validates the arguments every data entry point shares and resolves the
+// block table / workspace.  `out` may be NULL (index).
+int check_common(const mp_layout* L, const void* base, const void* const* experts, int32_t K,
+                 int32_t residency, const void* out, Common* c)
+{
+    int rc = validate_layout(L, &c->esize);
+    if (rc)
+        return rc;
+    if (K < 1 || K > kMaxK)
+        return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
+    if (residency != MP_DEVICE && residency != MP_HOST_PINNED)
+        return fail(MP_E_ARG, "residency %d is not MP_DEVICE or MP_HOST_PINNED", residency);
+    const int64_t G = count_blocks(L);
+    if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
+        return fail(MP_E_ARG, "K * G = %lld does not fit 32-bit unit ids", (long long)(G * K));
+    int64_t P = 0;
+    for (int32_t t = 0; t < L->n_tensors; ++t)
+        P += L->numel[t];
+    c->ckpt_bytes = (size_t)P * (size_t)c->esize;
+    if (experts == nullptr)
+        return fail(MP_E_ARG, "experts is NULL");
+    if ((rc = check_device_buffer(base, c->ckpt_bytes, "base")))
+        return rc;
+    std::vector<Range> ranges;
+    ranges.push_back({static_cast<const char*>(base), c->ckpt_bytes, "base"});
+    for (int i = 0; i < K; ++i) {
+        char nm[32];
+        std::snprintf(nm, sizeof nm, "experts[%d]", i);
+        if (residency == MP_DEVICE)
+            rc = check_device_buffer(experts[i], c->ckpt_bytes, nm);
+        else
+            rc = check_pinned_buffer(experts[i], c->ckpt_bytes, nm);
+        if (rc)
+            return rc;
+        c->ex.p[i] = experts[i];
+        ranges.push_back({static_cast<const char*>(experts[i]), c->ckpt_bytes, "expert"});
+    }
+    if (out != nullptr) {
+        if ((rc = check_device_buffer(out, c->ckpt_bytes, "out")))
+            return rc;
+        const Range o{static_cast<const char*>(out), c->ckpt_bytes, "out"};
+        for (const Range& r : ranges)
+            if (overlaps(o, r))
+                return fail(MP_E_ARG, "out overlaps %s", r.name);
+    }
+    if ((rc = get_table(L, c->esize, &c->bt)))
+        return rc;
+    if ((rc = get_ws(&c->ws)))
+        return rc;
+    return MP_OK;
+}
+
+__global__ void k_zero_u64(unsigned long long* p, int n)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        p[i] = 0ull;
+}
+
+int run_merge(const mp_layout* L, const void* base, const void* const* experts, int32_t K,
+              int32_t residency, const uint32_t* mask, void* out, mp_io_stats* io, hipStream_t s,
+              const MergeArgs& a)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    Common c;
+    int rc = check_common(L, base, experts, K, residency, out, &c);
+    if (rc)
+        return rc;
+    const BlockTable& bt = *c.bt;
+    if ((rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)bt.G, "mask")))
+        return rc;
+    if (a.op == Op::TIES && bt.max_len > (uint32_t)kTiesMaxBlock)
+        return fail(MP_E_UNSUPPORTED, "TIES supports blocks of at most %d elements", kTiesMaxBlock);
+    unsigned long long* ctr = io ? c.ws->counters : nullptr;
+    hipError_t e;
+    if (ctr) {
+        hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(256), 0, s, ctr, 256);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return hip_fail(e, "counter reset");
+    }
+    mp_io_stats st{};
+    if (residency == MP_DEVICE) {
+        if ((e = launch_merge(bt, a, base, c.ex, K, mask, out, ctr, s)) != hipSuccess)
+            return hip_fail(e, "merge launch");
+    } else {
+        if (!c.ws->pipe)
+            c.ws->pipe = std::make_unique<Pipeline>();
+        rc = c.ws->pipe->merge(bt, a, base, c.ex, K, mask, out, ctr, s, &st, &g_err);
+        if (rc)
+            return rc;
+    }
+    if (io) {
+        if ((e = hipMemcpyAsync(c.ws->h_counters, ctr, sizeof(unsigned long long) * 256,
+                                hipMemcpyDeviceToHost, s)) != hipSuccess)
+            return hip_fail(e, "counter readback");
+        if ((e = hipStreamSynchronize(s)) != hipSuccess)
+            return hip_fail(e, "hipStreamSynchronize");
+        unsigned long long sum = 0;
+        for (int q = 0; q < 256; ++q)
+            sum += c.ws->h_counters[q];
+        st.expert_bytes = sum;
+        st.base_bytes = (uint64_t)bt.P * (uint64_t)bt.esize;
+        st.out_bytes = st.base_bytes;
+        *io = st;
+    }
+    return MP_OK;
+}
+
+}  // namespace
+}  // namespace mp
+
+using namespace mp;
+
+extern "C" {
+
+int mp_layout_blocks(const mp_layout* layout, int64_t* n_blocks)
+{
+    g_err.clear();
+    int es = 0;
+    int rc = validate_layout(layout, &es);
+    if (rc)
+        return rc;
+    if (n_blocks == nullptr)
+        return fail(MP_E_ARG, "n_blocks is NULL");
+    *n_blocks = count_blocks(layout);
+    return MP_OK;
+}
+
+int mp_index_blocks(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                    int32_t residency, float* sumsq, void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    Common c;
+    int rc = check_common(layout, base, experts, K, residency, nullptr, &c);
+    if (rc)
+        return rc;
+    const BlockTable& bt = *c.bt;
+    if ((rc = check_device_buffer(sumsq, sizeof(float) * (size_t)(bt.G * K), "sumsq")))
+        return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (residency == MP_DEVICE) {
+        hipError_t e = launch_index(bt, base, c.ex, K, sumsq, s);
+        if (e != hipSuccess)
+            return hip_fail(e, "index launch");
+        return MP_OK;
+    }
+    if (!c.ws->pipe)
+        c.ws->pipe = std::make_unique<Pipeline>();
+    return c.ws->pipe->index(bt, base, c.ex, K, sumsq, s, &g_err);
+}
+
+int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float* w,
+            uint64_t budget_bytes, uint32_t flags, uint32_t* mask, mp_plan_stats* stats, void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    int es = 0;
+    int rc = validate_layout(layout, &es);
+    if (rc)
+        return rc;
+    if (K < 1 || K > kMaxK)
+        return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
+    if (flags != 0u)
+        return fail(MP_E_UNSUPPORTED, "plan flags 0x%x not supported", flags);
+    if (w == nullptr || stats == nullptr)
+        return fail(MP_E_ARG, "w and stats must not be NULL");
+    const int64_t G = count_blocks(layout);
+    if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
+        return fail(MP_E_ARG, "K * G does not fit 32-bit unit ids");
+    Coeffs cw{};
+    for (int i = 0; i < K; ++i) {
+        if (!std::isfinite(w[i]))
+            return fail(MP_E_ARG, "w[%d] is not finite", i);
+        cw.v[i] = w[i];
+    }
+    if ((rc = check_device_buffer(sumsq, sizeof(float) * (size_t)(G * K), "sumsq")))
+        return rc;
+    if ((rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)G, "mask")))
+        return rc;
+    BlockTable* bt = nullptr;
+    DeviceWs* ws = nullptr;
+    if ((rc = get_table(layout, es, &bt)) || (rc = get_ws(&ws)))
+        return rc;
+    if ((rc = ensure_lists(ws->plan, (int64_t)K * std::max<int64_t>(bt->n_short, 1))))
+        return rc;
+    uint64_t full = 0;
+    for (int64_t g = 0; g < bt->G; ++g)
+        full += (uint64_t)bt->h_len[(size_t)g];
+    full *= (uint64_t)es * (uint64_t)K;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = launch_plan(*bt, ws->plan, K, sumsq, cw, budget_bytes, full, mask, s);
+    if (e != hipSuccess)
+        return hip_fail(e, "plan launch");
+    if ((e = hipStreamSynchronize(s)) != hipSuccess)
+        return hip_fail(e, "hipStreamSynchronize");
+    const uint64_t* h = ws->plan.h_stats;
+    stats->budget_bytes = h[0];
+    stats->cost_bytes = h[1];
+    stats->full_bytes = h[2];
+    stats->n_selected = h[3];
+    stats->n_units = h[4];
+    stats->digest = h[5];
+    if (h[6] != 0)
+        return fail(MP_E_HIP, "plan kernels reported internal error %llu", (unsigned long long)h[6]);
+    if (stats->cost_bytes > budget_bytes)
+        return fail(MP_E_HIP, "plan cost %llu exceeds the budget %llu", (unsigned long long)stats->cost_bytes,
+                    (unsigned long long)budget_bytes);
+    return MP_OK;
+}
+
+int mp_merge_avg(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                 int32_t residency, const uint32_t* mask, const float* alpha, void* out,
+                 mp_io_stats* io, void* stream)
+{
+    MergeArgs a;
+    a.op = Op::AVG;
+    if (alpha == nullptr)
+        return fail(MP_E_ARG, "alpha is NULL");
+    if (K < 1 || K > kMaxK)
+        return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
+    for (int i = 0; i < K; ++i) {
+        if (!std::isfinite(alpha[i]))
+            return fail(MP_E_ARG, "alpha[%d] is not finite", i);
+        a.alpha.v[i] = alpha[i];
+    }
+    return run_merge(layout, base, experts, K, residency, mask, out, io, static_cast<hipStream_t>(stream), a);
+}
+
+int mp_merge_ties(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                  int32_t residency, const uint32_t* mask, double density, float lambda, void* out,
+                  mp_io_stats* io, void* stream)
+{
+    if (!(density >= 0.0 && density <= 1.0))
+        return fail(MP_E_ARG, "density %g must be in [0, 1]", density);
+    if (!std::isfinite(lambda))
+        return fail(MP_E_ARG, "lambda is not finite");
+    MergeArgs a;
+    a.op = Op::TIES;
+    a.density = density;
+    a.lambda = lambda;
+    return run_merge(layout, base, experts, K, residency, mask, out, io, static_cast<hipStream_t>(stream), a);
+}
+
+int mp_merge_dare(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                  int32_t residency, const uint32_t* mask, double p, uint32_t seed, int32_t combine,
+                  const float* alpha, float lambda, void* out, mp_io_stats* io, void* stream)
+{
+    if (!(p >= 0.0 && p < 1.0))
+        return fail(MP_E_ARG, "p %g must be in [0, 1)", p);
+    if (!std::isfinite(lambda))
+        return fail(MP_E_ARG, "lambda is not finite");
+    if (combine != MP_COMBINE_LINEAR && combine != MP_COMBINE_SIGN_ELECT)
+        return fail(MP_E_ARG, "combine %d is not MP_COMBINE_LINEAR or MP_COMBINE_SIGN_ELECT", combine);
+    if (K < 1 || K > kMaxK)
+        return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
+    MergeArgs a;
+    a.op = combine == MP_COMBINE_LINEAR ? Op::DARE_LINEAR : Op::DARE_SIGN;
+    a.p = p;
+    a.seed = seed;
+    a.lambda = lambda;
+    if (combine == MP_COMBINE_LINEAR) {
+        if (alpha == nullptr)
+            return fail(MP_E_ARG, "alpha is NULL");
+        for (int i = 0; i < K; ++i) {
+            if (!std::isfinite(alpha[i]))
+                return fail(MP_E_ARG, "alpha[%d] is not finite", i);
+            a.alpha.v[i] = alpha[i];
+        }
+    }
+    return run_merge(layout, base, experts, K, residency, mask, out, io, static_cast<hipStream_t>(stream), a);
+}
+
+const char* mp_last_error(void) { return g_err.c_str(); }
+
+void mp_release(void)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    for (auto& kv : g_tables)
+        free_table(*kv.second);
+    g_tables.clear();
+    for (auto& kv : g_ws)
+        free_ws(kv.first, *kv.second);
+    g_ws.clear();
+}
+
+}  // extern "C"

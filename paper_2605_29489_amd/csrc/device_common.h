@@ -1,0 +1,103 @@
+// Device helpers shared by the kernel files: element formats, 16-byte chunk
+// access and the counter-based RNG.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace mp {
+
+// ---------------------------------------------------------------- formats
+// A "chunk" is 16 bytes: 4 fp32 or 8 bf16 elements.  Every tensor starts
+// 16-byte aligned (numel is a multiple of the chunk width), and blocks are a
+// multiple of the chunk width long, so a chunk never straddles two blocks.
+
+template <int DT>
+struct Fmt;
+
+template <>
+struct Fmt<0> {  // fp32
+    static constexpr int V = 4;
+    static constexpr int esize = 4;
+    __device__ static inline void unpack(const uint4& c, float* f)
+    {
+        f[0] = __uint_as_float(c.x);
+        f[1] = __uint_as_float(c.y);
+        f[2] = __uint_as_float(c.z);
+        f[3] = __uint_as_float(c.w);
+    }
+    __device__ static inline uint4 pack(const float* f)
+    {
+        return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                          __float_as_uint(f[3]));
+    }
+};
+
+// bfloat16 -> fp32 is exact (the 16 high bits of the fp32 pattern).
+// fp32 -> bfloat16 rounds to nearest, ties to even (inputs are finite).
+__device__ static inline uint32_t bf16_rne_bits(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+template <>
+struct Fmt<1> {  // bf16
+    static constexpr int V = 8;
+    static constexpr int esize = 2;
+    __device__ static inline void unpack(const uint4& c, float* f)
+    {
+        f[0] = __uint_as_float(c.x << 16);
+        f[1] = __uint_as_float(c.x & 0xffff0000u);
+        f[2] = __uint_as_float(c.y << 16);
+        f[3] = __uint_as_float(c.y & 0xffff0000u);
+        f[4] = __uint_as_float(c.z << 16);
+        f[5] = __uint_as_float(c.z & 0xffff0000u);
+        f[6] = __uint_as_float(c.w << 16);
+        f[7] = __uint_as_float(c.w & 0xffff0000u);
+    }
+    __device__ static inline uint4 pack(const float* f)
+    {
+        return make_uint4(bf16_rne_bits(f[0]) | (bf16_rne_bits(f[1]) << 16),
+                          bf16_rne_bits(f[2]) | (bf16_rne_bits(f[3]) << 16),
+                          bf16_rne_bits(f[4]) | (bf16_rne_bits(f[5]) << 16),
+                          bf16_rne_bits(f[6]) | (bf16_rne_bits(f[7]) << 16));
+    }
+};
+
+__device__ static inline const uint4* chunk_ptr(const void* base, uint64_t elem_off, int esize)
+{
+    return reinterpret_cast<const uint4*>(static_cast<const char*>(base) + elem_off * (uint64_t)esize);
+}
+
+// ---------------------------------------------------------------- Philox4x32-10
+// Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3"
+// (SC 2011): ten rounds of two 32x32->64 multiplies with the Weyl-bumped key.
+__device__ static inline uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1)
+{
+    constexpr uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    constexpr uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint32_t lo0 = M0 * c.x, hi0 = __umulhi(M0, c.x);
+        const uint32_t lo1 = M1 * c.z, hi1 = __umulhi(M1, c.z);
+        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+        k0 += W0;
+        k1 += W1;
+    }
+    return c;
+}
+
+// SplitMix64 output function: the value SplitMix64 returns when its state
+// before the step is x (Steele, Lea, Flood 2014).
+__device__ static inline unsigned long long mix64(unsigned long long x)
+{
+    unsigned long long z = x + 0x9e3779b97f4a7c15ull;
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+}
+
+}  // namespace mp

@@ -1,0 +1,131 @@
+// Block-norm index (the catalog statistic of Section 2 / Section 3
+// "Catalog"): S[g*K + i] = sum over block g of d*d, d = x_i - x_0 in fp32.
+//
+// One 256-thread workgroup per block; wave w handles experts w, w+4, ...
+// Each lane streams 16-byte chunks l, l+64, l+128, ... of the block (one
+// coalesced 1 KiB row per wave load), accumulates its chunk elements in
+// order with fma into one fp32 partial, and the wave folds the 64 partials
+// with an xor butterfly.  This fixed order is the one the ABI documents, so
+// the scores -- and therefore the plan -- are reproducible bit for bit.
+// The base block is re-read per expert from L2 (it stays resident: 8-16 KiB
+// per workgroup), so HBM sees it once.
+#include "device_common.h"
+#include "mp_internal.h"
+
+namespace mp {
+
+namespace {
+
+constexpr int kRows = 8;  // chunk rows a lane keeps in flight per expert
+
+template <int DT>
+__device__ inline float block_sumsq(const uint4* __restrict__ b, const uint4* __restrict__ e,
+                                    uint32_t nch, int lane)
+{
+    constexpr int V = Fmt<DT>::V;
+    float p = 0.0f;
+    for (uint32_t c0 = 0; c0 < nch; c0 += 64 * kRows) {
+        uint4 xb[kRows], xe[kRows];
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+            const uint32_t c = c0 + r * 64 + lane;
+            if (c < nch) {
+                xb[r] = b[c];
+                xe[r] = e[c];
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+            const uint32_t c = c0 + r * 64 + lane;
+            if (c < nch) {
+                float fb[V], fe[V];
+                Fmt<DT>::unpack(xb[r], fb);
+                Fmt<DT>::unpack(xe[r], fe);
+#pragma unroll
+                for (int q = 0; q < V; ++q) {
+                    const float d = fe[q] - fb[q];
+                    p = fmaf(d, d, p);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1)
+        p = p + __shfl_xor(p, s);
+    return p;
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, ExpertPtrs ex, int K,
+                                               const uint64_t* __restrict__ boff,
+                                               const uint32_t* __restrict__ blen,
+                                               float* __restrict__ sumsq)
+{
+    const int64_t g = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const uint64_t off = boff[g];
+    const uint32_t nch = blen[g] / Fmt<DT>::V;
+    const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
+    for (int i = wave; i < K; i += 4) {
+        const uint4* e = chunk_ptr(ex.p[i], off, Fmt<DT>::esize);
+        const float s = block_sumsq<DT>(b, e, nch, lane);
+        if (lane == 0)
+            sumsq[g * K + i] = s;
+    }
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_index_staged(const void* __restrict__ base, ExpertPtrs sx,
+                                                      int K, const uint32_t* __restrict__ gid,
+                                                      const uint64_t* __restrict__ soff,
+                                                      const uint64_t* __restrict__ boff,
+                                                      const uint32_t* __restrict__ blen,
+                                                      float* __restrict__ sumsq)
+{
+    const int64_t b = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const uint32_t g = gid[b];
+    const uint32_t nch = blen[g] / Fmt<DT>::V;
+    const uint4* pb = chunk_ptr(base, boff[g], Fmt<DT>::esize);
+    for (int i = wave; i < K; i += 4) {
+        const uint4* pe = chunk_ptr(sx.p[i], soff[b], Fmt<DT>::esize);
+        const float s = block_sumsq<DT>(pb, pe, nch, lane);
+        if (lane == 0)
+            sumsq[(int64_t)g * K + i] = s;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
+                        float* sumsq, hipStream_t s)
+{
+    if (bt.G == 0)
+        return hipSuccess;
+    const dim3 grid((unsigned)bt.G), block(256);
+    if (bt.dtype == 0)
+        hipLaunchKernelGGL(k_index<0>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, sumsq);
+    else
+        hipLaunchKernelGGL(k_index<1>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, sumsq);
+    return hipGetLastError();
+}
+
+hipError_t launch_index_staged(const BlockTable& bt, const void* base, const ExpertPtrs& stage_ex,
+                               int K, const uint32_t* gid, const uint64_t* soff, int64_t nb,
+                               float* sumsq, hipStream_t s)
+{
+    if (nb == 0)
+        return hipSuccess;
+    const dim3 grid((unsigned)nb), block(256);
+    if (bt.dtype == 0)
+        hipLaunchKernelGGL(k_index_staged<0>, grid, block, 0, s, base, stage_ex, K, gid, soff,
+                           bt.d_off, bt.d_len, sumsq);
+    else
+        hipLaunchKernelGGL(k_index_staged<1>, grid, block, 0, s, base, stage_ex, K, gid, soff,
+                           bt.d_off, bt.d_len, sumsq);
+    return hipGetLastError();
+}
+
+}  // namespace mp

@@ -1,0 +1,424 @@
+// Algorithm 1 (PlanGen) on the GPU, bit-exact with a literal sort + greedy.
+//
+// Every unit u = (g, i) gets the 64-bit key  (~bits(score) << 32) | uid
+// with score = float(float(w_i*w_i) * S_u) >= +0, so ascending keys are the
+// candidate order of Algorithm 1 (decreasing score, ties by increasing uid)
+// and keys are unique.  The literal greedy takes every candidate before the
+// first one whose running cost overflows B (the "cut" p), skips p, and then
+// keeps scanning; after p only candidates cheaper than c_p can still fit.
+//
+// So no full sort is needed:
+//   round r:  find the cut key of the current candidate set by a
+//             cost-weighted MSD radix select (8 digit passes of 8 bits;
+//             each pass builds a cost histogram of the candidates that match
+//             the resolved key prefix, in LDS, then one wave scans it);
+//             select every candidate below the cut; the candidates above the
+//             cut that are cheaper than c_p form the next round's set (a
+//             compact uid list), with the remaining budget.
+//   A round whose candidates all fit selects them all and ends the plan.
+// Each round strictly lowers the cost bound, so the number of rounds is at
+// most the number of distinct block lengths of the layout.
+//
+// All control state lives on the device (PlanCtl); the host enqueues a fixed
+// kernel sequence and kernels that are no longer needed return at once.
+#include "device_common.h"
+#include "mp_internal.h"
+
+namespace mp {
+
+struct PlanCtl {
+    unsigned long long brem[9];       // remaining budget before resolving digit d
+    unsigned long long prefix[9];     // key prefix with digits < d resolved
+    unsigned long long hist[3][256];  // rotating cost histograms of digit passes
+    unsigned long long total0;        // candidate cost of the round (all-fit case)
+    unsigned long long sel_cost;
+    unsigned long long sel_count;
+    unsigned long long digest_acc;
+    unsigned long long stats[7];      // budget, cost, full, n_sel, n_units, digest, error
+    unsigned int all_fit;
+    unsigned int done;
+    unsigned int list_n[2];
+    unsigned int error;  // set if an internal invariant failed (reported by the host)
+};
+
+namespace {
+
+constexpr int kT = 256;
+
+__device__ inline unsigned long long unit_key(float S, float w, uint32_t uid)
+{
+    const float w2 = w * w;
+    const float sc = w2 * S;
+    return ((unsigned long long)(~__float_as_uint(sc)) << 32) | uid;
+}
+
+// Wave-level resolution of one digit: h[256] holds the cost of the matching
+// candidates per digit value.  Returns the smallest v with
+// sum_{v' <= v} h[v'] > brem (v = -1 if the total fits), the cost below v,
+// and the total.  Must be called by all 64 lanes of one wave.
+__device__ inline void resolve_digit(const unsigned long long* h, unsigned long long brem, int lane,
+                                     int* v_out, unsigned long long* below_out,
+                                     unsigned long long* total_out)
+{
+    unsigned long long c[4];
+    unsigned long long run = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        run += h[lane * 4 + q];
+        c[q] = run;
+    }
+    unsigned long long incl = run;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const unsigned long long y = __shfl_up(incl, (unsigned)off);
+        if (lane >= off)
+            incl += y;
+    }
+    const unsigned long long excl = incl - run;
+    const unsigned long long total = __shfl(incl, 63);
+    int v = -1;
+    unsigned long long below = 0;
+    if (excl <= brem && incl > brem) {
+        // c[] is non-decreasing and excl + c[3] > brem: q = first slot that overflows
+        const unsigned long long room = brem - excl;
+        const int q = (c[0] <= room) + (c[1] <= room) + (c[2] <= room);
+        v = lane * 4 + q;
+        below = excl + (q == 0 ? 0ull : (q == 1 ? c[0] : (q == 2 ? c[1] : c[2])));
+    }
+    // exactly one lane (or none) found the crossing
+    const unsigned long long bal = __ballot(v >= 0);
+    if (bal) {
+        const int src = __ffsll((long long)bal) - 1;
+        v = __shfl(v, src);
+        below = __shfl(below, src);
+    }
+    *v_out = v;
+    *below_out = below;
+    *total_out = total;
+}
+
+struct CandSrc {
+    // round 0: implicit (all units, one thread per block handling its K units)
+    // later rounds: explicit list of uids
+    const uint32_t* list;  // null in round 0
+    const unsigned int* list_n;
+    unsigned int cap;
+};
+
+__global__ __launch_bounds__(kT) void k_plan_init(PlanCtl* ctl, unsigned long long budget)
+{
+    const int t = threadIdx.x;
+    for (int q = t; q < 3 * 256; q += kT)
+        (&ctl->hist[0][0])[q] = 0ull;
+    if (t == 0) {
+        ctl->brem[0] = budget;
+        ctl->prefix[0] = 0ull;
+        ctl->total0 = 0ull;
+        ctl->sel_cost = 0ull;
+        ctl->sel_count = 0ull;
+        ctl->digest_acc = 0ull;
+        ctl->all_fit = 0u;
+        ctl->done = 0u;
+        ctl->list_n[0] = 0u;
+        ctl->list_n[1] = 0u;
+        ctl->error = 0u;
+    }
+}
+
+// Digit pass d of the current round: resolve digit d-1 (every workgroup does
+// it redundantly from the previous histogram; workgroup 0 publishes it), then
+// histogram digit d of the candidates matching the resolved prefix.
+__global__ __launch_bounds__(kT) void k_plan_hist(PlanCtl* ctl, int d, const float* __restrict__ sumsq,
+                                                  Coeffs w, int K, const uint32_t* __restrict__ blen,
+                                                  uint32_t esize, int64_t G, CandSrc src)
+{
+    __shared__ unsigned long long lh[256];
+    __shared__ unsigned long long s_prefix;
+    __shared__ int s_stop;
+    if (ctl->done || ctl->all_fit)
+        return;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    if (t < 64) {
+        unsigned long long prefix = 0ull, brem = ctl->brem[0];
+        int stop = 0;
+        if (d > 0) {
+            int v;
+            unsigned long long below, total;
+            resolve_digit(ctl->hist[(d - 1) % 3], ctl->brem[d - 1], lane, &v, &below, &total);
+            if (v < 0) {  // digit 0: every candidate fits; later digits: cannot happen
+                stop = 1;
+                if (blockIdx.x == 0 && lane == 0) {
+                    if (d == 1) {
+                        ctl->total0 = total;
+                        ctl->all_fit = 1u;
+                    } else {
+                        ctl->error = 3u;
+                    }
+                }
+            } else {
+                prefix = ctl->prefix[d - 1] | ((unsigned long long)v << (56 - 8 * (d - 1)));
+                brem = ctl->brem[d - 1] - below;
+                if (blockIdx.x == 0 && lane == 0) {
+                    ctl->prefix[d] = prefix;
+                    ctl->brem[d] = brem;
+                }
+            }
+        }
+        if (lane == 0) {
+            s_prefix = prefix;
+            s_stop = stop;
+        }
+    }
+    if (blockIdx.x == 0) {
+        unsigned long long* hn = ctl->hist[(d + 1) % 3];
+        for (int q = t; q < 256; q += kT)
+            hn[q] = 0ull;
+    }
+    lh[t] = 0ull;
+    __syncthreads();
+    if (s_stop)
+        return;
+    const unsigned long long prefix = s_prefix;
+    const int hi_shift = 64 - 8 * d;  // bits above the digit (d > 0)
+    const int dg_shift = 56 - 8 * d;
+    if (src.list == nullptr) {
+        for (int64_t g = (int64_t)blockIdx.x * kT + t; g < G; g += (int64_t)gridDim.x * kT) {
+            const unsigned long long c = (unsigned long long)blen[g] * esize;
+            for (int i = 0; i < K; ++i) {
+                const uint32_t uid = (uint32_t)(g * K + i);
+                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+                if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
+                    atomicAdd(&lh[(key >> dg_shift) & 255u], c);
+            }
+        }
+    } else {
+        const unsigned int n = min(*src.list_n, src.cap);
+        for (unsigned int q = blockIdx.x * kT + t; q < n; q += gridDim.x * kT) {
+            const uint32_t uid = src.list[q];
+            const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
+            const unsigned long long c = (unsigned long long)blen[g] * esize;
+            const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+            if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
+                atomicAdd(&lh[(key >> dg_shift) & 255u], c);
+        }
+    }
+    __syncthreads();
+    if (lh[t])
+        atomicAdd(&ctl->hist[d % 3][t], lh[t]);
+}
+
+// After digit pass 7: resolve the last digit (the cut key p), select the
+// candidates below it, and collect the next round's candidates (above p,
+// cheaper than c_p).  In the all-fit case select every candidate.
+__global__ __launch_bounds__(kT) void k_plan_mark(PlanCtl* ctl, const float* __restrict__ sumsq, Coeffs w,
+                                                  int K, const uint32_t* __restrict__ blen,
+                                                  uint32_t esize, int64_t G, CandSrc src,
+                                                  uint32_t* __restrict__ mask, uint32_t* __restrict__ next,
+                                                  unsigned int* __restrict__ next_n, unsigned int next_cap)
+{
+    __shared__ unsigned long long s_keyp, s_cp;
+    __shared__ int s_all;
+    __shared__ unsigned long long s_cost[4], s_cnt[4];
+    if (ctl->done)
+        return;
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    if (t < 64) {
+        int all = (int)ctl->all_fit;
+        unsigned long long keyp = 0ull, cp = 0ull;
+        if (!all) {
+            int v;
+            unsigned long long below, total;
+            resolve_digit(ctl->hist[7 % 3], ctl->brem[7], lane, &v, &below, &total);
+            keyp = ctl->prefix[7] | (unsigned long long)(unsigned)(v < 0 ? 0 : v);
+            const uint32_t gp = (uint32_t)keyp / (uint32_t)K;
+            if (v < 0 || (int64_t)gp >= G) {  // cannot happen: the cut is a real unit
+                if (lane == 0)
+                    ctl->error = 1u;
+                keyp = 0ull;  // select nothing more this round
+                cp = 0ull;
+            } else {
+                cp = (unsigned long long)blen[gp] * esize;
+            }
+            if (blockIdx.x == 0 && lane == 0) {
+                ctl->prefix[8] = keyp;
+                ctl->brem[8] = ctl->brem[7] - below;
+            }
+        }
+        if (lane == 0) {
+            s_keyp = keyp;
+            s_cp = cp;
+            s_all = all;
+        }
+    }
+    __syncthreads();
+    const unsigned long long keyp = s_keyp, cp = s_cp;
+    const int all = s_all;
+    unsigned long long my_cost = 0ull, my_cnt = 0ull;
+    if (src.list == nullptr) {
+        for (int64_t g = (int64_t)blockIdx.x * kT + t; g < G; g += (int64_t)gridDim.x * kT) {
+            const unsigned long long c = (unsigned long long)blen[g] * esize;
+            uint32_t word = 0u;
+            for (int i = 0; i < K; ++i) {
+                const uint32_t uid = (uint32_t)(g * K + i);
+                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+                if (all || key < keyp) {
+                    word |= 1u << i;
+                    my_cost += c;
+                    my_cnt += 1;
+                } else if (key > keyp && c < cp) {
+                    const unsigned int slot = atomicAdd(next_n, 1u);
+                    if (slot < next_cap)
+                        next[slot] = uid;
+                    else
+                        ctl->error = 2u;
+                }
+            }
+            mask[g] = word;
+        }
+    } else {
+        const unsigned int n = min(*src.list_n, src.cap);
+        for (unsigned int q = blockIdx.x * kT + t; q < n; q += gridDim.x * kT) {
+            const uint32_t uid = src.list[q];
+            const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
+            const unsigned long long c = (unsigned long long)blen[g] * esize;
+            const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+            if (all || key < keyp) {
+                atomicOr(&mask[g], 1u << i);
+                my_cost += c;
+                my_cnt += 1;
+            } else if (key > keyp && c < cp) {
+                const unsigned int slot = atomicAdd(next_n, 1u);
+                if (slot < next_cap)
+                    next[slot] = uid;
+                else
+                    ctl->error = 2u;
+            }
+        }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        my_cost += __shfl_xor(my_cost, off);
+        my_cnt += __shfl_xor(my_cnt, off);
+    }
+    if (lane == 0) {
+        s_cost[wave] = my_cost;
+        s_cnt[wave] = my_cnt;
+    }
+    __syncthreads();
+    if (t == 0) {
+        const unsigned long long cs = s_cost[0] + s_cost[1] + s_cost[2] + s_cost[3];
+        const unsigned long long cn = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
+        if (cn) {
+            atomicAdd(&ctl->sel_cost, cs);
+            atomicAdd(&ctl->sel_count, cn);
+        }
+    }
+}
+
+// Close round r: carry the remaining budget, reset the digit state, and
+// finish the plan when everything fit or no cheaper candidate is left.
+__global__ void k_plan_advance(PlanCtl* ctl, int next_list, int reuse_list)
+{
+    if (threadIdx.x != 0 || ctl->done)
+        return;
+    unsigned long long rem;
+    if (ctl->all_fit) {
+        rem = ctl->brem[0] - ctl->total0;
+        ctl->done = 1u;
+    } else {
+        rem = ctl->brem[8];
+        if (ctl->list_n[next_list] == 0u)
+            ctl->done = 1u;
+    }
+    ctl->brem[0] = rem;
+    ctl->prefix[0] = 0ull;
+    for (int q = 0; q < 3 * 256; ++q)
+        (&ctl->hist[0][0])[q] = 0ull;
+    ctl->all_fit = 0u;
+    ctl->list_n[reuse_list] = 0u;
+}
+
+__global__ __launch_bounds__(kT) void k_plan_digest(PlanCtl* ctl, const uint32_t* __restrict__ mask, int64_t G)
+{
+    __shared__ unsigned long long s[4];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    unsigned long long acc = 0ull;
+    for (int64_t g = (int64_t)blockIdx.x * kT + t; g < G; g += (int64_t)gridDim.x * kT)
+        acc += mix64(((unsigned long long)g << 32) | mask[g]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        acc += __shfl_xor(acc, off);
+    if (lane == 0)
+        s[wave] = acc;
+    __syncthreads();
+    if (t == 0)
+        atomicAdd(&ctl->digest_acc, s[0] + s[1] + s[2] + s[3]);
+}
+
+__global__ void k_plan_final(PlanCtl* ctl, unsigned long long budget, unsigned long long full,
+                             unsigned long long n_units)
+{
+    if (threadIdx.x != 0)
+        return;
+    ctl->stats[0] = budget;
+    ctl->stats[1] = ctl->sel_cost;
+    ctl->stats[2] = full;
+    ctl->stats[3] = ctl->sel_count;
+    ctl->stats[4] = n_units;
+    ctl->stats[5] = mix64(ctl->digest_acc ^ ctl->sel_cost);
+    ctl->stats[6] = ctl->error;
+}
+
+}  // namespace
+
+hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
+                       const Coeffs& w, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
+                       hipStream_t s)
+{
+    PlanCtl* ctl = ps.ctl;
+    const uint32_t es = (uint32_t)bt.esize;
+    hipLaunchKernelGGL(k_plan_init, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget);
+    if (bt.G > 0) {
+        const int64_t want = (bt.G + kT - 1) / kT;
+        const unsigned grid0 = (unsigned)(want < 2048 ? want : 2048);
+        const unsigned gridL = 64;
+        const int rounds = bt.n_distinct_len;
+        for (int r = 0; r < rounds; ++r) {
+            CandSrc src;
+            unsigned grid;
+            if (r == 0) {
+                src.list = nullptr;
+                src.list_n = nullptr;
+                src.cap = 0u;
+                grid = grid0;
+            } else {
+                src.list = ps.list[r & 1];
+                src.list_n = &ctl->list_n[r & 1];
+                src.cap = (unsigned)ps.list_cap;
+                grid = gridL;
+            }
+            const int nxt = (r + 1) & 1;
+            for (int d = 0; d < 8; ++d)
+                hipLaunchKernelGGL(k_plan_hist, dim3(grid), dim3(kT), 0, s, ctl, d, sumsq, w, K,
+                                   bt.d_len, es, bt.G, src);
+            hipLaunchKernelGGL(k_plan_mark, dim3(grid), dim3(kT), 0, s, ctl, sumsq, w, K, bt.d_len,
+                               es, bt.G, src, mask, ps.list[nxt], &ctl->list_n[nxt],
+                               (unsigned)ps.list_cap);
+            hipLaunchKernelGGL(k_plan_advance, dim3(1), dim3(64), 0, s, ctl, nxt, r & 1);
+        }
+        const unsigned gridD = grid0;
+        hipLaunchKernelGGL(k_plan_digest, dim3(gridD), dim3(kT), 0, s, ctl, mask, bt.G);
+    }
+    hipLaunchKernelGGL(k_plan_final, dim3(1), dim3(64), 0, s, ctl, (unsigned long long)budget,
+                       (unsigned long long)full_bytes, (unsigned long long)(bt.G * K));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    return hipMemcpyAsync(ps.h_stats, ctl->stats, sizeof(ctl->stats), hipMemcpyDeviceToHost, s);
+}
+
+hipError_t plan_ctl_alloc(PlanCtl** ctl) { return hipMalloc((void**)ctl, sizeof(PlanCtl)); }
+
+}  // namespace mp

@@ -1,0 +1,107 @@
+// Internal declarations shared by the host runtime and the kernel files of
+// libmergepipe.so.  Not part of the public ABI (include/mergepipe.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/mergepipe.h"
+
+namespace mp {
+
+constexpr int kMaxK = 32;
+constexpr int kTiesMaxBlock = 4096;  // elements per block the TIES kernel holds in registers
+
+// K expert base pointers, passed to kernels by value.
+struct ExpertPtrs {
+    const void* p[kMaxK];
+};
+
+// Per-expert fp32 coefficients, passed to kernels by value.
+struct Coeffs {
+    float v[kMaxK];
+};
+
+// Device-resident description of a layout's block partition (one per
+// (device, layout) pair, cached by the runtime).
+struct BlockTable {
+    int device = -1;
+    int32_t dtype = 0;
+    int32_t esize = 0;       // bytes per element
+    int64_t block_elems = 0;
+    int64_t n_tensors = 0;
+    int64_t G = 0;           // number of blocks
+    int64_t P = 0;           // elements per checkpoint
+    uint32_t max_len = 0;    // longest block
+    int n_distinct_len = 0;  // distinct block lengths (bounds the plan rounds)
+    int64_t n_short = 0;     // blocks shorter than block_elems
+    std::vector<int64_t> numel;
+    // host copies
+    std::vector<uint64_t> h_off;
+    std::vector<uint32_t> h_len;
+    // device arrays [G]
+    uint64_t* d_off = nullptr;     // element offset of the block in a checkpoint
+    uint32_t* d_len = nullptr;     // elements in the block
+    uint32_t* d_tensor = nullptr;  // tensor id
+    uint64_t* d_elem0 = nullptr;   // index of the block's first element inside its tensor
+};
+
+// Device control block of the plan (see k_plan.hip).
+struct PlanCtl;
+
+// Per-device plan scratch.
+struct PlanScratch {
+    PlanCtl* ctl = nullptr;
+    uint32_t* list[2] = {nullptr, nullptr};  // candidate uid lists for the later rounds
+    int64_t list_cap = 0;
+    uint64_t* h_stats = nullptr;  // pinned host mirror of the stats
+};
+
+// ---------------------------------------------------------------- launchers
+// All launchers enqueue on `s` and return the launch status.
+
+hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
+                        float* sumsq, hipStream_t s);
+
+// Index over an explicit list of blocks whose data sits in compact staging
+// buffers (host-streamed experts): block b of the list is block gid[b] of
+// the layout and its expert i data starts at stage_ex[i] + soff[b] elements;
+// the base block is read from base at its layout offset.
+hipError_t launch_index_staged(const BlockTable& bt, const void* base, const ExpertPtrs& stage_ex,
+                               int K, const uint32_t* gid, const uint64_t* soff, int64_t nb,
+                               float* sumsq, hipStream_t s);
+
+hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
+                       const Coeffs& w, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
+                       hipStream_t s);
+
+// Merge operators.  `counters` is null or a device array of 256 uint64
+// accumulating the expert bytes the kernels load.
+enum class Op { AVG = 0, TIES = 1, DARE_LINEAR = 2, DARE_SIGN = 3 };
+
+struct MergeArgs {
+    Op op = Op::AVG;
+    Coeffs alpha{};
+    double density = 0.0;
+    float lambda = 1.0f;
+    double p = 0.0;
+    uint32_t seed = 0;
+};
+
+hipError_t launch_merge(const BlockTable& bt, const MergeArgs& a, const void* base,
+                        const ExpertPtrs& ex, int K, const uint32_t* mask, void* out,
+                        unsigned long long* counters, hipStream_t s);
+
+// Merge over a subset of blocks whose selected expert data is packed in a
+// device staging buffer (host-streamed experts).  For list entry b (layout
+// block gid[b]) the selected experts' blocks lie back to back, in
+// increasing expert order, starting at byte soff[b] of `stage`.
+hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const void* base,
+                               const void* stage, int K, const uint32_t* mask,
+                               const uint32_t* gid, const uint64_t* soff, int64_t nb, void* out,
+                               unsigned long long* counters, hipStream_t s);
+
+}  // namespace mp

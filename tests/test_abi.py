@@ -1,0 +1,105 @@
+"""The C ABI library loads, exports every entry point include/mergepipe.h
+declares, and rejects invalid arguments before touching the GPU.  Runs on the
+CPU: none of the calls below reaches a HIP runtime call."""
+
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mergepipe.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mp_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def mp():
+    import paper_2605_29489_amd as m
+    return m
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ("mp_layout_blocks", "mp_index_blocks", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+              "mp_merge_dare", "mp_last_error", "mp_release"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(mp):
+    lib = C.CDLL(mp.LIB_PATH)
+    for n in _declared():
+        assert hasattr(lib, n), n
+    assert set(mp.EXPORTS) <= set(_declared())
+
+
+def test_struct_layouts_match_header(mp):
+    # mp_layout: int32, int32, pointer, int64 -> 24 bytes on LP64
+    assert C.sizeof(mp.mp_layout) == 24
+    assert C.sizeof(mp.mp_plan_stats) == 48
+    assert C.sizeof(mp.mp_io_stats) == 48
+
+
+def test_layout_blocks_counts(mp):
+    from workloads import family_spec
+    for name, G in (("qwen2.5-1.5b", 376989), ("llama3-8b", 1960513), ("qwen2.5-7b", 1859341), ("toy", 1024)):
+        lay = family_spec(name).layout
+        L = mp.Layout(lay.numel, lay.block_elems, lay.dtype_code)
+        assert mp.mp_layout_blocks(L) == G
+    assert mp.mp_layout_blocks(mp.Layout([], 4096, mp.MP_BF16)) == 0
+
+
+@pytest.mark.parametrize("numel,be,dt", [
+    ([4096], 4100, 1),   # block not a multiple of 8 bf16 elements
+    ([4100], 4096, 1),   # tensor not 16-byte aligned
+    ([4096], 0, 0),
+    ([-8], 4096, 0),
+    ([4096], 4096, 7),   # bad dtype
+])
+def test_layout_validation(mp, numel, be, dt):
+    L = mp.Layout(numel, be, dt)
+    with pytest.raises(mp.MPError) as e:
+        mp.mp_layout_blocks(L)
+    assert e.value.code == mp.MP_E_ARG
+    assert mp.mp_last_error() != ""
+
+
+def test_argument_errors_before_any_device_call(mp):
+    L = mp.Layout([4096], 4096, mp.MP_BF16)
+    lib = mp.lib
+    ptrs = (C.c_void_p * 33)()
+    # K out of range
+    for K in (0, 33):
+        assert lib.mp_index_blocks(L.ref, None, ptrs, K, 0, None, None) == mp.MP_E_ARG
+        st = mp.mp_plan_stats()
+        w = (C.c_float * 33)(*([1.0] * 33))
+        assert lib.mp_plan(L.ref, K, None, w, 0, 0, None, C.byref(st), None) == mp.MP_E_ARG
+    # bad residency
+    assert lib.mp_index_blocks(L.ref, None, ptrs, 1, 5, None, None) == mp.MP_E_ARG
+    # unsupported plan flags
+    st = mp.mp_plan_stats()
+    w = (C.c_float * 1)(1.0)
+    assert lib.mp_plan(L.ref, 1, None, w, 0, 1, None, C.byref(st), None) == mp.MP_E_UNSUPPORTED
+    # non-finite plan weight
+    wn = (C.c_float * 1)(float("nan"))
+    assert lib.mp_plan(L.ref, 1, None, wn, 0, 0, None, C.byref(st), None) == mp.MP_E_ARG
+    # TIES density and DARE p/combine ranges
+    assert lib.mp_merge_ties(L.ref, None, ptrs, 1, 0, None, 1.5, 1.0, None, None, None) == mp.MP_E_ARG
+    assert lib.mp_merge_ties(L.ref, None, ptrs, 1, 0, None, -0.1, 1.0, None, None, None) == mp.MP_E_ARG
+    a = (C.c_float * 1)(1.0)
+    assert lib.mp_merge_dare(L.ref, None, ptrs, 1, 0, None, 1.0, 0, 0, a, 1.0, None, None, None) == mp.MP_E_ARG
+    assert lib.mp_merge_dare(L.ref, None, ptrs, 1, 0, None, 0.5, 0, 9, a, 1.0, None, None, None) == mp.MP_E_ARG
+    assert lib.mp_merge_dare(L.ref, None, ptrs, 1, 0, None, 0.5, 0, 0, None, 1.0, None, None, None) == mp.MP_E_ARG
+    # AVG with NULL / non-finite alpha
+    assert lib.mp_merge_avg(L.ref, None, ptrs, 1, 0, None, None, None, None, None) == mp.MP_E_ARG
+    an = (C.c_float * 1)(float("inf"))
+    assert lib.mp_merge_avg(L.ref, None, ptrs, 1, 0, None, an, None, None, None) == mp.MP_E_ARG
+    # unit ids must fit 32 bits: 2^28 blocks x 32 experts
+    big = mp.Layout([4096 * (1 << 28)], 4096, mp.MP_BF16)
+    assert lib.mp_index_blocks(big.ref, None, ptrs, 32, 0, None, None) == mp.MP_E_ARG
+    assert "32-bit" in mp.mp_last_error()

@@ -1,0 +1,308 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle, on the
+same seeded inputs.
+
+Bars: index (sumsq), mask and plan statistics bit-exact; merged weights
+within 1e-6 relative (fp32) or 1 bf16 ulp after the final rounding
+(`assert_merge_equal`); the expert bytes the merge kernels load equal the
+plan's cost (Prop. 1: the executor reads only selected blocks).
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from tests.gpu_util import assert_merge_equal, gather_blocks, to_dev, to_host
+from workloads import FamilySpec, family_spec, make_family
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def mp():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2605_29489_amd as m
+    return m
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _mini_qwen(n_layers=2, K=4, dtype="bf16", be=4096):
+    """Small family with the Qwen tensor pattern: full blocks, biases and
+    norms (short blocks: 256 and 64 elements) and ragged tensor tails."""
+    hidden, ffn, vocab = 256, 704, 520
+    t = [("embed_tokens.weight", (vocab, hidden))]
+    for l in range(n_layers):
+        p = f"layers.{l}."
+        t += [(p + "q.weight", (hidden, hidden)), (p + "q.bias", (hidden,)),
+              (p + "k.weight", (64, hidden)), (p + "k.bias", (64,)),
+              (p + "v.weight", (64, hidden)), (p + "v.bias", (64,)),
+              (p + "o.weight", (hidden, hidden)),
+              (p + "gate.weight", (ffn, hidden)), (p + "up.weight", (ffn, hidden)),
+              (p + "down.weight", (hidden, ffn)),
+              (p + "input_layernorm.weight", (hidden,)), (p + "post_attention_layernorm.weight", (hidden,))]
+    t.append(("norm.weight", (hidden,)))
+    return FamilySpec("mini-qwen", tuple(t), dtype, be, K, ())
+
+
+def _ragged_f32(K=3):
+    t = (("a", (3 * 4096 + 4,)), ("b", (8,)), ("c", (4096,)), ("d", (2052,)), ("e", (4, 1025)))
+    return FamilySpec("ragged-f32", t, "f32", 4096, K, ())
+
+
+def _lay(mp, spec):
+    lay = spec.layout
+    return mp.Layout(lay.numel, lay.block_elems, lay.dtype_code), lay
+
+
+def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, **kw):
+    """Index, plan and merge on the GPU and with the oracle; compare."""
+    import torch
+    L, lay = _lay(mp, spec)
+    K = len(exps_np)
+    dtype = lay.dtype
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    G = blocks.G
+    base = to_dev(base_np, dtype)
+    exps = [to_dev(e, dtype) for e in exps_np]
+    sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
+    mp.mp_index_blocks(L, base, exps, sumsq)
+    S_gpu = sumsq.cpu().numpy()
+    S_orc = oracle.index(blocks, dtype, base_np, exps_np).reshape(-1)
+    assert np.array_equal(S_gpu.view(np.uint32), S_orc.view(np.uint32)), "index differs"
+    if w is None:
+        w = [1.0 / K] * K if op in ("avg", "dare_lin") else [1.0] * K
+    full = int(blocks.len.sum()) * lay.elem_bytes * K
+    out = torch.empty_like(base)
+    mask = torch.empty(G, dtype=torch.int32, device="cuda")
+    results = []
+    for f in budgets:
+        B = int(f * full) if isinstance(f, float) else int(f)
+        st = mp.mp_plan(L, K, sumsq, w, B, mask)
+        m_gpu = mask.cpu().numpy().view(np.uint32)
+        m_orc, st_orc = oracle.plan(blocks, dtype, K, S_orc, w, B)
+        assert np.array_equal(m_gpu, m_orc), f"mask differs at B={B}"
+        assert st["cost_bytes"] == st_orc["cost"] <= B
+        assert st["n_selected"] == st_orc["n_selected"]
+        assert st["full_bytes"] == st_orc["full_bytes"] == full
+        assert st["digest"] == st_orc["digest"]
+        assert st["n_units"] == G * K and st["budget_bytes"] == B
+        if op == "avg":
+            io = mp.mp_merge_avg(L, base, exps, mask, kw["alpha"], out, io=True)
+            want = oracle.merge_avg(blocks, dtype, base_np, exps_np, m_orc, kw["alpha"])
+        elif op == "ties":
+            io = mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out, io=True)
+            want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"])
+        else:
+            comb = 0 if op == "dare_lin" else 1
+            io = mp.mp_merge_dare(L, base, exps, mask, kw["p"], kw["seed"], comb, kw.get("alpha"), kw["lam"],
+                                  out, io=True)
+            want = oracle.merge_dare(blocks, dtype, base_np, exps_np, m_orc, kw["p"], kw["seed"], comb,
+                                     kw.get("alpha", [1.0] * K), kw["lam"])
+        got = to_host(out)
+        nb = assert_merge_equal(got, want, base_np, dtype, f"{op} B={B}")
+        assert io["expert_bytes"] == st["cost_bytes"], "kernels loaded bytes outside the plan"
+        results.append((B, st, nb))
+        _say(f"  {spec.name} {op} B={B}: cost={st['cost_bytes']} sel={st['n_selected']} non-bitwise={nb}")
+    return results
+
+
+# ---------------------------------------------------------------- small families
+
+@pytest.mark.parametrize("op", ["avg", "ties", "dare_lin", "dare_sign"])
+def test_mini_qwen_bf16_all_ops(mp, op):
+    spec = _mini_qwen()
+    base, exps = make_family(spec, seed=1)
+    kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0, p=0.9, seed=7)
+    _say(f"case mini-qwen bf16 {op}")
+    _run_all(mp, spec, base, exps, op, [0, 0.1, 0.25, 0.5, 0.77, 1.0, 2.0, 12345], **kw)
+
+
+@pytest.mark.parametrize("op", ["avg", "ties", "dare_lin", "dare_sign"])
+def test_ragged_fp32_all_ops(mp, op):
+    spec = _ragged_f32()
+    base, exps = make_family(spec, seed=2)
+    kw = dict(alpha=[0.5, 0.25, 0.25], density=0.1, lam=0.8, p=0.5, seed=3)
+    _say(f"case ragged fp32 {op}")
+    _run_all(mp, spec, base, exps, op, [0, 0.3, 0.6, 1.0], **kw)
+
+
+def test_toy_config_avg_full_parity(mp):
+    # BASELINE toy family: fp32 8 x (512x1024), K=4, AVG 1/K, B = 50%
+    spec = family_spec("toy")
+    base, exps = make_family(spec, seed=0)
+    _say("case toy fp32 avg")
+    _run_all(mp, spec, base, exps, "avg", [0.5, 0.25, 1.0], alpha=[0.25] * 4)
+
+
+@pytest.mark.parametrize("K", [1, 2, 7, 32])
+def test_expert_counts(mp, K):
+    spec = _mini_qwen(n_layers=1, K=K)
+    base, exps = make_family(spec, K=K, seed=10 + K)
+    _say(f"case mini-qwen K={K}")
+    _run_all(mp, spec, base, exps, "ties", [0.0, 0.4, 1.0], density=0.2, lam=1.0)
+    _run_all(mp, spec, base, exps, "avg", [0.4], alpha=[1.0 / K] * K)
+
+
+@pytest.mark.parametrize("be", [1024, 2048, 512])
+def test_block_sizes(mp, be):
+    spec = _mini_qwen(n_layers=1, be=be)
+    base, exps = make_family(spec, seed=4)
+    _say(f"case block_elems={be}")
+    _run_all(mp, spec, base, exps, "ties", [0.35, 1.0], density=0.3, lam=1.0)
+    _run_all(mp, spec, base, exps, "dare_lin", [0.5], alpha=[0.3, 0.2, 0.4, 0.1], p=0.3, seed=11, lam=1.0)
+
+
+def test_large_blocks_avg_dare_and_ties_unsupported(mp):
+    import torch
+    spec = _mini_qwen(n_layers=1, be=8192)
+    base, exps = make_family(spec, seed=5)
+    _say("case block_elems=8192")
+    _run_all(mp, spec, base, exps, "avg", [0.5], alpha=[0.25] * 4)
+    _run_all(mp, spec, base, exps, "dare_sign", [0.5], p=0.2, seed=1, lam=1.0)
+    L, lay = _lay(mp, spec)
+    b = to_dev(base, "bf16")
+    e = [to_dev(x, "bf16") for x in exps]
+    mask = torch.zeros(oracle.Blocks(lay.numel, 8192).G, dtype=torch.int32, device="cuda")
+    with pytest.raises(mp.MPError) as err:
+        mp.mp_merge_ties(L, b, e, mask, 0.2, 1.0, torch.empty_like(b))
+    assert err.value.code == mp.MP_E_UNSUPPORTED
+
+
+def test_ties_and_zero_and_identical_experts(mp):
+    # identical experts -> exact score ties (tie-break on uid); an all-zero
+    # expert -> zero scores; heavy value ties inside blocks (coarse deltas)
+    spec = _mini_qwen(n_layers=1, K=4)
+    base, exps = make_family(spec, seed=6)
+    exps = [exps[0], exps[0].copy(), base.copy(), exps[1]]
+    _say("case identical/zero experts")
+    _run_all(mp, spec, base, exps, "ties", [0.1, 0.3, 0.5, 0.74, 0.75, 0.76, 1.0], density=0.2, lam=1.0)
+    _run_all(mp, spec, base, exps, "avg", [0.3, 0.6], alpha=[0.25] * 4)
+    coarse = [base.copy() for _ in range(3)]
+    rng = np.random.default_rng(0)
+    for c in coarse:
+        sel = rng.random(c.size) < 0.5
+        c[sel] = (c[sel].astype(np.int32) + rng.integers(-2, 3, int(sel.sum()))).astype(np.uint16)
+    _say("case coarse ties")
+    _run_all(mp, spec, base, coarse, "ties", [0.5, 1.0], density=0.15, lam=1.0)
+
+
+def test_budget_boundaries_exact(mp):
+    # budgets at the exact cost of a greedy prefix, one byte below and above
+    spec = _mini_qwen(n_layers=1)
+    base, exps = make_family(spec, seed=8)
+    lay = spec.layout
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    S = oracle.index(blocks, "bf16", base, exps).reshape(-1)
+    _, st = oracle.plan(blocks, "bf16", 4, S, [1.0] * 4, int(0.37 * int(blocks.len.sum()) * 8))
+    c = st["cost"]
+    _say("case budget boundaries")
+    _run_all(mp, spec, base, exps, "ties", [c - 1, c, c + 1, 1, 511, 512, 513], density=0.2, lam=1.0)
+
+
+def test_empty_layout(mp):
+    import torch
+    L = mp.Layout([], 4096, mp.MP_BF16)
+    base = torch.zeros(8, dtype=torch.bfloat16, device="cuda")
+    exps = [torch.zeros(8, dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+    sumsq = torch.zeros(1, dtype=torch.float32, device="cuda")
+    mask = torch.zeros(1, dtype=torch.int32, device="cuda")
+    mp.mp_index_blocks(L, base, exps, sumsq)
+    st = mp.mp_plan(L, 2, sumsq, [1.0, 1.0], 100, mask)
+    assert st["cost_bytes"] == 0 and st["n_units"] == 0 and st["n_selected"] == 0
+    assert st["digest"] == oracle.mix64(0)
+    mp.mp_merge_ties(L, base, exps, mask, 0.2, 1.0, torch.empty_like(base))
+
+
+def test_non_anticipation_and_determinism(mp):
+    # P3: changing unselected expert blocks leaves the output bitwise unchanged;
+    # two runs are bit-identical.
+    import torch
+    spec = _mini_qwen(n_layers=1)
+    base_np, exps_np = make_family(spec, seed=9)
+    L, lay = _lay(mp, spec)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    base = to_dev(base_np, "bf16")
+    exps = [to_dev(e, "bf16") for e in exps_np]
+    sumsq = torch.empty(blocks.G * 4, dtype=torch.float32, device="cuda")
+    mp.mp_index_blocks(L, base, exps, sumsq)
+    mask = torch.empty(blocks.G, dtype=torch.int32, device="cuda")
+    full = int(blocks.len.sum()) * 2 * 4
+    mp.mp_plan(L, 4, sumsq, [1.0] * 4, full // 3, mask)
+    m = mask.cpu().numpy().view(np.uint32)
+    outs = {}
+    for op in ("ties", "avg", "dare_sign"):
+        o1, o2 = torch.empty_like(base), torch.empty_like(base)
+        run = {
+            "ties": lambda ex, o: mp.mp_merge_ties(L, base, ex, mask, 0.2, 1.0, o),
+            "avg": lambda ex, o: mp.mp_merge_avg(L, base, ex, mask, [0.25] * 4, o),
+            "dare_sign": lambda ex, o: mp.mp_merge_dare(L, base, ex, mask, 0.9, 7, 1, None, 1.0, o),
+        }[op]
+        run(exps, o1)
+        junk = [e.clone() for e in exps]
+        for i in range(4):
+            for g in np.nonzero(((m >> i) & 1) == 0)[0]:
+                junk[i][blocks.off[g]:blocks.off[g] + blocks.len[g]] = 7.0
+        run(junk, o2)
+        o3 = torch.empty_like(base)
+        run(exps, o3)
+        assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)), op
+        assert torch.equal(o1.view(torch.int16), o3.view(torch.int16)), op
+
+
+class _RawDeviceBuffer:
+    """An exact-size hipMalloc allocation (torch's caching allocator may hand
+    out a slice of a larger segment, which hides an undersized buffer)."""
+
+    def __init__(self, nbytes):
+        import ctypes
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._p = ctypes.c_void_p()
+        assert self._hip.hipMalloc(ctypes.byref(self._p), ctypes.c_size_t(nbytes)) == 0
+        self.nbytes = nbytes
+
+    def data_ptr(self):
+        return self._p.value
+
+    def free(self):
+        self._hip.hipFree(self._p)
+
+
+def test_invalid_device_arguments_rejected(mp):
+    import torch
+    spec = _mini_qwen(n_layers=1)
+    L, lay = _lay(mp, spec)
+    P = lay.n_params
+    base = torch.zeros(P, dtype=torch.bfloat16, device="cuda")
+    exps = [torch.zeros(P, dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+    G = oracle.Blocks(lay.numel, lay.block_elems).G
+    mask = torch.zeros(G, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(base)
+    host = torch.zeros(P, dtype=torch.bfloat16)
+    with pytest.raises(mp.MPError):  # host buffer where device memory is required
+        mp.mp_merge_avg(L, host, exps, mask, [0.5, 0.5], out)
+    with pytest.raises(mp.MPError):  # output aliases an expert
+        mp.mp_merge_avg(L, base, exps, mask, [0.5, 0.5], exps[1])
+    with pytest.raises(mp.MPError):  # pageable host expert with MP_HOST_PINNED
+        mp.mp_merge_avg(L, base, [host, host], mask, [0.5, 0.5], out, residency=mp.MP_HOST_PINNED)
+    small_out = _RawDeviceBuffer(P)  # half the bytes a bf16 checkpoint needs
+    small_mask = _RawDeviceBuffer(2 * G)
+    small_sumsq = _RawDeviceBuffer(4 * G)
+    try:
+        with pytest.raises(mp.MPError):
+            mp.mp_merge_avg(L, base, exps, mask, [0.5, 0.5], small_out)
+        with pytest.raises(mp.MPError):
+            mp.mp_merge_ties(L, base, exps, small_mask, 0.2, 1.0, out)
+        with pytest.raises(mp.MPError):
+            mp.mp_index_blocks(L, base, exps, small_sumsq)
+    finally:
+        torch.cuda.synchronize()
+        for b in (small_out, small_mask, small_sumsq):
+            b.free()
