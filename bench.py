@@ -1,0 +1,241 @@
+#!/usr/bin/env python3
+"""Benchmark of the budgeted-merge hot path on one MI355X.
+
+Workload: a synthetic Qwen2.5-1.5B-shaped bf16 checkpoint family (28 layers,
+hidden 1536, FFN 8960, 12 q / 2 kv heads x 128, vocab 151936, tied
+embeddings; P = 1,543,714,304 parameters, G = 376,989 blocks of 4096) with
+K = 4 experts, merged with budgeted TIES (keep density 0.2, lambda 1) at
+B = 25%, 50% and 100% of the expert bytes.
+
+One step = index the expert deltas once (per-block squared norms), then for
+each budget: plan (Algorithm 1) + TIES merge.  All inputs are resident in HBM
+before the timed region.  The metric is merged parameters per second (3 P
+per step); effective HBM GB/s and the roofline fraction come from HIP events
+around each kernel-launching call on the stream the kernels run on.
+
+The CPU baseline is the oracle (test infrastructure) on a bounded sample of
+the same family: every 2nd block, index + plan + TIES at the three budgets,
+on all host cores.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "merged params/sec + effective HBM GB/s, budgeted TIES merge at B=25/50/100%"
+HBM_PEAK = 8.0e12  # MI355X published HBM3E bandwidth, bytes/s
+BUDGETS = (0.25, 0.5, 1.0)
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "ties_merge_qwen2.5-1.5b_counters.md")
+KERNEL_SOURCES = ("paper_2605_29489_amd/csrc/k_merge.hip", "paper_2605_29489_amd/csrc/device_common.h")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic():
+    """HBM bytes per TIES launch from the committed counter profile, or None
+    if it is missing or was taken on a different kernel source."""
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_PROFILE):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            kv[k.strip()] = v.strip().strip("`")
+    if kv.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(spec, base, exps, blocks_stride=8):
+    """Time the oracle on every `blocks_stride`-th block (bounded sample)."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    lay = spec.layout
+    blk = oracle.Blocks(lay.numel, lay.block_elems)
+    ids = np.arange(0, blk.G, blocks_stride)
+    idx = np.concatenate([np.arange(blk.off[g], blk.off[g] + blk.len[g]) for g in ids])
+    ti = torch.from_numpy(idx).cuda()
+    host = lambda t: t[ti].view(torch.int16).cpu().numpy().view(np.uint16)
+    b_np = host(base)
+    e_np = [host(e) for e in exps]
+    del ti
+    doff = np.concatenate([[0], np.cumsum(blk.len[ids])[:-1]]).astype(np.int64)
+    # a sub-family made of the sampled blocks: same lengths, tensors, offsets
+    sub = oracle.Blocks([int(n) for n in blk.len[ids]], lay.block_elems)
+    K = len(exps)
+    nparams = int(blk.len[ids].sum())
+    full = nparams * 2 * K
+    t0 = time.perf_counter()
+    S = oracle.index(blk, "bf16", b_np, e_np, doff=doff, ids=ids).reshape(-1)
+    for f in BUDGETS:
+        mask, _ = oracle.plan(sub, "bf16", K, S, [1.0] * K, int(f * full))
+        oracle.merge_ties(blk, "bf16", b_np, e_np, mask, 0.2, 1.0, ids=ids, doff=doff)
+    dt = time.perf_counter() - t0
+    return {
+        "value": 3 * nparams / dt,
+        "unit": "params/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"every {blocks_stride}th block ({len(ids)} blocks, {nparams} params, all {K} experts): "
+                  f"index + plan + TIES at B=25/50/100% of the sample's expert bytes; {dt:.2f} s",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-stride", type=int, default=2)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build measures one GPU only; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2605_29489_amd as mp
+    from workloads import family_spec, make_family_device
+
+    torch.cuda.set_device(0)
+    spec = family_spec("qwen2.5-1.5b")
+    lay = spec.layout
+    K = spec.K
+    P = lay.n_params
+    L = mp.Layout(lay.numel, lay.block_elems, mp.MP_BF16)
+    G = mp.mp_layout_blocks(L)
+    log(f"generating {spec.description}: P={P} G={G}")
+    base, exps = make_family_device(spec, K=K, seed=0, device="cuda")
+    torch.cuda.synchronize()
+    sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
+    masks = [torch.empty(G, dtype=torch.int32, device="cuda") for _ in BUDGETS]
+    out = torch.empty_like(base)
+    full = P * 2 * K
+    budgets = [int(f * full) for f in BUDGETS]
+    stream = torch.cuda.current_stream()
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step(rec):
+        e_i0, e_i1 = ev(), ev()
+        e_i0.record(stream)
+        mp.mp_index_blocks(L, base, exps, sumsq, stream=stream)
+        e_i1.record(stream)
+        stats = []
+        plan_ev = []
+        for B, m in zip(budgets, masks):
+            a, b = ev(), ev()
+            a.record(stream)
+            stats.append(mp.mp_plan(L, K, sumsq, [1.0] * K, B, m, stream=stream))
+            b.record(stream)
+            plan_ev.append((a, b))
+        merge_ev = []
+        for m in masks:
+            a, b = ev(), ev()
+            a.record(stream)
+            mp.mp_merge_ties(L, base, exps, m, 0.2, 1.0, out, stream=stream)
+            b.record(stream)
+            merge_ev.append((a, b))
+        if rec is not None:
+            rec.append((e_i0, e_i1, plan_ev, merge_ev, stats))
+
+    for _ in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    recs = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(recs)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall / args.steps * 1e3
+
+    idx_ms = np.mean([a.elapsed_time(b) for a, b, _, _, _ in recs])
+    plan_ms = np.array([[a.elapsed_time(b) for a, b in r[2]] for r in recs]).mean(0)
+    merge_ms = np.array([[a.elapsed_time(b) for a, b in r[3]] for r in recs]).mean(0)
+    stats = recs[-1][4]
+    io = mp.mp_merge_ties(L, base, exps, masks[0], 0.2, 1.0, out, io=True, stream=stream)
+    assert io["expert_bytes"] == stats[0]["cost_bytes"]
+
+    ckpt = P * 2
+    per_budget = []
+    alg_bytes = []
+    for f, st, pm, mm in zip(BUDGETS, stats, plan_ms, merge_ms):
+        byts = 2 * ckpt + st["cost_bytes"] + 4 * G  # base + selected expert blocks + output + mask
+        alg_bytes.append(byts)
+        per_budget.append({
+            "budget_frac": f, "budget_bytes": st["budget_bytes"], "cost_bytes": st["cost_bytes"],
+            "n_selected": st["n_selected"], "plan_ms": round(float(pm), 4), "merge_ms": round(float(mm), 4),
+            "merge_params_per_s": P / (mm * 1e-3),
+            "merge_effective_GBps": byts / (mm * 1e-3) / 1e9,
+            "merge_hbm_frac": byts / (mm * 1e-3) / HBM_PEAK,
+            "digest": hex(st["digest"]),
+        })
+    idx_bytes = (K + 1) * ckpt + 4 * G * K
+    achieved = sum(alg_bytes) / (sum(merge_ms) * 1e-3)
+    traffic = stored_traffic()
+    result = {
+        "metric": METRIC,
+        "value": 3 * P / (ms_step * 1e-3),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "qwen2.5-1.5b-shaped bf16 family, K=4, index + (plan + TIES rho=0.2 lambda=1) "
+                        "at B=25/50/100% per step",
+            "storage_dtype": "bf16", "params": P, "blocks": G, "block_elems": lay.block_elems, "K": K,
+            "budgets_bytes": budgets, "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK,
+            "traffic": traffic,
+            "kernel": "k_merge_ties<bf16> (device-resident experts)",
+        },
+        "breakdown": {
+            "index_ms": round(float(idx_ms), 4),
+            "index_effective_GBps": idx_bytes / (idx_ms * 1e-3) / 1e9,
+            "index_hbm_frac": idx_bytes / (idx_ms * 1e-3) / HBM_PEAK,
+            "per_budget": per_budget,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(spec, base, exps, args.cpu_stride)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
