@@ -301,31 +301,36 @@ int orc_merge_avg(int64_t nb, const int64_t* doff, const int64_t* len, int32_t d
 /* sign-consistent entries"), shared by TIES and DARE's sign-elect      */
 /* combine.  t[r*n + j] holds the (trimmed or dropped) delta of the    */
 /* r-th selected expert, experts in increasing index order.            */
-/*   sigma_j = sum_r t_rj (fp32 adds from +0, increasing r);            */
-/*   gamma_j = sign(sigma_j) in {-1, 0, +1};                           */
-/*   agreeing set = { r : t_rj != 0 and sign(t_rj) == gamma_j };        */
-/*   mean_j = (sum over the agreeing set, fp32 adds from +0) / count,   */
-/*            0 when the set is empty;                                 */
+/*   P_j = sum of the positive t_rj, N_j = sum of the negative t_rj     */
+/*   (each in fp32, adds from +0, increasing r), with their counts;     */
+/*   gamma_j = sign of the total signed mass, i.e. +1 if P_j > -N_j,    */
+/*   -1 if P_j < -N_j, 0 if equal (the sign of the sum of the t_rj,     */
+/*   with positive and negative contributions summed separately --     */
+/*   the paper fixes no summation order);                              */
+/*   mean_j = P_j / count(+) if gamma = +1, N_j / count(-) if -1, else 0 */
+/*   (the sum over the agreeing entries divided by their number);      */
 /*   out_j = round(fma(lambda, mean_j, x0_j)).                          */
 /* ------------------------------------------------------------------ */
 
 static float sign_elect_mean(const float* t, int nsel, int64_t n, int64_t j)
 {
-    float sigma = 0.0f;
-    for (int r = 0; r < nsel; ++r)
-        sigma = sigma + t[(int64_t)r * n + j];
-    int gamma = (sigma > 0.0f) ? 1 : ((sigma < 0.0f) ? -1 : 0);
-    float num = 0.0f;
-    int cnt = 0;
+    float P = 0.0f, N = 0.0f;
+    int np = 0, nn = 0;
     for (int r = 0; r < nsel; ++r) {
         float v = t[(int64_t)r * n + j];
-        int sv = (v > 0.0f) ? 1 : ((v < 0.0f) ? -1 : 0);
-        if (v != 0.0f && sv == gamma) {
-            num = num + v;
-            ++cnt;
+        if (v > 0.0f) {
+            P = P + v;
+            ++np;
+        } else if (v < 0.0f) {
+            N = N + v;
+            ++nn;
         }
     }
-    return cnt > 0 ? num / (float)cnt : 0.0f;
+    if (P > -N)
+        return P / (float)np;
+    if (P < -N)
+        return N / (float)nn;
+    return 0.0f;
 }
 
 /* ------------------------------------------------------------------ */

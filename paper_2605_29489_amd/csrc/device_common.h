@@ -90,6 +90,45 @@ __device__ static inline uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1)
     return c;
 }
 
+// ---------------------------------------------------------------- wave64 cross-lane helpers
+// DPP row shifts / row broadcasts (GCN/CDNA wave64), no LDS round trip.
+template <int CTRL, int ROW_MASK, int BANK_MASK, bool BOUND_CTRL>
+__device__ static inline uint32_t dpp_u32(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, BANK_MASK, BOUND_CTRL);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (lane 0 first).
+__device__ static inline uint32_t wave_incl_sum(uint32_t v)
+{
+    uint32_t s = v;
+    s += dpp_u32<0x111, 0xf, 0xf, true>(v);   // row_shr:1
+    s += dpp_u32<0x112, 0xf, 0xf, true>(v);   // row_shr:2
+    s += dpp_u32<0x113, 0xf, 0xf, true>(v);   // row_shr:3
+    s += dpp_u32<0x114, 0xf, 0xe, false>(s);  // row_shr:4, banks 1-3
+    s += dpp_u32<0x118, 0xf, 0xc, false>(s);  // row_shr:8, banks 2-3
+    s += dpp_u32<0x142, 0xa, 0xf, false>(s);  // row_bcast:15 into rows 1, 3
+    s += dpp_u32<0x143, 0xc, 0xf, false>(s);  // row_bcast:31 into rows 2, 3
+    return s;
+}
+
+// Maximum over the 64 lanes of a wave, returned as a wave-uniform value.
+__device__ static inline uint32_t wave_max_u32(uint32_t v)
+{
+    v = max(v, dpp_u32<0xb1, 0xf, 0xf, true>(v));   // quad_perm [1,0,3,2]
+    v = max(v, dpp_u32<0x4e, 0xf, 0xf, true>(v));   // quad_perm [2,3,0,1]
+    v = max(v, dpp_u32<0x141, 0xf, 0xf, true>(v));  // row_half_mirror
+    v = max(v, dpp_u32<0x140, 0xf, 0xf, true>(v));  // row_mirror
+    v = max(v, dpp_u32<0x142, 0xa, 0xf, false>(v)); // row_bcast:15
+    v = max(v, dpp_u32<0x143, 0xc, 0xf, false>(v)); // row_bcast:31
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+__device__ static inline uint32_t uniform_u32(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+
 // SplitMix64 output function: the value SplitMix64 returns when its state
 // before the step is x (Steele, Lea, Flood 2014).
 __device__ static inline unsigned long long mix64(unsigned long long x)

@@ -30,6 +30,14 @@ namespace mp {
 namespace {
 
 constexpr int kT = 256;
+#ifndef MP_TIES_THREADS
+#define MP_TIES_THREADS 512
+#endif
+constexpr int kTiesThreads = MP_TIES_THREADS;  // threads per block of the TIES kernel
+#ifndef MP_TIES_GRID
+#define MP_TIES_GRID 1024
+#endif
+constexpr int64_t kTiesGrid = MP_TIES_GRID;  // persistent workgroups of the TIES kernel
 
 // ------------------------------------------------------------ addressing
 struct DevSrc {
@@ -178,11 +186,11 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
                             if (MODE == M_DARE_LIN) {
                                 acc[e] = fmaf(alpha.v[i], tv, acc[e]);
                             } else {
-                                acc[e] = acc[e] + tv;  // sigma
-                                ps[e] = ps[e] + fmaxf(tv, 0.0f);
-                                ns[e] = ns[e] + fminf(tv, 0.0f);
-                                pc[e] += (tv > 0.0f) ? 1u : 0u;
-                                nc[e] += (tv < 0.0f) ? 1u : 0u;
+                                const bool pos = tv > 0.0f, neg = tv < 0.0f;
+                                ps[e] = ps[e] + (pos ? tv : 0.0f);
+                                ns[e] = ns[e] + (neg ? tv : 0.0f);
+                                pc[e] += pos ? 1u : 0u;
+                                nc[e] += neg ? 1u : 0u;
                             }
                         }
                     }
@@ -203,10 +211,10 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
                 } else if (MODE == M_DARE_LIN) {
                     y[v] = fmaf(lambda, acc[e], x0[e]);
                 } else {
-                    float mean = 0.0f;
-                    if (acc[e] > 0.0f)
+                    float mean = 0.0f;  // elect the sign of the larger signed mass
+                    if (ps[e] > -ns[e])
                         mean = ps[e] / (float)pc[e];
-                    else if (acc[e] < 0.0f)
+                    else if (ps[e] < -ns[e])
                         mean = ns[e] / (float)nc[e];
                     y[v] = fmaf(lambda, mean, x0[e]);
                 }
@@ -217,263 +225,402 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
 }
 
 // ------------------------------------------------------------ TIES
+// Threshold search for one expert block: tau = the k-th largest |d|.
+// Magnitudes are compared as fp32 bit patterns (sign cleared).  Levels:
+//  window  one atomic per element into a 2048-bin histogram of the key
+//          |d| >> 14 (exponent + 9 mantissa bits) over the binade of the
+//          block maximum and the three below it; smaller elements (zeros
+//          included -- they are frequent in bf16 deltas and would all hit one
+//          counter) are not counted.  The high half of each counter counts
+//          elements whose 14 low bits are not zero.  If the k-th largest
+//          falls in a bucket that is either kept whole or holds only values
+//          with zero low bits (so all its values are equal), that bucket
+//          gives tau.
+//  refine  otherwise the bucket's elements are histogrammed on the next
+//          bits (13..3, then 2..0), with the same exactness test; if fewer
+//          than k elements lie in the window the search restarts on bits
+//          30..20 of all elements.
+// The window level is scanned by all waves at once: wave w owns a 256-bin
+// slice and publishes its total; after one barrier every wave finds the
+// slice holding the k-th largest and resolves the bin by re-reading that
+// slice.  Refinement levels (rare) are one atomic pass, a barrier, a scan
+// by one wave and a barrier.  Any tau' with max{|d| < tau} < tau' <= tau
+// gives the same keep decisions, so a bucket that is kept whole ends the
+// search.
 struct TiesSmem {
-    uint32_t hA[2][1024];
-    uint32_t hB[1024];
-    uint32_t hBmin[1024];
-    uint32_t hBmax[1024];
-    uint32_t hC[2048];
-    uint32_t sel[8];
+    uint32_t hw[2][2048];  // per round parity: window histogram, then refinement levels
+    uint32_t smax[2];      // block maximum |d| pattern per round parity
+    uint32_t res[2][4];    // scan result of the current level
+    uint32_t slice[2][8];  // per-wave slice totals of the window histogram
 };
 
-// Wave 0 only: walk the NB-bin histogram h from the top bin down and find
-// the bin holding the k-th largest element.  Writes sel[0..3] = {found,
-// bin, k - count above the bin, count in the bin}; found = 0 when fewer
-// than k elements were counted.
-template <int NB>
-__device__ inline void scan_from_top(const uint32_t* h, uint32_t k, int lane, uint32_t* sel)
+struct Cut {
+    uint32_t found, bin, rank, count, aux;  // wave-uniform (scalar registers)
+};
+
+// Wave-level, all lanes: walk histogram bins downward from `top` and find
+// the bin where the count from the top first reaches k.  Counts are the low
+// 16 bits of each counter; aux returns the bin's high 16 bits.  rank = k
+// minus the count above the bin.  Each round reads 256 bins, four
+// consecutive bins per lane (conflict-free 16-byte LDS reads), and
+// prefix-sums the lane totals across the wave with DPP.
+__device__ inline Cut wave_find_from_top(const uint32_t* __restrict__ h, int top, uint32_t k, int lane)
 {
-    constexpr int PER = NB / 64;
-    const int top = NB - PER * lane - 1;  // lane 0 owns the highest bins
-    uint32_t loc = 0;
-#pragma unroll
-    for (int j = 0; j < PER; ++j)
-        loc += h[top - j];
-    uint32_t incl = loc;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t y = __shfl_up(incl, (unsigned)off);
-        if (lane >= off)
-            incl += y;
-    }
-    const uint32_t excl = incl - loc;
-    const uint32_t total = __shfl(incl, 63);
-    if (lane == 0 && total < k)
-        sel[0] = 0u;
-    if (excl < k && k <= incl) {
-        uint32_t run = excl;
-        for (int j = 0; j < PER; ++j) {
-            const uint32_t cb = h[top - j];
-            if (run + cb >= k) {
-                sel[0] = 1u;
-                sel[1] = (uint32_t)(top - j);
-                sel[2] = k - run;
-                sel[3] = cb;
-                break;
+    Cut r{0u, 0u, 0u, 0u, 0u};
+    top |= 3;
+    uint32_t above = 0;
+    for (int hi = top; hi >= 0; hi -= 256) {
+        const int g4 = hi - 4 * lane - 3;  // multiple of 4: the lane's bins are g4 .. g4+3
+        uint4 raw = make_uint4(0u, 0u, 0u, 0u);
+        if (g4 >= 0)
+            raw = *reinterpret_cast<const uint4*>(h + g4);
+        const uint4 v = make_uint4(raw.x & 0xffffu, raw.y & 0xffffu, raw.z & 0xffffu, raw.w & 0xffffu);
+        const uint32_t s = v.x + v.y + v.z + v.w;
+        const uint32_t incl = wave_incl_sum(s);
+        const uint32_t before = above + incl - s;  // count in the bins above this lane's four
+        const bool hit = before < k && k <= above + incl;
+        const unsigned long long bal = __ballot(hit);
+        if (bal) {
+            uint32_t c = before, bin, cnt, aux;
+            if (c + v.w >= k) {
+                bin = g4 + 3; cnt = v.w; aux = raw.w;
+            } else {
+                c += v.w;
+                if (c + v.z >= k) {
+                    bin = g4 + 2; cnt = v.z; aux = raw.z;
+                } else {
+                    c += v.z;
+                    if (c + v.y >= k) {
+                        bin = g4 + 1; cnt = v.y; aux = raw.y;
+                    } else {
+                        c += v.y;
+                        bin = g4; cnt = v.x; aux = raw.x;
+                    }
+                }
             }
-            run += cb;
+            const int src = __ffsll((long long)bal) - 1;
+            r.found = 1u;
+            r.bin = (uint32_t)__builtin_amdgcn_readlane((int)bin, src);
+            r.rank = (uint32_t)__builtin_amdgcn_readlane((int)(k - c), src);
+            r.count = (uint32_t)__builtin_amdgcn_readlane((int)cnt, src);
+            r.aux = (uint32_t)__builtin_amdgcn_readlane((int)(aux >> 16), src);
+            return r;
         }
+        above += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
     }
+    return r;
 }
 
-// Block-wide: threshold tau' for the E magnitudes each thread holds (bit
-// patterns of |d|, 0 for padding).  Elements are kept iff mg >= tau' and
-// mg != 0.  Must be called by every thread of the workgroup.
-// On entry sm.hA[it & 1], sm.hB*, sm.hC are clear; on exit sm.hA[(it+1) & 1],
-// sm.hB* and sm.hC are clear again (each thread resets the pass-B/C bins it
-// touched), ready for the next expert.
-template <int E>
-__device__ inline uint32_t ties_threshold(const uint32_t (&mg)[E], uint32_t k, int it, TiesSmem& sm)
+// Sum over the lanes of a wave (wave-uniform result).
+__device__ inline uint32_t wave_sum_u32(uint32_t v)
 {
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    if (k == 0u)
-        return 0xffffffffu;  // keep nothing
-    uint32_t* HA = sm.hA[it & 1];
-    uint32_t* HAn = sm.hA[(it + 1) & 1];  // last used by the previous expert, whose scans are done
-    for (int q = t; q < 1024; q += kT)
-        HAn[q] = 0u;
-    uint32_t orv = 0u;
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-        orv |= mg[e];
-    if (__any(orv != 0u)) {  // a wave whose elements are all zero adds nothing above bin 0
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-            atomicAdd(&HA[mg[e] >> 21], 1u);
-    }
-    __syncthreads();
-    if (wave == 0)
-        scan_from_top<1024>(HA, k, lane, sm.sel);
-    __syncthreads();
-    if (sm.sel[0] == 0u)
-        return 1u;  // fewer than k counted: the k-th largest is 0, keep every nonzero
-    const uint32_t bA = sm.sel[1], kA = sm.sel[2], cA = sm.sel[3];
-    if (cA == kA)
-        return bA << 21;  // the whole bucket is kept
-    // pass B: bits 20..11 of the elements in bucket bA, with bucket min / max
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        if ((mg[e] >> 21) == bA) {
-            const uint32_t dg = (mg[e] >> 11) & 1023u;
-            atomicAdd(&sm.hB[dg], 1u);
-            atomicMin(&sm.hBmin[dg], mg[e]);
-            atomicMax(&sm.hBmax[dg], mg[e]);
-        }
-    }
-    __syncthreads();
-    if (wave == 0) {
-        scan_from_top<1024>(sm.hB, kA, lane, sm.sel);
-        if (lane == 0) {
-            sm.sel[4] = sm.hBmin[sm.sel[1]];
-            sm.sel[5] = sm.hBmax[sm.sel[1]];
-        }
-    }
-    __syncthreads();
-    const uint32_t bB = sm.sel[1], kB = sm.sel[2], cB = sm.sel[3];
-    const bool whole = (cB == kB) || (sm.sel[4] == sm.sel[5]);
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        if ((mg[e] >> 21) == bA) {
-            const uint32_t dg = (mg[e] >> 11) & 1023u;
-            sm.hB[dg] = 0u;
-            sm.hBmin[dg] = 0xffffffffu;
-            sm.hBmax[dg] = 0u;
-        }
-    }
-    const uint32_t lo = (bA << 21) | (bB << 11);
-    if (whole)
-        return lo;  // count matches, or every value in the bucket is equal (ties are all kept)
-    // pass C: bits 10..0 of the elements in bucket (bA, bB)
-    const uint32_t hiC = lo >> 11;
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-        if ((mg[e] >> 11) == hiC)
-            atomicAdd(&sm.hC[mg[e] & 2047u], 1u);
-    __syncthreads();
-    if (wave == 0)
-        scan_from_top<2048>(sm.hC, kB, lane, sm.sel);
-    __syncthreads();
-    const uint32_t tau = lo | sm.sel[1];
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-        if ((mg[e] >> 11) == hiC)
-            sm.hC[mg[e] & 2047u] = 0u;
-    return tau;
+    return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_sum(v), 63);
 }
 
-template <int DT, class Src>
-__global__ __launch_bounds__(kT) void k_merge_ties(Src src, const void* __restrict__ base,
+struct BlockInfo {
+    uint32_t g, n, m, k;
+    uint64_t off;
+};
+
+template <class Src>
+__device__ inline BlockInfo block_info(const Src& src, int64_t b, const uint32_t* __restrict__ mask,
+                                       const uint64_t* __restrict__ boff, const uint32_t* __restrict__ blen,
+                                       double density, uint32_t kmask)
+{
+    BlockInfo bi;
+    bi.g = uniform_u32(src.block(b));
+    bi.off = boff[bi.g];
+    bi.n = blen[bi.g];
+    const double kk = ceil(density * (double)bi.n);
+    bi.k = uniform_u32((kk >= (double)bi.n) ? bi.n : (uint32_t)kk);
+    bi.m = (bi.k != 0u) ? (mask[bi.g] & kmask) : 0u;  // density 0 keeps nothing: no expert is read
+    return bi;
+}
+
+template <int DT, int NT, int CPT>
+__device__ inline void load_chunks(const uint4* __restrict__ p, uint32_t nch, uint4 (&dst)[CPT])
+{
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int q = 0; q < CPT; ++q)
+        dst[q] = (q * NT + t < nch) ? p[q * NT + t] : make_uint4(0u, 0u, 0u, 0u);
+}
+
+// One workgroup merges blocks b, b + gridDim.x, ... (persistent).  While an
+// expert block is trimmed the next one -- or the next block's base and
+// first selected expert -- is already being loaded.
+template <int DT, int NT, class Src>
+__global__ __launch_bounds__(NT, NT / 128) void k_merge_ties(Src src, const void* __restrict__ base,
                                                    const uint32_t* __restrict__ mask,
                                                    const uint64_t* __restrict__ boff,
                                                    const uint32_t* __restrict__ blen, double density,
                                                    float lambda, uint32_t kmask, void* __restrict__ out,
-                                                   unsigned long long* __restrict__ ctr)
+                                                   unsigned long long* __restrict__ ctr, int64_t nblocks)
 {
     constexpr int V = Fmt<DT>::V;
     constexpr int ES = Fmt<DT>::esize;
-    constexpr int CPT = kTiesMaxBlock / kT / V;  // 2 (bf16) or 4 (fp32)
-    constexpr int E = CPT * V;                   // 16 elements per thread
+    constexpr int CPT = kTiesMaxBlock / NT / V;  // chunks per thread
+    constexpr int E = CPT * V;                   // elements per thread
+    static_assert(CPT >= 1, "block too small for the thread count");
     __shared__ TiesSmem sm;
-    const int64_t b = blockIdx.x;
     const int t = threadIdx.x;
-    const uint32_t g = src.block(b);
-    const uint64_t off = boff[g];
-    const uint32_t n = blen[g];
-    const uint32_t m = mask[g] & kmask;  // bits of experts >= K are ignored
-    const uint32_t nch = n / V;
-    const uint4* pb = chunk_ptr(base, off, ES);
-    uint4* po = reinterpret_cast<uint4*>(static_cast<char*>(out) + off * ES);
-    count_expert_bytes(ctr, m, n, ES);
+    const int lane = t & 63;
+    int64_t b = blockIdx.x;
+    if (b >= nblocks)
+        return;
 
-    const double kk = ceil(density * (double)n);
-    const uint32_t k = (kk >= (double)n) ? n : (uint32_t)kk;
-
-    bool ok[CPT];
-    float x0[E];
-#pragma unroll
-    for (int q = 0; q < CPT; ++q) {
-        const uint32_t c = q * kT + t;
-        ok[q] = c < nch;
-        uint4 raw = make_uint4(0, 0, 0, 0);
-        if (ok[q])
-            raw = pb[c];
-        Fmt<DT>::unpack(raw, &x0[q * V]);
-    }
-    float sg[E], ps[E], ns[E];
-    uint32_t cnt[E];  // positives in the low 16 bits, negatives in the high 16 bits
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        sg[e] = 0.0f;
-        ps[e] = 0.0f;
-        ns[e] = 0.0f;
-        cnt[e] = 0u;
-    }
-    for (int q = t; q < 1024; q += kT) {
-        sm.hA[0][q] = 0u;
-        sm.hB[q] = 0u;
-        sm.hBmin[q] = 0xffffffffu;
-        sm.hBmax[q] = 0u;
-    }
-    for (int q = t; q < 2048; q += kT)
-        sm.hC[q] = 0u;
+    static_assert(NT == 512, "the window scan gives each of the 8 waves a 256-bin slice");
+    for (int q = t; q < 2 * 2048; q += NT)
+        (&sm.hw[0][0])[q] = 0u;
+    if (t < 2)
+        sm.smax[t] = 0u;
     __syncthreads();
+    const int wave = t >> 6;
+    uint32_t par = 0u;  // parity of the expert round (LDS buffer set)
 
-    uint32_t mm = m;
-    uint4 nxt[CPT];
+    BlockInfo cur = block_info(src, b, mask, boff, blen, density, kmask);
+    uint4 x0raw[CPT], nx0raw[CPT], nxt[CPT];
+    load_chunks<DT, NT, CPT>(chunk_ptr(base, cur.off, ES), cur.n / V, x0raw);
+    uint32_t mm = cur.m;
     int rank = 0;
-    if (mm) {
-        const uint4* pe = src.expert(__builtin_ctz(mm), 0, b, off, n, ES);
+    if (mm)
+        load_chunks<DT, NT, CPT>(src.expert(__builtin_ctz(mm), 0, b, cur.off, cur.n, ES), cur.n / V, nxt);
+
+    for (;;) {
+        const int64_t b2 = b + gridDim.x;
+        const bool has_next = b2 < nblocks;
+        BlockInfo nx{};
+        if (has_next)
+            nx = block_info(src, b2, mask, boff, blen, density, kmask);
+        const uint32_t nch = cur.n / V;
+        count_expert_bytes(ctr, cur.m, cur.n, ES);
+        float x0[E];
 #pragma unroll
         for (int q = 0; q < CPT; ++q)
-            if (ok[q])
-                nxt[q] = pe[q * kT + t];
-    }
-    int it = 0;
-    while (mm) {
-        mm &= mm - 1u;
-        uint4 cur[CPT];
-#pragma unroll
-        for (int q = 0; q < CPT; ++q)
-            cur[q] = nxt[q];
-        if (mm) {  // prefetch the next selected expert while this one is trimmed
-            const uint4* pe = src.expert(__builtin_ctz(mm), rank + 1, b, off, n, ES);
-#pragma unroll
-            for (int q = 0; q < CPT; ++q)
-                if (ok[q])
-                    nxt[q] = pe[q * kT + t];
-        }
-        float d[E];
-        uint32_t mg[E];
-#pragma unroll
-        for (int q = 0; q < CPT; ++q) {
-            float x[V];
-            Fmt<DT>::unpack(ok[q] ? cur[q] : make_uint4(0, 0, 0, 0), x);
-#pragma unroll
-            for (int v = 0; v < V; ++v) {
-                const int e = q * V + v;
-                d[e] = ok[q] ? (x[v] - x0[e]) : 0.0f;
-                mg[e] = __float_as_uint(d[e]) & 0x7fffffffu;
-            }
-        }
-        const uint32_t tau = ties_threshold<E>(mg, k, it, sm);
+            Fmt<DT>::unpack(x0raw[q], &x0[q * V]);
+
+        float ps[E], ns[E];
+        uint32_t pc[E], nc[E];
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const bool keep = (mg[e] >= tau) && (mg[e] != 0u);
-            const float tv = keep ? d[e] : 0.0f;
-            sg[e] = sg[e] + tv;
-            ps[e] = ps[e] + fmaxf(tv, 0.0f);
-            ns[e] = ns[e] + fminf(tv, 0.0f);
-            cnt[e] += keep ? ((d[e] > 0.0f) ? 1u : 0x10000u) : 0u;
+            ps[e] = 0.0f;
+            ns[e] = 0.0f;
+            pc[e] = 0u;
+            nc[e] = 0u;
         }
-        ++it;
-        ++rank;
-    }
-#pragma unroll
-    for (int q = 0; q < CPT; ++q) {
-        if (!ok[q])
-            continue;
-        float y[V];
-#pragma unroll
-        for (int v = 0; v < V; ++v) {
-            const int e = q * V + v;
-            float mean = 0.0f;
-            if (sg[e] > 0.0f)
-                mean = ps[e] / (float)(cnt[e] & 0xffffu);
-            else if (sg[e] < 0.0f)
-                mean = ns[e] / (float)(cnt[e] >> 16);
-            y[v] = fmaf(lambda, mean, x0[e]);
+        if (mm == 0u && has_next) {  // nothing to trim here: start loading the next block now
+            load_chunks<DT, NT, CPT>(chunk_ptr(base, nx.off, ES), nx.n / V, nx0raw);
+            if (nx.m)
+                load_chunks<DT, NT, CPT>(src.expert(__builtin_ctz(nx.m), 0, b2, nx.off, nx.n, ES), nx.n / V, nxt);
         }
-        po[q * kT + t] = Fmt<DT>::pack(y);
+        while (mm) {
+            mm &= mm - 1u;
+            uint4 ce[CPT];
+#pragma unroll
+            for (int q = 0; q < CPT; ++q)
+                ce[q] = nxt[q];
+            if (mm) {
+                load_chunks<DT, NT, CPT>(src.expert(__builtin_ctz(mm), rank + 1, b, cur.off, cur.n, ES), nch, nxt);
+            } else if (has_next) {
+                load_chunks<DT, NT, CPT>(chunk_ptr(base, nx.off, ES), nx.n / V, nx0raw);
+                if (nx.m)
+                    load_chunks<DT, NT, CPT>(src.expert(__builtin_ctz(nx.m), 0, b2, nx.off, nx.n, ES), nx.n / V,
+                                             nxt);
+            }
+            float d[E];  // padding chunks were loaded as zeros: d = 0 there
+            uint32_t mg[E];
+#pragma unroll
+            for (int q = 0; q < CPT; ++q) {
+                float x[V];
+                Fmt<DT>::unpack(ce[q], x);
+#pragma unroll
+                for (int v = 0; v < V; ++v) {
+                    const int e = q * V + v;
+                    d[e] = x[v] - x0[e];
+                    mg[e] = __float_as_uint(d[e]) & 0x7fffffffu;
+                }
+            }
+            uint32_t* h = sm.hw[par];  // clean: cleared during the previous round
+            // ---- R1: block maximum
+            if (t == 0)
+                sm.smax[par ^ 1u] = 0u;  // for the next round
+            {
+                uint32_t mx = 0u;
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    mx = max(mx, mg[e]);
+                const uint32_t wmx = wave_max_u32(mx);
+                if (lane == 0 && wmx != 0u)
+                    atomicMax(&sm.smax[par], wmx);
+            }
+            __syncthreads();
+            // every wave is past the previous round: clear its buffer for the next round
+            *reinterpret_cast<uint4*>(&sm.hw[par ^ 1u][4 * t]) = make_uint4(0u, 0u, 0u, 0u);
+            const uint32_t bmax = uniform_u32(sm.smax[par]);
+            uint32_t tau = 1u;  // all-zero block: nothing is kept
+            if (bmax != 0u) {
+                // ---- R2: window histogram over [2^(E_max - 3), max] (E_max: binade of the max)
+                const uint32_t ebin = bmax >> 23;
+                const uint32_t wlo = (ebin > 3u ? ebin - 3u : 0u) << 9;  // first key of the window
+                const uint32_t top = (bmax >> 14) - wlo;                  // bin of the max, < 2048
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const uint32_t key = mg[e] >> 14;
+                    if (key >= wlo && mg[e] != 0u) {
+                        const uint32_t inc = (mg[e] & 0x3fffu) ? 0x10001u : 1u;
+                        atomicAdd(&h[key - wlo], inc);
+                    }
+                }
+                __syncthreads();
+                // ---- R3 (one wave): scan; then refine while the bucket is not resolved
+                // level state: elements with (mg >> pshift) == pref are histogrammed on
+                // (mg >> dshift) & dmask; tau so far = pref << pshift
+                // ---- all waves: slice totals
+                const int g4 = 2047 - 256 * wave - 4 * lane - 3;  // this lane's four bins (slice of this wave)
+                const uint4 raw = *reinterpret_cast<const uint4*>(h + g4);
+                const uint32_t cnt4 = (raw.x & 0xffffu) + (raw.y & 0xffffu) + (raw.z & 0xffffu) + (raw.w & 0xffffu);
+                const uint32_t stot = wave_sum_u32(cnt4);
+                if (lane == 0)
+                    sm.slice[par][wave] = stot;
+                __syncthreads();
+                // ---- every wave: the slice holding the k-th largest, then its bin
+                uint32_t st = 0u, v1 = 0u, v2 = 0u;  // st 0: done (v1 = tau), 1: refine bucket, 2: restart
+                {
+                    uint32_t above = 0u;
+                    int sl = -1;
+#pragma unroll
+                    for (int w = 0; w < 8; ++w) {
+                        const uint32_t tw = uniform_u32(sm.slice[par][w]);
+                        if (sl < 0) {
+                            if (above + tw >= cur.k)
+                                sl = w;
+                            else
+                                above += tw;
+                        }
+                    }
+                    if (sl < 0) {
+                        st = 2u;  // fewer than k nonzero elements in the window: search everything
+                        v2 = cur.k;
+                    } else {
+                        const Cut c = wave_find_from_top(h, 2047 - 256 * sl, cur.k - above, lane);
+                        const uint32_t bin = c.bin;
+                        if (c.count == c.rank || c.aux == 0u) {
+                            v1 = max((wlo + bin) << 14, 1u);  // the bucket is kept whole / holds one value
+                        } else {
+                            st = 1u;
+                            v1 = wlo + bin;  // bucket key
+                            v2 = c.rank;
+                        }
+                    }
+                }
+                tau = v1;
+                if (st != 0u) {
+                    // rare: refinement levels, all in one buffer (the other set is clean for
+                    // the next round, this one is cleared at the start of the round after it)
+                    uint32_t rk = v2;
+                    uint32_t pref = (st == 1u) ? tau : 0u;
+                    int pshift = (st == 1u) ? 14 : 31;
+                    int dshift = (st == 1u) ? 3 : 20;
+#pragma unroll 1
+                    for (;;) {
+                        __syncthreads();  // everyone has read the previous level's result
+                        for (int q = t; q < 2048; q += NT)
+                            h[q] = 0u;
+                        __syncthreads();
+                        const uint32_t lowm = (dshift > 0) ? ((1u << dshift) - 1u) : 0u;
+#pragma unroll
+                        for (int e = 0; e < E; ++e) {
+                            const uint32_t hi = (pshift >= 31) ? 0u : (mg[e] >> pshift);
+                            if (hi == pref) {
+                                const uint32_t bin = (mg[e] >> dshift) & 2047u;
+                                atomicAdd(&h[bin], (mg[e] & lowm) ? 0x10001u : 1u);
+                            }
+                        }
+                        __syncthreads();
+                        if (t < 64) {
+                            const Cut c = wave_find_from_top(h, 2047, rk, lane);
+                            if (lane == 0) {
+                                sm.res[par][0] = c.found;
+                                sm.res[par][1] = c.bin;
+                                sm.res[par][2] = c.rank;
+                                sm.res[par][3] = (c.count == c.rank || c.aux == 0u) ? 1u : 0u;
+                            }
+                        }
+                        __syncthreads();
+                        const uint32_t found = uniform_u32(sm.res[par][0]);
+                        const uint32_t bin = uniform_u32(sm.res[par][1]);
+                        rk = uniform_u32(sm.res[par][2]);
+                        const uint32_t whole = uniform_u32(sm.res[par][3]);
+                        pref = (pshift >= 31 ? 0u : (pref << (pshift - dshift))) | bin;
+                        if (!found) {
+                            tau = 1u;  // fewer than k nonzero: keep every nonzero
+                            break;
+                        }
+                        if (whole || dshift == 0) {
+                            tau = max(pref << dshift, 1u);
+                            break;
+                        }
+                        pshift = dshift;
+                        dshift = dshift > 11 ? dshift - 11 : 0;
+                    }
+                    __syncthreads();  // every wave is done with the buffer
+                    for (int q = t; q < 2048; q += NT)
+                        h[q] = 0u;
+                }
+            }
+            // ---- keep, and accumulate the signed masses and their counts
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const bool keep = mg[e] >= tau;  // tau >= 1: a kept delta is not zero
+                const bool posr = (int32_t)__float_as_uint(d[e]) > 0;
+                const bool pos = keep && posr;
+                const bool neg = keep && !posr;
+                ps[e] = ps[e] + (pos ? d[e] : 0.0f);
+                ns[e] = ns[e] + (neg ? d[e] : 0.0f);
+                pc[e] += pos ? 1u : 0u;
+                nc[e] += neg ? 1u : 0u;
+            }
+            par ^= 1u;
+            ++rank;
+        }
+        // ---- output of this block
+        uint4* po = reinterpret_cast<uint4*>(static_cast<char*>(out) + cur.off * ES);
+        // elect the sign of the larger signed mass; mean of the agreeing entries
+        float num[E];
+        uint32_t den[E];
+        bool any_div = false;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const bool up = ps[e] > -ns[e];
+            const bool dn = ps[e] < -ns[e];
+            num[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);
+            den[e] = up ? pc[e] : (dn ? nc[e] : 1u);
+            any_div |= den[e] > 1u;
+        }
+        if (__any(any_div)) {  // one agreeing entry (or none) needs no division
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                num[e] = num[e] / (float)den[e];
+        }
+#pragma unroll
+        for (int q = 0; q < CPT; ++q) {
+            if (q * NT + t >= nch)
+                continue;
+            float y[V];
+#pragma unroll
+            for (int v = 0; v < V; ++v)
+                y[v] = fmaf(lambda, num[q * V + v], x0[q * V + v]);
+            po[q * NT + t] = Fmt<DT>::pack(y);
+        }
+        if (!has_next)
+            break;
+        b = b2;
+        cur = nx;
+        mm = cur.m;
+        rank = 0;
+#pragma unroll
+        for (int q = 0; q < CPT; ++q)
+            x0raw[q] = nx0raw[q];
     }
 }
 
@@ -503,10 +650,12 @@ hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, T, scale,
                            a.seed, kmask, out, ctr);
         break;
-    case Op::TIES:
-        hipLaunchKernelGGL((k_merge_ties<DT, Src>), grid, block, 0, s, src, base, mask, bt.d_off,
-                           bt.d_len, a.density, a.lambda, kmask, out, ctr);
+    case Op::TIES: {
+        const int64_t gridT = nb < kTiesGrid ? nb : kTiesGrid;
+        hipLaunchKernelGGL((k_merge_ties<DT, kTiesThreads, Src>), dim3((unsigned)gridT), dim3(kTiesThreads), 0, s,
+                           src, base, mask, bt.d_off, bt.d_len, a.density, a.lambda, kmask, out, ctr, nb);
         break;
+    }
     }
     return hipGetLastError();
 }
