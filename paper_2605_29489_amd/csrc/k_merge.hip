@@ -1,22 +1,15 @@
 // Mask-aware merge operators Psi_op (Eq. 4; operators of Appendix A.1).
 //
-// One 256-thread workgroup per block.  The block's mask word is uniform, so
-// the loop over the selected experts is a scalar loop: unselected experts
-// are never touched (the zero-completed tuple of Appendix A.1 costs no
-// reads).  Blocks are streamed as 16-byte chunks with coalesced loads.
+// One workgroup per block.  The block's mask word is uniform, so the loop
+// over the selected experts is a scalar loop: unselected experts are never
+// touched (the zero-completed tuple of Appendix A.1 costs no reads).  Blocks
+// are streamed as 16-byte chunks with coalesced loads.
 //
 //  * AVG / DARE (linear or sign-elect): elementwise.  A thread owns CPT
 //    chunks of a tile and loads the chunks of up to 4 selected experts
 //    before consuming them in increasing expert order.
-//  * TIES: the whole block (<= 4096 elements, 16 per thread) stays in
-//    registers.  Per selected expert the trim threshold tau (k-th largest
-//    |d|) comes from an exact MSD radix select over the fp32 magnitude bit
-//    patterns in LDS: bits 30..21 (all elements), 20..11 (only the ones in
-//    the chosen bucket, with bucket min/max to stop early on ties), 10..0.
-//    Any tau' with  max{|d| < tau} < tau' <= tau  gives the same keep
-//    decisions, so the select stops as soon as the bucket that holds tau is
-//    known to be kept entirely.  The sign election and disjoint mean run in
-//    one pass over the experts with running sums per element.
+//  * TIES: the block's deltas stay in registers while the per-expert trim
+//    thresholds are selected in LDS (see the TIES section).
 //
 // Addressing: device-resident experts (expert i's block at its layout
 // offset) or staged experts (the selected blocks packed back to back in a
@@ -30,14 +23,6 @@ namespace mp {
 namespace {
 
 constexpr int kT = 256;
-#ifndef MP_TIES_THREADS
-#define MP_TIES_THREADS 512
-#endif
-constexpr int kTiesThreads = MP_TIES_THREADS;  // threads per block of the TIES kernel
-#ifndef MP_TIES_GRID
-#define MP_TIES_GRID 1024
-#endif
-constexpr int64_t kTiesGrid = MP_TIES_GRID;  // persistent workgroups of the TIES kernel
 
 // ------------------------------------------------------------ addressing
 struct DevSrc {
@@ -225,37 +210,50 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
 }
 
 // ------------------------------------------------------------ TIES
-// Threshold search for one expert block: tau = the k-th largest |d|.
-// Magnitudes are compared as fp32 bit patterns (sign cleared).  Levels:
-//  window  one atomic per element into a 2048-bin histogram of the key
-//          |d| >> 14 (exponent + 9 mantissa bits) over the binade of the
-//          block maximum and the three below it; smaller elements (zeros
-//          included -- they are frequent in bf16 deltas and would all hit one
-//          counter) are not counted.  The high half of each counter counts
-//          elements whose 14 low bits are not zero.  If the k-th largest
-//          falls in a bucket that is either kept whole or holds only values
-//          with zero low bits (so all its values are equal), that bucket
-//          gives tau.
-//  refine  otherwise the bucket's elements are histogrammed on the next
-//          bits (13..3, then 2..0), with the same exactness test; if fewer
-//          than k elements lie in the window the search restarts on bits
-//          30..20 of all elements.
-// The window level is scanned by all waves at once: wave w owns a 256-bin
-// slice and publishes its total; after one barrier every wave finds the
-// slice holding the k-th largest and resolves the bin by re-reading that
-// slice.  Refinement levels (rare) are one atomic pass, a barrier, a scan
-// by one wave and a barrier.  Any tau' with max{|d| < tau} < tau' <= tau
-// gives the same keep decisions, so a bucket that is kept whole ends the
-// search.
+// One 256-thread workgroup per block.  The block's deltas (<= 4096
+// elements: 16 per thread and expert) stay in registers, and up to four
+// selected experts are trimmed together so that they share the barriers.
+// Per expert, tau = the k-th largest |d| is found on the fp32 magnitude bit
+// patterns:
+//  A  the block maximum M (wave maxima, one value per wave in LDS);
+//  B  the elements of the four binades below the binade of M are counted
+//     into a 2048-bin histogram keyed by |d| >> 14 (exponent and 9 mantissa
+//     bits).  The high half of a counter counts the elements whose 14 low
+//     bits are not zero, i.e. that lie above the bin's floor.  Elements in
+//     M's binade are counted with wave ballots; smaller ones are not counted:
+//     they are the bulk of a block, hold few distinct values and would
+//     serialise the LDS atomics on a handful of counters;
+//  C  one wave per expert walks the histogram from the top to the bin where
+//     the count reaches k, needing r more elements from that bin.  If fewer
+//     than r of the bin's elements lie above its floor, the floor is the
+//     k-th largest value; if the whole bin is needed its floor keeps the
+//     same elements as the k-th largest.  Either way tau is found;
+//  D  otherwise (rare) the bin's elements are listed in LDS and one wave
+//     resolves the 14 low bits one at a time; if tau lies outside the window
+//     or the list overflows, an exact 3-level radix select over all
+//     elements runs instead.
+// Then one pass over the elements keeps |d| >= tau (tau is at least the
+// smallest positive pattern, so a kept delta is not zero), elects the sign
+// of the larger of the positive and negative kept masses and takes the mean
+// of the agreeing entries.
+namespace ties {
+constexpr int NT = 256;      // threads per workgroup
+constexpr int NW = NT / 64;  // waves per workgroup
+constexpr int GS = 4;        // experts trimmed together (one scanning wave each)
+constexpr int NB = 2048;     // window bins
+constexpr int KS = 14;       // pattern bits below a window key
+enum : uint32_t { DONE = 0u, LIST = 1u, RADIX = 2u };
+}  // namespace ties
+
 struct TiesSmem {
-    uint32_t hw[2][2048];  // per round parity: window histogram, then refinement levels
-    uint32_t smax[2];      // block maximum |d| pattern per round parity
-    uint32_t res[2][4];    // scan result of the current level
-    uint32_t slice[2][8];  // per-wave slice totals of the window histogram
+    uint32_t h[ties::GS][ties::NB];     // window histogram, then candidate list / radix levels
+    uint32_t wmax[ties::GS][ties::NW];  // per-wave maximum |d| pattern
+    uint32_t wtop[ties::GS][ties::NW];  // per-wave count of elements in the top binade
+    uint32_t st[ties::GS][4];           // state, tau (or bucket key), rank in the bucket, list length
 };
 
 struct Cut {
-    uint32_t found, bin, rank, count, aux;  // wave-uniform (scalar registers)
+    uint32_t found, bin, rank, count, aux;  // wave-uniform
 };
 
 // Wave-level, all lanes: walk histogram bins downward from `top` and find
@@ -317,26 +315,6 @@ __device__ inline uint32_t wave_sum_u32(uint32_t v)
     return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_sum(v), 63);
 }
 
-struct BlockInfo {
-    uint32_t g, n, m, k;
-    uint64_t off;
-};
-
-template <class Src>
-__device__ inline BlockInfo block_info(const Src& src, int64_t b, const uint32_t* __restrict__ mask,
-                                       const uint64_t* __restrict__ boff, const uint32_t* __restrict__ blen,
-                                       double density, uint32_t kmask)
-{
-    BlockInfo bi;
-    bi.g = uniform_u32(src.block(b));
-    bi.off = boff[bi.g];
-    bi.n = blen[bi.g];
-    const double kk = ceil(density * (double)bi.n);
-    bi.k = uniform_u32((kk >= (double)bi.n) ? bi.n : (uint32_t)kk);
-    bi.m = (bi.k != 0u) ? (mask[bi.g] & kmask) : 0u;  // density 0 keeps nothing: no expert is read
-    return bi;
-}
-
 template <int DT, int NT, int CPT>
 __device__ inline void load_chunks(const uint4* __restrict__ p, uint32_t nch, uint4 (&dst)[CPT])
 {
@@ -346,281 +324,438 @@ __device__ inline void load_chunks(const uint4* __restrict__ p, uint32_t nch, ui
         dst[q] = (q * NT + t < nch) ? p[q * NT + t] : make_uint4(0u, 0u, 0u, 0u);
 }
 
-// One workgroup merges blocks b, b + gridDim.x, ... (persistent).  While an
-// expert block is trimmed the next one -- or the next block's base and
-// first selected expert -- is already being loaded.
-template <int DT, int NT, class Src>
-__global__ __launch_bounds__(NT, NT / 128) void k_merge_ties(Src src, const void* __restrict__ base,
-                                                   const uint32_t* __restrict__ mask,
-                                                   const uint64_t* __restrict__ boff,
-                                                   const uint32_t* __restrict__ blen, double density,
-                                                   float lambda, uint32_t kmask, void* __restrict__ out,
-                                                   unsigned long long* __restrict__ ctr, int64_t nblocks)
+// Wave-level: the r-th largest of the n patterns in `list`, all of which
+// share the key (pattern >> KS); the low bits are fixed from the top down.
+__device__ inline uint32_t wave_select_list(const uint32_t* __restrict__ list, uint32_t n, uint32_t key,
+                                            uint32_t r, int lane)
 {
-    constexpr int V = Fmt<DT>::V;
-    constexpr int ES = Fmt<DT>::esize;
-    constexpr int CPT = kTiesMaxBlock / NT / V;  // chunks per thread
-    constexpr int E = CPT * V;                   // elements per thread
-    static_assert(CPT >= 1, "block too small for the thread count");
-    __shared__ TiesSmem sm;
-    const int t = threadIdx.x;
-    const int lane = t & 63;
-    int64_t b = blockIdx.x;
-    if (b >= nblocks)
-        return;
+    uint32_t pref = key << ties::KS;
+#pragma unroll 1
+    for (int bit = ties::KS - 1; bit >= 0; --bit) {
+        const uint32_t cand = pref | (1u << bit);
+        uint32_t c = 0u;
+        for (uint32_t i = (uint32_t)lane; i < n; i += 64u)
+            c += (list[i] >= cand) ? 1u : 0u;
+        if (wave_sum_u32(c) >= r)
+            pref = cand;
+    }
+    return pref;
+}
 
-    static_assert(NT == 512, "the window scan gives each of the 8 waves a 256-bin slice");
-    for (int q = t; q < 2 * 2048; q += NT)
-        (&sm.hw[0][0])[q] = 0u;
-    if (t < 2)
-        sm.smax[t] = 0u;
-    __syncthreads();
-    const int wave = t >> 6;
-    uint32_t par = 0u;  // parity of the expert round (LDS buffer set)
-
-    BlockInfo cur = block_info(src, b, mask, boff, blen, density, kmask);
-    uint4 x0raw[CPT], nx0raw[CPT], nxt[CPT];
-    load_chunks<DT, NT, CPT>(chunk_ptr(base, cur.off, ES), cur.n / V, x0raw);
-    uint32_t mm = cur.m;
-    int rank = 0;
-    if (mm)
-        load_chunks<DT, NT, CPT>(src.expert(__builtin_ctz(mm), 0, b, cur.off, cur.n, ES), cur.n / V, nxt);
-
-    for (;;) {
-        const int64_t b2 = b + gridDim.x;
-        const bool has_next = b2 < nblocks;
-        BlockInfo nx{};
-        if (has_next)
-            nx = block_info(src, b2, mask, boff, blen, density, kmask);
-        const uint32_t nch = cur.n / V;
-        count_expert_bytes(ctr, cur.m, cur.n, ES);
-        float x0[E];
-#pragma unroll
-        for (int q = 0; q < CPT; ++q)
-            Fmt<DT>::unpack(x0raw[q], &x0[q * V]);
-
-        float ps[E], ns[E];
-        uint32_t pc[E], nc[E];
+// Whole workgroup: exact k-th largest magnitude pattern of slot j over all
+// of its elements (padding elements are zeros, which cannot change the k
+// largest), by levels on bits 30..20, 19..9 and 8..0.  Returns the pattern
+// (at least 1: a zero threshold keeps every nonzero delta).
+template <int E>
+__device__ inline uint32_t block_radix_select(TiesSmem& sm, int j, const float (&dj)[E], uint32_t k, int t,
+                                              int lane, int wave)
+{
+    uint32_t* h = sm.h[j];
+    uint32_t pref = 0u, r = k;
+#pragma unroll 1
+    for (int lv = 0; lv < 3; ++lv) {
+        const int sh = (lv == 0) ? 20 : ((lv == 1) ? 9 : 0);
+        const int wd = (lv == 2) ? 9 : 11;
+        __syncthreads();  // earlier readers of h and st are done
+        for (int q = t; q < ties::NB; q += ties::NT)
+            h[q] = 0u;
+        __syncthreads();
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            ps[e] = 0.0f;
-            ns[e] = 0.0f;
-            pc[e] = 0u;
-            nc[e] = 0u;
+            const uint32_t mg = __float_as_uint(dj[e]) & 0x7fffffffu;
+            const uint32_t hi = (lv == 0) ? 0u : (mg >> (sh + wd));
+            if (hi == pref)
+                atomicAdd(&h[(mg >> sh) & ((1u << wd) - 1u)], 1u);
         }
-        if (mm == 0u && has_next) {  // nothing to trim here: start loading the next block now
-            load_chunks<DT, NT, CPT>(chunk_ptr(base, nx.off, ES), nx.n / V, nx0raw);
-            if (nx.m)
-                load_chunks<DT, NT, CPT>(src.expert(__builtin_ctz(nx.m), 0, b2, nx.off, nx.n, ES), nx.n / V, nxt);
-        }
-        while (mm) {
-            mm &= mm - 1u;
-            uint4 ce[CPT];
-#pragma unroll
-            for (int q = 0; q < CPT; ++q)
-                ce[q] = nxt[q];
-            if (mm) {
-                load_chunks<DT, NT, CPT>(src.expert(__builtin_ctz(mm), rank + 1, b, cur.off, cur.n, ES), nch, nxt);
-            } else if (has_next) {
-                load_chunks<DT, NT, CPT>(chunk_ptr(base, nx.off, ES), nx.n / V, nx0raw);
-                if (nx.m)
-                    load_chunks<DT, NT, CPT>(src.expert(__builtin_ctz(nx.m), 0, b2, nx.off, nx.n, ES), nx.n / V,
-                                             nxt);
+        __syncthreads();
+        if (wave == 0) {
+            const Cut c = wave_find_from_top(h, (1 << wd) - 1, r, lane);
+            if (lane == 0) {
+                sm.st[j][1] = c.bin;
+                sm.st[j][2] = c.rank;
             }
-            float d[E];  // padding chunks were loaded as zeros: d = 0 there
-            uint32_t mg[E];
+        }
+        __syncthreads();
+        pref = (pref << wd) | uniform_u32(sm.st[j][1]);
+        r = uniform_u32(sm.st[j][2]);
+    }
+    return max(pref, 1u);
+}
+
+// Loads and trims up to GS selected experts of one block (the set bits of
+// gm, in increasing expert order; rank0 = rank of the first among all the
+// block's selected experts).  Leaves the deltas in d and the thresholds in
+// tau (wave-uniform patterns).  Every thread of the workgroup calls it.
+template <int DT, int CPT, class Src>
+__device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, uint64_t off, uint32_t n,
+                                       uint32_t k, uint32_t gm, int rank0, const float (&x0)[CPT * Fmt<DT>::V],
+                                       float (&d)[ties::GS][CPT * Fmt<DT>::V], uint32_t (&tau)[ties::GS])
+{
+    using namespace ties;
+    constexpr int V = Fmt<DT>::V, ES = Fmt<DT>::esize, E = CPT * V;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int ns = __popc(gm);
+    const uint32_t nch = n / V;
+
+    uint4 raw[GS][CPT];
+    {
+        uint32_t mm = gm;
+#pragma unroll
+        for (int j = 0; j < GS; ++j) {
+            if (j < ns) {
+                const int i = __builtin_ctz(mm);
+                mm &= mm - 1u;
+                load_chunks<DT, NT, CPT>(src.expert(i, rank0 + j, b, off, n, ES), nch, raw[j]);
+            }
+        }
+    }
+    // rows of the slots in use start at zero (the previous group's readers
+    // passed a barrier since)
+#pragma unroll
+    for (int j = 0; j < GS; ++j) {
+        if (j < ns) {
+#pragma unroll
+            for (int q = 0; q < NB / (4 * NT); ++q)
+                *reinterpret_cast<uint4*>(&sm.h[j][4 * (q * NT + t)]) = make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+    // ---- A: deltas and block maxima
+#pragma unroll
+    for (int j = 0; j < GS; ++j) {
+        if (j < ns) {
+            float mx = 0.0f;
 #pragma unroll
             for (int q = 0; q < CPT; ++q) {
                 float x[V];
-                Fmt<DT>::unpack(ce[q], x);
+                Fmt<DT>::unpack(raw[j][q], x);
 #pragma unroll
                 for (int v = 0; v < V; ++v) {
-                    const int e = q * V + v;
-                    d[e] = x[v] - x0[e];
-                    mg[e] = __float_as_uint(d[e]) & 0x7fffffffu;
+                    d[j][q * V + v] = x[v] - x0[q * V + v];  // padding: 0 - 0
+                    mx = fmaxf(mx, fabsf(d[j][q * V + v]));
                 }
             }
-            uint32_t* h = sm.hw[par];  // clean: cleared during the previous round
-            // ---- R1: block maximum
-            if (t == 0)
-                sm.smax[par ^ 1u] = 0u;  // for the next round
-            {
-                uint32_t mx = 0u;
+            const uint32_t w = wave_max_u32(__float_as_uint(mx));
+            if (lane == 0)
+                sm.wmax[j][wave] = w;
+        }
+    }
+    __syncthreads();
+    // ---- B: window histograms and top-binade counts
+    uint32_t bmax[GS];
 #pragma unroll
-                for (int e = 0; e < E; ++e)
-                    mx = max(mx, mg[e]);
-                const uint32_t wmx = wave_max_u32(mx);
-                if (lane == 0 && wmx != 0u)
-                    atomicMax(&sm.smax[par], wmx);
-            }
-            __syncthreads();
-            // every wave is past the previous round: clear its buffer for the next round
-            *reinterpret_cast<uint4*>(&sm.hw[par ^ 1u][4 * t]) = make_uint4(0u, 0u, 0u, 0u);
-            const uint32_t bmax = uniform_u32(sm.smax[par]);
-            uint32_t tau = 1u;  // all-zero block: nothing is kept
-            if (bmax != 0u) {
-                // ---- R2: window histogram over [2^(E_max - 3), max] (E_max: binade of the max)
-                const uint32_t ebin = bmax >> 23;
-                const uint32_t wlo = (ebin > 3u ? ebin - 3u : 0u) << 9;  // first key of the window
-                const uint32_t top = (bmax >> 14) - wlo;                  // bin of the max, < 2048
+    for (int j = 0; j < GS; ++j) {
+        bmax[j] = 0u;
+        if (j < ns) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+                bmax[j] = max(bmax[j], uniform_u32(sm.wmax[j][w]));
+            if (bmax[j] != 0u) {
+                const int wb = (int)((bmax[j] >> 23) << 9) - NB;  // key of bin 0
+                uint32_t ntop = 0u;
 #pragma unroll
                 for (int e = 0; e < E; ++e) {
-                    const uint32_t key = mg[e] >> 14;
-                    if (key >= wlo && mg[e] != 0u) {
-                        const uint32_t inc = (mg[e] & 0x3fffu) ? 0x10001u : 1u;
-                        atomicAdd(&h[key - wlo], inc);
-                    }
+                    const uint32_t bits = __float_as_uint(d[j][e]);
+                    const int rel = (int)((bits >> KS) & 0x1ffffu) - wb;
+                    if ((uint32_t)rel < (uint32_t)NB)
+                        atomicAdd(&sm.h[j][rel], (bits & ((1u << KS) - 1u)) ? 0x10001u : 1u);
+                    ntop += (uint32_t)__popcll(__ballot(rel >= NB));
                 }
-                __syncthreads();
-                // ---- R3 (one wave): scan; then refine while the bucket is not resolved
-                // level state: elements with (mg >> pshift) == pref are histogrammed on
-                // (mg >> dshift) & dmask; tau so far = pref << pshift
-                // ---- all waves: slice totals
-                const int g4 = 2047 - 256 * wave - 4 * lane - 3;  // this lane's four bins (slice of this wave)
-                const uint4 raw = *reinterpret_cast<const uint4*>(h + g4);
-                const uint32_t cnt4 = (raw.x & 0xffffu) + (raw.y & 0xffffu) + (raw.z & 0xffffu) + (raw.w & 0xffffu);
-                const uint32_t stot = wave_sum_u32(cnt4);
                 if (lane == 0)
-                    sm.slice[par][wave] = stot;
-                __syncthreads();
-                // ---- every wave: the slice holding the k-th largest, then its bin
-                uint32_t st = 0u, v1 = 0u, v2 = 0u;  // st 0: done (v1 = tau), 1: refine bucket, 2: restart
-                {
-                    uint32_t above = 0u;
-                    int sl = -1;
-#pragma unroll
-                    for (int w = 0; w < 8; ++w) {
-                        const uint32_t tw = uniform_u32(sm.slice[par][w]);
-                        if (sl < 0) {
-                            if (above + tw >= cur.k)
-                                sl = w;
-                            else
-                                above += tw;
-                        }
-                    }
-                    if (sl < 0) {
-                        st = 2u;  // fewer than k nonzero elements in the window: search everything
-                        v2 = cur.k;
-                    } else {
-                        const Cut c = wave_find_from_top(h, 2047 - 256 * sl, cur.k - above, lane);
-                        const uint32_t bin = c.bin;
-                        if (c.count == c.rank || c.aux == 0u) {
-                            v1 = max((wlo + bin) << 14, 1u);  // the bucket is kept whole / holds one value
-                        } else {
-                            st = 1u;
-                            v1 = wlo + bin;  // bucket key
-                            v2 = c.rank;
-                        }
-                    }
-                }
-                tau = v1;
-                if (st != 0u) {
-                    // rare: refinement levels, all in one buffer (the other set is clean for
-                    // the next round, this one is cleared at the start of the round after it)
-                    uint32_t rk = v2;
-                    uint32_t pref = (st == 1u) ? tau : 0u;
-                    int pshift = (st == 1u) ? 14 : 31;
-                    int dshift = (st == 1u) ? 3 : 20;
-#pragma unroll 1
-                    for (;;) {
-                        __syncthreads();  // everyone has read the previous level's result
-                        for (int q = t; q < 2048; q += NT)
-                            h[q] = 0u;
-                        __syncthreads();
-                        const uint32_t lowm = (dshift > 0) ? ((1u << dshift) - 1u) : 0u;
-#pragma unroll
-                        for (int e = 0; e < E; ++e) {
-                            const uint32_t hi = (pshift >= 31) ? 0u : (mg[e] >> pshift);
-                            if (hi == pref) {
-                                const uint32_t bin = (mg[e] >> dshift) & 2047u;
-                                atomicAdd(&h[bin], (mg[e] & lowm) ? 0x10001u : 1u);
-                            }
-                        }
-                        __syncthreads();
-                        if (t < 64) {
-                            const Cut c = wave_find_from_top(h, 2047, rk, lane);
-                            if (lane == 0) {
-                                sm.res[par][0] = c.found;
-                                sm.res[par][1] = c.bin;
-                                sm.res[par][2] = c.rank;
-                                sm.res[par][3] = (c.count == c.rank || c.aux == 0u) ? 1u : 0u;
-                            }
-                        }
-                        __syncthreads();
-                        const uint32_t found = uniform_u32(sm.res[par][0]);
-                        const uint32_t bin = uniform_u32(sm.res[par][1]);
-                        rk = uniform_u32(sm.res[par][2]);
-                        const uint32_t whole = uniform_u32(sm.res[par][3]);
-                        pref = (pshift >= 31 ? 0u : (pref << (pshift - dshift))) | bin;
-                        if (!found) {
-                            tau = 1u;  // fewer than k nonzero: keep every nonzero
-                            break;
-                        }
-                        if (whole || dshift == 0) {
-                            tau = max(pref << dshift, 1u);
-                            break;
-                        }
-                        pshift = dshift;
-                        dshift = dshift > 11 ? dshift - 11 : 0;
-                    }
-                    __syncthreads();  // every wave is done with the buffer
-                    for (int q = t; q < 2048; q += NT)
-                        h[q] = 0u;
-                }
+                    sm.wtop[j][wave] = ntop;
             }
-            // ---- keep, and accumulate the signed masses and their counts
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const bool keep = mg[e] >= tau;  // tau >= 1: a kept delta is not zero
-                const bool posr = (int32_t)__float_as_uint(d[e]) > 0;
-                const bool pos = keep && posr;
-                const bool neg = keep && !posr;
-                ps[e] = ps[e] + (pos ? d[e] : 0.0f);
-                ns[e] = ns[e] + (neg ? d[e] : 0.0f);
-                pc[e] += pos ? 1u : 0u;
-                nc[e] += neg ? 1u : 0u;
-            }
-            par ^= 1u;
-            ++rank;
         }
-        // ---- output of this block
-        uint4* po = reinterpret_cast<uint4*>(static_cast<char*>(out) + cur.off * ES);
-        // elect the sign of the larger signed mass; mean of the agreeing entries
-        float num[E];
-        uint32_t den[E];
-        bool any_div = false;
+    }
+    __syncthreads();
+    // ---- C: one wave per expert finds the bin of the k-th largest
+    if (wave < ns) {
+        const int j = wave;
+        uint32_t bm = 0u;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+            bm = max(bm, uniform_u32(sm.wmax[j][w]));
+        uint32_t state = DONE, v1 = 1u, v2 = 0u;  // v1: tau, or the bucket key to refine
+        if (bm != 0u && k < n) {                  // all zero, or k = n: keep every nonzero
+            uint32_t atop = 0u;
+#pragma unroll
+            for (int w = 0; w < NW; ++w)
+                atop += uniform_u32(sm.wtop[j][w]);
+            if (atop >= k) {
+                state = RADIX;  // tau lies in the top binade
+            } else {
+                const Cut c = wave_find_from_top(sm.h[j], NB - 1, k - atop, lane);
+                const int wb = (int)((bm >> 23) << 9) - NB;
+                if (!c.found) {
+                    state = RADIX;  // tau lies below the window
+                } else if (c.aux < c.rank || c.count == c.rank) {
+                    v1 = max((uint32_t)(wb + (int)c.bin) << KS, 1u);
+                } else {
+                    state = LIST;
+                    v1 = (uint32_t)(wb + (int)c.bin);
+                    v2 = c.rank;
+                }
+            }
+        }
+        if (lane == 0) {
+            sm.st[j][0] = state;
+            sm.st[j][1] = v1;
+            sm.st[j][2] = v2;
+            sm.st[j][3] = 0u;
+        }
+    }
+    __syncthreads();
+    // ---- D (rare): resolve inside the bucket, or select exactly
+    uint32_t anyst = 0u;
+#pragma unroll
+    for (int j = 0; j < GS; ++j)
+        if (j < ns)
+            anyst |= uniform_u32(sm.st[j][0]);
+    if (anyst != 0u) {
+        if (anyst & LIST) {
+#pragma unroll
+            for (int j = 0; j < GS; ++j) {
+                if (j < ns && uniform_u32(sm.st[j][0]) == LIST) {
+                    const uint32_t key = uniform_u32(sm.st[j][1]);
+#pragma unroll
+                    for (int e = 0; e < E; ++e) {
+                        const uint32_t mg = __float_as_uint(d[j][e]) & 0x7fffffffu;
+                        const bool in = (mg >> KS) == key;
+                        const unsigned long long bal = __ballot(in);
+                        if (bal) {  // wave-uniform
+                            uint32_t pos0 = 0u;
+                            if (lane == 0)
+                                pos0 = atomicAdd(&sm.st[j][3], (uint32_t)__popcll(bal));
+                            pos0 = uniform_u32(pos0);
+                            const uint32_t pos =
+                                pos0 + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+                            if (in && pos < (uint32_t)NB)
+                                sm.h[j][pos] = mg;
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+            if (wave < ns && uniform_u32(sm.st[wave][0]) == LIST) {
+                const int j = wave;
+                const uint32_t cnt = uniform_u32(sm.st[j][3]);
+                if (cnt <= (uint32_t)NB) {
+                    const uint32_t tv = wave_select_list(sm.h[j], cnt, uniform_u32(sm.st[j][1]),
+                                                         uniform_u32(sm.st[j][2]), lane);
+                    if (lane == 0) {
+                        sm.st[j][0] = DONE;
+                        sm.st[j][1] = max(tv, 1u);
+                    }
+                } else if (lane == 0) {
+                    sm.st[j][0] = RADIX;
+                }
+            }
+            __syncthreads();
+        }
+#pragma unroll
+        for (int j = 0; j < GS; ++j) {
+            if (j < ns && uniform_u32(sm.st[j][0]) == RADIX) {
+                const uint32_t tv = block_radix_select<E>(sm, j, d[j], k, t, lane, wave);
+                __syncthreads();  // every thread has read the last level's result
+                if (t == 0) {
+                    sm.st[j][0] = DONE;
+                    sm.st[j][1] = tv;
+                }
+                __syncthreads();
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < GS; ++j)
+        tau[j] = (j < ns) ? uniform_u32(sm.st[j][1]) : 0xffffffffu;
+}
+
+// Keep test and the running signed masses of element e over NS slots.
+template <int NS>
+__device__ inline void ties_accumulate(const float (&d)[ties::GS][16], const uint32_t (&tau)[ties::GS], int e,
+                                       float& P, float& N, uint32_t& np, uint32_t& nn)
+{
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+        const float dj = d[j][e];
+        const bool keep = fabsf(dj) >= __uint_as_float(tau[j]);  // tau >= the smallest positive pattern
+        const bool pos = dj > 0.0f;
+        P = P + ((keep && pos) ? dj : 0.0f);
+        N = N + ((keep && !pos) ? dj : 0.0f);
+        np += (keep && pos) ? 1u : 0u;
+        nn += (keep && !pos) ? 1u : 0u;
+    }
+}
+
+// Sign election (the sign of the larger of the positive and negative kept
+// masses) and the mean of the agreeing entries, for the V elements of one
+// chunk; then y = lambda * mean + x0, rounded once, is stored.
+template <int DT>
+__device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const float (&N)[Fmt<DT>::V],
+                                        const uint32_t (&np)[Fmt<DT>::V], const uint32_t (&nn)[Fmt<DT>::V],
+                                        const float* x0, float lambda, uint4* __restrict__ dst, bool ok)
+{
+    constexpr int V = Fmt<DT>::V;
+    float num[V];
+    uint32_t den[V];
+    bool odd = false;  // some agreeing count is not a power of two
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        const bool up = P[v] > -N[v];
+        const bool dn = P[v] < -N[v];
+        num[v] = up ? P[v] : (dn ? N[v] : 0.0f);
+        den[v] = up ? np[v] : (dn ? nn[v] : 1u);
+        odd |= (den[v] & (den[v] - 1u)) != 0u;
+    }
+    if (__any(odd)) {
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+            num[v] = num[v] / (float)den[v];
+    } else {  // division by 2^s is exact scaling (correctly rounded, as the quotient)
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+            num[v] = ldexpf(num[v], -__builtin_ctz(den[v]));
+    }
+    if (ok) {
+        float y[V];
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+            y[v] = fmaf(lambda, num[v], x0[v]);
+        *dst = Fmt<DT>::pack(y);
+    }
+}
+
+// All selected experts trimmed in one group: accumulate and store chunk by
+// chunk.
+template <int DT, int NS>
+__device__ inline void ties_finish_single(const float (&d)[ties::GS][16], const uint32_t (&tau)[ties::GS],
+                                          const float (&x0)[16], float lambda, uint4* __restrict__ po, uint32_t nch)
+{
+    constexpr int V = Fmt<DT>::V, CPT = 16 / V;
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+        float P[V], N[V];
+        uint32_t np[V], nn[V];
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            P[v] = 0.0f;
+            N[v] = 0.0f;
+            np[v] = 0u;
+            nn[v] = 0u;
+            if (NS > 0)
+                ties_accumulate<NS>(d, tau, q * V + v, P[v], N[v], np[v], nn[v]);
+        }
+        ties_store_chunk<DT>(P, N, np, nn, &x0[q * V], lambda, po + q * ties::NT + t,
+                             q * ties::NT + t < (int)nch);
+    }
+}
+
+// Several groups: the signed masses and the counts (positive in the low,
+// negative in the high half) are carried across groups.
+template <int NS>
+__device__ inline void ties_accumulate_all(const float (&d)[ties::GS][16], const uint32_t (&tau)[ties::GS],
+                                           float (&P)[16], float (&N)[16], uint32_t (&cnt)[16])
+{
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        uint32_t np = 0u, nn = 0u;
+        ties_accumulate<NS>(d, tau, e, P[e], N[e], np, nn);
+        cnt[e] += np | (nn << 16);
+    }
+}
+
+// MULTI = false: K <= GS, every selected expert is trimmed in one group.
+// MULTI = true: groups of GS experts in increasing order, with the signed
+// masses and counts carried across groups.
+template <int DT, bool MULTI, class Src>
+__global__ __launch_bounds__(ties::NT, MULTI ? 2 : 4) void k_merge_ties(Src src, const void* __restrict__ base,
+                                                         const uint32_t* __restrict__ mask,
+                                                         const uint64_t* __restrict__ boff,
+                                                         const uint32_t* __restrict__ blen, double density,
+                                                         uint32_t n_full, uint32_t k_full, float lambda,
+                                                         uint32_t kmask, void* __restrict__ out,
+                                                         unsigned long long* __restrict__ ctr)
+{
+    using namespace ties;
+    constexpr int V = Fmt<DT>::V, ES = Fmt<DT>::esize;
+    constexpr int CPT = kTiesMaxBlock / NT / V;  // chunks per thread and expert
+    constexpr int E = CPT * V;
+    static_assert(E == 16, "16 elements per thread and expert");
+    __shared__ TiesSmem sm;
+    const int64_t b = blockIdx.x;
+    const uint32_t g = uniform_u32(src.block(b));
+    const uint64_t off = boff[g];
+    const uint32_t n = blen[g];
+    uint32_t k = k_full;
+    if (n != n_full) {
+        const double kk = ceil(density * (double)n);
+        k = (kk >= (double)n) ? n : (uint32_t)kk;
+    }
+    const uint32_t m = (k != 0u) ? (mask[g] & kmask) : 0u;  // density 0 keeps nothing: no expert is read
+    const uint32_t nch = n / V;
+    count_expert_bytes(ctr, m, n, ES);
+    uint4 x0raw[CPT];
+    load_chunks<DT, NT, CPT>(chunk_ptr(base, off, ES), nch, x0raw);
+    float x0[E];
+#pragma unroll
+    for (int q = 0; q < CPT; ++q)
+        Fmt<DT>::unpack(x0raw[q], &x0[q * V]);
+    uint4* po = reinterpret_cast<uint4*>(static_cast<char*>(out) + off * ES);
+
+    float d[GS][E];
+    uint32_t tau[GS];
+    if (!MULTI) {
+        const int ns = __popc(m);
+        if (ns != 0)
+            ties_trim_group<DT, CPT>(sm, src, b, off, n, k, m, 0, x0, d, tau);
+        switch (ns) {
+        case 0: ties_finish_single<DT, 0>(d, tau, x0, lambda, po, nch); break;
+        case 1: ties_finish_single<DT, 1>(d, tau, x0, lambda, po, nch); break;
+        case 2: ties_finish_single<DT, 2>(d, tau, x0, lambda, po, nch); break;
+        case 3: ties_finish_single<DT, 3>(d, tau, x0, lambda, po, nch); break;
+        default: ties_finish_single<DT, 4>(d, tau, x0, lambda, po, nch); break;
+        }
+    } else {
+        float P[E], N[E];
+        uint32_t cnt[E];
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const bool up = ps[e] > -ns[e];
-            const bool dn = ps[e] < -ns[e];
-            num[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);
-            den[e] = up ? pc[e] : (dn ? nc[e] : 1u);
-            any_div |= den[e] > 1u;
+            P[e] = 0.0f;
+            N[e] = 0.0f;
+            cnt[e] = 0u;
         }
-        if (__any(any_div)) {  // one agreeing entry (or none) needs no division
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                num[e] = num[e] / (float)den[e];
+        uint32_t mm = m;
+        int rank0 = 0;
+        while (mm) {  // wave-uniform
+            uint32_t gm = 0u;
+            for (int j = 0; j < GS && mm; ++j) {
+                gm |= mm & (0u - mm);
+                mm &= mm - 1u;
+            }
+            ties_trim_group<DT, CPT>(sm, src, b, off, n, k, gm, rank0, x0, d, tau);
+            const int ns = __popc(gm);
+            switch (ns) {
+            case 1: ties_accumulate_all<1>(d, tau, P, N, cnt); break;
+            case 2: ties_accumulate_all<2>(d, tau, P, N, cnt); break;
+            case 3: ties_accumulate_all<3>(d, tau, P, N, cnt); break;
+            default: ties_accumulate_all<4>(d, tau, P, N, cnt); break;
+            }
+            rank0 += ns;
         }
+        const int t = threadIdx.x;
 #pragma unroll
         for (int q = 0; q < CPT; ++q) {
-            if (q * NT + t >= nch)
-                continue;
-            float y[V];
+            float Pq[V], Nq[V];
+            uint32_t npq[V], nnq[V];
 #pragma unroll
-            for (int v = 0; v < V; ++v)
-                y[v] = fmaf(lambda, num[q * V + v], x0[q * V + v]);
-            po[q * NT + t] = Fmt<DT>::pack(y);
+            for (int v = 0; v < V; ++v) {
+                Pq[v] = P[q * V + v];
+                Nq[v] = N[q * V + v];
+                npq[v] = cnt[q * V + v] & 0xffffu;
+                nnq[v] = cnt[q * V + v] >> 16;
+            }
+            ties_store_chunk<DT>(Pq, Nq, npq, nnq, &x0[q * V], lambda, po + q * NT + t, q * NT + t < (int)nch);
         }
-        if (!has_next)
-            break;
-        b = b2;
-        cur = nx;
-        mm = cur.m;
-        rank = 0;
-#pragma unroll
-        for (int q = 0; q < CPT; ++q)
-            x0raw[q] = nx0raw[q];
     }
 }
 
@@ -651,9 +786,16 @@ hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src
                            a.seed, kmask, out, ctr);
         break;
     case Op::TIES: {
-        const int64_t gridT = nb < kTiesGrid ? nb : kTiesGrid;
-        hipLaunchKernelGGL((k_merge_ties<DT, kTiesThreads, Src>), dim3((unsigned)gridT), dim3(kTiesThreads), 0, s,
-                           src, base, mask, bt.d_off, bt.d_len, a.density, a.lambda, kmask, out, ctr, nb);
+        // k for full-length blocks, as the kernel computes it for short ones
+        const uint32_t n_full = (uint32_t)bt.block_elems;
+        const double kk = ceil(a.density * (double)n_full);
+        const uint32_t k_full = (kk >= (double)n_full) ? n_full : (uint32_t)kk;
+        if (K <= ties::GS)
+            hipLaunchKernelGGL((k_merge_ties<DT, false, Src>), grid, dim3(ties::NT), 0, s, src, base, mask,
+                               bt.d_off, bt.d_len, a.density, n_full, k_full, a.lambda, kmask, out, ctr);
+        else
+            hipLaunchKernelGGL((k_merge_ties<DT, true, Src>), grid, dim3(ties::NT), 0, s, src, base, mask,
+                               bt.d_off, bt.d_len, a.density, n_full, k_full, a.lambda, kmask, out, ctr);
         break;
     }
     }

@@ -194,6 +194,49 @@ def test_ties_and_zero_and_identical_experts(mp):
     _run_all(mp, spec, base, coarse, "ties", [0.5, 1.0], density=0.15, lam=1.0)
 
 
+def _bf16_family_from_deltas(base_np, deltas):
+    """Experts W_i = bf16(fl32(W0 + d_i)) for the given fp32 deltas."""
+    x0 = (base_np.astype(np.uint32) << 16).view(np.float32)
+    return [oracle.round_bf16((x0 + d.astype(np.float32)).astype(np.float32)) for d in deltas]
+
+
+def test_ties_threshold_search_paths(mp):
+    # Delta distributions that drive every branch of the trim-threshold
+    # search: uniform magnitudes (the k-th largest lies in the binade of the
+    # block maximum), rare huge outliers (it lies far below the max), mostly
+    # unchanged weights (fewer than k nonzero deltas: everything nonzero is
+    # kept), bucket-dense values with distinct low bits, and densities that
+    # give k = 1 and k = n.
+    spec = _mini_qwen(n_layers=1, K=4)
+    base, _ = make_family(spec, seed=12)
+    P = base.size
+    rng = np.random.default_rng(12)
+    uni = rng.uniform(-0.01, 0.01, P)
+    heavy = rng.normal(0.0, 1e-4, P)
+    out_idx = rng.random(P) < 0.01
+    heavy[out_idx] = rng.normal(0.0, 1.0, int(out_idx.sum()))
+    sparse = np.where(rng.random(P) < 0.1, rng.normal(0.0, 1e-3, P), 0.0)
+    dense = 1e-3 * (1.0 + rng.integers(0, 4, P) / 64.0) * np.sign(rng.normal(size=P))
+    exps = _bf16_family_from_deltas(base, [uni, heavy, sparse, dense])
+    for dens in (0.2, 0.05, 1.0 / 4096, 1.0):
+        _say(f"case threshold paths density={dens}")
+        _run_all(mp, spec, base, exps, "ties", [0.5, 1.0], density=dens, lam=1.0)
+
+
+def test_ties_subnormal_deltas(mp):
+    # base weights near the bottom of the normal range, deltas subnormal in
+    # fp32: the magnitude patterns and the keep test must treat them exactly
+    spec = _mini_qwen(n_layers=1, K=3)
+    P = sum(int(np.prod(s)) for _, s in spec.tensors)
+    rng = np.random.default_rng(13)
+    base = oracle.round_bf16(rng.normal(0.0, 2e-38, P).astype(np.float32))
+    deltas = [rng.normal(0.0, s, P) for s in (1e-39, 5e-39, 3e-40)]
+    exps = _bf16_family_from_deltas(base, deltas)
+    _say("case subnormal deltas")
+    _run_all(mp, spec, base, exps, "ties", [0.4, 1.0], density=0.2, lam=1.0)
+    _run_all(mp, spec, base, exps, "ties", [1.0], density=0.3, lam=0.5)
+
+
 def test_budget_boundaries_exact(mp):
     # budgets at the exact cost of a greedy prefix, one byte below and above
     spec = _mini_qwen(n_layers=1)
