@@ -111,6 +111,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-stride", type=int, default=2)
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="after the timed region, run the AVG merge once with an empty mask: a plain copy "
+                         "of the base (reads 2P + 4G bytes, writes 2P) for scaling hardware byte counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build measures one GPU only; run with --gpus 1", file=sys.stderr)
@@ -181,6 +184,10 @@ def main():
     stats = recs[-1][4]
     io = mp.mp_merge_ties(L, base, exps, masks[0], 0.2, 1.0, out, io=True, stream=stream)
     assert io["expert_bytes"] == stats[0]["cost_bytes"]
+    if args.calibration_copy:
+        empty = torch.zeros(G, dtype=torch.int32, device="cuda")
+        mp.mp_merge_avg(L, base, exps, empty, [0.25] * K, out, stream=stream)
+        torch.cuda.synchronize()
 
     ckpt = P * 2
     per_budget = []

@@ -36,12 +36,6 @@ struct Fmt<0> {  // fp32
 
 // bfloat16 -> fp32 is exact (the 16 high bits of the fp32 pattern).
 // fp32 -> bfloat16 rounds to nearest, ties to even (inputs are finite).
-__device__ static inline uint32_t bf16_rne_bits(float f)
-{
-    uint32_t u = __float_as_uint(f);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-}
 
 template <>
 struct Fmt<1> {  // bf16
@@ -58,12 +52,18 @@ struct Fmt<1> {  // bf16
         f[6] = __uint_as_float(c.w << 16);
         f[7] = __uint_as_float(c.w & 0xffff0000u);
     }
+    // Hardware conversion (v_cvt_pk_bf16_f32, round to nearest even).  On
+    // gfx950 it gives (u + 0x7fff + ((u >> 16) & 1)) >> 16 of the fp32
+    // pattern u for every finite input (checked exhaustively, both halves).
+    __device__ static inline uint32_t pack2(float a, float b)
+    {
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        const bf16x2 v = {(__bf16)a, (__bf16)b};
+        return __builtin_bit_cast(uint32_t, v);
+    }
     __device__ static inline uint4 pack(const float* f)
     {
-        return make_uint4(bf16_rne_bits(f[0]) | (bf16_rne_bits(f[1]) << 16),
-                          bf16_rne_bits(f[2]) | (bf16_rne_bits(f[3]) << 16),
-                          bf16_rne_bits(f[4]) | (bf16_rne_bits(f[5]) << 16),
-                          bf16_rne_bits(f[6]) | (bf16_rne_bits(f[7]) << 16));
+        return make_uint4(pack2(f[0], f[1]), pack2(f[2], f[3]), pack2(f[4], f[5]), pack2(f[6], f[7]));
     }
 };
 

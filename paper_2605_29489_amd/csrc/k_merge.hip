@@ -236,12 +236,27 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
 // smallest positive pattern, so a kept delta is not zero), elects the sign
 // of the larger of the positive and negative kept masses and takes the mean
 // of the agreeing entries.
+#ifndef MP_TIES_MB
+#define MP_TIES_MB 7
+#endif
+#ifndef MP_TIES_NC
+#define MP_TIES_NC 4
+#endif
+#ifndef MP_TIES_ASM
+#define MP_TIES_ASM 1
+#endif
 namespace ties {
-constexpr int NT = 256;      // threads per workgroup
-constexpr int NW = NT / 64;  // waves per workgroup
-constexpr int GS = 4;        // experts trimmed together (one scanning wave each)
-constexpr int NB = 2048;     // window bins
-constexpr int KS = 14;       // pattern bits below a window key
+constexpr int NT = 256;         // threads per workgroup
+constexpr int NW = NT / 64;     // waves per workgroup
+constexpr int GS = 4;           // experts trimmed together (one scanning wave each)
+constexpr int MB = MP_TIES_MB;  // mantissa bits in a window key
+constexpr int NC = MP_TIES_NC;  // copies of each window bin (lanes spread over them)
+constexpr int KS = 23 - MB;     // pattern bits below a key
+constexpr int NBIN = 4 << MB;   // window bins: four binades
+constexpr int NB = 2048;        // words per histogram row
+static_assert(NBIN * NC == NB, "a histogram row holds every copy of every bin");
+static_assert(NC == 1 || NC == 2 || NC == 4 || NC == 8 || NC == 16, "bins are 16-byte aligned or fill one");
+constexpr int LG = (NC == 1) ? 2 : (NC == 2) ? 3 : (NC == 4) ? 4 : (NC == 8) ? 5 : 6;  // log2(4 NC)
 enum : uint32_t { DONE = 0u, LIST = 1u, RADIX = 2u };
 }  // namespace ties
 
@@ -256,44 +271,85 @@ struct Cut {
     uint32_t found, bin, rank, count, aux;  // wave-uniform
 };
 
-// Wave-level, all lanes: walk histogram bins downward from `top` and find
-// the bin where the count from the top first reaches k.  Counts are the low
-// 16 bits of each counter; aux returns the bin's high 16 bits.  rank = k
-// minus the count above the bin.  Each round reads 256 bins, four
-// consecutive bins per lane (conflict-free 16-byte LDS reads), and
+// Wave-level, all lanes: walk histogram bins downward from bin `top` and
+// find the bin where the count from the top first reaches k.  A bin is NC
+// consecutive words; counts are the low 16 bits of the word sums and aux
+// returns the bin's high-half sum.  rank = k minus the count above the bin.
+// Each round reads 1 KB: 16 consecutive bytes per lane (conflict-free), and
 // prefix-sums the lane totals across the wave with DPP.
+template <int NC>
 __device__ inline Cut wave_find_from_top(const uint32_t* __restrict__ h, int top, uint32_t k, int lane)
 {
+    if (NC >= 4) {  // one bin per lane per round
+        Cut r{0u, 0u, 0u, 0u, 0u};
+        uint32_t above = 0;
+        for (int hb = top; hb >= 0; hb -= 64) {
+            const int bin = hb - lane;
+            uint32_t w = 0u;
+            if (bin >= 0) {
+                const uint4* p = reinterpret_cast<const uint4*>(h + bin * NC);
+#pragma unroll
+                for (int u = 0; u < NC / 4; ++u) {
+                    const uint4 raw = p[u];
+                    w += raw.x + raw.y + raw.z + raw.w;
+                }
+            }
+            const uint32_t s = w & 0xffffu;
+            const uint32_t incl = wave_incl_sum(s);
+            const uint32_t before = above + incl - s;
+            const bool hit = before < k && k <= above + incl;
+            const unsigned long long bal = __ballot(hit);
+            if (bal) {
+                const int src = __ffsll((long long)bal) - 1;
+                r.found = 1u;
+                r.bin = (uint32_t)__builtin_amdgcn_readlane(bin, src);
+                r.rank = (uint32_t)__builtin_amdgcn_readlane((int)(k - before), src);
+                r.count = (uint32_t)__builtin_amdgcn_readlane((int)s, src);
+                r.aux = (uint32_t)__builtin_amdgcn_readlane((int)(w >> 16), src);
+                return r;
+            }
+            above += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+        }
+        return r;
+    }
+    constexpr int BPL = NC >= 4 ? 1 : 4 / NC;  // bins per lane per round
     Cut r{0u, 0u, 0u, 0u, 0u};
-    top |= 3;
+    const int topw = top * NC + NC - 1;  // highest word
     uint32_t above = 0;
-    for (int hi = top; hi >= 0; hi -= 256) {
-        const int g4 = hi - 4 * lane - 3;  // multiple of 4: the lane's bins are g4 .. g4+3
+    for (int hi = topw | 3; hi >= 0; hi -= 256) {
+        const int g4 = hi - 4 * lane - 3;  // multiple of 4: the lane's words are g4 .. g4+3
         uint4 raw = make_uint4(0u, 0u, 0u, 0u);
         if (g4 >= 0)
             raw = *reinterpret_cast<const uint4*>(h + g4);
-        const uint4 v = make_uint4(raw.x & 0xffffu, raw.y & 0xffffu, raw.z & 0xffffu, raw.w & 0xffffu);
-        const uint32_t s = v.x + v.y + v.z + v.w;
+        uint32_t bw[BPL];  // bin sums, highest bin first
+        if (NC == 1) {
+            bw[0] = raw.w; bw[BPL > 1 ? 1 : 0] = raw.z; bw[BPL > 2 ? 2 : 0] = raw.y; bw[BPL > 3 ? 3 : 0] = raw.x;
+        } else if (NC == 2) {
+            bw[0] = raw.z + raw.w; bw[BPL > 1 ? 1 : 0] = raw.x + raw.y;
+        } else {
+            bw[0] = raw.x + raw.y + raw.z + raw.w;
+        }
+        uint32_t s = 0u;
+#pragma unroll
+        for (int q = 0; q < BPL; ++q)
+            s += bw[q] & 0xffffu;
         const uint32_t incl = wave_incl_sum(s);
-        const uint32_t before = above + incl - s;  // count in the bins above this lane's four
+        const uint32_t before = above + incl - s;  // count in the bins above this lane's
         const bool hit = before < k && k <= above + incl;
         const unsigned long long bal = __ballot(hit);
         if (bal) {
-            uint32_t c = before, bin, cnt, aux;
-            if (c + v.w >= k) {
-                bin = g4 + 3; cnt = v.w; aux = raw.w;
-            } else {
-                c += v.w;
-                if (c + v.z >= k) {
-                    bin = g4 + 2; cnt = v.z; aux = raw.z;
-                } else {
-                    c += v.z;
-                    if (c + v.y >= k) {
-                        bin = g4 + 1; cnt = v.y; aux = raw.y;
-                    } else {
-                        c += v.y;
-                        bin = g4; cnt = v.x; aux = raw.x;
-                    }
+            uint32_t c = before, bin = 0u, cnt = 0u, aux = 0u;
+            bool got = false;
+#pragma unroll
+            for (int q = 0; q < BPL; ++q) {
+                const uint32_t cq = bw[q] & 0xffffu;
+                if (!got && (c + cq >= k || q == BPL - 1)) {
+                    got = true;
+                    bin = (uint32_t)(g4 / NC + BPL - 1 - q);
+                    cnt = cq;
+                    aux = bw[q] >> 16;
+                } else if (!got) {
+                    c += cq;
                 }
             }
             const int src = __ffsll((long long)bal) - 1;
@@ -301,7 +357,7 @@ __device__ inline Cut wave_find_from_top(const uint32_t* __restrict__ h, int top
             r.bin = (uint32_t)__builtin_amdgcn_readlane((int)bin, src);
             r.rank = (uint32_t)__builtin_amdgcn_readlane((int)(k - c), src);
             r.count = (uint32_t)__builtin_amdgcn_readlane((int)cnt, src);
-            r.aux = (uint32_t)__builtin_amdgcn_readlane((int)(aux >> 16), src);
+            r.aux = (uint32_t)__builtin_amdgcn_readlane((int)aux, src);
             return r;
         }
         above += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
@@ -369,7 +425,7 @@ __device__ inline uint32_t block_radix_select(TiesSmem& sm, int j, const float (
         }
         __syncthreads();
         if (wave == 0) {
-            const Cut c = wave_find_from_top(h, (1 << wd) - 1, r, lane);
+            const Cut c = wave_find_from_top<1>(h, (1 << wd) - 1, r, lane);
             if (lane == 0) {
                 sm.st[j][1] = c.bin;
                 sm.st[j][2] = c.rank;
@@ -450,15 +506,37 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
             for (int w = 0; w < NW; ++w)
                 bmax[j] = max(bmax[j], uniform_u32(sm.wmax[j][w]));
             if (bmax[j] != 0u) {
-                const int wb = (int)((bmax[j] >> 23) << 9) - NB;  // key of bin 0
+                const int wb = (int)((bmax[j] >> 23) << MB) - NBIN;  // key of bin 0
+                // byte offset of key kk in this lane's copy: (kk << LG) + koff; out of
+                // the window it wraps past the row
+                const uint32_t koff = (uint32_t)(lane & (NC - 1)) * 4u - (uint32_t)wb * (uint32_t)(4 * NC);
+                const float topf = __uint_as_float((bmax[j] >> 23) << 23);  // first value of M's binade
+                char* row = reinterpret_cast<char*>(sm.h[j]);
                 uint32_t ntop = 0u;
 #pragma unroll
                 for (int e = 0; e < E; ++e) {
                     const uint32_t bits = __float_as_uint(d[j][e]);
-                    const int rel = (int)((bits >> KS) & 0x1ffffu) - wb;
-                    if ((uint32_t)rel < (uint32_t)NB)
-                        atomicAdd(&sm.h[j][rel], (bits & ((1u << KS) - 1u)) ? 0x10001u : 1u);
-                    ntop += (uint32_t)__popcll(__ballot(rel >= NB));
+#if MP_TIES_ASM
+                    static_assert(KS == 16, "the low bits are the low half-word");
+                    uint32_t key, boff;
+                    asm("v_bfe_u32 %0, %1, %2, %3" : "=v"(key) : "v"(bits), "i"(KS), "i"(31 - KS));
+                    asm("v_lshl_add_u32 %0, %1, %2, %3" : "=v"(boff) : "v"(key), "i"(LG), "v"(koff));
+#else
+                    const uint32_t boff = (__builtin_amdgcn_ubfe(bits, KS, 31 - KS) << LG) + koff;
+#endif
+                    if (boff < (uint32_t)(NB * 4)) {
+                        // count in the high half when the low bits are not zero
+#if MP_TIES_ASM
+                        uint32_t nz;
+                        asm("v_min_u32_sdwa %0, %1, 1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD"
+                            : "=v"(nz) : "v"(bits));
+                        const uint32_t inc = (nz << 16) + 1u;
+#else
+                        const uint32_t inc = (min(bits & ((1u << KS) - 1u), 1u) << 16) + 1u;
+#endif
+                        atomicAdd(reinterpret_cast<uint32_t*>(row + boff), inc);
+                    }
+                    ntop += (uint32_t)__popcll(__ballot(fabsf(d[j][e]) >= topf));
                 }
                 if (lane == 0)
                     sm.wtop[j][wave] = ntop;
@@ -482,8 +560,8 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
             if (atop >= k) {
                 state = RADIX;  // tau lies in the top binade
             } else {
-                const Cut c = wave_find_from_top(sm.h[j], NB - 1, k - atop, lane);
-                const int wb = (int)((bm >> 23) << 9) - NB;
+                const Cut c = wave_find_from_top<NC>(sm.h[j], NBIN - 1, k - atop, lane);
+                const int wb = (int)((bm >> 23) << MB) - NBIN;
                 if (!c.found) {
                     state = RADIX;  // tau lies below the window
                 } else if (c.aux < c.rank || c.count == c.rank) {
@@ -569,30 +647,44 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
         tau[j] = (j < ns) ? uniform_u32(sm.st[j][1]) : 0xffffffffu;
 }
 
-// Keep test and the running signed masses of element e over NS slots.
+// Keep test and the running signed masses of element e over NS slots; the
+// kept counts go to cnt (positive in the low, negative in the high half).
 template <int NS>
 __device__ inline void ties_accumulate(const float (&d)[ties::GS][16], const uint32_t (&tau)[ties::GS], int e,
-                                       float& P, float& N, uint32_t& np, uint32_t& nn)
+                                       float& P, float& N, uint32_t& cnt)
 {
 #pragma unroll
     for (int j = 0; j < NS; ++j) {
         const float dj = d[j][e];
         const bool keep = fabsf(dj) >= __uint_as_float(tau[j]);  // tau >= the smallest positive pattern
-        const bool pos = dj > 0.0f;
-        P = P + ((keep && pos) ? dj : 0.0f);
-        N = N + ((keep && !pos) ? dj : 0.0f);
-        np += (keep && pos) ? 1u : 0u;
-        nn += (keep && !pos) ? 1u : 0u;
+        const bool kp = keep && dj > 0.0f;
+        const bool kn = keep && !(dj > 0.0f);
+        P = P + (kp ? dj : 0.0f);
+        N = N + (kn ? dj : 0.0f);
+        cnt += kp ? 1u : (kn ? 0x10000u : 0u);
     }
+}
+
+// x / 3 correctly rounded for every finite nonzero x: the product with the
+// rounded reciprocal is within one ulp, and one FMA residual step fixes it
+// (Markstein's correction; checked against IEEE division on all 2^32 fp32
+// patterns -- only -0 comes out as +0, and a mean of three entries that
+// agree in sign is never zero).
+__device__ inline float div3(float x)
+{
+    const float y = 0x1.555556p-2f;  // fl32(1/3)
+    const float q = x * y;
+    return fmaf(fmaf(-3.0f, q, x), y, q);
 }
 
 // Sign election (the sign of the larger of the positive and negative kept
 // masses) and the mean of the agreeing entries, for the V elements of one
-// chunk; then y = lambda * mean + x0, rounded once, is stored.
-template <int DT>
+// chunk; then y = lambda * mean + x0, rounded once, is stored.  SMALLK: at
+// most 4 entries agree, so the count is 1, 2, 3 or 4.
+template <int DT, bool SMALLK>
 __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const float (&N)[Fmt<DT>::V],
-                                        const uint32_t (&np)[Fmt<DT>::V], const uint32_t (&nn)[Fmt<DT>::V],
-                                        const float* x0, float lambda, uint4* __restrict__ dst, bool ok)
+                                        const uint32_t (&cnt)[Fmt<DT>::V], const float* x0, float lambda,
+                                        uint4* __restrict__ dst, bool ok)
 {
     constexpr int V = Fmt<DT>::V;
     float num[V];
@@ -603,17 +695,24 @@ __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const floa
         const bool up = P[v] > -N[v];
         const bool dn = P[v] < -N[v];
         num[v] = up ? P[v] : (dn ? N[v] : 0.0f);
-        den[v] = up ? np[v] : (dn ? nn[v] : 1u);
+        den[v] = up ? (cnt[v] & 0xffffu) : (dn ? (cnt[v] >> 16) : 1u);
         odd |= (den[v] & (den[v] - 1u)) != 0u;
     }
-    if (__any(odd)) {
+    if (SMALLK) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            // division by 2^s is exact scaling (correctly rounded, as the quotient)
+            const float qp = num[v] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[v])) << 23);
+            num[v] = (den[v] == 3u) ? div3(num[v]) : qp;
+        }
+    } else if (__any(odd)) {
 #pragma unroll
         for (int v = 0; v < V; ++v)
             num[v] = num[v] / (float)den[v];
-    } else {  // division by 2^s is exact scaling (correctly rounded, as the quotient)
+    } else {
 #pragma unroll
         for (int v = 0; v < V; ++v)
-            num[v] = ldexpf(num[v], -__builtin_ctz(den[v]));
+            num[v] = num[v] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[v])) << 23);
     }
     if (ok) {
         float y[V];
@@ -635,33 +734,29 @@ __device__ inline void ties_finish_single(const float (&d)[ties::GS][16], const 
 #pragma unroll
     for (int q = 0; q < CPT; ++q) {
         float P[V], N[V];
-        uint32_t np[V], nn[V];
+        uint32_t cnt[V];
 #pragma unroll
         for (int v = 0; v < V; ++v) {
             P[v] = 0.0f;
             N[v] = 0.0f;
-            np[v] = 0u;
-            nn[v] = 0u;
+            cnt[v] = 0u;
             if (NS > 0)
-                ties_accumulate<NS>(d, tau, q * V + v, P[v], N[v], np[v], nn[v]);
+                ties_accumulate<NS>(d, tau, q * V + v, P[v], N[v], cnt[v]);
         }
-        ties_store_chunk<DT>(P, N, np, nn, &x0[q * V], lambda, po + q * ties::NT + t,
-                             q * ties::NT + t < (int)nch);
+        ties_store_chunk<DT, true>(P, N, cnt, &x0[q * V], lambda, po + q * ties::NT + t,
+                                   q * ties::NT + t < (int)nch);
     }
 }
 
-// Several groups: the signed masses and the counts (positive in the low,
-// negative in the high half) are carried across groups.
+// Several groups: the signed masses and the counts are carried across
+// groups.
 template <int NS>
 __device__ inline void ties_accumulate_all(const float (&d)[ties::GS][16], const uint32_t (&tau)[ties::GS],
                                            float (&P)[16], float (&N)[16], uint32_t (&cnt)[16])
 {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-        uint32_t np = 0u, nn = 0u;
-        ties_accumulate<NS>(d, tau, e, P[e], N[e], np, nn);
-        cnt[e] += np | (nn << 16);
-    }
+    for (int e = 0; e < 16; ++e)
+        ties_accumulate<NS>(d, tau, e, P[e], N[e], cnt[e]);
 }
 
 // MULTI = false: K <= GS, every selected expert is trimmed in one group.
@@ -746,15 +841,14 @@ __global__ __launch_bounds__(ties::NT, MULTI ? 2 : 4) void k_merge_ties(Src src,
 #pragma unroll
         for (int q = 0; q < CPT; ++q) {
             float Pq[V], Nq[V];
-            uint32_t npq[V], nnq[V];
+            uint32_t cq[V];
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 Pq[v] = P[q * V + v];
                 Nq[v] = N[q * V + v];
-                npq[v] = cnt[q * V + v] & 0xffffu;
-                nnq[v] = cnt[q * V + v] >> 16;
+                cq[v] = cnt[q * V + v];
             }
-            ties_store_chunk<DT>(Pq, Nq, npq, nnq, &x0[q * V], lambda, po + q * NT + t, q * NT + t < (int)nch);
+            ties_store_chunk<DT, false>(Pq, Nq, cq, &x0[q * V], lambda, po + q * NT + t, q * NT + t < (int)nch);
         }
     }
 }

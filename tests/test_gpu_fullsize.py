@@ -82,6 +82,7 @@ def _full_run(mp, name, K, op, budgets, n_random=192, **kw):
         assert io["expert_bytes"] == st["cost_bytes"]
         got, _ = gather_blocks(out, blocks, ids)
         nb = assert_merge_equal(got, want, None, "bf16", f"{name} {op} B={f}")
+        assert nb == 0, f"{name} {op} B={f}: {nb} sampled values within tolerance but not bitwise equal"
         _say(f"  B={f}: cost={st['cost_bytes']} selected={st['n_selected']} sampled non-bitwise={nb}")
     del base, exps, out
     torch.cuda.empty_cache()

@@ -3,8 +3,10 @@ same seeded inputs.
 
 Bars: index (sumsq), mask and plan statistics bit-exact; merged weights
 within 1e-6 relative (fp32) or 1 bf16 ulp after the final rounding
-(`assert_merge_equal`); the expert bytes the merge kernels load equal the
-plan's cost (Prop. 1: the executor reads only selected blocks).
+(`assert_merge_equal`), and in fact bitwise equal: both sides fix the same
+operation order, so any difference is reported; the expert bytes the merge
+kernels load equal the plan's cost (Prop. 1: the executor reads only
+selected blocks).
 """
 
 import math
@@ -108,6 +110,7 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, **kw):
                                      kw.get("alpha", [1.0] * K), kw["lam"])
         got = to_host(out)
         nb = assert_merge_equal(got, want, base_np, dtype, f"{op} B={B}")
+        assert nb == 0, f"{op} B={B}: {nb} values within tolerance but not bitwise equal"
         assert io["expert_bytes"] == st["cost_bytes"], "kernels loaded bytes outside the plan"
         results.append((B, st, nb))
         _say(f"  {spec.name} {op} B={B}: cost={st['cost_bytes']} sel={st['n_selected']} non-bitwise={nb}")
