@@ -24,10 +24,13 @@
  * Memory.  Unless stated otherwise pointers are device pointers (memory of
  *   the current HIP device).  `experts` is a HOST array of K pointers; with
  *   residency MP_HOST_PINNED those K pointers are pinned host memory
- *   (hipHostMalloc / pinned torch tensors), otherwise device memory.  The
- *   caller owns every buffer; the library only reads inputs and writes the
- *   named outputs.  The library keeps a per-device workspace (block tables,
- *   plan scratch, staging buffers, a side stream) that mp_release() frees.
+ *   (hipHostMalloc / pinned torch tensors) and the kernels read expert
+ *   blocks straight from it over PCIe -- only the blocks a call touches
+ *   cross the link, with no staging copy (the host-to-device feed of
+ *   Algorithm 2).  Otherwise they are device memory.  The caller owns every
+ *   buffer; the library only reads inputs and writes the named outputs.
+ *   The library keeps a per-device workspace (block tables, plan scratch,
+ *   byte counters) that mp_release() frees.
  * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Work is
  *   enqueued on it; calls return once enqueued unless stated otherwise.
  *   Calls that fill a host-side stats struct synchronise the stream first.
@@ -57,7 +60,6 @@ extern "C" {
 #define MP_E_UNSUPPORTED (-2) /* valid request this build does not handle */
 #define MP_E_NOMEM (-3)       /* workspace allocation failed */
 #define MP_E_HIP (-4)         /* a HIP runtime call failed */
-#define MP_E_IO (-5)          /* host-to-device streaming failed */
 
 typedef enum { MP_F32 = 0, MP_BF16 = 1 } mp_dtype;
 typedef enum { MP_DEVICE = 0, MP_HOST_PINNED = 1 } mp_residency;
@@ -83,9 +85,7 @@ typedef struct mp_io_stats {
     uint64_t expert_bytes; /* expert bytes the merge kernels loaded */
     uint64_t base_bytes;   /* base bytes read */
     uint64_t out_bytes;    /* output bytes written */
-    uint64_t h2d_bytes;    /* bytes copied host -> device (MP_HOST_PINNED) */
-    uint64_t h2d_copies;   /* number of host -> device copies issued */
-    uint64_t n_stages;     /* pipeline stages (MP_HOST_PINNED) */
+    uint64_t h2d_bytes;    /* expert bytes read over PCIe (MP_HOST_PINNED), else 0 */
 } mp_io_stats;
 
 /* Number of blocks G of a layout (Section 2's block partition).
@@ -101,10 +101,8 @@ int mp_layout_blocks(const mp_layout* layout, int64_t* n_blocks);
  * becomes p_l + p_(l xor s); S = p_0.  (The paper fixes no order; a fixed
  * one makes plans reproducible bit for bit.)
  *   sumsq: device float[G*K], written at uid = g*K + i.
- * MP_DEVICE: asynchronous on `stream`.  MP_HOST_PINNED: every expert byte
- * crosses PCIe once (amortised catalog construction); the call returns
- * after the work is enqueued and the staging buffers are released, i.e.
- * it synchronises `stream`. */
+ * Asynchronous on `stream`.  With MP_HOST_PINNED every expert byte crosses
+ * PCIe once (the amortised catalog construction). */
 int mp_index_blocks(const mp_layout* layout, const void* base,
                     const void* const* experts, int32_t K, int32_t residency,
                     float* sumsq, void* stream);
@@ -134,19 +132,22 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq,
  * alpha: HOST float[K], fixed (no renormalisation over the selected
  * experts).  Unselected experts are never read.  mask: device uint32[G].
  * io: optional (NULL = none); when given the call synchronises `stream`
- * and reports the bytes the kernels loaded and stored. */
+ * and reports the bytes the kernels loaded and stored (Prop. 1: the expert
+ * bytes equal the cost of the mask, since only selected blocks are read). */
 int mp_merge_avg(const mp_layout* layout, const void* base,
                  const void* const* experts, int32_t K, int32_t residency,
                  const uint32_t* mask, const float* alpha, void* out,
                  mp_io_stats* io, void* stream);
 
-/* Budgeted TIES (Appendix A.1: trim, elect signs, disjoint mean after
- * masking).  Trim is per selected (expert, block): k = min(n, ceil(density
- * * n)) in fp64, tau = the k-th largest |d| of the block; d is kept iff
- * |d| >= tau and |d| > 0.  Per element: sigma = sum of kept d over selected
- * experts (fp32 adds from +0, increasing i); gamma = sign(sigma); mean =
- * (sum of kept d with sign gamma) / (their count), 0 if none;
- * out = round(fma(lambda, mean, x_0)).  0 <= density <= 1.
+/* Budgeted TIES (Appendix A.1: trim, sign election and disjoint mean over
+ * the masked deltas).  Trim is per selected (expert, block): k = min(n,
+ * ceil(density * n)) in fp64, tau = the k-th largest |d| of the block; d is
+ * kept iff |d| >= tau and |d| > 0.  Per element, over the selected experts
+ * in increasing order: P = sum of the positive kept d, N = sum of the
+ * negative kept d (fp32 adds from +0), with their counts; the elected sign
+ * is + if P > -N, - if P < -N, none if equal (the sign of the total kept
+ * mass; the paper fixes no summation order); mean = P / count(+), N /
+ * count(-) or 0; out = round(fma(lambda, mean, x_0)).  0 <= density <= 1.
  * block_elems must be <= 4096 (MP_E_UNSUPPORTED otherwise). */
 int mp_merge_ties(const mp_layout* layout, const void* base,
                   const void* const* experts, int32_t K, int32_t residency,

@@ -26,7 +26,6 @@ MP_E_ARG = -1
 MP_E_UNSUPPORTED = -2
 MP_E_NOMEM = -3
 MP_E_HIP = -4
-MP_E_IO = -5
 MP_F32, MP_BF16 = 0, 1
 MP_DEVICE, MP_HOST_PINNED = 0, 1
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
@@ -50,7 +49,7 @@ class mp_plan_stats(C.Structure):
 
 class mp_io_stats(C.Structure):
     _fields_ = [("expert_bytes", C.c_uint64), ("base_bytes", C.c_uint64), ("out_bytes", C.c_uint64),
-                ("h2d_bytes", C.c_uint64), ("h2d_copies", C.c_uint64), ("n_stages", C.c_uint64)]
+                ("h2d_bytes", C.c_uint64)]
 
     def as_dict(self):
         return {f: int(getattr(self, f)) for f, _ in self._fields_}

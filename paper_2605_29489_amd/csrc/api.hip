@@ -17,7 +17,6 @@
 #include <vector>
 
 #include "mp_internal.h"
-#include "pipeline.h"
 
 namespace mp {
 
@@ -48,7 +47,6 @@ struct DeviceWs {
     PlanScratch plan;
     unsigned long long* counters = nullptr;  // [256]
     unsigned long long* h_counters = nullptr;  // pinned [256]
-    std::unique_ptr<Pipeline> pipe;
 };
 
 std::mutex g_mu;
@@ -72,7 +70,6 @@ void free_ws(int dev, DeviceWs& w)
     int cur = 0;
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(dev);
-    w.pipe.reset();
     (void)hipFree(w.plan.ctl);
     (void)hipFree(w.plan.list[0]);
     (void)hipFree(w.plan.list[1]);
@@ -278,10 +275,13 @@ int check_device_buffer(const void* p, size_t bytes, const char* name)
     return MP_OK;
 }
 
-int check_pinned_buffer(const void* p, size_t bytes, const char* name)
+// Pinned host memory of at least `bytes` bytes from p; *dev receives the
+// address at which device kernels read it (they then load over PCIe).
+int check_pinned_buffer(const void* p, size_t bytes, const char* name, const void** dev)
 {
     if (p == nullptr)
         return fail(MP_E_ARG, "%s is NULL", name);
+    *dev = p;
     if (bytes == 0)
         return MP_OK;
     hipPointerAttribute_t a;
@@ -293,6 +293,23 @@ int check_pinned_buffer(const void* p, size_t bytes, const char* name)
     }
     if (a.type != hipMemoryTypeHost)
         return fail(MP_E_ARG, "%s is not pinned host memory", name);
+    void* base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(reinterpret_cast<hipDeviceptr_t*>(&base), &size,
+                              reinterpret_cast<hipDeviceptr_t>(const_cast<void*>(p))) != hipSuccess ||
+        base == nullptr) {
+        (void)hipGetLastError();
+        return fail(MP_E_ARG, "%s: the size of its pinned allocation is unknown", name);
+    }
+    const size_t used = (size_t)(static_cast<const char*>(p) - static_cast<const char*>(base));
+    if (used > size || size - used < bytes)
+        return fail(MP_E_ARG, "%s holds %zu bytes from the pointer, %zu needed", name,
+                    used > size ? (size_t)0 : size - used, bytes);
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, const_cast<void*>(p), 0) == hipSuccess && d != nullptr)
+        *dev = d;
+    else
+        (void)hipGetLastError();  // unified addressing: the host address is the device address
     return MP_OK;
 }
 
@@ -337,13 +354,14 @@ int check_common(const mp_layout* L, const void* base, const void* const* expert
     for (int i = 0; i < K; ++i) {
         char nm[32];
         std::snprintf(nm, sizeof nm, "experts[%d]", i);
+        const void* dev = experts[i];
         if (residency == MP_DEVICE)
             rc = check_device_buffer(experts[i], c->ckpt_bytes, nm);
         else
-            rc = check_pinned_buffer(experts[i], c->ckpt_bytes, nm);
+            rc = check_pinned_buffer(experts[i], c->ckpt_bytes, nm, &dev);
         if (rc)
             return rc;
-        c->ex.p[i] = experts[i];
+        c->ex.p[i] = dev;
         ranges.push_back({static_cast<const char*>(experts[i]), c->ckpt_bytes, "expert"});
     }
     if (out != nullptr) {
@@ -391,16 +409,8 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
             return hip_fail(e, "counter reset");
     }
     mp_io_stats st{};
-    if (residency == MP_DEVICE) {
-        if ((e = launch_merge(bt, a, base, c.ex, K, mask, out, ctr, s)) != hipSuccess)
-            return hip_fail(e, "merge launch");
-    } else {
-        if (!c.ws->pipe)
-            c.ws->pipe = std::make_unique<Pipeline>();
-        rc = c.ws->pipe->merge(bt, a, base, c.ex, K, mask, out, ctr, s, &st, &g_err);
-        if (rc)
-            return rc;
-    }
+    if ((e = launch_merge(bt, a, base, c.ex, K, mask, out, ctr, s)) != hipSuccess)
+        return hip_fail(e, "merge launch");
     if (io) {
         if ((e = hipMemcpyAsync(c.ws->h_counters, ctr, sizeof(unsigned long long) * 256,
                                 hipMemcpyDeviceToHost, s)) != hipSuccess)
@@ -411,6 +421,8 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
         for (int q = 0; q < 256; ++q)
             sum += c.ws->h_counters[q];
         st.expert_bytes = sum;
+        if (residency == MP_HOST_PINNED)
+            st.h2d_bytes = sum;  // expert blocks are read over PCIe, nothing else crosses it
         st.base_bytes = (uint64_t)bt.P * (uint64_t)bt.esize;
         st.out_bytes = st.base_bytes;
         *io = st;
@@ -451,15 +463,10 @@ int mp_index_blocks(const mp_layout* layout, const void* base, const void* const
     if ((rc = check_device_buffer(sumsq, sizeof(float) * (size_t)(bt.G * K), "sumsq")))
         return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (residency == MP_DEVICE) {
-        hipError_t e = launch_index(bt, base, c.ex, K, sumsq, s);
-        if (e != hipSuccess)
-            return hip_fail(e, "index launch");
-        return MP_OK;
-    }
-    if (!c.ws->pipe)
-        c.ws->pipe = std::make_unique<Pipeline>();
-    return c.ws->pipe->index(bt, base, c.ex, K, sumsq, s, &g_err);
+    hipError_t e = launch_index(bt, base, c.ex, K, sumsq, s);
+    if (e != hipSuccess)
+        return hip_fail(e, "index launch");
+    return MP_OK;
 }
 
 int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float* w,

@@ -75,28 +75,6 @@ __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, Ex
     }
 }
 
-template <int DT>
-__global__ __launch_bounds__(256) void k_index_staged(const void* __restrict__ base, ExpertPtrs sx,
-                                                      int K, const uint32_t* __restrict__ gid,
-                                                      const uint64_t* __restrict__ soff,
-                                                      const uint64_t* __restrict__ boff,
-                                                      const uint32_t* __restrict__ blen,
-                                                      float* __restrict__ sumsq)
-{
-    const int64_t b = blockIdx.x;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const uint32_t g = gid[b];
-    const uint32_t nch = blen[g] / Fmt<DT>::V;
-    const uint4* pb = chunk_ptr(base, boff[g], Fmt<DT>::esize);
-    for (int i = wave; i < K; i += 4) {
-        const uint4* pe = chunk_ptr(sx.p[i], soff[b], Fmt<DT>::esize);
-        const float s = block_sumsq<DT>(pb, pe, nch, lane);
-        if (lane == 0)
-            sumsq[(int64_t)g * K + i] = s;
-    }
-}
-
 }  // namespace
 
 hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
@@ -109,22 +87,6 @@ hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs
         hipLaunchKernelGGL(k_index<0>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, sumsq);
     else
         hipLaunchKernelGGL(k_index<1>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, sumsq);
-    return hipGetLastError();
-}
-
-hipError_t launch_index_staged(const BlockTable& bt, const void* base, const ExpertPtrs& stage_ex,
-                               int K, const uint32_t* gid, const uint64_t* soff, int64_t nb,
-                               float* sumsq, hipStream_t s)
-{
-    if (nb == 0)
-        return hipSuccess;
-    const dim3 grid((unsigned)nb), block(256);
-    if (bt.dtype == 0)
-        hipLaunchKernelGGL(k_index_staged<0>, grid, block, 0, s, base, stage_ex, K, gid, soff,
-                           bt.d_off, bt.d_len, sumsq);
-    else
-        hipLaunchKernelGGL(k_index_staged<1>, grid, block, 0, s, base, stage_ex, K, gid, soff,
-                           bt.d_off, bt.d_len, sumsq);
     return hipGetLastError();
 }
 

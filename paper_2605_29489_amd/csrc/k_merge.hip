@@ -11,10 +11,8 @@
 //  * TIES: the block's deltas stay in registers while the per-expert trim
 //    thresholds are selected in LDS (see the TIES section).
 //
-// Addressing: device-resident experts (expert i's block at its layout
-// offset) or staged experts (the selected blocks packed back to back in a
-// device buffer, in increasing expert order, as the host pipeline copies
-// them).
+// Addressing: expert i's block sits at its layout offset in expert i's
+// buffer, which is device memory or pinned host memory read over PCIe.
 #include "device_common.h"
 #include "mp_internal.h"
 
@@ -32,17 +30,6 @@ struct DevSrc {
     __device__ const uint4* expert(int i, int r, int64_t b, uint64_t off, uint32_t n, int es) const
     {
         return chunk_ptr(ex.p[i], off, es);
-    }
-};
-
-struct StagedSrc {
-    const char* stage;
-    const uint32_t* gid;
-    const uint64_t* soff;  // byte offset of the block's first selected expert
-    __device__ uint32_t block(int64_t b) const { return gid[b]; }
-    __device__ const uint4* expert(int i, int r, int64_t b, uint64_t off, uint32_t n, int es) const
-    {
-        return reinterpret_cast<const uint4*>(stage + soff[b] + (uint64_t)r * n * (uint64_t)es);
     }
 };
 
@@ -906,17 +893,6 @@ hipError_t launch_merge(const BlockTable& bt, const MergeArgs& a, const void* ba
     if (bt.dtype == 0)
         return launch_typed<0>(bt, a, src, base, K, mask, bt.G, out, counters, s);
     return launch_typed<1>(bt, a, src, base, K, mask, bt.G, out, counters, s);
-}
-
-hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const void* base,
-                               const void* stage, int K, const uint32_t* mask,
-                               const uint32_t* gid, const uint64_t* soff, int64_t nb, void* out,
-                               unsigned long long* counters, hipStream_t s)
-{
-    StagedSrc src{static_cast<const char*>(stage), gid, soff};
-    if (bt.dtype == 0)
-        return launch_typed<0>(bt, a, src, base, K, mask, nb, out, counters, s);
-    return launch_typed<1>(bt, a, src, base, K, mask, nb, out, counters, s);
 }
 
 }  // namespace mp

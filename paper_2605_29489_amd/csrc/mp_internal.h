@@ -63,17 +63,12 @@ struct PlanScratch {
 // ---------------------------------------------------------------- launchers
 // All launchers enqueue on `s` and return the launch status.
 
+// Expert pointers are device addresses: device memory or the device view of
+// pinned host memory (the kernels then read over PCIe).
 hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
                         float* sumsq, hipStream_t s);
 
-// Index over an explicit list of blocks whose data sits in compact staging
-// buffers (host-streamed experts): block b of the list is block gid[b] of
-// the layout and its expert i data starts at stage_ex[i] + soff[b] elements;
-// the base block is read from base at its layout offset.
-hipError_t launch_index_staged(const BlockTable& bt, const void* base, const ExpertPtrs& stage_ex,
-                               int K, const uint32_t* gid, const uint64_t* soff, int64_t nb,
-                               float* sumsq, hipStream_t s);
-
+// Algorithm 1 on the device (k_plan.hip).
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
                        const Coeffs& w, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
                        hipStream_t s);
@@ -94,14 +89,5 @@ struct MergeArgs {
 hipError_t launch_merge(const BlockTable& bt, const MergeArgs& a, const void* base,
                         const ExpertPtrs& ex, int K, const uint32_t* mask, void* out,
                         unsigned long long* counters, hipStream_t s);
-
-// Merge over a subset of blocks whose selected expert data is packed in a
-// device staging buffer (host-streamed experts).  For list entry b (layout
-// block gid[b]) the selected experts' blocks lie back to back, in
-// increasing expert order, starting at byte soff[b] of `stage`.
-hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const void* base,
-                               const void* stage, int K, const uint32_t* mask,
-                               const uint32_t* gid, const uint64_t* soff, int64_t nb, void* out,
-                               unsigned long long* counters, hipStream_t s);
 
 }  // namespace mp

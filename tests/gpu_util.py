@@ -12,6 +12,17 @@ def to_dev(a, dtype, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(device)
 
 
+def to_pinned(a, dtype):
+    """A new pinned host tensor holding the array (allocated pinned, never
+    registered after the fact)."""
+    import torch
+    if dtype == "bf16":
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(a, np.float32))
+    return t.pin_memory()
+
+
 def to_host(t):
     import torch
     if t.dtype == torch.bfloat16:

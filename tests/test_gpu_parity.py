@@ -16,7 +16,7 @@ import numpy as np
 import pytest
 
 import oracle
-from tests.gpu_util import assert_merge_equal, gather_blocks, to_dev, to_host
+from tests.gpu_util import assert_merge_equal, gather_blocks, to_dev, to_host, to_pinned
 from workloads import FamilySpec, family_spec, make_family
 
 pytestmark = pytest.mark.gpu
@@ -64,18 +64,23 @@ def _lay(mp, spec):
     return mp.Layout(lay.numel, lay.block_elems, lay.dtype_code), lay
 
 
-def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, **kw):
-    """Index, plan and merge on the GPU and with the oracle; compare."""
+def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **kw):
+    """Index, plan and merge on the GPU and with the oracle; compare.  With
+    residency MP_HOST_PINNED the experts stay in pinned host memory."""
     import torch
     L, lay = _lay(mp, spec)
     K = len(exps_np)
     dtype = lay.dtype
     blocks = oracle.Blocks(lay.numel, lay.block_elems)
     G = blocks.G
+    res = mp.MP_DEVICE if residency is None else residency
     base = to_dev(base_np, dtype)
-    exps = [to_dev(e, dtype) for e in exps_np]
+    if res == mp.MP_HOST_PINNED:
+        exps = [to_pinned(e, dtype) for e in exps_np]
+    else:
+        exps = [to_dev(e, dtype) for e in exps_np]
     sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
-    mp.mp_index_blocks(L, base, exps, sumsq)
+    mp.mp_index_blocks(L, base, exps, sumsq, residency=res)
     S_gpu = sumsq.cpu().numpy()
     S_orc = oracle.index(blocks, dtype, base_np, exps_np).reshape(-1)
     assert np.array_equal(S_gpu.view(np.uint32), S_orc.view(np.uint32)), "index differs"
@@ -97,21 +102,25 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, **kw):
         assert st["digest"] == st_orc["digest"]
         assert st["n_units"] == G * K and st["budget_bytes"] == B
         if op == "avg":
-            io = mp.mp_merge_avg(L, base, exps, mask, kw["alpha"], out, io=True)
+            io = mp.mp_merge_avg(L, base, exps, mask, kw["alpha"], out, residency=res, io=True)
             want = oracle.merge_avg(blocks, dtype, base_np, exps_np, m_orc, kw["alpha"])
         elif op == "ties":
-            io = mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out, io=True)
+            io = mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out, residency=res, io=True)
             want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"])
         else:
             comb = 0 if op == "dare_lin" else 1
             io = mp.mp_merge_dare(L, base, exps, mask, kw["p"], kw["seed"], comb, kw.get("alpha"), kw["lam"],
-                                  out, io=True)
+                                  out, residency=res, io=True)
             want = oracle.merge_dare(blocks, dtype, base_np, exps_np, m_orc, kw["p"], kw["seed"], comb,
                                      kw.get("alpha", [1.0] * K), kw["lam"])
         got = to_host(out)
         nb = assert_merge_equal(got, want, base_np, dtype, f"{op} B={B}")
         assert nb == 0, f"{op} B={B}: {nb} values within tolerance but not bitwise equal"
         assert io["expert_bytes"] == st["cost_bytes"], "kernels loaded bytes outside the plan"
+        if res == mp.MP_HOST_PINNED:  # only the selected blocks cross PCIe (Prop. 1)
+            assert io["h2d_bytes"] == st["cost_bytes"]
+        else:
+            assert io["h2d_bytes"] == 0
         results.append((B, st, nb))
         _say(f"  {spec.name} {op} B={B}: cost={st['cost_bytes']} sel={st['n_selected']} non-bitwise={nb}")
     return results
@@ -135,6 +144,52 @@ def test_ragged_fp32_all_ops(mp, op):
     kw = dict(alpha=[0.5, 0.25, 0.25], density=0.1, lam=0.8, p=0.5, seed=3)
     _say(f"case ragged fp32 {op}")
     _run_all(mp, spec, base, exps, op, [0, 0.3, 0.6, 1.0], **kw)
+
+
+@pytest.mark.parametrize("op", ["avg", "ties", "dare_lin", "dare_sign"])
+def test_host_pinned_experts_all_ops(mp, op):
+    # experts in pinned host memory: the kernels read the selected blocks
+    # over PCIe; results are the same bits as with device-resident experts
+    spec = _mini_qwen()
+    base, exps = make_family(spec, seed=1)
+    kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0, p=0.9, seed=7)
+    _say(f"case mini-qwen bf16 {op}, pinned host experts")
+    _run_all(mp, spec, base, exps, op, [0, 0.3, 1.0], residency=mp.MP_HOST_PINNED, **kw)
+
+
+def test_host_pinned_ragged_fp32_multi_group(mp):
+    spec = _ragged_f32(K=6)
+    base, exps = make_family(spec, K=6, seed=21)
+    _say("case ragged fp32 K=6, pinned host experts")
+    _run_all(mp, spec, base, exps, "ties", [0.5, 1.0], residency=mp.MP_HOST_PINNED, density=0.1, lam=0.8)
+    _run_all(mp, spec, base, exps, "avg", [0.5], residency=mp.MP_HOST_PINNED, alpha=[1.0 / 6] * 6)
+
+
+def test_host_pinned_rejects_device_and_pageable_experts(mp):
+    import torch
+    spec = _mini_qwen(n_layers=1)
+    L, lay = _lay(mp, spec)
+    base, exps = make_family(spec, seed=3)
+    b = to_dev(base, "bf16")
+    G = oracle.Blocks(lay.numel, lay.block_elems).G
+    sumsq = torch.empty(G * 4, dtype=torch.float32, device="cuda")
+    dev = [to_dev(e, "bf16") for e in exps]
+    pageable = [torch.from_numpy(e.view(np.int16)).view(torch.bfloat16) for e in exps]
+    for bad in (dev, pageable):
+        with pytest.raises(mp.MPError) as err:
+            mp.mp_index_blocks(L, b, bad, sumsq, residency=mp.MP_HOST_PINNED)
+        assert err.value.code == mp.MP_E_ARG
+    # exact-size pinned allocations one byte short of a checkpoint (torch's
+    # pinned cache may hand out a larger block, which hides an undersized one)
+    short = [_RawPinnedBuffer(e.nbytes - 1) for e in exps]
+    try:
+        with pytest.raises(mp.MPError) as err:
+            mp.mp_index_blocks(L, b, short, sumsq, residency=mp.MP_HOST_PINNED)
+        assert err.value.code == mp.MP_E_ARG
+    finally:
+        torch.cuda.synchronize()
+        for x in short:
+            x.free()
 
 
 def test_toy_config_avg_full_parity(mp):
@@ -319,6 +374,23 @@ class _RawDeviceBuffer:
 
     def free(self):
         self._hip.hipFree(self._p)
+
+
+class _RawPinnedBuffer:
+    """An exact-size hipHostMalloc allocation."""
+
+    def __init__(self, nbytes):
+        import ctypes
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._p = ctypes.c_void_p()
+        assert self._hip.hipHostMalloc(ctypes.byref(self._p), ctypes.c_size_t(nbytes), ctypes.c_uint(0)) == 0
+        self.nbytes = nbytes
+
+    def data_ptr(self):
+        return self._p.value
+
+    def free(self):
+        self._hip.hipHostFree(self._p)
 
 
 def test_invalid_device_arguments_rejected(mp):
