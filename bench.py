@@ -29,6 +29,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+from workloads import CONFIGS  # noqa: E402  (shape tables only; no GPU work at import)
+
 METRIC = "merged params/sec + effective HBM GB/s, budgeted TIES merge at B=25/50/100%"
 HBM_PEAK = 8.0e12  # MI355X published HBM3E bandwidth, bytes/s
 BUDGETS = (0.25, 0.5, 1.0)
@@ -104,6 +106,107 @@ def cpu_baseline(spec, base, exps, blocks_stride=8):
     }
 
 
+PCIE_PEAK = 64.0e9  # PCIe Gen5 x16, one direction, nominal bytes/s
+
+
+def run_sweep(args):
+    """One of the other workload shapes: index once, then plan + merge at each
+    budget of its sweep.  Experts are device-resident or stay in pinned host
+    memory (kernels read the selected blocks over PCIe)."""
+    import numpy as np
+    import torch
+
+    import paper_2605_29489_amd as mp
+    from workloads import family_spec, make_family_device
+
+    cfg = CONFIGS[args.workload]
+    torch.cuda.set_device(0)
+    spec = family_spec(cfg["family"], n_layers=args.layers)
+    lay = spec.layout
+    K = spec.K
+    P = lay.n_params
+    pinned = cfg["residency"] == "host_pinned"
+    res = mp.MP_HOST_PINNED if pinned else mp.MP_DEVICE
+    dt = mp.MP_F32 if lay.dtype == "f32" else mp.MP_BF16
+    L = mp.Layout(lay.numel, lay.block_elems, dt)
+    G = mp.mp_layout_blocks(L)
+    log(f"generating {spec.description}: P={P} G={G} experts {'pinned host' if pinned else 'device'}")
+    base, exps = make_family_device(spec, K=K, seed=0, device="cuda", experts_on_host_pinned=pinned)
+    torch.cuda.synchronize()
+    sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
+    mask = torch.empty(G, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(base)
+    es = lay.elem_bytes
+    full = P * es * K
+    op = cfg["op"]
+    w = [1.0 / K] * K if op == "avg" else [1.0] * K
+    stream = torch.cuda.current_stream()
+
+    def merge(io=False):
+        if op == "avg":
+            return mp.mp_merge_avg(L, base, exps, mask, [1.0 / K] * K, out, residency=res, io=io, stream=stream)
+        if op == "ties":
+            return mp.mp_merge_ties(L, base, exps, mask, cfg["density"], cfg["lam"], out, residency=res, io=io,
+                                    stream=stream)
+        comb = mp.MP_COMBINE_SIGN_ELECT if cfg["combine"] == "sign_elect" else mp.MP_COMBINE_LINEAR
+        return mp.mp_merge_dare(L, base, exps, mask, cfg["p"], cfg["seed"], comb, None, cfg["lam"], out,
+                                residency=res, io=io, stream=stream)
+
+    def timed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        r = fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b), r
+
+    reps = max(1, args.steps)
+    for _ in range(max(0, args.warmup)):
+        mp.mp_index_blocks(L, base, exps, sumsq, residency=res, stream=stream)
+    idx_ms = float(np.median([timed(lambda: mp.mp_index_blocks(L, base, exps, sumsq, residency=res,
+                                                                stream=stream))[0] for _ in range(reps)]))
+    rows = []
+    for f in cfg["budgets"]:
+        B = int(f * full)
+        plan_ms, st = timed(lambda: mp.mp_plan(L, K, sumsq, w, B, mask, stream=stream))
+        io = merge(io=True)
+        assert io["expert_bytes"] == st["cost_bytes"]
+        for _ in range(max(0, args.warmup)):
+            merge()
+        ms = float(np.median([timed(merge)[0] for _ in range(reps)]))
+        alg = 2 * P * es + st["cost_bytes"] + 4 * G if not pinned else st["cost_bytes"]
+        rows.append({"budget_frac": round(f, 4), "budget_bytes": B, "cost_bytes": st["cost_bytes"],
+                     "h2d_bytes": io["h2d_bytes"], "n_selected": st["n_selected"], "plan_ms": round(plan_ms, 4),
+                     "merge_ms": round(ms, 4), "merge_params_per_s": P / (ms * 1e-3),
+                     ("h2d_GBps" if pinned else "merge_effective_GBps"): alg / (ms * 1e-3) / 1e9})
+    step_ms = idx_ms + sum(r["plan_ms"] + r["merge_ms"] for r in rows)
+    dma = None
+    if pinned:  # measured peak: one pinned expert -> device with the copy engine
+        dst = torch.empty_like(base)
+        dst.copy_(exps[0], non_blocking=True)
+        dma_ms, _ = timed(lambda: dst.copy_(exps[0], non_blocking=True))
+        dma = P * es / (dma_ms * 1e-3)
+        del dst
+    tot_bytes = sum(r["cost_bytes"] if pinned else 2 * P * es + r["cost_bytes"] + 4 * G for r in rows)
+    tot_ms = sum(r["merge_ms"] for r in rows)
+    achieved = tot_bytes / (tot_ms * 1e-3)
+    peak = PCIE_PEAK if pinned else HBM_PEAK
+    result = {
+        "metric": f"merged params/sec, budgeted {op.upper()} merge sweep",
+        "value": len(rows) * P / (step_ms * 1e-3), "unit": "params/s", "n_gpus": 1, "steps": reps,
+        "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{spec.description}; {op} {cfg}", "storage_dtype": lay.dtype, "params": P,
+                   "blocks": G, "K": K, "experts": "pinned host" if pinned else "device",
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "pcie" if pinned else "hbm", "achieved": achieved / 1e9, "peak": peak / 1e9,
+                     "unit": "GB/s", "frac": achieved / peak, "traffic": None,
+                     "measured_dma_h2d_GBps": None if dma is None else dma / 1e9},
+        "breakdown": {"index_ms": round(idx_ms, 4), "per_budget": rows},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -111,6 +214,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-stride", type=int, default=2)
+    ap.add_argument("--workload", default="qwen2.5-1.5b", choices=sorted(CONFIGS),
+                    help="the headline (default) or one of the other workload shapes")
+    ap.add_argument("--layers", type=int, default=None,
+                    help="other workloads: keep only this many transformer layers (host memory)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="after the timed region, run the AVG merge once with an empty mask: a plain copy "
                          "of the base (reads 2P + 4G bytes, writes 2P) for scaling hardware byte counters")
@@ -118,6 +225,9 @@ def main():
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build measures one GPU only; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload != "qwen2.5-1.5b":
+        return run_sweep(args)
 
     import numpy as np
     import torch

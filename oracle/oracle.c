@@ -80,8 +80,8 @@ int orc_num_threads(void)
 /* Reading: each tensor is flattened row-major and cut into            */
 /* consecutive blocks of block_elems elements; the last block of a     */
 /* tensor may be shorter; blocks never cross tensors; blocks are       */
-/* numbered in tensor order.  (Prop. 2 assumes such a disjoint          */
-/* partition of the parameter vector.)                                 */
+/* numbered in tensor order.  (Prop. 2 relies on the blocks covering    */
+/* every parameter exactly once.)                                      */
 /* ------------------------------------------------------------------ */
 
 int64_t orc_num_blocks(int32_t n_tensors, const int64_t* numel, int64_t block_elems)
@@ -297,8 +297,8 @@ int orc_merge_avg(int64_t nb, const int64_t* doff, const int64_t* len, int32_t d
 }
 
 /* ------------------------------------------------------------------ */
-/* Sign election and disjoint mean (TIES: "elects signs, and averages   */
-/* sign-consistent entries"), shared by TIES and DARE's sign-elect      */
+/* Sign election and disjoint mean (the second and third TIES steps of */
+/* Appendix A.1), shared by TIES and DARE's sign-elect                  */
 /* combine.  t[r*n + j] holds the (trimmed or dropped) delta of the    */
 /* r-th selected expert, experts in increasing index order.            */
 /*   P_j = sum of the positive t_rj, N_j = sum of the negative t_rj     */
@@ -334,8 +334,8 @@ static float sign_elect_mean(const float* t, int nsel, int64_t n, int64_t j)
 }
 
 /* ------------------------------------------------------------------ */
-/* TIES (Appendix A.1: "trims, elects signs, and averages               */
-/* sign-consistent entries after masking").                            */
+/* TIES (Appendix A.1: magnitude trim, sign election and the mean of    */
+/* the entries agreeing with the elected sign, on the masked deltas).  */
 /* Reading: trim is per (selected expert, block) -- Eq. 1 and Eq. 4     */
 /* make the operator a function of that block's deltas only.  Keep     */
 /* density rho: k = min(n, ceil(rho * n)) computed in fp64; tau = the   */
@@ -457,8 +457,8 @@ void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t ou
 }
 
 /* ------------------------------------------------------------------ */
-/* DARE (Appendix A.1: "applies the same idea before random            */
-/* drop/rescale, using a fixed seed or mask omega").                   */
+/* DARE (Appendix A.1: TIES-like combination after a random drop and   */
+/* rescale whose randomness is fixed by a seed or a given mask omega). */
 /* Reading: the drop decision for expert i, tensor t, element e of     */
 /* that tensor comes from Philox4x32-10 with key (seed, i) and counter  */
 /* (low32(e/4), high32(e/4), t, 0); output word e mod 4 is u; the       */

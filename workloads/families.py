@@ -2,8 +2,8 @@
 
 A checkpoint is one flat buffer holding its tensors back to back, each tensor
 flattened row-major, in the order listed by the shape table.  The paper's
-checkpoints are homologous families fine-tuned from a shared base (Section 1,
-Section 2); the recipe below imitates that structure:
+checkpoints are experts obtained by fine-tuning one common base model
+(Sections 1 and 2); the recipe below imitates that structure:
 
 * base weights ~ N(0, 0.02^2); normalisation weights 1 + N(0, 0.02^2);
   generated in fp32, then rounded to the family dtype;
@@ -250,6 +250,33 @@ def make_family(spec: FamilySpec, K: Optional[int] = None, seed: int = 0):
     return base.view(torch.int16).numpy().view(np.uint16), [e.view(torch.int16).numpy().view(np.uint16) for e in experts]
 
 
+def pinned_empty(n: int, dtype_name: str):
+    """A CPU tensor of n elements whose storage is an exact-size hipHostMalloc
+    allocation (pinned host memory), freed when the tensor is collected.
+
+    torch's own pinned allocator rounds every request up to a power of two,
+    which doubles the footprint of 16 GB experts."""
+    import ctypes
+    import weakref
+
+    import torch
+
+    hip = ctypes.CDLL("libamdhip64.so")
+    es = DTYPE_BYTES[dtype_name]
+    ptr = ctypes.c_void_p()
+    rc = hip.hipHostMalloc(ctypes.byref(ptr), ctypes.c_size_t(max(n * es, 1)), ctypes.c_uint(0))
+    if rc != 0 or not ptr.value:
+        raise MemoryError(f"hipHostMalloc of {n * es} bytes failed (error {rc})")
+    raw = (ctypes.c_uint8 * (n * es)).from_address(ptr.value)
+    arr = np.frombuffer(raw, dtype=np.int16 if es == 2 else np.float32, count=n)
+    t = torch.from_numpy(arr)
+    if dtype_name == "bf16":
+        t = t.view(torch.bfloat16)
+    weakref.finalize(arr, hip.hipHostFree, ptr)
+    t._pinned_owner = arr  # keeps the allocation alive as long as the tensor
+    return t
+
+
 def make_family_device(spec: FamilySpec, K: Optional[int] = None, seed: int = 0, device="cuda",
                        experts_on_host_pinned: bool = False):
     """Generate base + K experts as torch tensors on ``device``.
@@ -277,7 +304,7 @@ def make_family_device(spec: FamilySpec, K: Optional[int] = None, seed: int = 0,
     _fill(torch, spec, 0, seed, device, base, [])
     for i in range(K):
         _fill_one_expert(torch, spec, i, seed, device, base, scratch)
-        h = torch.empty(P, dtype=tdt, pin_memory=True)
+        h = pinned_empty(P, lay.dtype)
         h.copy_(scratch)
         experts.append(h)
     del scratch
