@@ -170,6 +170,29 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
             }
             rank += cnt;
         }
+        if (MODE == M_DARE_SIGN) {
+            // elect the sign of the larger signed mass; mean of the agreeing
+            // entries (a count that is a power of two divides by exact scaling,
+            // correctly rounded as the quotient; otherwise IEEE division)
+            bool odd = false;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const bool up = ps[e] > -ns[e];
+                const bool dn = ps[e] < -ns[e];
+                acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);
+                pc[e] = up ? pc[e] : (dn ? nc[e] : 1u);
+                odd |= (pc[e] & (pc[e] - 1u)) != 0u;
+            }
+            if (__any(odd)) {
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    acc[e] = acc[e] / (float)pc[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(pc[e])) << 23);
+            }
+        }
 #pragma unroll
         for (int q = 0; q < CPT; ++q) {
             if (!ok[q])
@@ -178,18 +201,10 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int e = q * V + v;
-                if (MODE == M_AVG) {
+                if (MODE == M_AVG)
                     y[v] = x0[e] + acc[e];
-                } else if (MODE == M_DARE_LIN) {
+                else
                     y[v] = fmaf(lambda, acc[e], x0[e]);
-                } else {
-                    float mean = 0.0f;  // elect the sign of the larger signed mass
-                    if (ps[e] > -ns[e])
-                        mean = ps[e] / (float)pc[e];
-                    else if (ps[e] < -ns[e])
-                        mean = ns[e] / (float)nc[e];
-                    y[v] = fmaf(lambda, mean, x0[e]);
-                }
             }
             po[tile + q * kT + t] = Fmt<DT>::pack(y);
         }
@@ -233,7 +248,11 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
 #define MP_TIES_ASM 1
 #endif
 namespace ties {
-constexpr int NT = 256;         // threads per workgroup
+#ifndef MP_TIES_NT
+#define MP_TIES_NT 256
+#endif
+constexpr int NT = MP_TIES_NT;  // threads per workgroup
+constexpr int EPT = kTiesMaxBlock / NT;  // elements per thread and expert
 constexpr int NW = NT / 64;     // waves per workgroup
 constexpr int GS = 4;           // experts trimmed together (one scanning wave each)
 constexpr int MB = MP_TIES_MB;  // mantissa bits in a window key
@@ -637,7 +656,7 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
 // Keep test and the running signed masses of element e over NS slots; the
 // kept counts go to cnt (positive in the low, negative in the high half).
 template <int NS>
-__device__ inline void ties_accumulate(const float (&d)[ties::GS][16], const uint32_t (&tau)[ties::GS], int e,
+__device__ inline void ties_accumulate(const float (&d)[ties::GS][ties::EPT], const uint32_t (&tau)[ties::GS], int e,
                                        float& P, float& N, uint32_t& cnt)
 {
 #pragma unroll
@@ -667,8 +686,8 @@ __device__ inline float div3(float x)
 // Sign election (the sign of the larger of the positive and negative kept
 // masses) and the mean of the agreeing entries, for the V elements of one
 // chunk; then y = lambda * mean + x0, rounded once, is stored.  SMALLK: at
-// most 4 entries agree, so the count is 1, 2, 3 or 4.
-template <int DT, bool SMALLK>
+// most 4 entries agree, so the count is 1, 2, 3 or 4 (at most MAXDEN).
+template <int DT, bool SMALLK, int MAXDEN = 32>
 __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const float (&N)[Fmt<DT>::V],
                                         const uint32_t (&cnt)[Fmt<DT>::V], const float* x0, float lambda,
                                         uint4* __restrict__ dst, bool ok)
@@ -685,7 +704,11 @@ __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const floa
         den[v] = up ? (cnt[v] & 0xffffu) : (dn ? (cnt[v] >> 16) : 1u);
         odd |= (den[v] & (den[v] - 1u)) != 0u;
     }
-    if (SMALLK) {
+    if (SMALLK && MAXDEN <= 2) {
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+            num[v] = (den[v] == 2u) ? num[v] * 0.5f : num[v];  // exact halving
+    } else if (SMALLK) {
 #pragma unroll
         for (int v = 0; v < V; ++v) {
             // division by 2^s is exact scaling (correctly rounded, as the quotient)
@@ -713,13 +736,32 @@ __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const floa
 // All selected experts trimmed in one group: accumulate and store chunk by
 // chunk.
 template <int DT, int NS>
-__device__ inline void ties_finish_single(const float (&d)[ties::GS][16], const uint32_t (&tau)[ties::GS],
-                                          const float (&x0)[16], float lambda, uint4* __restrict__ po, uint32_t nch)
+__device__ inline void ties_finish_single(const float (&d)[ties::GS][ties::EPT], const uint32_t (&tau)[ties::GS],
+                                          const float (&x0)[ties::EPT], float lambda, uint4* __restrict__ po,
+                                          uint32_t nch)
 {
-    constexpr int V = Fmt<DT>::V, CPT = 16 / V;
+    constexpr int V = Fmt<DT>::V, CPT = ties::EPT / V;
     const int t = threadIdx.x;
 #pragma unroll
     for (int q = 0; q < CPT; ++q) {
+        if (NS <= 1) {
+            // one expert (or none): the elected sign is the kept delta's own, and
+            // the mean of one entry is the entry
+            if (q * ties::NT + t < (int)nch) {
+                float y[V];
+#pragma unroll
+                for (int v = 0; v < V; ++v) {
+                    float mean = 0.0f;
+                    if (NS == 1) {
+                        const float dj = d[0][q * V + v];
+                        mean = (fabsf(dj) >= __uint_as_float(tau[0])) ? dj : 0.0f;
+                    }
+                    y[v] = fmaf(lambda, mean, x0[q * V + v]);
+                }
+                po[q * ties::NT + t] = Fmt<DT>::pack(y);
+            }
+            continue;
+        }
         float P[V], N[V];
         uint32_t cnt[V];
 #pragma unroll
@@ -727,22 +769,21 @@ __device__ inline void ties_finish_single(const float (&d)[ties::GS][16], const 
             P[v] = 0.0f;
             N[v] = 0.0f;
             cnt[v] = 0u;
-            if (NS > 0)
-                ties_accumulate<NS>(d, tau, q * V + v, P[v], N[v], cnt[v]);
+            ties_accumulate<NS>(d, tau, q * V + v, P[v], N[v], cnt[v]);
         }
-        ties_store_chunk<DT, true>(P, N, cnt, &x0[q * V], lambda, po + q * ties::NT + t,
-                                   q * ties::NT + t < (int)nch);
+        ties_store_chunk<DT, true, NS>(P, N, cnt, &x0[q * V], lambda, po + q * ties::NT + t,
+                                       q * ties::NT + t < (int)nch);
     }
 }
 
 // Several groups: the signed masses and the counts are carried across
 // groups.
 template <int NS>
-__device__ inline void ties_accumulate_all(const float (&d)[ties::GS][16], const uint32_t (&tau)[ties::GS],
-                                           float (&P)[16], float (&N)[16], uint32_t (&cnt)[16])
+__device__ inline void ties_accumulate_all(const float (&d)[ties::GS][ties::EPT], const uint32_t (&tau)[ties::GS],
+                                           float (&P)[ties::EPT], float (&N)[ties::EPT], uint32_t (&cnt)[ties::EPT])
 {
 #pragma unroll
-    for (int e = 0; e < 16; ++e)
+    for (int e = 0; e < ties::EPT; ++e)
         ties_accumulate<NS>(d, tau, e, P[e], N[e], cnt[e]);
 }
 
@@ -750,7 +791,10 @@ __device__ inline void ties_accumulate_all(const float (&d)[ties::GS][16], const
 // MULTI = true: groups of GS experts in increasing order, with the signed
 // masses and counts carried across groups.
 template <int DT, bool MULTI, class Src>
-__global__ __launch_bounds__(ties::NT, MULTI ? 2 : 4) void k_merge_ties(Src src, const void* __restrict__ base,
+#ifndef MP_TIES_WAVES
+#define MP_TIES_WAVES (ties::NT / 64)
+#endif
+__global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) void k_merge_ties(Src src, const void* __restrict__ base,
                                                          const uint32_t* __restrict__ mask,
                                                          const uint64_t* __restrict__ boff,
                                                          const uint32_t* __restrict__ blen, double density,
@@ -762,7 +806,7 @@ __global__ __launch_bounds__(ties::NT, MULTI ? 2 : 4) void k_merge_ties(Src src,
     constexpr int V = Fmt<DT>::V, ES = Fmt<DT>::esize;
     constexpr int CPT = kTiesMaxBlock / NT / V;  // chunks per thread and expert
     constexpr int E = CPT * V;
-    static_assert(E == 16, "16 elements per thread and expert");
+    static_assert(E == EPT, "elements per thread and expert");
     __shared__ TiesSmem sm;
     const int64_t b = blockIdx.x;
     const uint32_t g = uniform_u32(src.block(b));
