@@ -43,7 +43,10 @@ __device__ inline void count_expert_bytes(unsigned long long* ctr, uint32_t m, u
 enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2 };
 
 template <int DT, int MODE, class Src>
-__global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restrict__ base,
+// DARE's Philox and sign-election state would otherwise take up to 134
+// VGPRs (3 waves per SIMD); at most 128 keeps 4 waves resident, which hides
+// more memory latency.  AVG is light enough either way.
+__global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src src, const void* __restrict__ base,
                                                    const uint32_t* __restrict__ mask,
                                                    const uint64_t* __restrict__ boff,
                                                    const uint32_t* __restrict__ blen,
@@ -87,14 +90,13 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
             Fmt<DT>::unpack(raw, &x0[q * V]);
         }
         float acc[E], ps[E], ns[E];
-        uint32_t pc[E], nc[E];
+        uint32_t cpn[E];  // sign-elect: positive count in the low, negative in the high half
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             acc[e] = 0.0f;
             ps[e] = 0.0f;
             ns[e] = 0.0f;
-            pc[e] = 0u;
-            nc[e] = 0u;
+            cpn[e] = 0u;
         }
         uint32_t mm = m;
         int rank = 0;
@@ -161,8 +163,7 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
                                 const bool pos = tv > 0.0f, neg = tv < 0.0f;
                                 ps[e] = ps[e] + (pos ? tv : 0.0f);
                                 ns[e] = ns[e] + (neg ? tv : 0.0f);
-                                pc[e] += pos ? 1u : 0u;
-                                nc[e] += neg ? 1u : 0u;
+                                cpn[e] += pos ? 1u : (neg ? 0x10000u : 0u);
                             }
                         }
                     }
@@ -179,18 +180,19 @@ __global__ __launch_bounds__(kT) void k_merge_elem(Src src, const void* __restri
             for (int e = 0; e < E; ++e) {
                 const bool up = ps[e] > -ns[e];
                 const bool dn = ps[e] < -ns[e];
-                acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);
-                pc[e] = up ? pc[e] : (dn ? nc[e] : 1u);
-                odd |= (pc[e] & (pc[e] - 1u)) != 0u;
+                acc[e] = dn ? ns[e] : (up ? ps[e] : 0.0f);
+                // with no elected sign acc is 0 and any count >= 1 gives 0
+                cpn[e] = max(__builtin_amdgcn_ubfe(cpn[e], dn ? 16u : 0u, 16u), 1u);
+                odd |= (cpn[e] & (cpn[e] - 1u)) != 0u;
             }
             if (__any(odd)) {
 #pragma unroll
                 for (int e = 0; e < E; ++e)
-                    acc[e] = acc[e] / (float)pc[e];
+                    acc[e] = acc[e] / (float)cpn[e];
             } else {
 #pragma unroll
                 for (int e = 0; e < E; ++e)
-                    acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(pc[e])) << 23);
+                    acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(cpn[e])) << 23);
             }
         }
 #pragma unroll
