@@ -47,6 +47,10 @@ def lib():
         L.orc_mix64.restype = C.c_uint64
         L.orc_mix64.argtypes = [C.c_uint64]
         L.orc_round_bf16.argtypes = [C.c_void_p, C.c_void_p, C.c_int64]
+        L.orc_ties_thresholds.argtypes = [C.c_int64, i64p, i64p, C.c_int32, C.c_void_p, C.POINTER(C.c_void_p),
+                                          C.c_int32, C.c_double, C.c_void_p]
+        L.orc_merge_ties_tau.argtypes = [C.c_int64, i64p, i64p, C.c_int32, C.c_void_p, C.POINTER(C.c_void_p),
+                                         C.c_int32, C.c_void_p, C.c_void_p, C.c_float, C.c_void_p]
         L.orc_ties_k.restype = C.c_int64
         L.orc_ties_k.argtypes = [C.c_int64, C.c_double]
         L.orc_num_threads.restype = C.c_int
@@ -160,6 +164,33 @@ def merge_ties(blocks, dtype, base, experts, mask, density, lam, out=None, ids=N
     _check(L.orc_merge_ties(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
                             len(experts), mask.ctypes.data, float(density), float(lam),
                             out.ctypes.data), "ties")
+    return out
+
+
+def ties_thresholds(blocks, dtype, base, experts, density, ids=None, doff=None):
+    """Per-unit TIES trim thresholds (uint32 fp32 patterns), [len(ids), K]."""
+    L = lib()
+    ids, doff = _merge_args(blocks, ids, doff)
+    tau = np.zeros((len(ids), len(experts)), np.uint32)
+    d_a, d_p = _i64(doff)
+    l_a, l_p = _i64(blocks.len[ids])
+    _check(L.orc_ties_thresholds(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
+                                 len(experts), float(density), tau.ctypes.data), "ties thresholds")
+    return tau
+
+
+def merge_ties_tau(blocks, dtype, base, experts, mask, tau, lam, out=None, ids=None, doff=None):
+    """TIES with given per-unit thresholds tau [len(ids), K]."""
+    L = lib()
+    ids, doff = _merge_args(blocks, ids, doff)
+    out = np.empty_like(base) if out is None else out
+    mask = np.ascontiguousarray(mask, np.uint32)
+    tau = np.ascontiguousarray(tau, np.uint32)
+    d_a, d_p = _i64(doff)
+    l_a, l_p = _i64(blocks.len[ids])
+    _check(L.orc_merge_ties_tau(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
+                                len(experts), mask.ctypes.data, tau.ctypes.data, float(lam),
+                                out.ctypes.data), "ties tau")
     return out
 
 

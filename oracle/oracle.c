@@ -361,6 +361,28 @@ static int desc_float(const void* pa, const void* pb)
     return (a > b) ? -1 : ((a < b) ? 1 : 0);
 }
 
+/* The trim threshold of one (expert, block) unit: m[0..n-1] holds |d|; the
+ * result is the fp32 bit pattern of the k-th largest of them (multiplicity
+ * counted), or the pattern of +infinity when k = 0 (nothing is kept).  m is
+ * sorted in place. */
+static uint32_t kth_largest_pattern(float* m, int64_t n, int64_t k)
+{
+    if (k == 0)
+        return 0x7f800000u;
+    qsort(m, (size_t)n, sizeof(float), desc_float);
+    float tau = m[k - 1];
+    uint32_t u;
+    memcpy(&u, &tau, sizeof u);
+    return u;
+}
+
+static float pattern_float(uint32_t u)
+{
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
 int orc_merge_ties(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
                    const void* base, const void* const* experts, int32_t K,
                    const uint32_t* mask, double density, float lambda, void* out)
@@ -393,17 +415,11 @@ int orc_merge_ties(int64_t nb, const int64_t* doff, const int64_t* len, int32_t 
                 ti[j] = load(experts[i], dtype, o + j) - load(base, dtype, o + j);
                 m[j] = fabsf(ti[j]);
             }
-            if (k == 0) {
-                for (int64_t j = 0; j < n; ++j)
+            float tau = pattern_float(kth_largest_pattern(m, n, k));
+            for (int64_t j = 0; j < n; ++j) {
+                float a = fabsf(ti[j]);
+                if (!(a >= tau && a > 0.0f))
                     ti[j] = 0.0f;
-            } else {
-                qsort(m, (size_t)n, sizeof(float), desc_float);
-                float tau = m[k - 1];
-                for (int64_t j = 0; j < n; ++j) {
-                    float a = fabsf(ti[j]);
-                    if (!(a >= tau && a > 0.0f))
-                        ti[j] = 0.0f;
-                }
             }
             ++r;
         }
@@ -414,6 +430,86 @@ int orc_merge_ties(int64_t nb, const int64_t* doff, const int64_t* len, int32_t 
         }
         free(t);
         free(m);
+    }
+    return bad ? -2 : 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* The TIES trim threshold depends only on the (expert, block) unit and */
+/* the density, never on the access mask (Appendix A.1's trim is read  */
+/* per unit, see above).  It can therefore be computed once per unit   */
+/* and reused by merges at any budget.  tau[b*K + i] = the threshold   */
+/* pattern of unit (block b, expert i) as kth_largest_pattern defines  */
+/* it.                                                                 */
+/* ------------------------------------------------------------------ */
+
+int orc_ties_thresholds(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                        const void* base, const void* const* experts, int32_t K, double density,
+                        uint32_t* tau)
+{
+    if (check_common(dtype, K, nb) || !(density >= 0.0 && density <= 1.0))
+        return -1;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t b = 0; b < nb; ++b) {
+        int64_t n = len[b], o = doff[b];
+        float* m = (float*)malloc(sizeof(float) * (size_t)(n + 1));
+        if (!m) {
+#pragma omp atomic write
+            bad = 1;
+            continue;
+        }
+        int64_t k = orc_ties_k(n, density);
+        for (int32_t i = 0; i < K; ++i) {
+            for (int64_t j = 0; j < n; ++j)
+                m[j] = fabsf(load(experts[i], dtype, o + j) - load(base, dtype, o + j));
+            tau[b * K + i] = kth_largest_pattern(m, n, k);
+        }
+        free(m);
+    }
+    return bad ? -2 : 0;
+}
+
+/* TIES with the thresholds given: d is kept iff |d| >= float(tau) and  */
+/* |d| > 0, then the election and mean of sign_elect_mean.  With the    */
+/* thresholds of orc_ties_thresholds this is orc_merge_ties exactly.    */
+int orc_merge_ties_tau(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                       const void* base, const void* const* experts, int32_t K,
+                       const uint32_t* mask, const uint32_t* tau, float lambda, void* out)
+{
+    if (check_common(dtype, K, nb))
+        return -1;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t b = 0; b < nb; ++b) {
+        int64_t n = len[b], o = doff[b];
+        int nsel = 0;
+        for (int32_t i = 0; i < K; ++i)
+            nsel += (mask[b] >> i) & 1u;
+        float* t = (float*)malloc(sizeof(float) * (size_t)((nsel > 0 ? nsel : 1) * n + 1));
+        if (!t) {
+#pragma omp atomic write
+            bad = 1;
+            continue;
+        }
+        int r = 0;
+        for (int32_t i = 0; i < K; ++i) {
+            if (!((mask[b] >> i) & 1u))
+                continue;
+            float th = pattern_float(tau[b * K + i]);
+            float* ti = t + (int64_t)r * n;
+            for (int64_t j = 0; j < n; ++j) {
+                float d = load(experts[i], dtype, o + j) - load(base, dtype, o + j);
+                float a = fabsf(d);
+                ti[j] = (a >= th && a > 0.0f) ? d : 0.0f;
+            }
+            ++r;
+        }
+        for (int64_t j = 0; j < n; ++j) {
+            float x0 = load(base, dtype, o + j);
+            store(out, dtype, o + j, fmaf(lambda, sign_elect_mean(t, nsel, n, j), x0));
+        }
+        free(t);
     }
     return bad ? -2 : 0;
 }

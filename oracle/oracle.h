@@ -57,6 +57,17 @@ int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
                    const uint32_t* mask, double p, uint32_t seed, int32_t combine,
                    const float* alpha, float lambda, void* out);
 
+/* TIES trim thresholds per unit (mask-independent): tau[b*K + i] = fp32
+ * pattern of the k-th largest |d| of unit (block b, expert i), k =
+ * orc_ties_k(len, density); +infinity's pattern when k = 0. */
+int orc_ties_thresholds(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                        const void* base, const void* const* experts, int32_t K, double density,
+                        uint32_t* tau);
+/* TIES with given thresholds (keep iff |d| >= float(tau) and |d| > 0). */
+int orc_merge_ties_tau(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                       const void* base, const void* const* experts, int32_t K,
+                       const uint32_t* mask, const uint32_t* tau, float lambda, void* out);
+
 /* Building blocks exposed so the tests can pin them. */
 void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
 uint64_t orc_mix64(uint64_t x);

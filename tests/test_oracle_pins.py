@@ -457,6 +457,53 @@ def test_ties_trim_keeps_exactly_top_k():
             assert np.array_equal(out[o:o + n][list(top)], d[o:o + n][list(top)])
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ties_thresholds_are_kth_largest_magnitudes(dtype):
+    # the per-unit threshold is the k-th largest |d| (numpy partition of the
+    # fp32 deltas), +inf when k = 0; ragged and short blocks included
+    rng = np.random.default_rng(41)
+    numel = [4096, 1536, 256, 24, 4096]
+    b = oracle.Blocks(numel, 1024)
+    P = sum(numel)
+    K = 3
+    if dtype == "f32":
+        base = rng.standard_normal(P).astype(np.float32)
+        exps = [(base + rng.standard_normal(P).astype(np.float32) * s).astype(np.float32) for s in (1e-3, 1e-2, 0.0)]
+        f = lambda a: a
+    else:
+        base = _bits_bf16(rng.normal(0, 0.02, P))
+        exps = [_bits_bf16(_f32_of_bf16(base) + rng.normal(0, s, P)) for s in (1e-3, 3e-4, 0.0)]
+        f = _f32_of_bf16
+    for rho in (0.0, 0.2, 0.013, 1.0):
+        tau = oracle.ties_thresholds(b, dtype, base, exps, rho)
+        assert tau.shape == (b.G, K)
+        for g in range(b.G):
+            o, n = b.off[g], b.len[g]
+            k = min(n, math.ceil(rho * n))
+            for i in range(K):
+                m = np.abs((f(exps[i][o:o + n]) - f(base[o:o + n])).astype(np.float32))
+                want = 0x7F800000 if k == 0 else int(np.partition(m, n - k)[n - k].view(np.uint32))
+                assert int(tau[g, i]) == want
+
+
+def test_ties_with_thresholds_equals_ties():
+    # merging with the per-unit thresholds reproduces the TIES merge bit for
+    # bit, for every mask of a tiny family and for random masks of a larger one
+    rng = np.random.default_rng(42)
+    numel = [2048, 512, 40]
+    b = oracle.Blocks(numel, 512)
+    P = sum(numel)
+    base = _bits_bf16(rng.normal(0, 0.02, P))
+    exps = [_bits_bf16(_f32_of_bf16(base) + rng.normal(0, s, P)) for s in (1e-3, 2e-3, 5e-4, 1e-3)]
+    for rho, lam in ((0.2, 1.0), (0.05, 0.7), (1.0, 1.0), (0.0, 1.0)):
+        tau = oracle.ties_thresholds(b, "bf16", base, exps, rho)
+        for trial in range(6):
+            mask = rng.integers(0, 16, b.G).astype(np.uint32)
+            want = oracle.merge_ties(b, "bf16", base, exps, mask, rho, lam)
+            got = oracle.merge_ties_tau(b, "bf16", base, exps, mask, tau, lam)
+            assert np.array_equal(got, want)
+
+
 def test_ties_threshold_ties_all_kept_and_zeros_never():
     b = oracle.Blocks([16], 16)
     d = np.array([3, 3, 3, 3, 2, 2, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0], np.float32)
