@@ -107,6 +107,24 @@ int mp_index_blocks(const mp_layout* layout, const void* base,
                     const void* const* experts, int32_t K, int32_t residency,
                     float* sumsq, void* stream);
 
+/* Catalog statistics for TIES (Section 3 "Catalog"; Appendix A.1's trim):
+ * for every unit, the per-unit trim threshold
+ *   tau[g*K + i] = fp32 bit pattern of the k-th largest |d| of the block
+ *                  (multiplicity counted), k = min(n, ceil(density * n)) in
+ *                  fp64, n = the block length; the pattern of +infinity if
+ *                  k = 0,
+ * and, when sumsq is not NULL, the sum of squares of mp_index_blocks (the
+ * same bits) in the same pass.  The threshold depends on the unit and the
+ * density only, never on an access mask, so one catalog pass serves TIES
+ * merges at every budget (mp_merge_ties_tau).
+ *   tau: device uint32[G*K].  sumsq: device float[G*K] or NULL.
+ * block_elems must be <= 4096 (MP_E_UNSUPPORTED otherwise).
+ * Asynchronous on `stream`; with MP_HOST_PINNED every expert byte crosses
+ * PCIe once. */
+int mp_index_ties(const mp_layout* layout, const void* base,
+                  const void* const* experts, int32_t K, int32_t residency,
+                  double density, float* sumsq, uint32_t* tau, void* stream);
+
 /* Algorithm 1 (PlanGen) over all units, budget-feasible by construction
  * (Prop. 1: C_expert(A) <= B):
  *   score  s_u = float(float(w_i * w_i) * S_u), which ranks units as
@@ -153,6 +171,16 @@ int mp_merge_ties(const mp_layout* layout, const void* base,
                   const void* const* experts, int32_t K, int32_t residency,
                   const uint32_t* mask, double density, float lambda, void* out,
                   mp_io_stats* io, void* stream);
+
+/* Budgeted TIES with catalog thresholds: as mp_merge_ties, with d kept
+ * iff |d| >= float(tau[g*K + i]) and |d| > 0 for the selected unit (g, i).
+ * With the thresholds of mp_index_ties for a density the result equals
+ * mp_merge_ties at that density bit for bit.  tau: device uint32[G*K].
+ * Any block size. */
+int mp_merge_ties_tau(const mp_layout* layout, const void* base,
+                      const void* const* experts, int32_t K, int32_t residency,
+                      const uint32_t* mask, const uint32_t* tau, float lambda,
+                      void* out, mp_io_stats* io, void* stream);
 
 /* Budgeted DARE (Appendix A.1: random drop and rescale with a fixed seed).
  * Element e of tensor t of expert i is dropped iff u < floor(p * 2^32),

@@ -30,8 +30,8 @@ MP_F32, MP_BF16 = 0, 1
 MP_DEVICE, MP_HOST_PINNED = 0, 1
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
 
-EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_plan", "mp_merge_avg", "mp_merge_ties",
-           "mp_merge_dare", "mp_last_error", "mp_release")
+EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+           "mp_merge_ties_tau", "mp_merge_dare", "mp_last_error", "mp_release")
 
 
 class mp_layout(C.Structure):
@@ -69,17 +69,21 @@ def _load():
     lp = C.POINTER(mp_layout)
     L.mp_layout_blocks.argtypes = [lp, C.POINTER(C.c_int64)]
     L.mp_index_blocks.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, vp]
+    L.mp_index_ties.argtypes = [lp, vp, C.POINTER(vp), i32, i32, C.c_double, vp, vp, vp]
     L.mp_plan.argtypes = [lp, i32, vp, C.POINTER(C.c_float), u64, u32, vp, C.POINTER(mp_plan_stats), vp]
     L.mp_merge_avg.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.POINTER(C.c_float), vp,
                                C.POINTER(mp_io_stats), vp]
     L.mp_merge_ties.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, C.c_float, vp,
                                 C.POINTER(mp_io_stats), vp]
+    L.mp_merge_ties_tau.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, vp, C.c_float, vp,
+                                    C.POINTER(mp_io_stats), vp]
     L.mp_merge_dare.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, u32, i32,
                                 C.POINTER(C.c_float), C.c_float, vp, C.POINTER(mp_io_stats), vp]
     L.mp_last_error.restype = C.c_char_p
     L.mp_last_error.argtypes = []
     L.mp_release.argtypes = []
-    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+                 "mp_merge_ties_tau",
                  "mp_merge_dare"):
         getattr(L, name).restype = C.c_int
     return L
@@ -156,6 +160,13 @@ def mp_index_blocks(layout: Layout, base, experts, sumsq, residency: int = MP_DE
                                _ptr(sumsq), _stream(stream)))
 
 
+def mp_index_ties(layout: Layout, base, experts, density: float, tau, sumsq=None, residency: int = MP_DEVICE,
+                  stream=None):
+    """Per-unit TIES thresholds (uint32 patterns in `tau`, G*K) and, if given, sumsq."""
+    _check(lib.mp_index_ties(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, float(density),
+                             _ptr(sumsq), _ptr(tau), _stream(stream)))
+
+
 def mp_plan(layout: Layout, K: int, sumsq, w, budget_bytes: int, mask, flags: int = 0, stream=None) -> dict:
     st = mp_plan_stats()
     _check(lib.mp_plan(layout.ref, K, _ptr(sumsq), _floats(w, K), int(budget_bytes), flags, _ptr(mask),
@@ -180,6 +191,14 @@ def mp_merge_ties(layout: Layout, base, experts, mask, density: float, lam: floa
     st = mp_io_stats() if io else None
     _check(lib.mp_merge_ties(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
                              float(density), float(lam), _ptr(out), _io(st), _stream(stream)))
+    return st.as_dict() if io else None
+
+
+def mp_merge_ties_tau(layout: Layout, base, experts, mask, tau, lam: float, out, residency: int = MP_DEVICE,
+                      io: bool = False, stream=None) -> Optional[dict]:
+    st = mp_io_stats() if io else None
+    _check(lib.mp_merge_ties_tau(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+                                 _ptr(tau), float(lam), _ptr(out), _io(st), _stream(stream)))
     return st.as_dict() if io else None
 
 

@@ -401,6 +401,8 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
         return rc;
     if (a.op == Op::TIES && bt.max_len > (uint32_t)kTiesMaxBlock)
         return fail(MP_E_UNSUPPORTED, "TIES supports blocks of at most %d elements", kTiesMaxBlock);
+    if (a.op == Op::TIES_TAU && (rc = check_device_buffer(a.tau, sizeof(uint32_t) * (size_t)(bt.G * K), "tau")))
+        return rc;
     unsigned long long* ctr = io ? c.ws->counters : nullptr;
     hipError_t e;
     if (ctr) {
@@ -464,6 +466,30 @@ int mp_index_blocks(const mp_layout* layout, const void* base, const void* const
         return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = launch_index(bt, base, c.ex, K, sumsq, s);
+    if (e != hipSuccess)
+        return hip_fail(e, "index launch");
+    return MP_OK;
+}
+
+int mp_index_ties(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                  int32_t residency, double density, float* sumsq, uint32_t* tau, void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    if (!(density >= 0.0 && density <= 1.0))
+        return fail(MP_E_ARG, "density %g must be in [0, 1]", density);
+    Common c;
+    int rc = check_common(layout, base, experts, K, residency, nullptr, &c);
+    if (rc)
+        return rc;
+    const BlockTable& bt = *c.bt;
+    if (bt.max_len > (uint32_t)kTiesMaxBlock)
+        return fail(MP_E_UNSUPPORTED, "TIES supports blocks of at most %d elements", kTiesMaxBlock);
+    if (sumsq != nullptr && (rc = check_device_buffer(sumsq, sizeof(float) * (size_t)(bt.G * K), "sumsq")))
+        return rc;
+    if ((rc = check_device_buffer(tau, sizeof(uint32_t) * (size_t)(bt.G * K), "tau")))
+        return rc;
+    hipError_t e = launch_index_ties(bt, base, c.ex, K, density, sumsq, tau, static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return hip_fail(e, "index launch");
     return MP_OK;
@@ -558,6 +584,19 @@ int mp_merge_ties(const mp_layout* layout, const void* base, const void* const* 
     a.op = Op::TIES;
     a.density = density;
     a.lambda = lambda;
+    return run_merge(layout, base, experts, K, residency, mask, out, io, static_cast<hipStream_t>(stream), a);
+}
+
+int mp_merge_ties_tau(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                      int32_t residency, const uint32_t* mask, const uint32_t* tau, float lambda, void* out,
+                      mp_io_stats* io, void* stream)
+{
+    if (!std::isfinite(lambda))
+        return fail(MP_E_ARG, "lambda is not finite");
+    MergeArgs a;
+    a.op = Op::TIES_TAU;
+    a.lambda = lambda;
+    a.tau = tau;
     return run_merge(layout, base, experts, K, residency, mask, out, io, static_cast<hipStream_t>(stream), a);
 }
 

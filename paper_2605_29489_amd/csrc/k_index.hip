@@ -11,6 +11,7 @@
 // per workgroup), so HBM sees it once.
 #include "device_common.h"
 #include "mp_internal.h"
+#include "ties_select.h"
 
 namespace mp {
 
@@ -75,7 +76,99 @@ __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, Ex
     }
 }
 
+// Catalog statistics for TIES: per unit, the sum of squares of k_index
+// (same order, same bits; optional) and the trim threshold, the fp32
+// pattern of the k-th largest |d| of the (expert, block) unit for a keep
+// density (+infinity's pattern when k = 0).  The threshold depends on the
+// unit and the density only, never on an access mask, so merges at any
+// budget can reuse it.  Wave w takes experts w, w+4, ... of the block: it
+// holds the whole block in registers (64 deltas per lane; lane l owns
+// chunks l, l+64, ...) and selects with its own LDS row, so the workgroup
+// never synchronises.
+#ifndef MP_CAT_WAVES
+#define MP_CAT_WAVES 3
+#endif
+template <int DT>
+__global__ __launch_bounds__(256, MP_CAT_WAVES) void k_index_ties(const void* __restrict__ base, ExpertPtrs ex,
+                                                                  int K, const uint64_t* __restrict__ boff,
+                                                                  const uint32_t* __restrict__ blen,
+                                                                  uint32_t n_full, uint32_t k_full, double density,
+                                                                  float* __restrict__ sumsq,
+                                                                  uint32_t* __restrict__ tau)
+{
+    constexpr int V = Fmt<DT>::V;
+    constexpr int R = kTiesMaxBlock / 64 / V;  // chunk rows per lane
+    constexpr int E = R * V;                   // deltas per lane
+    __shared__ uint32_t rows[4][ties::NB];
+    const int64_t g = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const uint64_t off = boff[g];
+    const uint32_t n = blen[g];
+    const uint32_t nch = n / V;
+    uint32_t k = k_full;
+    if (n != n_full) {
+        const double kk = ceil(density * (double)n);
+        k = (kk >= (double)n) ? n : (uint32_t)kk;
+    }
+    const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
+    for (int i = wave; i < K; i += 4) {
+        const uint4* e = chunk_ptr(ex.p[i], off, Fmt<DT>::esize);
+        uint4 xb[R], xe[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const uint32_t c = (uint32_t)(r * 64 + lane);
+            xb[r] = make_uint4(0u, 0u, 0u, 0u);
+            xe[r] = make_uint4(0u, 0u, 0u, 0u);
+            if (c < nch) {
+                xb[r] = b[c];
+                xe[r] = e[c];
+            }
+        }
+        float d[E];
+        float p = 0.0f;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            float fb[V], fe[V];
+            Fmt<DT>::unpack(xb[r], fb);
+            Fmt<DT>::unpack(xe[r], fe);
+#pragma unroll
+            for (int q = 0; q < V; ++q) {
+                d[r * V + q] = fe[q] - fb[q];             // padding: 0 - 0
+                p = fmaf(d[r * V + q], d[r * V + q], p);  // + 0 on padding, exact
+            }
+        }
+#pragma unroll
+        for (int s = 32; s >= 1; s >>= 1)
+            p = p + __shfl_xor(p, s);
+        const uint32_t t = (k == 0u) ? 0x7f800000u : wave_kth_largest<E>(rows[wave], d, k, lane);
+        if (lane == 0) {
+            if (sumsq != nullptr)
+                sumsq[g * K + i] = p;
+            tau[g * K + i] = t;
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_index_ties(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
+                             double density, float* sumsq, uint32_t* tau, hipStream_t s)
+{
+    if (bt.G == 0)
+        return hipSuccess;
+    const uint32_t n_full = (uint32_t)bt.block_elems;
+    const double kk = ceil(density * (double)n_full);
+    const uint32_t k_full = (kk >= (double)n_full) ? n_full : (uint32_t)kk;
+    const dim3 grid((unsigned)bt.G), block(256);
+    if (bt.dtype == 0)
+        hipLaunchKernelGGL(k_index_ties<0>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, n_full, k_full,
+                           density, sumsq, tau);
+    else
+        hipLaunchKernelGGL(k_index_ties<1>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, n_full, k_full,
+                           density, sumsq, tau);
+    return hipGetLastError();
+}
 
 hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
                         float* sumsq, hipStream_t s)

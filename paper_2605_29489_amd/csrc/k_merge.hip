@@ -15,6 +15,7 @@
 // buffer, which is device memory or pinned host memory read over PCIe.
 #include "device_common.h"
 #include "mp_internal.h"
+#include "ties_select.h"
 
 namespace mp {
 
@@ -40,7 +41,7 @@ __device__ inline void count_expert_bytes(unsigned long long* ctr, uint32_t m, u
 }
 
 // ------------------------------------------------------------ elementwise family
-enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2 };
+enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2, M_TIES_TAU = 3 };
 
 template <int DT, int MODE, class Src>
 // DARE's Philox and sign-election state would otherwise take up to 134
@@ -54,11 +55,14 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
                                                    const uint64_t* __restrict__ belem0, Coeffs alpha,
                                                    float lambda, uint32_t drop_T, float scale,
                                                    uint32_t seed, uint32_t kmask, void* __restrict__ out,
-                                                   unsigned long long* __restrict__ ctr)
+                                                   unsigned long long* __restrict__ ctr,
+                                                   const uint32_t* __restrict__ tau, int K)
 {
     constexpr int V = Fmt<DT>::V;
     constexpr int ES = Fmt<DT>::esize;
     constexpr int CPT = (DT == 1) ? 2 : 4;  // chunks per thread per tile (4096-element blocks: 1 tile)
+    constexpr bool DARE = MODE == M_DARE_LIN || MODE == M_DARE_SIGN;
+    constexpr bool SIGN = MODE == M_DARE_SIGN || MODE == M_TIES_TAU;
     constexpr int E = CPT * V;
     const int64_t b = blockIdx.x;
     const int t = threadIdx.x;
@@ -72,7 +76,7 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
     count_expert_bytes(ctr, m, n, ES);
     uint32_t tens = 0;
     uint64_t e0 = 0;
-    if (MODE != M_AVG) {
+    if (DARE) {
         tens = btensor[g];
         e0 = belem0[g];
     }
@@ -128,6 +132,11 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
                 if (j >= cnt)
                     break;
                 const int i = idx[j];
+                // TIES from catalog thresholds: keep |d| >= tau (at least the
+                // smallest positive pattern, so a kept delta is not zero)
+                float tauf = 0.0f;
+                if (MODE == M_TIES_TAU)
+                    tauf = __uint_as_float(max(tau[(uint64_t)g * (uint32_t)K + (uint32_t)i], 1u));
 #pragma unroll
                 for (int q = 0; q < CPT; ++q) {
                     if (!ok[q])
@@ -135,7 +144,7 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
                     float x[V];
                     Fmt<DT>::unpack(raw[j][q], x);
                     uint32_t word[V];
-                    if (MODE != M_AVG) {
+                    if (DARE) {
                         // Philox words for elements e .. e+V-1 of tensor `tens` (V is 4 or 8)
                         const uint64_t e = e0 + (uint64_t)(tile + q * kT + t) * V;
 #pragma unroll
@@ -156,7 +165,11 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
                         if (MODE == M_AVG) {
                             acc[e] = fmaf(alpha.v[i], d, acc[e]);
                         } else {
-                            const float tv = (word[v] < drop_T) ? 0.0f : d * scale;
+                            float tv;
+                            if (MODE == M_TIES_TAU)
+                                tv = (fabsf(d) >= tauf) ? d : 0.0f;
+                            else
+                                tv = (word[v] < drop_T) ? 0.0f : d * scale;
                             if (MODE == M_DARE_LIN) {
                                 acc[e] = fmaf(alpha.v[i], tv, acc[e]);
                             } else {
@@ -171,7 +184,7 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
             }
             rank += cnt;
         }
-        if (MODE == M_DARE_SIGN) {
+        if (SIGN) {
             // elect the sign of the larger signed mass; mean of the agreeing
             // entries (a count that is a power of two divides by exact scaling,
             // correctly rounded as the quotient; otherwise IEEE division)
@@ -218,54 +231,32 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
 // elements: 16 per thread and expert) stay in registers, and up to four
 // selected experts are trimmed together so that they share the barriers.
 // Per expert, tau = the k-th largest |d| is found on the fp32 magnitude bit
-// patterns:
+// patterns (window, bins and fallbacks as in ties_select.h):
 //  A  the block maximum M (wave maxima, one value per wave in LDS);
 //  B  the elements of the four binades below the binade of M are counted
-//     into a 2048-bin histogram keyed by |d| >> 14 (exponent and 9 mantissa
-//     bits).  The high half of a counter counts the elements whose 14 low
-//     bits are not zero, i.e. that lie above the bin's floor.  Elements in
-//     M's binade are counted with wave ballots; smaller ones are not counted:
-//     they are the bulk of a block, hold few distinct values and would
-//     serialise the LDS atomics on a handful of counters;
+//     into the window histogram; the top binade is counted with ballots;
 //  C  one wave per expert walks the histogram from the top to the bin where
 //     the count reaches k, needing r more elements from that bin.  If fewer
 //     than r of the bin's elements lie above its floor, the floor is the
 //     k-th largest value; if the whole bin is needed its floor keeps the
-//     same elements as the k-th largest.  Either way tau is found;
+//     same elements as the k-th largest.  Either way the keep set is known;
 //  D  otherwise (rare) the bin's elements are listed in LDS and one wave
-//     resolves the 14 low bits one at a time; if tau lies outside the window
+//     resolves the low bits one at a time; if tau lies outside the window
 //     or the list overflows, an exact 3-level radix select over all
 //     elements runs instead.
 // Then one pass over the elements keeps |d| >= tau (tau is at least the
 // smallest positive pattern, so a kept delta is not zero), elects the sign
 // of the larger of the positive and negative kept masses and takes the mean
 // of the agreeing entries.
-#ifndef MP_TIES_MB
-#define MP_TIES_MB 7
-#endif
-#ifndef MP_TIES_NC
-#define MP_TIES_NC 4
-#endif
-#ifndef MP_TIES_ASM
-#define MP_TIES_ASM 1
-#endif
 namespace ties {
+using namespace ::mp::ties;  // window constants of ties_select.h
 #ifndef MP_TIES_NT
 #define MP_TIES_NT 256
 #endif
-constexpr int NT = MP_TIES_NT;  // threads per workgroup
+constexpr int NT = MP_TIES_NT;           // threads per workgroup
 constexpr int EPT = kTiesMaxBlock / NT;  // elements per thread and expert
-constexpr int NW = NT / 64;     // waves per workgroup
-constexpr int GS = 4;           // experts trimmed together (one scanning wave each)
-constexpr int MB = MP_TIES_MB;  // mantissa bits in a window key
-constexpr int NC = MP_TIES_NC;  // copies of each window bin (lanes spread over them)
-constexpr int KS = 23 - MB;     // pattern bits below a key
-constexpr int NBIN = 4 << MB;   // window bins: four binades
-constexpr int NB = 2048;        // words per histogram row
-static_assert(NBIN * NC == NB, "a histogram row holds every copy of every bin");
-static_assert(NC == 1 || NC == 2 || NC == 4 || NC == 8 || NC == 16, "bins are 16-byte aligned or fill one");
-constexpr int LG = (NC == 1) ? 2 : (NC == 2) ? 3 : (NC == 4) ? 4 : (NC == 8) ? 5 : 6;  // log2(4 NC)
-enum : uint32_t { DONE = 0u, LIST = 1u, RADIX = 2u };
+constexpr int NW = NT / 64;              // waves per workgroup
+constexpr int GS = 4;                    // experts trimmed together (one scanning wave each)
 }  // namespace ties
 
 struct TiesSmem {
@@ -275,110 +266,6 @@ struct TiesSmem {
     uint32_t st[ties::GS][4];           // state, tau (or bucket key), rank in the bucket, list length
 };
 
-struct Cut {
-    uint32_t found, bin, rank, count, aux;  // wave-uniform
-};
-
-// Wave-level, all lanes: walk histogram bins downward from bin `top` and
-// find the bin where the count from the top first reaches k.  A bin is NC
-// consecutive words; counts are the low 16 bits of the word sums and aux
-// returns the bin's high-half sum.  rank = k minus the count above the bin.
-// Each round reads 1 KB: 16 consecutive bytes per lane (conflict-free), and
-// prefix-sums the lane totals across the wave with DPP.
-template <int NC>
-__device__ inline Cut wave_find_from_top(const uint32_t* __restrict__ h, int top, uint32_t k, int lane)
-{
-    if (NC >= 4) {  // one bin per lane per round
-        Cut r{0u, 0u, 0u, 0u, 0u};
-        uint32_t above = 0;
-        for (int hb = top; hb >= 0; hb -= 64) {
-            const int bin = hb - lane;
-            uint32_t w = 0u;
-            if (bin >= 0) {
-                const uint4* p = reinterpret_cast<const uint4*>(h + bin * NC);
-#pragma unroll
-                for (int u = 0; u < NC / 4; ++u) {
-                    const uint4 raw = p[u];
-                    w += raw.x + raw.y + raw.z + raw.w;
-                }
-            }
-            const uint32_t s = w & 0xffffu;
-            const uint32_t incl = wave_incl_sum(s);
-            const uint32_t before = above + incl - s;
-            const bool hit = before < k && k <= above + incl;
-            const unsigned long long bal = __ballot(hit);
-            if (bal) {
-                const int src = __ffsll((long long)bal) - 1;
-                r.found = 1u;
-                r.bin = (uint32_t)__builtin_amdgcn_readlane(bin, src);
-                r.rank = (uint32_t)__builtin_amdgcn_readlane((int)(k - before), src);
-                r.count = (uint32_t)__builtin_amdgcn_readlane((int)s, src);
-                r.aux = (uint32_t)__builtin_amdgcn_readlane((int)(w >> 16), src);
-                return r;
-            }
-            above += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
-        }
-        return r;
-    }
-    constexpr int BPL = NC >= 4 ? 1 : 4 / NC;  // bins per lane per round
-    Cut r{0u, 0u, 0u, 0u, 0u};
-    const int topw = top * NC + NC - 1;  // highest word
-    uint32_t above = 0;
-    for (int hi = topw | 3; hi >= 0; hi -= 256) {
-        const int g4 = hi - 4 * lane - 3;  // multiple of 4: the lane's words are g4 .. g4+3
-        uint4 raw = make_uint4(0u, 0u, 0u, 0u);
-        if (g4 >= 0)
-            raw = *reinterpret_cast<const uint4*>(h + g4);
-        uint32_t bw[BPL];  // bin sums, highest bin first
-        if (NC == 1) {
-            bw[0] = raw.w; bw[BPL > 1 ? 1 : 0] = raw.z; bw[BPL > 2 ? 2 : 0] = raw.y; bw[BPL > 3 ? 3 : 0] = raw.x;
-        } else if (NC == 2) {
-            bw[0] = raw.z + raw.w; bw[BPL > 1 ? 1 : 0] = raw.x + raw.y;
-        } else {
-            bw[0] = raw.x + raw.y + raw.z + raw.w;
-        }
-        uint32_t s = 0u;
-#pragma unroll
-        for (int q = 0; q < BPL; ++q)
-            s += bw[q] & 0xffffu;
-        const uint32_t incl = wave_incl_sum(s);
-        const uint32_t before = above + incl - s;  // count in the bins above this lane's
-        const bool hit = before < k && k <= above + incl;
-        const unsigned long long bal = __ballot(hit);
-        if (bal) {
-            uint32_t c = before, bin = 0u, cnt = 0u, aux = 0u;
-            bool got = false;
-#pragma unroll
-            for (int q = 0; q < BPL; ++q) {
-                const uint32_t cq = bw[q] & 0xffffu;
-                if (!got && (c + cq >= k || q == BPL - 1)) {
-                    got = true;
-                    bin = (uint32_t)(g4 / NC + BPL - 1 - q);
-                    cnt = cq;
-                    aux = bw[q] >> 16;
-                } else if (!got) {
-                    c += cq;
-                }
-            }
-            const int src = __ffsll((long long)bal) - 1;
-            r.found = 1u;
-            r.bin = (uint32_t)__builtin_amdgcn_readlane((int)bin, src);
-            r.rank = (uint32_t)__builtin_amdgcn_readlane((int)(k - c), src);
-            r.count = (uint32_t)__builtin_amdgcn_readlane((int)cnt, src);
-            r.aux = (uint32_t)__builtin_amdgcn_readlane((int)aux, src);
-            return r;
-        }
-        above += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
-    }
-    return r;
-}
-
-// Sum over the lanes of a wave (wave-uniform result).
-__device__ inline uint32_t wave_sum_u32(uint32_t v)
-{
-    return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_sum(v), 63);
-}
-
 template <int DT, int NT, int CPT>
 __device__ inline void load_chunks(const uint4* __restrict__ p, uint32_t nch, uint4 (&dst)[CPT])
 {
@@ -386,24 +273,6 @@ __device__ inline void load_chunks(const uint4* __restrict__ p, uint32_t nch, ui
 #pragma unroll
     for (int q = 0; q < CPT; ++q)
         dst[q] = (q * NT + t < nch) ? p[q * NT + t] : make_uint4(0u, 0u, 0u, 0u);
-}
-
-// Wave-level: the r-th largest of the n patterns in `list`, all of which
-// share the key (pattern >> KS); the low bits are fixed from the top down.
-__device__ inline uint32_t wave_select_list(const uint32_t* __restrict__ list, uint32_t n, uint32_t key,
-                                            uint32_t r, int lane)
-{
-    uint32_t pref = key << ties::KS;
-#pragma unroll 1
-    for (int bit = ties::KS - 1; bit >= 0; --bit) {
-        const uint32_t cand = pref | (1u << bit);
-        uint32_t c = 0u;
-        for (uint32_t i = (uint32_t)lane; i < n; i += 64u)
-            c += (list[i] >= cand) ? 1u : 0u;
-        if (wave_sum_u32(c) >= r)
-            pref = cand;
-    }
-    return pref;
 }
 
 // Whole workgroup: exact k-th largest magnitude pattern of slot j over all
@@ -514,36 +383,14 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
             for (int w = 0; w < NW; ++w)
                 bmax[j] = max(bmax[j], uniform_u32(sm.wmax[j][w]));
             if (bmax[j] != 0u) {
-                const int wb = (int)((bmax[j] >> 23) << MB) - NBIN;  // key of bin 0
-                // byte offset of key kk in this lane's copy: (kk << LG) + koff; out of
-                // the window it wraps past the row
-                const uint32_t koff = (uint32_t)(lane & (NC - 1)) * 4u - (uint32_t)wb * (uint32_t)(4 * NC);
+                int wb;
+                const uint32_t koff = window_koff(bmax[j], lane, &wb);
                 const float topf = __uint_as_float((bmax[j] >> 23) << 23);  // first value of M's binade
                 char* row = reinterpret_cast<char*>(sm.h[j]);
                 uint32_t ntop = 0u;
 #pragma unroll
                 for (int e = 0; e < E; ++e) {
-                    const uint32_t bits = __float_as_uint(d[j][e]);
-#if MP_TIES_ASM
-                    static_assert(KS == 16, "the low bits are the low half-word");
-                    uint32_t key, boff;
-                    asm("v_bfe_u32 %0, %1, %2, %3" : "=v"(key) : "v"(bits), "i"(KS), "i"(31 - KS));
-                    asm("v_lshl_add_u32 %0, %1, %2, %3" : "=v"(boff) : "v"(key), "i"(LG), "v"(koff));
-#else
-                    const uint32_t boff = (__builtin_amdgcn_ubfe(bits, KS, 31 - KS) << LG) + koff;
-#endif
-                    if (boff < (uint32_t)(NB * 4)) {
-                        // count in the high half when the low bits are not zero
-#if MP_TIES_ASM
-                        uint32_t nz;
-                        asm("v_min_u32_sdwa %0, %1, 1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD"
-                            : "=v"(nz) : "v"(bits));
-                        const uint32_t inc = (nz << 16) + 1u;
-#else
-                        const uint32_t inc = (min(bits & ((1u << KS) - 1u), 1u) << 16) + 1u;
-#endif
-                        atomicAdd(reinterpret_cast<uint32_t*>(row + boff), inc);
-                    }
+                    window_add(row, __float_as_uint(d[j][e]), koff);
                     ntop += (uint32_t)__popcll(__ballot(fabsf(d[j][e]) >= topf));
                 }
                 if (lane == 0)
@@ -900,17 +747,23 @@ hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src
     switch (a.op) {
     case Op::AVG:
         hipLaunchKernelGGL((k_merge_elem<DT, M_AVG, Src>), grid, block, 0, s, src, base, mask, bt.d_off,
-                           bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask, out, ctr);
+                           bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask, out, ctr,
+                           nullptr, K);
         break;
     case Op::DARE_LINEAR:
         hipLaunchKernelGGL((k_merge_elem<DT, M_DARE_LIN, Src>), grid, block, 0, s, src, base, mask,
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, T, scale,
-                           a.seed, kmask, out, ctr);
+                           a.seed, kmask, out, ctr, nullptr, K);
         break;
     case Op::DARE_SIGN:
         hipLaunchKernelGGL((k_merge_elem<DT, M_DARE_SIGN, Src>), grid, block, 0, s, src, base, mask,
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, T, scale,
-                           a.seed, kmask, out, ctr);
+                           a.seed, kmask, out, ctr, nullptr, K);
+        break;
+    case Op::TIES_TAU:
+        hipLaunchKernelGGL((k_merge_elem<DT, M_TIES_TAU, Src>), grid, block, 0, s, src, base, mask,
+                           bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask,
+                           out, ctr, a.tau, K);
         break;
     case Op::TIES: {
         // k for full-length blocks, as the kernel computes it for short ones

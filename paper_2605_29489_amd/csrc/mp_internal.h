@@ -68,6 +68,11 @@ struct PlanScratch {
 hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
                         float* sumsq, hipStream_t s);
 
+// Index plus the per-unit TIES thresholds for `density` (sumsq may be null).
+// Blocks must hold at most kTiesMaxBlock elements.
+hipError_t launch_index_ties(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
+                             double density, float* sumsq, uint32_t* tau, hipStream_t s);
+
 // Algorithm 1 on the device (k_plan.hip).
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
                        const Coeffs& w, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
@@ -75,7 +80,7 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
 
 // Merge operators.  `counters` is null or a device array of 256 uint64
 // accumulating the expert bytes the kernels load.
-enum class Op { AVG = 0, TIES = 1, DARE_LINEAR = 2, DARE_SIGN = 3 };
+enum class Op { AVG = 0, TIES = 1, DARE_LINEAR = 2, DARE_SIGN = 3, TIES_TAU = 4 };
 
 struct MergeArgs {
     Op op = Op::AVG;
@@ -84,6 +89,7 @@ struct MergeArgs {
     float lambda = 1.0f;
     double p = 0.0;
     uint32_t seed = 0;
+    const uint32_t* tau = nullptr;  // TIES_TAU: per-unit thresholds [G*K]
 };
 
 hipError_t launch_merge(const BlockTable& bt, const MergeArgs& a, const void* base,

@@ -59,6 +59,16 @@ def _full_run(mp, name, K, op, budgets, n_random=192, **kw):
     S_orc = oracle.index(blocks, "bf16", b_np, e_np, doff=doff, ids=ids)
     assert np.array_equal(S.reshape(G, K)[ids].view(np.uint32), S_orc.view(np.uint32)), "index differs on samples"
     _say(f"  index ok on {len(ids)} sampled blocks")
+    tau = None
+    if op == "ties":  # catalog thresholds (and the same sums of squares) in one pass
+        tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
+        sumsq2 = torch.empty_like(sumsq)
+        mp.mp_index_ties(L, base, exps, kw["density"], tau, sumsq=sumsq2)
+        assert torch.equal(sumsq2.view(torch.int32), sumsq.view(torch.int32)), "catalog sums of squares differ"
+        t_orc = oracle.ties_thresholds(blocks, "bf16", b_np, e_np, kw["density"], ids=ids, doff=doff)
+        assert np.array_equal(tau.cpu().numpy().view(np.uint32).reshape(G, K)[ids], t_orc), "thresholds differ"
+        _say(f"  thresholds ok on {len(ids)} sampled blocks")
+        del sumsq2
     mask = torch.empty(G, dtype=torch.int32, device="cuda")
     out = torch.empty_like(base)
     full = lay.n_params * 2 * K
@@ -75,6 +85,12 @@ def _full_run(mp, name, K, op, budgets, n_random=192, **kw):
             io = mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out, io=True)
             want = oracle.merge_ties(blocks, "bf16", b_np, e_np, m_orc[ids], kw["density"], kw["lam"],
                                      ids=ids, doff=doff)
+            # catalog thresholds: the same bits for the whole checkpoint
+            out2 = torch.empty_like(out)
+            io2 = mp.mp_merge_ties_tau(L, base, exps, mask, tau, kw["lam"], out2, io=True)
+            assert io2["expert_bytes"] == st["cost_bytes"]
+            assert torch.equal(out.view(torch.int16), out2.view(torch.int16)), f"catalog-threshold TIES differs at B={f}"
+            del out2
         else:
             io = mp.mp_merge_dare(L, base, exps, mask, kw["p"], kw["seed"], 1, None, kw["lam"], out, io=True)
             want = oracle.merge_dare(blocks, "bf16", b_np, e_np, m_orc[ids], kw["p"], kw["seed"], 1,

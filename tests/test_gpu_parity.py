@@ -80,7 +80,14 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
     else:
         exps = [to_dev(e, dtype) for e in exps_np]
     sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
-    mp.mp_index_blocks(L, base, exps, sumsq, residency=res)
+    tau = None
+    if op == "ties_tau":  # catalog pass: sums of squares and per-unit thresholds together
+        tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
+        mp.mp_index_ties(L, base, exps, kw["density"], tau, sumsq=sumsq, residency=res)
+        t_orc = oracle.ties_thresholds(blocks, dtype, base_np, exps_np, kw["density"]).reshape(-1)
+        assert np.array_equal(tau.cpu().numpy().view(np.uint32), t_orc), "thresholds differ"
+    else:
+        mp.mp_index_blocks(L, base, exps, sumsq, residency=res)
     S_gpu = sumsq.cpu().numpy()
     S_orc = oracle.index(blocks, dtype, base_np, exps_np).reshape(-1)
     assert np.array_equal(S_gpu.view(np.uint32), S_orc.view(np.uint32)), "index differs"
@@ -107,6 +114,14 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
         elif op == "ties":
             io = mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out, residency=res, io=True)
             want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"])
+        elif op == "ties_tau":
+            io = mp.mp_merge_ties_tau(L, base, exps, mask, tau, kw["lam"], out, residency=res, io=True)
+            want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"])
+            # the in-merge trim gives the same bits
+            out2 = torch.empty_like(base)
+            mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out2, residency=res)
+            assert torch.equal(out.view(torch.int16) if out.dtype == torch.bfloat16 else out.view(torch.int32),
+                               out2.view(torch.int16) if out2.dtype == torch.bfloat16 else out2.view(torch.int32))
         else:
             comb = 0 if op == "dare_lin" else 1
             io = mp.mp_merge_dare(L, base, exps, mask, kw["p"], kw["seed"], comb, kw.get("alpha"), kw["lam"],
@@ -116,9 +131,12 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
         got = to_host(out)
         nb = assert_merge_equal(got, want, base_np, dtype, f"{op} B={B}")
         assert nb == 0, f"{op} B={B}: {nb} values within tolerance but not bitwise equal"
-        assert io["expert_bytes"] == st["cost_bytes"], "kernels loaded bytes outside the plan"
-        if res == mp.MP_HOST_PINNED:  # only the selected blocks cross PCIe (Prop. 1)
-            assert io["h2d_bytes"] == st["cost_bytes"]
+        # the kernels read exactly the selected expert blocks (Prop. 1); TIES with
+        # density 0 keeps nothing and reads no expert at all
+        read = 0 if (op == "ties" and kw.get("density") == 0.0) else st["cost_bytes"]
+        assert io["expert_bytes"] == read, "kernels loaded bytes outside the plan"
+        if res == mp.MP_HOST_PINNED:  # only those blocks cross PCIe
+            assert io["h2d_bytes"] == read
         else:
             assert io["h2d_bytes"] == 0
         results.append((B, st, nb))
@@ -128,7 +146,7 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
 
 # ---------------------------------------------------------------- small families
 
-@pytest.mark.parametrize("op", ["avg", "ties", "dare_lin", "dare_sign"])
+@pytest.mark.parametrize("op", ["avg", "ties", "ties_tau", "dare_lin", "dare_sign"])
 def test_mini_qwen_bf16_all_ops(mp, op):
     spec = _mini_qwen()
     base, exps = make_family(spec, seed=1)
@@ -137,7 +155,7 @@ def test_mini_qwen_bf16_all_ops(mp, op):
     _run_all(mp, spec, base, exps, op, [0, 0.1, 0.25, 0.5, 0.77, 1.0, 2.0, 12345], **kw)
 
 
-@pytest.mark.parametrize("op", ["avg", "ties", "dare_lin", "dare_sign"])
+@pytest.mark.parametrize("op", ["avg", "ties", "ties_tau", "dare_lin", "dare_sign"])
 def test_ragged_fp32_all_ops(mp, op):
     spec = _ragged_f32()
     base, exps = make_family(spec, seed=2)
@@ -146,7 +164,7 @@ def test_ragged_fp32_all_ops(mp, op):
     _run_all(mp, spec, base, exps, op, [0, 0.3, 0.6, 1.0], **kw)
 
 
-@pytest.mark.parametrize("op", ["avg", "ties", "dare_lin", "dare_sign"])
+@pytest.mark.parametrize("op", ["avg", "ties", "ties_tau", "dare_lin", "dare_sign"])
 def test_host_pinned_experts_all_ops(mp, op):
     # experts in pinned host memory: the kernels read the selected blocks
     # over PCIe; results are the same bits as with device-resident experts
@@ -206,6 +224,7 @@ def test_expert_counts(mp, K):
     base, exps = make_family(spec, K=K, seed=10 + K)
     _say(f"case mini-qwen K={K}")
     _run_all(mp, spec, base, exps, "ties", [0.0, 0.4, 1.0], density=0.2, lam=1.0)
+    _run_all(mp, spec, base, exps, "ties_tau", [0.4, 1.0], density=0.2, lam=1.0)
     _run_all(mp, spec, base, exps, "avg", [0.4], alpha=[1.0 / K] * K)
 
 
@@ -215,6 +234,7 @@ def test_block_sizes(mp, be):
     base, exps = make_family(spec, seed=4)
     _say(f"case block_elems={be}")
     _run_all(mp, spec, base, exps, "ties", [0.35, 1.0], density=0.3, lam=1.0)
+    _run_all(mp, spec, base, exps, "ties_tau", [0.35, 1.0], density=0.3, lam=1.0)
     _run_all(mp, spec, base, exps, "dare_lin", [0.5], alpha=[0.3, 0.2, 0.4, 0.1], p=0.3, seed=11, lam=1.0)
 
 
@@ -250,6 +270,7 @@ def test_ties_and_zero_and_identical_experts(mp):
         c[sel] = (c[sel].astype(np.int32) + rng.integers(-2, 3, int(sel.sum()))).astype(np.uint16)
     _say("case coarse ties")
     _run_all(mp, spec, base, coarse, "ties", [0.5, 1.0], density=0.15, lam=1.0)
+    _run_all(mp, spec, base, coarse, "ties_tau", [0.5, 1.0], density=0.15, lam=1.0)
 
 
 def _bf16_family_from_deltas(base_np, deltas):
@@ -276,9 +297,10 @@ def test_ties_threshold_search_paths(mp):
     sparse = np.where(rng.random(P) < 0.1, rng.normal(0.0, 1e-3, P), 0.0)
     dense = 1e-3 * (1.0 + rng.integers(0, 4, P) / 64.0) * np.sign(rng.normal(size=P))
     exps = _bf16_family_from_deltas(base, [uni, heavy, sparse, dense])
-    for dens in (0.2, 0.05, 1.0 / 4096, 1.0):
+    for dens in (0.2, 0.05, 1.0 / 4096, 1.0, 0.0):
         _say(f"case threshold paths density={dens}")
         _run_all(mp, spec, base, exps, "ties", [0.5, 1.0], density=dens, lam=1.0)
+        _run_all(mp, spec, base, exps, "ties_tau", [0.5, 1.0], density=dens, lam=1.0)
 
 
 def test_ties_subnormal_deltas(mp):
@@ -292,6 +314,7 @@ def test_ties_subnormal_deltas(mp):
     exps = _bf16_family_from_deltas(base, deltas)
     _say("case subnormal deltas")
     _run_all(mp, spec, base, exps, "ties", [0.4, 1.0], density=0.2, lam=1.0)
+    _run_all(mp, spec, base, exps, "ties_tau", [0.4, 1.0], density=0.2, lam=1.0)
     _run_all(mp, spec, base, exps, "ties", [1.0], density=0.3, lam=0.5)
 
 
