@@ -233,15 +233,15 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
 // Per expert, tau = the k-th largest |d| is found on the fp32 magnitude bit
 // patterns (window, bins and fallbacks as in ties_select.h):
 //  A  the block maximum M (wave maxima, one value per wave in LDS);
-//  B  the elements of the four binades below the binade of M are counted
-//     into the window histogram; the top binade is counted with ballots;
+//  B  the elements of the binade of M and of the three binades below it
+//     are counted into the window histogram (nothing lies above it);
 //  C  one wave per expert walks the histogram from the top to the bin where
 //     the count reaches k, needing r more elements from that bin.  If fewer
 //     than r of the bin's elements lie above its floor, the floor is the
 //     k-th largest value; if the whole bin is needed its floor keeps the
 //     same elements as the k-th largest.  Either way the keep set is known;
 //  D  otherwise (rare) the bin's elements are listed in LDS and one wave
-//     resolves the low bits one at a time; if tau lies outside the window
+//     resolves the low bits one at a time; if tau lies below the window
 //     or the list overflows, an exact 3-level radix select over all
 //     elements runs instead.
 // Then one pass over the elements keeps |d| >= tau (tau is at least the
@@ -262,8 +262,8 @@ constexpr int GS = 4;                    // experts trimmed together (one scanni
 struct TiesSmem {
     uint32_t h[ties::GS][ties::NB];     // window histogram, then candidate list / radix levels
     uint32_t wmax[ties::GS][ties::NW];  // per-wave maximum |d| pattern
-    uint32_t wtop[ties::GS][ties::NW];  // per-wave count of elements in the top binade
     uint32_t st[ties::GS][4];           // state, tau (or bucket key), rank in the bucket, list length
+    float2 rd[8];                       // divisors {den, 1/den} of the small-K mean
 };
 
 template <int DT, int NT, int CPT>
@@ -362,10 +362,11 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
                 float x[V];
                 Fmt<DT>::unpack(raw[j][q], x);
 #pragma unroll
-                for (int v = 0; v < V; ++v) {
+                for (int v = 0; v < V; ++v)
                     d[j][q * V + v] = x[v] - x0[q * V + v];  // padding: 0 - 0
-                    mx = fmaxf(mx, fabsf(d[j][q * V + v]));
-                }
+#pragma unroll
+                for (int v = 0; v < V; v += 2)  // pairs: one three-way maximum each
+                    mx = fmaxf(mx, fmaxf(fabsf(d[j][q * V + v]), fabsf(d[j][q * V + v + 1])));
             }
             const uint32_t w = wave_max_u32(__float_as_uint(mx));
             if (lane == 0)
@@ -373,7 +374,7 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
         }
     }
     __syncthreads();
-    // ---- B: window histograms and top-binade counts
+    // ---- B: window histograms
     uint32_t bmax[GS];
 #pragma unroll
     for (int j = 0; j < GS; ++j) {
@@ -385,16 +386,10 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
             if (bmax[j] != 0u) {
                 int wb;
                 const uint32_t koff = window_koff(bmax[j], lane, &wb);
-                const float topf = __uint_as_float((bmax[j] >> 23) << 23);  // first value of M's binade
                 char* row = reinterpret_cast<char*>(sm.h[j]);
-                uint32_t ntop = 0u;
 #pragma unroll
-                for (int e = 0; e < E; ++e) {
+                for (int e = 0; e < E; ++e)
                     window_add(row, __float_as_uint(d[j][e]), koff);
-                    ntop += (uint32_t)__popcll(__ballot(fabsf(d[j][e]) >= topf));
-                }
-                if (lane == 0)
-                    sm.wtop[j][wave] = ntop;
             }
         }
     }
@@ -408,24 +403,16 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
             bm = max(bm, uniform_u32(sm.wmax[j][w]));
         uint32_t state = DONE, v1 = 1u, v2 = 0u;  // v1: tau, or the bucket key to refine
         if (bm != 0u && k < n) {                  // all zero, or k = n: keep every nonzero
-            uint32_t atop = 0u;
-#pragma unroll
-            for (int w = 0; w < NW; ++w)
-                atop += uniform_u32(sm.wtop[j][w]);
-            if (atop >= k) {
-                state = RADIX;  // tau lies in the top binade
+            const Cut c = wave_find_from_top<NC>(sm.h[j], NBIN - 1, k, lane);
+            const int wb = window_base(bm);
+            if (!c.found) {
+                state = RADIX;  // tau lies below the window
+            } else if (c.aux < c.rank || c.count == c.rank) {
+                v1 = max((uint32_t)(wb + (int)c.bin) << KS, 1u);
             } else {
-                const Cut c = wave_find_from_top<NC>(sm.h[j], NBIN - 1, k - atop, lane);
-                const int wb = (int)((bm >> 23) << MB) - NBIN;
-                if (!c.found) {
-                    state = RADIX;  // tau lies below the window
-                } else if (c.aux < c.rank || c.count == c.rank) {
-                    v1 = max((uint32_t)(wb + (int)c.bin) << KS, 1u);
-                } else {
-                    state = LIST;
-                    v1 = (uint32_t)(wb + (int)c.bin);
-                    v2 = c.rank;
-                }
+                state = LIST;
+                v1 = (uint32_t)(wb + (int)c.bin);
+                v2 = c.rank;
             }
         }
         if (lane == 0) {
@@ -502,41 +489,76 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
         tau[j] = (j < ns) ? uniform_u32(sm.st[j][1]) : 0xffffffffu;
 }
 
-// Keep test and the running signed masses of element e over NS slots; the
-// kept counts go to cnt (positive in the low, negative in the high half).
+// Keep test and the running signed masses of element e over NS slots, with
+// the kept counts np (positive) and nn (negative).  tau is at least the
+// smallest positive pattern, so d >= tau keeps a positive delta and
+// -d >= tau a negative one; a zero or NaN delta is never kept.
 template <int NS>
 __device__ inline void ties_accumulate(const float (&d)[ties::GS][ties::EPT], const uint32_t (&tau)[ties::GS], int e,
-                                       float& P, float& N, uint32_t& cnt)
+                                       float& P, float& N, uint32_t& np, uint32_t& nn)
 {
 #pragma unroll
     for (int j = 0; j < NS; ++j) {
         const float dj = d[j][e];
-        const bool keep = fabsf(dj) >= __uint_as_float(tau[j]);  // tau >= the smallest positive pattern
-        const bool kp = keep && dj > 0.0f;
-        const bool kn = keep && !(dj > 0.0f);
+        const float t = __uint_as_float(tau[j]);
+        const bool kp = dj >= t;
+        const bool kn = -dj >= t;
         P = P + (kp ? dj : 0.0f);
         N = N + (kn ? dj : 0.0f);
-        cnt += kp ? 1u : (kn ? 0x10000u : 0u);
+        np += kp ? 1u : 0u;
+        nn += kn ? 1u : 0u;
     }
 }
 
-// x / 3 correctly rounded for every finite nonzero x: the product with the
-// rounded reciprocal is within one ulp, and one FMA residual step fixes it
-// (Markstein's correction; checked against IEEE division on all 2^32 fp32
-// patterns -- only -0 comes out as +0, and a mean of three entries that
-// agree in sign is never zero).
-__device__ inline float div3(float x)
+// Divisors for the mean of at most four agreeing entries: {den, fl32(1/den)}
+// at index den (1..4; the others are unused and hold {1, 1}).
+__device__ inline float2 ties_divisor(int i)
 {
-    const float y = 0x1.555556p-2f;  // fl32(1/3)
-    const float q = x * y;
-    return fmaf(fmaf(-3.0f, q, x), y, q);
+    const float r = (i == 2) ? 0.5f : (i == 3) ? 0x1.555556p-2f : (i == 4) ? 0.25f : 1.0f;
+    return make_float2((i >= 2 && i <= 4) ? (float)i : 1.0f, r);
 }
 
 // Sign election (the sign of the larger of the positive and negative kept
 // masses) and the mean of the agreeing entries, for the V elements of one
-// chunk; then y = lambda * mean + x0, rounded once, is stored.  SMALLK: at
-// most 4 entries agree, so the count is 1, 2, 3 or 4 (at most MAXDEN).
-template <int DT, bool SMALLK, int MAXDEN = 32>
+// chunk of a block with NS (2..4) selected experts; then y = lambda * mean
+// + x0, rounded once, is stored.  With at most two agreeing entries the mean
+// is the entry or an exact halving.  Otherwise q = mean * fl32(1/den) and one
+// residual step q + fl32(mean - den*q) * fl32(1/den) give the correctly
+// rounded quotient: for den = 1, 2, 4 the product is already correctly
+// rounded and the residual term adds exactly nothing; for den = 3 this is
+// Markstein's correction, checked against IEEE division on all 2^32 fp32
+// patterns (only -0 comes out as +0, and an elected mass is never zero).
+template <int DT, int NS>
+__device__ inline void ties_store_small(const float (&P)[Fmt<DT>::V], const float (&N)[Fmt<DT>::V],
+                                        const uint32_t (&np)[Fmt<DT>::V], const uint32_t (&nn)[Fmt<DT>::V],
+                                        const float* x0, float lambda, const float2* rd,
+                                        uint4* __restrict__ dst, bool ok)
+{
+    constexpr int V = Fmt<DT>::V;
+    float y[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        const bool up = P[v] > -N[v];
+        const bool dn = P[v] < -N[v];
+        const float num = up ? P[v] : (dn ? N[v] : 0.0f);
+        const uint32_t den = up ? np[v] : (dn ? nn[v] : 1u);
+        float q;
+        if (NS <= 2) {
+            q = (den == 2u) ? num * 0.5f : num;
+        } else {
+            const float2 c = rd[den];
+            const float q0 = num * c.y;
+            q = fmaf(fmaf(-c.x, q0, num), c.y, q0);
+        }
+        y[v] = fmaf(lambda, q, x0[v]);
+    }
+    if (ok)
+        *dst = Fmt<DT>::pack(y);
+}
+
+// Election and mean for any number of agreeing entries (counts packed:
+// positive in the low, negative in the high half), then the store.
+template <int DT>
 __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const float (&N)[Fmt<DT>::V],
                                         const uint32_t (&cnt)[Fmt<DT>::V], const float* x0, float lambda,
                                         uint4* __restrict__ dst, bool ok)
@@ -553,22 +575,12 @@ __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const floa
         den[v] = up ? (cnt[v] & 0xffffu) : (dn ? (cnt[v] >> 16) : 1u);
         odd |= (den[v] & (den[v] - 1u)) != 0u;
     }
-    if (SMALLK && MAXDEN <= 2) {
-#pragma unroll
-        for (int v = 0; v < V; ++v)
-            num[v] = (den[v] == 2u) ? num[v] * 0.5f : num[v];  // exact halving
-    } else if (SMALLK) {
-#pragma unroll
-        for (int v = 0; v < V; ++v) {
-            // division by 2^s is exact scaling (correctly rounded, as the quotient)
-            const float qp = num[v] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[v])) << 23);
-            num[v] = (den[v] == 3u) ? div3(num[v]) : qp;
-        }
-    } else if (__any(odd)) {
+    if (__any(odd)) {
 #pragma unroll
         for (int v = 0; v < V; ++v)
             num[v] = num[v] / (float)den[v];
     } else {
+        // division by 2^s is exact scaling (correctly rounded, as the quotient)
 #pragma unroll
         for (int v = 0; v < V; ++v)
             num[v] = num[v] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[v])) << 23);
@@ -586,8 +598,8 @@ __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const floa
 // chunk.
 template <int DT, int NS>
 __device__ inline void ties_finish_single(const float (&d)[ties::GS][ties::EPT], const uint32_t (&tau)[ties::GS],
-                                          const float (&x0)[ties::EPT], float lambda, uint4* __restrict__ po,
-                                          uint32_t nch)
+                                          const float (&x0)[ties::EPT], float lambda, const float2* rd,
+                                          uint4* __restrict__ po, uint32_t nch)
 {
     constexpr int V = Fmt<DT>::V, CPT = ties::EPT / V;
     const int t = threadIdx.x;
@@ -612,28 +624,32 @@ __device__ inline void ties_finish_single(const float (&d)[ties::GS][ties::EPT],
             continue;
         }
         float P[V], N[V];
-        uint32_t cnt[V];
+        uint32_t np[V], nn[V];
 #pragma unroll
         for (int v = 0; v < V; ++v) {
             P[v] = 0.0f;
             N[v] = 0.0f;
-            cnt[v] = 0u;
-            ties_accumulate<NS>(d, tau, q * V + v, P[v], N[v], cnt[v]);
+            np[v] = 0u;
+            nn[v] = 0u;
+            ties_accumulate<NS>(d, tau, q * V + v, P[v], N[v], np[v], nn[v]);
         }
-        ties_store_chunk<DT, true, NS>(P, N, cnt, &x0[q * V], lambda, po + q * ties::NT + t,
-                                       q * ties::NT + t < (int)nch);
+        ties_store_small<DT, NS>(P, N, np, nn, &x0[q * V], lambda, rd, po + q * ties::NT + t,
+                                 q * ties::NT + t < (int)nch);
     }
 }
 
-// Several groups: the signed masses and the counts are carried across
+// Several groups: the signed masses and the packed counts are carried across
 // groups.
 template <int NS>
 __device__ inline void ties_accumulate_all(const float (&d)[ties::GS][ties::EPT], const uint32_t (&tau)[ties::GS],
                                            float (&P)[ties::EPT], float (&N)[ties::EPT], uint32_t (&cnt)[ties::EPT])
 {
 #pragma unroll
-    for (int e = 0; e < ties::EPT; ++e)
-        ties_accumulate<NS>(d, tau, e, P[e], N[e], cnt[e]);
+    for (int e = 0; e < ties::EPT; ++e) {
+        uint32_t np = 0u, nn = 0u;
+        ties_accumulate<NS>(d, tau, e, P[e], N[e], np, nn);
+        cnt[e] += np + (nn << 16);
+    }
 }
 
 // MULTI = false: K <= GS, every selected expert is trimmed in one group.
@@ -657,6 +673,8 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
     constexpr int E = CPT * V;
     static_assert(E == EPT, "elements per thread and expert");
     __shared__ TiesSmem sm;
+    if (threadIdx.x < 8)  // read after the trim's barriers
+        sm.rd[threadIdx.x] = ties_divisor((int)threadIdx.x);
     const int64_t b = blockIdx.x;
     const uint32_t g = uniform_u32(src.block(b));
     const uint64_t off = boff[g];
@@ -684,11 +702,11 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
         if (ns != 0)
             ties_trim_group<DT, CPT>(sm, src, b, off, n, k, m, 0, x0, d, tau);
         switch (ns) {
-        case 0: ties_finish_single<DT, 0>(d, tau, x0, lambda, po, nch); break;
-        case 1: ties_finish_single<DT, 1>(d, tau, x0, lambda, po, nch); break;
-        case 2: ties_finish_single<DT, 2>(d, tau, x0, lambda, po, nch); break;
-        case 3: ties_finish_single<DT, 3>(d, tau, x0, lambda, po, nch); break;
-        default: ties_finish_single<DT, 4>(d, tau, x0, lambda, po, nch); break;
+        case 0: ties_finish_single<DT, 0>(d, tau, x0, lambda, sm.rd, po, nch); break;
+        case 1: ties_finish_single<DT, 1>(d, tau, x0, lambda, sm.rd, po, nch); break;
+        case 2: ties_finish_single<DT, 2>(d, tau, x0, lambda, sm.rd, po, nch); break;
+        case 3: ties_finish_single<DT, 3>(d, tau, x0, lambda, sm.rd, po, nch); break;
+        default: ties_finish_single<DT, 4>(d, tau, x0, lambda, sm.rd, po, nch); break;
         }
     } else {
         float P[E], N[E];
@@ -728,7 +746,7 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
                 Nq[v] = N[q * V + v];
                 cq[v] = cnt[q * V + v];
             }
-            ties_store_chunk<DT, false>(Pq, Nq, cq, &x0[q * V], lambda, po + q * NT + t, q * NT + t < (int)nch);
+            ties_store_chunk<DT>(Pq, Nq, cq, &x0[q * V], lambda, po + q * NT + t, q * NT + t < (int)nch);
         }
     }
 }

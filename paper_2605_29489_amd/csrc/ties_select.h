@@ -4,11 +4,12 @@
 //
 // Magnitudes are compared as fp32 bit patterns with the sign cleared (the
 // same order as the values, since they are not negative).  The window is the
-// four binades below the binade of the block maximum, keyed by |d| >> KS
-// (exponent and MB mantissa bits): NBIN bins, each with NC copies so that
-// lanes holding equal values (frequent in bf16 deltas) update different
-// words.  The low half of a counter counts the bin's elements, the high half
-// the ones above the bin's floor (low bits not zero).
+// binade of the block maximum and the three binades below it, keyed by
+// |d| >> KS (exponent and MB mantissa bits): NBIN bins, each with NC copies
+// so that lanes holding equal values (frequent in bf16 deltas) update
+// different words.  No magnitude lies above the window.  The low half of a
+// counter counts the bin's elements, the high half the ones above the bin's
+// floor (low bits not zero).
 #pragma once
 
 #include "device_common.h"
@@ -199,12 +200,20 @@ __device__ inline void window_add(char* row, uint32_t bits, uint32_t koff)
     }
 }
 
+// Key of bin 0 of the window anchored at the block maximum's pattern: the
+// top bin holds the last key of the maximum's binade.
+__device__ inline int window_base(uint32_t bmax)
+{
+    using namespace ties;
+    return (int)((bmax >> 23) << MB) + (1 << MB) - NBIN;
+}
+
 // Byte offset term of window_add for the lane's copy, given the block
 // maximum's pattern: key kk goes to ((kk - wb) * NC + (lane % NC)) * 4.
 __device__ inline uint32_t window_koff(uint32_t bmax, int lane, int* wb_out)
 {
     using namespace ties;
-    const int wb = (int)((bmax >> 23) << MB) - NBIN;  // key of bin 0
+    const int wb = window_base(bmax);
     *wb_out = wb;
     return (uint32_t)(lane & (NC - 1)) * 4u - (uint32_t)wb * (uint32_t)(4 * NC);
 }
@@ -230,42 +239,32 @@ __device__ inline uint32_t wave_kth_largest(uint32_t* __restrict__ h, const floa
     wave_lds_sync();
     int wb;
     const uint32_t koff = window_koff(bmax, lane, &wb);
-    const float topf = __uint_as_float((bmax >> 23) << 23);  // first value of the maximum's binade
-    uint32_t ntop = 0u;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
+    for (int e = 0; e < E; ++e)
         window_add(reinterpret_cast<char*>(h), __float_as_uint(d[e]), koff);
-        ntop += (uint32_t)__popcll(__ballot(fabsf(d[e]) >= topf));
-    }
     wave_lds_sync();
-    bool radix = ntop >= k;  // the k-th largest lies in the top binade
-    if (!radix) {
-        const Cut c = wave_find_from_top<NC>(h, NBIN - 1, k - ntop, lane);
-        if (!c.found) {
-            radix = true;  // below the window
-        } else if (c.aux < c.rank) {
+    const Cut c = wave_find_from_top<NC>(h, NBIN - 1, k, lane);
+    if (c.found) {  // else the k-th largest lies below the window
+        if (c.aux < c.rank)
             return (uint32_t)(wb + (int)c.bin) << KS;  // the rank-th largest of the bin is its floor
-        } else {
-            // list the bin's values, then fix their low bits one at a time
-            const uint32_t key = (uint32_t)(wb + (int)c.bin);
-            wave_lds_sync();
-            uint32_t n = 0u;
+        // list the bin's values, then fix their low bits one at a time
+        const uint32_t key = (uint32_t)(wb + (int)c.bin);
+        wave_lds_sync();
+        uint32_t n = 0u;
 #pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const uint32_t mg = __float_as_uint(d[e]) & 0x7fffffffu;
-                const bool in = (mg >> KS) == key;
-                const unsigned long long bal = __ballot(in);
-                const uint32_t pos =
-                    n + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-                if (in && pos < (uint32_t)NB)
-                    h[pos] = mg;
-                n += (uint32_t)__popcll(bal);
-            }
-            wave_lds_sync();
-            if (n <= (uint32_t)NB)
-                return wave_select_list(h, n, key, c.rank, lane);
-            radix = true;
+        for (int e = 0; e < E; ++e) {
+            const uint32_t mg = __float_as_uint(d[e]) & 0x7fffffffu;
+            const bool in = (mg >> KS) == key;
+            const unsigned long long bal = __ballot(in);
+            const uint32_t pos =
+                n + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+            if (in && pos < (uint32_t)NB)
+                h[pos] = mg;
+            n += (uint32_t)__popcll(bal);
         }
+        wave_lds_sync();
+        if (n <= (uint32_t)NB)
+            return wave_select_list(h, n, key, c.rank, lane);
     }
     // exact radix select over all values: bits 30..20, 19..9, 8..0
     uint32_t pref = 0u, r = k;
