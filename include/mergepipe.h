@@ -111,8 +111,8 @@ int mp_index_blocks(const mp_layout* layout, const void* base,
  * for every unit, the per-unit trim threshold
  *   tau[g*K + i] = fp32 bit pattern of the k-th largest |d| of the block
  *                  (multiplicity counted), k = min(n, ceil(density * n)) in
- *                  fp64, n = the block length; the pattern of +infinity if
- *                  k = 0,
+ *                  fp64, n = the block length; all ones (a NaN pattern,
+ *                  which no magnitude meets: nothing is kept) if k = 0,
  * and, when sumsq is not NULL, the sum of squares of mp_index_blocks (the
  * same bits) in the same pass.  The threshold depends on the unit and the
  * density only, never on an access mask, so one catalog pass serves TIES

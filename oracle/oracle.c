@@ -363,12 +363,12 @@ static int desc_float(const void* pa, const void* pb)
 
 /* The trim threshold of one (expert, block) unit: m[0..n-1] holds |d|; the
  * result is the fp32 bit pattern of the k-th largest of them (multiplicity
- * counted), or the pattern of +infinity when k = 0 (nothing is kept).  m is
- * sorted in place. */
+ * counted), or all ones when k = 0: a NaN pattern, which no magnitude meets,
+ * so nothing is kept (an infinite delta included).  m is sorted in place. */
 static uint32_t kth_largest_pattern(float* m, int64_t n, int64_t k)
 {
     if (k == 0)
-        return 0x7f800000u;
+        return 0xffffffffu;
     qsort(m, (size_t)n, sizeof(float), desc_float);
     float tau = m[k - 1];
     uint32_t u;

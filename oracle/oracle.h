@@ -59,7 +59,8 @@ int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
 
 /* TIES trim thresholds per unit (mask-independent): tau[b*K + i] = fp32
  * pattern of the k-th largest |d| of unit (block b, expert i), k =
- * orc_ties_k(len, density); +infinity's pattern when k = 0. */
+ * orc_ties_k(len, density); all ones (a NaN pattern: nothing kept) when
+ * k = 0. */
 int orc_ties_thresholds(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
                         const void* base, const void* const* experts, int32_t K, double density,
                         uint32_t* tau);

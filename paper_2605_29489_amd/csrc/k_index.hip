@@ -79,30 +79,31 @@ __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, Ex
 // Catalog statistics for TIES: per unit, the sum of squares of k_index
 // (same order, same bits; optional) and the trim threshold, the fp32
 // pattern of the k-th largest |d| of the (expert, block) unit for a keep
-// density (+infinity's pattern when k = 0).  The threshold depends on the
-// unit and the density only, never on an access mask, so merges at any
-// budget can reuse it.  Wave w takes experts w, w+4, ... of the block: it
-// holds the whole block in registers (64 deltas per lane; lane l owns
-// chunks l, l+64, ...) and selects with its own LDS row, so the workgroup
+// density (all ones when k = 0: a NaN pattern, which keeps nothing).  The
+// threshold depends on the unit and the density only, never on an access
+// mask, so merges at any budget can reuse it.  The base block is staged in
+// LDS once; wave w takes experts w, w+4, ... of the block: it holds the
+// whole unit's deltas in registers (64 per lane; lane l owns chunks l, l+64,
+// ...) and selects with its own LDS row, so after the staging the workgroup
 // never synchronises.
 #ifndef MP_CAT_WAVES
 #define MP_CAT_WAVES 3
 #endif
 template <int DT>
-__global__ __launch_bounds__(256, MP_CAT_WAVES) void k_index_ties(const void* __restrict__ base, ExpertPtrs ex,
-                                                                  int K, const uint64_t* __restrict__ boff,
-                                                                  const uint32_t* __restrict__ blen,
-                                                                  uint32_t n_full, uint32_t k_full, double density,
-                                                                  float* __restrict__ sumsq,
-                                                                  uint32_t* __restrict__ tau)
+__global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 2) void k_index_ties(
+    const void* __restrict__ base, ExpertPtrs ex, int K, const uint64_t* __restrict__ boff,
+    const uint32_t* __restrict__ blen, uint32_t n_full, uint32_t k_full, double density,
+    float* __restrict__ sumsq, uint32_t* __restrict__ tau)
 {
     constexpr int V = Fmt<DT>::V;
     constexpr int R = kTiesMaxBlock / 64 / V;  // chunk rows per lane
     constexpr int E = R * V;                   // deltas per lane
     __shared__ uint32_t rows[4][ties::NB];
+    __shared__ uint4 xb[R * 64];  // the base block's chunks (zeros past its end)
     const int64_t g = blockIdx.x;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = t >> 6;
     const uint64_t off = boff[g];
     const uint32_t n = blen[g];
     const uint32_t nch = n / V;
@@ -112,25 +113,26 @@ __global__ __launch_bounds__(256, MP_CAT_WAVES) void k_index_ties(const void* __
         k = (kk >= (double)n) ? n : (uint32_t)kk;
     }
     const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
+#pragma unroll
+    for (int q = 0; q < R / 4; ++q) {
+        const uint32_t c = (uint32_t)(q * 256 + t);
+        xb[c] = (c < nch) ? b[c] : make_uint4(0u, 0u, 0u, 0u);
+    }
+    __syncthreads();
     for (int i = wave; i < K; i += 4) {
         const uint4* e = chunk_ptr(ex.p[i], off, Fmt<DT>::esize);
-        uint4 xb[R], xe[R];
+        uint4 xe[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const uint32_t c = (uint32_t)(r * 64 + lane);
-            xb[r] = make_uint4(0u, 0u, 0u, 0u);
-            xe[r] = make_uint4(0u, 0u, 0u, 0u);
-            if (c < nch) {
-                xb[r] = b[c];
-                xe[r] = e[c];
-            }
+            xe[r] = (c < nch) ? e[c] : make_uint4(0u, 0u, 0u, 0u);
         }
         float d[E];
         float p = 0.0f;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             float fb[V], fe[V];
-            Fmt<DT>::unpack(xb[r], fb);
+            Fmt<DT>::unpack(xb[r * 64 + lane], fb);
             Fmt<DT>::unpack(xe[r], fe);
 #pragma unroll
             for (int q = 0; q < V; ++q) {
@@ -141,11 +143,11 @@ __global__ __launch_bounds__(256, MP_CAT_WAVES) void k_index_ties(const void* __
 #pragma unroll
         for (int s = 32; s >= 1; s >>= 1)
             p = p + __shfl_xor(p, s);
-        const uint32_t t = (k == 0u) ? 0x7f800000u : wave_kth_largest<E>(rows[wave], d, k, lane);
+        const uint32_t th = (k == 0u) ? 0xffffffffu : wave_kth_largest<E>(rows[wave], d, k, lane);
         if (lane == 0) {
             if (sumsq != nullptr)
                 sumsq[g * K + i] = p;
-            tau[g * K + i] = t;
+            tau[g * K + i] = th;
         }
     }
 }

@@ -40,6 +40,14 @@ __device__ inline void count_expert_bytes(unsigned long long* ctr, uint32_t m, u
         atomicAdd(&ctr[blockIdx.x & 255u], (unsigned long long)__popc(m) * n * (unsigned long long)es);
 }
 
+// Divisors for the mean of at most four agreeing entries: {den, fl32(1/den)}
+// at index den (1..4; the others are unused and hold {1, 1}).
+__device__ inline float2 ties_divisor(int i)
+{
+    const float r = (i == 2) ? 0.5f : (i == 3) ? 0x1.555556p-2f : (i == 4) ? 0.25f : 1.0f;
+    return make_float2((i >= 2 && i <= 4) ? (float)i : 1.0f, r);
+}
+
 // ------------------------------------------------------------ elementwise family
 enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2, M_TIES_TAU = 3 };
 
@@ -64,8 +72,18 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
     constexpr bool DARE = MODE == M_DARE_LIN || MODE == M_DARE_SIGN;
     constexpr bool SIGN = MODE == M_DARE_SIGN || MODE == M_TIES_TAU;
     constexpr int E = CPT * V;
+    // experts loaded together: the sign-elect state leaves room for the raw
+    // chunks of two experts only with fp32 data or with DARE's generator
+    constexpr int EG = (SIGN && (DT == 0 || MODE == M_DARE_SIGN)) ? 2 : 4;
     const int64_t b = blockIdx.x;
     const int t = threadIdx.x;
+    // TIES with at most four experts: divisors {den, 1/den} of the mean
+    __shared__ float2 rd[8];
+    if (MODE == M_TIES_TAU) {
+        if (t < 8)
+            rd[t] = ties_divisor(t);
+        __syncthreads();
+    }
     const uint32_t g = src.block(b);
     const uint64_t off = boff[g];
     const uint32_t n = blen[g];
@@ -94,21 +112,24 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
             Fmt<DT>::unpack(raw, &x0[q * V]);
         }
         float acc[E], ps[E], ns[E];
-        uint32_t cpn[E];  // sign-elect: positive count in the low, negative in the high half
+        // sign-elect counts: DARE packs positive (low) and negative (high
+        // half) in cpn; TIES keeps them apart in cpn and cng
+        uint32_t cpn[E], cng[E];
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             acc[e] = 0.0f;
             ps[e] = 0.0f;
             ns[e] = 0.0f;
             cpn[e] = 0u;
+            cng[e] = 0u;
         }
         uint32_t mm = m;
         int rank = 0;
         while (mm) {
-            int idx[4];
+            int idx[EG];
             int cnt = 0;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < EG; ++j) {
                 idx[j] = -1;
                 if (mm) {
                     idx[j] = __builtin_ctz(mm);
@@ -116,9 +137,9 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
                     ++cnt;
                 }
             }
-            uint4 raw[4][CPT];
+            uint4 raw[EG][CPT];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < EG; ++j) {
                 if (j < cnt) {
                     const uint4* pe = src.expert(idx[j], rank + j, b, off, n, ES);
 #pragma unroll
@@ -128,7 +149,7 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
                 }
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < EG; ++j) {
                 if (j >= cnt)
                     break;
                 const int i = idx[j];
@@ -164,12 +185,15 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
                         const float d = x[v] - x0[e];
                         if (MODE == M_AVG) {
                             acc[e] = fmaf(alpha.v[i], d, acc[e]);
+                        } else if (MODE == M_TIES_TAU) {
+                            // d >= tau keeps a positive delta, -d >= tau a negative one
+                            const bool kp = d >= tauf, kn = -d >= tauf;
+                            ps[e] = ps[e] + (kp ? d : 0.0f);
+                            ns[e] = ns[e] + (kn ? d : 0.0f);
+                            cpn[e] += kp ? 1u : 0u;
+                            cng[e] += kn ? 1u : 0u;
                         } else {
-                            float tv;
-                            if (MODE == M_TIES_TAU)
-                                tv = (fabsf(d) >= tauf) ? d : 0.0f;
-                            else
-                                tv = (word[v] < drop_T) ? 0.0f : d * scale;
+                            const float tv = (word[v] < drop_T) ? 0.0f : d * scale;
                             if (MODE == M_DARE_LIN) {
                                 acc[e] = fmaf(alpha.v[i], tv, acc[e]);
                             } else {
@@ -184,7 +208,54 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
             }
             rank += cnt;
         }
-        if (SIGN) {
+        if (MODE == M_TIES_TAU) {
+            // elect the sign of the larger signed mass; mean of the agreeing
+            // entries: with at most four experts by the divisor table and one
+            // residual step (correctly rounded for a finite mass, as in
+            // ties_store_small; a wave with an infinite mass divides),
+            // otherwise as below
+            uint32_t den[E];
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const bool up = ps[e] > -ns[e];
+                const bool dn = ps[e] < -ns[e];
+                acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);
+                den[e] = up ? cpn[e] : (dn ? cng[e] : 1u);
+            }
+            if (K <= 4) {
+                bool bad = false;
+                float q[E];
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const float2 c = rd[den[e]];
+                    const float q0 = acc[e] * c.y;
+                    q[e] = fmaf(fmaf(-c.x, q0, acc[e]), c.y, q0);
+                    bad |= q[e] != q[e];
+                }
+                if (__any(bad)) {
+#pragma unroll
+                    for (int e = 0; e < E; ++e)
+                        q[e] = acc[e] / (float)den[e];
+                }
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    acc[e] = q[e];
+            } else {
+                bool odd = false;
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    odd |= (den[e] & (den[e] - 1u)) != 0u;
+                if (__any(odd)) {
+#pragma unroll
+                    for (int e = 0; e < E; ++e)
+                        acc[e] = acc[e] / (float)den[e];
+                } else {
+#pragma unroll
+                    for (int e = 0; e < E; ++e)
+                        acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
+                }
+            }
+        } else if (SIGN) {
             // elect the sign of the larger signed mass; mean of the agreeing
             // entries (a count that is a power of two divides by exact scaling,
             // correctly rounded as the quotient; otherwise IEEE division)
@@ -315,35 +386,37 @@ __device__ inline uint32_t block_radix_select(TiesSmem& sm, int j, const float (
     return max(pref, 1u);
 }
 
-// Loads and trims up to GS selected experts of one block (the set bits of
-// gm, in increasing expert order; rank0 = rank of the first among all the
-// block's selected experts).  Leaves the deltas in d and the thresholds in
-// tau (wave-uniform patterns).  Every thread of the workgroup calls it.
+// Issues the loads of up to GS selected experts of one block (the set bits
+// of gm, in increasing expert order; rank0 = rank of the first among all the
+// block's selected experts) into raw.
 template <int DT, int CPT, class Src>
-__device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, uint64_t off, uint32_t n,
-                                       uint32_t k, uint32_t gm, int rank0, const float (&x0)[CPT * Fmt<DT>::V],
-                                       float (&d)[ties::GS][CPT * Fmt<DT>::V], uint32_t (&tau)[ties::GS])
+__device__ inline void ties_load_group(const Src& src, int64_t b, uint64_t off, uint32_t n, uint32_t gm, int rank0,
+                                       uint4 (&raw)[ties::GS][CPT])
 {
-    using namespace ties;
-    constexpr int V = Fmt<DT>::V, ES = Fmt<DT>::esize, E = CPT * V;
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    constexpr int ES = Fmt<DT>::esize;
     const int ns = __popc(gm);
-    const uint32_t nch = n / V;
-
-    uint4 raw[GS][CPT];
-    {
-        uint32_t mm = gm;
+    const uint32_t nch = n / Fmt<DT>::V;
+    uint32_t mm = gm;
 #pragma unroll
-        for (int j = 0; j < GS; ++j) {
-            if (j < ns) {
-                const int i = __builtin_ctz(mm);
-                mm &= mm - 1u;
-                load_chunks<DT, NT, CPT>(src.expert(i, rank0 + j, b, off, n, ES), nch, raw[j]);
-            }
+    for (int j = 0; j < ties::GS; ++j) {
+        if (j < ns) {
+            const int i = __builtin_ctz(mm);
+            mm &= mm - 1u;
+            load_chunks<DT, ties::NT, CPT>(src.expert(i, rank0 + j, b, off, n, ES), nch, raw[j]);
         }
     }
-    // rows of the slots in use start at zero (the previous group's readers
-    // passed a barrier since)
+}
+
+// Phase A of a trim group: clears the histogram rows of the ns slots in use
+// (their previous readers passed a barrier since), forms the deltas and
+// publishes the wave maxima of |d|.
+template <int DT, int CPT>
+__device__ inline void ties_deltas(TiesSmem& sm, const uint4 (&raw)[ties::GS][CPT], int ns,
+                                   const float (&x0)[CPT * Fmt<DT>::V], float (&d)[ties::GS][CPT * Fmt<DT>::V])
+{
+    using namespace ties;
+    constexpr int V = Fmt<DT>::V;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
 #pragma unroll
     for (int j = 0; j < GS; ++j) {
         if (j < ns) {
@@ -352,7 +425,6 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
                 *reinterpret_cast<uint4*>(&sm.h[j][4 * (q * NT + t)]) = make_uint4(0u, 0u, 0u, 0u);
         }
     }
-    // ---- A: deltas and block maxima
 #pragma unroll
     for (int j = 0; j < GS; ++j) {
         if (j < ns) {
@@ -373,6 +445,18 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
                 sm.wmax[j][wave] = w;
         }
     }
+}
+
+// Phases B-D of a trim group whose deltas are in d and whose wave maxima
+// were published by ties_deltas: leaves the thresholds in tau (wave-uniform
+// patterns) and returns the largest |d| pattern of the group's slots.  Every
+// thread of the workgroup calls it.
+template <int E>
+__device__ inline uint32_t ties_select_group(TiesSmem& sm, uint32_t n, uint32_t k, int ns,
+                                             const float (&d)[ties::GS][E], uint32_t (&tau)[ties::GS])
+{
+    using namespace ties;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     __syncthreads();
     // ---- B: window histograms
     uint32_t bmax[GS];
@@ -487,13 +571,35 @@ __device__ inline void ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, 
 #pragma unroll
     for (int j = 0; j < GS; ++j)
         tau[j] = (j < ns) ? uniform_u32(sm.st[j][1]) : 0xffffffffu;
+    uint32_t top = 0u;
+#pragma unroll
+    for (int j = 0; j < GS; ++j)
+        top = max(top, bmax[j]);
+    return top;
+}
+
+// Loads and trims up to GS selected experts of one block (see
+// ties_load_group): leaves the deltas in d and the thresholds in tau, and
+// returns the largest |d| pattern of the group.
+template <int DT, int CPT, class Src>
+__device__ inline uint32_t ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, uint64_t off, uint32_t n,
+                                       uint32_t k, uint32_t gm, int rank0, const float (&x0)[CPT * Fmt<DT>::V],
+                                       float (&d)[ties::GS][CPT * Fmt<DT>::V], uint32_t (&tau)[ties::GS])
+{
+    uint4 raw[ties::GS][CPT];
+    ties_load_group<DT, CPT>(src, b, off, n, gm, rank0, raw);
+    const int ns = __popc(gm);
+    ties_deltas<DT, CPT>(sm, raw, ns, x0, d);
+    return ties_select_group<CPT * Fmt<DT>::V>(sm, n, k, ns, d, tau);
 }
 
 // Keep test and the running signed masses of element e over NS slots, with
 // the kept counts np (positive) and nn (negative).  tau is at least the
 // smallest positive pattern, so d >= tau keeps a positive delta and
-// -d >= tau a negative one; a zero or NaN delta is never kept.
-template <int NS>
+// -d >= tau a negative one; a zero or NaN delta is never kept.  FRESH: the
+// masses and counts start here (+0 + x is x for every term, which is +0 or
+// a nonzero delta, so the first term is assigned).
+template <int NS, bool FRESH>
 __device__ inline void ties_accumulate(const float (&d)[ties::GS][ties::EPT], const uint32_t (&tau)[ties::GS], int e,
                                        float& P, float& N, uint32_t& np, uint32_t& nn)
 {
@@ -503,19 +609,18 @@ __device__ inline void ties_accumulate(const float (&d)[ties::GS][ties::EPT], co
         const float t = __uint_as_float(tau[j]);
         const bool kp = dj >= t;
         const bool kn = -dj >= t;
-        P = P + (kp ? dj : 0.0f);
-        N = N + (kn ? dj : 0.0f);
-        np += kp ? 1u : 0u;
-        nn += kn ? 1u : 0u;
+        if (FRESH && j == 0) {
+            P = kp ? dj : 0.0f;
+            N = kn ? dj : 0.0f;
+            np = kp ? 1u : 0u;
+            nn = kn ? 1u : 0u;
+        } else {
+            P = P + (kp ? dj : 0.0f);
+            N = N + (kn ? dj : 0.0f);
+            np += kp ? 1u : 0u;
+            nn += kn ? 1u : 0u;
+        }
     }
-}
-
-// Divisors for the mean of at most four agreeing entries: {den, fl32(1/den)}
-// at index den (1..4; the others are unused and hold {1, 1}).
-__device__ inline float2 ties_divisor(int i)
-{
-    const float r = (i == 2) ? 0.5f : (i == 3) ? 0x1.555556p-2f : (i == 4) ? 0.25f : 1.0f;
-    return make_float2((i >= 2 && i <= 4) ? (float)i : 1.0f, r);
 }
 
 // Sign election (the sign of the larger of the positive and negative kept
@@ -524,11 +629,14 @@ __device__ inline float2 ties_divisor(int i)
 // + x0, rounded once, is stored.  With at most two agreeing entries the mean
 // is the entry or an exact halving.  Otherwise q = mean * fl32(1/den) and one
 // residual step q + fl32(mean - den*q) * fl32(1/den) give the correctly
-// rounded quotient: for den = 1, 2, 4 the product is already correctly
-// rounded and the residual term adds exactly nothing; for den = 3 this is
-// Markstein's correction, checked against IEEE division on all 2^32 fp32
-// patterns (only -0 comes out as +0, and an elected mass is never zero).
-template <int DT, int NS>
+// rounded quotient of a finite mass: for den = 1, 2, 4 the product is
+// already correctly rounded and the residual term adds exactly nothing; for
+// den = 3 this is Markstein's correction, checked against IEEE division on
+// all 2^32 fp32 patterns (only -0 comes out as +0, and an elected mass is
+// never zero).  IEEE: the block holds a |d| of at least 2^125, so a mass of
+// up to four terms may be infinite (the residual step would make it NaN);
+// such blocks divide.
+template <int DT, int NS, bool IEEE>
 __device__ inline void ties_store_small(const float (&P)[Fmt<DT>::V], const float (&N)[Fmt<DT>::V],
                                         const uint32_t (&np)[Fmt<DT>::V], const uint32_t (&nn)[Fmt<DT>::V],
                                         const float* x0, float lambda, const float2* rd,
@@ -545,6 +653,8 @@ __device__ inline void ties_store_small(const float (&P)[Fmt<DT>::V], const floa
         float q;
         if (NS <= 2) {
             q = (den == 2u) ? num * 0.5f : num;
+        } else if (IEEE) {
+            q = num / (float)den;
         } else {
             const float2 c = rd[den];
             const float q0 = num * c.y;
@@ -595,8 +705,8 @@ __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const floa
 }
 
 // All selected experts trimmed in one group: accumulate and store chunk by
-// chunk.
-template <int DT, int NS>
+// chunk (IEEE as for ties_store_small).
+template <int DT, int NS, bool IEEE = false>
 __device__ inline void ties_finish_single(const float (&d)[ties::GS][ties::EPT], const uint32_t (&tau)[ties::GS],
                                           const float (&x0)[ties::EPT], float lambda, const float2* rd,
                                           uint4* __restrict__ po, uint32_t nch)
@@ -626,15 +736,10 @@ __device__ inline void ties_finish_single(const float (&d)[ties::GS][ties::EPT],
         float P[V], N[V];
         uint32_t np[V], nn[V];
 #pragma unroll
-        for (int v = 0; v < V; ++v) {
-            P[v] = 0.0f;
-            N[v] = 0.0f;
-            np[v] = 0u;
-            nn[v] = 0u;
-            ties_accumulate<NS>(d, tau, q * V + v, P[v], N[v], np[v], nn[v]);
-        }
-        ties_store_small<DT, NS>(P, N, np, nn, &x0[q * V], lambda, rd, po + q * ties::NT + t,
-                                 q * ties::NT + t < (int)nch);
+        for (int v = 0; v < V; ++v)
+            ties_accumulate<NS, true>(d, tau, q * V + v, P[v], N[v], np[v], nn[v]);
+        ties_store_small<DT, NS, IEEE>(P, N, np, nn, &x0[q * V], lambda, rd, po + q * ties::NT + t,
+                                       q * ties::NT + t < (int)nch);
     }
 }
 
@@ -647,7 +752,7 @@ __device__ inline void ties_accumulate_all(const float (&d)[ties::GS][ties::EPT]
 #pragma unroll
     for (int e = 0; e < ties::EPT; ++e) {
         uint32_t np = 0u, nn = 0u;
-        ties_accumulate<NS>(d, tau, e, P[e], N[e], np, nn);
+        ties_accumulate<NS, false>(d, tau, e, P[e], N[e], np, nn);
         cnt[e] += np + (nn << 16);
     }
 }
@@ -699,14 +804,26 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
     uint32_t tau[GS];
     if (!MULTI) {
         const int ns = __popc(m);
+        uint32_t top = 0u;
         if (ns != 0)
-            ties_trim_group<DT, CPT>(sm, src, b, off, n, k, m, 0, x0, d, tau);
+            top = ties_trim_group<DT, CPT>(sm, src, b, off, n, k, m, 0, x0, d, tau);
+        const bool big = top >= 0x7e000000u;  // some |d| >= 2^125: masses may overflow
         switch (ns) {
         case 0: ties_finish_single<DT, 0>(d, tau, x0, lambda, sm.rd, po, nch); break;
         case 1: ties_finish_single<DT, 1>(d, tau, x0, lambda, sm.rd, po, nch); break;
         case 2: ties_finish_single<DT, 2>(d, tau, x0, lambda, sm.rd, po, nch); break;
-        case 3: ties_finish_single<DT, 3>(d, tau, x0, lambda, sm.rd, po, nch); break;
-        default: ties_finish_single<DT, 4>(d, tau, x0, lambda, sm.rd, po, nch); break;
+        case 3:
+            if (big)
+                ties_finish_single<DT, 3, true>(d, tau, x0, lambda, sm.rd, po, nch);
+            else
+                ties_finish_single<DT, 3>(d, tau, x0, lambda, sm.rd, po, nch);
+            break;
+        default:
+            if (big)
+                ties_finish_single<DT, 4, true>(d, tau, x0, lambda, sm.rd, po, nch);
+            else
+                ties_finish_single<DT, 4>(d, tau, x0, lambda, sm.rd, po, nch);
+            break;
         }
     } else {
         float P[E], N[E];

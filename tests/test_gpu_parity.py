@@ -318,6 +318,24 @@ def test_ties_subnormal_deltas(mp):
     _run_all(mp, spec, base, exps, "ties", [1.0], density=0.3, lam=0.5)
 
 
+def test_ties_infinite_masses(mp):
+    # deltas near the top of the fp32 range, some infinite: kept masses of
+    # several entries overflow, and the mean must be IEEE's (inf / count is
+    # inf) in both TIES paths; density 0 keeps none of them
+    spec = _mini_qwen(n_layers=1, K=4)
+    P = sum(int(np.prod(s)) for _, s in spec.tensors)
+    rng = np.random.default_rng(17)
+    base = oracle.round_bf16(rng.normal(0.0, 1e36, P).astype(np.float32))
+    deltas = [np.clip(rng.normal(0.0, s, P), -3e38, 3e38) for s in (1.2e38, 1.5e38, 1.0e38, 1.3e38)]
+    exps = _bf16_family_from_deltas(base, deltas)
+    for i, e in enumerate(exps):
+        e[rng.choice(P, 40, replace=False)] = np.uint16(0x7F80 if i % 2 == 0 else 0xFF80)
+    _say("case infinite masses")
+    _run_all(mp, spec, base, exps, "ties", [1.0, 0.6], density=0.2, lam=1.0)
+    _run_all(mp, spec, base, exps, "ties_tau", [1.0, 0.6], density=0.2, lam=1.0)
+    _run_all(mp, spec, base, exps, "ties_tau", [1.0], density=0.0, lam=1.0)
+
+
 def test_budget_boundaries_exact(mp):
     # budgets at the exact cost of a greedy prefix, one byte below and above
     spec = _mini_qwen(n_layers=1)

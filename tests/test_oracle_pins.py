@@ -460,7 +460,8 @@ def test_ties_trim_keeps_exactly_top_k():
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_ties_thresholds_are_kth_largest_magnitudes(dtype):
     # the per-unit threshold is the k-th largest |d| (numpy partition of the
-    # fp32 deltas), +inf when k = 0; ragged and short blocks included
+    # fp32 deltas), all ones (a NaN pattern: nothing kept) when k = 0; ragged
+    # and short blocks included
     rng = np.random.default_rng(41)
     numel = [4096, 1536, 256, 24, 4096]
     b = oracle.Blocks(numel, 1024)
@@ -482,7 +483,7 @@ def test_ties_thresholds_are_kth_largest_magnitudes(dtype):
             k = min(n, math.ceil(rho * n))
             for i in range(K):
                 m = np.abs((f(exps[i][o:o + n]) - f(base[o:o + n])).astype(np.float32))
-                want = 0x7F800000 if k == 0 else int(np.partition(m, n - k)[n - k].view(np.uint32))
+                want = 0xFFFFFFFF if k == 0 else int(np.partition(m, n - k)[n - k].view(np.uint32))
                 assert int(tau[g, i]) == want
 
 
@@ -502,6 +503,20 @@ def test_ties_with_thresholds_equals_ties():
             want = oracle.merge_ties(b, "bf16", base, exps, mask, rho, lam)
             got = oracle.merge_ties_tau(b, "bf16", base, exps, mask, tau, lam)
             assert np.array_equal(got, want)
+    # infinite deltas: density 0 keeps none of them either way, and a larger
+    # density keeps them and gives an infinite mean
+    b1 = oracle.Blocks([8], 8)
+    x0 = np.zeros(8, np.float32)
+    e1 = np.array([np.inf, -np.inf, 1, -1, 2, 0, 0, 0], np.float32)
+    for rho in (0.0, 0.25, 1.0):
+        tau = oracle.ties_thresholds(b1, "f32", x0, [e1], rho)
+        want = oracle.merge_ties(b1, "f32", x0, [e1], np.ones(1, np.uint32), rho, 1.0)
+        got = oracle.merge_ties_tau(b1, "f32", x0, [e1], np.ones(1, np.uint32), tau, 1.0)
+        assert np.array_equal(got, want)
+        if rho == 0.0:
+            assert np.array_equal(want, x0)
+        else:
+            assert np.isinf(want[0]) and np.isinf(want[1])
 
 
 def test_ties_threshold_ties_all_kept_and_zeros_never():
