@@ -87,10 +87,10 @@ __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, Ex
 // ...) and selects with its own LDS row, so after the staging the workgroup
 // never synchronises.
 #ifndef MP_CAT_WAVES
-#define MP_CAT_WAVES 3
+#define MP_CAT_WAVES 4
 #endif
 template <int DT>
-__global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 2) void k_index_ties(
+__global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
     const void* __restrict__ base, ExpertPtrs ex, int K, const uint64_t* __restrict__ boff,
     const uint32_t* __restrict__ blen, uint32_t n_full, uint32_t k_full, double density,
     float* __restrict__ sumsq, uint32_t* __restrict__ tau)
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 2) void k_index_ties(
             const uint32_t c = (uint32_t)(r * 64 + lane);
             xe[r] = (c < nch) ? e[c] : make_uint4(0u, 0u, 0u, 0u);
         }
-        float d[E];
+        uint32_t mg[E];  // |d| patterns
         float p = 0.0f;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -136,14 +136,15 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 2) void k_index_ties(
             Fmt<DT>::unpack(xe[r], fe);
 #pragma unroll
             for (int q = 0; q < V; ++q) {
-                d[r * V + q] = fe[q] - fb[q];             // padding: 0 - 0
-                p = fmaf(d[r * V + q], d[r * V + q], p);  // + 0 on padding, exact
+                const float d = fe[q] - fb[q];  // padding: 0 - 0
+                p = fmaf(d, d, p);              // + 0 on padding, exact
+                mg[r * V + q] = __float_as_uint(d) & 0x7fffffffu;
             }
         }
 #pragma unroll
         for (int s = 32; s >= 1; s >>= 1)
             p = p + __shfl_xor(p, s);
-        const uint32_t th = (k == 0u) ? 0xffffffffu : wave_kth_largest<E>(rows[wave], d, k, lane);
+        const uint32_t th = (k == 0u) ? 0xffffffffu : wave_kth_largest<E>(rows[wave], mg, k, lane);
         if (lane == 0) {
             if (sumsq != nullptr)
                 sumsq[g * K + i] = p;

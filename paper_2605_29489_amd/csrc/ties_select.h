@@ -218,18 +218,19 @@ __device__ inline uint32_t window_koff(uint32_t bmax, int lane, int* wb_out)
     return (uint32_t)(lane & (NC - 1)) * 4u - (uint32_t)wb * (uint32_t)(4 * NC);
 }
 
-// Wave-level, all lanes: exact k-th largest magnitude pattern (multiplicity
-// counted) of the E values each lane holds in d, 1 <= k <= the number of
-// values that are not padding; padding values are zeros, which cannot
-// change the k largest.  h is a wave-private LDS row of NB words.
+// Wave-level, all lanes: exact k-th largest (multiplicity counted) of the
+// E magnitude patterns (fp32 patterns with the sign cleared) each lane
+// holds in mg, 1 <= k <= the number of values that are not padding; padding
+// values are zeros, which cannot change the k largest.  h is a wave-private
+// LDS row of NB words.
 template <int E>
-__device__ inline uint32_t wave_kth_largest(uint32_t* __restrict__ h, const float (&d)[E], uint32_t k, int lane)
+__device__ inline uint32_t wave_kth_largest(uint32_t* __restrict__ h, const uint32_t (&mg)[E], uint32_t k, int lane)
 {
     using namespace ties;
     uint32_t mx = 0u;
 #pragma unroll
-    for (int e = 0; e < E; ++e)
-        mx = max(mx, __float_as_uint(d[e]) & 0x7fffffffu);
+    for (int e = 0; e < E; e += 2)
+        mx = max(mx, max(mg[e], mg[e + 1]));
     const uint32_t bmax = wave_max_u32(mx);
     if (bmax == 0u)
         return 0u;  // all zero
@@ -241,7 +242,7 @@ __device__ inline uint32_t wave_kth_largest(uint32_t* __restrict__ h, const floa
     const uint32_t koff = window_koff(bmax, lane, &wb);
 #pragma unroll
     for (int e = 0; e < E; ++e)
-        window_add(reinterpret_cast<char*>(h), __float_as_uint(d[e]), koff);
+        window_add(reinterpret_cast<char*>(h), mg[e], koff);
     wave_lds_sync();
     const Cut c = wave_find_from_top<NC>(h, NBIN - 1, k, lane);
     if (c.found) {  // else the k-th largest lies below the window
@@ -253,13 +254,12 @@ __device__ inline uint32_t wave_kth_largest(uint32_t* __restrict__ h, const floa
         uint32_t n = 0u;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const uint32_t mg = __float_as_uint(d[e]) & 0x7fffffffu;
-            const bool in = (mg >> KS) == key;
+            const bool in = (mg[e] >> KS) == key;
             const unsigned long long bal = __ballot(in);
             const uint32_t pos =
                 n + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
             if (in && pos < (uint32_t)NB)
-                h[pos] = mg;
+                h[pos] = mg[e];
             n += (uint32_t)__popcll(bal);
         }
         wave_lds_sync();
@@ -279,10 +279,9 @@ __device__ inline uint32_t wave_kth_largest(uint32_t* __restrict__ h, const floa
         wave_lds_sync();
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const uint32_t mg = __float_as_uint(d[e]) & 0x7fffffffu;
-            const uint32_t hi = (lv == 0) ? 0u : (mg >> (sh + wd));
+            const uint32_t hi = (lv == 0) ? 0u : (mg[e] >> (sh + wd));
             if (hi == pref)
-                atomicAdd(&h[(mg >> sh) & ((1u << wd) - 1u)], 1u);
+                atomicAdd(&h[(mg[e] >> sh) & ((1u << wd) - 1u)], 1u);
         }
         wave_lds_sync();
         const Cut c = wave_find_from_top<1>(h, (1 << wd) - 1, r, lane);
