@@ -7,15 +7,21 @@ embeddings; P = 1,543,714,304 parameters, G = 376,989 blocks of 4096) with
 K = 4 experts, merged with budgeted TIES (keep density 0.2, lambda 1) at
 B = 25%, 50% and 100% of the expert bytes.
 
-One step = index the expert deltas once (per-block squared norms), then for
-each budget: plan (Algorithm 1) + TIES merge.  All inputs are resident in HBM
-before the timed region.  The metric is merged parameters per second (3 P
-per step); effective HBM GB/s and the roofline fraction come from HIP events
-around each kernel-launching call on the stream the kernels run on.
+One step = index the expert deltas once, then for each budget: plan
+(Algorithm 1) + TIES merge.  Two routes compute the same bits:
+  catalog (default): the index pass also stores every unit's TIES trim
+      threshold (mask-independent), and each merge reads it;
+  in-merge: the index pass stores the squared norms only, and each merge
+      finds the thresholds of its selected units itself.
+All inputs are resident in HBM before the timed region.  The metric is
+merged parameters per second (3 P per step); effective HBM GB/s and the
+roofline fraction come from HIP events around each kernel-launching call on
+the stream the kernels run on.  After the timed region the other route's
+merges are timed once for reference.
 
 The CPU baseline is the oracle (test infrastructure) on a bounded sample of
-the same family: every 2nd block, index + plan + TIES at the three budgets,
-on all host cores.
+the same family: every 2nd block, the same route (index, thresholds for the
+catalog route, plan and TIES at the three budgets), on all host cores.
 """
 
 import argparse
@@ -34,8 +40,12 @@ from workloads import CONFIGS  # noqa: E402  (shape tables only; no GPU work at 
 METRIC = "merged params/sec + effective HBM GB/s, budgeted TIES merge at B=25/50/100%"
 HBM_PEAK = 8.0e12  # MI355X published HBM3E bandwidth, bytes/s
 BUDGETS = (0.25, 0.5, 1.0)
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "ties_merge_qwen2.5-1.5b_counters.md")
-KERNEL_SOURCES = ("paper_2605_29489_amd/csrc/k_merge.hip", "paper_2605_29489_amd/csrc/device_common.h")
+TRAFFIC_PROFILES = {
+    "catalog": os.path.join(ROOT, "profiles", "ties_threshold_merge_qwen2.5-1.5b_counters.md"),
+    "in-merge": os.path.join(ROOT, "profiles", "ties_merge_qwen2.5-1.5b_counters.md"),
+}
+KERNEL_SOURCES = ("paper_2605_29489_amd/csrc/k_merge.hip", "paper_2605_29489_amd/csrc/device_common.h",
+                  "paper_2605_29489_amd/csrc/ties_select.h")
 
 
 def log(*a):
@@ -50,13 +60,15 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic():
-    """HBM bytes per TIES launch from the committed counter profile, or None
-    if it is missing or was taken on a different kernel source."""
-    if not os.path.exists(TRAFFIC_PROFILE):
+def stored_traffic(route):
+    """HBM bytes per merge launch of the route from the committed counter
+    profile, or None if it is missing or was taken on a different kernel
+    source."""
+    path = TRAFFIC_PROFILES[route]
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_PROFILE):
+    for line in open(path):
         if ":" in line and line.startswith("- "):
             k, v = line[2:].split(":", 1)
             kv[k.strip()] = v.strip().strip("`")
@@ -68,7 +80,7 @@ def stored_traffic():
         return None
 
 
-def cpu_baseline(spec, base, exps, blocks_stride=8):
+def cpu_baseline(spec, base, exps, route, blocks_stride=8):
     """Time the oracle on every `blocks_stride`-th block (bounded sample)."""
     import numpy as np
     import torch
@@ -92,9 +104,13 @@ def cpu_baseline(spec, base, exps, blocks_stride=8):
     full = nparams * 2 * K
     t0 = time.perf_counter()
     S = oracle.index(blk, "bf16", b_np, e_np, doff=doff, ids=ids).reshape(-1)
+    tau = oracle.ties_thresholds(blk, "bf16", b_np, e_np, 0.2, ids=ids, doff=doff) if route == "catalog" else None
     for f in BUDGETS:
         mask, _ = oracle.plan(sub, "bf16", K, S, [1.0] * K, int(f * full))
-        oracle.merge_ties(blk, "bf16", b_np, e_np, mask, 0.2, 1.0, ids=ids, doff=doff)
+        if route == "catalog":
+            oracle.merge_ties_tau(blk, "bf16", b_np, e_np, mask, tau, 1.0, ids=ids, doff=doff)
+        else:
+            oracle.merge_ties(blk, "bf16", b_np, e_np, mask, 0.2, 1.0, ids=ids, doff=doff)
     dt = time.perf_counter() - t0
     return {
         "value": 3 * nparams / dt,
@@ -102,7 +118,8 @@ def cpu_baseline(spec, base, exps, blocks_stride=8):
         "cores": oracle.num_threads(),
         "kind": "oracle",
         "sample": f"every {blocks_stride}th block ({len(ids)} blocks, {nparams} params, all {K} experts): "
-                  f"index + plan + TIES at B=25/50/100% of the sample's expert bytes; {dt:.2f} s",
+                  f"index{' + thresholds' if route == 'catalog' else ''} + plan + TIES at B=25/50/100% "
+                  f"of the sample's expert bytes; {dt:.2f} s",
     }
 
 
@@ -218,6 +235,8 @@ def main():
                     help="the headline (default) or one of the other workload shapes")
     ap.add_argument("--layers", type=int, default=None,
                     help="other workloads: keep only this many transformer layers (host memory)")
+    ap.add_argument("--ties", default="catalog", choices=("catalog", "in-merge"),
+                    help="where the TIES trim thresholds are found: in the index pass (catalog) or in each merge")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="after the timed region, run the AVG merge once with an empty mask: a plain copy "
                          "of the base (reads 2P + 4G bytes, writes 2P) for scaling hardware byte counters")
@@ -246,7 +265,9 @@ def main():
     base, exps = make_family_device(spec, K=K, seed=0, device="cuda")
     torch.cuda.synchronize()
     sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
+    tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
     masks = [torch.empty(G, dtype=torch.int32, device="cuda") for _ in BUDGETS]
+    catalog = args.ties == "catalog"
     out = torch.empty_like(base)
     full = P * 2 * K
     budgets = [int(f * full) for f in BUDGETS]
@@ -257,7 +278,10 @@ def main():
     def step(rec):
         e_i0, e_i1 = ev(), ev()
         e_i0.record(stream)
-        mp.mp_index_blocks(L, base, exps, sumsq, stream=stream)
+        if catalog:
+            mp.mp_index_ties(L, base, exps, 0.2, tau, sumsq=sumsq, stream=stream)
+        else:
+            mp.mp_index_blocks(L, base, exps, sumsq, stream=stream)
         e_i1.record(stream)
         stats = []
         plan_ev = []
@@ -271,7 +295,10 @@ def main():
         for m in masks:
             a, b = ev(), ev()
             a.record(stream)
-            mp.mp_merge_ties(L, base, exps, m, 0.2, 1.0, out, stream=stream)
+            if catalog:
+                mp.mp_merge_ties_tau(L, base, exps, m, tau, 1.0, out, stream=stream)
+            else:
+                mp.mp_merge_ties(L, base, exps, m, 0.2, 1.0, out, stream=stream)
             b.record(stream)
             merge_ev.append((a, b))
         if rec is not None:
@@ -292,8 +319,28 @@ def main():
     plan_ms = np.array([[a.elapsed_time(b) for a, b in r[2]] for r in recs]).mean(0)
     merge_ms = np.array([[a.elapsed_time(b) for a, b in r[3]] for r in recs]).mean(0)
     stats = recs[-1][4]
-    io = mp.mp_merge_ties(L, base, exps, masks[0], 0.2, 1.0, out, io=True, stream=stream)
+    if catalog:
+        io = mp.mp_merge_ties_tau(L, base, exps, masks[0], tau, 1.0, out, io=True, stream=stream)
+    else:
+        io = mp.mp_merge_ties(L, base, exps, masks[0], 0.2, 1.0, out, io=True, stream=stream)
     assert io["expert_bytes"] == stats[0]["cost_bytes"]
+    # the other route, once, for reference (its own index pass first)
+    if catalog:
+        mp.mp_index_blocks(L, base, exps, sumsq, stream=stream)
+    else:
+        mp.mp_index_ties(L, base, exps, 0.2, tau, sumsq=sumsq, stream=stream)
+    alt = []
+    for m in masks:
+        a, b = ev(), ev()
+        a.record(stream)
+        if catalog:
+            mp.mp_merge_ties(L, base, exps, m, 0.2, 1.0, out, stream=stream)
+        else:
+            mp.mp_merge_ties_tau(L, base, exps, m, tau, 1.0, out, stream=stream)
+        b.record(stream)
+        alt.append((a, b))
+    torch.cuda.synchronize()
+    alt_ms = [a.elapsed_time(b) for a, b in alt]
     if args.calibration_copy:
         empty = torch.zeros(G, dtype=torch.int32, device="cuda")
         mp.mp_merge_avg(L, base, exps, empty, [0.25] * K, out, stream=stream)
@@ -303,7 +350,8 @@ def main():
     per_budget = []
     alg_bytes = []
     for f, st, pm, mm in zip(BUDGETS, stats, plan_ms, merge_ms):
-        byts = 2 * ckpt + st["cost_bytes"] + 4 * G  # base + selected expert blocks + output + mask
+        # base + selected expert blocks + output + mask (+ one threshold per selected unit)
+        byts = 2 * ckpt + st["cost_bytes"] + 4 * G + (4 * st["n_selected"] if catalog else 0)
         alg_bytes.append(byts)
         per_budget.append({
             "budget_frac": f, "budget_bytes": st["budget_bytes"], "cost_bytes": st["cost_bytes"],
@@ -313,9 +361,9 @@ def main():
             "merge_hbm_frac": byts / (mm * 1e-3) / HBM_PEAK,
             "digest": hex(st["digest"]),
         })
-    idx_bytes = (K + 1) * ckpt + 4 * G * K
+    idx_bytes = (K + 1) * ckpt + (8 if catalog else 4) * G * K
     achieved = sum(alg_bytes) / (sum(merge_ms) * 1e-3)
-    traffic = stored_traffic()
+    traffic = stored_traffic(args.ties)
     result = {
         "metric": METRIC,
         "value": 3 * P / (ms_step * 1e-3),
@@ -332,6 +380,7 @@ def main():
         "config": {
             "workload": "qwen2.5-1.5b-shaped bf16 family, K=4, index + (plan + TIES rho=0.2 lambda=1) "
                         "at B=25/50/100% per step",
+            "ties_route": args.ties,
             "storage_dtype": "bf16", "params": P, "blocks": G, "block_elems": lay.block_elems, "K": K,
             "budgets_bytes": budgets, "parallelism": "single GPU",
         },
@@ -339,18 +388,22 @@ def main():
             "bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
             "frac": achieved / HBM_PEAK,
             "traffic": traffic,
-            "kernel": "k_merge_ties<bf16> (device-resident experts)",
+            "kernel": ("k_merge_elem<bf16, TIES from catalog thresholds>" if catalog else "k_merge_ties<bf16>")
+                      + " (device-resident experts)",
         },
         "breakdown": {
             "index_ms": round(float(idx_ms), 4),
+            "index_kernel": "k_index_ties<bf16> (sums of squares + thresholds)" if catalog else "k_index<bf16>",
             "index_effective_GBps": idx_bytes / (idx_ms * 1e-3) / 1e9,
             "index_hbm_frac": idx_bytes / (idx_ms * 1e-3) / HBM_PEAK,
             "per_budget": per_budget,
+            "other_route": {"route": "in-merge" if catalog else "catalog",
+                            "merge_ms": [round(float(x), 4) for x in alt_ms]},
         },
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(spec, base, exps, args.cpu_stride)
+        result["cpu_baseline"] = cpu_baseline(spec, base, exps, args.ties, args.cpu_stride)
     print(json.dumps(result), flush=True)
 
 
