@@ -529,10 +529,8 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float*
         return rc;
     if ((rc = ensure_lists(ws->plan, (int64_t)K * std::max<int64_t>(bt->n_short, 1))))
         return rc;
-    uint64_t full = 0;
-    for (int64_t g = 0; g < bt->G; ++g)
-        full += (uint64_t)bt->h_len[(size_t)g];
-    full *= (uint64_t)es * (uint64_t)K;
+    // the blocks partition the checkpoint: their lengths sum to P
+    const uint64_t full = (uint64_t)bt->P * (uint64_t)es * (uint64_t)K;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = launch_plan(*bt, ws->plan, K, sumsq, cw, budget_bytes, full, mask, s);
     if (e != hipSuccess)

@@ -19,8 +19,11 @@
 // Each round strictly lowers the cost bound, so the number of rounds is at
 // most the number of distinct block lengths of the layout.
 //
-// All control state lives on the device (PlanCtl); the host enqueues a fixed
-// kernel sequence and kernels that are no longer needed return at once.
+// Round 0 (all units) runs as one launch per digit pass over the whole
+// device; the later rounds, whose candidate lists are short, run together
+// in one single-workgroup launch.  All control state lives on the device
+// (PlanCtl); the host enqueues a fixed kernel sequence and kernels that are
+// no longer needed return at once.
 #include "device_common.h"
 #include "mp_internal.h"
 
@@ -340,6 +343,145 @@ __global__ void k_plan_advance(PlanCtl* ctl, int next_list, int reuse_list)
     ctl->list_n[reuse_list] = 0u;
 }
 
+// Rounds r_begin .. r_end-1 (the later rounds, whose candidates are the
+// short lists left by the round before) in one workgroup: the same digit
+// passes, cut and selection as k_plan_hist / k_plan_mark / k_plan_advance,
+// with the round state in LDS and barriers instead of launches.
+__device__ inline uint32_t plan_list_load(const uint32_t* p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ __launch_bounds__(kT) void k_plan_rest(PlanCtl* ctl, const float* __restrict__ sumsq, Coeffs w, int K,
+                                                  const uint32_t* __restrict__ blen, uint32_t esize, int64_t G,
+                                                  uint32_t* list0, uint32_t* list1, unsigned int cap,
+                                                  uint32_t* __restrict__ mask, int r_begin, int r_end)
+{
+    __shared__ unsigned long long lh[256];
+    __shared__ unsigned long long s_brem0, s_below, s_total;
+    __shared__ unsigned long long s_cost[4], s_cnt[4];
+    __shared__ unsigned int s_n, s_next_n, s_err;
+    __shared__ int s_v, s_done;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    if (t == 0) {
+        s_done = (int)ctl->done;
+        s_brem0 = ctl->brem[0];
+        s_n = ctl->list_n[r_begin & 1];
+        s_err = 0u;
+    }
+    unsigned long long sel_cost = 0ull, sel_cnt = 0ull;  // this thread's selections
+    for (int r = r_begin; r < r_end; ++r) {
+        __syncthreads();
+        if (s_done)
+            break;
+        const uint32_t* list = (r & 1) ? list1 : list0;
+        uint32_t* next = (r & 1) ? list0 : list1;
+        const unsigned int n = min(s_n, cap);
+        const unsigned long long brem0 = s_brem0;
+        unsigned long long prefix = 0ull, brem = brem0, total0 = 0ull;
+        bool all = false;
+        for (int d = 0; d < 8; ++d) {
+            lh[t] = 0ull;
+            if (t == 0)
+                s_next_n = 0u;
+            __syncthreads();
+            const int hi_shift = 64 - 8 * d, dg_shift = 56 - 8 * d;
+            for (unsigned int q = t; q < n; q += kT) {
+                const uint32_t uid = plan_list_load(&list[q]);
+                const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
+                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+                if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
+                    atomicAdd(&lh[(key >> dg_shift) & 255u], (unsigned long long)blen[g] * esize);
+            }
+            __syncthreads();
+            if (wave == 0) {
+                int v;
+                unsigned long long below, total;
+                resolve_digit(lh, brem, lane, &v, &below, &total);
+                if (lane == 0) {
+                    s_v = v;
+                    s_below = below;
+                    s_total = total;
+                }
+            }
+            __syncthreads();
+            const int v = s_v;
+            if (v < 0) {  // digit 0: every candidate fits; later digits: cannot happen
+                if (d == 0) {
+                    all = true;
+                    total0 = s_total;
+                } else if (t == 0) {
+                    s_err = 3u;
+                }
+                break;
+            }
+            prefix |= (unsigned long long)v << (56 - 8 * d);
+            brem -= s_below;
+        }
+        // the cut key p = prefix; select below it, keep the cheaper ones above
+        unsigned long long cp = 0ull;
+        bool cut_ok = true;
+        if (!all) {
+            const uint32_t gp = (uint32_t)prefix / (uint32_t)K;
+            if ((int64_t)gp >= G) {  // cannot happen: the cut is a real unit
+                cut_ok = false;
+                if (t == 0)
+                    s_err = 1u;
+            } else {
+                cp = (unsigned long long)blen[gp] * esize;
+            }
+        }
+        if (all || cut_ok) {
+            for (unsigned int q = t; q < n; q += kT) {
+                const uint32_t uid = plan_list_load(&list[q]);
+                const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
+                const unsigned long long c = (unsigned long long)blen[g] * esize;
+                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+                if (all || key < prefix) {
+                    atomicOr(&mask[g], 1u << i);
+                    sel_cost += c;
+                    sel_cnt += 1;
+                } else if (key > prefix && c < cp) {
+                    const unsigned int slot = atomicAdd(&s_next_n, 1u);
+                    if (slot < cap)
+                        next[slot] = uid;
+                    else
+                        s_err = 2u;
+                }
+            }
+        }
+        __threadfence();  // the next list is in memory before the next round reads it
+        __syncthreads();
+        if (t == 0) {
+            s_brem0 = all ? brem0 - total0 : brem;
+            s_done = (all || !cut_ok || s_next_n == 0u) ? 1 : 0;
+            s_n = s_next_n;
+        }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        sel_cost += __shfl_xor(sel_cost, off);
+        sel_cnt += __shfl_xor(sel_cnt, off);
+    }
+    __syncthreads();
+    if (lane == 0) {
+        s_cost[wave] = sel_cost;
+        s_cnt[wave] = sel_cnt;
+    }
+    __syncthreads();
+    if (t == 0) {
+        const unsigned long long cs = s_cost[0] + s_cost[1] + s_cost[2] + s_cost[3];
+        const unsigned long long cn = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
+        if (cn) {
+            atomicAdd(&ctl->sel_cost, cs);
+            atomicAdd(&ctl->sel_count, cn);
+        }
+        if (s_err)
+            ctl->error = s_err;
+        ctl->done = 1u;
+    }
+}
+
 __global__ __launch_bounds__(kT) void k_plan_digest(PlanCtl* ctl, const uint32_t* __restrict__ mask, int64_t G)
 {
     __shared__ unsigned long long s[4];
@@ -385,7 +527,7 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
         const unsigned grid0 = (unsigned)(want < 2048 ? want : 2048);
         const unsigned gridL = 64;
         const int rounds = bt.n_distinct_len;
-        for (int r = 0; r < rounds; ++r) {
+        for (int r = 0; r < std::min(rounds, 1); ++r) {
             CandSrc src;
             unsigned grid;
             if (r == 0) {
@@ -408,6 +550,9 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
                                (unsigned)ps.list_cap);
             hipLaunchKernelGGL(k_plan_advance, dim3(1), dim3(64), 0, s, ctl, nxt, r & 1);
         }
+        if (rounds > 1)
+            hipLaunchKernelGGL(k_plan_rest, dim3(1), dim3(kT), 0, s, ctl, sumsq, w, K, bt.d_len, es, bt.G,
+                               ps.list[0], ps.list[1], (unsigned)ps.list_cap, mask, 1, rounds);
         const unsigned gridD = grid0;
         hipLaunchKernelGGL(k_plan_digest, dim3(gridD), dim3(kT), 0, s, ctl, mask, bt.G);
     }
