@@ -51,11 +51,19 @@ __device__ inline float2 ties_divisor(int i)
 // ------------------------------------------------------------ elementwise family
 enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2, M_TIES_TAU = 3 };
 
+// Occupancy of the elementwise kernels: the sign-elect modes (DARE with
+// sign election, TIES from thresholds) keep their per-element state for
+// half a block per pass (two passes per 4096-element block), which leaves
+// room for 8 waves per SIMD with bf16 (6 with fp32) to hide memory latency;
+// DARE-linear holds a whole block within 128 VGPRs (4 waves); AVG is light
+// enough either way.
+template <int MODE>
+constexpr bool elem_sign_mode() { return MODE == M_DARE_SIGN || MODE == M_TIES_TAU; }
+template <int DT, int MODE>
+constexpr int elem_waves() { return MODE == M_AVG ? 1 : (elem_sign_mode<MODE>() ? (DT == 1 ? 8 : 6) : 4); }
+
 template <int DT, int MODE, class Src>
-// DARE's Philox and sign-election state would otherwise take up to 134
-// VGPRs (3 waves per SIMD); at most 128 keeps 4 waves resident, which hides
-// more memory latency.  AVG is light enough either way.
-__global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src src, const void* __restrict__ base,
+__global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src src, const void* __restrict__ base,
                                                    const uint32_t* __restrict__ mask,
                                                    const uint64_t* __restrict__ boff,
                                                    const uint32_t* __restrict__ blen,
@@ -68,7 +76,9 @@ __global__ __launch_bounds__(kT, MODE == M_AVG ? 1 : 4) void k_merge_elem(Src sr
 {
     constexpr int V = Fmt<DT>::V;
     constexpr int ES = Fmt<DT>::esize;
-    constexpr int CPT = (DT == 1) ? 2 : 4;  // chunks per thread per tile (4096-element blocks: 1 tile)
+    // chunks per thread per tile (4096-element blocks: 1 tile; 2 for the
+    // sign-elect modes)
+    constexpr int CPT = ((DT == 1) ? 2 : 4) / (elem_sign_mode<MODE>() ? 2 : 1);
     constexpr bool DARE = MODE == M_DARE_LIN || MODE == M_DARE_SIGN;
     constexpr bool SIGN = MODE == M_DARE_SIGN || MODE == M_TIES_TAU;
     constexpr int E = CPT * V;
@@ -795,18 +805,23 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
     uint4 x0raw[CPT];
     load_chunks<DT, NT, CPT>(chunk_ptr(base, off, ES), nch, x0raw);
     float x0[E];
-#pragma unroll
-    for (int q = 0; q < CPT; ++q)
-        Fmt<DT>::unpack(x0raw[q], &x0[q * V]);
     uint4* po = reinterpret_cast<uint4*>(static_cast<char*>(out) + off * ES);
 
     float d[GS][E];
     uint32_t tau[GS];
     if (!MULTI) {
         const int ns = __popc(m);
+        // every load of the block is issued before the base is unpacked
+        uint4 raw[GS][CPT];
+        ties_load_group<DT, CPT>(src, b, off, n, m, 0, raw);
+#pragma unroll
+        for (int q = 0; q < CPT; ++q)
+            Fmt<DT>::unpack(x0raw[q], &x0[q * V]);
         uint32_t top = 0u;
-        if (ns != 0)
-            top = ties_trim_group<DT, CPT>(sm, src, b, off, n, k, m, 0, x0, d, tau);
+        if (ns != 0) {
+            ties_deltas<DT, CPT>(sm, raw, ns, x0, d);
+            top = ties_select_group<E>(sm, n, k, ns, d, tau);
+        }
         const bool big = top >= 0x7e000000u;  // some |d| >= 2^125: masses may overflow
         switch (ns) {
         case 0: ties_finish_single<DT, 0>(d, tau, x0, lambda, sm.rd, po, nch); break;
@@ -826,6 +841,9 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
             break;
         }
     } else {
+#pragma unroll
+        for (int q = 0; q < CPT; ++q)
+            Fmt<DT>::unpack(x0raw[q], &x0[q * V]);
         float P[E], N[E];
         uint32_t cnt[E];
 #pragma unroll
