@@ -51,16 +51,15 @@ __device__ inline float2 ties_divisor(int i)
 // ------------------------------------------------------------ elementwise family
 enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2, M_TIES_TAU = 3 };
 
-// Occupancy of the elementwise kernels: the sign-elect modes (DARE with
-// sign election, TIES from thresholds) keep their per-element state for
-// half a block per pass (two passes per 4096-element block), which leaves
-// room for 8 waves per SIMD with bf16 (6 with fp32) to hide memory latency;
-// DARE-linear holds a whole block within 128 VGPRs (4 waves); AVG is light
-// enough either way.
-template <int MODE>
-constexpr bool elem_sign_mode() { return MODE == M_DARE_SIGN || MODE == M_TIES_TAU; }
+// Occupancy of the elementwise kernels: DARE (either combination) and TIES
+// from thresholds keep their per-element state for half a block per pass
+// (two passes per 4096-element block), which leaves room for 8 waves per
+// SIMD with bf16 (6 with fp32) to hide memory latency; AVG holds a whole
+// block per pass (measured faster than halves at 8 waves).
 template <int DT, int MODE>
-constexpr int elem_waves() { return MODE == M_AVG ? 1 : (elem_sign_mode<MODE>() ? (DT == 1 ? 8 : 6) : 4); }
+constexpr int elem_waves() { return MODE == M_AVG ? 1 : (DT == 1 ? 8 : 6); }
+template <int MODE>
+constexpr int elem_div() { return MODE == M_AVG ? 1 : 2; }
 
 template <int DT, int MODE, class Src>
 __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src src, const void* __restrict__ base,
@@ -76,9 +75,9 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
 {
     constexpr int V = Fmt<DT>::V;
     constexpr int ES = Fmt<DT>::esize;
-    // chunks per thread per tile (4096-element blocks: 1 tile; 2 for the
-    // sign-elect modes)
-    constexpr int CPT = ((DT == 1) ? 2 : 4) / (elem_sign_mode<MODE>() ? 2 : 1);
+    // chunks per thread per tile (4096-element blocks: 1 tile for AVG, 2
+    // for the others)
+    constexpr int CPT = ((DT == 1) ? 2 : 4) / elem_div<MODE>();
     constexpr bool DARE = MODE == M_DARE_LIN || MODE == M_DARE_SIGN;
     constexpr bool SIGN = MODE == M_DARE_SIGN || MODE == M_TIES_TAU;
     constexpr int E = CPT * V;
