@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
 #pragma unroll
         for (int s = 32; s >= 1; s >>= 1)
             p = p + __shfl_xor(p, s);
-        const uint32_t th = (k == 0u) ? 0xffffffffu : wave_kth_largest<E>(rows[wave], mg, k, lane);
+        const uint32_t th = (k == 0u) ? 0xffffffffu : wave_kth_largest<E>(reinterpret_cast<char*>(&rows[0][0]), wave * ties::NB * 4, mg, k, lane);
         if (lane == 0) {
             if (sumsq != nullptr)
                 sumsq[g * K + i] = p;

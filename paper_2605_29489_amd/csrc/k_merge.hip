@@ -479,10 +479,12 @@ __device__ inline uint32_t ties_select_group(TiesSmem& sm, uint32_t n, uint32_t 
             if (bmax[j] != 0u) {
                 int wb;
                 const uint32_t koff = window_koff(bmax[j], lane, &wb);
+                const uint32_t flo = window_floor(wb);
                 char* row = reinterpret_cast<char*>(sm.h[j]);
+                uint32_t inc = 1u;
 #pragma unroll
                 for (int e = 0; e < E; ++e)
-                    window_add(row, __float_as_uint(d[j][e]), koff);
+                    window_add<false>(row, __float_as_uint(d[j][e]), flo, koff, inc);
             }
         }
     }

@@ -172,32 +172,43 @@ __device__ inline void wave_lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Adds one element's magnitude pattern to the window histogram at `row`
-// (byte offset (key << LG) + koff for the lane's copy); out-of-window keys
-// wrap past the row and are skipped.
-__device__ inline void window_add(char* row, uint32_t bits, uint32_t koff)
+// Adds one element to the window histogram.  base + koff + (key << LG) is
+// the byte address of the lane's copy of the element's bin (koff holds the
+// row's offset from base, the lane's copy and -wb bins; see window_koff).
+// Nothing lies above the window, so one test against the window's floor
+// pattern selects the elements to count.  MAG: bits is a magnitude pattern
+// (sign cleared; compared as an integer); otherwise a signed fp32 pattern
+// whose magnitude is compared (NaN is never counted).  inc is the counter
+// increment: its low half-word must hold 1; its high half-word is set to 1
+// when the element lies above its bin's floor (low bits not zero).
+template <bool MAG>
+__device__ inline void window_add(char* base, uint32_t bits, uint32_t floor_bits, uint32_t koff, uint32_t& inc)
 {
     using namespace ties;
+    const bool in = MAG ? bits >= floor_bits : fabsf(__uint_as_float(bits)) >= __uint_as_float(floor_bits);
+    // the address and increment are formed in every lane (one instruction
+    // each either way), so inc flows from element to element unmerged
 #if MP_TIES_ASM
     static_assert(KS == 16, "the low bits are the low half-word");
     uint32_t key, boff;
     asm("v_bfe_u32 %0, %1, %2, %3" : "=v"(key) : "v"(bits), "i"(KS), "i"(31 - KS));
     asm("v_lshl_add_u32 %0, %1, %2, %3" : "=v"(boff) : "v"(key), "i"(LG), "v"(koff));
+    // high half-word of inc = min(low half-word of bits, 1); low half-word kept
+    asm("v_min_u32_sdwa %0, %1, 1 dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:WORD_0 src1_sel:DWORD"
+        : "+v"(inc) : "v"(bits));
 #else
     const uint32_t boff = (__builtin_amdgcn_ubfe(bits, KS, 31 - KS) << LG) + koff;
+    inc = (min(bits & ((1u << KS) - 1u), 1u) << 16) + 1u;
 #endif
-    if (boff < (uint32_t)(NB * 4)) {
-        // count in the high half when the low bits are not zero
-#if MP_TIES_ASM
-        uint32_t nz;
-        asm("v_min_u32_sdwa %0, %1, 1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:DWORD"
-            : "=v"(nz) : "v"(bits));
-        const uint32_t inc = (nz << 16) + 1u;
-#else
-        const uint32_t inc = (min(bits & ((1u << KS) - 1u), 1u) << 16) + 1u;
-#endif
-        atomicAdd(reinterpret_cast<uint32_t*>(row + boff), inc);
-    }
+    if (in)
+        atomicAdd(reinterpret_cast<uint32_t*>(base + boff), inc);
+}
+
+// Floor pattern of the window whose bin 0 has key wb (everything at or
+// above it lies in the window).
+__device__ inline uint32_t window_floor(int wb)
+{
+    return (uint32_t)(wb > 0 ? wb : 0) << ties::KS;
 }
 
 // Key of bin 0 of the window anchored at the block maximum's pattern: the
@@ -221,12 +232,13 @@ __device__ inline uint32_t window_koff(uint32_t bmax, int lane, int* wb_out)
 // Wave-level, all lanes: exact k-th largest (multiplicity counted) of the
 // E magnitude patterns (fp32 patterns with the sign cleared) each lane
 // holds in mg, 1 <= k <= the number of values that are not padding; padding
-// values are zeros, which cannot change the k largest.  h is a wave-private
-// LDS row of NB words.
+// values are zeros, which cannot change the k largest.  The wave-private
+// LDS row of NB words starts row_off bytes after base.
 template <int E>
-__device__ inline uint32_t wave_kth_largest(uint32_t* __restrict__ h, const uint32_t (&mg)[E], uint32_t k, int lane)
+__device__ inline uint32_t wave_kth_largest(char* base, int row_off, const uint32_t (&mg)[E], uint32_t k, int lane)
 {
     using namespace ties;
+    uint32_t* __restrict__ h = reinterpret_cast<uint32_t*>(base + row_off);
     uint32_t mx = 0u;
 #pragma unroll
     for (int e = 0; e < E; e += 2)
@@ -239,10 +251,12 @@ __device__ inline uint32_t wave_kth_largest(uint32_t* __restrict__ h, const uint
         *reinterpret_cast<uint4*>(&h[4 * (q * 64 + lane)]) = make_uint4(0u, 0u, 0u, 0u);
     wave_lds_sync();
     int wb;
-    const uint32_t koff = window_koff(bmax, lane, &wb);
+    const uint32_t koff = window_koff(bmax, lane, &wb) + (uint32_t)row_off;
+    const uint32_t flo = window_floor(wb);
+    uint32_t inc = 1u;
 #pragma unroll
     for (int e = 0; e < E; ++e)
-        window_add(reinterpret_cast<char*>(h), mg[e], koff);
+        window_add<true>(base, mg[e], flo, koff, inc);
     wave_lds_sync();
     const Cut c = wave_find_from_top<NC>(h, NBIN - 1, k, lane);
     if (c.found) {  // else the k-th largest lies below the window
