@@ -127,7 +127,7 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
             const uint32_t c = (uint32_t)(r * 64 + lane);
             xe[r] = (c < nch) ? e[c] : make_uint4(0u, 0u, 0u, 0u);
         }
-        uint32_t mg[E];  // |d| patterns
+        float d[E];
         float p = 0.0f;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -136,15 +136,14 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
             Fmt<DT>::unpack(xe[r], fe);
 #pragma unroll
             for (int q = 0; q < V; ++q) {
-                const float d = fe[q] - fb[q];  // padding: 0 - 0
-                p = fmaf(d, d, p);              // + 0 on padding, exact
-                mg[r * V + q] = __float_as_uint(d) & 0x7fffffffu;
+                d[r * V + q] = fe[q] - fb[q];             // padding: 0 - 0
+                p = fmaf(d[r * V + q], d[r * V + q], p);  // + 0 on padding, exact
             }
         }
 #pragma unroll
         for (int s = 32; s >= 1; s >>= 1)
             p = p + __shfl_xor(p, s);
-        const uint32_t th = (k == 0u) ? 0xffffffffu : wave_kth_largest<E>(reinterpret_cast<char*>(&rows[0][0]), wave * ties::NB * 4, mg, k, lane);
+        const uint32_t th = (k == 0u) ? 0xffffffffu : wave_kth_largest<E>(reinterpret_cast<char*>(&rows[0][0]), wave * ties::NB * 4, d, k, lane);
         if (lane == 0) {
             if (sumsq != nullptr)
                 sumsq[g * K + i] = p;

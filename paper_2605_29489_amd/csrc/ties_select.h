@@ -229,21 +229,31 @@ __device__ inline uint32_t window_koff(uint32_t bmax, int lane, int* wb_out)
     return (uint32_t)(lane & (NC - 1)) * 4u - (uint32_t)wb * (uint32_t)(4 * NC);
 }
 
-// Wave-level, all lanes: exact k-th largest (multiplicity counted) of the
-// E magnitude patterns (fp32 patterns with the sign cleared) each lane
-// holds in mg, 1 <= k <= the number of values that are not padding; padding
+// |x|'s pattern, formed where it is used: the rare fallbacks below do not
+// keep a second copy of the values (the compiler would otherwise share one
+// between them).
+__device__ inline uint32_t mag_bits(float x)
+{
+    uint32_t r;
+    asm volatile("v_and_b32 %0, 0x7fffffff, %1" : "=v"(r) : "v"(x));
+    return r;
+}
+
+// Wave-level, all lanes: exact k-th largest magnitude pattern (multiplicity
+// counted) of the E values each lane holds in d (NaN is not ordered: keep
+// it out), 1 <= k <= the number of values that are not padding; padding
 // values are zeros, which cannot change the k largest.  The wave-private
 // LDS row of NB words starts row_off bytes after base.
 template <int E>
-__device__ inline uint32_t wave_kth_largest(char* base, int row_off, const uint32_t (&mg)[E], uint32_t k, int lane)
+__device__ inline uint32_t wave_kth_largest(char* base, int row_off, const float (&d)[E], uint32_t k, int lane)
 {
     using namespace ties;
     uint32_t* __restrict__ h = reinterpret_cast<uint32_t*>(base + row_off);
-    uint32_t mx = 0u;
+    float mxf = 0.0f;
 #pragma unroll
-    for (int e = 0; e < E; e += 2)
-        mx = max(mx, max(mg[e], mg[e + 1]));
-    const uint32_t bmax = wave_max_u32(mx);
+    for (int e = 0; e < E; e += 2)  // pairs: one three-way maximum each
+        mxf = fmaxf(mxf, fmaxf(fabsf(d[e]), fabsf(d[e + 1])));
+    const uint32_t bmax = wave_max_u32(__float_as_uint(mxf));
     if (bmax == 0u)
         return 0u;  // all zero
 #pragma unroll
@@ -256,7 +266,7 @@ __device__ inline uint32_t wave_kth_largest(char* base, int row_off, const uint3
     uint32_t inc = 1u;
 #pragma unroll
     for (int e = 0; e < E; ++e)
-        window_add<true>(base, mg[e], flo, koff, inc);
+        window_add<false>(base, __float_as_uint(d[e]), flo, koff, inc);
     wave_lds_sync();
     const Cut c = wave_find_from_top<NC>(h, NBIN - 1, k, lane);
     if (c.found) {  // else the k-th largest lies below the window
@@ -268,12 +278,13 @@ __device__ inline uint32_t wave_kth_largest(char* base, int row_off, const uint3
         uint32_t n = 0u;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const bool in = (mg[e] >> KS) == key;
+            const uint32_t mg = mag_bits(d[e]);
+            const bool in = (mg >> KS) == key;
             const unsigned long long bal = __ballot(in);
             const uint32_t pos =
                 n + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
             if (in && pos < (uint32_t)NB)
-                h[pos] = mg[e];
+                h[pos] = mg;
             n += (uint32_t)__popcll(bal);
         }
         wave_lds_sync();
@@ -293,9 +304,10 @@ __device__ inline uint32_t wave_kth_largest(char* base, int row_off, const uint3
         wave_lds_sync();
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const uint32_t hi = (lv == 0) ? 0u : (mg[e] >> (sh + wd));
+            const uint32_t mg = mag_bits(d[e]);
+            const uint32_t hi = (lv == 0) ? 0u : (mg >> (sh + wd));
             if (hi == pref)
-                atomicAdd(&h[(mg[e] >> sh) & ((1u << wd) - 1u)], 1u);
+                atomicAdd(&h[(mg >> sh) & ((1u << wd) - 1u)], 1u);
         }
         wave_lds_sync();
         const Cut c = wave_find_from_top<1>(h, (1 << wd) - 1, r, lane);
