@@ -180,6 +180,11 @@ int orc_index(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype
 /*  sort by decreasing score, ties by increasing uid (earlier          */
 /*  tensor/block first, then lower expert);                            */
 /*  greedy: take a candidate iff C + c <= B, and keep scanning.         */
+/* Options (flags):                                                     */
+/*  1 per byte: s = float(double(s) / double(c)), retained utility per */
+/*    byte of expert read (Eq. 6's ratio of utility to cost);           */
+/*  2 skip zero: a unit with S_u = 0 (its block is unchanged up to      */
+/*    squares that underflow) is not a candidate.                       */
 /* Digest (the "selected-block digest"; the hash is this reading):     */
 /*  D = sum over blocks g of mix64((g << 32) | mask[g]) mod 2^64,       */
 /*  digest = mix64(D xor C).                                           */
@@ -216,7 +221,7 @@ int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
              uint32_t* mask, uint64_t* stats)
 {
     int s = elem_bytes(dtype);
-    if (s == 0 || K < 1 || K > 32 || G < 0 || flags != 0)
+    if (s == 0 || K < 1 || K > 32 || G < 0 || (flags & ~3u) != 0)
         return -1;
     if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
         return -1;
@@ -225,19 +230,27 @@ int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
     if (!q)
         return -2;
     uint64_t full = 0;
+    int64_t nq = 0; /* candidates */
     for (int64_t u = 0; u < nu; ++u) {
         int32_t i = (int32_t)(u % K);
+        uint64_t c = (uint64_t)len[u / K] * (uint64_t)s;
+        full += c;
+        if ((flags & 2u) && sumsq[u] == 0.0f)
+            continue;
         float w2 = w[i] * w[i];
-        q[u].score = w2 * sumsq[u];
-        q[u].uid = (uint32_t)u;
-        full += (uint64_t)len[u / K] * (uint64_t)s;
+        float sc = w2 * sumsq[u];
+        if (flags & 1u)
+            sc = (float)((double)sc / (double)c);
+        q[nq].score = sc;
+        q[nq].uid = (uint32_t)u;
+        ++nq;
     }
-    qsort(q, (size_t)nu, sizeof(cand_t), cand_cmp);
+    qsort(q, (size_t)nq, sizeof(cand_t), cand_cmp);
 
     for (int64_t g = 0; g < G; ++g)
         mask[g] = 0;
     uint64_t C = 0, nsel = 0;
-    for (int64_t r = 0; r < nu; ++r) {
+    for (int64_t r = 0; r < nq; ++r) {
         uint32_t u = q[r].uid;
         uint64_t c = (uint64_t)len[u / K] * (uint64_t)s;
         if (C + c <= budget) {

@@ -38,8 +38,9 @@ int orc_index(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype
               const void* base, const void* const* experts, int32_t K, float* sumsq);
 
 /* Algorithm 1 (PlanGen), literal: score, sort, skip-and-continue greedy.
- * stats[0]=selected cost, [1]=selected units, [2]=full cost, [3]=digest,
- * [4]=number of units. */
+ * flags: 1 = score per byte of cost, 2 = units with a zero sum of squares
+ * are not candidates.  stats[0]=selected cost, [1]=selected units, [2]=full
+ * cost, [3]=digest, [4]=number of units. */
 int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
              const float* sumsq, const float* w, uint64_t budget, uint32_t flags,
              uint32_t* mask, uint64_t* stats);

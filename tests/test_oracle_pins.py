@@ -229,6 +229,66 @@ def test_plan_worked_example():
         assert st["digest"] == oracle.mix64(D ^ st["cost"])
 
 
+def test_plan_per_byte_worked_example():
+    # Per-byte scores (flag 1): fp32 blocks of 8, 2 and 2 elements cost 32, 8
+    # and 8 bytes; K = 1, S = (4, 3, 2.5), w = 1.  Plain scores 4 > 3 > 2.5
+    # put the big block first; per-byte scores 4/32 = 0.125, 3/8 = 0.375,
+    # 2.5/8 = 0.3125 put it last.
+    b = oracle.Blocks([8, 2, 2], 8)
+    S = np.array([4.0, 3.0, 2.5], np.float32)
+    for B, plain, per_byte in ((32, [1, 0, 0], [0, 1, 1]), (40, [1, 1, 0], [0, 1, 1]),
+                               (48, [1, 1, 1], [1, 1, 1]), (12, [0, 1, 0], [0, 1, 0])):
+        m0, st0 = oracle.plan(b, "f32", 1, S, [1.0], B)
+        m1, st1 = oracle.plan(b, "f32", 1, S, [1.0], B, flags=1)
+        assert list(m0) == plain and list(m1) == per_byte
+        assert st1["cost"] == sum(c for c, t in zip((32, 8, 8), per_byte) if t) <= B
+        assert st1["n_units"] == 3 and st1["full_bytes"] == 48
+
+
+def test_plan_per_byte_with_uniform_power_of_two_costs_is_the_plain_plan():
+    # dividing every score by the same power of two (exact for normal
+    # values) keeps the order, so the mask is the plain one
+    rng = np.random.default_rng(31)
+    for trial in range(60):
+        G, K = int(rng.integers(1, 40)), int(rng.integers(1, 6))
+        b = oracle.Blocks([16] * G, 16)
+        S = (rng.integers(0, 5, G * K) * rng.random(G * K) + 1e-3).astype(np.float32)
+        S[rng.random(G * K) < 0.2] = 0.0
+        w = (rng.random(K) + 0.5).astype(np.float32)
+        full = 16 * 4 * G * K
+        for B in (0, 64, full // 3, full // 2, full):
+            m0, st0 = oracle.plan(b, "f32", K, S, w, B)
+            m1, st1 = oracle.plan(b, "f32", K, S, w, B, flags=1)
+            assert np.array_equal(m0, m1) and st0 == st1
+
+
+def test_plan_skip_zero_drops_exactly_the_zero_units():
+    # Units with S = 0 score 0 and come last in the plain order, so the
+    # greedy decides every positive unit the same way with or without them:
+    # flag 2's mask is the plain mask without the zero units, at any budget.
+    rng = np.random.default_rng(37)
+    for trial in range(200):
+        G, K = int(rng.integers(1, 15)), int(rng.integers(1, 5))
+        b = oracle.Blocks(list(rng.choice([16, 8, 4, 12], size=G)), 16)
+        S = (rng.random(G * K) * 10 + 0.01).astype(np.float32)
+        S[rng.random(G * K) < 0.3] = 0.0
+        w = (rng.random(K) + 0.5).astype(np.float32)
+        full = int(b.len.sum()) * 4 * K
+        B = int(rng.integers(0, full + 20))
+        m0, st0 = oracle.plan(b, "f32", K, S, w, B)
+        m2, st2 = oracle.plan(b, "f32", K, S, w, B, flags=2)
+        zero = np.zeros(G, np.uint32)
+        for u in np.nonzero(S == 0)[0]:
+            zero[u // K] |= np.uint32(1 << (u % K))
+        assert np.array_equal(m2, m0 & ~zero)
+        cost = sum(int(b.len[g]) * 4 for g in range(G) for i in range(K) if (int(m2[g]) >> i) & 1)
+        assert st2["cost"] == cost and st2["n_selected"] == int(sum(bin(int(x)).count("1") for x in m2))
+        assert st2["full_bytes"] == full and st2["n_units"] == G * K
+    # all-zero experts: nothing is a candidate
+    m, st = oracle.plan(oracle.Blocks([16], 16), "f32", 2, np.zeros(2, np.float32), [1.0, 1.0], 10**6, flags=2)
+    assert int(m[0]) == 0 and st["cost"] == 0 and st["n_selected"] == 0
+
+
 def _random_plan_case(rng, G, K, uniform, ties=False):
     if uniform:
         numel = [16] * G
