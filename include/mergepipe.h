@@ -64,6 +64,8 @@ extern "C" {
 typedef enum { MP_F32 = 0, MP_BF16 = 1 } mp_dtype;
 typedef enum { MP_DEVICE = 0, MP_HOST_PINNED = 1 } mp_residency;
 typedef enum { MP_COMBINE_LINEAR = 0, MP_COMBINE_SIGN_ELECT = 1 } mp_combine;
+/* mp_plan options (bit flags; 0 is the literal Algorithm 1). */
+typedef enum { MP_PLAN_PER_BYTE = 1, MP_PLAN_SKIP_ZERO = 2 } mp_plan_flags;
 
 typedef struct mp_layout {
     int32_t n_tensors;     /* number of tensors (>= 0) */
@@ -134,7 +136,15 @@ int mp_index_ties(const mp_layout* layout, const void* base,
  *   greedy take u iff Chat + c_u <= B, and continue past candidates that
  *          do not fit (skip-and-continue).
  *   sumsq: device float[G*K] from mp_index_blocks.  w: HOST float[K]
- *   (alpha for AVG and DARE-linear, 1 for TIES and sign-elect).  flags: 0.
+ *   (alpha for AVG and DARE-linear, 1 for TIES and sign-elect).
+ *   flags: 0, or a combination of
+ *     MP_PLAN_PER_BYTE   score per byte read, as Eq. 6 trades utility
+ *                        against a byte budget: s_u = float(double(s_u) /
+ *                        double(c_u)), one rounding from the fp64 quotient;
+ *     MP_PLAN_SKIP_ZERO  units with S_u = 0 are not candidates (their
+ *                        block is the base's, up to squares that
+ *                        underflow); they are never selected.
+ *   Other bits: MP_E_UNSUPPORTED.
  *   mask: device uint32[G], written for every block.
  *   stats: HOST, filled; digest = mix64(D xor Chat) with D = sum over g of
  *   mix64((g << 32) | mask[g]) mod 2^64 and mix64 the SplitMix64 output

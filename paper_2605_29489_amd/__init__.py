@@ -29,6 +29,7 @@ MP_E_HIP = -4
 MP_F32, MP_BF16 = 0, 1
 MP_DEVICE, MP_HOST_PINNED = 0, 1
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
+MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 
 EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_ties",
            "mp_merge_ties_tau", "mp_merge_dare", "mp_last_error", "mp_release")

@@ -506,7 +506,7 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float*
         return rc;
     if (K < 1 || K > kMaxK)
         return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
-    if (flags != 0u)
+    if ((flags & ~(uint32_t)(MP_PLAN_PER_BYTE | MP_PLAN_SKIP_ZERO)) != 0u)
         return fail(MP_E_UNSUPPORTED, "plan flags 0x%x not supported", flags);
     if (w == nullptr || stats == nullptr)
         return fail(MP_E_ARG, "w and stats must not be NULL");
@@ -532,7 +532,7 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float*
     // the blocks partition the checkpoint: their lengths sum to P
     const uint64_t full = (uint64_t)bt->P * (uint64_t)es * (uint64_t)K;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = launch_plan(*bt, ws->plan, K, sumsq, cw, budget_bytes, full, mask, s);
+    hipError_t e = launch_plan(*bt, ws->plan, K, sumsq, cw, flags, budget_bytes, full, mask, s);
     if (e != hipSuccess)
         return hip_fail(e, "plan launch");
     if ((e = hipStreamSynchronize(s)) != hipSuccess)

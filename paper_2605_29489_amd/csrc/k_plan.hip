@@ -48,12 +48,22 @@ namespace {
 
 constexpr int kT = 256;
 
-__device__ inline unsigned long long unit_key(float S, float w, uint32_t uid)
+// Plan options (the flags of mp_plan).
+constexpr uint32_t kPlanPerByte = 1u;   // score per byte of cost
+constexpr uint32_t kPlanSkipZero = 2u;  // units with a zero sum of squares are not candidates
+
+// The unit's sort key; c is its cost in bytes.  Per byte: the fp32 score
+// divided by c in fp64, rounded once to fp32.
+__device__ inline unsigned long long unit_key(float S, float w, uint32_t uid, unsigned long long c, uint32_t flags)
 {
     const float w2 = w * w;
-    const float sc = w2 * S;
+    float sc = w2 * S;
+    if (flags & kPlanPerByte)
+        sc = (float)((double)sc / (double)c);
     return ((unsigned long long)(~__float_as_uint(sc)) << 32) | uid;
 }
+
+__device__ inline bool plan_skips(float S, uint32_t flags) { return (flags & kPlanSkipZero) && S == 0.0f; }
 
 // Wave-level resolution of one digit: h[256] holds the cost of the matching
 // candidates per digit value.  Returns the smallest v with
@@ -132,8 +142,9 @@ __global__ __launch_bounds__(kT) void k_plan_init(PlanCtl* ctl, unsigned long lo
 // it redundantly from the previous histogram; workgroup 0 publishes it), then
 // histogram digit d of the candidates matching the resolved prefix.
 __global__ __launch_bounds__(kT) void k_plan_hist(PlanCtl* ctl, int d, const float* __restrict__ sumsq,
-                                                  Coeffs w, int K, const uint32_t* __restrict__ blen,
-                                                  uint32_t esize, int64_t G, CandSrc src)
+                                                  Coeffs w, uint32_t flags, int K,
+                                                  const uint32_t* __restrict__ blen, uint32_t esize, int64_t G,
+                                                  CandSrc src)
 {
     __shared__ unsigned long long lh[256];
     __shared__ unsigned long long s_prefix;
@@ -190,18 +201,22 @@ __global__ __launch_bounds__(kT) void k_plan_hist(PlanCtl* ctl, int d, const flo
             const unsigned long long c = (unsigned long long)blen[g] * esize;
             for (int i = 0; i < K; ++i) {
                 const uint32_t uid = (uint32_t)(g * K + i);
-                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+                const float S = sumsq[uid];
+                if (plan_skips(S, flags))
+                    continue;
+                const unsigned long long key = unit_key(S, w.v[i], uid, c, flags);
                 if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
                     atomicAdd(&lh[(key >> dg_shift) & 255u], c);
             }
         }
     } else {
+        // listed units are candidates already
         const unsigned int n = min(*src.list_n, src.cap);
         for (unsigned int q = blockIdx.x * kT + t; q < n; q += gridDim.x * kT) {
             const uint32_t uid = src.list[q];
             const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
             const unsigned long long c = (unsigned long long)blen[g] * esize;
-            const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+            const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid, c, flags);
             if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
                 atomicAdd(&lh[(key >> dg_shift) & 255u], c);
         }
@@ -215,7 +230,7 @@ __global__ __launch_bounds__(kT) void k_plan_hist(PlanCtl* ctl, int d, const flo
 // candidates below it, and collect the next round's candidates (above p,
 // cheaper than c_p).  In the all-fit case select every candidate.
 __global__ __launch_bounds__(kT) void k_plan_mark(PlanCtl* ctl, const float* __restrict__ sumsq, Coeffs w,
-                                                  int K, const uint32_t* __restrict__ blen,
+                                                  uint32_t flags, int K, const uint32_t* __restrict__ blen,
                                                   uint32_t esize, int64_t G, CandSrc src,
                                                   uint32_t* __restrict__ mask, uint32_t* __restrict__ next,
                                                   unsigned int* __restrict__ next_n, unsigned int next_cap)
@@ -265,7 +280,10 @@ __global__ __launch_bounds__(kT) void k_plan_mark(PlanCtl* ctl, const float* __r
             uint32_t word = 0u;
             for (int i = 0; i < K; ++i) {
                 const uint32_t uid = (uint32_t)(g * K + i);
-                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+                const float S = sumsq[uid];
+                if (plan_skips(S, flags))
+                    continue;
+                const unsigned long long key = unit_key(S, w.v[i], uid, c, flags);
                 if (all || key < keyp) {
                     word |= 1u << i;
                     my_cost += c;
@@ -286,7 +304,7 @@ __global__ __launch_bounds__(kT) void k_plan_mark(PlanCtl* ctl, const float* __r
             const uint32_t uid = src.list[q];
             const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
             const unsigned long long c = (unsigned long long)blen[g] * esize;
-            const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+            const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid, c, flags);
             if (all || key < keyp) {
                 atomicOr(&mask[g], 1u << i);
                 my_cost += c;
@@ -352,7 +370,8 @@ __device__ inline uint32_t plan_list_load(const uint32_t* p)
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__global__ __launch_bounds__(kT) void k_plan_rest(PlanCtl* ctl, const float* __restrict__ sumsq, Coeffs w, int K,
+__global__ __launch_bounds__(kT) void k_plan_rest(PlanCtl* ctl, const float* __restrict__ sumsq, Coeffs w,
+                                                  uint32_t flags, int K,
                                                   const uint32_t* __restrict__ blen, uint32_t esize, int64_t G,
                                                   uint32_t* list0, uint32_t* list1, unsigned int cap,
                                                   uint32_t* __restrict__ mask, int r_begin, int r_end)
@@ -389,9 +408,10 @@ __global__ __launch_bounds__(kT) void k_plan_rest(PlanCtl* ctl, const float* __r
             for (unsigned int q = t; q < n; q += kT) {
                 const uint32_t uid = plan_list_load(&list[q]);
                 const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
-                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+                const unsigned long long c = (unsigned long long)blen[g] * esize;
+                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid, c, flags);
                 if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
-                    atomicAdd(&lh[(key >> dg_shift) & 255u], (unsigned long long)blen[g] * esize);
+                    atomicAdd(&lh[(key >> dg_shift) & 255u], c);
             }
             __syncthreads();
             if (wave == 0) {
@@ -436,7 +456,7 @@ __global__ __launch_bounds__(kT) void k_plan_rest(PlanCtl* ctl, const float* __r
                 const uint32_t uid = plan_list_load(&list[q]);
                 const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
                 const unsigned long long c = (unsigned long long)blen[g] * esize;
-                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid);
+                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid, c, flags);
                 if (all || key < prefix) {
                     atomicOr(&mask[g], 1u << i);
                     sel_cost += c;
@@ -516,7 +536,7 @@ __global__ void k_plan_final(PlanCtl* ctl, unsigned long long budget, unsigned l
 }  // namespace
 
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
-                       const Coeffs& w, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
+                       const Coeffs& w, uint32_t flags, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
                        hipStream_t s)
 {
     PlanCtl* ctl = ps.ctl;
@@ -543,15 +563,15 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
             }
             const int nxt = (r + 1) & 1;
             for (int d = 0; d < 8; ++d)
-                hipLaunchKernelGGL(k_plan_hist, dim3(grid), dim3(kT), 0, s, ctl, d, sumsq, w, K,
+                hipLaunchKernelGGL(k_plan_hist, dim3(grid), dim3(kT), 0, s, ctl, d, sumsq, w, flags, K,
                                    bt.d_len, es, bt.G, src);
-            hipLaunchKernelGGL(k_plan_mark, dim3(grid), dim3(kT), 0, s, ctl, sumsq, w, K, bt.d_len,
+            hipLaunchKernelGGL(k_plan_mark, dim3(grid), dim3(kT), 0, s, ctl, sumsq, w, flags, K, bt.d_len,
                                es, bt.G, src, mask, ps.list[nxt], &ctl->list_n[nxt],
                                (unsigned)ps.list_cap);
             hipLaunchKernelGGL(k_plan_advance, dim3(1), dim3(64), 0, s, ctl, nxt, r & 1);
         }
         if (rounds > 1)
-            hipLaunchKernelGGL(k_plan_rest, dim3(1), dim3(kT), 0, s, ctl, sumsq, w, K, bt.d_len, es, bt.G,
+            hipLaunchKernelGGL(k_plan_rest, dim3(1), dim3(kT), 0, s, ctl, sumsq, w, flags, K, bt.d_len, es, bt.G,
                                ps.list[0], ps.list[1], (unsigned)ps.list_cap, mask, 1, rounds);
         const unsigned gridD = grid0;
         hipLaunchKernelGGL(k_plan_digest, dim3(gridD), dim3(kT), 0, s, ctl, mask, bt.G);

@@ -75,7 +75,7 @@ hipError_t launch_index_ties(const BlockTable& bt, const void* base, const Exper
 
 // Algorithm 1 on the device (k_plan.hip).
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
-                       const Coeffs& w, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
+                       const Coeffs& w, uint32_t flags, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
                        hipStream_t s);
 
 // Merge operators.  `counters` is null or a device array of 256 uint64

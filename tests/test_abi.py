@@ -81,10 +81,11 @@ def test_argument_errors_before_any_device_call(mp):
         assert lib.mp_plan(L.ref, K, None, w, 0, 0, None, C.byref(st), None) == mp.MP_E_ARG
     # bad residency
     assert lib.mp_index_blocks(L.ref, None, ptrs, 1, 5, None, None) == mp.MP_E_ARG
-    # unsupported plan flags
+    # unsupported plan flags (bits other than per-byte and skip-zero)
     st = mp.mp_plan_stats()
     w = (C.c_float * 1)(1.0)
-    assert lib.mp_plan(L.ref, 1, None, w, 0, 1, None, C.byref(st), None) == mp.MP_E_UNSUPPORTED
+    for fl in (4, 8, 0x80000000, 4 | mp.MP_PLAN_PER_BYTE):
+        assert lib.mp_plan(L.ref, 1, None, w, 0, fl, None, C.byref(st), None) == mp.MP_E_UNSUPPORTED
     # non-finite plan weight
     wn = (C.c_float * 1)(float("nan"))
     assert lib.mp_plan(L.ref, 1, None, wn, 0, 0, None, C.byref(st), None) == mp.MP_E_ARG

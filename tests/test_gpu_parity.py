@@ -336,6 +336,86 @@ def test_ties_infinite_masses(mp):
     _run_all(mp, spec, base, exps, "ties_tau", [1.0], density=0.0, lam=1.0)
 
 
+def test_skip_zero_full_budget_merges_equal_full_merges(mp):
+    # With the skip-zero option, units whose block equals the base (S = 0:
+    # the family's untouched blocks) are never selected; at full budget every
+    # merge operator still gives the full merge bit for bit, and reads
+    # exactly the nonzero units' bytes.
+    import torch
+    spec = _mini_qwen(K=4)
+    base_np, exps_np = make_family(spec, seed=5)
+    L, lay = _lay(mp, spec)
+    K = len(exps_np)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    G = blocks.G
+    base = to_dev(base_np, lay.dtype)
+    exps = [to_dev(e, lay.dtype) for e in exps_np]
+    sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
+    mp.mp_index_blocks(L, base, exps, sumsq)
+    S = sumsq.cpu().numpy()
+    assert (S == 0).sum() > 0, "the family has untouched blocks"
+    full = int(blocks.len.sum()) * lay.elem_bytes * K
+    m_all = torch.empty(G, dtype=torch.int32, device="cuda")
+    m_nz = torch.empty(G, dtype=torch.int32, device="cuda")
+    mp.mp_plan(L, K, sumsq, [1.0] * K, full, m_all)
+    st = mp.mp_plan(L, K, sumsq, [1.0] * K, full, m_nz, flags=mp.MP_PLAN_SKIP_ZERO)
+    nz_cost = sum(int(blocks.len[u // K]) * lay.elem_bytes for u in np.nonzero(S != 0)[0])
+    assert st["cost_bytes"] == nz_cost and st["n_selected"] == int((S != 0).sum())
+    _say("case skip-zero at full budget")
+    o1, o2 = torch.empty_like(base), torch.empty_like(base)
+    tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
+    mp.mp_index_ties(L, base, exps, 0.2, tau)
+    runs = [
+        lambda m, o: mp.mp_merge_avg(L, base, exps, m, [0.25] * K, o, io=True),
+        lambda m, o: mp.mp_merge_ties(L, base, exps, m, 0.2, 1.0, o, io=True),
+        lambda m, o: mp.mp_merge_ties_tau(L, base, exps, m, tau, 1.0, o, io=True),
+        lambda m, o: mp.mp_merge_dare(L, base, exps, m, 0.9, 7, 0, [0.25] * K, 1.0, o, io=True),
+        lambda m, o: mp.mp_merge_dare(L, base, exps, m, 0.9, 7, 1, None, 1.0, o, io=True),
+    ]
+    for run in runs:
+        run(m_all, o1)
+        io = run(m_nz, o2)
+        assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+        assert io["expert_bytes"] == nz_cost
+
+
+def test_plan_many_rounds(mp):
+    # Many distinct block lengths, scores with deliberate ties (equal sums
+    # of squares, equal weights) and zero scores: after the first cut, the
+    # cheaper candidates above it are planned in later rounds.  Mask, cost,
+    # count and digest match the oracle's literal sort + greedy at every
+    # budget, including budgets where many rounds remain.
+    import torch
+    numel = [4096 * 3 + 64, 4096 + 512, 2048, 1024 + 256, 4096 * 2 + 1536, 768, 4096, 384, 128, 4096 + 2560]
+    L = mp.Layout(numel, 4096, mp.MP_BF16)
+    blocks = oracle.Blocks(numel, 4096)
+    K = 5
+    G = blocks.G
+    rng = np.random.default_rng(23)
+    S = rng.choice(np.array([0.0, 1e-4, 2.5e-3, 2.5e-3, 7e-2, 1.0, 3.0], np.float32), size=G * K)
+    S = (S * rng.choice(np.array([1.0, 1.0, 0.5], np.float32), size=G * K)).astype(np.float32)
+    sumsq = torch.from_numpy(S).cuda()
+    mask = torch.empty(G, dtype=torch.int32, device="cuda")
+    full = int(blocks.len.sum()) * 2 * K
+    lens = sorted(set(int(x) for x in blocks.len))
+    assert len(lens) >= 8
+    _say(f"case plan rounds: G={G}, {len(lens)} distinct lengths")
+    budgets = sorted(set([0, 1, 127, 128, 129, full // 7, full // 3, full // 2, full - 1, full, full + 5]
+                         + [int(x) for x in rng.integers(0, full, 40)]))
+    # flags: 0 literal, 1 per-byte scores, 2 skip zero units, 3 both
+    for flags in (0, mp.MP_PLAN_PER_BYTE, mp.MP_PLAN_SKIP_ZERO, mp.MP_PLAN_PER_BYTE | mp.MP_PLAN_SKIP_ZERO):
+        for w in ([1.0] * K, [0.5, 1.0, 1.0, 0.25, 2.0]):
+            for B in budgets:
+                st = mp.mp_plan(L, K, sumsq, w, B, mask, flags=flags)
+                m_orc, st_orc = oracle.plan(blocks, "bf16", K, S, w, B, flags=flags)
+                assert np.array_equal(mask.cpu().numpy().view(np.uint32), m_orc), \
+                    f"mask differs at B={B} w={w} flags={flags}"
+                assert st["cost_bytes"] == st_orc["cost"] <= B
+                assert st["n_selected"] == st_orc["n_selected"]
+                assert st["digest"] == st_orc["digest"]
+                assert st["full_bytes"] == st_orc["full_bytes"] and st["n_units"] == G * K
+
+
 def test_budget_boundaries_exact(mp):
     # budgets at the exact cost of a greedy prefix, one byte below and above
     spec = _mini_qwen(n_layers=1)
