@@ -27,10 +27,17 @@
  *   (hipHostMalloc / pinned torch tensors) and the kernels read expert
  *   blocks straight from it over PCIe -- only the blocks a call touches
  *   cross the link, with no staging copy (the host-to-device feed of
- *   Algorithm 2).  Otherwise they are device memory.  The caller owns every
- *   buffer; the library only reads inputs and writes the named outputs.
- *   The library keeps a per-device workspace (block tables, plan scratch,
- *   byte counters) that mp_release() frees.
+ *   Algorithm 2).  With residency MP_HOST_PAGEABLE they are host memory of
+ *   any kind (ordinary pageable allocations included; each must hold the
+ *   whole checkpoint, which the library cannot check): the call packs the
+ *   blocks it needs into pinned staging buffers on host threads, copies
+ *   them to the device on a side stream and runs the kernels over each
+ *   staged chunk (Algorithm 2's stage-and-merge pipeline); it returns once
+ *   every chunk is enqueued, and the experts are no longer read.  Otherwise
+ *   they are device memory.  The caller owns every buffer; the library only
+ *   reads inputs and writes the named outputs.  The library keeps a
+ *   per-device workspace (block tables, plan scratch, byte counters,
+ *   staging buffers) that mp_release() frees.
  * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Work is
  *   enqueued on it; calls return once enqueued unless stated otherwise.
  *   Calls that fill a host-side stats struct synchronise the stream first.
@@ -62,7 +69,7 @@ extern "C" {
 #define MP_E_HIP (-4)         /* a HIP runtime call failed */
 
 typedef enum { MP_F32 = 0, MP_BF16 = 1 } mp_dtype;
-typedef enum { MP_DEVICE = 0, MP_HOST_PINNED = 1 } mp_residency;
+typedef enum { MP_DEVICE = 0, MP_HOST_PINNED = 1, MP_HOST_PAGEABLE = 2 } mp_residency;
 typedef enum { MP_COMBINE_LINEAR = 0, MP_COMBINE_SIGN_ELECT = 1 } mp_combine;
 /* mp_plan options (bit flags; 0 is the literal Algorithm 1). */
 typedef enum { MP_PLAN_PER_BYTE = 1, MP_PLAN_SKIP_ZERO = 2 } mp_plan_flags;
@@ -87,7 +94,8 @@ typedef struct mp_io_stats {
     uint64_t expert_bytes; /* expert bytes the merge kernels loaded */
     uint64_t base_bytes;   /* base bytes read */
     uint64_t out_bytes;    /* output bytes written */
-    uint64_t h2d_bytes;    /* expert bytes read over PCIe (MP_HOST_PINNED), else 0 */
+    uint64_t h2d_bytes;    /* expert bytes moved over PCIe (MP_HOST_PINNED: read by
+                              the kernels; MP_HOST_PAGEABLE: staged copies), else 0 */
 } mp_io_stats;
 
 /* Number of blocks G of a layout (Section 2's block partition).
@@ -103,8 +111,8 @@ int mp_layout_blocks(const mp_layout* layout, int64_t* n_blocks);
  * becomes p_l + p_(l xor s); S = p_0.  (The paper fixes no order; a fixed
  * one makes plans reproducible bit for bit.)
  *   sumsq: device float[G*K], written at uid = g*K + i.
- * Asynchronous on `stream`.  With MP_HOST_PINNED every expert byte crosses
- * PCIe once (the amortised catalog construction). */
+ * Asynchronous on `stream`.  With MP_HOST_PINNED or MP_HOST_PAGEABLE every
+ * expert byte crosses PCIe once (the amortised catalog construction). */
 int mp_index_blocks(const mp_layout* layout, const void* base,
                     const void* const* experts, int32_t K, int32_t residency,
                     float* sumsq, void* stream);
@@ -206,6 +214,13 @@ int mp_merge_dare(const mp_layout* layout, const void* base,
                   const uint32_t* mask, double p, uint32_t seed, int32_t combine,
                   const float* alpha, float lambda, void* out, mp_io_stats* io,
                   void* stream);
+
+/* Staging for MP_HOST_PAGEABLE: the bytes of each of the two pinned host
+ * buffers (and of their two device counterparts) that chunks of packed
+ * expert blocks pass through; default 256 MiB, rounded down to 256 bytes.
+ * Takes effect at the next host-pageable call (buffers are reallocated).
+ * MP_E_ARG outside [1 MiB, 4 GiB]. */
+int mp_set_stage_bytes(uint64_t bytes);
 
 /* Message for the last failing call on this thread ("" if none). */
 const char* mp_last_error(void);

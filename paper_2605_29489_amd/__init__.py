@@ -27,12 +27,12 @@ MP_E_UNSUPPORTED = -2
 MP_E_NOMEM = -3
 MP_E_HIP = -4
 MP_F32, MP_BF16 = 0, 1
-MP_DEVICE, MP_HOST_PINNED = 0, 1
+MP_DEVICE, MP_HOST_PINNED, MP_HOST_PAGEABLE = 0, 1, 2
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
 MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 
 EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_ties",
-           "mp_merge_ties_tau", "mp_merge_dare", "mp_last_error", "mp_release")
+           "mp_merge_ties_tau", "mp_merge_dare", "mp_set_stage_bytes", "mp_last_error", "mp_release")
 
 
 class mp_layout(C.Structure):
@@ -81,6 +81,8 @@ def _load():
     L.mp_merge_dare.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, u32, i32,
                                 C.POINTER(C.c_float), C.c_float, vp, C.POINTER(mp_io_stats), vp]
     L.mp_last_error.restype = C.c_char_p
+    L.mp_set_stage_bytes.argtypes = [u64]
+    L.mp_set_stage_bytes.restype = i32
     L.mp_last_error.argtypes = []
     L.mp_release.argtypes = []
     for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_ties",
@@ -215,6 +217,10 @@ def mp_merge_dare(layout: Layout, base, experts, mask, p: float, seed: int, comb
 
 def mp_last_error() -> str:
     return lib.mp_last_error().decode()
+
+
+def mp_set_stage_bytes(nbytes: int):
+    _check(lib.mp_set_stage_bytes(int(nbytes)))
 
 
 def mp_release():

@@ -313,6 +313,24 @@ int check_pinned_buffer(const void* p, size_t bytes, const char* name, const voi
     return MP_OK;
 }
 
+// Host memory of any kind (pageable or pinned) for MP_HOST_PAGEABLE: the
+// library reads it on the host only.  Device memory is refused; the size of
+// an ordinary host allocation cannot be checked (the caller guarantees it).
+int check_host_buffer(const void* p, const char* name)
+{
+    if (p == nullptr)
+        return fail(MP_E_ARG, "%s is NULL", name);
+    hipPointerAttribute_t a;
+    std::memset(&a, 0, sizeof a);
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();  // unknown to HIP: ordinary host memory
+        return MP_OK;
+    }
+    if (a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeArray)
+        return fail(MP_E_ARG, "%s is device memory (use MP_DEVICE)", name);
+    return MP_OK;
+}
+
 bool overlaps(const Range& a, const Range& b)
 {
     return a.n && b.n && a.p < b.p + b.n && b.p < a.p + a.n;
@@ -336,8 +354,8 @@ int check_common(const mp_layout* L, const void* base, const void* const* expert
         return rc;
     if (K < 1 || K > kMaxK)
         return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
-    if (residency != MP_DEVICE && residency != MP_HOST_PINNED)
-        return fail(MP_E_ARG, "residency %d is not MP_DEVICE or MP_HOST_PINNED", residency);
+    if (residency != MP_DEVICE && residency != MP_HOST_PINNED && residency != MP_HOST_PAGEABLE)
+        return fail(MP_E_ARG, "residency %d is not MP_DEVICE, MP_HOST_PINNED or MP_HOST_PAGEABLE", residency);
     const int64_t G = count_blocks(L);
     if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
         return fail(MP_E_ARG, "K * G = %lld does not fit 32-bit unit ids", (long long)(G * K));
@@ -357,8 +375,10 @@ int check_common(const mp_layout* L, const void* base, const void* const* expert
         const void* dev = experts[i];
         if (residency == MP_DEVICE)
             rc = check_device_buffer(experts[i], c->ckpt_bytes, nm);
-        else
+        else if (residency == MP_HOST_PINNED)
             rc = check_pinned_buffer(experts[i], c->ckpt_bytes, nm, &dev);
+        else
+            rc = check_host_buffer(experts[i], nm);
         if (rc)
             return rc;
         c->ex.p[i] = dev;
@@ -411,8 +431,13 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
             return hip_fail(e, "counter reset");
     }
     mp_io_stats st{};
-    if ((e = launch_merge(bt, a, base, c.ex, K, mask, out, ctr, s)) != hipSuccess)
+    uint64_t staged = 0;
+    if (residency == MP_HOST_PAGEABLE) {
+        if ((e = stage_merge(bt, a, base, experts, K, mask, out, ctr, s, &staged)) != hipSuccess)
+            return hip_fail(e, "staged merge");
+    } else if ((e = launch_merge(bt, a, base, c.ex, K, mask, out, ctr, s)) != hipSuccess) {
         return hip_fail(e, "merge launch");
+    }
     if (io) {
         if ((e = hipMemcpyAsync(c.ws->h_counters, ctr, sizeof(unsigned long long) * 256,
                                 hipMemcpyDeviceToHost, s)) != hipSuccess)
@@ -425,6 +450,8 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
         st.expert_bytes = sum;
         if (residency == MP_HOST_PINNED)
             st.h2d_bytes = sum;  // expert blocks are read over PCIe, nothing else crosses it
+        else if (residency == MP_HOST_PAGEABLE)
+            st.h2d_bytes = staged;  // the packed selected blocks
         st.base_bytes = (uint64_t)bt.P * (uint64_t)bt.esize;
         st.out_bytes = st.base_bytes;
         *io = st;
@@ -465,7 +492,13 @@ int mp_index_blocks(const mp_layout* layout, const void* base, const void* const
     if ((rc = check_device_buffer(sumsq, sizeof(float) * (size_t)(bt.G * K), "sumsq")))
         return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = launch_index(bt, base, c.ex, K, sumsq, s);
+    hipError_t e;
+    if (residency == MP_HOST_PAGEABLE) {
+        uint64_t staged = 0;
+        e = stage_index(bt, base, experts, K, false, 0.0, sumsq, nullptr, s, &staged);
+    } else {
+        e = launch_index(bt, base, c.ex, K, sumsq, s);
+    }
     if (e != hipSuccess)
         return hip_fail(e, "index launch");
     return MP_OK;
@@ -489,7 +522,14 @@ int mp_index_ties(const mp_layout* layout, const void* base, const void* const* 
         return rc;
     if ((rc = check_device_buffer(tau, sizeof(uint32_t) * (size_t)(bt.G * K), "tau")))
         return rc;
-    hipError_t e = launch_index_ties(bt, base, c.ex, K, density, sumsq, tau, static_cast<hipStream_t>(stream));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (residency == MP_HOST_PAGEABLE) {
+        uint64_t staged = 0;
+        e = stage_index(bt, base, experts, K, true, density, sumsq, tau, s, &staged);
+    } else {
+        e = launch_index_ties(bt, base, c.ex, K, density, sumsq, tau, s);
+    }
     if (e != hipSuccess)
         return hip_fail(e, "index launch");
     return MP_OK;
@@ -629,9 +669,20 @@ int mp_merge_dare(const mp_layout* layout, const void* base, const void* const* 
 
 const char* mp_last_error(void) { return g_err.c_str(); }
 
+int mp_set_stage_bytes(uint64_t bytes)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    if (bytes < (uint64_t(1) << 20) || bytes > (uint64_t(4) << 30))
+        return fail(MP_E_ARG, "staging size %llu must be in [1 MiB, 4 GiB]", (unsigned long long)bytes);
+    set_stage_bytes((size_t)(bytes & ~uint64_t(255)));
+    return MP_OK;
+}
+
 void mp_release(void)
 {
     std::lock_guard<std::mutex> lock(g_mu);
+    release_stagers();
     for (auto& kv : g_tables)
         free_table(*kv.second);
     g_tables.clear();

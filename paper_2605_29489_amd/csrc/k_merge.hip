@@ -34,6 +34,20 @@ struct DevSrc {
     }
 };
 
+// Selected expert blocks staged in device memory (host experts): the
+// launch covers blocks b0 .. b0 + grid - 1; block b0 + j's selected experts
+// lie back to back, in increasing expert order (rank r), from stage + soff[j].
+struct StagedSrc {
+    const char* stage;
+    const uint64_t* soff;
+    int64_t b0;
+    __device__ uint32_t block(int64_t b) const { return (uint32_t)(b0 + b); }
+    __device__ const uint4* expert(int i, int r, int64_t b, uint64_t off, uint32_t n, int es) const
+    {
+        return reinterpret_cast<const uint4*>(stage + soff[b] + (uint64_t)r * n * (uint64_t)es);
+    }
+};
+
 __device__ inline void count_expert_bytes(unsigned long long* ctr, uint32_t m, uint32_t n, int es)
 {
     if (ctr != nullptr && threadIdx.x == 0 && m != 0u)
@@ -946,6 +960,16 @@ hipError_t launch_merge(const BlockTable& bt, const MergeArgs& a, const void* ba
     if (bt.dtype == 0)
         return launch_typed<0>(bt, a, src, base, K, mask, bt.G, out, counters, s);
     return launch_typed<1>(bt, a, src, base, K, mask, bt.G, out, counters, s);
+}
+
+hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const void* base, int K,
+                               const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s,
+                               const void* stage, const uint64_t* soff, int64_t b0, int64_t nb)
+{
+    StagedSrc src{static_cast<const char*>(stage), soff, b0};
+    if (bt.dtype == 0)
+        return launch_typed<0>(bt, a, src, base, K, mask, nb, out, counters, s);
+    return launch_typed<1>(bt, a, src, base, K, mask, nb, out, counters, s);
 }
 
 }  // namespace mp

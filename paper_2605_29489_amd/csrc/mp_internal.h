@@ -96,4 +96,24 @@ hipError_t launch_merge(const BlockTable& bt, const MergeArgs& a, const void* ba
                         const ExpertPtrs& ex, int K, const uint32_t* mask, void* out,
                         unsigned long long* counters, hipStream_t s);
 
+// The merge over blocks [b0, b0 + nb) with the selected expert blocks staged
+// in device memory: block b0 + j's selected experts lie back to back, in
+// increasing expert order, from stage + soff[j].
+hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const void* base, int K,
+                               const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s,
+                               const void* stage, const uint64_t* soff, int64_t b0, int64_t nb);
+
+// ---------------------------------------------------------------- host experts (stage.hip)
+// Experts in host memory of any kind, streamed through pinned staging
+// buffers; h2d receives the bytes copied to the device.  The functions
+// return once every chunk is enqueued on `s` (the experts are no longer
+// read); staging buffers are reused by the next call after its kernels.
+void set_stage_bytes(size_t bytes);
+void release_stagers();
+hipError_t stage_index(const BlockTable& bt, const void* base, const void* const* experts, int K, bool ties,
+                       double density, float* sumsq, uint32_t* tau, hipStream_t s, uint64_t* h2d);
+hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* base, const void* const* experts,
+                       int K, const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s,
+                       uint64_t* h2d);
+
 }  // namespace mp

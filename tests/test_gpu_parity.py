@@ -77,6 +77,8 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
     base = to_dev(base_np, dtype)
     if res == mp.MP_HOST_PINNED:
         exps = [to_pinned(e, dtype) for e in exps_np]
+    elif res == mp.MP_HOST_PAGEABLE:  # ordinary host memory (the numpy arrays themselves)
+        exps = [torch.from_numpy(e) for e in exps_np]
     else:
         exps = [to_dev(e, dtype) for e in exps_np]
     sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
@@ -137,6 +139,8 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
         assert io["expert_bytes"] == read, "kernels loaded bytes outside the plan"
         if res == mp.MP_HOST_PINNED:  # only those blocks cross PCIe
             assert io["h2d_bytes"] == read
+        elif res == mp.MP_HOST_PAGEABLE:  # the staged copies are exactly the selected blocks
+            assert io["h2d_bytes"] == st["cost_bytes"]
         else:
             assert io["h2d_bytes"] == 0
         results.append((B, st, nb))
@@ -210,8 +214,60 @@ def test_host_pinned_rejects_device_and_pageable_experts(mp):
             x.free()
 
 
+@pytest.mark.parametrize("op", ["avg", "ties", "ties_tau", "dare_lin", "dare_sign"])
+def test_host_pageable_experts_all_ops(mp, op):
+    # experts in ordinary host memory: the selected blocks are packed into
+    # pinned staging, copied to the device and merged chunk by chunk; same
+    # bits as device-resident experts, and the staged bytes are the plan cost
+    spec = _mini_qwen()
+    base, exps = make_family(spec, seed=1)
+    kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0, p=0.9, seed=7)
+    _say(f"case mini-qwen bf16 {op}, pageable host experts")
+    _run_all(mp, spec, base, exps, op, [0, 0.3, 1.0], residency=mp.MP_HOST_PAGEABLE, **kw)
+
+
+def test_host_pageable_small_staging_many_chunks(mp):
+    # 1 MiB staging buffers: the index (6.7 MB of experts) and the merges
+    # cross many chunks, reusing both buffers several times; then ragged
+    # fp32 blocks with K = 6 (groups of experts in the TIES kernel)
+    mp.mp_set_stage_bytes(1 << 20)
+    try:
+        spec = _mini_qwen(n_layers=1)
+        base, exps = make_family(spec, seed=4)
+        kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0, p=0.9, seed=7)
+        for op in ("avg", "ties", "ties_tau", "dare_lin", "dare_sign"):
+            _say(f"case mini-qwen bf16 {op}, pageable host experts, 1 MiB staging")
+            _run_all(mp, spec, base, exps, op, [0.1, 0.45, 1.0], residency=mp.MP_HOST_PAGEABLE, **kw)
+        spec = _ragged_f32(K=6)
+        base, exps = make_family(spec, K=6, seed=21)
+        kw = dict(alpha=[1.0 / 6] * 6, density=0.3, lam=1.0, p=0.7, seed=11)
+        for op in ("avg", "ties", "ties_tau", "dare_sign"):
+            _say(f"case ragged fp32 K=6 {op}, pageable host experts, 1 MiB staging")
+            _run_all(mp, spec, base, exps, op, [0.2, 0.65, 1.0], residency=mp.MP_HOST_PAGEABLE, **kw)
+    finally:
+        mp.mp_set_stage_bytes(256 << 20)
+
+
+def test_host_pageable_rejects_device_experts_and_bad_staging(mp):
+    import torch
+    spec = _mini_qwen(n_layers=1)
+    L, lay = _lay(mp, spec)
+    base, exps = make_family(spec, seed=3)
+    b = to_dev(base, "bf16")
+    G = oracle.Blocks(lay.numel, lay.block_elems).G
+    sumsq = torch.empty(G * 4, dtype=torch.float32, device="cuda")
+    dev = [to_dev(e, "bf16") for e in exps]
+    with pytest.raises(mp.MPError) as err:
+        mp.mp_index_blocks(L, b, dev, sumsq, residency=mp.MP_HOST_PAGEABLE)
+    assert err.value.code == mp.MP_E_ARG
+    for n in (0, (1 << 20) - 1, (4 << 30) + 1):
+        with pytest.raises(mp.MPError) as err:
+            mp.mp_set_stage_bytes(n)
+        assert err.value.code == mp.MP_E_ARG
+
+
 def test_toy_config_avg_full_parity(mp):
-    # BASELINE toy family: fp32 8 x (512x1024), K=4, AVG 1/K, B = 50%
+    # the toy family: fp32 8 x (512x1024), K=4, AVG 1/K, B = 50%
     spec = family_spec("toy")
     base, exps = make_family(spec, seed=0)
     _say("case toy fp32 avg")
