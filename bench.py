@@ -128,8 +128,9 @@ PCIE_PEAK = 64.0e9  # PCIe Gen5 x16, one direction, nominal bytes/s
 
 def run_sweep(args):
     """One of the other workload shapes: index once, then plan + merge at each
-    budget of its sweep.  Experts are device-resident or stay in pinned host
-    memory (kernels read the selected blocks over PCIe)."""
+    budget of its sweep.  Experts are device-resident, stay in pinned host
+    memory (kernels read the selected blocks over PCIe), or stay in ordinary
+    host memory (the selected blocks are staged and copied over PCIe)."""
     import numpy as np
     import torch
 
@@ -142,13 +143,19 @@ def run_sweep(args):
     lay = spec.layout
     K = spec.K
     P = lay.n_params
-    pinned = cfg["residency"] == "host_pinned"
-    res = mp.MP_HOST_PINNED if pinned else mp.MP_DEVICE
+    where = {"config": cfg["residency"], "device": "device", "pinned": "host_pinned",
+             "pageable": "host_pageable"}[args.residency]
+    pinned = where == "host_pinned"
+    pageable = where == "host_pageable"
+    host = pinned or pageable  # experts cross PCIe: that link bounds the merge
+    res = mp.MP_HOST_PINNED if pinned else (mp.MP_HOST_PAGEABLE if pageable else mp.MP_DEVICE)
     dt = mp.MP_F32 if lay.dtype == "f32" else mp.MP_BF16
     L = mp.Layout(lay.numel, lay.block_elems, dt)
     G = mp.mp_layout_blocks(L)
-    log(f"generating {spec.description}: P={P} G={G} experts {'pinned host' if pinned else 'device'}")
-    base, exps = make_family_device(spec, K=K, seed=0, device="cuda", experts_on_host_pinned=pinned)
+    where_txt = {"host_pinned": "pinned host", "host_pageable": "pageable host"}.get(where, "device")
+    log(f"generating {spec.description}: P={P} G={G} experts {where_txt}")
+    base, exps = make_family_device(spec, K=K, seed=0, device="cuda",
+                                    experts_on_host="pinned" if pinned else ("pageable" if pageable else None))
     torch.cuda.synchronize()
     sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
     mask = torch.empty(G, dtype=torch.int32, device="cuda")
@@ -191,32 +198,34 @@ def run_sweep(args):
         for _ in range(max(0, args.warmup)):
             merge()
         ms = float(np.median([timed(merge)[0] for _ in range(reps)]))
-        alg = 2 * P * es + st["cost_bytes"] + 4 * G if not pinned else st["cost_bytes"]
+        alg = 2 * P * es + st["cost_bytes"] + 4 * G if not host else st["cost_bytes"]
         rows.append({"budget_frac": round(f, 4), "budget_bytes": B, "cost_bytes": st["cost_bytes"],
                      "h2d_bytes": io["h2d_bytes"], "n_selected": st["n_selected"], "plan_ms": round(plan_ms, 4),
                      "merge_ms": round(ms, 4), "merge_params_per_s": P / (ms * 1e-3),
-                     ("h2d_GBps" if pinned else "merge_effective_GBps"): alg / (ms * 1e-3) / 1e9})
+                     ("h2d_GBps" if host else "merge_effective_GBps"): alg / (ms * 1e-3) / 1e9})
     step_ms = idx_ms + sum(r["plan_ms"] + r["merge_ms"] for r in rows)
     dma = None
-    if pinned:  # measured peak: one pinned expert -> device with the copy engine
-        dst = torch.empty_like(base)
-        dst.copy_(exps[0], non_blocking=True)
-        dma_ms, _ = timed(lambda: dst.copy_(exps[0], non_blocking=True))
-        dma = P * es / (dma_ms * 1e-3)
-        del dst
-    tot_bytes = sum(r["cost_bytes"] if pinned else 2 * P * es + r["cost_bytes"] + 4 * G for r in rows)
+    if host:  # measured peak: pinned host -> device with the copy engine (1 GiB, or one expert)
+        n = P if pinned else min(P, (1 << 30) // es)
+        src = exps[0] if pinned else exps[0][:n].pin_memory()
+        dst = torch.empty(n, dtype=base.dtype, device=base.device)
+        dst.copy_(src[:n], non_blocking=True)
+        dma_ms, _ = timed(lambda: dst.copy_(src[:n], non_blocking=True))
+        dma = n * es / (dma_ms * 1e-3)
+        del dst, src
+    tot_bytes = sum(r["cost_bytes"] if host else 2 * P * es + r["cost_bytes"] + 4 * G for r in rows)
     tot_ms = sum(r["merge_ms"] for r in rows)
     achieved = tot_bytes / (tot_ms * 1e-3)
-    peak = PCIE_PEAK if pinned else HBM_PEAK
+    peak = PCIE_PEAK if host else HBM_PEAK
     result = {
         "metric": f"merged params/sec, budgeted {op.upper()} merge sweep",
         "value": len(rows) * P / (step_ms * 1e-3), "unit": "params/s", "n_gpus": 1, "steps": reps,
         "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": f"{spec.description}; {op} {cfg}", "storage_dtype": lay.dtype, "params": P,
-                   "blocks": G, "K": K, "experts": "pinned host" if pinned else "device",
+                   "blocks": G, "K": K, "experts": where_txt,
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "pcie" if pinned else "hbm", "achieved": achieved / 1e9, "peak": peak / 1e9,
+        "roofline": {"bound": "pcie" if host else "hbm", "achieved": achieved / 1e9, "peak": peak / 1e9,
                      "unit": "GB/s", "frac": achieved / peak, "traffic": None,
                      "measured_dma_h2d_GBps": None if dma is None else dma / 1e9},
         "breakdown": {"index_ms": round(idx_ms, 4), "per_budget": rows},
@@ -235,6 +244,8 @@ def main():
                     help="the headline (default) or one of the other workload shapes")
     ap.add_argument("--layers", type=int, default=None,
                     help="other workloads: keep only this many transformer layers (host memory)")
+    ap.add_argument("--residency", default="config", choices=("config", "device", "pinned", "pageable"),
+                    help="other workloads: where the experts live (default: the workload's own)")
     ap.add_argument("--ties", default="catalog", choices=("catalog", "in-merge"),
                     help="where the TIES trim thresholds are found: in the index pass (catalog) or in each merge")
     ap.add_argument("--calibration-copy", action="store_true",

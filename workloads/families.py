@@ -278,11 +278,12 @@ def pinned_empty(n: int, dtype_name: str):
 
 
 def make_family_device(spec: FamilySpec, K: Optional[int] = None, seed: int = 0, device="cuda",
-                       experts_on_host_pinned: bool = False):
+                       experts_on_host_pinned: bool = False, experts_on_host: Optional[str] = None):
     """Generate base + K experts as torch tensors on ``device``.
 
-    With ``experts_on_host_pinned`` the experts are generated on the device one
-    at a time and copied into pinned host tensors (the base stays on device).
+    ``experts_on_host`` = "pinned" (or ``experts_on_host_pinned``) or
+    "pageable": the experts are generated on the device one at a time and
+    copied into pinned, or ordinary, host tensors (the base stays on device).
     The values depend on the device's RNG, so families generated on different
     devices differ; consumers that need the same bytes copy them.
     """
@@ -292,19 +293,22 @@ def make_family_device(spec: FamilySpec, K: Optional[int] = None, seed: int = 0,
     lay = spec.layout
     tdt = torch.float32 if lay.dtype == "f32" else torch.bfloat16
     P = lay.n_params
+    host = experts_on_host or ("pinned" if experts_on_host_pinned else None)
+    if host not in (None, "pinned", "pageable"):
+        raise ValueError(f"experts_on_host must be 'pinned' or 'pageable', not {host!r}")
     base = torch.empty(P, dtype=tdt, device=device)
-    if not experts_on_host_pinned:
+    if host is None:
         experts = [torch.empty(P, dtype=tdt, device=device) for _ in range(K)]
         _fill(torch, spec, K, seed, device, base, experts)
         return base, experts
-    # one device scratch expert at a time, then copy to pinned host memory
+    # one device scratch expert at a time, then copy to host memory
     experts = []
     scratch = torch.empty(P, dtype=tdt, device=device)
     # generate base once with K=0 then each expert with the same per-expert streams
     _fill(torch, spec, 0, seed, device, base, [])
     for i in range(K):
         _fill_one_expert(torch, spec, i, seed, device, base, scratch)
-        h = pinned_empty(P, lay.dtype)
+        h = pinned_empty(P, lay.dtype) if host == "pinned" else torch.empty(P, dtype=tdt)
         h.copy_(scratch)
         experts.append(h)
     del scratch
