@@ -75,6 +75,17 @@ __device__ static inline const uint4* chunk_ptr(const void* base, uint64_t elem_
 // ---------------------------------------------------------------- Philox4x32-10
 // Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3"
 // (SC 2011): ten rounds of two 32x32->64 multiplies with the Weyl-bumped key.
+// a ^ b ^ k with k wave-uniform, as one CDNA4 three-input bitwise op (truth
+// table 0x96 is the odd-parity function of its inputs).  Left to itself the
+// compiler issues two v_xor_b32 here, and Philox's rounds are most of the
+// VALU work of the DARE kernels.
+__device__ static inline uint32_t xor3_u32(uint32_t a, uint32_t b, uint32_t k)
+{
+    uint32_t r;
+    asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(k));
+    return r;
+}
+
 __device__ static inline uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1)
 {
     constexpr uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
@@ -86,7 +97,7 @@ __device__ static inline uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1)
         const uint64_t p1 = (uint64_t)M1 * c.z;
         const uint32_t lo0 = (uint32_t)p0, hi0 = (uint32_t)(p0 >> 32);
         const uint32_t lo1 = (uint32_t)p1, hi1 = (uint32_t)(p1 >> 32);
-        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+        c = make_uint4(xor3_u32(hi1, c.y, k0), lo1, xor3_u32(hi0, c.w, k1), lo0);
         k0 += W0;
         k1 += W1;
     }
