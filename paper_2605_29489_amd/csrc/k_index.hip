@@ -64,7 +64,8 @@ __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, Ex
 {
     const int64_t g = blockIdx.x;
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    // wave-uniform, so that ex.p[i] is a scalar load
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint64_t off = boff[g];
     const uint32_t nch = blen[g] / Fmt<DT>::V;
     const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
@@ -103,7 +104,7 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
     const int64_t g = blockIdx.x;
     const int t = threadIdx.x;
     const int lane = t & 63;
-    const int wave = t >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);  // wave-uniform: ex.p[i] is a scalar load
     const uint64_t off = boff[g];
     const uint32_t n = blen[g];
     const uint32_t nch = n / V;
@@ -112,21 +113,8 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
         const double kk = ceil(density * (double)n);
         k = (kk >= (double)n) ? n : (uint32_t)kk;
     }
-    const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
-#pragma unroll
-    for (int q = 0; q < R / 4; ++q) {
-        const uint32_t c = (uint32_t)(q * 256 + t);
-        xb[c] = (c < nch) ? b[c] : make_uint4(0u, 0u, 0u, 0u);
-    }
-    __syncthreads();
-    for (int i = wave; i < K; i += 4) {
-        const uint4* e = chunk_ptr(ex.p[i], off, Fmt<DT>::esize);
-        uint4 xe[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const uint32_t c = (uint32_t)(r * 64 + lane);
-            xe[r] = (c < nch) ? e[c] : make_uint4(0u, 0u, 0u, 0u);
-        }
+    // one unit: expert i's chunks (xe) against the staged base
+    auto unit = [&](int i, const uint4 (&xe)[R]) {
         float d[E];
         float p = 0.0f;
 #pragma unroll
@@ -149,6 +137,33 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
                 sumsq[g * K + i] = p;
             tau[g * K + i] = th;
         }
+    };
+    auto load_expert = [&](int i, uint4 (&xe)[R]) {
+        const uint4* e = chunk_ptr(ex.p[i], off, Fmt<DT>::esize);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const uint32_t c = (uint32_t)(r * 64 + lane);
+            xe[r] = (c < nch) ? e[c] : make_uint4(0u, 0u, 0u, 0u);
+        }
+    };
+    // the wave's first expert is read before the base is staged, so that the
+    // two reads overlap; further experts (K > 4) are read one at a time
+    uint4 xf[R];
+    if (wave < K)
+        load_expert(wave, xf);
+    const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
+#pragma unroll
+    for (int q = 0; q < R / 4; ++q) {
+        const uint32_t c = (uint32_t)(q * 256 + t);
+        xb[c] = (c < nch) ? b[c] : make_uint4(0u, 0u, 0u, 0u);
+    }
+    __syncthreads();
+    if (wave < K)
+        unit(wave, xf);
+    for (int i = wave + 4; i < K; i += 4) {
+        uint4 xe[R];
+        load_expert(i, xe);
+        unit(i, xe);
     }
 }
 
