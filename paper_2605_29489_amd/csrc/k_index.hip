@@ -9,6 +9,8 @@
 // the scores -- and therefore the plan -- are reproducible bit for bit.
 // The base block is re-read per expert from L2 (it stays resident: 8-16 KiB
 // per workgroup), so HBM sees it once.
+#include <cmath>
+
 #include "device_common.h"
 #include "mp_internal.h"
 #include "ties_select.h"
@@ -93,7 +95,7 @@ __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, Ex
 template <int DT>
 __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
     const void* __restrict__ base, ExpertPtrs ex, int K, const uint64_t* __restrict__ boff,
-    const uint32_t* __restrict__ blen, uint32_t n_full, uint32_t k_full, double density,
+    const uint32_t* __restrict__ blen, uint32_t n_full, uint32_t k_full, double density, float gcoef,
     float* __restrict__ sumsq, uint32_t* __restrict__ tau)
 {
     constexpr int V = Fmt<DT>::V;
@@ -131,7 +133,11 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
 #pragma unroll
         for (int s = 32; s >= 1; s >>= 1)
             p = p + __shfl_xor(p, s);
-        const uint32_t th = (k == 0u) ? 0xffffffffu : wave_kth_largest<E>(reinterpret_cast<char*>(&rows[0][0]), wave * ties::NB * 4, d, k, lane);
+        // a guess at tau: gcoef times the deltas' root mean square
+        const uint32_t guess = __float_as_uint(gcoef * sqrtf(p / (float)n));
+        const uint32_t th = (k == 0u) ? 0xffffffffu
+                                      : wave_kth_largest<E>(reinterpret_cast<char*>(&rows[0][0]), wave * ties::NB * 4,
+                                                            d, k, lane, guess);
         if (lane == 0) {
             if (sumsq != nullptr)
                 sumsq[g * K + i] = p;
@@ -169,6 +175,22 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
 
 }  // namespace
 
+// z with P(|Z| > z) = rho for a standard normal Z (bisection on erfc).
+static double normal_two_sided_quantile(double rho)
+{
+    if (!(rho > 0.0) || rho >= 1.0)
+        return 0.0;
+    double lo = 0.0, hi = 40.0;
+    for (int it = 0; it < 200; ++it) {
+        const double mid = 0.5 * (lo + hi);
+        if (erfc(mid / sqrt(2.0)) > rho)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
 hipError_t launch_index_ties(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
                              double density, float* sumsq, uint32_t* tau, hipStream_t s)
 {
@@ -177,13 +199,18 @@ hipError_t launch_index_ties(const BlockTable& bt, const void* base, const Exper
     const uint32_t n_full = (uint32_t)bt.block_elems;
     const double kk = ceil(density * (double)n_full);
     const uint32_t k_full = (kk >= (double)n_full) ? n_full : (uint32_t)kk;
+    // The selector's first guess at a unit's threshold: 0.6 of the rho-tail
+    // quantile of a normal with the deltas' RMS (for normal deltas about
+    // 0.6 tau).  It only decides which values the first histogram pass
+    // counts; the thresholds are exact for any data.
+    const float gcoef = (float)(0.6 * normal_two_sided_quantile(density));
     const dim3 grid((unsigned)bt.G), block(256);
     if (bt.dtype == 0)
         hipLaunchKernelGGL(k_index_ties<0>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, n_full, k_full,
-                           density, sumsq, tau);
+                           density, gcoef, sumsq, tau);
     else
         hipLaunchKernelGGL(k_index_ties<1>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, n_full, k_full,
-                           density, sumsq, tau);
+                           density, gcoef, sumsq, tau);
     return hipGetLastError();
 }
 

@@ -255,8 +255,16 @@ __device__ inline float max3_abs(float m, float a, float b)
 // it out), 1 <= k <= the number of values that are not padding; padding
 // values are zeros, which cannot change the k largest.  The wave-private
 // LDS row of NB words starts row_off bytes after base.
+//
+// guess (wave-uniform) is a magnitude pattern expected at or below the
+// answer, 0 for none.  The histogram then first counts only the values at or
+// above the floor of guess's bin: the bins from there up are exact, so a cut
+// found among them is the answer, and one not found means the answer lies
+// lower, when the whole window is counted again.  A good guess leaves most
+// values out of the LDS atomics (and their bank conflicts).
 template <int E>
-__device__ inline uint32_t wave_kth_largest(char* base, int row_off, const float (&d)[E], uint32_t k, int lane)
+__device__ inline uint32_t wave_kth_largest(char* base, int row_off, const float (&d)[E], uint32_t k, int lane,
+                                            uint32_t guess = 0u)
 {
     using namespace ties;
     uint32_t* __restrict__ h = reinterpret_cast<uint32_t*>(base + row_off);
@@ -267,19 +275,28 @@ __device__ inline uint32_t wave_kth_largest(char* base, int row_off, const float
     const uint32_t bmax = wave_max_u32(__float_as_uint(mxf));
     if (bmax == 0u)
         return 0u;  // all zero
-#pragma unroll
-    for (int q = 0; q < NB / 256; ++q)
-        *reinterpret_cast<uint4*>(&h[4 * (q * 64 + lane)]) = make_uint4(0u, 0u, 0u, 0u);
-    wave_lds_sync();
     int wb;
     const uint32_t koff = window_koff(bmax, lane, &wb) + (uint32_t)row_off;
-    const uint32_t flo = window_floor(wb);
-    uint32_t inc = 1u;
+    const uint32_t wfloor = window_floor(wb);
+    uint32_t flo = (guess > wfloor) ? (guess >> KS) << KS : wfloor;
+    Cut c;
+#pragma unroll 1
+    for (;;) {
 #pragma unroll
-    for (int e = 0; e < E; ++e)
-        window_add<false>(base, __float_as_uint(d[e]), flo, koff, inc);
-    wave_lds_sync();
-    const Cut c = wave_find_from_top<NC>(h, NBIN - 1, k, lane);
+        for (int q = 0; q < NB / 256; ++q)
+            *reinterpret_cast<uint4*>(&h[4 * (q * 64 + lane)]) = make_uint4(0u, 0u, 0u, 0u);
+        wave_lds_sync();
+        uint32_t inc = 1u;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            window_add<false>(base, __float_as_uint(d[e]), flo, koff, inc);
+        wave_lds_sync();
+        c = wave_find_from_top<NC>(h, NBIN - 1, k, lane);
+        if (c.found || flo == wfloor)
+            break;
+        flo = wfloor;  // below the guess: count the whole window
+        wave_lds_sync();
+    }
     if (c.found) {  // else the k-th largest lies below the window
         if (c.aux < c.rank)
             return (uint32_t)(wb + (int)c.bin) << KS;  // the rank-th largest of the bin is its floor

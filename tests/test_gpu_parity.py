@@ -359,6 +359,25 @@ def test_ties_threshold_search_paths(mp):
         _run_all(mp, spec, base, exps, "ties_tau", [0.5, 1.0], density=dens, lam=1.0)
 
 
+def test_ties_threshold_guess_above_tau(mp):
+    # The catalog's selector first counts only values above a guess taken
+    # from the deltas' RMS.  Bimodal deltas (a tenth near 1.0, the rest in
+    # [0.13, 0.2]) put that guess above the k-th largest at density 0.2
+    # while the k-th largest still lies in the window below the maximum: the
+    # full-window pass must find it.  A normal expert takes the first pass.
+    spec = _mini_qwen(n_layers=1, K=2)
+    P = sum(int(np.prod(s)) for _, s in spec.tensors)
+    rng = np.random.default_rng(19)
+    base = oracle.round_bf16(rng.normal(0.0, 0.02, P).astype(np.float32))
+    big = rng.random(P) < 0.1
+    mag = np.where(big, rng.uniform(0.9, 1.1, P), rng.uniform(0.13, 0.2, P))
+    bimodal = mag * np.sign(rng.normal(size=P))
+    exps = _bf16_family_from_deltas(base, [bimodal, rng.normal(0.0, 0.01, P)])
+    for dens in (0.2, 0.12, 0.5):
+        _say(f"case guess above tau density={dens}")
+        _run_all(mp, spec, base, exps, "ties_tau", [1.0], density=dens, lam=1.0)
+
+
 def test_ties_subnormal_deltas(mp):
     # base weights near the bottom of the normal range, deltas subnormal in
     # fp32: the magnitude patterns and the keep test must treat them exactly
