@@ -29,6 +29,12 @@
 
 namespace mp {
 
+// Workgroups of the round-0 kernels (at most).  Each workgroup ends a pass
+// with device-scope atomic adds into the shared histogram, which serialize
+// per address; 512 workgroups measured fastest (2048: the atomics dominate
+// the first digit pass; 256: no faster).
+constexpr int kPlanGrid = 512;
+
 struct PlanCtl {
     unsigned long long brem[9];       // remaining budget before resolving digit d
     unsigned long long prefix[9];     // key prefix with digits < d resolved
@@ -42,6 +48,12 @@ struct PlanCtl {
     unsigned int done;
     unsigned int list_n[2];
     unsigned int error;  // set if an internal invariant failed (reported by the host)
+    // per-workgroup partial sums of the round-0 kernels (selected cost and
+    // count of k_plan_mark, digest terms of k_plan_digest): one plain store
+    // per workgroup, summed by the one-workgroup kernel that follows.  Many
+    // workgroups adding to one device-scope word serialize at the memory
+    // side (the L2 caches are per XCD), which cost tens of microseconds.
+    unsigned long long part[3][kPlanGrid];
 };
 
 namespace {
@@ -329,21 +341,49 @@ __global__ __launch_bounds__(kT) void k_plan_mark(PlanCtl* ctl, const float* __r
     }
     __syncthreads();
     if (t == 0) {
-        const unsigned long long cs = s_cost[0] + s_cost[1] + s_cost[2] + s_cost[3];
-        const unsigned long long cn = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
-        if (cn) {
-            atomicAdd(&ctl->sel_cost, cs);
-            atomicAdd(&ctl->sel_count, cn);
-        }
+        ctl->part[0][blockIdx.x] = s_cost[0] + s_cost[1] + s_cost[2] + s_cost[3];
+        ctl->part[1][blockIdx.x] = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
     }
+}
+
+// Sum of part[row][0 .. n) over one 256-thread workgroup (all threads call
+// it; every thread gets the sum).  The loads are issued together.
+__device__ inline unsigned long long block_sum_parts(const PlanCtl* ctl, int row, int n)
+{
+    __shared__ unsigned long long s[4];
+    const int t = threadIdx.x;
+    unsigned long long a = 0ull;
+#pragma unroll
+    for (int j = 0; j < (kPlanGrid + kT - 1) / kT; ++j) {
+        const int q = j * kT + t;
+        a += (q < n) ? ctl->part[row][q] : 0ull;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        a += __shfl_xor(a, off);
+    __syncthreads();
+    if ((t & 63) == 0)
+        s[t >> 6] = a;
+    __syncthreads();
+    return s[0] + s[1] + s[2] + s[3];
 }
 
 // Close round r: carry the remaining budget, reset the digit state, and
 // finish the plan when everything fit or no cheaper candidate is left.
-__global__ void k_plan_advance(PlanCtl* ctl, int next_list, int reuse_list)
+__global__ __launch_bounds__(kT) void k_plan_advance(PlanCtl* ctl, int next_list, int reuse_list, int n_part)
 {
-    if (threadIdx.x != 0 || ctl->done)
+    // takes in the selections of k_plan_mark's n_part workgroups
+    const int t = threadIdx.x;
+    if (ctl->done)
         return;
+    const unsigned long long cs = block_sum_parts(ctl, 0, n_part);
+    const unsigned long long cn = block_sum_parts(ctl, 1, n_part);
+    for (int q = t; q < 3 * 256; q += kT)
+        (&ctl->hist[0][0])[q] = 0ull;
+    if (t != 0)
+        return;
+    ctl->sel_cost += cs;
+    ctl->sel_count += cn;
     unsigned long long rem;
     if (ctl->all_fit) {
         rem = ctl->brem[0] - ctl->total0;
@@ -355,8 +395,6 @@ __global__ void k_plan_advance(PlanCtl* ctl, int next_list, int reuse_list)
     }
     ctl->brem[0] = rem;
     ctl->prefix[0] = 0ull;
-    for (int q = 0; q < 3 * 256; ++q)
-        (&ctl->hist[0][0])[q] = 0ull;
     ctl->all_fit = 0u;
     ctl->list_n[reuse_list] = 0u;
 }
@@ -516,14 +554,17 @@ __global__ __launch_bounds__(kT) void k_plan_digest(PlanCtl* ctl, const uint32_t
         s[wave] = acc;
     __syncthreads();
     if (t == 0)
-        atomicAdd(&ctl->digest_acc, s[0] + s[1] + s[2] + s[3]);
+        ctl->part[2][blockIdx.x] = s[0] + s[1] + s[2] + s[3];
 }
 
-__global__ void k_plan_final(PlanCtl* ctl, unsigned long long budget, unsigned long long full,
-                             unsigned long long n_units)
+__global__ __launch_bounds__(kT) void k_plan_final(PlanCtl* ctl, unsigned long long budget, unsigned long long full,
+                                                   unsigned long long n_units, int n_part)
 {
+    // takes in the digest terms of k_plan_digest's n_part workgroups
+    const unsigned long long dg = block_sum_parts(ctl, 2, n_part);
     if (threadIdx.x != 0)
         return;
+    ctl->digest_acc += dg;
     ctl->stats[0] = budget;
     ctl->stats[1] = ctl->sel_cost;
     ctl->stats[2] = full;
@@ -544,7 +585,7 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
     hipLaunchKernelGGL(k_plan_init, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget);
     if (bt.G > 0) {
         const int64_t want = (bt.G + kT - 1) / kT;
-        const unsigned grid0 = (unsigned)(want < 2048 ? want : 2048);
+        const unsigned grid0 = (unsigned)std::min<int64_t>(want, kPlanGrid);
         const unsigned gridL = 64;
         const int rounds = bt.n_distinct_len;
         for (int r = 0; r < std::min(rounds, 1); ++r) {
@@ -568,7 +609,7 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
             hipLaunchKernelGGL(k_plan_mark, dim3(grid), dim3(kT), 0, s, ctl, sumsq, w, flags, K, bt.d_len,
                                es, bt.G, src, mask, ps.list[nxt], &ctl->list_n[nxt],
                                (unsigned)ps.list_cap);
-            hipLaunchKernelGGL(k_plan_advance, dim3(1), dim3(64), 0, s, ctl, nxt, r & 1);
+            hipLaunchKernelGGL(k_plan_advance, dim3(1), dim3(kT), 0, s, ctl, nxt, r & 1, (int)grid);
         }
         if (rounds > 1)
             hipLaunchKernelGGL(k_plan_rest, dim3(1), dim3(kT), 0, s, ctl, sumsq, w, flags, K, bt.d_len, es, bt.G,
@@ -576,8 +617,9 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
         const unsigned gridD = grid0;
         hipLaunchKernelGGL(k_plan_digest, dim3(gridD), dim3(kT), 0, s, ctl, mask, bt.G);
     }
-    hipLaunchKernelGGL(k_plan_final, dim3(1), dim3(64), 0, s, ctl, (unsigned long long)budget,
-                       (unsigned long long)full_bytes, (unsigned long long)(bt.G * K));
+    const int n_digest = bt.G > 0 ? (int)std::min<int64_t>((bt.G + kT - 1) / kT, kPlanGrid) : 0;
+    hipLaunchKernelGGL(k_plan_final, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget,
+                       (unsigned long long)full_bytes, (unsigned long long)(bt.G * K), n_digest);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
