@@ -38,6 +38,7 @@ def lib():
                                C.c_uint64, C.c_uint32, C.c_void_p, C.c_void_p]
         L.orc_merge_avg.argtypes = [C.c_int64, i64p, i64p, C.c_int32, C.c_void_p, C.POINTER(C.c_void_p),
                                     C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
+        L.orc_merge_avg_renorm.argtypes = L.orc_merge_avg.argtypes
         L.orc_merge_ties.argtypes = [C.c_int64, i64p, i64p, C.c_int32, C.c_void_p, C.POINTER(C.c_void_p),
                                      C.c_int32, C.c_void_p, C.c_double, C.c_float, C.c_void_p]
         L.orc_merge_dare.argtypes = [C.c_int64, i64p, i64p, C.POINTER(C.c_int32), i64p, C.c_int32,
@@ -151,6 +152,21 @@ def merge_avg(blocks, dtype, base, experts, mask, alpha, out=None, ids=None, dof
     l_a, l_p = _i64(blocks.len[ids])
     _check(L.orc_merge_avg(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
                            len(experts), mask.ctypes.data, alpha.ctypes.data, out.ctypes.data), "avg")
+    return out
+
+
+def merge_avg_renorm(blocks, dtype, base, experts, mask, alpha, out=None, ids=None, doff=None):
+    """Selected-only AVG: alpha renormalised over each block's selected experts."""
+    L = lib()
+    ids, doff = _merge_args(blocks, ids, doff)
+    out = np.empty_like(base) if out is None else out
+    mask = np.ascontiguousarray(mask, np.uint32)
+    alpha = np.ascontiguousarray(alpha, np.float32)
+    d_a, d_p = _i64(doff)
+    l_a, l_p = _i64(blocks.len[ids])
+    _check(L.orc_merge_avg_renorm(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
+                                  len(experts), mask.ctypes.data, alpha.ctypes.data, out.ctypes.data),
+           "avg_renorm")
     return out
 
 

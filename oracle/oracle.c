@@ -310,6 +310,46 @@ int orc_merge_avg(int64_t nb, const int64_t* doff, const int64_t* len, int32_t d
 }
 
 /* ------------------------------------------------------------------ */
+/* Selected-only AVG (Appendix A.1, the coefficient-drift variant):    */
+/* the merge renormalises the coefficients over the experts selected   */
+/* in each block.  For block b, s_b = sum of alpha_i over the selected */
+/* i (fp32 adds from +0, increasing i); beta_i = alpha_i / s_b (IEEE   */
+/* fp32 division) for a selected i and 0 otherwise; s_b = 0 gives      */
+/* beta = 0, so such a block keeps the base.  Then as AVG:             */
+/* acc = fma(beta_i, d_i, acc) over the selected i in increasing       */
+/* order from +0, out = round(x0 + acc).                               */
+/* ------------------------------------------------------------------ */
+int orc_merge_avg_renorm(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                         const void* base, const void* const* experts, int32_t K,
+                         const uint32_t* mask, const float* alpha, void* out)
+{
+    if (check_common(dtype, K, nb))
+        return -1;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int64_t b = 0; b < nb; ++b) {
+        float s = 0.0f;
+        for (int32_t i = 0; i < K; ++i)
+            if ((mask[b] >> i) & 1u)
+                s = s + alpha[i];
+        float beta[32];
+        for (int32_t i = 0; i < K; ++i)
+            beta[i] = (((mask[b] >> i) & 1u) && s != 0.0f) ? alpha[i] / s : 0.0f;
+        for (int64_t j = doff[b]; j < doff[b] + len[b]; ++j) {
+            float x0 = load(base, dtype, j);
+            float acc = 0.0f;
+            for (int32_t i = 0; i < K; ++i) {
+                if (!((mask[b] >> i) & 1u))
+                    continue;
+                float d = load(experts[i], dtype, j) - x0;
+                acc = fmaf(beta[i], d, acc);
+            }
+            store(out, dtype, j, x0 + acc);
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
 /* Sign election and disjoint mean (the second and third TIES steps of */
 /* Appendix A.1), shared by TIES and DARE's sign-elect                  */
 /* combine.  t[r*n + j] holds the (trimmed or dropped) delta of the    */

@@ -49,6 +49,11 @@ int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
 int orc_merge_avg(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
                   const void* base, const void* const* experts, int32_t K,
                   const uint32_t* mask, const float* alpha, void* out);
+/* Selected-only AVG: the coefficients renormalised over each block's
+ * selected experts (Appendix A.1's coefficient-drift variant). */
+int orc_merge_avg_renorm(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
+                         const void* base, const void* const* experts, int32_t K,
+                         const uint32_t* mask, const float* alpha, void* out);
 int orc_merge_ties(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
                    const void* base, const void* const* experts, int32_t K,
                    const uint32_t* mask, double density, float lambda, void* out);

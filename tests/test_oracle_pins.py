@@ -481,6 +481,114 @@ def test_avg_non_anticipatory():
 
 
 # --------------------------------------------------------------------------
+# selected-only (renormalised) AVG, Appendix A.1's coefficient-drift variant
+# --------------------------------------------------------------------------
+
+def test_avg_renorm_single_selected_expert_is_that_expert():
+    # With one selected expert a block's coefficient is alpha_i / alpha_i = 1
+    # whatever alpha_i is, so the block is that expert's block; a block with
+    # nothing selected is the base.
+    rng = np.random.default_rng(21)
+    numel = [4096, 1536, 256, 4096, 4096]
+    b = oracle.Blocks(numel, 4096)
+    for dtype in ("f32", "bf16"):
+        base, exps = _tiny_family(rng, numel, 4, dtype, scale=1e-3)
+        pick = rng.integers(-1, 4, b.G)
+        mask = np.array([0 if i < 0 else 1 << i for i in pick], np.uint32)
+        out = oracle.merge_avg_renorm(b, dtype, base, exps, mask, [0.3, 0.7, 0.1, 1.9])
+        for g in range(b.G):
+            sl = slice(b.off[g], b.off[g] + b.len[g])
+            want = base[sl] if pick[g] < 0 else exps[pick[g]][sl]
+            assert np.array_equal(out[sl], want), (dtype, g)
+
+
+def test_avg_renorm_invariant_to_power_of_two_scaling_of_alpha():
+    # beta = alpha_i / sum(selected alpha) is unchanged, exactly, when every
+    # alpha is scaled by a power of two; plain AVG is not.
+    rng = np.random.default_rng(22)
+    numel = [4096, 1536, 256, 4096]
+    b = oracle.Blocks(numel, 4096)
+    for dtype in ("f32", "bf16"):
+        base, exps = _tiny_family(rng, numel, 3, dtype)
+        mask = rng.integers(0, 8, b.G).astype(np.uint32)
+        alpha = np.array([0.3, 0.45, 0.11], np.float32)
+        ref = oracle.merge_avg_renorm(b, dtype, base, exps, mask, alpha)
+        for sc in (8.0, 1.0 / 16):
+            got = oracle.merge_avg_renorm(b, dtype, base, exps, mask, alpha * np.float32(sc))
+            assert np.array_equal(got, ref), (dtype, sc)
+        plain = oracle.merge_avg(b, dtype, base, exps, mask, alpha * np.float32(8.0))
+        assert not np.array_equal(plain, ref)
+
+
+def test_avg_renorm_full_mask_with_unit_sum_is_avg():
+    # alpha summing to exactly 1 in fp32 and every expert selected: beta =
+    # alpha, so the selected-only merge is the (pinned) full-read AVG.
+    rng = np.random.default_rng(23)
+    numel = [4096, 1536, 256]
+    b = oracle.Blocks(numel, 4096)
+    for dtype, alpha in (("bf16", [0.125, 0.375, 0.5]), ("f32", [0.25, 0.25, 0.25, 0.25])):
+        K = len(alpha)
+        base, exps = _tiny_family(rng, numel, K, dtype)
+        full = np.full(b.G, (1 << K) - 1, np.uint32)
+        assert np.array_equal(oracle.merge_avg_renorm(b, dtype, base, exps, full, alpha),
+                              oracle.merge_avg(b, dtype, base, exps, full, alpha))
+
+
+def test_avg_renorm_is_a_convex_combination_of_the_selected_experts():
+    # Positive alpha: the betas are positive and sum to 1 (to rounding), so
+    # each output lies between the selected experts' values there.
+    rng = np.random.default_rng(24)
+    numel = [4096, 1536, 256, 4096]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 4, "f32")
+    mask = rng.integers(1, 16, b.G).astype(np.uint32)
+    out = oracle.merge_avg_renorm(b, "f32", base, exps, mask, [0.1, 0.2, 0.3, 0.4])
+    for g in range(b.G):
+        sl = slice(b.off[g], b.off[g] + b.len[g])
+        sel = np.stack([exps[i][sl] for i in range(4) if (mask[g] >> i) & 1])
+        lo, hi = sel.min(axis=0), sel.max(axis=0)
+        tol = 4 * np.spacing(np.maximum(np.abs(lo), np.abs(hi)))
+        assert np.all(out[sl] >= lo - tol) and np.all(out[sl] <= hi + tol), g
+
+
+def test_avg_renorm_coefficient_drift_identity_and_bound_all_masks():
+    # Appendix A.1: M_full - M_A = sum_i (alpha_i - beta_i(A)) Delta_i with
+    # beta_i(A) = 0 where A_i = 0, and ||M_full - M_A|| <= (sum_b r_b^2)^(1/2),
+    # r_b = sum_i |alpha_i - beta_i| ||Delta_i,b||.  beta is taken exactly
+    # (fp64) from its definition; the oracle's fp32 rounding is the slack.
+    rng = np.random.default_rng(25)
+    numel = [8, 8, 4]
+    b = oracle.Blocks(numel, 8)
+    K = 3
+    P = sum(numel)
+    base = (rng.integers(-64, 64, P) / 1024.0).astype(np.float32)
+    deltas = [(rng.integers(-16, 16, P) / 4096.0).astype(np.float32) for _ in range(K)]
+    exps = [base + d for d in deltas]
+    alpha = np.array([0.2, 0.5, 0.3], np.float32)
+    Mf = oracle.merge_avg(b, "f32", base, exps, np.full(b.G, 7, np.uint32), alpha).astype(np.float64)
+    mag = np.abs(base).astype(np.float64) + sum(np.abs(d).astype(np.float64) for d in deltas)
+    slack = 8 * np.spacing(mag.astype(np.float32)).astype(np.float64)
+    nu = b.G * K
+    for bits in range(1 << nu):
+        A = np.array([[(bits >> (g * K + i)) & 1 for i in range(K)] for g in range(b.G)])
+        mask = np.array([sum(int(A[g, i]) << i for i in range(K)) for g in range(b.G)], np.uint32)
+        MA = oracle.merge_avg_renorm(b, "f32", base, exps, mask, alpha).astype(np.float64)
+        ident = np.zeros(P)
+        r = np.zeros(b.G)
+        for g in range(b.G):
+            o, n = b.off[g], b.len[g]
+            s = sum(float(alpha[i]) for i in range(K) if A[g, i])
+            for i in range(K):
+                beta = float(alpha[i]) / s if (A[g, i] and s != 0.0) else 0.0
+                dd = deltas[i][o:o + n].astype(np.float64)
+                ident[o:o + n] += (float(alpha[i]) - beta) * dd
+                r[g] += abs(float(alpha[i]) - beta) * np.linalg.norm(dd)
+        diff = Mf - MA
+        assert np.all(np.abs(diff - ident) <= slack), bits
+        assert np.linalg.norm(diff) <= math.sqrt(np.sum(r**2)) + np.linalg.norm(slack), bits
+
+
+# --------------------------------------------------------------------------
 # TIES
 # --------------------------------------------------------------------------
 
