@@ -175,6 +175,19 @@ int mp_merge_avg(const mp_layout* layout, const void* base,
                  const uint32_t* mask, const float* alpha, void* out,
                  mp_io_stats* io, void* stream);
 
+/* Selected-only budgeted AVG (Appendix A.1, the variant that renormalises
+ * an additive merge over the selected experts; the coefficient-drift bound
+ * there, not Prop. 2's omission bound, describes its error).  Per block g:
+ * s_g = sum of alpha_i over the experts selected in g (fp32 adds from +0,
+ * increasing i); beta_i = alpha_i / s_g (IEEE fp32 division) for a
+ * selected i; s_g = 0 gives no coefficients (the block keeps the base).
+ * Then per element as mp_merge_avg with beta in place of alpha.  Arguments,
+ * residencies, reads and io as mp_merge_avg. */
+int mp_merge_avg_renorm(const mp_layout* layout, const void* base,
+                        const void* const* experts, int32_t K, int32_t residency,
+                        const uint32_t* mask, const float* alpha, void* out,
+                        mp_io_stats* io, void* stream);
+
 /* Budgeted TIES (Appendix A.1: trim, sign election and disjoint mean over
  * the masked deltas).  Trim is per selected (expert, block): k = min(n,
  * ceil(density * n)) in fp64, tau = the k-th largest |d| of the block; d is

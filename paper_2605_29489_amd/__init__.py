@@ -31,7 +31,8 @@ MP_DEVICE, MP_HOST_PINNED, MP_HOST_PAGEABLE = 0, 1, 2
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
 MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 
-EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_avg_renorm",
+           "mp_merge_ties",
            "mp_merge_ties_tau", "mp_merge_dare", "mp_set_stage_bytes", "mp_last_error", "mp_release")
 
 
@@ -74,6 +75,7 @@ def _load():
     L.mp_plan.argtypes = [lp, i32, vp, C.POINTER(C.c_float), u64, u32, vp, C.POINTER(mp_plan_stats), vp]
     L.mp_merge_avg.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.POINTER(C.c_float), vp,
                                C.POINTER(mp_io_stats), vp]
+    L.mp_merge_avg_renorm.argtypes = L.mp_merge_avg.argtypes
     L.mp_merge_ties.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, C.c_float, vp,
                                 C.POINTER(mp_io_stats), vp]
     L.mp_merge_ties_tau.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, vp, C.c_float, vp,
@@ -85,7 +87,8 @@ def _load():
     L.mp_set_stage_bytes.restype = i32
     L.mp_last_error.argtypes = []
     L.mp_release.argtypes = []
-    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg",
+                 "mp_merge_avg_renorm", "mp_merge_ties",
                  "mp_merge_ties_tau",
                  "mp_merge_dare"):
         getattr(L, name).restype = C.c_int
@@ -186,6 +189,15 @@ def mp_merge_avg(layout: Layout, base, experts, mask, alpha, out, residency: int
     st = mp_io_stats() if io else None
     _check(lib.mp_merge_avg(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
                             _floats(alpha, len(experts)), _ptr(out), _io(st), _stream(stream)))
+    return st.as_dict() if io else None
+
+
+def mp_merge_avg_renorm(layout: Layout, base, experts, mask, alpha, out, residency: int = MP_DEVICE,
+                        io: bool = False, stream=None) -> Optional[dict]:
+    """Selected-only AVG: alpha renormalised over each block's selected experts."""
+    st = mp_io_stats() if io else None
+    _check(lib.mp_merge_avg_renorm(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+                                   _floats(alpha, len(experts)), _ptr(out), _io(st), _stream(stream)))
     return st.as_dict() if io else None
 
 

@@ -592,12 +592,12 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float*
     return MP_OK;
 }
 
-int mp_merge_avg(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
-                 int32_t residency, const uint32_t* mask, const float* alpha, void* out,
-                 mp_io_stats* io, void* stream)
+static int merge_additive(Op op, const mp_layout* layout, const void* base, const void* const* experts,
+                          int32_t K, int32_t residency, const uint32_t* mask, const float* alpha, void* out,
+                          mp_io_stats* io, void* stream)
 {
     MergeArgs a;
-    a.op = Op::AVG;
+    a.op = op;
     if (alpha == nullptr)
         return fail(MP_E_ARG, "alpha is NULL");
     if (K < 1 || K > kMaxK)
@@ -608,6 +608,20 @@ int mp_merge_avg(const mp_layout* layout, const void* base, const void* const* e
         a.alpha.v[i] = alpha[i];
     }
     return run_merge(layout, base, experts, K, residency, mask, out, io, static_cast<hipStream_t>(stream), a);
+}
+
+int mp_merge_avg(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                 int32_t residency, const uint32_t* mask, const float* alpha, void* out,
+                 mp_io_stats* io, void* stream)
+{
+    return merge_additive(Op::AVG, layout, base, experts, K, residency, mask, alpha, out, io, stream);
+}
+
+int mp_merge_avg_renorm(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                        int32_t residency, const uint32_t* mask, const float* alpha, void* out,
+                        mp_io_stats* io, void* stream)
+{
+    return merge_additive(Op::AVG_RENORM, layout, base, experts, K, residency, mask, alpha, out, io, stream);
 }
 
 int mp_merge_ties(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,

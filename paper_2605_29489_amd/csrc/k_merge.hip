@@ -63,17 +63,20 @@ __device__ inline float2 ties_divisor(int i)
 }
 
 // ------------------------------------------------------------ elementwise family
-enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2, M_TIES_TAU = 3 };
+enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2, M_TIES_TAU = 3, M_AVG_RENORM = 4 };
 
 // Occupancy of the elementwise kernels: DARE (either combination) and TIES
 // from thresholds keep their per-element state for half a block per pass
 // (two passes per 4096-element block), which leaves room for 8 waves per
-// SIMD with bf16 (6 with fp32) to hide memory latency; AVG holds a whole
-// block per pass (measured faster than halves at 8 waves).
-template <int DT, int MODE>
-constexpr int elem_waves() { return MODE == M_AVG ? 1 : (DT == 1 ? 8 : 6); }
+// SIMD with bf16 (6 with fp32) to hide memory latency; AVG (either
+// coefficient rule) holds a whole block per pass (measured faster than
+// halves at 8 waves).
 template <int MODE>
-constexpr int elem_div() { return MODE == M_AVG ? 1 : 2; }
+constexpr bool is_avg() { return MODE == M_AVG || MODE == M_AVG_RENORM; }
+template <int DT, int MODE>
+constexpr int elem_waves() { return is_avg<MODE>() ? 1 : (DT == 1 ? 8 : 6); }
+template <int MODE>
+constexpr int elem_div() { return is_avg<MODE>() ? 1 : 2; }
 
 template <int DT, int MODE, class Src>
 __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src src, const void* __restrict__ base,
@@ -121,6 +124,10 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
         tens = btensor[g];
         e0 = belem0[g];
     }
+    // selected-only AVG: the coefficients are alpha_i / s, s = the sum of
+    // the selected alpha_i in increasing i (no coefficient when s = 0); s
+    // is formed at its first use, once the first expert reads are issued
+    float s_sel = 0.0f;
 
     for (uint32_t tile = 0; tile < nch; tile += CPT * kT) {
         float x0[E];
@@ -181,6 +188,22 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
                 float tauf = 0.0f;
                 if (MODE == M_TIES_TAU)
                     tauf = __uint_as_float(max(tau[(uint64_t)g * (uint32_t)K + (uint32_t)i], 1u));
+                float coef = alpha.v[i];
+                if (MODE == M_AVG_RENORM) {
+                    if (rank == 0 && j == 0) {
+                        // constant indices: a few wide scalar loads rather
+                        // than one dependent load per selected expert; kept
+                        // behind the expert reads already issued
+                        uint32_t ms = m;
+                        __asm__ volatile("" : "+s"(ms) : : "memory");
+                        s_sel = 0.0f;
+#pragma unroll
+                        for (int q = 0; q < 32; ++q)
+                            if ((ms >> q) & 1u)
+                                s_sel = s_sel + alpha.v[q];
+                    }
+                    coef = (s_sel != 0.0f) ? coef / s_sel : 0.0f;
+                }
 #pragma unroll
                 for (int q = 0; q < CPT; ++q) {
                     if (!ok[q])
@@ -206,8 +229,8 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
                     for (int v = 0; v < V; ++v) {
                         const int e = q * V + v;
                         const float d = x[v] - x0[e];
-                        if (MODE == M_AVG) {
-                            acc[e] = fmaf(alpha.v[i], d, acc[e]);
+                        if (is_avg<MODE>()) {
+                            acc[e] = fmaf(coef, d, acc[e]);
                         } else if (MODE == M_TIES_TAU) {
                             // d >= tau keeps a positive delta, -d >= tau a negative one
                             const bool kp = d >= tauf, kn = -d >= tauf;
@@ -310,7 +333,7 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int e = q * V + v;
-                if (MODE == M_AVG)
+                if (is_avg<MODE>())
                     y[v] = x0[e] + acc[e];
                 else
                     y[v] = fmaf(lambda, acc[e], x0[e]);
@@ -915,6 +938,11 @@ hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src
     switch (a.op) {
     case Op::AVG:
         hipLaunchKernelGGL((k_merge_elem<DT, M_AVG, Src>), grid, block, 0, s, src, base, mask, bt.d_off,
+                           bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask, out, ctr,
+                           nullptr, K);
+        break;
+    case Op::AVG_RENORM:
+        hipLaunchKernelGGL((k_merge_elem<DT, M_AVG_RENORM, Src>), grid, block, 0, s, src, base, mask, bt.d_off,
                            bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask, out, ctr,
                            nullptr, K);
         break;

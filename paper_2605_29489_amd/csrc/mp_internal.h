@@ -80,7 +80,7 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
 
 // Merge operators.  `counters` is null or a device array of 256 uint64
 // accumulating the expert bytes the kernels load.
-enum class Op { AVG = 0, TIES = 1, DARE_LINEAR = 2, DARE_SIGN = 3, TIES_TAU = 4 };
+enum class Op { AVG = 0, TIES = 1, DARE_LINEAR = 2, DARE_SIGN = 3, TIES_TAU = 4, AVG_RENORM = 5 };
 
 struct MergeArgs {
     Op op = Op::AVG;

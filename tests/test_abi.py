@@ -26,7 +26,7 @@ def mp():
 
 def test_header_declares_the_boundary():
     names = _declared()
-    for n in ("mp_layout_blocks", "mp_index_blocks", "mp_plan", "mp_merge_avg", "mp_merge_ties",
+    for n in ("mp_layout_blocks", "mp_index_blocks", "mp_plan", "mp_merge_avg", "mp_merge_avg_renorm", "mp_merge_ties",
               "mp_merge_dare", "mp_last_error", "mp_release"):
         assert n in names
 
@@ -100,6 +100,8 @@ def test_argument_errors_before_any_device_call(mp):
     assert lib.mp_merge_avg(L.ref, None, ptrs, 1, 0, None, None, None, None, None) == mp.MP_E_ARG
     an = (C.c_float * 1)(float("inf"))
     assert lib.mp_merge_avg(L.ref, None, ptrs, 1, 0, None, an, None, None, None) == mp.MP_E_ARG
+    assert lib.mp_merge_avg_renorm(L.ref, None, ptrs, 1, 0, None, None, None, None, None) == mp.MP_E_ARG
+    assert lib.mp_merge_avg_renorm(L.ref, None, ptrs, 1, 0, None, an, None, None, None) == mp.MP_E_ARG
     # unit ids must fit 32 bits: 2^28 blocks x 32 experts
     big = mp.Layout([4096 * (1 << 28)], 4096, mp.MP_BF16)
     assert lib.mp_index_blocks(big.ref, None, ptrs, 32, 0, None, None) == mp.MP_E_ARG

@@ -94,7 +94,7 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
     S_orc = oracle.index(blocks, dtype, base_np, exps_np).reshape(-1)
     assert np.array_equal(S_gpu.view(np.uint32), S_orc.view(np.uint32)), "index differs"
     if w is None:
-        w = [1.0 / K] * K if op in ("avg", "dare_lin") else [1.0] * K
+        w = [1.0 / K] * K if op in ("avg", "avg_renorm", "dare_lin") else [1.0] * K
     full = int(blocks.len.sum()) * lay.elem_bytes * K
     out = torch.empty_like(base)
     mask = torch.empty(G, dtype=torch.int32, device="cuda")
@@ -113,6 +113,9 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
         if op == "avg":
             io = mp.mp_merge_avg(L, base, exps, mask, kw["alpha"], out, residency=res, io=True)
             want = oracle.merge_avg(blocks, dtype, base_np, exps_np, m_orc, kw["alpha"])
+        elif op == "avg_renorm":
+            io = mp.mp_merge_avg_renorm(L, base, exps, mask, kw["alpha"], out, residency=res, io=True)
+            want = oracle.merge_avg_renorm(blocks, dtype, base_np, exps_np, m_orc, kw["alpha"])
         elif op == "ties":
             io = mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out, residency=res, io=True)
             want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"])
@@ -150,7 +153,7 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
 
 # ---------------------------------------------------------------- small families
 
-@pytest.mark.parametrize("op", ["avg", "ties", "ties_tau", "dare_lin", "dare_sign"])
+@pytest.mark.parametrize("op", ["avg", "avg_renorm", "ties", "ties_tau", "dare_lin", "dare_sign"])
 def test_mini_qwen_bf16_all_ops(mp, op):
     spec = _mini_qwen()
     base, exps = make_family(spec, seed=1)
@@ -159,7 +162,7 @@ def test_mini_qwen_bf16_all_ops(mp, op):
     _run_all(mp, spec, base, exps, op, [0, 0.1, 0.25, 0.5, 0.77, 1.0, 2.0, 12345], **kw)
 
 
-@pytest.mark.parametrize("op", ["avg", "ties", "ties_tau", "dare_lin", "dare_sign"])
+@pytest.mark.parametrize("op", ["avg", "avg_renorm", "ties", "ties_tau", "dare_lin", "dare_sign"])
 def test_ragged_fp32_all_ops(mp, op):
     spec = _ragged_f32()
     base, exps = make_family(spec, seed=2)
@@ -168,7 +171,7 @@ def test_ragged_fp32_all_ops(mp, op):
     _run_all(mp, spec, base, exps, op, [0, 0.3, 0.6, 1.0], **kw)
 
 
-@pytest.mark.parametrize("op", ["avg", "ties", "ties_tau", "dare_lin", "dare_sign"])
+@pytest.mark.parametrize("op", ["avg", "avg_renorm", "ties", "ties_tau", "dare_lin", "dare_sign"])
 def test_host_pinned_experts_all_ops(mp, op):
     # experts in pinned host memory: the kernels read the selected blocks
     # over PCIe; results are the same bits as with device-resident experts
@@ -214,7 +217,7 @@ def test_host_pinned_rejects_device_and_pageable_experts(mp):
             x.free()
 
 
-@pytest.mark.parametrize("op", ["avg", "ties", "ties_tau", "dare_lin", "dare_sign"])
+@pytest.mark.parametrize("op", ["avg", "avg_renorm", "ties", "ties_tau", "dare_lin", "dare_sign"])
 def test_host_pageable_experts_all_ops(mp, op):
     # experts in ordinary host memory: the selected blocks are packed into
     # pinned staging, copied to the device and merged chunk by chunk; same
@@ -235,7 +238,7 @@ def test_host_pageable_small_staging_many_chunks(mp):
         spec = _mini_qwen(n_layers=1)
         base, exps = make_family(spec, seed=4)
         kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0, p=0.9, seed=7)
-        for op in ("avg", "ties", "ties_tau", "dare_lin", "dare_sign"):
+        for op in ("avg", "avg_renorm", "ties", "ties_tau", "dare_lin", "dare_sign"):
             _say(f"case mini-qwen bf16 {op}, pageable host experts, 1 MiB staging")
             _run_all(mp, spec, base, exps, op, [0.1, 0.45, 1.0], residency=mp.MP_HOST_PAGEABLE, **kw)
         spec = _ragged_f32(K=6)
@@ -282,6 +285,7 @@ def test_expert_counts(mp, K):
     _run_all(mp, spec, base, exps, "ties", [0.0, 0.4, 1.0], density=0.2, lam=1.0)
     _run_all(mp, spec, base, exps, "ties_tau", [0.4, 1.0], density=0.2, lam=1.0)
     _run_all(mp, spec, base, exps, "avg", [0.4], alpha=[1.0 / K] * K)
+    _run_all(mp, spec, base, exps, "avg_renorm", [0.4, 1.0], alpha=[1.0 / K] * K)
 
 
 @pytest.mark.parametrize("be", [1024, 2048, 512])
@@ -292,6 +296,20 @@ def test_block_sizes(mp, be):
     _run_all(mp, spec, base, exps, "ties", [0.35, 1.0], density=0.3, lam=1.0)
     _run_all(mp, spec, base, exps, "ties_tau", [0.35, 1.0], density=0.3, lam=1.0)
     _run_all(mp, spec, base, exps, "dare_lin", [0.5], alpha=[0.3, 0.2, 0.4, 0.1], p=0.3, seed=11, lam=1.0)
+
+
+def test_avg_renorm_coefficients(mp):
+    # Selected-only AVG with unequal, non-dyadic coefficients (the quotients
+    # alpha_i / s are inexact) and a zero coefficient: blocks whose only
+    # selected expert has alpha 0 sum to s = 0 and keep the base.
+    spec = _mini_qwen(n_layers=1)
+    base, exps = make_family(spec, seed=6)
+    _say("case avg_renorm coefficients")
+    _run_all(mp, spec, base, exps, "avg_renorm", [0.0, 0.2, 0.55, 1.0], w=[1.0, 0.9, 0.8, 0.7],
+             alpha=[0.3, 0.0, 0.11, 1.9])
+    spec = _ragged_f32(K=3)
+    base, exps = make_family(spec, seed=8)
+    _run_all(mp, spec, base, exps, "avg_renorm", [0.15, 0.5, 1.0], alpha=[0.2, 0.7, 0.1])
 
 
 def test_large_blocks_avg_dare_and_ties_unsupported(mp):

@@ -165,6 +165,8 @@ CONFIGS = {
     "toy": dict(family="toy", op="avg", budgets=(0.5,), residency="device"),
     "qwen2.5-1.5b": dict(family="qwen2.5-1.5b", op="ties", density=0.2, lam=1.0,
                          budgets=(0.25, 0.5, 1.0), residency="device"),
+    "qwen2.5-1.5b-avg-renorm": dict(family="qwen2.5-1.5b", op="avg_renorm", budgets=(0.25, 0.5, 1.0),
+                                    residency="device"),
     "llama3-8b": dict(family="llama3-8b", op="avg", budgets=tuple(x / 10 for x in range(1, 11)),
                       residency="host_pinned"),
     "qwen2.5-7b": dict(family="qwen2.5-7b", op="dare", p=0.9, seed=7, combine="sign_elect", lam=1.0,
