@@ -126,6 +126,36 @@ def cpu_baseline(spec, base, exps, route, blocks_stride=8):
 PCIE_PEAK = 64.0e9  # PCIe Gen5 x16, one direction, nominal bytes/s
 
 
+def fidelity(out, m_full, blen, n_sel, n_units):
+    """Fidelity of a budgeted merge against the full-read one (reporting only,
+    outside every timed region): Rel. l2 = ||M_A - M_full|| / ||M_full|| over
+    the checkpoint, P95 block = the 95th percentile over blocks of
+    ||M_A - M_full|| / ||M_full|| per block, Touched = selected units / (K G).
+    fp64, in block-aligned chunks of about 2^27 elements."""
+    import torch
+    ends = torch.cumsum(blen, 0)
+    num_all, den_all = [], []
+    g0, e0, G = 0, 0, int(blen.numel())
+    while g0 < G:
+        g1 = int(torch.searchsorted(ends, e0 + (1 << 27), right=True))
+        g1 = max(g1, g0 + 1)
+        e1 = int(ends[g1 - 1])
+        a = out[e0:e1].double()
+        b = m_full[e0:e1].double()
+        a.sub_(b).square_()
+        b.square_()
+        num_all.append(torch.segment_reduce(a, "sum", lengths=blen[g0:g1]))
+        den_all.append(torch.segment_reduce(b, "sum", lengths=blen[g0:g1]))
+        del a, b
+        g0, e0 = g1, e1
+    num, den = torch.cat(num_all), torch.cat(den_all)
+    rel = float(num.sum().sqrt() / den.sum().sqrt())
+    ok = den > 0
+    blk = (num[ok] / den[ok]).sqrt().float()
+    p95 = float(torch.quantile(blk, 0.95)) if blk.numel() else 0.0
+    return {"rel_l2": rel, "p95_block": p95, "touched": n_sel / n_units}
+
+
 def run_sweep(args):
     """One of the other workload shapes: index once, then plan + merge at each
     budget of its sweep.  Experts are device-resident, stay in pinned host
@@ -193,20 +223,30 @@ def run_sweep(args):
     idx_ms = float(np.median([timed(lambda: mp.mp_index_blocks(L, base, exps, sumsq, residency=res,
                                                                 stream=stream))[0] for _ in range(reps)]))
     rows = []
-    mp.mp_plan(L, K, sumsq, w, full, mask, stream=stream)  # first call sets up the plan workspace
+    flags = {"none": 0, "per_byte": mp.MP_PLAN_PER_BYTE, "skip_zero": mp.MP_PLAN_SKIP_ZERO,
+             "both": mp.MP_PLAN_PER_BYTE | mp.MP_PLAN_SKIP_ZERO}[args.plan_flags]
+    mp.mp_plan(L, K, sumsq, w, full, mask, flags=flags, stream=stream)  # first call sets up the workspace
+    m_full = None
+    if args.fidelity:  # the full-read merge M_full, for the fidelity metrics
+        merge()
+        m_full = out.clone()
+        blen = torch.from_numpy(np.asarray(lay.block_lengths(), np.int64)).to(base.device)
     for f in cfg["budgets"]:
         B = int(f * full)
-        plan_ms, st = timed(lambda: mp.mp_plan(L, K, sumsq, w, B, mask, stream=stream))
+        plan_ms, st = timed(lambda: mp.mp_plan(L, K, sumsq, w, B, mask, flags=flags, stream=stream))
         io = merge(io=True)
         assert io["expert_bytes"] == st["cost_bytes"]
         for _ in range(max(0, args.warmup)):
             merge()
         ms = float(np.median([timed(merge)[0] for _ in range(reps)]))
+        fid = fidelity(out, m_full, blen, st["n_selected"], K * G) if args.fidelity else None
         alg = 2 * P * es + st["cost_bytes"] + 4 * G if not host else st["cost_bytes"]
         rows.append({"budget_frac": round(f, 4), "budget_bytes": B, "cost_bytes": st["cost_bytes"],
                      "h2d_bytes": io["h2d_bytes"], "n_selected": st["n_selected"], "plan_ms": round(plan_ms, 4),
                      "merge_ms": round(ms, 4), "merge_params_per_s": P / (ms * 1e-3),
                      ("h2d_GBps" if host else "merge_effective_GBps"): alg / (ms * 1e-3) / 1e9})
+        if fid is not None:
+            rows[-1]["fidelity"] = fid
     step_ms = idx_ms + sum(r["plan_ms"] + r["merge_ms"] for r in rows)
     dma = None
     if host:  # measured peak: pinned host -> device with the copy engine (1 GiB, or one expert)
@@ -226,7 +266,8 @@ def run_sweep(args):
         "value": len(rows) * P / (step_ms * 1e-3), "unit": "params/s", "n_gpus": 1, "steps": reps,
         "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"{spec.description}; {op} {cfg}", "storage_dtype": lay.dtype, "params": P,
+        "config": {"workload": f"{spec.description}; {op} {cfg}", "plan_flags": args.plan_flags,
+                   "storage_dtype": lay.dtype, "params": P,
                    "blocks": G, "K": K, "experts": where_txt,
                    "parallelism": "single GPU"},
         "roofline": {"bound": "pcie" if host else "hbm", "achieved": achieved / 1e9, "peak": peak / 1e9,
@@ -252,6 +293,10 @@ def main():
                     help="other workloads: where the experts live (default: the workload's own)")
     ap.add_argument("--ties", default="catalog", choices=("catalog", "in-merge"),
                     help="where the TIES trim thresholds are found: in the index pass (catalog) or in each merge")
+    ap.add_argument("--plan-flags", default="none", choices=("none", "per_byte", "skip_zero", "both"),
+                    help="other workloads: mp_plan options (default: the literal Algorithm 1)")
+    ap.add_argument("--fidelity", action="store_true",
+                    help="other workloads: also report Rel. l2, P95 block and Touched against the full merge")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="after the timed region, run the AVG merge once with an empty mask: a plain copy "
                          "of the base (reads 2P + 4G bytes, writes 2P) for scaling hardware byte counters")

@@ -55,6 +55,15 @@ class Layout:
     def ckpt_bytes(self) -> int:
         return self.n_params * self.elem_bytes
 
+    def block_lengths(self) -> List[int]:
+        """Element counts of the blocks in order (each tensor cut into
+        block_elems runs, the last one short)."""
+        out = []
+        for n in self.numel:
+            full, tail = divmod(int(n), self.block_elems)
+            out += [self.block_elems] * full + ([tail] if tail else [])
+        return out
+
 
 @dataclass(frozen=True)
 class FamilySpec:
@@ -165,6 +174,8 @@ CONFIGS = {
     "toy": dict(family="toy", op="avg", budgets=(0.5,), residency="device"),
     "qwen2.5-1.5b": dict(family="qwen2.5-1.5b", op="ties", density=0.2, lam=1.0,
                          budgets=(0.25, 0.5, 1.0), residency="device"),
+    "qwen2.5-1.5b-ties-sweep": dict(family="qwen2.5-1.5b", op="ties", density=0.2, lam=1.0,
+                                    budgets=(1.0, 0.9, 0.8, 0.7, 0.6, 0.5), residency="device"),
     "qwen2.5-1.5b-avg-renorm": dict(family="qwen2.5-1.5b", op="avg_renorm", budgets=(0.25, 0.5, 1.0),
                                     residency="device"),
     "llama3-8b": dict(family="llama3-8b", op="avg", budgets=tuple(x / 10 for x in range(1, 11)),
