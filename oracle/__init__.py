@@ -68,8 +68,11 @@ def _i64(a):
     return a, a.ctypes.data_as(C.POINTER(C.c_int64))
 
 
-def _dt(dtype):
-    return DTYPE[dtype] if isinstance(dtype, str) else int(dtype)
+DELTA = 0x100  # experts hold Delta_i = W_i - W_0 (the explicit-delta source)
+
+
+def _dt(dtype, delta=False):
+    return (DTYPE[dtype] if isinstance(dtype, str) else int(dtype)) | (DELTA if delta else 0)
 
 
 def _ptrs(arrs):
@@ -104,7 +107,7 @@ class Blocks:
         self.G = int(G)
 
 
-def index(blocks: Blocks, dtype, base, experts, doff=None, ids=None):
+def index(blocks: Blocks, dtype, base, experts, doff=None, ids=None, delta=False):
     """Sum of squared deltas per (block, expert); returns float32 [nb, K].
 
     ``ids`` restricts to a subset of blocks; ``doff`` overrides where each
@@ -116,7 +119,7 @@ def index(blocks: Blocks, dtype, base, experts, doff=None, ids=None):
     d_a, d_p = _i64(doff)
     l_a, l_p = _i64(blocks.len[ids])
     out = np.zeros((len(ids), K), np.float32)
-    _check(L.orc_index(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts), K,
+    _check(L.orc_index(len(ids), d_p, l_p, _dt(dtype, delta), base.ctypes.data, _ptrs(experts), K,
                        out.ctypes.data), "index")
     return out
 
@@ -142,7 +145,7 @@ def _merge_args(blocks, ids, doff):
     return ids, doff
 
 
-def merge_avg(blocks, dtype, base, experts, mask, alpha, out=None, ids=None, doff=None):
+def merge_avg(blocks, dtype, base, experts, mask, alpha, out=None, ids=None, doff=None, delta=False):
     L = lib()
     ids, doff = _merge_args(blocks, ids, doff)
     out = np.empty_like(base) if out is None else out
@@ -150,12 +153,12 @@ def merge_avg(blocks, dtype, base, experts, mask, alpha, out=None, ids=None, dof
     alpha = np.ascontiguousarray(alpha, np.float32)
     d_a, d_p = _i64(doff)
     l_a, l_p = _i64(blocks.len[ids])
-    _check(L.orc_merge_avg(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
+    _check(L.orc_merge_avg(len(ids), d_p, l_p, _dt(dtype, delta), base.ctypes.data, _ptrs(experts),
                            len(experts), mask.ctypes.data, alpha.ctypes.data, out.ctypes.data), "avg")
     return out
 
 
-def merge_avg_renorm(blocks, dtype, base, experts, mask, alpha, out=None, ids=None, doff=None):
+def merge_avg_renorm(blocks, dtype, base, experts, mask, alpha, out=None, ids=None, doff=None, delta=False):
     """Selected-only AVG: alpha renormalised over each block's selected experts."""
     L = lib()
     ids, doff = _merge_args(blocks, ids, doff)
@@ -164,38 +167,38 @@ def merge_avg_renorm(blocks, dtype, base, experts, mask, alpha, out=None, ids=No
     alpha = np.ascontiguousarray(alpha, np.float32)
     d_a, d_p = _i64(doff)
     l_a, l_p = _i64(blocks.len[ids])
-    _check(L.orc_merge_avg_renorm(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
+    _check(L.orc_merge_avg_renorm(len(ids), d_p, l_p, _dt(dtype, delta), base.ctypes.data, _ptrs(experts),
                                   len(experts), mask.ctypes.data, alpha.ctypes.data, out.ctypes.data),
            "avg_renorm")
     return out
 
 
-def merge_ties(blocks, dtype, base, experts, mask, density, lam, out=None, ids=None, doff=None):
+def merge_ties(blocks, dtype, base, experts, mask, density, lam, out=None, ids=None, doff=None, delta=False):
     L = lib()
     ids, doff = _merge_args(blocks, ids, doff)
     out = np.empty_like(base) if out is None else out
     mask = np.ascontiguousarray(mask, np.uint32)
     d_a, d_p = _i64(doff)
     l_a, l_p = _i64(blocks.len[ids])
-    _check(L.orc_merge_ties(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
+    _check(L.orc_merge_ties(len(ids), d_p, l_p, _dt(dtype, delta), base.ctypes.data, _ptrs(experts),
                             len(experts), mask.ctypes.data, float(density), float(lam),
                             out.ctypes.data), "ties")
     return out
 
 
-def ties_thresholds(blocks, dtype, base, experts, density, ids=None, doff=None):
+def ties_thresholds(blocks, dtype, base, experts, density, ids=None, doff=None, delta=False):
     """Per-unit TIES trim thresholds (uint32 fp32 patterns), [len(ids), K]."""
     L = lib()
     ids, doff = _merge_args(blocks, ids, doff)
     tau = np.zeros((len(ids), len(experts)), np.uint32)
     d_a, d_p = _i64(doff)
     l_a, l_p = _i64(blocks.len[ids])
-    _check(L.orc_ties_thresholds(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
+    _check(L.orc_ties_thresholds(len(ids), d_p, l_p, _dt(dtype, delta), base.ctypes.data, _ptrs(experts),
                                  len(experts), float(density), tau.ctypes.data), "ties thresholds")
     return tau
 
 
-def merge_ties_tau(blocks, dtype, base, experts, mask, tau, lam, out=None, ids=None, doff=None):
+def merge_ties_tau(blocks, dtype, base, experts, mask, tau, lam, out=None, ids=None, doff=None, delta=False):
     """TIES with given per-unit thresholds tau [len(ids), K]."""
     L = lib()
     ids, doff = _merge_args(blocks, ids, doff)
@@ -204,14 +207,14 @@ def merge_ties_tau(blocks, dtype, base, experts, mask, tau, lam, out=None, ids=N
     tau = np.ascontiguousarray(tau, np.uint32)
     d_a, d_p = _i64(doff)
     l_a, l_p = _i64(blocks.len[ids])
-    _check(L.orc_merge_ties_tau(len(ids), d_p, l_p, _dt(dtype), base.ctypes.data, _ptrs(experts),
+    _check(L.orc_merge_ties_tau(len(ids), d_p, l_p, _dt(dtype, delta), base.ctypes.data, _ptrs(experts),
                                 len(experts), mask.ctypes.data, tau.ctypes.data, float(lam),
                                 out.ctypes.data), "ties tau")
     return out
 
 
 def merge_dare(blocks, dtype, base, experts, mask, p, seed, combine, alpha, lam,
-               out=None, ids=None, doff=None):
+               out=None, ids=None, doff=None, delta=False):
     """combine: 0 = linear, 1 = sign-elect."""
     L = lib()
     ids, doff = _merge_args(blocks, ids, doff)
@@ -223,7 +226,7 @@ def merge_dare(blocks, dtype, base, experts, mask, p, seed, combine, alpha, lam,
     t_a = np.ascontiguousarray(blocks.tensor[ids], np.int32)
     e_a, e_p = _i64(blocks.elem0[ids])
     _check(L.orc_merge_dare(len(ids), d_p, l_p, t_a.ctypes.data_as(C.POINTER(C.c_int32)), e_p,
-                            _dt(dtype), base.ctypes.data, _ptrs(experts), len(experts),
+                            _dt(dtype, delta), base.ctypes.data, _ptrs(experts), len(experts),
                             mask.ctypes.data, float(p), int(seed) & 0xFFFFFFFF, int(combine),
                             alpha.ctypes.data, float(lam), out.ctypes.data), "dare")
     return out

@@ -23,7 +23,20 @@
 /* element access                                                      */
 /* ------------------------------------------------------------------ */
 
-static int elem_bytes(int32_t dtype) { return dtype == 0 ? 4 : (dtype == 1 ? 2 : 0); }
+/* The dtype argument: bits 0-7 give the element type (0 fp32, 1 bf16);
+ * bit 8 (ORC_DELTA) says the expert buffers hold the deltas
+ * Delta_i = W_i - W_0 themselves (the executor's "explicit deltas" source,
+ * Section 3) instead of fine-tuned weights.  Then d = fl32(Delta_i), read
+ * without the base; the base still anchors the merged output. */
+#define ORC_DELTA 0x100
+static int32_t etype(int32_t dtype) { return dtype & 0xff; }
+static int elem_bytes(int32_t dtype)
+{
+    if (dtype & ~(ORC_DELTA | 0xff))
+        return 0;
+    dtype = etype(dtype);
+    return dtype == 0 ? 4 : (dtype == 1 ? 2 : 0);
+}
 
 static float bf16_to_f32(uint16_t h)
 {
@@ -47,17 +60,31 @@ static uint16_t f32_to_bf16(float f)
 
 static float load(const void* p, int32_t dtype, int64_t j)
 {
-    if (dtype == 0)
+    if (etype(dtype) == 0)
         return ((const float*)p)[j];
     return bf16_to_f32(((const uint16_t*)p)[j]);
 }
 
 static void store(void* p, int32_t dtype, int64_t j, float v)
 {
-    if (dtype == 0)
+    if (etype(dtype) == 0)
         ((float*)p)[j] = v;
     else
         ((uint16_t*)p)[j] = f32_to_bf16(v);
+}
+
+/* Delta of expert buffer ex at element j: fl32(x_i - x_0) for weights (x0
+ * is x_0 there), the stored delta itself under ORC_DELTA. */
+static float delta_at(const void* ex, int32_t dtype, int64_t j, float x0)
+{
+    const float x = load(ex, dtype, j);
+    return (dtype & ORC_DELTA) ? x : x - x0;
+}
+
+/* The same, reading x_0 from the base only where it is needed. */
+static float delta_vs_base(const void* ex, const void* base, int32_t dtype, int64_t j)
+{
+    return (dtype & ORC_DELTA) ? load(ex, dtype, j) : load(ex, dtype, j) - load(base, dtype, j);
 }
 
 void orc_round_bf16(const float* x, uint16_t* y, int64_t n)
@@ -144,7 +171,7 @@ static float block_sumsq(const void* base, const void* ex, int32_t dtype, int64_
                 int64_t j = (r * 64 + l) * V + e;
                 if (j >= n)
                     continue;
-                float d = load(ex, dtype, doff + j) - load(base, dtype, doff + j);
+                float d = delta_vs_base(ex, base, dtype, doff + j);
                 p[l] = fmaf(d, d, p[l]);
             }
         }
@@ -300,7 +327,7 @@ int orc_merge_avg(int64_t nb, const int64_t* doff, const int64_t* len, int32_t d
             for (int32_t i = 0; i < K; ++i) {
                 if (!((mask[b] >> i) & 1u))
                     continue;
-                float d = load(experts[i], dtype, j) - x0;
+                float d = delta_at(experts[i], dtype, j, x0);
                 acc = fmaf(alpha[i], d, acc);
             }
             store(out, dtype, j, x0 + acc);
@@ -340,7 +367,7 @@ int orc_merge_avg_renorm(int64_t nb, const int64_t* doff, const int64_t* len, in
             for (int32_t i = 0; i < K; ++i) {
                 if (!((mask[b] >> i) & 1u))
                     continue;
-                float d = load(experts[i], dtype, j) - x0;
+                float d = delta_at(experts[i], dtype, j, x0);
                 acc = fmaf(beta[i], d, acc);
             }
             store(out, dtype, j, x0 + acc);
@@ -465,7 +492,7 @@ int orc_merge_ties(int64_t nb, const int64_t* doff, const int64_t* len, int32_t 
                 continue;
             float* ti = t + (int64_t)r * n;
             for (int64_t j = 0; j < n; ++j) {
-                ti[j] = load(experts[i], dtype, o + j) - load(base, dtype, o + j);
+                ti[j] = delta_vs_base(experts[i], base, dtype, o + j);
                 m[j] = fabsf(ti[j]);
             }
             float tau = pattern_float(kth_largest_pattern(m, n, k));
@@ -515,7 +542,7 @@ int orc_ties_thresholds(int64_t nb, const int64_t* doff, const int64_t* len, int
         int64_t k = orc_ties_k(n, density);
         for (int32_t i = 0; i < K; ++i) {
             for (int64_t j = 0; j < n; ++j)
-                m[j] = fabsf(load(experts[i], dtype, o + j) - load(base, dtype, o + j));
+                m[j] = fabsf(delta_vs_base(experts[i], base, dtype, o + j));
             tau[b * K + i] = kth_largest_pattern(m, n, k);
         }
         free(m);
@@ -552,7 +579,7 @@ int orc_merge_ties_tau(int64_t nb, const int64_t* doff, const int64_t* len, int3
             float th = pattern_float(tau[b * K + i]);
             float* ti = t + (int64_t)r * n;
             for (int64_t j = 0; j < n; ++j) {
-                float d = load(experts[i], dtype, o + j) - load(base, dtype, o + j);
+                float d = delta_vs_base(experts[i], base, dtype, o + j);
                 float a = fabsf(d);
                 ti[j] = (a >= th && a > 0.0f) ? d : 0.0f;
             }
@@ -654,7 +681,7 @@ int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
                 uint32_t word[4];
                 orc_philox4x32_10(ctr, key, word);
                 uint32_t u = word[e & 3u];
-                float d = load(experts[i], dtype, o + j) - load(base, dtype, o + j);
+                float d = delta_vs_base(experts[i], base, dtype, o + j);
                 t[(int64_t)r * n + j] = (u < T) ? 0.0f : d * scale;
             }
             ++r;

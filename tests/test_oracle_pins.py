@@ -589,6 +589,72 @@ def test_avg_renorm_coefficient_drift_identity_and_bound_all_masks():
 
 
 # --------------------------------------------------------------------------
+# experts stored as explicit deltas (Section 3's executor sources)
+# --------------------------------------------------------------------------
+
+def _dyadic_family(rng, numel, K):
+    # base and deltas on a coarse dyadic grid: W_i = W_0 + Delta_i and
+    # W_i - W_0 are exact in fp32, so both expert forms carry the same deltas
+    P = sum(numel)
+    base = (rng.integers(-2048, 2048, P) / 2.0**16).astype(np.float32)
+    deltas = [(rng.integers(-512, 512, P) / 2.0**18).astype(np.float32) for _ in range(K)]
+    return base, deltas, [base + d for d in deltas]
+
+
+def test_delta_experts_equal_weight_experts_when_exact():
+    rng = np.random.default_rng(31)
+    numel = [4096, 1536, 256, 4096, 2052]
+    b = oracle.Blocks(numel, 4096)
+    K = 4
+    base, deltas, weights = _dyadic_family(rng, numel, K)
+    assert all(np.array_equal(w - base, d) for w, d in zip(weights, deltas))
+    mask = rng.integers(0, 16, b.G).astype(np.uint32)
+    assert np.array_equal(oracle.index(b, "f32", base, deltas, delta=True), oracle.index(b, "f32", base, weights))
+    assert np.array_equal(oracle.ties_thresholds(b, "f32", base, deltas, 0.2, delta=True),
+                          oracle.ties_thresholds(b, "f32", base, weights, 0.2))
+    runs = [
+        lambda ex, dl: oracle.merge_avg(b, "f32", base, ex, mask, [0.1, 0.2, 0.3, 0.4], delta=dl),
+        lambda ex, dl: oracle.merge_avg_renorm(b, "f32", base, ex, mask, [0.1, 0.2, 0.3, 0.4], delta=dl),
+        lambda ex, dl: oracle.merge_ties(b, "f32", base, ex, mask, 0.3, 0.9, delta=dl),
+        lambda ex, dl: oracle.merge_dare(b, "f32", base, ex, mask, 0.6, 5, 0, [0.25] * 4, 1.0, delta=dl),
+        lambda ex, dl: oracle.merge_dare(b, "f32", base, ex, mask, 0.6, 5, 1, [1.0] * 4, 0.7, delta=dl),
+    ]
+    for r in runs:
+        assert np.array_equal(r(deltas, True), r(weights, False))
+
+
+def test_delta_experts_index_does_not_read_the_base():
+    # With explicit deltas the sums of squares and trim thresholds are
+    # functions of the deltas alone; the merged output moves with the base.
+    rng = np.random.default_rng(32)
+    numel = [4096, 1536, 256]
+    b = oracle.Blocks(numel, 4096)
+    base, deltas, _ = _dyadic_family(rng, numel, 3)
+    other = (rng.standard_normal(sum(numel)) * 3.0).astype(np.float32)
+    assert np.array_equal(oracle.index(b, "f32", base, deltas, delta=True),
+                          oracle.index(b, "f32", other, deltas, delta=True))
+    assert np.array_equal(oracle.ties_thresholds(b, "f32", base, deltas, 0.25, delta=True),
+                          oracle.ties_thresholds(b, "f32", other, deltas, 0.25, delta=True))
+    full = np.full(b.G, 7, np.uint32)
+    zero = np.zeros_like(base)
+    # base 0: the AVG output is the weighted delta sum itself; base W_0 adds W_0 (exact here)
+    acc = oracle.merge_avg(b, "f32", zero, deltas, full, [0.25, 0.25, 0.5], delta=True)
+    got = oracle.merge_avg(b, "f32", base, deltas, full, [0.25, 0.25, 0.5], delta=True)
+    assert np.array_equal(got, base + acc)
+
+
+def test_delta_experts_bf16_constant_delta_closed_form():
+    # A constant bf16 delta c = 2^-5 in every element: S = n c^2 exactly.
+    numel = [4096, 1536, 520]
+    b = oracle.Blocks(numel, 4096)
+    P = sum(numel)
+    base = _bits_bf16(np.random.default_rng(33).standard_normal(P).astype(np.float32))
+    d = _bits_bf16(np.full(P, 2.0**-5, np.float32))
+    S = oracle.index(b, "bf16", base, [d], delta=True).reshape(-1)
+    assert np.array_equal(S, (b.len * 2.0**-10).astype(np.float32))
+
+
+# --------------------------------------------------------------------------
 # TIES
 # --------------------------------------------------------------------------
 
