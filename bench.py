@@ -186,6 +186,14 @@ def run_sweep(args):
     log(f"generating {spec.description}: P={P} G={G} experts {where_txt}")
     base, exps = make_family_device(spec, K=K, seed=0, device="cuda",
                                     experts_on_host="pinned" if pinned else ("pageable" if pageable else None))
+    dl = bool(args.experts_delta)
+    if dl:  # the experts as stored deltas fl32(W_i - W_0) in the checkpoint dtype (set-up, not timed)
+        if host:
+            sys.exit("bench.py: --experts-delta supports device-resident experts only")
+        for e in exps:
+            for c0 in range(0, P, 1 << 28):
+                c1 = min(P, c0 + (1 << 28))
+                e[c0:c1] = (e[c0:c1].float() - base[c0:c1].float()).to(e.dtype)
     torch.cuda.synchronize()
     sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
     mask = torch.empty(G, dtype=torch.int32, device="cuda")
@@ -198,16 +206,17 @@ def run_sweep(args):
 
     def merge(io=False):
         if op == "avg":
-            return mp.mp_merge_avg(L, base, exps, mask, [1.0 / K] * K, out, residency=res, io=io, stream=stream)
+            return mp.mp_merge_avg(L, base, exps, mask, [1.0 / K] * K, out, residency=res, io=io, stream=stream,
+                                   delta=dl)
         if op == "avg_renorm":
             return mp.mp_merge_avg_renorm(L, base, exps, mask, [1.0 / K] * K, out, residency=res, io=io,
-                                          stream=stream)
+                                          stream=stream, delta=dl)
         if op == "ties":
             return mp.mp_merge_ties(L, base, exps, mask, cfg["density"], cfg["lam"], out, residency=res, io=io,
-                                    stream=stream)
+                                    stream=stream, delta=dl)
         comb = mp.MP_COMBINE_SIGN_ELECT if cfg["combine"] == "sign_elect" else mp.MP_COMBINE_LINEAR
         return mp.mp_merge_dare(L, base, exps, mask, cfg["p"], cfg["seed"], comb, None, cfg["lam"], out,
-                                residency=res, io=io, stream=stream)
+                                residency=res, io=io, stream=stream, delta=dl)
 
     def timed(fn):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -219,9 +228,9 @@ def run_sweep(args):
 
     reps = max(1, args.steps)
     for _ in range(max(0, args.warmup)):
-        mp.mp_index_blocks(L, base, exps, sumsq, residency=res, stream=stream)
+        mp.mp_index_blocks(L, base, exps, sumsq, residency=res, stream=stream, delta=dl)
     idx_ms = float(np.median([timed(lambda: mp.mp_index_blocks(L, base, exps, sumsq, residency=res,
-                                                                stream=stream))[0] for _ in range(reps)]))
+                                                                stream=stream, delta=dl))[0] for _ in range(reps)]))
     rows = []
     flags = {"none": 0, "per_byte": mp.MP_PLAN_PER_BYTE, "skip_zero": mp.MP_PLAN_SKIP_ZERO,
              "both": mp.MP_PLAN_PER_BYTE | mp.MP_PLAN_SKIP_ZERO}[args.plan_flags]
@@ -267,6 +276,7 @@ def run_sweep(args):
         "warmup": args.warmup, "ms_per_step": round(step_ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": f"{spec.description}; {op} {cfg}", "plan_flags": args.plan_flags,
+                   "experts_form": "explicit deltas" if dl else "fine-tuned weights",
                    "storage_dtype": lay.dtype, "params": P,
                    "blocks": G, "K": K, "experts": where_txt,
                    "parallelism": "single GPU"},
@@ -295,6 +305,8 @@ def main():
                     help="where the TIES trim thresholds are found: in the index pass (catalog) or in each merge")
     ap.add_argument("--plan-flags", default="none", choices=("none", "per_byte", "skip_zero", "both"),
                     help="other workloads: mp_plan options (default: the literal Algorithm 1)")
+    ap.add_argument("--experts-delta", action="store_true",
+                    help="other workloads: pass the experts as stored deltas W_i - W_0 (MP_EXPERTS_DELTA)")
     ap.add_argument("--fidelity", action="store_true",
                     help="other workloads: also report Rel. l2, P95 block and Touched against the full merge")
     ap.add_argument("--calibration-copy", action="store_true",

@@ -70,6 +70,12 @@ extern "C" {
 
 typedef enum { MP_F32 = 0, MP_BF16 = 1 } mp_dtype;
 typedef enum { MP_DEVICE = 0, MP_HOST_PINNED = 1, MP_HOST_PAGEABLE = 2 } mp_residency;
+/* OR-ed into `residency`: the expert buffers hold the deltas
+ * Delta_i = W_i - W_0 themselves (Section 3's "explicit deltas" source)
+ * instead of fine-tuned weights, in the checkpoint dtype.  Then
+ * d = fl32(Delta_i): the index reads no base, the merges read the base only
+ * to add the merged delta to it.  Everything else is unchanged. */
+enum { MP_EXPERTS_DELTA = 16 };
 typedef enum { MP_COMBINE_LINEAR = 0, MP_COMBINE_SIGN_ELECT = 1 } mp_combine;
 /* mp_plan options (bit flags; 0 is the literal Algorithm 1). */
 typedef enum { MP_PLAN_PER_BYTE = 1, MP_PLAN_SKIP_ZERO = 2 } mp_plan_flags;

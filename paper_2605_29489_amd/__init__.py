@@ -28,6 +28,7 @@ MP_E_NOMEM = -3
 MP_E_HIP = -4
 MP_F32, MP_BF16 = 0, 1
 MP_DEVICE, MP_HOST_PINNED, MP_HOST_PAGEABLE = 0, 1, 2
+MP_EXPERTS_DELTA = 16  # OR-ed into residency: experts hold W_i - W_0
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
 MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 
@@ -161,15 +162,17 @@ def mp_layout_blocks(layout: Layout) -> int:
     return int(g.value)
 
 
-def mp_index_blocks(layout: Layout, base, experts, sumsq, residency: int = MP_DEVICE, stream=None):
-    _check(lib.mp_index_blocks(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency,
+def mp_index_blocks(layout: Layout, base, experts, sumsq, residency: int = MP_DEVICE, stream=None,
+                    delta: bool = False):
+    _check(lib.mp_index_blocks(layout.ref, _ptr(base), _ptrs(experts), len(experts), _res(residency, delta),
                                _ptr(sumsq), _stream(stream)))
 
 
 def mp_index_ties(layout: Layout, base, experts, density: float, tau, sumsq=None, residency: int = MP_DEVICE,
-                  stream=None):
+                  stream=None, delta: bool = False):
     """Per-unit TIES thresholds (uint32 patterns in `tau`, G*K) and, if given, sumsq."""
-    _check(lib.mp_index_ties(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, float(density),
+    _check(lib.mp_index_ties(layout.ref, _ptr(base), _ptrs(experts), len(experts), _res(residency, delta),
+                             float(density),
                              _ptr(sumsq), _ptr(tau), _stream(stream)))
 
 
@@ -180,48 +183,55 @@ def mp_plan(layout: Layout, K: int, sumsq, w, budget_bytes: int, mask, flags: in
     return st.as_dict()
 
 
+def _res(residency: int, delta: bool) -> int:
+    return residency | (MP_EXPERTS_DELTA if delta else 0)
+
+
 def _io(io):
     return C.byref(io) if io is not None else None
 
 
 def mp_merge_avg(layout: Layout, base, experts, mask, alpha, out, residency: int = MP_DEVICE,
-                 io: bool = False, stream=None) -> Optional[dict]:
+                 io: bool = False, stream=None, delta: bool = False) -> Optional[dict]:
     st = mp_io_stats() if io else None
-    _check(lib.mp_merge_avg(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+    _check(lib.mp_merge_avg(layout.ref, _ptr(base), _ptrs(experts), len(experts), _res(residency, delta), _ptr(mask),
                             _floats(alpha, len(experts)), _ptr(out), _io(st), _stream(stream)))
     return st.as_dict() if io else None
 
 
 def mp_merge_avg_renorm(layout: Layout, base, experts, mask, alpha, out, residency: int = MP_DEVICE,
-                        io: bool = False, stream=None) -> Optional[dict]:
+                        io: bool = False, stream=None, delta: bool = False) -> Optional[dict]:
     """Selected-only AVG: alpha renormalised over each block's selected experts."""
     st = mp_io_stats() if io else None
-    _check(lib.mp_merge_avg_renorm(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+    _check(lib.mp_merge_avg_renorm(layout.ref, _ptr(base), _ptrs(experts), len(experts), _res(residency, delta),
+                                   _ptr(mask),
                                    _floats(alpha, len(experts)), _ptr(out), _io(st), _stream(stream)))
     return st.as_dict() if io else None
 
 
 def mp_merge_ties(layout: Layout, base, experts, mask, density: float, lam: float, out,
-                  residency: int = MP_DEVICE, io: bool = False, stream=None) -> Optional[dict]:
+                  residency: int = MP_DEVICE, io: bool = False, stream=None, delta: bool = False) -> Optional[dict]:
     st = mp_io_stats() if io else None
-    _check(lib.mp_merge_ties(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+    _check(lib.mp_merge_ties(layout.ref, _ptr(base), _ptrs(experts), len(experts), _res(residency, delta), _ptr(mask),
                              float(density), float(lam), _ptr(out), _io(st), _stream(stream)))
     return st.as_dict() if io else None
 
 
 def mp_merge_ties_tau(layout: Layout, base, experts, mask, tau, lam: float, out, residency: int = MP_DEVICE,
-                      io: bool = False, stream=None) -> Optional[dict]:
+                      io: bool = False, stream=None, delta: bool = False) -> Optional[dict]:
     st = mp_io_stats() if io else None
-    _check(lib.mp_merge_ties_tau(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+    _check(lib.mp_merge_ties_tau(layout.ref, _ptr(base), _ptrs(experts), len(experts), _res(residency, delta),
+                                 _ptr(mask),
                                  _ptr(tau), float(lam), _ptr(out), _io(st), _stream(stream)))
     return st.as_dict() if io else None
 
 
 def mp_merge_dare(layout: Layout, base, experts, mask, p: float, seed: int, combine: int, alpha, lam: float,
-                  out, residency: int = MP_DEVICE, io: bool = False, stream=None) -> Optional[dict]:
+                  out, residency: int = MP_DEVICE, io: bool = False, stream=None,
+                  delta: bool = False) -> Optional[dict]:
     st = mp_io_stats() if io else None
     a = _floats(alpha, len(experts)) if alpha is not None else None
-    _check(lib.mp_merge_dare(layout.ref, _ptr(base), _ptrs(experts), len(experts), residency, _ptr(mask),
+    _check(lib.mp_merge_dare(layout.ref, _ptr(base), _ptrs(experts), len(experts), _res(residency, delta), _ptr(mask),
                              float(p), int(seed) & 0xFFFFFFFF, int(combine), a, float(lam), _ptr(out), _io(st),
                              _stream(stream)))
     return st.as_dict() if io else None

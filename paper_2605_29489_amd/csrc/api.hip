@@ -406,12 +406,22 @@ __global__ void k_zero_u64(unsigned long long* p, int n)
         p[i] = 0ull;
 }
 
+// Splits a residency argument into where the experts live and whether they
+// hold explicit deltas (MP_EXPERTS_DELTA).
+bool take_delta(int32_t* residency)
+{
+    const bool delta = (*residency & MP_EXPERTS_DELTA) != 0;
+    *residency &= ~MP_EXPERTS_DELTA;
+    return delta;
+}
+
 int run_merge(const mp_layout* L, const void* base, const void* const* experts, int32_t K,
               int32_t residency, const uint32_t* mask, void* out, mp_io_stats* io, hipStream_t s,
-              const MergeArgs& a)
+              MergeArgs a)
 {
     std::lock_guard<std::mutex> lock(g_mu);
     g_err.clear();
+    a.bsub = take_delta(&residency) ? 0.0f : 1.0f;
     Common c;
     int rc = check_common(L, base, experts, K, residency, out, &c);
     if (rc)
@@ -484,6 +494,7 @@ int mp_index_blocks(const mp_layout* layout, const void* base, const void* const
 {
     std::lock_guard<std::mutex> lock(g_mu);
     g_err.clear();
+    const bool delta = take_delta(&residency);
     Common c;
     int rc = check_common(layout, base, experts, K, residency, nullptr, &c);
     if (rc)
@@ -495,9 +506,9 @@ int mp_index_blocks(const mp_layout* layout, const void* base, const void* const
     hipError_t e;
     if (residency == MP_HOST_PAGEABLE) {
         uint64_t staged = 0;
-        e = stage_index(bt, base, experts, K, false, 0.0, sumsq, nullptr, s, &staged);
+        e = stage_index(bt, base, experts, K, false, 0.0, sumsq, nullptr, s, &staged, delta);
     } else {
-        e = launch_index(bt, base, c.ex, K, sumsq, s);
+        e = launch_index(bt, base, c.ex, K, sumsq, s, delta);
     }
     if (e != hipSuccess)
         return hip_fail(e, "index launch");
@@ -511,6 +522,7 @@ int mp_index_ties(const mp_layout* layout, const void* base, const void* const* 
     g_err.clear();
     if (!(density >= 0.0 && density <= 1.0))
         return fail(MP_E_ARG, "density %g must be in [0, 1]", density);
+    const bool delta = take_delta(&residency);
     Common c;
     int rc = check_common(layout, base, experts, K, residency, nullptr, &c);
     if (rc)
@@ -526,9 +538,9 @@ int mp_index_ties(const mp_layout* layout, const void* base, const void* const* 
     hipError_t e;
     if (residency == MP_HOST_PAGEABLE) {
         uint64_t staged = 0;
-        e = stage_index(bt, base, experts, K, true, density, sumsq, tau, s, &staged);
+        e = stage_index(bt, base, experts, K, true, density, sumsq, tau, s, &staged, delta);
     } else {
-        e = launch_index_ties(bt, base, c.ex, K, density, sumsq, tau, s);
+        e = launch_index_ties(bt, base, c.ex, K, density, sumsq, tau, s, delta);
     }
     if (e != hipSuccess)
         return hip_fail(e, "index launch");

@@ -21,7 +21,8 @@ namespace {
 
 constexpr int kRows = 8;  // chunk rows a lane keeps in flight per expert
 
-template <int DT>
+// DELTA: the expert buffers hold the deltas themselves (no base read).
+template <int DT, bool DELTA>
 __device__ inline float block_sumsq(const uint4* __restrict__ b, const uint4* __restrict__ e,
                                     uint32_t nch, int lane)
 {
@@ -33,7 +34,8 @@ __device__ inline float block_sumsq(const uint4* __restrict__ b, const uint4* __
         for (int r = 0; r < kRows; ++r) {
             const uint32_t c = c0 + r * 64 + lane;
             if (c < nch) {
-                xb[r] = b[c];
+                if (!DELTA)
+                    xb[r] = b[c];
                 xe[r] = e[c];
             }
         }
@@ -42,11 +44,12 @@ __device__ inline float block_sumsq(const uint4* __restrict__ b, const uint4* __
             const uint32_t c = c0 + r * 64 + lane;
             if (c < nch) {
                 float fb[V], fe[V];
-                Fmt<DT>::unpack(xb[r], fb);
+                if (!DELTA)
+                    Fmt<DT>::unpack(xb[r], fb);
                 Fmt<DT>::unpack(xe[r], fe);
 #pragma unroll
                 for (int q = 0; q < V; ++q) {
-                    const float d = fe[q] - fb[q];
+                    const float d = DELTA ? fe[q] : fe[q] - fb[q];
                     p = fmaf(d, d, p);
                 }
             }
@@ -58,7 +61,7 @@ __device__ inline float block_sumsq(const uint4* __restrict__ b, const uint4* __
     return p;
 }
 
-template <int DT>
+template <int DT, bool DELTA>
 __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, ExpertPtrs ex, int K,
                                                const uint64_t* __restrict__ boff,
                                                const uint32_t* __restrict__ blen,
@@ -73,7 +76,7 @@ __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, Ex
     const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
     for (int i = wave; i < K; i += 4) {
         const uint4* e = chunk_ptr(ex.p[i], off, Fmt<DT>::esize);
-        const float s = block_sumsq<DT>(b, e, nch, lane);
+        const float s = block_sumsq<DT, DELTA>(b, e, nch, lane);
         if (lane == 0)
             sumsq[g * K + i] = s;
     }
@@ -92,7 +95,7 @@ __global__ __launch_bounds__(256) void k_index(const void* __restrict__ base, Ex
 #ifndef MP_CAT_WAVES
 #define MP_CAT_WAVES 4
 #endif
-template <int DT>
+template <int DT, bool DELTA>
 __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
     const void* __restrict__ base, ExpertPtrs ex, int K, const uint64_t* __restrict__ boff,
     const uint32_t* __restrict__ blen, uint32_t n_full, uint32_t k_full, double density, float gcoef,
@@ -122,11 +125,12 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             float fb[V], fe[V];
-            Fmt<DT>::unpack(xb[r * 64 + lane], fb);
+            if (!DELTA)
+                Fmt<DT>::unpack(xb[r * 64 + lane], fb);
             Fmt<DT>::unpack(xe[r], fe);
 #pragma unroll
             for (int q = 0; q < V; ++q) {
-                d[r * V + q] = fe[q] - fb[q];             // padding: 0 - 0
+                d[r * V + q] = DELTA ? fe[q] : fe[q] - fb[q];  // padding: 0 - 0
                 p = fmaf(d[r * V + q], d[r * V + q], p);  // + 0 on padding, exact
             }
         }
@@ -157,13 +161,15 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
     uint4 xf[R];
     if (wave < K)
         load_expert(wave, xf);
-    const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
+    if (!DELTA) {  // explicit deltas need no base
+        const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
 #pragma unroll
-    for (int q = 0; q < R / 4; ++q) {
-        const uint32_t c = (uint32_t)(q * 256 + t);
-        xb[c] = (c < nch) ? b[c] : make_uint4(0u, 0u, 0u, 0u);
+        for (int q = 0; q < R / 4; ++q) {
+            const uint32_t c = (uint32_t)(q * 256 + t);
+            xb[c] = (c < nch) ? b[c] : make_uint4(0u, 0u, 0u, 0u);
+        }
+        __syncthreads();
     }
-    __syncthreads();
     if (wave < K)
         unit(wave, xf);
     for (int i = wave + 4; i < K; i += 4) {
@@ -192,7 +198,7 @@ static double normal_two_sided_quantile(double rho)
 }
 
 hipError_t launch_index_ties(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
-                             double density, float* sumsq, uint32_t* tau, hipStream_t s)
+                             double density, float* sumsq, uint32_t* tau, hipStream_t s, bool delta)
 {
     if (bt.G == 0)
         return hipSuccess;
@@ -205,25 +211,30 @@ hipError_t launch_index_ties(const BlockTable& bt, const void* base, const Exper
     // counts; the thresholds are exact for any data.
     const float gcoef = (float)(0.6 * normal_two_sided_quantile(density));
     const dim3 grid((unsigned)bt.G), block(256);
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, n_full, k_full, density, gcoef,
+                           sumsq, tau);
+    };
     if (bt.dtype == 0)
-        hipLaunchKernelGGL(k_index_ties<0>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, n_full, k_full,
-                           density, gcoef, sumsq, tau);
+        delta ? go(k_index_ties<0, true>) : go(k_index_ties<0, false>);
     else
-        hipLaunchKernelGGL(k_index_ties<1>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, n_full, k_full,
-                           density, gcoef, sumsq, tau);
+        delta ? go(k_index_ties<1, true>) : go(k_index_ties<1, false>);
     return hipGetLastError();
 }
 
 hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
-                        float* sumsq, hipStream_t s)
+                        float* sumsq, hipStream_t s, bool delta)
 {
     if (bt.G == 0)
         return hipSuccess;
     const dim3 grid((unsigned)bt.G), block(256);
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, sumsq);
+    };
     if (bt.dtype == 0)
-        hipLaunchKernelGGL(k_index<0>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, sumsq);
+        delta ? go(k_index<0, true>) : go(k_index<0, false>);
     else
-        hipLaunchKernelGGL(k_index<1>, grid, block, 0, s, base, ex, K, bt.d_off, bt.d_len, sumsq);
+        delta ? go(k_index<1, true>) : go(k_index<1, false>);
     return hipGetLastError();
 }
 

@@ -88,7 +88,7 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
                                                    float lambda, uint32_t drop_T, float scale,
                                                    uint32_t seed, uint32_t kmask, void* __restrict__ out,
                                                    unsigned long long* __restrict__ ctr,
-                                                   const uint32_t* __restrict__ tau, int K)
+                                                   const uint32_t* __restrict__ tau, int K, float bsub)
 {
     constexpr int V = Fmt<DT>::V;
     constexpr int ES = Fmt<DT>::esize;
@@ -228,7 +228,9 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
 #pragma unroll
                     for (int v = 0; v < V; ++v) {
                         const int e = q * V + v;
-                        const float d = x[v] - x0[e];
+                        // x - x0 (bsub = 1: exactly the difference), or the stored
+                        // delta itself (bsub = 0: explicit deltas)
+                        const float d = fmaf(-bsub, x0[e], x[v]);
                         if (is_avg<MODE>()) {
                             acc[e] = fmaf(coef, d, acc[e]);
                         } else if (MODE == M_TIES_TAU) {
@@ -458,7 +460,8 @@ __device__ inline void ties_load_group(const Src& src, int64_t b, uint64_t off, 
 // publishes the wave maxima of |d|.
 template <int DT, int CPT>
 __device__ inline void ties_deltas(TiesSmem& sm, const uint4 (&raw)[ties::GS][CPT], int ns,
-                                   const float (&x0)[CPT * Fmt<DT>::V], float (&d)[ties::GS][CPT * Fmt<DT>::V])
+                                   const float (&x0)[CPT * Fmt<DT>::V], float (&d)[ties::GS][CPT * Fmt<DT>::V],
+                                   float bsub)
 {
     using namespace ties;
     constexpr int V = Fmt<DT>::V;
@@ -481,7 +484,7 @@ __device__ inline void ties_deltas(TiesSmem& sm, const uint4 (&raw)[ties::GS][CP
                 Fmt<DT>::unpack(raw[j][q], x);
 #pragma unroll
                 for (int v = 0; v < V; ++v)
-                    d[j][q * V + v] = x[v] - x0[q * V + v];  // padding: 0 - 0
+                    d[j][q * V + v] = fmaf(-bsub, x0[q * V + v], x[v]);  // x - x0 or the delta; padding 0
 #pragma unroll
                 for (int v = 0; v < V; v += 2)  // pairs: one three-way maximum each
                     mx = fmaxf(mx, fmaxf(fabsf(d[j][q * V + v]), fabsf(d[j][q * V + v + 1])));
@@ -632,12 +635,13 @@ __device__ inline uint32_t ties_select_group(TiesSmem& sm, uint32_t n, uint32_t 
 template <int DT, int CPT, class Src>
 __device__ inline uint32_t ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, uint64_t off, uint32_t n,
                                        uint32_t k, uint32_t gm, int rank0, const float (&x0)[CPT * Fmt<DT>::V],
-                                       float (&d)[ties::GS][CPT * Fmt<DT>::V], uint32_t (&tau)[ties::GS])
+                                       float (&d)[ties::GS][CPT * Fmt<DT>::V], uint32_t (&tau)[ties::GS],
+                                       float bsub)
 {
     uint4 raw[ties::GS][CPT];
     ties_load_group<DT, CPT>(src, b, off, n, gm, rank0, raw);
     const int ns = __popc(gm);
-    ties_deltas<DT, CPT>(sm, raw, ns, x0, d);
+    ties_deltas<DT, CPT>(sm, raw, ns, x0, d, bsub);
     return ties_select_group<CPT * Fmt<DT>::V>(sm, n, k, ns, d, tau);
 }
 
@@ -818,7 +822,7 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
                                                          const uint32_t* __restrict__ blen, double density,
                                                          uint32_t n_full, uint32_t k_full, float lambda,
                                                          uint32_t kmask, void* __restrict__ out,
-                                                         unsigned long long* __restrict__ ctr)
+                                                         unsigned long long* __restrict__ ctr, float bsub)
 {
     using namespace ties;
     constexpr int V = Fmt<DT>::V, ES = Fmt<DT>::esize;
@@ -857,7 +861,7 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
             Fmt<DT>::unpack(x0raw[q], &x0[q * V]);
         uint32_t top = 0u;
         if (ns != 0) {
-            ties_deltas<DT, CPT>(sm, raw, ns, x0, d);
+            ties_deltas<DT, CPT>(sm, raw, ns, x0, d, bsub);
             top = ties_select_group<E>(sm, n, k, ns, d, tau);
         }
         const bool big = top >= 0x7e000000u;  // some |d| >= 2^125: masses may overflow
@@ -898,7 +902,7 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
                 gm |= mm & (0u - mm);
                 mm &= mm - 1u;
             }
-            ties_trim_group<DT, CPT>(sm, src, b, off, n, k, gm, rank0, x0, d, tau);
+            ties_trim_group<DT, CPT>(sm, src, b, off, n, k, gm, rank0, x0, d, tau, bsub);
             const int ns = __popc(gm);
             switch (ns) {
             case 1: ties_accumulate_all<1>(d, tau, P, N, cnt); break;
@@ -939,27 +943,27 @@ hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src
     case Op::AVG:
         hipLaunchKernelGGL((k_merge_elem<DT, M_AVG, Src>), grid, block, 0, s, src, base, mask, bt.d_off,
                            bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask, out, ctr,
-                           nullptr, K);
+                           nullptr, K, a.bsub);
         break;
     case Op::AVG_RENORM:
         hipLaunchKernelGGL((k_merge_elem<DT, M_AVG_RENORM, Src>), grid, block, 0, s, src, base, mask, bt.d_off,
                            bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask, out, ctr,
-                           nullptr, K);
+                           nullptr, K, a.bsub);
         break;
     case Op::DARE_LINEAR:
         hipLaunchKernelGGL((k_merge_elem<DT, M_DARE_LIN, Src>), grid, block, 0, s, src, base, mask,
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, T, scale,
-                           a.seed, kmask, out, ctr, nullptr, K);
+                           a.seed, kmask, out, ctr, nullptr, K, a.bsub);
         break;
     case Op::DARE_SIGN:
         hipLaunchKernelGGL((k_merge_elem<DT, M_DARE_SIGN, Src>), grid, block, 0, s, src, base, mask,
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, T, scale,
-                           a.seed, kmask, out, ctr, nullptr, K);
+                           a.seed, kmask, out, ctr, nullptr, K, a.bsub);
         break;
     case Op::TIES_TAU:
         hipLaunchKernelGGL((k_merge_elem<DT, M_TIES_TAU, Src>), grid, block, 0, s, src, base, mask,
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask,
-                           out, ctr, a.tau, K);
+                           out, ctr, a.tau, K, a.bsub);
         break;
     case Op::TIES: {
         // k for full-length blocks, as the kernel computes it for short ones
@@ -968,10 +972,10 @@ hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src
         const uint32_t k_full = (kk >= (double)n_full) ? n_full : (uint32_t)kk;
         if (K <= ties::GS)
             hipLaunchKernelGGL((k_merge_ties<DT, false, Src>), grid, dim3(ties::NT), 0, s, src, base, mask,
-                               bt.d_off, bt.d_len, a.density, n_full, k_full, a.lambda, kmask, out, ctr);
+                               bt.d_off, bt.d_len, a.density, n_full, k_full, a.lambda, kmask, out, ctr, a.bsub);
         else
             hipLaunchKernelGGL((k_merge_ties<DT, true, Src>), grid, dim3(ties::NT), 0, s, src, base, mask,
-                               bt.d_off, bt.d_len, a.density, n_full, k_full, a.lambda, kmask, out, ctr);
+                               bt.d_off, bt.d_len, a.density, n_full, k_full, a.lambda, kmask, out, ctr, a.bsub);
         break;
     }
     }

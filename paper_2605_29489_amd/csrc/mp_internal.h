@@ -66,12 +66,12 @@ struct PlanScratch {
 // Expert pointers are device addresses: device memory or the device view of
 // pinned host memory (the kernels then read over PCIe).
 hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
-                        float* sumsq, hipStream_t s);
+                        float* sumsq, hipStream_t s, bool delta = false);
 
 // Index plus the per-unit TIES thresholds for `density` (sumsq may be null).
 // Blocks must hold at most kTiesMaxBlock elements.
 hipError_t launch_index_ties(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
-                             double density, float* sumsq, uint32_t* tau, hipStream_t s);
+                             double density, float* sumsq, uint32_t* tau, hipStream_t s, bool delta = false);
 
 // Algorithm 1 on the device (k_plan.hip).
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
@@ -90,6 +90,7 @@ struct MergeArgs {
     double p = 0.0;
     uint32_t seed = 0;
     const uint32_t* tau = nullptr;  // TIES_TAU: per-unit thresholds [G*K]
+    float bsub = 1.0f;  // d = x_i - bsub * x_0: 1 for fine-tuned weights, 0 for explicit deltas
 };
 
 hipError_t launch_merge(const BlockTable& bt, const MergeArgs& a, const void* base,
@@ -111,7 +112,8 @@ hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const v
 void set_stage_bytes(size_t bytes);
 void release_stagers();
 hipError_t stage_index(const BlockTable& bt, const void* base, const void* const* experts, int K, bool ties,
-                       double density, float* sumsq, uint32_t* tau, hipStream_t s, uint64_t* h2d);
+                       double density, float* sumsq, uint32_t* tau, hipStream_t s, uint64_t* h2d,
+                       bool delta = false);
 hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* base, const void* const* experts,
                        int K, const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s,
                        uint64_t* h2d);

@@ -191,7 +191,7 @@ void release_stagers()
 }
 
 hipError_t stage_index(const BlockTable& bt, const void* base, const void* const* experts, int K, bool ties,
-                       double density, float* sumsq, uint32_t* tau, hipStream_t s, uint64_t* h2d)
+                       double density, float* sumsq, uint32_t* tau, hipStream_t s, uint64_t* h2d, bool delta)
 {
     *h2d = 0;
     if (bt.G == 0)
@@ -236,8 +236,8 @@ hipError_t stage_index(const BlockTable& bt, const void* base, const void* const
                                                     (uintptr_t)(e0 * es));
         const BlockTable v = view_of(bt, b0, nb);
         float* sq = sumsq ? sumsq + b0 * K : nullptr;
-        e = ties ? launch_index_ties(v, base, ex, K, density, sq, tau + b0 * K, s)
-                 : launch_index(v, base, ex, K, sq, s);
+        e = ties ? launch_index_ties(v, base, ex, K, density, sq, tau + b0 * K, s, delta)
+                 : launch_index(v, base, ex, K, sq, s, delta);
         if (e != hipSuccess || (e = hipEventRecord(st->consumed[k], s)) != hipSuccess)
             return e;
         *h2d += bytes;

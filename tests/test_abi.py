@@ -81,6 +81,10 @@ def test_argument_errors_before_any_device_call(mp):
         assert lib.mp_plan(L.ref, K, None, w, 0, 0, None, C.byref(st), None) == mp.MP_E_ARG
     # bad residency
     assert lib.mp_index_blocks(L.ref, None, ptrs, 1, 5, None, None) == mp.MP_E_ARG
+    # the explicit-delta bit combines with a valid residency only
+    assert lib.mp_index_blocks(L.ref, None, ptrs, 1, mp.MP_EXPERTS_DELTA | 3, None, None) == mp.MP_E_ARG
+    assert lib.mp_index_blocks(L.ref, None, ptrs, 1, 32, None, None) == mp.MP_E_ARG
+    assert "residency" in mp.mp_last_error()
     # unsupported plan flags (bits other than per-byte and skip-zero)
     st = mp.mp_plan_stats()
     w = (C.c_float * 1)(1.0)

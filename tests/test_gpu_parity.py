@@ -64,9 +64,10 @@ def _lay(mp, spec):
     return mp.Layout(lay.numel, lay.block_elems, lay.dtype_code), lay
 
 
-def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **kw):
+def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, delta=False, **kw):
     """Index, plan and merge on the GPU and with the oracle; compare.  With
-    residency MP_HOST_PINNED the experts stay in pinned host memory."""
+    residency MP_HOST_PINNED the experts stay in pinned host memory; with
+    delta the expert arrays are explicit deltas (MP_EXPERTS_DELTA)."""
     import torch
     L, lay = _lay(mp, spec)
     K = len(exps_np)
@@ -85,13 +86,13 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
     tau = None
     if op == "ties_tau":  # catalog pass: sums of squares and per-unit thresholds together
         tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
-        mp.mp_index_ties(L, base, exps, kw["density"], tau, sumsq=sumsq, residency=res)
-        t_orc = oracle.ties_thresholds(blocks, dtype, base_np, exps_np, kw["density"]).reshape(-1)
+        mp.mp_index_ties(L, base, exps, kw["density"], tau, sumsq=sumsq, residency=res, delta=delta)
+        t_orc = oracle.ties_thresholds(blocks, dtype, base_np, exps_np, kw["density"], delta=delta).reshape(-1)
         assert np.array_equal(tau.cpu().numpy().view(np.uint32), t_orc), "thresholds differ"
     else:
-        mp.mp_index_blocks(L, base, exps, sumsq, residency=res)
+        mp.mp_index_blocks(L, base, exps, sumsq, residency=res, delta=delta)
     S_gpu = sumsq.cpu().numpy()
-    S_orc = oracle.index(blocks, dtype, base_np, exps_np).reshape(-1)
+    S_orc = oracle.index(blocks, dtype, base_np, exps_np, delta=delta).reshape(-1)
     assert np.array_equal(S_gpu.view(np.uint32), S_orc.view(np.uint32)), "index differs"
     if w is None:
         w = [1.0 / K] * K if op in ("avg", "avg_renorm", "dare_lin") else [1.0] * K
@@ -111,28 +112,29 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, **
         assert st["digest"] == st_orc["digest"]
         assert st["n_units"] == G * K and st["budget_bytes"] == B
         if op == "avg":
-            io = mp.mp_merge_avg(L, base, exps, mask, kw["alpha"], out, residency=res, io=True)
-            want = oracle.merge_avg(blocks, dtype, base_np, exps_np, m_orc, kw["alpha"])
+            io = mp.mp_merge_avg(L, base, exps, mask, kw["alpha"], out, residency=res, io=True, delta=delta)
+            want = oracle.merge_avg(blocks, dtype, base_np, exps_np, m_orc, kw["alpha"], delta=delta)
         elif op == "avg_renorm":
-            io = mp.mp_merge_avg_renorm(L, base, exps, mask, kw["alpha"], out, residency=res, io=True)
-            want = oracle.merge_avg_renorm(blocks, dtype, base_np, exps_np, m_orc, kw["alpha"])
+            io = mp.mp_merge_avg_renorm(L, base, exps, mask, kw["alpha"], out, residency=res, io=True, delta=delta)
+            want = oracle.merge_avg_renorm(blocks, dtype, base_np, exps_np, m_orc, kw["alpha"], delta=delta)
         elif op == "ties":
-            io = mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out, residency=res, io=True)
-            want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"])
+            io = mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out, residency=res, io=True,
+                                  delta=delta)
+            want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"], delta=delta)
         elif op == "ties_tau":
-            io = mp.mp_merge_ties_tau(L, base, exps, mask, tau, kw["lam"], out, residency=res, io=True)
-            want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"])
+            io = mp.mp_merge_ties_tau(L, base, exps, mask, tau, kw["lam"], out, residency=res, io=True, delta=delta)
+            want = oracle.merge_ties(blocks, dtype, base_np, exps_np, m_orc, kw["density"], kw["lam"], delta=delta)
             # the in-merge trim gives the same bits
             out2 = torch.empty_like(base)
-            mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out2, residency=res)
+            mp.mp_merge_ties(L, base, exps, mask, kw["density"], kw["lam"], out2, residency=res, delta=delta)
             assert torch.equal(out.view(torch.int16) if out.dtype == torch.bfloat16 else out.view(torch.int32),
                                out2.view(torch.int16) if out2.dtype == torch.bfloat16 else out2.view(torch.int32))
         else:
             comb = 0 if op == "dare_lin" else 1
             io = mp.mp_merge_dare(L, base, exps, mask, kw["p"], kw["seed"], comb, kw.get("alpha"), kw["lam"],
-                                  out, residency=res, io=True)
+                                  out, residency=res, io=True, delta=delta)
             want = oracle.merge_dare(blocks, dtype, base_np, exps_np, m_orc, kw["p"], kw["seed"], comb,
-                                     kw.get("alpha", [1.0] * K), kw["lam"])
+                                     kw.get("alpha", [1.0] * K), kw["lam"], delta=delta)
         got = to_host(out)
         nb = assert_merge_equal(got, want, base_np, dtype, f"{op} B={B}")
         assert nb == 0, f"{op} B={B}: {nb} values within tolerance but not bitwise equal"
@@ -296,6 +298,43 @@ def test_block_sizes(mp, be):
     _run_all(mp, spec, base, exps, "ties", [0.35, 1.0], density=0.3, lam=1.0)
     _run_all(mp, spec, base, exps, "ties_tau", [0.35, 1.0], density=0.3, lam=1.0)
     _run_all(mp, spec, base, exps, "dare_lin", [0.5], alpha=[0.3, 0.2, 0.4, 0.1], p=0.3, seed=11, lam=1.0)
+
+
+def _as_deltas(base_np, exps_np, dtype):
+    """Explicit-delta experts of a family: fl32(W_i - W_0) in the checkpoint
+    dtype (any arrays of that dtype are valid deltas)."""
+    if dtype == "f32":
+        return [(e - base_np).astype(np.float32) for e in exps_np]
+    f = lambda u: (u.astype(np.uint32) << 16).view(np.float32)
+    return [oracle.round_bf16(f(e) - f(base_np)) for e in exps_np]
+
+
+@pytest.mark.parametrize("op", ["avg", "avg_renorm", "ties", "ties_tau", "dare_lin", "dare_sign"])
+def test_explicit_delta_experts_all_ops(mp, op):
+    # experts given as stored deltas (MP_EXPERTS_DELTA): the index reads no
+    # base, the merges add the merged delta to the base; bf16 and ragged fp32
+    spec = _mini_qwen()
+    base, exps = make_family(spec, seed=1)
+    kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0, p=0.9, seed=7)
+    _say(f"case mini-qwen bf16 {op}, explicit deltas")
+    _run_all(mp, spec, base, _as_deltas(base, exps, "bf16"), op, [0, 0.3, 0.7, 1.0], delta=True, **kw)
+    spec = _ragged_f32()
+    base, exps = make_family(spec, seed=2)
+    kw = dict(alpha=[0.5, 0.25, 0.25], density=0.1, lam=0.8, p=0.5, seed=3)
+    _say(f"case ragged fp32 {op}, explicit deltas")
+    _run_all(mp, spec, base, _as_deltas(base, exps, "f32"), op, [0.3, 1.0], delta=True, **kw)
+
+
+def test_explicit_delta_experts_on_the_host(mp):
+    # the delta flag combined with both host feeds
+    spec = _mini_qwen(n_layers=1)
+    base, exps = make_family(spec, seed=9)
+    d = _as_deltas(base, exps, "bf16")
+    kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0)
+    for res in (mp.MP_HOST_PINNED, mp.MP_HOST_PAGEABLE):
+        for op in ("avg", "ties_tau"):
+            _say(f"case explicit deltas, residency {res}, {op}")
+            _run_all(mp, spec, base, d, op, [0.4, 1.0], residency=res, delta=True, **kw)
 
 
 def test_avg_renorm_coefficients(mp):
