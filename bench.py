@@ -396,6 +396,18 @@ def main():
     else:
         io = mp.mp_merge_ties(L, base, exps, masks[0], 0.2, 1.0, out, io=True, stream=stream)
     assert io["expert_bytes"] == stats[0]["cost_bytes"]
+    # the run's manifest for the first budget (after the timed region): coverage
+    # per (tensor, expert), realized reads per expert, plan replay
+    from paper_2605_29489_amd.manifest import build_manifest, replay
+    a, b = ev(), ev()
+    a.record(stream)
+    cov = mp.mp_coverage(L, K, masks[0], stream=stream)
+    b.record(stream)
+    torch.cuda.synchronize()
+    man = build_manifest(L, K, stats[0], io, cov, "ties", {"density": 0.2, "lambda": 1.0})
+    rp = replay(man, mp, L, K, sumsq, [1.0] * K, masks[0], stream=stream)
+    manifest_check = {"coverage_ms": round(a.elapsed_time(b), 4), "within_plan": man["realized"]["within_plan"],
+                      "reads_match_coverage": man["realized"]["matches_coverage"], "replay_ok": rp["ok"]}
     # the other route, once, for reference (its own index pass first)
     if catalog:
         mp.mp_index_blocks(L, base, exps, sumsq, stream=stream)
@@ -471,6 +483,7 @@ def main():
             "per_budget": per_budget,
             "other_route": {"route": "in-merge" if catalog else "catalog",
                             "merge_ms": [round(float(x), 4) for x in alt_ms]},
+            "manifest_B0": manifest_check,
         },
     }
     if not args.no_cpu_baseline:

@@ -102,6 +102,7 @@ typedef struct mp_io_stats {
     uint64_t out_bytes;    /* output bytes written */
     uint64_t h2d_bytes;    /* expert bytes moved over PCIe (MP_HOST_PINNED: read by
                               the kernels; MP_HOST_PAGEABLE: staged copies), else 0 */
+    uint64_t expert_bytes_by_expert[32]; /* expert_bytes split by expert i (0 past K) */
 } mp_io_stats;
 
 /* Number of blocks G of a layout (Section 2's block partition).
@@ -167,6 +168,15 @@ int mp_index_ties(const mp_layout* layout, const void* base,
 int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq,
             const float* w, uint64_t budget_bytes, uint32_t flags,
             uint32_t* mask, mp_plan_stats* stats, void* stream);
+
+/* Coverage of an access mask for the run's manifest (Section 3: the
+ * executor records touched blocks and contributing experts).
+ * cov: HOST uint64[n_tensors * K]; cov[t*K + i] = number of elements of
+ * tensor t in blocks that select expert i (0: expert i contributes nothing
+ * to tensor t).  mask: device uint32[G] as written by mp_plan (bits of
+ * experts >= K are ignored).  Synchronises `stream` before returning. */
+int mp_coverage(const mp_layout* layout, int32_t K, const uint32_t* mask,
+                uint64_t* cov, void* stream);
 
 /* Budgeted AVG (Eq. 4 with Appendix A.1's Psi_AVG): per element
  * acc = +0; for selected i in increasing order acc = fma(alpha_i, d_i, acc);

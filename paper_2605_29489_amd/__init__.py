@@ -32,7 +32,7 @@ MP_EXPERTS_DELTA = 16  # OR-ed into residency: experts hold W_i - W_0
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
 MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 
-EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg", "mp_merge_avg_renorm",
+EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
            "mp_merge_ties",
            "mp_merge_ties_tau", "mp_merge_dare", "mp_set_stage_bytes", "mp_last_error", "mp_release")
 
@@ -52,10 +52,12 @@ class mp_plan_stats(C.Structure):
 
 class mp_io_stats(C.Structure):
     _fields_ = [("expert_bytes", C.c_uint64), ("base_bytes", C.c_uint64), ("out_bytes", C.c_uint64),
-                ("h2d_bytes", C.c_uint64)]
+                ("h2d_bytes", C.c_uint64), ("expert_bytes_by_expert", C.c_uint64 * 32)]
 
     def as_dict(self):
-        return {f: int(getattr(self, f)) for f, _ in self._fields_}
+        d = {f: int(getattr(self, f)) for f, _ in self._fields_[:4]}
+        d["expert_bytes_by_expert"] = [int(x) for x in self.expert_bytes_by_expert]
+        return d
 
 
 class MPError(RuntimeError):
@@ -77,6 +79,7 @@ def _load():
     L.mp_merge_avg.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.POINTER(C.c_float), vp,
                                C.POINTER(mp_io_stats), vp]
     L.mp_merge_avg_renorm.argtypes = L.mp_merge_avg.argtypes
+    L.mp_coverage.argtypes = [lp, i32, vp, C.POINTER(C.c_uint64), vp]
     L.mp_merge_ties.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, C.c_float, vp,
                                 C.POINTER(mp_io_stats), vp]
     L.mp_merge_ties_tau.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, vp, C.c_float, vp,
@@ -88,7 +91,7 @@ def _load():
     L.mp_set_stage_bytes.restype = i32
     L.mp_last_error.argtypes = []
     L.mp_release.argtypes = []
-    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_merge_avg",
+    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_coverage", "mp_merge_avg",
                  "mp_merge_avg_renorm", "mp_merge_ties",
                  "mp_merge_ties_tau",
                  "mp_merge_dare"):
@@ -189,6 +192,14 @@ def _res(residency: int, delta: bool) -> int:
 
 def _io(io):
     return C.byref(io) if io is not None else None
+
+
+def mp_coverage(layout: Layout, K: int, mask, stream=None):
+    """Touched elements per (tensor, expert) of a mask: numpy uint64 [n_tensors, K]."""
+    import numpy as np
+    cov = np.zeros(len(layout.numel) * K, np.uint64)
+    _check(lib.mp_coverage(layout.ref, K, _ptr(mask), cov.ctypes.data_as(C.POINTER(C.c_uint64)), _stream(stream)))
+    return cov.reshape(len(layout.numel), K)
 
 
 def mp_merge_avg(layout: Layout, base, experts, mask, alpha, out, residency: int = MP_DEVICE,

@@ -47,6 +47,8 @@ struct DeviceWs {
     PlanScratch plan;
     unsigned long long* counters = nullptr;  // [256]
     unsigned long long* h_counters = nullptr;  // pinned [256]
+    unsigned long long* cov = nullptr;         // coverage counters, grown on demand
+    int64_t cov_cap = 0;
 };
 
 std::mutex g_mu;
@@ -76,6 +78,7 @@ void free_ws(int dev, DeviceWs& w)
     (void)hipHostFree(w.plan.h_stats);
     (void)hipFree(w.counters);
     (void)hipHostFree(w.h_counters);
+    (void)hipFree(w.cov);
     (void)hipSetDevice(cur);
 }
 
@@ -455,8 +458,10 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
         if ((e = hipStreamSynchronize(s)) != hipSuccess)
             return hip_fail(e, "hipStreamSynchronize");
         unsigned long long sum = 0;
-        for (int q = 0; q < 256; ++q)
+        for (int q = 0; q < 256; ++q) {  // slot (block mod 8) * 32 + expert
+            st.expert_bytes_by_expert[q & 31] += c.ws->h_counters[q];
             sum += c.ws->h_counters[q];
+        }
         st.expert_bytes = sum;
         if (residency == MP_HOST_PINNED)
             st.h2d_bytes = sum;  // expert blocks are read over PCIe, nothing else crosses it
@@ -544,6 +549,45 @@ int mp_index_ties(const mp_layout* layout, const void* base, const void* const* 
     }
     if (e != hipSuccess)
         return hip_fail(e, "index launch");
+    return MP_OK;
+}
+
+int mp_coverage(const mp_layout* layout, int32_t K, const uint32_t* mask, uint64_t* cov, void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    int es = 0;
+    int rc = validate_layout(layout, &es);
+    if (rc)
+        return rc;
+    if (K < 1 || K > kMaxK)
+        return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
+    if (cov == nullptr)
+        return fail(MP_E_ARG, "cov is NULL");
+    BlockTable* bt = nullptr;
+    DeviceWs* ws = nullptr;
+    if ((rc = get_table(layout, es, &bt)) || (rc = get_ws(&ws)))
+        return rc;
+    if ((rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)bt->G, "mask")))
+        return rc;
+    const int64_t n = bt->n_tensors * K;
+    hipError_t e;
+    if (n > ws->cov_cap) {
+        (void)hipFree(ws->cov);
+        ws->cov = nullptr;
+        ws->cov_cap = 0;
+        if ((e = hipMalloc((void**)&ws->cov, sizeof(unsigned long long) * (size_t)n)) != hipSuccess)
+            return fail(MP_E_NOMEM, "coverage buffer: %s", hipGetErrorString(e));
+        ws->cov_cap = n;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((e = launch_coverage(*bt, K, mask, ws->cov, s)) != hipSuccess)
+        return hip_fail(e, "coverage launch");
+    if (n > 0 && (e = hipMemcpyAsync(cov, ws->cov, sizeof(uint64_t) * (size_t)n, hipMemcpyDeviceToHost, s)) !=
+                     hipSuccess)
+        return hip_fail(e, "coverage readback");
+    if ((e = hipStreamSynchronize(s)) != hipSuccess)
+        return hip_fail(e, "hipStreamSynchronize");
     return MP_OK;
 }
 

@@ -48,10 +48,14 @@ struct StagedSrc {
     }
 };
 
+// Realized expert reads (Prop. 1's N^run): thread i adds the block's bytes
+// of expert i when it is selected, into slot (block mod 8) * 32 + i, so the
+// 256 counters sum per expert and spread the atomics over 8 words each.
 __device__ inline void count_expert_bytes(unsigned long long* ctr, uint32_t m, uint32_t n, int es)
 {
-    if (ctr != nullptr && threadIdx.x == 0 && m != 0u)
-        atomicAdd(&ctr[blockIdx.x & 255u], (unsigned long long)__popc(m) * n * (unsigned long long)es);
+    const uint32_t i = threadIdx.x;
+    if (ctr != nullptr && i < 32u && ((m >> i) & 1u))
+        atomicAdd(&ctr[((blockIdx.x & 7u) << 5) | i], (unsigned long long)n * (unsigned long long)es);
 }
 
 // Divisors for the mean of at most four agreeing entries: {den, fl32(1/den)}

@@ -628,4 +628,61 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
 
 hipError_t plan_ctl_alloc(PlanCtl** ctl) { return hipMalloc((void**)ctl, sizeof(PlanCtl)); }
 
+// ---------------------------------------------------------------- coverage
+// Touched elements per (tensor, expert) of an access mask, for the run's
+// manifest (Section 3: touched blocks and contributing experts):
+// cov[t * K + i] = sum of the lengths of tensor t's blocks selecting expert
+// i.  One thread per block; a wave whose selecting blocks all lie in one
+// tensor (the usual case: blocks run in tensor order) adds one wave sum per
+// expert, other waves add per block.
+namespace {
+__global__ __launch_bounds__(256) void k_zero_cov(unsigned long long* p, int64_t n)
+{
+    for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n; q += (int64_t)gridDim.x * 256)
+        p[q] = 0ull;
+}
+
+__global__ __launch_bounds__(256) void k_coverage(const uint32_t* __restrict__ mask, const uint32_t* __restrict__ len,
+                                                  const uint32_t* __restrict__ tensor, int64_t G, int K,
+                                                  uint32_t kmask, unsigned long long* __restrict__ cov)
+{
+    const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const bool in = g < G;
+    const uint32_t m = in ? (mask[g] & kmask) : 0u;
+    const uint32_t t = in ? tensor[g] : 0u;
+    const unsigned long long n = in ? len[g] : 0ull;
+    const unsigned long long any = __ballot(m != 0u);
+    if (any == 0ull)
+        return;
+    const uint32_t t0 = __shfl(t, __ffsll((long long)any) - 1);
+    if (__ballot(m != 0u && t != t0) == 0ull) {
+        for (int i = 0; i < K; ++i) {
+            unsigned long long v = ((m >> i) & 1u) ? n : 0ull;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1)
+                v += __shfl_xor(v, off);
+            if ((threadIdx.x & 63) == 0 && v != 0ull)
+                atomicAdd(&cov[(uint64_t)t0 * (uint32_t)K + (uint32_t)i], v);
+        }
+    } else {
+        for (uint32_t mm = m; mm; mm &= mm - 1u)
+            atomicAdd(&cov[(uint64_t)t * (uint32_t)K + (uint32_t)__builtin_ctz(mm)], n);
+    }
+}
+}  // namespace
+
+hipError_t launch_coverage(const BlockTable& bt, int K, const uint32_t* mask, unsigned long long* cov, hipStream_t s)
+{
+    const int64_t n = bt.n_tensors * K;
+    if (n > 0)
+        hipLaunchKernelGGL(k_zero_cov, dim3((unsigned)std::min<int64_t>((n + 255) / 256, 1024)), dim3(256), 0, s,
+                           cov, n);
+    if (bt.G > 0) {
+        const uint32_t kmask = (K >= 32) ? 0xffffffffu : ((1u << K) - 1u);
+        hipLaunchKernelGGL(k_coverage, dim3((unsigned)((bt.G + 255) / 256)), dim3(256), 0, s, mask, bt.d_len,
+                           bt.d_tensor, bt.G, K, kmask, cov);
+    }
+    return hipGetLastError();
+}
+
 }  // namespace mp

@@ -73,13 +73,19 @@ hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs
 hipError_t launch_index_ties(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
                              double density, float* sumsq, uint32_t* tau, hipStream_t s, bool delta = false);
 
+// Touched elements per (tensor, expert) of a mask: cov[t * K + i] (device;
+// k_plan.hip).
+hipError_t launch_coverage(const BlockTable& bt, int K, const uint32_t* mask, unsigned long long* cov,
+                           hipStream_t s);
+
 // Algorithm 1 on the device (k_plan.hip).
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
                        const Coeffs& w, uint32_t flags, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
                        hipStream_t s);
 
 // Merge operators.  `counters` is null or a device array of 256 uint64
-// accumulating the expert bytes the kernels load.
+// accumulating the expert bytes the kernels load: slot (block mod 8) * 32 + i
+// holds expert i's.
 enum class Op { AVG = 0, TIES = 1, DARE_LINEAR = 2, DARE_SIGN = 3, TIES_TAU = 4, AVG_RENORM = 5 };
 
 struct MergeArgs {

@@ -42,7 +42,7 @@ def test_struct_layouts_match_header(mp):
     # mp_layout: int32, int32, pointer, int64 -> 24 bytes on LP64
     assert C.sizeof(mp.mp_layout) == 24
     assert C.sizeof(mp.mp_plan_stats) == 48
-    assert C.sizeof(mp.mp_io_stats) == 32
+    assert C.sizeof(mp.mp_io_stats) == 32 + 8 * 32  # four totals + per-expert bytes
 
 
 def test_layout_blocks_counts(mp):

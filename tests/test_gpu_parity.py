@@ -337,6 +337,55 @@ def test_explicit_delta_experts_on_the_host(mp):
             _run_all(mp, spec, base, d, op, [0.4, 1.0], residency=res, delta=True, **kw)
 
 
+def test_manifest_coverage_realized_reads_and_replay(mp):
+    # Section 3's run record: mp_coverage equals the mask's touched elements
+    # per (tensor, expert) by definition; the in-kernel per-expert read
+    # counters equal the coverage bytes (N^run = A) on every feed; the plan
+    # replays to the recorded digest and a tampered budget does not.
+    import json
+    import torch
+    from paper_2605_29489_amd.manifest import build_manifest, dumps, replay
+    spec = _mini_qwen(n_layers=1)
+    base_np, exps_np = make_family(spec, seed=13)
+    L, lay = _lay(mp, spec)
+    K = len(exps_np)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    base = to_dev(base_np, lay.dtype)
+    sumsq = torch.empty(blocks.G * K, dtype=torch.float32, device="cuda")
+    mask = torch.empty(blocks.G, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(base)
+    full = int(blocks.len.sum()) * lay.elem_bytes * K
+    for res in (mp.MP_DEVICE, mp.MP_HOST_PINNED, mp.MP_HOST_PAGEABLE):
+        if res == mp.MP_HOST_PINNED:
+            exps = [to_pinned(e, lay.dtype) for e in exps_np]
+        elif res == mp.MP_HOST_PAGEABLE:
+            exps = [torch.from_numpy(e) for e in exps_np]
+        else:
+            exps = [to_dev(e, lay.dtype) for e in exps_np]
+        _say(f"case manifest, residency {res}")
+        mp.mp_index_blocks(L, base, exps, sumsq, residency=res)
+        st = mp.mp_plan(L, K, sumsq, [0.25] * K, int(0.37 * full), mask)
+        io = mp.mp_merge_avg(L, base, exps, mask, [0.25] * K, out, residency=res, io=True)
+        cov = mp.mp_coverage(L, K, mask)
+        m_np = mask.cpu().numpy().view(np.uint32)
+        want = np.zeros((len(lay.numel), K), np.uint64)
+        for g in range(blocks.G):
+            for i in range(K):
+                if (m_np[g] >> i) & 1:
+                    want[blocks.tensor[g], i] += blocks.len[g]
+        assert np.array_equal(cov, want)
+        assert [int(x) for x in io["expert_bytes_by_expert"][:K]] == [int(c) * lay.elem_bytes for c in want.sum(0)]
+        assert all(x == 0 for x in io["expert_bytes_by_expert"][K:])
+        man = build_manifest(L, K, st, io, cov, "avg", {"alpha": [0.25] * K},
+                             tensor_names=[n for n, _ in spec.tensors], inputs={"family": spec.name, "seed": 13})
+        assert man["realized"]["within_plan"] and man["realized"]["matches_coverage"]
+        man = json.loads(dumps(man))
+        assert replay(man, mp, L, K, sumsq, [0.25] * K, mask)["ok"]
+        bad = json.loads(dumps(man))
+        bad["plan"]["budget_bytes"] = int(0.5 * full)
+        assert not replay(bad, mp, L, K, sumsq, [0.25] * K, mask)["ok"]
+
+
 def test_avg_renorm_coefficients(mp):
     # Selected-only AVG with unequal, non-dyadic coefficients (the quotients
     # alpha_i / s are inexact) and a zero coefficient: blocks whose only
