@@ -50,6 +50,9 @@ def lib():
         L.orc_round_bf16.argtypes = [C.c_void_p, C.c_void_p, C.c_int64]
         L.orc_ties_thresholds.argtypes = [C.c_int64, i64p, i64p, C.c_int32, C.c_void_p, C.POINTER(C.c_void_p),
                                           C.c_int32, C.c_double, C.c_void_p]
+        L.orc_ties_tensor_thresholds.argtypes = [C.c_int64, i64p, i64p, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
+                                                 C.c_void_p, C.POINTER(C.c_void_p), C.c_int32, C.c_void_p,
+                                                 C.c_double, C.c_void_p]
         L.orc_merge_ties_tau.argtypes = [C.c_int64, i64p, i64p, C.c_int32, C.c_void_p, C.POINTER(C.c_void_p),
                                          C.c_int32, C.c_void_p, C.c_void_p, C.c_float, C.c_void_p]
         L.orc_ties_k.restype = C.c_int64
@@ -196,6 +199,28 @@ def ties_thresholds(blocks, dtype, base, experts, density, ids=None, doff=None, 
     _check(L.orc_ties_thresholds(len(ids), d_p, l_p, _dt(dtype, delta), base.ctypes.data, _ptrs(experts),
                                  len(experts), float(density), tau.ctypes.data), "ties thresholds")
     return tau
+
+
+def ties_tensor_thresholds(blocks, dtype, base, experts, mask, density, delta=False):
+    """Per-tensor trim thresholds over the zero-completed masked deltas:
+    uint32 [n_tensors, K] (see orc_ties_tensor_thresholds)."""
+    L = lib()
+    K = len(experts)
+    T = int(blocks.tensor.max()) + 1 if blocks.G else 0
+    mask = np.ascontiguousarray(mask, np.uint32)
+    tau = np.zeros(T * K, np.uint32)
+    d_a, d_p = _i64(blocks.off)
+    l_a, l_p = _i64(blocks.len)
+    t_a = np.ascontiguousarray(blocks.tensor, np.int32)
+    _check(L.orc_ties_tensor_thresholds(blocks.G, d_p, l_p, t_a.ctypes.data_as(C.POINTER(C.c_int32)), T,
+                                        _dt(dtype, delta), base.ctypes.data, _ptrs(experts), K, mask.ctypes.data,
+                                        float(density), tau.ctypes.data), "ties_tensor_thresholds")
+    return tau.reshape(T, K)
+
+
+def expand_tensor_thresholds(blocks, tau_t):
+    """Per-unit thresholds [G * K] from per-tensor ones: unit (g, i) takes its tensor's."""
+    return np.ascontiguousarray(tau_t[blocks.tensor], np.uint32).reshape(-1)
 
 
 def merge_ties_tau(blocks, dtype, base, experts, mask, tau, lam, out=None, ids=None, doff=None, delta=False):

@@ -550,6 +550,82 @@ int orc_ties_thresholds(int64_t nb, const int64_t* doff, const int64_t* len, int
     return bad ? -2 : 0;
 }
 
+/* ------------------------------------------------------------------ */
+/* TIES with a per-tensor trim scope (the original TIES granularity     */
+/* applied per tensor, a variant of Appendix A.1's trim after masking). */
+/* For expert i and tensor t the trim runs over the tensor's zero-      */
+/* completed masked deltas: unselected blocks count as zeros and are    */
+/* never read.  k = orc_ties_k(n_t, density) over the tensor's n_t      */
+/* elements; tau = the k-th largest |d| pattern among them.  With m     */
+/* selected elements and m < k the k-th largest is a completed zero, so */
+/* tau = 0 (every nonzero selected delta is kept); k = 0 gives all ones */
+/* (nothing kept).  Output tau_t[t * K + i].  The blocks of a tensor    */
+/* are consecutive (the partition's order), tensor[b] their tensor id.  */
+/* ------------------------------------------------------------------ */
+int orc_ties_tensor_thresholds(int64_t nb, const int64_t* doff, const int64_t* len, const int32_t* tensor,
+                               int32_t n_tensors, int32_t dtype, const void* base, const void* const* experts,
+                               int32_t K, const uint32_t* mask, double density, uint32_t* tau_t)
+{
+    if (check_common(dtype, K, nb) || n_tensors < 0 || !(density >= 0.0 && density <= 1.0))
+        return -1;
+    int64_t* first = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n_tensors + 1));
+    int64_t* last = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n_tensors + 1));
+    if (!first || !last) {
+        free(first);
+        free(last);
+        return -2;
+    }
+    for (int32_t t = 0; t < n_tensors; ++t)
+        first[t] = last[t] = -1;
+    for (int64_t b = 0; b < nb; ++b) {
+        const int32_t t = tensor[b];
+        if (t < 0 || t >= n_tensors || (last[t] >= 0 && last[t] != b - 1)) {
+            free(first);
+            free(last);
+            return -1;  /* not the partition's consecutive order */
+        }
+        if (first[t] < 0)
+            first[t] = b;
+        last[t] = b;
+    }
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t q = 0; q < (int64_t)n_tensors * K; ++q) {
+        const int32_t t = (int32_t)(q / K), i = (int32_t)(q % K);
+        int64_t n_t = 0, m = 0;
+        for (int64_t b = first[t]; b >= 0 && b <= last[t]; ++b) {
+            n_t += len[b];
+            if ((mask[b] >> i) & 1u)
+                m += len[b];
+        }
+        const int64_t k = orc_ties_k(n_t, density);
+        if (k == 0) {
+            tau_t[q] = 0xffffffffu;
+            continue;
+        }
+        if (m < k) {
+            tau_t[q] = 0u;
+            continue;
+        }
+        float* mag = (float*)malloc(sizeof(float) * (size_t)m);
+        if (!mag) {
+#pragma omp atomic write
+            bad = 1;
+            continue;
+        }
+        int64_t c = 0;
+        for (int64_t b = first[t]; b <= last[t]; ++b)
+            if ((mask[b] >> i) & 1u)
+                for (int64_t j = 0; j < len[b]; ++j)
+                    mag[c++] = fabsf(delta_vs_base(experts[i], base, dtype, doff[b] + j));
+        tau_t[q] = kth_largest_pattern(mag, m, k);
+        free(mag);
+    }
+    free(first);
+    free(last);
+    return bad ? -2 : 0;
+}
+
 /* TIES with the thresholds given: d is kept iff |d| >= float(tau) and  */
 /* |d| > 0, then the election and mean of sign_elect_mean.  With the    */
 /* thresholds of orc_ties_thresholds this is orc_merge_ties exactly.    */

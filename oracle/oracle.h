@@ -70,6 +70,13 @@ int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
 int orc_ties_thresholds(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
                         const void* base, const void* const* experts, int32_t K, double density,
                         uint32_t* tau);
+/* Per-tensor trim thresholds over the zero-completed masked deltas:
+ * tau_t[t*K + i] = the k-th largest |d| pattern of tensor t for expert i,
+ * k = orc_ties_k(n_t, density); 0 when fewer than k elements are selected;
+ * all ones when k = 0.  tensor[b]: tensor id of block b (consecutive). */
+int orc_ties_tensor_thresholds(int64_t nb, const int64_t* doff, const int64_t* len, const int32_t* tensor,
+                               int32_t n_tensors, int32_t dtype, const void* base, const void* const* experts,
+                               int32_t K, const uint32_t* mask, double density, uint32_t* tau_t);
 /* TIES with given thresholds (keep iff |d| >= float(tau) and |d| > 0). */
 int orc_merge_ties_tau(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
                        const void* base, const void* const* experts, int32_t K,

@@ -589,6 +589,71 @@ def test_avg_renorm_coefficient_drift_identity_and_bound_all_masks():
 
 
 # --------------------------------------------------------------------------
+# TIES with a per-tensor trim scope
+# --------------------------------------------------------------------------
+
+def _mag_f32(dtype, x):
+    return _f32_of_bf16(x) if dtype == "bf16" else np.asarray(x, np.float32)
+
+
+def test_ties_tensor_thresholds_are_kth_largest_of_the_zero_completed_tensor():
+    # Definition by a library selection: per (tensor, expert) the tensor's
+    # |d| with unselected blocks set to zero, and np.partition's k-th largest.
+    rng = np.random.default_rng(41)
+    numel = [4096 * 3 + 8, 1536, 16, 4096 * 2]
+    b = oracle.Blocks(numel, 4096)
+    for dtype in ("f32", "bf16"):
+        base, exps = _tiny_family(rng, numel, 3, dtype)
+        for dens in (0.2, 0.05, 0.6, 1.0, 0.0):
+            mask = rng.integers(0, 8, b.G).astype(np.uint32)
+            tau = oracle.ties_tensor_thresholds(b, dtype, base, exps, mask, dens)
+            x0 = _mag_f32(dtype, base)
+            for t in range(len(numel)):
+                gs = np.nonzero(b.tensor == t)[0]
+                lo, hi = b.off[gs[0]], b.off[gs[-1]] + b.len[gs[-1]]
+                for i in range(3):
+                    mag = np.zeros(hi - lo, np.float32)
+                    for g in gs:
+                        if (mask[g] >> i) & 1:
+                            sl = slice(b.off[g], b.off[g] + b.len[g])
+                            mag[b.off[g] - lo:b.off[g] - lo + b.len[g]] = np.abs(_mag_f32(dtype, exps[i][sl]) - x0[sl])
+                    k = oracle.ties_k(hi - lo, dens)
+                    want = 0xFFFFFFFF if k == 0 else int(np.partition(mag, mag.size - k)[mag.size - k].view(np.uint32))
+                    assert int(tau[t, i]) == want, (dtype, dens, t, i)
+
+
+def test_ties_tensor_scope_on_single_block_tensors_is_the_block_scope():
+    # when every tensor is one block the two trim scopes coincide: thresholds
+    # and the full-mask merge equal the (pinned) per-block TIES
+    rng = np.random.default_rng(42)
+    numel = [4096, 1536, 256, 4000]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 4, "bf16")
+    full = np.full(b.G, 15, np.uint32)
+    for dens in (0.2, 0.5):
+        tt = oracle.ties_tensor_thresholds(b, "bf16", base, exps, full, dens)
+        tu = oracle.expand_tensor_thresholds(b, tt)
+        assert np.array_equal(tu, oracle.ties_thresholds(b, "bf16", base, exps, dens).reshape(-1))
+        assert np.array_equal(oracle.merge_ties_tau(b, "bf16", base, exps, full, tu, 1.0),
+                              oracle.merge_ties(b, "bf16", base, exps, full, dens, 1.0))
+
+
+def test_ties_tensor_thresholds_non_anticipatory():
+    rng = np.random.default_rng(43)
+    numel = [4096 * 3, 1536]
+    b = oracle.Blocks(numel, 4096)
+    base, exps = _tiny_family(rng, numel, 3, "bf16")
+    mask = np.array([5, 0, 3, 6], np.uint32)
+    t1 = oracle.ties_tensor_thresholds(b, "bf16", base, exps, mask, 0.3)
+    junk = [e.copy() for e in exps]
+    for g in range(b.G):
+        for i in range(3):
+            if not (mask[g] >> i) & 1:
+                junk[i][b.off[g]:b.off[g] + b.len[g]] = rng.integers(0, 2**15, b.len[g]).astype(np.uint16)
+    assert np.array_equal(t1, oracle.ties_tensor_thresholds(b, "bf16", base, junk, mask, 0.3))
+
+
+# --------------------------------------------------------------------------
 # experts stored as explicit deltas (Section 3's executor sources)
 # --------------------------------------------------------------------------
 
