@@ -203,6 +203,7 @@ def run_sweep(args):
     op = cfg["op"]
     w = [1.0 / K] * K if op in ("avg", "avg_renorm") else [1.0] * K
     stream = torch.cuda.current_stream()
+    tau_t = torch.empty(G * K, dtype=torch.int32, device="cuda") if op == "ties_tensor" else None
 
     def merge(io=False):
         if op == "avg":
@@ -214,6 +215,11 @@ def run_sweep(args):
         if op == "ties":
             return mp.mp_merge_ties(L, base, exps, mask, cfg["density"], cfg["lam"], out, residency=res, io=io,
                                     stream=stream, delta=dl)
+        if op == "ties_tensor":  # thresholds at tensor scope for this mask, then the threshold merge
+            mp.mp_ties_tensor_thresholds(L, base, exps, mask, cfg["density"], tau_t, residency=res, stream=stream,
+                                         delta=dl)
+            return mp.mp_merge_ties_tau(L, base, exps, mask, tau_t, cfg["lam"], out, residency=res, io=io,
+                                        stream=stream, delta=dl)
         comb = mp.MP_COMBINE_SIGN_ELECT if cfg["combine"] == "sign_elect" else mp.MP_COMBINE_LINEAR
         return mp.mp_merge_dare(L, base, exps, mask, cfg["p"], cfg["seed"], comb, None, cfg["lam"], out,
                                 residency=res, io=io, stream=stream, delta=dl)
@@ -250,6 +256,8 @@ def run_sweep(args):
         ms = float(np.median([timed(merge)[0] for _ in range(reps)]))
         fid = fidelity(out, m_full, blen, st["n_selected"], K * G) if args.fidelity else None
         alg = 2 * P * es + st["cost_bytes"] + 4 * G if not host else st["cost_bytes"]
+        if op == "ties_tensor":  # three digit passes, each reading every selected unit's expert and base block
+            alg += 3 * st["cost_bytes"] * (1 if dl else 2)
         rows.append({"budget_frac": round(f, 4), "budget_bytes": B, "cost_bytes": st["cost_bytes"],
                      "h2d_bytes": io["h2d_bytes"], "n_selected": st["n_selected"], "plan_ms": round(plan_ms, 4),
                      "merge_ms": round(ms, 4), "merge_params_per_s": P / (ms * 1e-3),
@@ -267,6 +275,8 @@ def run_sweep(args):
         dma = n * es / (dma_ms * 1e-3)
         del dst, src
     tot_bytes = sum(r["cost_bytes"] if host else 2 * P * es + r["cost_bytes"] + 4 * G for r in rows)
+    if op == "ties_tensor":
+        tot_bytes += sum(3 * r["cost_bytes"] * (1 if dl else 2) for r in rows)
     tot_ms = sum(r["merge_ms"] for r in rows)
     achieved = tot_bytes / (tot_ms * 1e-3)
     peak = PCIE_PEAK if host else HBM_PEAK

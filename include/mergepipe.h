@@ -219,6 +219,22 @@ int mp_merge_ties(const mp_layout* layout, const void* base,
                   const uint32_t* mask, double density, float lambda, void* out,
                   mp_io_stats* io, void* stream);
 
+/* TIES trim thresholds at tensor scope (the per-tensor variant of
+ * Appendix A.1's trim after masking): for each unit (g, i),
+ * tau[g*K + i] = the k-th largest |d| pattern over the zero-completed
+ * masked deltas of expert i in block g's tensor t (unselected blocks count
+ * as zeros and are not read), k = min(n_t, ceil(density * n_t)) in fp64
+ * over the tensor's n_t elements; 0 when fewer than k elements of t are
+ * selected; all ones (nothing kept) when k = 0.  mp_merge_ties_tau with
+ * these thresholds is the tensor-scope TIES merge.  mask: device uint32[G]
+ * (the mask the merge will use); tau: device uint32[G*K].  Residency
+ * MP_DEVICE or MP_HOST_PINNED (MP_E_UNSUPPORTED for MP_HOST_PAGEABLE),
+ * optionally with MP_EXPERTS_DELTA.  Asynchronous on `stream`. */
+int mp_ties_tensor_thresholds(const mp_layout* layout, const void* base,
+                              const void* const* experts, int32_t K, int32_t residency,
+                              const uint32_t* mask, double density, uint32_t* tau,
+                              void* stream);
+
 /* Budgeted TIES with catalog thresholds: as mp_merge_ties, with d kept
  * iff |d| >= float(tau[g*K + i]) and |d| > 0 for the selected unit (g, i).
  * With the thresholds of mp_index_ties for a density the result equals

@@ -32,7 +32,8 @@ MP_EXPERTS_DELTA = 16  # OR-ed into residency: experts hold W_i - W_0
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
 MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 
-EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
+EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
+           "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
            "mp_merge_ties",
            "mp_merge_ties_tau", "mp_merge_dare", "mp_set_stage_bytes", "mp_last_error", "mp_release")
 
@@ -80,6 +81,7 @@ def _load():
                                C.POINTER(mp_io_stats), vp]
     L.mp_merge_avg_renorm.argtypes = L.mp_merge_avg.argtypes
     L.mp_coverage.argtypes = [lp, i32, vp, C.POINTER(C.c_uint64), vp]
+    L.mp_ties_tensor_thresholds.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, vp, vp]
     L.mp_merge_ties.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, C.c_float, vp,
                                 C.POINTER(mp_io_stats), vp]
     L.mp_merge_ties_tau.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, vp, C.c_float, vp,
@@ -91,7 +93,8 @@ def _load():
     L.mp_set_stage_bytes.restype = i32
     L.mp_last_error.argtypes = []
     L.mp_release.argtypes = []
-    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_plan", "mp_coverage", "mp_merge_avg",
+    for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
+                 "mp_coverage", "mp_merge_avg",
                  "mp_merge_avg_renorm", "mp_merge_ties",
                  "mp_merge_ties_tau",
                  "mp_merge_dare"):
@@ -192,6 +195,14 @@ def _res(residency: int, delta: bool) -> int:
 
 def _io(io):
     return C.byref(io) if io is not None else None
+
+
+def mp_ties_tensor_thresholds(layout: Layout, base, experts, mask, density: float, tau,
+                              residency: int = MP_DEVICE, stream=None, delta: bool = False):
+    """Per-unit TIES thresholds at tensor scope for this mask (device uint32 [G*K])."""
+    _check(lib.mp_ties_tensor_thresholds(layout.ref, _ptr(base), _ptrs(experts), len(experts),
+                                         _res(residency, delta), _ptr(mask), float(density), _ptr(tau),
+                                         _stream(stream)))
 
 
 def mp_coverage(layout: Layout, K: int, mask, stream=None):

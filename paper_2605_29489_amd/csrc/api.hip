@@ -49,6 +49,9 @@ struct DeviceWs {
     unsigned long long* h_counters = nullptr;  // pinned [256]
     unsigned long long* cov = nullptr;         // coverage counters, grown on demand
     int64_t cov_cap = 0;
+    uint32_t* tt_hist = nullptr;               // tensor-scope TIES: digit histograms per (expert, tensor)
+    uint4* tt_state = nullptr;                 //   and the select state per pair
+    int64_t tt_pairs = 0;
 };
 
 std::mutex g_mu;
@@ -64,6 +67,8 @@ void free_table(BlockTable& bt)
     (void)hipFree(bt.d_len);
     (void)hipFree(bt.d_tensor);
     (void)hipFree(bt.d_elem0);
+    (void)hipFree(bt.d_chunk);
+    (void)hipFree(bt.d_tnumel);
     (void)hipSetDevice(cur);
 }
 
@@ -79,6 +84,8 @@ void free_ws(int dev, DeviceWs& w)
     (void)hipFree(w.counters);
     (void)hipHostFree(w.h_counters);
     (void)hipFree(w.cov);
+    (void)hipFree(w.tt_hist);
+    (void)hipFree(w.tt_state);
     (void)hipSetDevice(cur);
 }
 
@@ -173,18 +180,33 @@ int get_table(const mp_layout* L, int esize, BlockTable** out)
     }
     bt->P = start;
     bt->n_distinct_len = (int)lens.size();
+    // runs of consecutive blocks of one tensor (the tensor-scope TIES passes)
+    std::vector<uint4> chunks;
+    std::vector<uint64_t> tnumel(L->numel, L->numel + L->n_tensors);
+    for (int64_t a = 0; a < G;) {
+        int64_t z = a + 1;
+        while (z < G && z - a < kChunkBlocks && tens[(size_t)z] == tens[(size_t)a])
+            ++z;
+        chunks.push_back(make_uint4((uint32_t)a, (uint32_t)z, tens[(size_t)a], 0u));
+        a = z;
+    }
+    bt->n_chunks = (int64_t)chunks.size();
     if (G > 0) {
         if ((e = hipMalloc((void**)&bt->d_off, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
             (e = hipMalloc((void**)&bt->d_len, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
             (e = hipMalloc((void**)&bt->d_tensor, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_elem0, sizeof(uint64_t) * (size_t)G)) != hipSuccess) {
+            (e = hipMalloc((void**)&bt->d_elem0, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
+            (e = hipMalloc((void**)&bt->d_chunk, sizeof(uint4) * chunks.size())) != hipSuccess ||
+            (e = hipMalloc((void**)&bt->d_tnumel, sizeof(uint64_t) * tnumel.size())) != hipSuccess) {
             free_table(*bt);
             return fail(MP_E_NOMEM, "block table allocation failed: %s", hipGetErrorString(e));
         }
         if ((e = hipMemcpy(bt->d_off, bt->h_off.data(), sizeof(uint64_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
             (e = hipMemcpy(bt->d_len, bt->h_len.data(), sizeof(uint32_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
             (e = hipMemcpy(bt->d_tensor, tens.data(), sizeof(uint32_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
-            (e = hipMemcpy(bt->d_elem0, e0.data(), sizeof(uint64_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess) {
+            (e = hipMemcpy(bt->d_elem0, e0.data(), sizeof(uint64_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
+            (e = hipMemcpy(bt->d_chunk, chunks.data(), sizeof(uint4) * chunks.size(), hipMemcpyHostToDevice)) != hipSuccess ||
+            (e = hipMemcpy(bt->d_tnumel, tnumel.data(), sizeof(uint64_t) * tnumel.size(), hipMemcpyHostToDevice)) != hipSuccess) {
             free_table(*bt);
             return hip_fail(e, "block table upload");
         }
@@ -588,6 +610,46 @@ int mp_coverage(const mp_layout* layout, int32_t K, const uint32_t* mask, uint64
         return hip_fail(e, "coverage readback");
     if ((e = hipStreamSynchronize(s)) != hipSuccess)
         return hip_fail(e, "hipStreamSynchronize");
+    return MP_OK;
+}
+
+int mp_ties_tensor_thresholds(const mp_layout* layout, const void* base, const void* const* experts, int32_t K,
+                              int32_t residency, const uint32_t* mask, double density, uint32_t* tau,
+                              void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    if (!(density >= 0.0 && density <= 1.0))
+        return fail(MP_E_ARG, "density %g must be in [0, 1]", density);
+    const bool delta = take_delta(&residency);
+    if (residency == MP_HOST_PAGEABLE)
+        return fail(MP_E_UNSUPPORTED, "tensor-scope thresholds need device or pinned experts");
+    Common c;
+    int rc = check_common(layout, base, experts, K, residency, nullptr, &c);
+    if (rc)
+        return rc;
+    const BlockTable& bt = *c.bt;
+    if ((rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)bt.G, "mask")))
+        return rc;
+    if ((rc = check_device_buffer(tau, sizeof(uint32_t) * (size_t)(bt.G * K), "tau")))
+        return rc;
+    const int64_t pairs = (int64_t)K * bt.n_tensors;
+    hipError_t e;
+    DeviceWs& ws = *c.ws;
+    if (pairs > ws.tt_pairs) {
+        (void)hipFree(ws.tt_hist);
+        (void)hipFree(ws.tt_state);
+        ws.tt_hist = nullptr;
+        ws.tt_state = nullptr;
+        ws.tt_pairs = 0;
+        if ((e = hipMalloc((void**)&ws.tt_hist, sizeof(uint32_t) * 2048 * (size_t)pairs)) != hipSuccess ||
+            (e = hipMalloc((void**)&ws.tt_state, sizeof(uint4) * (size_t)pairs)) != hipSuccess)
+            return fail(MP_E_NOMEM, "tensor-scope TIES buffers: %s", hipGetErrorString(e));
+        ws.tt_pairs = pairs;
+    }
+    if ((e = launch_ties_tensor(bt, base, c.ex, K, mask, density, tau, ws.tt_hist, ws.tt_state,
+                                static_cast<hipStream_t>(stream), delta)) != hipSuccess)
+        return hip_fail(e, "tensor-scope thresholds launch");
     return MP_OK;
 }
 

@@ -47,7 +47,13 @@ struct BlockTable {
     uint32_t* d_len = nullptr;     // elements in the block
     uint32_t* d_tensor = nullptr;  // tensor id
     uint64_t* d_elem0 = nullptr;   // index of the block's first element inside its tensor
+    // runs of at most kChunkBlocks consecutive blocks of one tensor: {g0, g1 (end), tensor, 0}
+    int64_t n_chunks = 0;
+    uint4* d_chunk = nullptr;
+    uint64_t* d_tnumel = nullptr;  // elements per tensor [n_tensors]
 };
+
+constexpr int kChunkBlocks = 16;
 
 // Device control block of the plan (see k_plan.hip).
 struct PlanCtl;
@@ -82,6 +88,13 @@ hipError_t launch_coverage(const BlockTable& bt, int K, const uint32_t* mask, un
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
                        const Coeffs& w, uint32_t flags, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
                        hipStream_t s);
+
+// TIES thresholds at tensor scope (k_tensor_ties.hip): per unit (g, i) the
+// k-th largest |d| of tensor(g)'s zero-completed masked deltas of expert i.
+// hist: device uint32[K * n_tensors * 2048], state: device uint4[K * n_tensors].
+hipError_t launch_ties_tensor(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
+                              const uint32_t* mask, double density, uint32_t* tau, uint32_t* hist, uint4* state,
+                              hipStream_t s, bool delta);
 
 // Merge operators.  `counters` is null or a device array of 256 uint64
 // accumulating the expert bytes the kernels load: slot (block mod 8) * 32 + i

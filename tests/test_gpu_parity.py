@@ -386,6 +386,71 @@ def test_manifest_coverage_realized_reads_and_replay(mp):
         assert not replay(bad, mp, L, K, sumsq, [0.25] * K, mask)["ok"]
 
 
+def _tensor_ties_case(mp, spec, base_np, exps_np, budgets, density, lam, residency=None, delta=False):
+    """Tensor-scope TIES: per-unit thresholds from mp_ties_tensor_thresholds
+    for each plan's mask, then the threshold merge; both against the oracle."""
+    import torch
+    L, lay = _lay(mp, spec)
+    K = len(exps_np)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    G = blocks.G
+    res = mp.MP_DEVICE if residency is None else residency
+    base = to_dev(base_np, lay.dtype)
+    exps = [to_pinned(e, lay.dtype) for e in exps_np] if res == mp.MP_HOST_PINNED else \
+        [to_dev(e, lay.dtype) for e in exps_np]
+    sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
+    mp.mp_index_blocks(L, base, exps, sumsq, residency=res, delta=delta)
+    mask = torch.empty(G, dtype=torch.int32, device="cuda")
+    tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(base)
+    full = int(blocks.len.sum()) * lay.elem_bytes * K
+    for f in budgets:
+        st = mp.mp_plan(L, K, sumsq, [1.0] * K, int(f * full), mask)
+        mp.mp_ties_tensor_thresholds(L, base, exps, mask, density, tau, residency=res, delta=delta)
+        m_np = mask.cpu().numpy().view(np.uint32)
+        t_orc = oracle.expand_tensor_thresholds(
+            blocks, oracle.ties_tensor_thresholds(blocks, lay.dtype, base_np, exps_np, m_np, density, delta=delta))
+        assert np.array_equal(tau.cpu().numpy().view(np.uint32), t_orc), f"thresholds differ at B={f}"
+        io = mp.mp_merge_ties_tau(L, base, exps, mask, tau, lam, out, residency=res, io=True, delta=delta)
+        want = oracle.merge_ties_tau(blocks, lay.dtype, base_np, exps_np, m_np, t_orc, lam, delta=delta)
+        nb = assert_merge_equal(to_host(out), want, base_np, lay.dtype, f"tensor TIES B={f}")
+        assert nb == 0
+        assert io["expert_bytes"] == st["cost_bytes"]
+        _say(f"  {spec.name} tensor TIES rho={density} B={f}: sel={st['n_selected']}")
+
+
+def test_ties_tensor_scope(mp):
+    # the per-tensor trim: every density edge, both dtypes, heavy tails
+    spec = _mini_qwen(n_layers=2)
+    base, exps = make_family(spec, seed=31)
+    for dens in (0.2, 0.05, 1.0, 0.0, 1.0 / 4096):
+        _say(f"case tensor-scope TIES mini-qwen bf16 rho={dens}")
+        _tensor_ties_case(mp, spec, base, exps, [0.0, 0.15, 0.5, 1.0], dens, 1.0)
+    spec = _ragged_f32(K=3)
+    base, exps = make_family(spec, seed=32)
+    _say("case tensor-scope TIES ragged fp32")
+    _tensor_ties_case(mp, spec, base, exps, [0.3, 1.0], 0.3, 0.8)
+    spec = _mini_qwen(n_layers=1, K=2)
+    P = sum(int(np.prod(s)) for _, s in spec.tensors)
+    rng = np.random.default_rng(33)
+    b0 = oracle.round_bf16(rng.normal(0.0, 0.02, P).astype(np.float32))
+    heavy = rng.normal(0.0, 1e-4, P)
+    out_idx = rng.random(P) < 0.01
+    heavy[out_idx] = rng.normal(0.0, 1.0, int(out_idx.sum()))
+    ex = _bf16_family_from_deltas(b0, [heavy, rng.normal(0.0, 1e-3, P)])
+    _say("case tensor-scope TIES heavy tails")
+    _tensor_ties_case(mp, spec, b0, ex, [0.4, 1.0], 0.1, 1.0)
+
+
+def test_ties_tensor_scope_deltas_and_pinned(mp):
+    spec = _mini_qwen(n_layers=1)
+    base, exps = make_family(spec, seed=34)
+    _say("case tensor-scope TIES explicit deltas")
+    _tensor_ties_case(mp, spec, base, _as_deltas(base, exps, "bf16"), [0.3, 1.0], 0.2, 1.0, delta=True)
+    _say("case tensor-scope TIES pinned experts")
+    _tensor_ties_case(mp, spec, base, exps, [0.3, 1.0], 0.2, 1.0, residency=mp.MP_HOST_PINNED)
+
+
 def test_avg_renorm_coefficients(mp):
     # Selected-only AVG with unequal, non-dyadic coefficients (the quotients
     # alpha_i / s are inexact) and a zero coefficient: blocks whose only
