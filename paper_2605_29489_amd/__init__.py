@@ -26,8 +26,9 @@ MP_E_ARG = -1
 MP_E_UNSUPPORTED = -2
 MP_E_NOMEM = -3
 MP_E_HIP = -4
+MP_E_IO = -5
 MP_F32, MP_BF16 = 0, 1
-MP_DEVICE, MP_HOST_PINNED, MP_HOST_PAGEABLE = 0, 1, 2
+MP_DEVICE, MP_HOST_PINNED, MP_HOST_PAGEABLE, MP_HOST_FILE = 0, 1, 2, 3
 MP_EXPERTS_DELTA = 16  # OR-ed into residency: experts hold W_i - W_0
 MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
 MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
@@ -70,6 +71,13 @@ class MPError(RuntimeError):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+    # Buffers come from torch, which ships its own HIP runtime.  Load that one
+    # first, so this library binds to the same runtime: loaded the other way
+    # round, the library's runtime does not know torch's allocations.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     L = C.CDLL(LIB_PATH)
     vp, i32, u32, u64 = C.c_void_p, C.c_int32, C.c_uint32, C.c_uint64
     lp = C.POINTER(mp_layout)
@@ -141,7 +149,19 @@ def _ptr(t) -> int:
 
 
 def _ptrs(ts):
-    return (C.c_void_p * max(len(ts), 1))(*[_ptr(t) for t in ts])
+    """Array of expert pointers: tensors by address, file paths (MP_HOST_FILE)
+    as NUL-terminated strings kept alive with the array."""
+    keep, vals = [], []
+    for t in ts:
+        if isinstance(t, (str, bytes, os.PathLike)):
+            b = C.create_string_buffer(os.fsencode(t))
+            keep.append(b)
+            vals.append(C.addressof(b))
+        else:
+            vals.append(_ptr(t))
+    arr = (C.c_void_p * max(len(ts), 1))(*vals)
+    arr._keep = keep
+    return arr
 
 
 def _floats(xs, K):
