@@ -67,9 +67,10 @@ extern "C" {
 #define MP_E_UNSUPPORTED (-2) /* valid request this build does not handle */
 #define MP_E_NOMEM (-3)       /* workspace allocation failed */
 #define MP_E_HIP (-4)         /* a HIP runtime call failed */
+#define MP_E_IO (-5)          /* reading an expert file failed */
 
 typedef enum { MP_F32 = 0, MP_BF16 = 1 } mp_dtype;
-typedef enum { MP_DEVICE = 0, MP_HOST_PINNED = 1, MP_HOST_PAGEABLE = 2 } mp_residency;
+typedef enum { MP_DEVICE = 0, MP_HOST_PINNED = 1, MP_HOST_PAGEABLE = 2, MP_HOST_FILE = 3 } mp_residency;
 /* OR-ed into `residency`: the expert buffers hold the deltas
  * Delta_i = W_i - W_0 themselves (Section 3's "explicit deltas" source)
  * instead of fine-tuned weights, in the checkpoint dtype.  Then

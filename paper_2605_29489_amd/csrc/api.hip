@@ -4,7 +4,12 @@
 // kernels; this file only checks, allocates, copies tables and enqueues.
 #include <hip/hip_runtime.h>
 
+#include <fcntl.h>
+#include <sys/stat.h>
+#include <unistd.h>
+
 #include <algorithm>
+#include <cerrno>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -367,7 +372,25 @@ struct Common {
     DeviceWs* ws = nullptr;
     ExpertPtrs ex{};
     size_t ckpt_bytes = 0;
+    std::vector<int> fds;  // MP_HOST_FILE: the opened expert files (closed with the call)
+    ~Common()
+    {
+        for (int fd : fds)
+            if (fd >= 0)
+                (void)close(fd);
+    }
 };
+
+// The experts of a staged call (MP_HOST_PAGEABLE memory or MP_HOST_FILE files).
+void host_experts(const Common& c, const void* const* experts, HostExperts* hx)
+{
+    if (c.fds.empty())
+        hx->ptr = experts;
+    else
+        hx->fd = c.fds.data();
+}
+
+bool staged(int32_t residency) { return residency == MP_HOST_PAGEABLE || residency == MP_HOST_FILE; }
 
 // Validates the arguments every data entry point shares and resolves the
 // block table / workspace.  `out` may be NULL (index).
@@ -379,8 +402,10 @@ int check_common(const mp_layout* L, const void* base, const void* const* expert
         return rc;
     if (K < 1 || K > kMaxK)
         return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
-    if (residency != MP_DEVICE && residency != MP_HOST_PINNED && residency != MP_HOST_PAGEABLE)
-        return fail(MP_E_ARG, "residency %d is not MP_DEVICE, MP_HOST_PINNED or MP_HOST_PAGEABLE", residency);
+    if (residency != MP_DEVICE && residency != MP_HOST_PINNED && residency != MP_HOST_PAGEABLE &&
+        residency != MP_HOST_FILE)
+        return fail(MP_E_ARG, "residency %d is not MP_DEVICE, MP_HOST_PINNED, MP_HOST_PAGEABLE or MP_HOST_FILE",
+                    residency);
     const int64_t G = count_blocks(L);
     if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
         return fail(MP_E_ARG, "K * G = %lld does not fit 32-bit unit ids", (long long)(G * K));
@@ -398,6 +423,21 @@ int check_common(const mp_layout* L, const void* base, const void* const* expert
         char nm[32];
         std::snprintf(nm, sizeof nm, "experts[%d]", i);
         const void* dev = experts[i];
+        if (residency == MP_HOST_FILE) {  // experts[i] is the path of a file holding the checkpoint
+            if (experts[i] == nullptr)
+                return fail(MP_E_ARG, "%s: path is NULL", nm);
+            const char* path = static_cast<const char*>(experts[i]);
+            const int fd = open(path, O_RDONLY | O_CLOEXEC);
+            if (fd < 0)
+                return fail(MP_E_IO, "%s: cannot open %s: %s", nm, path, std::strerror(errno));
+            c->fds.push_back(fd);
+            struct stat sb;
+            if (fstat(fd, &sb) != 0 || (uint64_t)sb.st_size < (uint64_t)c->ckpt_bytes)
+                return fail(MP_E_ARG, "%s: %s holds fewer than the checkpoint's %zu bytes", nm, path,
+                            c->ckpt_bytes);
+            c->ex.p[i] = nullptr;
+            continue;
+        }
         if (residency == MP_DEVICE)
             rc = check_device_buffer(experts[i], c->ckpt_bytes, nm);
         else if (residency == MP_HOST_PINNED)
@@ -466,9 +506,14 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
             return hip_fail(e, "counter reset");
     }
     mp_io_stats st{};
-    uint64_t staged = 0;
-    if (residency == MP_HOST_PAGEABLE) {
-        if ((e = stage_merge(bt, a, base, experts, K, mask, out, ctr, s, &staged)) != hipSuccess)
+    uint64_t staged_bytes = 0;
+    if (staged(residency)) {
+        HostExperts hx;
+        host_experts(c, experts, &hx);
+        e = stage_merge(bt, a, base, hx, K, mask, out, ctr, s, &staged_bytes);
+        if (hx.failed.load())
+            return fail(MP_E_IO, "reading an expert file failed");
+        if (e != hipSuccess)
             return hip_fail(e, "staged merge");
     } else if ((e = launch_merge(bt, a, base, c.ex, K, mask, out, ctr, s)) != hipSuccess) {
         return hip_fail(e, "merge launch");
@@ -487,8 +532,8 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
         st.expert_bytes = sum;
         if (residency == MP_HOST_PINNED)
             st.h2d_bytes = sum;  // expert blocks are read over PCIe, nothing else crosses it
-        else if (residency == MP_HOST_PAGEABLE)
-            st.h2d_bytes = staged;  // the packed selected blocks
+        else if (staged(residency))
+            st.h2d_bytes = staged_bytes;  // the packed selected blocks
         st.base_bytes = (uint64_t)bt.P * (uint64_t)bt.esize;
         st.out_bytes = st.base_bytes;
         *io = st;
@@ -531,9 +576,13 @@ int mp_index_blocks(const mp_layout* layout, const void* base, const void* const
         return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
-    if (residency == MP_HOST_PAGEABLE) {
-        uint64_t staged = 0;
-        e = stage_index(bt, base, experts, K, false, 0.0, sumsq, nullptr, s, &staged, delta);
+    if (staged(residency)) {
+        uint64_t staged_bytes = 0;
+        HostExperts hx;
+        host_experts(c, experts, &hx);
+        e = stage_index(bt, base, hx, K, false, 0.0, sumsq, nullptr, s, &staged_bytes, delta);
+        if (hx.failed.load())
+            return fail(MP_E_IO, "reading an expert file failed");
     } else {
         e = launch_index(bt, base, c.ex, K, sumsq, s, delta);
     }
@@ -563,9 +612,13 @@ int mp_index_ties(const mp_layout* layout, const void* base, const void* const* 
         return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
-    if (residency == MP_HOST_PAGEABLE) {
-        uint64_t staged = 0;
-        e = stage_index(bt, base, experts, K, true, density, sumsq, tau, s, &staged, delta);
+    if (staged(residency)) {
+        uint64_t staged_bytes = 0;
+        HostExperts hx;
+        host_experts(c, experts, &hx);
+        e = stage_index(bt, base, hx, K, true, density, sumsq, tau, s, &staged_bytes, delta);
+        if (hx.failed.load())
+            return fail(MP_E_IO, "reading an expert file failed");
     } else {
         e = launch_index_ties(bt, base, c.ex, K, density, sumsq, tau, s, delta);
     }
@@ -622,7 +675,7 @@ int mp_ties_tensor_thresholds(const mp_layout* layout, const void* base, const v
     if (!(density >= 0.0 && density <= 1.0))
         return fail(MP_E_ARG, "density %g must be in [0, 1]", density);
     const bool delta = take_delta(&residency);
-    if (residency == MP_HOST_PAGEABLE)
+    if (staged(residency))
         return fail(MP_E_UNSUPPORTED, "tensor-scope thresholds need device or pinned experts");
     Common c;
     int rc = check_common(layout, base, experts, K, residency, nullptr, &c);

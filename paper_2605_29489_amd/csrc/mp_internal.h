@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -124,16 +125,26 @@ hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const v
                                const void* stage, const uint64_t* soff, int64_t b0, int64_t nb);
 
 // ---------------------------------------------------------------- host experts (stage.hip)
+// Expert checkpoints on the host: memory (ptr[i]) or files (fd[i], read
+// with pread).  read() copies bytes [pos, pos + n) of expert i; a failed
+// file read sets `failed` and returns false.
+struct HostExperts {
+    const void* const* ptr = nullptr;
+    const int* fd = nullptr;
+    mutable std::atomic<int> failed{0};
+    bool read(int i, void* dst, size_t pos, size_t n) const;
+};
+
 // Experts in host memory of any kind, streamed through pinned staging
 // buffers; h2d receives the bytes copied to the device.  The functions
 // return once every chunk is enqueued on `s` (the experts are no longer
 // read); staging buffers are reused by the next call after its kernels.
 void set_stage_bytes(size_t bytes);
 void release_stagers();
-hipError_t stage_index(const BlockTable& bt, const void* base, const void* const* experts, int K, bool ties,
+hipError_t stage_index(const BlockTable& bt, const void* base, const HostExperts& experts, int K, bool ties,
                        double density, float* sumsq, uint32_t* tau, hipStream_t s, uint64_t* h2d,
                        bool delta = false);
-hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* base, const void* const* experts,
+hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* base, const HostExperts& experts,
                        int K, const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s,
                        uint64_t* h2d);
 

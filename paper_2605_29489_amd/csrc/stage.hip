@@ -10,7 +10,10 @@
 // the staged blocks are computed on the device from the mask.
 #include <hip/hip_runtime.h>
 
+#include <unistd.h>
+
 #include <algorithm>
+#include <cerrno>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -190,7 +193,29 @@ void release_stagers()
     g_stagers.clear();
 }
 
-hipError_t stage_index(const BlockTable& bt, const void* base, const void* const* experts, int K, bool ties,
+bool HostExperts::read(int i, void* dst, size_t pos, size_t n) const
+{
+    if (fd == nullptr) {
+        std::memcpy(dst, static_cast<const char*>(ptr[i]) + pos, n);
+        return true;
+    }
+    char* p = static_cast<char*>(dst);
+    while (n > 0) {
+        const ssize_t r = pread(fd[i], p, n, (off_t)pos);
+        if (r < 0 && errno == EINTR)
+            continue;
+        if (r <= 0) {
+            failed.store(1);
+            return false;
+        }
+        p += r;
+        pos += (size_t)r;
+        n -= (size_t)r;
+    }
+    return true;
+}
+
+hipError_t stage_index(const BlockTable& bt, const void* base, const HostExperts& experts, int K, bool ties,
                        double density, float* sumsq, uint32_t* tau, hipStream_t s, uint64_t* h2d, bool delta)
 {
     *h2d = 0;
@@ -221,10 +246,11 @@ hipError_t stage_index(const BlockTable& bt, const void* base, const void* const
             for (int64_t w = lo; w < hi; ++w) {
                 const int i = (int)(w / 16), part = (int)(w % 16);
                 const size_t a = chunk * part / 16, z = chunk * (part + 1) / 16;
-                std::memcpy(st->h[k] + (size_t)i * chunk + a,
-                            static_cast<const char*>(experts[i]) + e0 * es + a, z - a);
+                experts.read(i, st->h[k] + (size_t)i * chunk + a, e0 * es + a, z - a);
             }
         });
+        if (experts.failed.load())
+            return hipErrorInvalidValue;
         const size_t bytes = chunk * (size_t)K;
         if ((e = hipMemcpyAsync(st->d[k], st->h[k], bytes, hipMemcpyHostToDevice, st->side)) != hipSuccess ||
             (e = hipEventRecord(st->copied[k], st->side)) != hipSuccess ||
@@ -245,7 +271,7 @@ hipError_t stage_index(const BlockTable& bt, const void* base, const void* const
     return hipSuccess;
 }
 
-hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* base, const void* const* experts,
+hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* base, const HostExperts& experts,
                        int K, const uint32_t* mask, void* out, unsigned long long* ctr, hipStream_t s,
                        uint64_t* h2d)
 {
@@ -296,12 +322,13 @@ hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* bas
                     while (m) {
                         const int i = __builtin_ctz(m);
                         m &= m - 1u;
-                        std::memcpy(st->h[k] + dst, static_cast<const char*>(experts[i]) + bt.h_off[(size_t)gg] * es,
-                                    n);
+                        experts.read(i, st->h[k] + dst, bt.h_off[(size_t)gg] * es, n);
                         dst += n;
                     }
                 }
             });
+            if (experts.failed.load())
+                return hipErrorInvalidValue;
             if ((e = hipMemcpyAsync(st->d[k], st->h[k], bytes, hipMemcpyHostToDevice, st->side)) != hipSuccess ||
                 (e = hipEventRecord(st->copied[k], st->side)) != hipSuccess)
                 return e;

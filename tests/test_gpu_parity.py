@@ -10,6 +10,7 @@ selected blocks).
 """
 
 import math
+import os
 import sys
 
 import numpy as np
@@ -59,6 +60,18 @@ def _ragged_f32(K=3):
     return FamilySpec("ragged-f32", t, "f32", 4096, K, ())
 
 
+def _expert_files(exps_np):
+    """Writes each expert checkpoint to a file of its own; returns the paths."""
+    import tempfile
+    d = tempfile.mkdtemp(prefix="mp_experts_")
+    paths = []
+    for i, e in enumerate(exps_np):
+        p = os.path.join(d, f"expert{i}.bin")
+        np.ascontiguousarray(e).tofile(p)
+        paths.append(p)
+    return paths
+
+
 def _lay(mp, spec):
     lay = spec.layout
     return mp.Layout(lay.numel, lay.block_elems, lay.dtype_code), lay
@@ -80,6 +93,8 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, de
         exps = [to_pinned(e, dtype) for e in exps_np]
     elif res == mp.MP_HOST_PAGEABLE:  # ordinary host memory (the numpy arrays themselves)
         exps = [torch.from_numpy(e) for e in exps_np]
+    elif res == mp.MP_HOST_FILE:  # files holding the flat checkpoints
+        exps = _expert_files(exps_np)
     else:
         exps = [to_dev(e, dtype) for e in exps_np]
     sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
@@ -144,7 +159,7 @@ def _run_all(mp, spec, base_np, exps_np, op, budgets, w=None, residency=None, de
         assert io["expert_bytes"] == read, "kernels loaded bytes outside the plan"
         if res == mp.MP_HOST_PINNED:  # only those blocks cross PCIe
             assert io["h2d_bytes"] == read
-        elif res == mp.MP_HOST_PAGEABLE:  # the staged copies are exactly the selected blocks
+        elif res in (mp.MP_HOST_PAGEABLE, mp.MP_HOST_FILE):  # the staged copies are exactly the selected blocks
             assert io["h2d_bytes"] == st["cost_bytes"]
         else:
             assert io["h2d_bytes"] == 0
@@ -229,6 +244,46 @@ def test_host_pageable_experts_all_ops(mp, op):
     kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0, p=0.9, seed=7)
     _say(f"case mini-qwen bf16 {op}, pageable host experts")
     _run_all(mp, spec, base, exps, op, [0, 0.3, 1.0], residency=mp.MP_HOST_PAGEABLE, **kw)
+
+
+@pytest.mark.parametrize("op", ["avg", "avg_renorm", "ties", "ties_tau", "dare_lin", "dare_sign"])
+def test_host_file_experts_all_ops(mp, op):
+    # experts in files (the paper's disk-resident regime): the selected
+    # blocks are read with pread into pinned staging and merged from the
+    # staged copy; same bits as device-resident experts, staged bytes == cost
+    spec = _mini_qwen()
+    base, exps = make_family(spec, seed=1)
+    kw = dict(alpha=[0.25] * 4, density=0.2, lam=1.0, p=0.9, seed=7)
+    _say(f"case mini-qwen bf16 {op}, expert files")
+    _run_all(mp, spec, base, exps, op, [0, 0.3, 1.0], residency=mp.MP_HOST_FILE, **kw)
+
+
+def test_host_file_experts_small_staging_deltas_and_errors(mp):
+    import torch
+    mp.mp_set_stage_bytes(1 << 20)
+    try:
+        spec = _ragged_f32(K=3)
+        base, exps = make_family(spec, seed=22)
+        _say("case ragged fp32 expert files, 1 MiB staging, explicit deltas")
+        _run_all(mp, spec, base, _as_deltas(base, exps, "f32"), "ties_tau", [0.2, 1.0], residency=mp.MP_HOST_FILE,
+                 delta=True, density=0.3, lam=1.0)
+    finally:
+        mp.mp_set_stage_bytes(256 << 20)
+    spec = _mini_qwen(n_layers=1)
+    base_np, exps_np = make_family(spec, seed=23)
+    L, lay = _lay(mp, spec)
+    base = to_dev(base_np, lay.dtype)
+    G = mp.mp_layout_blocks(L)
+    sumsq = torch.empty(G * len(exps_np), dtype=torch.float32, device="cuda")
+    paths = _expert_files(exps_np)
+    with pytest.raises(mp.MPError) as e:
+        mp.mp_index_blocks(L, base, paths[:-1] + [paths[-1] + ".missing"], sumsq, residency=mp.MP_HOST_FILE)
+    assert e.value.code == mp.MP_E_IO
+    with open(paths[0], "r+b") as f:  # one byte short of a checkpoint
+        f.truncate(os.path.getsize(paths[0]) - 1)
+    with pytest.raises(mp.MPError) as e:
+        mp.mp_index_blocks(L, base, paths, sumsq, residency=mp.MP_HOST_FILE)
+    assert e.value.code == mp.MP_E_ARG
 
 
 def test_host_pageable_small_staging_many_chunks(mp):
