@@ -156,6 +156,37 @@ def fidelity(out, m_full, blen, n_sel, n_units):
     return {"rel_l2": rel, "p95_block": p95, "touched": n_sel / n_units}
 
 
+def write_expert_files(exps, P):
+    """Writes each (device) expert to a file under $MP_BENCH_DIR (default /tmp),
+    frees the device copies, and returns the paths with a function that asks
+    the kernel to drop the files from the page cache, so that reads come from
+    storage."""
+    import tempfile
+    import torch
+    d = tempfile.mkdtemp(prefix="mp_experts_", dir=os.environ.get("MP_BENCH_DIR", "/tmp"))
+    paths = []
+    for i in range(len(exps)):
+        p = os.path.join(d, f"expert{i}.bin")
+        with open(p, "wb") as f:
+            for c0 in range(0, P, 1 << 27):
+                f.write(exps[i][c0:c0 + (1 << 27)].view(torch.int16 if exps[i].dtype == torch.bfloat16
+                                                       else torch.int32).cpu().numpy().tobytes())
+            f.flush()
+            os.fsync(f.fileno())
+        exps[i] = None
+        paths.append(p)
+        log(f"wrote {p}")
+    torch.cuda.empty_cache()
+
+    def drop():
+        for p in paths:
+            fd = os.open(p, os.O_RDONLY)
+            os.posix_fadvise(fd, 0, 0, os.POSIX_FADV_DONTNEED)
+            os.close(fd)
+
+    return paths, drop
+
+
 def run_sweep(args):
     """One of the other workload shapes: index once, then plan + merge at each
     budget of its sweep.  Experts are device-resident, stay in pinned host
@@ -174,27 +205,33 @@ def run_sweep(args):
     K = spec.K
     P = lay.n_params
     where = {"config": cfg["residency"], "device": "device", "pinned": "host_pinned",
-             "pageable": "host_pageable"}[args.residency]
+             "pageable": "host_pageable", "file": "host_file"}[args.residency]
     pinned = where == "host_pinned"
     pageable = where == "host_pageable"
-    host = pinned or pageable  # experts cross PCIe: that link bounds the merge
-    res = mp.MP_HOST_PINNED if pinned else (mp.MP_HOST_PAGEABLE if pageable else mp.MP_DEVICE)
+    files = where == "host_file"
+    host = pinned or pageable or files  # experts cross PCIe: that link (or the storage) bounds the merge
+    res = mp.MP_HOST_PINNED if pinned else (mp.MP_HOST_PAGEABLE if pageable else
+                                            (mp.MP_HOST_FILE if files else mp.MP_DEVICE))
     dt = mp.MP_F32 if lay.dtype == "f32" else mp.MP_BF16
     L = mp.Layout(lay.numel, lay.block_elems, dt)
     G = mp.mp_layout_blocks(L)
-    where_txt = {"host_pinned": "pinned host", "host_pageable": "pageable host"}.get(where, "device")
+    where_txt = {"host_pinned": "pinned host", "host_pageable": "pageable host",
+                 "host_file": "files"}.get(where, "device")
     log(f"generating {spec.description}: P={P} G={G} experts {where_txt}")
     base, exps = make_family_device(spec, K=K, seed=0, device="cuda",
                                     experts_on_host="pinned" if pinned else ("pageable" if pageable else None))
     dl = bool(args.experts_delta)
     if dl:  # the experts as stored deltas fl32(W_i - W_0) in the checkpoint dtype (set-up, not timed)
-        if host:
-            sys.exit("bench.py: --experts-delta supports device-resident experts only")
+        if pinned or pageable:
+            sys.exit("bench.py: --experts-delta supports device-resident experts or files only")
         for e in exps:
             for c0 in range(0, P, 1 << 28):
                 c1 = min(P, c0 + (1 << 28))
                 e[c0:c1] = (e[c0:c1].float() - base[c0:c1].float()).to(e.dtype)
     torch.cuda.synchronize()
+    drop = None
+    if files:  # one file per expert (set-up); the page cache is dropped before every timed call
+        exps, drop = write_expert_files(exps, P)
     sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
     mask = torch.empty(G, dtype=torch.int32, device="cuda")
     out = torch.empty_like(base)
@@ -225,6 +262,8 @@ def run_sweep(args):
                                 residency=res, io=io, stream=stream, delta=dl)
 
     def timed(fn):
+        if drop is not None:
+            drop()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
         r = fn()
@@ -266,7 +305,22 @@ def run_sweep(args):
             rows[-1]["fidelity"] = fid
     step_ms = idx_ms + sum(r["plan_ms"] + r["merge_ms"] for r in rows)
     dma = None
-    if host:  # measured peak: pinned host -> device with the copy engine (1 GiB, or one expert)
+    fread = None
+    if files:  # measured peak: sequential read of one expert file (up to 1 GiB) after a cache drop
+        import time
+        drop()
+        n = min(P * es, 1 << 30)
+        buf = bytearray(64 << 20)
+        t0 = time.perf_counter()
+        with open(exps[0], "rb", buffering=0) as f:
+            got = 0
+            while got < n:
+                r = f.readinto(buf)
+                if not r:
+                    break
+                got += r
+        fread = got / (time.perf_counter() - t0)
+    if pinned or pageable:  # measured peak: pinned host -> device with the copy engine (1 GiB, or one expert)
         n = P if pinned else min(P, (1 << 30) // es)
         src = exps[0] if pinned else exps[0][:n].pin_memory()
         dst = torch.empty(n, dtype=base.dtype, device=base.device)
@@ -280,6 +334,8 @@ def run_sweep(args):
     tot_ms = sum(r["merge_ms"] for r in rows)
     achieved = tot_bytes / (tot_ms * 1e-3)
     peak = PCIE_PEAK if host else HBM_PEAK
+    if files and fread:  # storage bounds it: the measured sequential read rate is the peak
+        peak = fread
     result = {
         "metric": f"merged params/sec, budgeted {op.upper()} merge sweep",
         "value": len(rows) * P / (step_ms * 1e-3), "unit": "params/s", "n_gpus": 1, "steps": reps,
@@ -290,9 +346,11 @@ def run_sweep(args):
                    "storage_dtype": lay.dtype, "params": P,
                    "blocks": G, "K": K, "experts": where_txt,
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "pcie" if host else "hbm", "achieved": achieved / 1e9, "peak": peak / 1e9,
+        "roofline": {"bound": "storage" if files else ("pcie" if host else "hbm"), "achieved": achieved / 1e9,
+                     "peak": peak / 1e9,
                      "unit": "GB/s", "frac": achieved / peak, "traffic": None,
-                     "measured_dma_h2d_GBps": None if dma is None else dma / 1e9},
+                     "measured_dma_h2d_GBps": None if dma is None else dma / 1e9,
+                     "measured_file_read_GBps": None if fread is None else fread / 1e9},
         "breakdown": {"index_ms": round(idx_ms, 4), "per_budget": rows},
     }
     print(json.dumps(result), flush=True)
@@ -309,7 +367,7 @@ def main():
                     help="the headline (default) or one of the other workload shapes")
     ap.add_argument("--layers", type=int, default=None,
                     help="other workloads: keep only this many transformer layers (host memory)")
-    ap.add_argument("--residency", default="config", choices=("config", "device", "pinned", "pageable"),
+    ap.add_argument("--residency", default="config", choices=("config", "device", "pinned", "pageable", "file"),
                     help="other workloads: where the experts live (default: the workload's own)")
     ap.add_argument("--ties", default="catalog", choices=("catalog", "in-merge"),
                     help="where the TIES trim thresholds are found: in the index pass (catalog) or in each merge")

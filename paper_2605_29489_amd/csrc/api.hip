@@ -431,6 +431,8 @@ int check_common(const mp_layout* L, const void* base, const void* const* expert
             if (fd < 0)
                 return fail(MP_E_IO, "%s: cannot open %s: %s", nm, path, std::strerror(errno));
             c->fds.push_back(fd);
+            // only the selected blocks may be read (Prop. 1): no readahead of their neighbours
+            (void)posix_fadvise(fd, 0, 0, POSIX_FADV_RANDOM);
             struct stat sb;
             if (fstat(fd, &sb) != 0 || (uint64_t)sb.st_size < (uint64_t)c->ckpt_bytes)
                 return fail(MP_E_ARG, "%s: %s holds fewer than the checkpoint's %zu bytes", nm, path,

@@ -10,6 +10,7 @@
 // the staged blocks are computed on the device from the mask.
 #include <hip/hip_runtime.h>
 
+#include <sys/uio.h>
 #include <unistd.h>
 
 #include <algorithm>
@@ -146,12 +147,14 @@ hipError_t get_stager(Stager** out)
     return hipSuccess;
 }
 
-// Runs fn(lo, hi) over [0, n) split into contiguous parts on host threads.
+// Runs fn(lo, hi) over [0, n) split into contiguous parts on host threads:
+// up to 16 for copies from memory; for file reads (blocking I/O) up to 64,
+// which keeps that many reads in flight.
 template <class Fn>
-void parallel_for(int64_t n, Fn fn)
+void parallel_for(int64_t n, Fn fn, bool io = false)
 {
-    const int T = (int)std::max<int64_t>(1, std::min<int64_t>(
-        {(int64_t)std::max(1u, std::thread::hardware_concurrency()), (int64_t)16, n}));
+    const int64_t cpu = io ? 64 : std::min<int64_t>(16, std::max(1u, std::thread::hardware_concurrency()));
+    const int T = (int)std::max<int64_t>(1, std::min<int64_t>(cpu, n));
     if (T <= 1) {
         fn((int64_t)0, n);
         return;
@@ -215,6 +218,34 @@ bool HostExperts::read(int i, void* dst, size_t pos, size_t n) const
     return true;
 }
 
+namespace {
+// Reads the contiguous file range [pos, pos + sum of lengths) of fd into
+// the buffers of iov (a run of consecutive selected blocks of one expert,
+// each landing at its staging slot); false on an error or end of file.
+bool read_run(int fd, struct iovec* iov, int cnt, size_t pos)
+{
+    while (cnt > 0) {
+        const ssize_t r = preadv(fd, iov, std::min(cnt, IOV_MAX), (off_t)pos);
+        if (r < 0 && errno == EINTR)
+            continue;
+        if (r <= 0)
+            return false;
+        pos += (size_t)r;
+        size_t left = (size_t)r;
+        while (cnt > 0 && left >= iov->iov_len) {  // drop the filled buffers
+            left -= iov->iov_len;
+            ++iov;
+            --cnt;
+        }
+        if (cnt > 0 && left > 0) {  // a partly filled buffer
+            iov->iov_base = static_cast<char*>(iov->iov_base) + left;
+            iov->iov_len -= left;
+        }
+    }
+    return true;
+}
+}  // namespace
+
 hipError_t stage_index(const BlockTable& bt, const void* base, const HostExperts& experts, int K, bool ties,
                        double density, float* sumsq, uint32_t* tau, hipStream_t s, uint64_t* h2d, bool delta)
 {
@@ -248,7 +279,7 @@ hipError_t stage_index(const BlockTable& bt, const void* base, const HostExperts
                 const size_t a = chunk * part / 16, z = chunk * (part + 1) / 16;
                 experts.read(i, st->h[k] + (size_t)i * chunk + a, e0 * es + a, z - a);
             }
-        });
+        }, experts.fd != nullptr);
         if (experts.failed.load())
             return hipErrorInvalidValue;
         const size_t bytes = chunk * (size_t)K;
@@ -313,20 +344,57 @@ hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* bas
                 off[(size_t)b] = run;
                 run += size_of(b0 + b);
             }
-            parallel_for(nb, [&](int64_t lo, int64_t hi) {
-                for (int64_t b = lo; b < hi; ++b) {
-                    const int64_t gg = b0 + b;
-                    const size_t n = (size_t)bt.h_len[(size_t)gg] * es;
-                    uint32_t m = hm[(size_t)gg] & kmask;
-                    size_t dst = off[(size_t)b];
-                    while (m) {
-                        const int i = __builtin_ctz(m);
-                        m &= m - 1u;
-                        experts.read(i, st->h[k] + dst, bt.h_off[(size_t)gg] * es, n);
-                        dst += n;
+            if (experts.fd == nullptr) {  // memory: one copy per selected block
+                parallel_for(nb, [&](int64_t lo, int64_t hi) {
+                    for (int64_t b = lo; b < hi; ++b) {
+                        const int64_t gg = b0 + b;
+                        const size_t n = (size_t)bt.h_len[(size_t)gg] * es;
+                        uint32_t m = hm[(size_t)gg] & kmask;
+                        size_t dst = off[(size_t)b];
+                        while (m) {
+                            const int i = __builtin_ctz(m);
+                            m &= m - 1u;
+                            experts.read(i, st->h[k] + dst, bt.h_off[(size_t)gg] * es, n);
+                            dst += n;
+                        }
+                    }
+                });
+            } else {  // files: one vectored read per run of consecutive selected blocks of an expert
+                struct Run {
+                    int i;
+                    int64_t b, e;  // blocks [b, e) of the chunk
+                };
+                std::vector<Run> runs;
+                for (int i = 0; i < K; ++i) {
+                    int64_t b = 0;
+                    while (b < nb) {
+                        while (b < nb && !((hm[(size_t)(b0 + b)] >> i) & 1u))
+                            ++b;
+                        const int64_t rb = b;
+                        while (b < nb && ((hm[(size_t)(b0 + b)] >> i) & 1u))
+                            ++b;
+                        if (b > rb)
+                            runs.push_back({i, rb, b});
                     }
                 }
-            });
+                parallel_for((int64_t)runs.size(), [&](int64_t lo, int64_t hi) {
+                    std::vector<struct iovec> iov;
+                    for (int64_t q = lo; q < hi; ++q) {
+                        const Run& r = runs[(size_t)q];
+                        iov.clear();
+                        for (int64_t b = r.b; b < r.e; ++b) {
+                            const int64_t gg = b0 + b;
+                            const size_t n = (size_t)bt.h_len[(size_t)gg] * es;
+                            // the expert's slot: after the block's lower selected experts
+                            const uint32_t below = hm[(size_t)gg] & kmask & ((1u << r.i) - 1u);
+                            iov.push_back({st->h[k] + off[(size_t)b] + (size_t)__builtin_popcount(below) * n, n});
+                        }
+                        if (!read_run(experts.fd[r.i], iov.data(), (int)iov.size(),
+                                      bt.h_off[(size_t)(b0 + r.b)] * es))
+                            experts.failed.store(1);
+                    }
+                }, true);
+            }
             if (experts.failed.load())
                 return hipErrorInvalidValue;
             if ((e = hipMemcpyAsync(st->d[k], st->h[k], bytes, hipMemcpyHostToDevice, st->side)) != hipSuccess ||
