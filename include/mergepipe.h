@@ -166,6 +166,9 @@ int mp_index_ties(const mp_layout* layout, const void* base,
  *   mix64((g << 32) | mask[g]) mod 2^64 and mix64 the SplitMix64 output
  *   function.  B >= full_bytes yields the all-ones mask.
  * Synchronises `stream` before returning (the one blocking point). */
+/* sumsq may be NULL when no block catalog exists: the planner then falls back
+ * (Section 3) to a deterministic order, every unit's statistic being 1 --
+ * units by w_i^2, ties by uid, i.e. whole blocks in layout order. */
 int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq,
             const float* w, uint64_t budget_bytes, uint32_t flags,
             uint32_t* mask, mp_plan_stats* stats, void* stream);

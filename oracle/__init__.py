@@ -128,15 +128,18 @@ def index(blocks: Blocks, dtype, base, experts, doff=None, ids=None, delta=False
 
 
 def plan(blocks: Blocks, dtype, K: int, sumsq, w, budget: int, flags: int = 0):
-    """Algorithm 1; returns (mask uint32[G], stats dict)."""
+    """Algorithm 1; returns (mask uint32[G], stats dict).  sumsq None: no
+    catalog, the deterministic fallback (every unit's statistic 1)."""
     L = lib()
-    sumsq = np.ascontiguousarray(sumsq, np.float32).reshape(-1)
+    if sumsq is not None:
+        sumsq = np.ascontiguousarray(sumsq, np.float32).reshape(-1)
+        assert sumsq.size == blocks.G * K
     w = np.ascontiguousarray(w, np.float32)
-    assert sumsq.size == blocks.G * K and w.size == K
+    assert w.size == K
     l_a, l_p = _i64(blocks.len)
     mask = np.zeros(blocks.G, np.uint32)
     st = np.zeros(5, np.uint64)
-    _check(L.orc_plan(blocks.G, l_p, _dt(dtype), K, sumsq.ctypes.data, w.ctypes.data,
+    _check(L.orc_plan(blocks.G, l_p, _dt(dtype), K, None if sumsq is None else sumsq.ctypes.data, w.ctypes.data,
                       int(budget), flags, mask.ctypes.data, st.ctypes.data), "plan")
     return mask, dict(cost=int(st[0]), n_selected=int(st[1]), full_bytes=int(st[2]),
                       digest=int(st[3]), n_units=int(st[4]))

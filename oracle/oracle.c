@@ -262,10 +262,13 @@ int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
         int32_t i = (int32_t)(u % K);
         uint64_t c = (uint64_t)len[u / K] * (uint64_t)s;
         full += c;
-        if ((flags & 2u) && sumsq[u] == 0.0f)
+        /* no catalog (sumsq NULL): the planner's deterministic fallback
+           gives every unit the same statistic, 1 */
+        const float S = sumsq ? sumsq[u] : 1.0f;
+        if ((flags & 2u) && S == 0.0f)
             continue;
         float w2 = w[i] * w[i];
-        float sc = w2 * sumsq[u];
+        float sc = w2 * S;
         if (flags & 1u)
             sc = (float)((double)sc / (double)c);
         q[nq].score = sc;

@@ -38,6 +38,9 @@ int orc_index(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype
               const void* base, const void* const* experts, int32_t K, float* sumsq);
 
 /* Algorithm 1 (PlanGen), literal: score, sort, skip-and-continue greedy.
+ * sumsq NULL (no block catalog): every unit's statistic is 1, so units rank
+ * by w_i^2 and then by uid, i.e. blocks in layout order (Section 3's
+ * deterministic fallback when block metadata are missing).
  * flags: 1 = score per byte of cost, 2 = units with a zero sum of squares
  * are not candidates.  stats[0]=selected cost, [1]=selected units, [2]=full
  * cost, [3]=digest, [4]=number of units. */

@@ -732,7 +732,8 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float*
             return fail(MP_E_ARG, "w[%d] is not finite", i);
         cw.v[i] = w[i];
     }
-    if ((rc = check_device_buffer(sumsq, sizeof(float) * (size_t)(G * K), "sumsq")))
+    // sumsq NULL: no catalog, the deterministic fallback ranking
+    if (sumsq != nullptr && (rc = check_device_buffer(sumsq, sizeof(float) * (size_t)(G * K), "sumsq")))
         return rc;
     if ((rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)G, "mask")))
         return rc;

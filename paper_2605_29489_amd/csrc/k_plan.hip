@@ -77,6 +77,13 @@ __device__ inline unsigned long long unit_key(float S, float w, uint32_t uid, un
 
 __device__ inline bool plan_skips(float S, uint32_t flags) { return (flags & kPlanSkipZero) && S == 0.0f; }
 
+// A unit's catalog statistic; without a catalog (sumsq null) the fallback
+// gives every unit 1, so the plan takes units by weight, then in uid order.
+__device__ inline float plan_stat(const float* __restrict__ sumsq, uint32_t uid)
+{
+    return sumsq != nullptr ? sumsq[uid] : 1.0f;
+}
+
 // Wave-level resolution of one digit: h[256] holds the cost of the matching
 // candidates per digit value.  Returns the smallest v with
 // sum_{v' <= v} h[v'] > brem (v = -1 if the total fits), the cost below v,
@@ -213,7 +220,7 @@ __global__ __launch_bounds__(kT) void k_plan_hist(PlanCtl* ctl, int d, const flo
             const unsigned long long c = (unsigned long long)blen[g] * esize;
             for (int i = 0; i < K; ++i) {
                 const uint32_t uid = (uint32_t)(g * K + i);
-                const float S = sumsq[uid];
+                const float S = plan_stat(sumsq, uid);
                 if (plan_skips(S, flags))
                     continue;
                 const unsigned long long key = unit_key(S, w.v[i], uid, c, flags);
@@ -228,7 +235,7 @@ __global__ __launch_bounds__(kT) void k_plan_hist(PlanCtl* ctl, int d, const flo
             const uint32_t uid = src.list[q];
             const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
             const unsigned long long c = (unsigned long long)blen[g] * esize;
-            const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid, c, flags);
+            const unsigned long long key = unit_key(plan_stat(sumsq, uid), w.v[i], uid, c, flags);
             if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
                 atomicAdd(&lh[(key >> dg_shift) & 255u], c);
         }
@@ -292,7 +299,7 @@ __global__ __launch_bounds__(kT) void k_plan_mark(PlanCtl* ctl, const float* __r
             uint32_t word = 0u;
             for (int i = 0; i < K; ++i) {
                 const uint32_t uid = (uint32_t)(g * K + i);
-                const float S = sumsq[uid];
+                const float S = plan_stat(sumsq, uid);
                 if (plan_skips(S, flags))
                     continue;
                 const unsigned long long key = unit_key(S, w.v[i], uid, c, flags);
@@ -316,7 +323,7 @@ __global__ __launch_bounds__(kT) void k_plan_mark(PlanCtl* ctl, const float* __r
             const uint32_t uid = src.list[q];
             const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
             const unsigned long long c = (unsigned long long)blen[g] * esize;
-            const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid, c, flags);
+            const unsigned long long key = unit_key(plan_stat(sumsq, uid), w.v[i], uid, c, flags);
             if (all || key < keyp) {
                 atomicOr(&mask[g], 1u << i);
                 my_cost += c;
@@ -447,7 +454,7 @@ __global__ __launch_bounds__(kT) void k_plan_rest(PlanCtl* ctl, const float* __r
                 const uint32_t uid = plan_list_load(&list[q]);
                 const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
                 const unsigned long long c = (unsigned long long)blen[g] * esize;
-                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid, c, flags);
+                const unsigned long long key = unit_key(plan_stat(sumsq, uid), w.v[i], uid, c, flags);
                 if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
                     atomicAdd(&lh[(key >> dg_shift) & 255u], c);
             }
@@ -494,7 +501,7 @@ __global__ __launch_bounds__(kT) void k_plan_rest(PlanCtl* ctl, const float* __r
                 const uint32_t uid = plan_list_load(&list[q]);
                 const uint32_t g = uid / (uint32_t)K, i = uid % (uint32_t)K;
                 const unsigned long long c = (unsigned long long)blen[g] * esize;
-                const unsigned long long key = unit_key(sumsq[uid], w.v[i], uid, c, flags);
+                const unsigned long long key = unit_key(plan_stat(sumsq, uid), w.v[i], uid, c, flags);
                 if (all || key < prefix) {
                     atomicOr(&mask[g], 1u << i);
                     sel_cost += c;

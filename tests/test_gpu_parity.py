@@ -717,6 +717,31 @@ def test_plan_many_rounds(mp):
                 assert st["full_bytes"] == st_orc["full_bytes"] and st["n_units"] == G * K
 
 
+def test_plan_without_catalog(mp):
+    # no block catalog (sumsq NULL): the deterministic fallback ranking,
+    # bit-exact against the oracle, then a merge over that mask
+    import torch
+    spec = _mini_qwen(n_layers=1)
+    base_np, exps_np = make_family(spec, seed=35)
+    L, lay = _lay(mp, spec)
+    K = len(exps_np)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    mask = torch.empty(blocks.G, dtype=torch.int32, device="cuda")
+    full = int(blocks.len.sum()) * lay.elem_bytes * K
+    for w in ([1.0] * K, [0.5, 2.0, 1.0, 1.5]):
+        for f in (0.0, 0.33, 0.8, 1.0):
+            st = mp.mp_plan(L, K, None, w, int(f * full), mask)
+            m_orc, st_orc = oracle.plan(blocks, lay.dtype, K, None, w, int(f * full))
+            assert np.array_equal(mask.cpu().numpy().view(np.uint32), m_orc)
+            assert st["cost_bytes"] == st_orc["cost"] and st["digest"] == st_orc["digest"]
+    base = to_dev(base_np, lay.dtype)
+    exps = [to_dev(e, lay.dtype) for e in exps_np]
+    out = torch.empty_like(base)
+    mp.mp_merge_ties(L, base, exps, mask, 0.2, 1.0, out)
+    want = oracle.merge_ties(blocks, lay.dtype, base_np, exps_np, m_orc, 0.2, 1.0)
+    assert assert_merge_equal(to_host(out), want, base_np, lay.dtype, "ties without catalog") == 0
+
+
 def test_budget_boundaries_exact(mp):
     # budgets at the exact cost of a greedy prefix, one byte below and above
     spec = _mini_qwen(n_layers=1)

@@ -289,6 +289,23 @@ def test_plan_skip_zero_drops_exactly_the_zero_units():
     assert int(m[0]) == 0 and st["cost"] == 0 and st["n_selected"] == 0
 
 
+def test_plan_without_catalog_takes_units_by_weight_then_layout_order():
+    # Section 3's fallback when block metadata are missing: with equal block
+    # costs and equal weights the plan is the longest prefix of units in uid
+    # (layout) order that fits; a heavier expert's units all come first.
+    numel = [4096 * 5, 4096 * 3]
+    b = oracle.Blocks(numel, 4096)
+    K = 3
+    c = 4096 * 2
+    for n_fit in (0, 1, 7, 10, 24):
+        m, st = oracle.plan(b, "bf16", K, None, [1.0] * K, n_fit * c + c // 2)
+        sel = [u for u in range(b.G * K) if (m[u // K] >> (u % K)) & 1]
+        assert sel == list(range(n_fit)) and st["cost"] == n_fit * c
+    m, st = oracle.plan(b, "bf16", K, None, [1.0, 2.0, 1.0], 9 * c)
+    sel = [u for u in range(b.G * K) if (m[u // K] >> (u % K)) & 1]
+    assert sel == sorted([g * K + 1 for g in range(8)] + [0])  # expert 1's units, then uid 0
+
+
 def _random_plan_case(rng, G, K, uniform, ties=False):
     if uniform:
         numel = [16] * G
