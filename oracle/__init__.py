@@ -55,6 +55,8 @@ def lib():
                                                  C.c_double, C.c_void_p]
         L.orc_merge_ties_tau.argtypes = [C.c_int64, i64p, i64p, C.c_int32, C.c_void_p, C.POINTER(C.c_void_p),
                                          C.c_int32, C.c_void_p, C.c_void_p, C.c_float, C.c_void_p]
+        L.orc_lora_delta.argtypes = [C.c_int32, C.c_int64, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p,
+                                     C.c_float, C.c_void_p]
         L.orc_ties_k.restype = C.c_int64
         L.orc_ties_k.argtypes = [C.c_int64, C.c_double]
         L.orc_num_threads.restype = C.c_int
@@ -257,6 +259,49 @@ def merge_dare(blocks, dtype, base, experts, mask, p, seed, combine, alpha, lam,
                             _dt(dtype, delta), base.ctypes.data, _ptrs(experts), len(experts),
                             mask.ctypes.data, float(p), int(seed) & 0xFFFFFFFF, int(combine),
                             alpha.ctypes.data, float(lam), out.ctypes.data), "dare")
+    return out
+
+
+def lora_delta(dtype, rows: int, cols: int, A, B, scale: float):
+    """One adapted tensor's delta, [rows * cols] in the checkpoint dtype.
+
+    A: [rank, cols], B: [rows, rank] (row-major, checkpoint dtype)."""
+    A = np.ascontiguousarray(A)
+    B = np.ascontiguousarray(B)
+    rank = A.shape[0]
+    if A.shape != (rank, cols) or B.shape != (rows, rank) or A.dtype != B.dtype:
+        raise ValueError("adapter shapes do not match the tensor")
+    out = np.zeros(rows * cols, A.dtype)
+    _check(lib().orc_lora_delta(_dt(dtype), rows, cols, rank, A.ctypes.data, B.ctypes.data, float(scale),
+                                out.ctypes.data), "lora delta")
+    return out
+
+
+def lora_materialize(blocks: Blocks, dtype, numel, loras, adapters, mask=None, fill=None):
+    """Explicit delta checkpoints drawn from LoRA adapters (one per expert).
+
+    ``loras``: records (tensor, rows, cols, rank, a_off, b_off, scale); expert
+    i's A and B of a record lie at those element offsets of ``adapters[i]``.
+    Tensors without a record have zero deltas.  Unit (g, i) is written when
+    bit i of mask[g] is set (every unit when mask is None); the other
+    elements keep ``fill[i]`` (zeros when fill is None)."""
+    numel = [int(n) for n in numel]
+    toff = np.concatenate([[0], np.cumsum(numel)]).astype(np.int64)
+    P = int(toff[-1])
+    out = []
+    for i, ad in enumerate(adapters):
+        ad = np.ascontiguousarray(ad)
+        full = np.zeros(P, ad.dtype)
+        for (t, rows, cols, rank, a_off, b_off, scale) in loras:
+            A = ad[a_off:a_off + rank * cols].reshape(rank, cols)
+            B = ad[b_off:b_off + rows * rank].reshape(rows, rank)
+            full[toff[t]:toff[t] + rows * cols] = lora_delta(dtype, rows, cols, A, B, scale)
+        d = np.zeros(P, ad.dtype) if fill is None else np.array(fill[i], copy=True)
+        for g in range(blocks.G):
+            if mask is None or (int(mask[g]) >> i) & 1:
+                o, n = int(blocks.off[g]), int(blocks.len[g])
+                d[o:o + n] = full[o:o + n]
+        out.append(d)
     return out
 
 

@@ -787,3 +787,34 @@ int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
     }
     return bad ? -2 : 0;
 }
+
+/* ------------------------------------------------------------------ */
+/* Low-rank adapters as a delta source                                 */
+/* ------------------------------------------------------------------ */
+
+/* Section 3 (Executor): the delta iterator may draw an expert's deltas from
+ * LoRA-style adapters (Hu et al., 2022).  Tensor t, viewed as a rows x cols
+ * row-major matrix, has the delta scale * B A with A (rank x cols) and B
+ * (rows x rank), both row-major in the checkpoint dtype.  Reading (the paper
+ * fixes no precision): y = fp32 rounding of the exact sum over k of
+ * B[r][k] * A[k][c]; d = fl32(scale * y), stored in the checkpoint dtype.
+ * Products of fp32 or bf16 values are exact in fp64 and are summed in fp64
+ * in k order, which is the exact sum whenever it fits fp64's 53 bits.
+ * out: rows * cols elements in the checkpoint dtype. */
+int orc_lora_delta(int32_t dtype, int64_t rows, int64_t cols, int32_t rank, const void* A, const void* B,
+                   float scale, void* out)
+{
+    if (elem_bytes(dtype) == 0 || (dtype & ORC_DELTA) || rows < 0 || cols < 0 || rank < 1)
+        return -1;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        for (int64_t c = 0; c < cols; ++c) {
+            double s = 0.0;
+            for (int32_t k = 0; k < rank; ++k)
+                s += (double)load(B, dtype, r * rank + k) * (double)load(A, dtype, (int64_t)k * cols + c);
+            const float y = (float)s;
+            store(out, dtype, r * cols + c, scale * y);
+        }
+    }
+    return 0;
+}

@@ -85,6 +85,14 @@ int orc_merge_ties_tau(int64_t nb, const int64_t* doff, const int64_t* len, int3
                        const void* base, const void* const* experts, int32_t K,
                        const uint32_t* mask, const uint32_t* tau, float lambda, void* out);
 
+/* One tensor's delta from a LoRA adapter (Section 3's low-rank delta
+ * source): out[r*cols + c] = fl32(scale * y) in the checkpoint dtype, y the
+ * fp32 rounding of sum_k B[r*rank + k] * A[k*cols + c] (exact products,
+ * summed in fp64).  A: rank x cols, B: rows x rank, row-major, checkpoint
+ * dtype (no ORC_DELTA bit). */
+int orc_lora_delta(int32_t dtype, int64_t rows, int64_t cols, int32_t rank, const void* A, const void* B,
+                   float scale, void* out);
+
 /* Building blocks exposed so the tests can pin them. */
 void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
 uint64_t orc_mix64(uint64_t x);

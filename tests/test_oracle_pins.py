@@ -737,6 +737,136 @@ def test_delta_experts_bf16_constant_delta_closed_form():
 
 
 # --------------------------------------------------------------------------
+# LoRA adapters as a delta source (Section 3, Executor)
+# --------------------------------------------------------------------------
+
+def _round_f32_exact(fr):
+    # the fp32 nearest to the rational fr, ties to even: float(fr) is within
+    # one fp32 ulp of it, so the answer is that value or a neighbour
+    from fractions import Fraction
+    x = np.float32(float(fr))
+    cands = [np.nextafter(x, np.float32(-np.inf)), x, np.nextafter(x, np.float32(np.inf))]
+    return min(cands, key=lambda c: (abs(Fraction(float(c)) - fr), int(np.float32(c).view(np.uint32)) & 1))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_lora_delta_brute_force_exact_sum(dtype):
+    # Each element is the exact rational sum of the rank products, rounded
+    # once to fp32, times the scale in fp32, stored in the dtype.  A 5 x 6
+    # tensor with rank 3 (no square shapes: a transposed operand fails).
+    from fractions import Fraction
+    rng = np.random.default_rng(51)
+    rows, cols, rank = 5, 6, 3
+    A = (rng.standard_normal((rank, cols)) * np.exp(rng.uniform(-8, 8, (rank, cols)))).astype(np.float32)
+    B = (rng.standard_normal((rows, rank)) * np.exp(rng.uniform(-8, 8, (rows, rank)))).astype(np.float32)
+    scale = np.float32(0.7)
+    if dtype == "bf16":
+        A, B = _bits_bf16(A), _bits_bf16(B)
+        Af, Bf = _f32_of_bf16(A), _f32_of_bf16(B)
+    else:
+        Af, Bf = A, B
+    got = oracle.lora_delta(dtype, rows, cols, A, B, scale)
+    want = np.zeros(rows * cols, np.float32)
+    for r in range(rows):
+        for c in range(cols):
+            fr = sum(Fraction(float(Bf[r, k])) * Fraction(float(Af[k, c])) for k in range(rank))
+            want[r * cols + c] = scale * _round_f32_exact(fr)
+    if dtype == "bf16":
+        want = _bits_bf16(want)
+    assert np.array_equal(got, want)
+
+
+def test_lora_delta_rank_one_and_identity_factors():
+    # rank 1: scale * outer(u, v); A = I (rank = cols): scale * B;
+    # B = I (rank = rows): scale * A.  Dyadic values make every sum exact.
+    rng = np.random.default_rng(52)
+    rows, cols = 7, 12
+    u = (rng.integers(-64, 64, rows) / 64.0).astype(np.float32)
+    v = (rng.integers(-64, 64, cols) / 32.0).astype(np.float32)
+    got = oracle.lora_delta("f32", rows, cols, v.reshape(1, cols), u.reshape(rows, 1), 0.5)
+    assert np.array_equal(got, (0.5 * np.outer(u, v)).astype(np.float32).reshape(-1))
+    B = (rng.integers(-100, 100, (rows, cols)) / 16.0).astype(np.float32)
+    got = oracle.lora_delta("f32", rows, cols, np.eye(cols, dtype=np.float32), B, 2.0)
+    assert np.array_equal(got, (2.0 * B).reshape(-1))
+    A = (rng.integers(-100, 100, (rows, cols)) / 16.0).astype(np.float32)
+    got = oracle.lora_delta("f32", rows, cols, A, np.eye(rows, dtype=np.float32), 0.25)
+    assert np.array_equal(got, (0.25 * A).reshape(-1))
+    # the same in bf16 (the values are bf16-exact)
+    got = oracle.lora_delta("bf16", rows, cols, _bits_bf16(A), _bits_bf16(np.eye(rows, dtype=np.float32)), 0.25)
+    assert np.array_equal(got, _bits_bf16(0.25 * A).reshape(-1))
+
+
+def test_lora_delta_is_additive_over_rank_components():
+    # Stacking two adapters along the rank gives the sum of their deltas
+    # (every sum exact on this grid): no rank term is dropped.
+    rng = np.random.default_rng(53)
+    rows, cols, r1, r2 = 9, 20, 5, 11
+    def grid(shape):
+        return (rng.integers(-16, 16, shape) / 16.0).astype(np.float32)
+    A1, A2, B1, B2 = grid((r1, cols)), grid((r2, cols)), grid((rows, r1)), grid((rows, r2))
+    d1 = oracle.lora_delta("f32", rows, cols, A1, B1, 1.0)
+    d2 = oracle.lora_delta("f32", rows, cols, A2, B2, 1.0)
+    d = oracle.lora_delta("f32", rows, cols, np.vstack([A1, A2]), np.hstack([B1, B2]), 1.0)
+    assert np.array_equal(d, d1 + d2)
+    assert np.array_equal(d.reshape(rows, cols), B1 @ A1 + B2 @ A2)
+
+
+def _lora_family(rng, numel, shapes, K, rank, dtype="f32"):
+    # adapters on a dyadic grid: every rank sum is exact, so W_i = W_0 + d
+    # is exact too; records pack A then B per tensor
+    loras, off = [], 0
+    for t, (rows, cols) in shapes.items():
+        loras.append((t, rows, cols, rank, off, off + rank * cols, 0.5))
+        off += rank * (rows + cols)
+    ads = [(rng.integers(-8, 8, off) / 64.0).astype(np.float32) for _ in range(K)]
+    if dtype == "bf16":
+        ads = [_bits_bf16(a) for a in ads]
+    return loras, ads
+
+
+def test_lora_materialize_masks_fill_and_unadapted_tensors():
+    rng = np.random.default_rng(54)
+    numel = [24 * 40, 520, 16 * 72, 4096]
+    b = oracle.Blocks(numel, 256)
+    K = 3
+    loras, ads = _lora_family(rng, numel, {0: (24, 40), 2: (16, 72)}, K, 6)
+    full = oracle.lora_materialize(b, "f32", numel, loras, ads)
+    toff = np.concatenate([[0], np.cumsum(numel)])
+    for i in range(K):
+        assert not full[i][toff[1]:toff[2]].any() and not full[i][toff[3]:].any()  # no adapter: zero
+        A = ads[i][0:6 * 40].reshape(6, 40)
+        B = ads[i][6 * 40:6 * 64].reshape(24, 6)
+        assert np.array_equal(full[i][:960], (0.5 * (B @ A)).astype(np.float32).reshape(-1))
+    mask = rng.integers(0, 8, b.G).astype(np.uint32)
+    fill = [np.full(sum(numel), 9.0, np.float32) for _ in range(K)]
+    part = oracle.lora_materialize(b, "f32", numel, loras, ads, mask=mask, fill=fill)
+    for i in range(K):
+        for g in range(b.G):
+            o, n = b.off[g], b.len[g]
+            want = full[i][o:o + n] if (mask[g] >> i) & 1 else fill[i][o:o + n]
+            assert np.array_equal(part[i][o:o + n], want)
+
+
+def test_lora_deltas_merge_like_the_weights_they_define():
+    # The merge only sees deltas: adapters materialised as explicit deltas
+    # give the merge of the checkpoints W_i = W_0 + scale * B A, here exact.
+    rng = np.random.default_rng(55)
+    numel = [32 * 48, 16, 40 * 64, 520]
+    b = oracle.Blocks(numel, 512)
+    K = 4
+    loras, ads = _lora_family(rng, numel, {0: (32, 48), 2: (40, 64)}, K, 8)
+    base = (rng.integers(-2048, 2048, sum(numel)) / 2.0**10).astype(np.float32)
+    deltas = oracle.lora_materialize(b, "f32", numel, loras, ads)
+    weights = [base + d for d in deltas]
+    assert all(np.array_equal(w - base, d) for w, d in zip(weights, deltas))
+    mask = rng.integers(0, 16, b.G).astype(np.uint32)
+    assert np.array_equal(oracle.merge_ties(b, "f32", base, deltas, mask, 0.3, 1.0, delta=True),
+                          oracle.merge_ties(b, "f32", base, weights, mask, 0.3, 1.0))
+    assert np.array_equal(oracle.merge_avg(b, "f32", base, deltas, mask, [0.25] * 4, delta=True),
+                          oracle.merge_avg(b, "f32", base, weights, mask, [0.25] * 4))
+
+
+# --------------------------------------------------------------------------
 # TIES
 # --------------------------------------------------------------------------
 
