@@ -264,6 +264,41 @@ int mp_merge_dare(const mp_layout* layout, const void* base,
                   const float* alpha, float lambda, void* out, mp_io_stats* io,
                   void* stream);
 
+/* One low-rank adapter record (Section 3: the delta iterator's LoRA-style
+ * adapters, Hu et al. 2022).  Tensor `tensor` of the layout, viewed as a
+ * rows x cols row-major matrix (rows * cols = its numel), has the delta
+ * scale * B A, with A (rank x cols) and B (rows x rank) row-major in the
+ * layout's dtype at element offsets a_off and b_off of each expert's
+ * adapter buffer.  1 <= rank <= 64; cols a multiple of 4; numel < 2^32. */
+typedef struct mp_lora_tensor {
+    int32_t tensor;
+    int32_t rank;
+    int64_t rows;
+    int64_t cols;
+    int64_t a_off;
+    int64_t b_off;
+    float scale;
+} mp_lora_tensor;
+
+/* Deltas drawn from adapters (Section 3, the executor's delta iterator):
+ * writes expert i's delta of every selected unit (g, i) -- every unit when
+ * mask is NULL -- into deltas[i], an explicit-delta checkpoint (layout
+ * order, layout dtype) for the MP_EXPERTS_DELTA residency bit.  For an
+ * adapted tensor, element (r, c) is float(scale * y) rounded to the dtype
+ * (to nearest even), y the fp32 sum over k of B[r][k] * A[k][c] computed on
+ * the matrix cores (exact products, fp32 accumulation; equal to the
+ * correctly rounded sum whenever every partial sum is exact in fp32).
+ * Tensors without a record get zeros.  Elements of unselected units are not
+ * written.  adapters: HOST array of K device pointers (each at least the
+ * largest a_off + rank*cols, b_off + rows*rank elements; the array may be
+ * NULL when n_lora = 0); deltas: HOST array of K device checkpoints, disjoint from
+ * each other and from the adapters; mask: device uint32[G] or NULL.
+ * Records are validated and their device table is cached per (device,
+ * layout, records).  Asynchronous on `stream`. */
+int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, int32_t n_lora,
+                        const void* const* adapters, int32_t K, const uint32_t* mask,
+                        void* const* deltas, void* stream);
+
 /* Staging for MP_HOST_PAGEABLE: the bytes of each of the two pinned host
  * buffers (and of their two device counterparts) that chunks of packed
  * expert blocks pass through; default 256 MiB, rounded down to 256 bytes.

@@ -36,7 +36,8 @@ MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
            "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
            "mp_merge_ties",
-           "mp_merge_ties_tau", "mp_merge_dare", "mp_set_stage_bytes", "mp_last_error", "mp_release")
+           "mp_merge_ties_tau", "mp_merge_dare", "mp_lora_materialize", "mp_set_stage_bytes", "mp_last_error",
+           "mp_release")
 
 
 class mp_layout(C.Structure):
@@ -60,6 +61,11 @@ class mp_io_stats(C.Structure):
         d = {f: int(getattr(self, f)) for f, _ in self._fields_[:4]}
         d["expert_bytes_by_expert"] = [int(x) for x in self.expert_bytes_by_expert]
         return d
+
+
+class mp_lora_tensor(C.Structure):
+    _fields_ = [("tensor", C.c_int32), ("rank", C.c_int32), ("rows", C.c_int64), ("cols", C.c_int64),
+                ("a_off", C.c_int64), ("b_off", C.c_int64), ("scale", C.c_float)]
 
 
 class MPError(RuntimeError):
@@ -96,6 +102,8 @@ def _load():
                                     C.POINTER(mp_io_stats), vp]
     L.mp_merge_dare.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.c_double, u32, i32,
                                 C.POINTER(C.c_float), C.c_float, vp, C.POINTER(mp_io_stats), vp]
+    L.mp_lora_materialize.argtypes = [lp, C.POINTER(mp_lora_tensor), i32, C.POINTER(vp), i32, vp, C.POINTER(vp),
+                                      vp]
     L.mp_last_error.restype = C.c_char_p
     L.mp_set_stage_bytes.argtypes = [u64]
     L.mp_set_stage_bytes.restype = i32
@@ -105,7 +113,7 @@ def _load():
                  "mp_coverage", "mp_merge_avg",
                  "mp_merge_avg_renorm", "mp_merge_ties",
                  "mp_merge_ties_tau",
-                 "mp_merge_dare"):
+                 "mp_merge_dare", "mp_lora_materialize"):
         getattr(L, name).restype = C.c_int
     return L
 
@@ -277,6 +285,20 @@ def mp_merge_dare(layout: Layout, base, experts, mask, p: float, seed: int, comb
                              float(p), int(seed) & 0xFFFFFFFF, int(combine), a, float(lam), _ptr(out), _io(st),
                              _stream(stream)))
     return st.as_dict() if io else None
+
+
+def mp_lora_materialize(layout: Layout, loras, adapters, deltas, mask=None, stream=None):
+    """Explicit-delta checkpoints drawn from LoRA adapters (selected units only).
+
+    ``loras``: records (tensor, rows, cols, rank, a_off, b_off, scale);
+    ``adapters``/``deltas``: K device tensors each (adapters may be empty
+    when there are no records)."""
+    recs = (mp_lora_tensor * max(len(loras), 1))(
+        *[mp_lora_tensor(int(t), int(rank), int(rows), int(cols), int(a), int(b), float(sc))
+          for (t, rows, cols, rank, a, b, sc) in loras])
+    K = len(deltas)
+    _check(lib.mp_lora_materialize(layout.ref, recs, len(loras), _ptrs(adapters) if loras else None, K, _ptr(mask),
+                                   _ptrs(deltas), _stream(stream)))
 
 
 def mp_last_error() -> str:

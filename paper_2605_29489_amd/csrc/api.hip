@@ -62,6 +62,21 @@ struct DeviceWs {
 std::mutex g_mu;
 std::map<std::string, std::unique_ptr<BlockTable>> g_tables;
 std::map<int, std::unique_ptr<DeviceWs>> g_ws;
+struct LoraEntry {
+    int device = -1;
+    LoraTable t;
+};
+std::map<std::string, std::unique_ptr<LoraEntry>> g_loras;
+
+void free_lora(LoraEntry& e)
+{
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(e.device);
+    (void)hipFree(e.t.d_desc);
+    (void)hipFree(e.t.d_zero);
+    (void)hipSetDevice(cur);
+}
 
 void free_table(BlockTable& bt)
 {
@@ -855,6 +870,166 @@ int mp_merge_dare(const mp_layout* layout, const void* base, const void* const* 
     return run_merge(layout, base, experts, K, residency, mask, out, io, static_cast<hipStream_t>(stream), a);
 }
 
+// Validates the adapter records against a validated layout (host only).
+// *need receives the elements every adapter buffer must hold.
+static int validate_loras(const mp_layout* L, const mp_lora_tensor* loras, int32_t n_lora, int64_t* need)
+{
+    if (n_lora < 0 || (n_lora > 0 && loras == nullptr))
+        return fail(MP_E_ARG, "n_lora = %d with loras %s", n_lora, loras ? "set" : "NULL");
+    if (n_lora > L->n_tensors)
+        return fail(MP_E_ARG, "n_lora = %d exceeds the layout's %d tensors", n_lora, L->n_tensors);
+    std::vector<char> adapted((size_t)L->n_tensors, 0);
+    *need = 0;
+    for (int32_t r = 0; r < n_lora; ++r) {
+        const mp_lora_tensor& x = loras[r];
+        if (x.tensor < 0 || x.tensor >= L->n_tensors)
+            return fail(MP_E_ARG, "loras[%d].tensor = %d is not a tensor of the layout", r, x.tensor);
+        if (adapted[(size_t)x.tensor])
+            return fail(MP_E_ARG, "loras[%d]: tensor %d has two adapters", r, x.tensor);
+        adapted[(size_t)x.tensor] = 1;
+        if (x.rank < 1 || x.rank > kMaxLoraRank)
+            return fail(MP_E_ARG, "loras[%d].rank = %d must be in [1, %d]", r, x.rank, kMaxLoraRank);
+        const int64_t n = L->numel[x.tensor];
+        if (x.rows < 1 || x.cols < 1 || x.cols % 4 != 0 || x.rows > n || x.rows * x.cols != n)
+            return fail(MP_E_ARG, "loras[%d]: %lld x %lld does not shape tensor %d (%lld elements; cols a multiple of 4)",
+                        r, (long long)x.rows, (long long)x.cols, x.tensor, (long long)n);
+        if (n >= ((int64_t)1 << 32))
+            return fail(MP_E_UNSUPPORTED, "loras[%d]: tensor %d has 2^32 or more elements", r, x.tensor);
+        if (x.a_off < 0 || x.b_off < 0 || !std::isfinite(x.scale))
+            return fail(MP_E_ARG, "loras[%d]: negative offset or non-finite scale", r);
+        *need = std::max(*need, std::max(x.a_off + (int64_t)x.rank * x.cols, x.b_off + x.rows * (int64_t)x.rank));
+    }
+    return MP_OK;
+}
+
+// Looks up or builds the device table of validated adapter records.
+static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lora_tensor* loras, int32_t n_lora,
+                          LoraTable** out)
+{
+    std::vector<int64_t> toff((size_t)L->n_tensors + 1, 0), tg0((size_t)L->n_tensors + 1, 0);
+    for (int32_t t = 0; t < L->n_tensors; ++t) {
+        toff[(size_t)t + 1] = toff[(size_t)t] + L->numel[t];
+        tg0[(size_t)t + 1] = tg0[(size_t)t] + (L->numel[t] + L->block_elems - 1) / L->block_elems;
+    }
+    std::vector<char> adapted((size_t)L->n_tensors, 0);
+    for (int32_t r = 0; r < n_lora; ++r)
+        adapted[(size_t)loras[r].tensor] = 1;
+    std::string key = layout_key(bt.device, L);
+    key.append(reinterpret_cast<const char*>(loras), sizeof(mp_lora_tensor) * (size_t)n_lora);
+    auto it = g_loras.find(key);
+    if (it != g_loras.end()) {
+        *out = &it->second->t;
+        return MP_OK;
+    }
+    auto e = std::make_unique<LoraEntry>();
+    e->device = bt.device;
+    std::vector<LoraDesc> desc;
+    uint64_t tiles = 0;
+    for (int32_t r = 0; r < n_lora; ++r) {  // descriptors in layout order
+        const mp_lora_tensor& x = loras[r];
+        LoraDesc d{};
+        d.toff = (uint64_t)toff[(size_t)x.tensor];
+        d.a_off = (uint64_t)x.a_off;
+        d.b_off = (uint64_t)x.b_off;
+        d.rows = (uint32_t)x.rows;
+        d.cols = (uint32_t)x.cols;
+        d.rank = (uint32_t)x.rank;
+        d.scale = x.scale;
+        d.g0 = (uint32_t)tg0[(size_t)x.tensor];
+        desc.push_back(d);
+    }
+    std::sort(desc.begin(), desc.end(), [](const LoraDesc& a, const LoraDesc& b) { return a.toff < b.toff; });
+    for (LoraDesc& d : desc) {
+        d.tile0 = (uint32_t)tiles;
+        tiles += lora_tiles(d.rows, d.cols, &d.tiles_n);
+        if (tiles >= ((uint64_t)1 << 31))
+            return fail(MP_E_UNSUPPORTED, "adapted tensors need 2^31 or more output tiles");
+    }
+    std::vector<uint32_t> zero;
+    for (int32_t t = 0; t < L->n_tensors; ++t)
+        if (!adapted[(size_t)t])
+            for (int64_t g = tg0[(size_t)t]; g < tg0[(size_t)t + 1]; ++g)
+                zero.push_back((uint32_t)g);
+    e->t.n_desc = (int)desc.size();
+    e->t.n_tiles = (uint32_t)tiles;
+    e->t.n_zero = (uint32_t)zero.size();
+    hipError_t he = hipSuccess;
+    if ((!desc.empty() && ((he = hipMalloc((void**)&e->t.d_desc, sizeof(LoraDesc) * desc.size())) != hipSuccess ||
+                           (he = hipMemcpy(e->t.d_desc, desc.data(), sizeof(LoraDesc) * desc.size(),
+                                           hipMemcpyHostToDevice)) != hipSuccess)) ||
+        (!zero.empty() && ((he = hipMalloc((void**)&e->t.d_zero, sizeof(uint32_t) * zero.size())) != hipSuccess ||
+                           (he = hipMemcpy(e->t.d_zero, zero.data(), sizeof(uint32_t) * zero.size(),
+                                           hipMemcpyHostToDevice)) != hipSuccess))) {
+        free_lora(*e);
+        return fail(MP_E_NOMEM, "adapter table: %s", hipGetErrorString(he));
+    }
+    *out = &e->t;
+    g_loras.emplace(key, std::move(e));
+    return MP_OK;
+}
+
+int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, int32_t n_lora,
+                        const void* const* adapters, int32_t K, const uint32_t* mask, void* const* deltas,
+                        void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    int es = 0;
+    int rc = validate_layout(layout, &es);
+    if (rc)
+        return rc;
+    if (K < 1 || K > kMaxK)
+        return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
+    if ((n_lora > 0 && adapters == nullptr) || deltas == nullptr)
+        return fail(MP_E_ARG, "adapters or deltas is NULL");
+    const int64_t G = count_blocks(layout);
+    if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
+        return fail(MP_E_ARG, "K * G = %lld does not fit 32-bit unit ids", (long long)(G * K));
+    int64_t need = 0;
+    if ((rc = validate_loras(layout, loras, n_lora, &need)))
+        return rc;
+    BlockTable* bt = nullptr;
+    LoraTable* lt = nullptr;
+    if ((rc = get_table(layout, es, &bt)) || (rc = get_lora_table(layout, *bt, loras, n_lora, &lt)))
+        return rc;
+    const size_t ckpt = (size_t)bt->P * (size_t)es;
+    std::vector<Range> ins, outs;
+    ExpertPtrs ad{};
+    OutPtrs dl{};
+    for (int i = 0; i < K; ++i) {
+        char nm[32];
+        std::snprintf(nm, sizeof nm, "adapters[%d]", i);
+        if (n_lora > 0) {
+            if ((rc = check_device_buffer(adapters[i], (size_t)need * (size_t)es, nm)))
+                return rc;
+            ins.push_back({static_cast<const char*>(adapters[i]), (size_t)need * (size_t)es, "an adapter"});
+        }
+        ad.p[i] = n_lora > 0 ? adapters[i] : nullptr;
+        std::snprintf(nm, sizeof nm, "deltas[%d]", i);
+        if ((rc = check_device_buffer(deltas[i], ckpt, nm)))
+            return rc;
+        const Range o{static_cast<const char*>(deltas[i]), ckpt, "deltas"};
+        for (const Range& r : ins)
+            if (overlaps(o, r))
+                return fail(MP_E_ARG, "deltas[%d] overlaps %s", i, r.name);
+        for (const Range& r : outs)
+            if (overlaps(o, r))
+                return fail(MP_E_ARG, "deltas[%d] overlaps another delta buffer", i);
+        outs.push_back(o);
+        dl.p[i] = deltas[i];
+    }
+    for (const Range& o : outs)
+        for (const Range& r : ins)
+            if (overlaps(o, r))
+                return fail(MP_E_ARG, "a delta buffer overlaps %s", r.name);
+    if (mask != nullptr && (rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)G, "mask")))
+        return rc;
+    hipError_t e = launch_lora(*bt, *lt, ad, dl, K, mask, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return hip_fail(e, "adapter delta launch");
+    return MP_OK;
+}
+
 const char* mp_last_error(void) { return g_err.c_str(); }
 
 int mp_set_stage_bytes(uint64_t bytes)
@@ -874,6 +1049,9 @@ void mp_release(void)
     for (auto& kv : g_tables)
         free_table(*kv.second);
     g_tables.clear();
+    for (auto& kv : g_loras)
+        free_lora(*kv.second);
+    g_loras.clear();
     for (auto& kv : g_ws)
         free_ws(kv.first, *kv.second);
     g_ws.clear();

@@ -97,6 +97,43 @@ hipError_t launch_ties_tensor(const BlockTable& bt, const void* base, const Expe
                               const uint32_t* mask, double density, uint32_t* tau, uint32_t* hist, uint4* state,
                               hipStream_t s, bool delta);
 
+// ---------------------------------------------------------------- LoRA source (k_lora.hip)
+constexpr int kMaxLoraRank = 64;
+
+// Expert output pointers (the explicit-delta checkpoints written), by value.
+struct OutPtrs {
+    void* p[kMaxK];
+};
+
+// One adapted tensor on the device; its output tiles are tile0 ..
+// tile0 + tiles_m * tiles_n - 1 of the launch (row-major over the tile grid).
+struct LoraDesc {
+    uint64_t toff;  // element offset of the tensor in a checkpoint
+    uint64_t a_off, b_off;  // element offsets of A and B in an adapter buffer
+    uint32_t rows, cols, rank;
+    float scale;
+    uint32_t g0;  // the tensor's first block
+    uint32_t tiles_n;
+    uint32_t tile0;
+    uint32_t pad;
+};
+
+// A validated set of adapter records for a layout, cached per device.
+struct LoraTable {
+    LoraDesc* d_desc = nullptr;  // sorted by tile0
+    int n_desc = 0;
+    uint32_t n_tiles = 0;
+    uint32_t* d_zero = nullptr;  // blocks of tensors without an adapter
+    uint32_t n_zero = 0;
+};
+
+// Tiles of a rows x cols tensor; *tiles_n receives the tiles per tile row.
+uint32_t lora_tiles(uint32_t rows, uint32_t cols, uint32_t* tiles_n);
+
+// Writes the selected units' deltas (all units when mask is null).
+hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& dl, int K,
+                       const uint32_t* mask, hipStream_t s);
+
 // Merge operators.  `counters` is null or a device array of 256 uint64
 // accumulating the expert bytes the kernels load: slot (block mod 8) * 32 + i
 // holds expert i's.

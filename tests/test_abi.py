@@ -43,6 +43,36 @@ def test_struct_layouts_match_header(mp):
     assert C.sizeof(mp.mp_layout) == 24
     assert C.sizeof(mp.mp_plan_stats) == 48
     assert C.sizeof(mp.mp_io_stats) == 32 + 8 * 32  # four totals + per-expert bytes
+    assert C.sizeof(mp.mp_lora_tensor) == 48  # int32 x2, int64 x4, float + tail padding
+
+
+def test_lora_records_rejected_before_any_device_work(mp):
+    lib = mp.lib
+    L = mp.Layout([64 * 96, 512, 32 * 48], 256, mp.MP_BF16)
+    ptrs = (C.c_void_p * 2)(None, None)
+
+    def rc(recs, K=2, adapters=ptrs, deltas=ptrs):  # records in the C field order
+        arr = (mp.mp_lora_tensor * max(len(recs), 1))(*[mp.mp_lora_tensor(*r) for r in recs])
+        return lib.mp_lora_materialize(L.ref, arr, len(recs), adapters, K, None, deltas, None)
+
+    good = (0, 16, 64, 96, 0, 16 * 96, 0.5)
+    bad = [
+        [(3, 16, 64, 96, 0, 0, 1.0)],            # no such tensor
+        [good, (0, 8, 64, 96, 0, 0, 1.0)],       # two adapters for one tensor
+        [(0, 0, 64, 96, 0, 0, 1.0)],             # rank 0
+        [(0, 65, 64, 96, 0, 0, 1.0)],            # rank above 64
+        [(0, 16, 96, 60, 0, 0, 1.0), (2, 4, 48, 32, 0, 0, 1.0)],  # shape does not match numel
+        [(1, 4, 2, 256, 0, 0, 1.0), (2, 4, 16, 100, 0, 0, 1.0)],  # ok, then rows x cols != numel
+        [(1, 4, 128, 4, 0, 0, 1.0), (0, 4, 64, 96, -1, 0, 1.0)],  # negative offset
+        [(0, 4, 64, 96, 0, 0, float("inf"))],    # non-finite scale
+        [(1, 4, 256, 2, 0, 0, 1.0)],             # cols not a multiple of 4
+    ]
+    for recs in bad:
+        assert rc(recs) == mp.MP_E_ARG, recs
+    assert rc([good], K=0) == mp.MP_E_ARG
+    assert rc([good], K=33) == mp.MP_E_ARG
+    assert rc([good], adapters=None) == mp.MP_E_ARG
+    assert rc([good], deltas=None) == mp.MP_E_ARG
 
 
 def test_layout_blocks_counts(mp):

@@ -15,4 +15,6 @@ from .families import (  # noqa: F401
     family_spec,
     make_family,
     make_family_device,
+    lora_records,
+    make_lora_adapters,
 )

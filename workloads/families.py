@@ -349,3 +349,44 @@ def _fill_one_expert(torch, spec: FamilySpec, i: int, seed: int, device, base, o
         off += n
         blk += nb
     return out
+
+
+# ---------------------------------------------------------------- low-rank adapter experts
+
+LORA_TARGETS = ("q_proj.weight", "k_proj.weight", "v_proj.weight", "o_proj.weight",
+                "gate_proj.weight", "up_proj.weight", "down_proj.weight")
+
+
+def lora_records(spec: FamilySpec, rank: int, scale: float, targets=LORA_TARGETS):
+    """Adapter records for the spec's 2-D tensors whose names end with one of
+    ``targets`` (None: every 2-D tensor): tuples (tensor, rows, cols, rank,
+    a_off, b_off, scale), with A (rank x cols) then B (rows x rank) packed per
+    tensor in layout order.  Returns (records, elements per adapter buffer)."""
+    recs, off = [], 0
+    for t, (name, shape) in enumerate(spec.tensors):
+        if len(shape) != 2 or (targets is not None and not name.endswith(tuple(targets))):
+            continue
+        rows, cols = shape
+        recs.append((t, rows, cols, rank, off, off + rank * cols, float(scale)))
+        off += rank * (rows + cols)
+    return recs, off
+
+
+def make_lora_adapters(n: int, K: int, dtype: str, seed: int = 0, grid: bool = False, std: float = 0.02):
+    """K adapter buffers of n elements, as numpy arrays (float32, or uint16
+    bfloat16 patterns).  grid=True draws j/64 with j uniform in [-8, 8): on
+    that grid every rank sum of products is exact in fp32.  Otherwise
+    N(0, std^2), rounded to the dtype."""
+    import torch
+
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(K):
+        if grid:
+            x = (rng.integers(-8, 8, n) / 64.0).astype(np.float32)
+        else:
+            x = (rng.standard_normal(n) * std).astype(np.float32)
+        if dtype == "bf16":
+            x = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        out.append(x)
+    return out
