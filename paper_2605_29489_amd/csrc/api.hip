@@ -941,9 +941,11 @@ static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lor
     std::sort(desc.begin(), desc.end(), [](const LoraDesc& a, const LoraDesc& b) { return a.toff < b.toff; });
     for (LoraDesc& d : desc) {
         d.tile0 = (uint32_t)tiles;
-        tiles += lora_tiles(d.rows, d.cols, &d.tiles_n);
+        tiles += lora_bands(d.rows, d.cols, &d.tiles_n);
         if (tiles >= ((uint64_t)1 << 31))
-            return fail(MP_E_UNSUPPORTED, "adapted tensors need 2^31 or more output tiles");
+            return fail(MP_E_UNSUPPORTED, "adapted tensors need 2^31 or more row bands");
+        const uint64_t cv = 16 / (uint64_t)bt.esize;  // elements per 16 bytes
+        d.vec = (d.a_off % cv == 0 && d.cols % cv == 0) ? 1u : 0u;
     }
     std::vector<uint32_t> zero;
     for (int32_t t = 0; t < L->n_tensors; ++t)

@@ -4,15 +4,18 @@
 // an explicit-delta checkpoint for the selected units only.
 //
 // The contraction runs on the matrix cores.  One 256-thread workgroup takes
-// a 64-row x 128-column output tile of one tensor for one expert; wave w
-// owns rows w*16 .. w*16+15 and computes the tile transposed, D^T = A^T B^T,
-// in eight 16 x 16 MFMA tiles along the columns:
-//   MFMA rows    = output columns (operand from A, staged transposed in LDS)
-//   MFMA columns = output rows    (operand from B, staged row-major in LDS)
+// a band of 64 rows of one tensor for one expert: it stages the band's B
+// rows in LDS once, then walks the band's 128-column tiles, staging each
+// tile's A columns transposed in LDS (16-byte loads of the next tile are in
+// flight while the current one computes and stores).  Wave w owns rows
+// w*16 .. w*16+15 and computes the tile transposed, D^T = A^T B^T, in eight
+// 16 x 16 MFMA tiles along the columns:
+//   MFMA rows    = output columns (operand from A)
+//   MFMA columns = output rows    (operand from B)
 // so that a lane's four accumulators are four consecutive columns of one
 // output row: one 8-byte (bf16) or 16-byte (fp32) store each.  The rank is
-// zero-padded to the MFMA depth (16 for bf16, 4 for fp32).  A tile with no
-// selected element returns before reading its adapters.
+// zero-padded to the MFMA depth (16 for bf16, 4 for fp32).  Column tiles
+// with no selected element are neither loaded nor computed.
 //
 // Blocks of tensors without an adapter get zeros (k_lora_zero).
 #include <type_traits>
@@ -45,94 +48,169 @@ __device__ inline int find_desc(const LoraDesc* __restrict__ desc, int n, uint32
     return lo;
 }
 
+// A workgroup barrier that orders LDS only: unlike __syncthreads it does not
+// wait for the wave's outstanding global loads and stores.
+__device__ inline void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <int DT>
-__global__ __launch_bounds__(256) void k_lora_tile(const LoraDesc* __restrict__ desc, int n_desc,
+__global__ __launch_bounds__(256) void k_lora_band(const LoraDesc* __restrict__ desc, int n_desc,
                                                    ExpertPtrs ad, OutPtrs dl, const uint32_t* __restrict__ mask,
-                                                   uint32_t block_elems)
+                                                   uint32_t block_elems, int aligned)
 {
     using E = typename std::conditional<DT == 0, float, uint16_t>::type;
-    constexpr int KS = DT == 0 ? 4 : 16;  // MFMA depth
-    constexpr int RS = kMaxLoraRank + 4;  // LDS row stride in elements (breaks bank aliasing, keeps 8 B alignment)
+    constexpr int KS = DT == 0 ? 4 : 16;    // MFMA depth
+    constexpr int CV = 16 / sizeof(E);      // elements per 16-byte chunk
+    constexpr int RS = kMaxLoraRank + 4;    // LDS row stride in elements (breaks bank aliasing, keeps 8 B alignment)
+    constexpr int APT = kMaxLoraRank * kTN / CV / 256;  // A chunks per thread at the largest rank
     __shared__ E As[kTN * RS];  // As[n * RS + k] = A[k][n0 + n]
     __shared__ E Bs[kTM * RS];  // Bs[m * RS + k] = B[m0 + m][k]
+    __shared__ uint32_t flags[2][4];
     const int i = blockIdx.y;
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
     const int d = __builtin_amdgcn_readfirstlane(find_desc(desc, n_desc, blockIdx.x));
     const LoraDesc D = desc[d];
-    const uint32_t q = blockIdx.x - D.tile0;
-    const uint32_t m0 = (q / D.tiles_n) * kTM, n0 = (q % D.tiles_n) * kTN;
+    const uint32_t m0 = (blockIdx.x - D.tile0) * kTM;
     const uint32_t rows = D.rows, cols = D.cols, rank = D.rank;
+    const uint32_t rp = (rank + KS - 1) / KS * KS;
     const uint32_t row = m0 + wave * 16 + (lane & 15);
     const uint32_t cg = 4u * (uint32_t)(lane >> 4);  // the lane's first column inside each 16-column tile
-    // selection of the lane's four-column groups (a group never straddles a
-    // block: block_elems and cols are multiples of 4)
-    uint32_t sel = 0u;
-    if (row < rows) {
-#pragma unroll
-        for (int ct = 0; ct < kCT; ++ct) {
-            const uint32_t col = n0 + ct * 16 + cg;
-            if (col < cols) {
-                const uint32_t e = row * cols + col;  // < numel < 2^32
-                const uint32_t g = D.g0 + e / block_elems;
-                if (mask == nullptr || ((mask[g] >> i) & 1u))
-                    sel |= 1u << ct;
-            }
-        }
-    }
-    if (!__syncthreads_or(sel != 0u))
-        return;
-    const uint32_t rp = (rank + KS - 1) / KS * KS;
     const E* __restrict__ A = static_cast<const E*>(ad.p[i]) + D.a_off;
     const E* __restrict__ B = static_cast<const E*>(ad.p[i]) + D.b_off;
-    for (uint32_t x = t; x < rp * kTN; x += 256) {  // coalesced along A's columns
-        const uint32_t k = x / kTN, n = x % kTN;
-        As[n * RS + k] = (k < rank && n0 + n < cols) ? A[(uint64_t)k * cols + n0 + n] : E(0);
-    }
+    E* __restrict__ out = static_cast<E*>(dl.p[i]) + D.toff;
+    const bool vec = D.vec != 0u && aligned != 0;  // A's rows are 16-byte aligned: chunked loads
+    // the band's B rows, once
     for (uint32_t x = t; x < rp * kTM; x += 256) {  // B's rows m0.. are contiguous
         const uint32_t m = x / rp, k = x % rp;
         Bs[m * RS + k] = (k < rank && m0 + m < rows) ? B[(uint64_t)(m0 + m) * rank + k] : E(0);
     }
-    __syncthreads();
+    // A chunk c of a column tile: depth k = c / (kTN / CV), columns n = (c % (kTN / CV)) * CV ..
+    auto load_a = [&](uint32_t n0, uint4 (&ra)[APT]) {
+#pragma unroll
+        for (int j = 0; j < APT; ++j) {
+            const uint32_t c = (uint32_t)(j * 256 + t);
+            const uint32_t k = c / (kTN / CV), n = (c % (kTN / CV)) * CV;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (k < rank && n0 + n < cols) {
+                const E* src = A + (uint64_t)k * cols + n0 + n;
+                if (vec) {
+                    v = *reinterpret_cast<const uint4*>(src);
+                } else {
+                    E tmp[CV];
+#pragma unroll
+                    for (int q = 0; q < CV; ++q)
+                        tmp[q] = (n0 + n + q < cols) ? src[q] : E(0);
+                    v = *reinterpret_cast<const uint4*>(tmp);
+                }
+            }
+            ra[j] = v;
+        }
+    };
+    auto store_a = [&](const uint4 (&ra)[APT]) {
+#pragma unroll
+        for (int j = 0; j < APT; ++j) {
+            const uint32_t c = (uint32_t)(j * 256 + t);
+            const uint32_t k = c / (kTN / CV), n = (c % (kTN / CV)) * CV;
+            if (k < rp) {
+                const E* v = reinterpret_cast<const E*>(&ra[j]);
+#pragma unroll
+                for (int q = 0; q < CV; ++q)
+                    As[(n + q) * RS + k] = v[q];
+            }
+        }
+    };
+    auto selection = [&](uint32_t n0) {
+        uint32_t sel = 0u;
+        if (row < rows) {
+#pragma unroll
+            for (int ct = 0; ct < kCT; ++ct) {
+                const uint32_t col = n0 + ct * 16 + cg;
+                if (col < cols) {
+                    const uint32_t e = row * cols + col;  // < numel < 2^32
+                    if (mask == nullptr || ((mask[D.g0 + e / block_elems] >> i) & 1u))
+                        sel |= 1u << ct;
+                }
+            }
+        }
+        return sel;
+    };
+    // workgroup "any lane selected" through LDS, one flag word per wave,
+    // double-buffered so that a flag is rewritten only two barriers later
+    auto any_selected = [&](uint32_t sel, int parity) {
+        const bool w = __ballot(sel != 0u) != 0ull;
+        if (lane == 0)
+            flags[parity][wave] = w ? 1u : 0u;
+        lds_barrier();
+        return (flags[parity][0] | flags[parity][1] | flags[parity][2] | flags[parity][3]) != 0u;
+    };
     const int mr = wave * 16 + (lane & 15);  // the B operand row (an output row)
-    float4_t acc[kCT];
-#pragma unroll
-    for (int ct = 0; ct < kCT; ++ct)
-        acc[ct] = float4_t{0.f, 0.f, 0.f, 0.f};
-    for (uint32_t k0 = 0; k0 < rp; k0 += KS) {
-        if constexpr (DT == 1) {
-            const uint32_t kk = k0 + cg;  // lanes 16j.. hold depth 4j..4j+3
-            const short4_t b = *reinterpret_cast<const short4_t*>(&Bs[mr * RS + kk]);
-#pragma unroll
-            for (int ct = 0; ct < kCT; ++ct) {
-                const short4_t a = *reinterpret_cast<const short4_t*>(&As[(ct * 16 + (lane & 15)) * RS + kk]);
-                acc[ct] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, acc[ct], 0, 0, 0);
-            }
-        } else {
-            const uint32_t kk = k0 + (uint32_t)(lane >> 4);  // lanes 16j.. hold depth j
-            const float b = Bs[mr * RS + kk];
-#pragma unroll
-            for (int ct = 0; ct < kCT; ++ct) {
-                const float a = As[(ct * 16 + (lane & 15)) * RS + kk];
-                acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[ct], 0, 0, 0);
-            }
-        }
-    }
-    // accumulator j of tile ct is output (row, n0 + ct*16 + cg + j)
     const float scale = D.scale;
-    E* __restrict__ out = static_cast<E*>(dl.p[i]) + D.toff;
-#pragma unroll
-    for (int ct = 0; ct < kCT; ++ct) {
-        if (!((sel >> ct) & 1u))
-            continue;
-        const uint64_t e = (uint64_t)row * cols + n0 + ct * 16 + cg;
-        const float y0 = scale * acc[ct][0], y1 = scale * acc[ct][1];
-        const float y2 = scale * acc[ct][2], y3 = scale * acc[ct][3];
-        if constexpr (DT == 1) {
-            *reinterpret_cast<uint2*>(out + e) = make_uint2(Fmt<1>::pack2(y0, y1), Fmt<1>::pack2(y2, y3));
-        } else {
-            *reinterpret_cast<float4*>(out + e) = make_float4(y0, y1, y2, y3);
+    uint4 ra[APT];
+    uint32_t sel = selection(0);
+    load_a(0, ra);
+    bool any = any_selected(sel, 0);  // also orders the B staging before its first use
+    for (uint32_t tn = 0; tn < D.tiles_n; ++tn) {
+        const uint32_t n0 = tn * kTN, n1 = n0 + kTN;
+        const bool more = tn + 1 < D.tiles_n;
+        if (any) {
+            store_a(ra);
+            lds_barrier();
         }
+        // the next tile's mask words and A chunks are issued before this
+        // tile's stores, so waiting for them never waits for the stores
+        const uint32_t sel_next = more ? selection(n1) : 0u;
+        if (any) {
+            float4_t acc[kCT];
+#pragma unroll
+            for (int ct = 0; ct < kCT; ++ct)
+                acc[ct] = float4_t{0.f, 0.f, 0.f, 0.f};
+            for (uint32_t k0 = 0; k0 < rp; k0 += KS) {
+                if constexpr (DT == 1) {
+                    const uint32_t kk = k0 + cg;  // lanes 16j.. hold depth 4j..4j+3
+                    const short4_t b = *reinterpret_cast<const short4_t*>(&Bs[mr * RS + kk]);
+#pragma unroll
+                    for (int ct = 0; ct < kCT; ++ct) {
+                        const short4_t a =
+                            *reinterpret_cast<const short4_t*>(&As[(ct * 16 + (lane & 15)) * RS + kk]);
+                        acc[ct] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, acc[ct], 0, 0, 0);
+                    }
+                } else {
+                    const uint32_t kk = k0 + (uint32_t)(lane >> 4);  // lanes 16j.. hold depth j
+                    const float b = Bs[mr * RS + kk];
+#pragma unroll
+                    for (int ct = 0; ct < kCT; ++ct) {
+                        const float a = As[(ct * 16 + (lane & 15)) * RS + kk];
+                        acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[ct], 0, 0, 0);
+                    }
+                }
+            }
+            if (more)
+                load_a(n1, ra);
+            // accumulator j of tile ct is output (row, n0 + ct*16 + cg + j)
+#pragma unroll
+            for (int ct = 0; ct < kCT; ++ct) {
+                if (!((sel >> ct) & 1u))
+                    continue;
+                const uint64_t e = (uint64_t)row * cols + n0 + ct * 16 + cg;
+                const float y0 = scale * acc[ct][0], y1 = scale * acc[ct][1];
+                const float y2 = scale * acc[ct][2], y3 = scale * acc[ct][3];
+                if constexpr (DT == 1) {
+                    *reinterpret_cast<uint2*>(out + e) = make_uint2(Fmt<1>::pack2(y0, y1), Fmt<1>::pack2(y2, y3));
+                } else {
+                    *reinterpret_cast<float4*>(out + e) = make_float4(y0, y1, y2, y3);
+                }
+            }
+        } else if (more) {
+            load_a(n1, ra);
+        }
+        // this barrier also ends every wave's reads of As for this tile
+        any = any_selected(sel_next, (int)((tn + 1) & 1u));
+        sel = sel_next;
     }
 }
 
@@ -154,10 +232,10 @@ __global__ __launch_bounds__(256) void k_lora_zero(const uint32_t* __restrict__ 
 
 }  // namespace
 
-uint32_t lora_tiles(uint32_t rows, uint32_t cols, uint32_t* tiles_n)
+uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n)
 {
     *tiles_n = (cols + kTN - 1) / kTN;
-    return ((rows + kTM - 1) / kTM) * *tiles_n;
+    return (rows + kTM - 1) / kTM;
 }
 
 hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& dl, int K,
@@ -165,12 +243,17 @@ hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPt
 {
     if (lt.n_tiles > 0) {
         const dim3 grid((unsigned)lt.n_tiles, (unsigned)K);
+        const uint32_t be = (uint32_t)bt.block_elems;
+        int aligned = 1;  // every adapter buffer starts 16-byte aligned
+        for (int i = 0; i < K; ++i)
+            if (reinterpret_cast<uintptr_t>(ad.p[i]) % 16 != 0)
+                aligned = 0;
         if (bt.dtype == 0)
-            hipLaunchKernelGGL(k_lora_tile<0>, grid, dim3(256), 0, s, lt.d_desc, lt.n_desc, ad, dl, mask,
-                               (uint32_t)bt.block_elems);
+            hipLaunchKernelGGL(k_lora_band<0>, grid, dim3(256), 0, s, lt.d_desc, lt.n_desc, ad, dl, mask, be,
+                               aligned);
         else
-            hipLaunchKernelGGL(k_lora_tile<1>, grid, dim3(256), 0, s, lt.d_desc, lt.n_desc, ad, dl, mask,
-                               (uint32_t)bt.block_elems);
+            hipLaunchKernelGGL(k_lora_band<1>, grid, dim3(256), 0, s, lt.d_desc, lt.n_desc, ad, dl, mask, be,
+                               aligned);
     }
     if (lt.n_zero > 0)
         hipLaunchKernelGGL(k_lora_zero, dim3((unsigned)lt.n_zero, (unsigned)K), dim3(256), 0, s, lt.d_zero,

@@ -105,30 +105,30 @@ struct OutPtrs {
     void* p[kMaxK];
 };
 
-// One adapted tensor on the device; its output tiles are tile0 ..
-// tile0 + tiles_m * tiles_n - 1 of the launch (row-major over the tile grid).
+// One adapted tensor on the device; its 64-row bands are workgroups
+// tile0 .. tile0 + ceil(rows / 64) - 1 of the launch.
 struct LoraDesc {
     uint64_t toff;  // element offset of the tensor in a checkpoint
     uint64_t a_off, b_off;  // element offsets of A and B in an adapter buffer
     uint32_t rows, cols, rank;
     float scale;
     uint32_t g0;  // the tensor's first block
-    uint32_t tiles_n;
+    uint32_t tiles_n;  // 128-column tiles per band
     uint32_t tile0;
-    uint32_t pad;
+    uint32_t vec;  // every row of A starts 16-byte aligned (relative to the adapter buffer)
 };
 
 // A validated set of adapter records for a layout, cached per device.
 struct LoraTable {
     LoraDesc* d_desc = nullptr;  // sorted by tile0
     int n_desc = 0;
-    uint32_t n_tiles = 0;
+    uint32_t n_tiles = 0;  // row bands (workgroups per expert)
     uint32_t* d_zero = nullptr;  // blocks of tensors without an adapter
     uint32_t n_zero = 0;
 };
 
-// Tiles of a rows x cols tensor; *tiles_n receives the tiles per tile row.
-uint32_t lora_tiles(uint32_t rows, uint32_t cols, uint32_t* tiles_n);
+// Row bands of a rows x cols tensor; *tiles_n receives the column tiles per band.
+uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n);
 
 // Writes the selected units' deltas (all units when mask is null).
 hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& dl, int K,

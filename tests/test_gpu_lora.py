@@ -36,10 +36,11 @@ def _say(*a):
 
 
 def _awkward(dtype, be=512):
-    """Adapted matrices with rows and columns off the 64 x 128 tile grid,
-    blocks that cut rows, and tensors without an adapter in between."""
+    """Adapted matrices with rows and columns off the 64 x 128 tile grid
+    (44 columns: rows of A not 16-byte aligned in bf16), blocks that cut
+    rows, and tensors without an adapter in between."""
     t = (("w0", (200, 136)), ("v0", (64,)), ("w1", (130, 264)), ("w2", (96, 8)), ("v1", (520,)),
-         ("w3", (72, 1000)), ("w4", (64, 128)), ("e", (40, 48)))
+         ("w3", (72, 1000)), ("w4", (64, 128)), ("e", (40, 48)), ("w5", (30, 44)))
     return FamilySpec("awkward", t, dtype, be, 3, ())
 
 
@@ -88,7 +89,7 @@ def _materialize(mp, spec, recs, ads_np, mask_np=None, prefill=True):
 def test_lora_materialize_exact_grid_bitwise(mp, dtype, rank):
     spec = _awkward(dtype)
     lay = spec.layout
-    recs, n = lora_records(spec, rank, 0.5, targets=("w0", "w1", "w2", "w3", "w4"))
+    recs, n = lora_records(spec, rank, 0.5, targets=("w0", "w1", "w2", "w3", "w4", "w5"))
     ads = make_lora_adapters(n, 3, dtype, seed=rank, grid=True)
     blocks = oracle.Blocks(lay.numel, lay.block_elems)
     rng = np.random.default_rng(rank)
@@ -97,6 +98,26 @@ def test_lora_materialize_exact_grid_bitwise(mp, dtype, rank):
         _, outs = _materialize(mp, spec, recs, ads, mask)
         fill = [_sentinel(lay.n_params, dtype, i) for i in range(3)]
         want = oracle.lora_materialize(blocks, dtype, lay.numel, recs, ads, mask=mask, fill=fill)
+        for i in range(3):
+            got = to_host(outs[i])
+            assert np.array_equal(got, want[i]), f"expert {i}: {int((got != want[i]).sum())} elements differ"
+
+
+@pytest.mark.parametrize("rank", [8, 16, 64])
+def test_lora_materialize_exact_grid_bitwise_aligned_rows(mp, rank):
+    # bf16 with every row of A 16-byte aligned: the 16-byte loads of A
+    spec = _awkward("bf16")
+    lay = spec.layout
+    recs, n = lora_records(spec, rank, 0.5, targets=("w0", "w1", "w2", "w3", "w4"))
+    assert all(r[4] % 8 == 0 and r[2] % 8 == 0 for r in recs)
+    ads = make_lora_adapters(n, 3, "bf16", seed=rank + 1, grid=True)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    rng = np.random.default_rng(rank + 1)
+    for mask in (None, rng.integers(0, 8, blocks.G).astype(np.uint32), np.zeros(blocks.G, np.uint32)):
+        _say(f"case lora exact aligned rank={rank} mask={'all' if mask is None else int(mask.sum())}")
+        _, outs = _materialize(mp, spec, recs, ads, mask)
+        fill = [_sentinel(lay.n_params, "bf16", i) for i in range(3)]
+        want = oracle.lora_materialize(blocks, "bf16", lay.numel, recs, ads, mask=mask, fill=fill)
         for i in range(3):
             got = to_host(outs[i])
             assert np.array_equal(got, want[i]), f"expert {i}: {int((got != want[i]).sum())} elements differ"

@@ -178,6 +178,8 @@ CONFIGS = {
                                     budgets=(1.0, 0.9, 0.8, 0.7, 0.6, 0.5), residency="device"),
     "qwen2.5-1.5b-ties-tensor": dict(family="qwen2.5-1.5b", op="ties_tensor", density=0.2, lam=1.0,
                                      budgets=(0.25, 0.5, 1.0), residency="device"),
+    "qwen2.5-1.5b-lora-ties": dict(family="qwen2.5-1.5b", op="lora_ties", rank=16, scale=2.0, density=0.2,
+                                   lam=1.0, budgets=(0.25, 0.5, 1.0), residency="device"),
     "qwen2.5-1.5b-avg-renorm": dict(family="qwen2.5-1.5b", op="avg_renorm", budgets=(0.25, 0.5, 1.0),
                                     residency="device"),
     "llama3-8b": dict(family="llama3-8b", op="avg", budgets=tuple(x / 10 for x in range(1, 11)),
