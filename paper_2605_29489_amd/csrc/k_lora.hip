@@ -13,7 +13,9 @@
 //   MFMA rows    = output columns (operand from A)
 //   MFMA columns = output rows    (operand from B)
 // so that a lane's four accumulators are four consecutive columns of one
-// output row: one 8-byte (bf16) or 16-byte (fp32) store each.  The rank is
+// output row: one 16-byte store each in fp32; in bf16 (columns a multiple of
+// 8) the wave passes its rows through LDS so that lanes store 16 contiguous
+// bytes and each store instruction writes whole row segments.  The rank is
 // zero-padded to the MFMA depth (16 for bf16, 4 for fp32).  Column tiles
 // with no selected element are neither loaded nor computed.
 //
@@ -58,7 +60,7 @@ __device__ inline void lds_barrier()
 }
 
 template <int DT>
-__global__ __launch_bounds__(256) void k_lora_band(const LoraDesc* __restrict__ desc, int n_desc,
+__global__ __launch_bounds__(256, DT == 1 ? 4 : 2) void k_lora_band(const LoraDesc* __restrict__ desc, int n_desc,
                                                    ExpertPtrs ad, OutPtrs dl, const uint32_t* __restrict__ mask,
                                                    uint32_t block_elems, int aligned)
 {
@@ -69,6 +71,8 @@ __global__ __launch_bounds__(256) void k_lora_band(const LoraDesc* __restrict__ 
     constexpr int APT = kMaxLoraRank * kTN / CV / 256;  // A chunks per thread at the largest rank
     __shared__ E As[kTN * RS];  // As[n * RS + k] = A[k][n0 + n]
     __shared__ E Bs[kTM * RS];  // Bs[m * RS + k] = B[m0 + m][k]
+    constexpr int OS = kTN / 2 + 8;  // bf16 output strip row stride (16-byte aligned rows)
+    __shared__ uint16_t Os[DT == 1 ? kTM * OS : 8];
     __shared__ uint32_t flags[2][4];
     const int i = blockIdx.y;
     const int t = threadIdx.x, lane = t & 63;
@@ -126,14 +130,25 @@ __global__ __launch_bounds__(256) void k_lora_band(const LoraDesc* __restrict__ 
     };
     auto selection = [&](uint32_t n0) {
         uint32_t sel = 0u;
-        if (row < rows) {
+        const uint32_t c0 = n0 + cg;
+        if (row < rows && c0 < cols) {
+            // the lane's groups lie in one row, within 116 columns: at most two
+            // blocks when blocks are at least that long (one or two mask words)
+            const uint32_t last = min(n0 + (kCT - 1) * 16 + cg, (cols - 1) & ~3u);
+            const uint32_t e0 = row * cols + c0;  // < numel < 2^32
+            const uint32_t b0 = e0 / block_elems, b1 = (row * cols + last) / block_elems;
+            const bool two = block_elems >= 116u;
+            const uint32_t w0 = mask != nullptr && two ? mask[D.g0 + b0] : 0u;
+            const uint32_t w1 = mask != nullptr && two && b1 != b0 ? mask[D.g0 + b1] : w0;
 #pragma unroll
             for (int ct = 0; ct < kCT; ++ct) {
-                const uint32_t col = n0 + ct * 16 + cg;
+                const uint32_t col = c0 + ct * 16;
                 if (col < cols) {
-                    const uint32_t e = row * cols + col;  // < numel < 2^32
-                    if (mask == nullptr || ((mask[D.g0 + e / block_elems] >> i) & 1u))
-                        sel |= 1u << ct;
+                    const uint32_t b = (row * cols + col) / block_elems;
+                    const uint32_t w = mask == nullptr ? 0xffffffffu
+                                       : two          ? (b == b0 ? w0 : w1)
+                                                      : mask[D.g0 + b];
+                    sel |= ((w >> i) & 1u) << ct;
                 }
             }
         }
@@ -192,18 +207,58 @@ __global__ __launch_bounds__(256) void k_lora_band(const LoraDesc* __restrict__ 
             if (more)
                 load_a(n1, ra);
             // accumulator j of tile ct is output (row, n0 + ct*16 + cg + j)
+            auto direct_store = [&]() {
 #pragma unroll
-            for (int ct = 0; ct < kCT; ++ct) {
-                if (!((sel >> ct) & 1u))
-                    continue;
-                const uint64_t e = (uint64_t)row * cols + n0 + ct * 16 + cg;
-                const float y0 = scale * acc[ct][0], y1 = scale * acc[ct][1];
-                const float y2 = scale * acc[ct][2], y3 = scale * acc[ct][3];
-                if constexpr (DT == 1) {
-                    *reinterpret_cast<uint2*>(out + e) = make_uint2(Fmt<1>::pack2(y0, y1), Fmt<1>::pack2(y2, y3));
-                } else {
-                    *reinterpret_cast<float4*>(out + e) = make_float4(y0, y1, y2, y3);
+                for (int ct = 0; ct < kCT; ++ct) {
+                    if (!((sel >> ct) & 1u))
+                        continue;
+                    const uint64_t e = (uint64_t)row * cols + n0 + ct * 16 + cg;
+                    const float y0 = scale * acc[ct][0], y1 = scale * acc[ct][1];
+                    const float y2 = scale * acc[ct][2], y3 = scale * acc[ct][3];
+                    if constexpr (DT == 1) {
+                        *reinterpret_cast<uint2*>(out + e) =
+                            make_uint2(Fmt<1>::pack2(y0, y1), Fmt<1>::pack2(y2, y3));
+                    } else {
+                        *reinterpret_cast<float4*>(out + e) = make_float4(y0, y1, y2, y3);
+                    }
                 }
+            };
+            if constexpr (DT == 1) {
+                if ((cols & 7u) == 0u) {
+                    // bf16 rows through the wave's own LDS strip, 64 columns at a
+                    // time: each lane then stores 16 contiguous bytes and a store
+                    // instruction writes 8 whole 128-byte row segments.  Only this
+                    // wave touches its strip; its LDS operations run in order.
+                    uint16_t* ow = &Os[wave * 16 * OS];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+                        for (int q = 0; q < kCT / 2; ++q) {
+                            const int ct = h * (kCT / 2) + q;
+                            const float y0 = scale * acc[ct][0], y1 = scale * acc[ct][1];
+                            const float y2 = scale * acc[ct][2], y3 = scale * acc[ct][3];
+                            *reinterpret_cast<uint2*>(&ow[(lane & 15) * OS + q * 16 + cg]) =
+                                make_uint2(Fmt<1>::pack2(y0, y1), Fmt<1>::pack2(y2, y3));
+                        }
+#pragma unroll
+                        for (int it = 0; it < 2; ++it) {
+                            const int c = it * 64 + lane;  // 16 rows x 8 chunks of 8 columns
+                            const int r = c >> 3, cc = (c & 7) * 8;
+                            // the chunk's selection is the bit of its first four-column
+                            // group, held by the lane of row r and that group (a chunk
+                            // never straddles a block or the row end)
+                            const uint32_t so = (uint32_t)__shfl((int)sel, r + 16 * ((cc & 15) >> 2));
+                            if ((so >> (h * (kCT / 2) + (cc >> 4))) & 1u) {
+                                const uint32_t e = (m0 + wave * 16 + r) * cols + n0 + h * 64 + cc;
+                                *reinterpret_cast<uint4*>(out + e) = *reinterpret_cast<const uint4*>(&ow[r * OS + cc]);
+                            }
+                        }
+                    }
+                } else {
+                    direct_store();
+                }
+            } else {
+                direct_store();
             }
         } else if (more) {
             load_a(n1, ra);

@@ -124,6 +124,26 @@ def test_lora_materialize_exact_grid_bitwise_aligned_rows(mp, rank):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("be", [8, 64, 112, 120])
+def test_lora_materialize_short_blocks_bitwise(mp, dtype, be):
+    # blocks shorter than a lane's 116-column span (several blocks per lane
+    # and tile row) and just above it
+    spec = _awkward(dtype, be=be)
+    lay = spec.layout
+    recs, n = lora_records(spec, 16, 0.5, targets=("w0", "w1", "w3", "w4"))
+    ads = make_lora_adapters(n, 3, dtype, seed=be, grid=True)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    mask = np.random.default_rng(be).integers(0, 8, blocks.G).astype(np.uint32)
+    _say(f"case lora short blocks {dtype} be={be} G={blocks.G}")
+    _, outs = _materialize(mp, spec, recs, ads, mask)
+    fill = [_sentinel(lay.n_params, dtype, i) for i in range(3)]
+    want = oracle.lora_materialize(blocks, dtype, lay.numel, recs, ads, mask=mask, fill=fill)
+    for i in range(3):
+        got = to_host(outs[i])
+        assert np.array_equal(got, want[i]), f"expert {i}: {int((got != want[i]).sum())} elements differ"
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("rank", [16, 64])
 def test_lora_materialize_normal_adapters_within_bound(mp, dtype, rank):
     spec = _awkward(dtype)
