@@ -187,6 +187,47 @@ def write_expert_files(exps, P):
     return paths, drop
 
 
+def cpu_baseline_lora(spec, recs, ads_np, base, cfg, n_layers=5):
+    """Time the oracle on the whole LoRA step for the adapted tensors of the
+    first n_layers layers (a bounded sample): pull every unit, index, then per
+    budget plan, pull the selected units and merge."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    lay = spec.layout
+    K = len(ads_np)
+    toff = np.concatenate([[0], np.cumsum(lay.numel)]).astype(np.int64)
+    names = [n for n, _ in spec.tensors]
+    pick = [r for r in recs if names[r[0]].startswith(tuple(f"layers.{l}." for l in range(n_layers)))]
+    numel = [r[1] * r[2] for r in pick]
+    sub = oracle.Blocks(numel, lay.block_elems)
+    b_np = np.concatenate([base[int(toff[r[0]]):int(toff[r[0]]) + r[1] * r[2]].view(torch.int16).cpu().numpy()
+                           .view(np.uint16) for r in pick])
+    sub_recs = [(j,) + tuple(r[1:]) for j, r in enumerate(pick)]  # tensor ids of the sub-layout
+    nparams = int(sum(numel))
+    full = nparams * 2 * K
+    t0 = time.perf_counter()
+    d_all = oracle.lora_materialize(sub, lay.dtype, numel, sub_recs, ads_np)
+    S = oracle.index(sub, lay.dtype, b_np, d_all, delta=True).reshape(-1)
+    for f in cfg["budgets"]:
+        mask, _ = oracle.plan(sub, lay.dtype, K, S, [1.0] * K, int(f * full), flags=2)
+        d = oracle.lora_materialize(sub, lay.dtype, numel, sub_recs, ads_np, mask=mask)
+        oracle.merge_ties(sub, lay.dtype, b_np, d, mask, cfg["density"], cfg["lam"], delta=True)
+    dt = time.perf_counter() - t0
+    return {
+        "value": len(cfg["budgets"]) * nparams / dt,
+        "unit": "params/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"the {len(pick)} adapted tensors of layers 0-{n_layers - 1} ({nparams} params, all {K} experts): "
+                  f"pull of every unit + "
+                  f"index + per budget (B=25/50/100% of the sample's expert bytes) plan, pull of the selected "
+                  f"units and TIES; {dt:.2f} s",
+    }
+
+
 def run_lora(args):
     """Experts given as low-rank adapters: the catalog materialises every
     expert's deltas once and indexes them; each budget then plans, pulls only
@@ -215,7 +256,8 @@ def run_lora(args):
     base, _ = make_family_device(spec, K=1, seed=0, device="cuda")
     tdt = torch.bfloat16 if lay.dtype == "bf16" else torch.float32
     ads = []
-    for a in make_lora_adapters(n_ad, K, lay.dtype, seed=0, std=0.02):
+    ads_np = make_lora_adapters(n_ad, K, lay.dtype, seed=0, std=0.02)
+    for a in ads_np:
         t = torch.from_numpy(a.view(np.int16) if lay.dtype == "bf16" else a).cuda()
         ads.append(t.view(tdt) if lay.dtype == "bf16" else t)
     deltas = [torch.empty(P, dtype=tdt, device="cuda") for _ in range(K)]
@@ -279,6 +321,9 @@ def run_lora(args):
                      "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": None},
         "breakdown": {"pull_all_ms": round(pull_all_ms, 4), "index_ms": round(idx_ms, 4), "per_budget": rows},
     }
+    if not args.no_cpu_baseline and lay.dtype == "bf16":
+        log("timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline_lora(spec, recs, ads_np, base, cfg)
     print(json.dumps(result), flush=True)
 
 

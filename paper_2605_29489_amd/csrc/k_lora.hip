@@ -36,7 +36,7 @@ constexpr int kCT = kTN / 16;
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
-// The tile's descriptor: the last entry with tile0 <= x (wave-uniform search).
+// The band's descriptor: the last entry with tile0 <= x (wave-uniform search).
 __device__ inline int find_desc(const LoraDesc* __restrict__ desc, int n, uint32_t x)
 {
     int lo = 0, hi = n - 1;
@@ -69,10 +69,10 @@ __global__ __launch_bounds__(256, DT == 1 ? 4 : 2) void k_lora_band(const LoraDe
     constexpr int CV = 16 / sizeof(E);      // elements per 16-byte chunk
     constexpr int RS = kMaxLoraRank + 4;    // LDS row stride in elements (breaks bank aliasing, keeps 8 B alignment)
     constexpr int APT = kMaxLoraRank * kTN / CV / 256;  // A chunks per thread at the largest rank
-    __shared__ E As[kTN * RS];  // As[n * RS + k] = A[k][n0 + n]
-    __shared__ E Bs[kTM * RS];  // Bs[m * RS + k] = B[m0 + m][k]
+    __shared__ __align__(16) E As[kTN * RS];  // As[n * RS + k] = A[k][n0 + n]
+    __shared__ __align__(16) E Bs[kTM * RS];  // Bs[m * RS + k] = B[m0 + m][k]
     constexpr int OS = kTN / 2 + 8;  // bf16 output strip row stride (16-byte aligned rows)
-    __shared__ uint16_t Os[DT == 1 ? kTM * OS : 8];
+    __shared__ __align__(16) uint16_t Os[DT == 1 ? kTM * OS : 8];  // vector reads and writes
     __shared__ uint32_t flags[2][4];
     const int i = blockIdx.y;
     const int t = threadIdx.x, lane = t & 63;
