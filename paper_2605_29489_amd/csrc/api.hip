@@ -890,13 +890,15 @@ static int validate_loras(const mp_layout* L, const mp_lora_tensor* loras, int32
         if (x.rank < 1 || x.rank > kMaxLoraRank)
             return fail(MP_E_ARG, "loras[%d].rank = %d must be in [1, %d]", r, x.rank, kMaxLoraRank);
         const int64_t n = L->numel[x.tensor];
-        if (x.rows < 1 || x.cols < 1 || x.cols % 4 != 0 || x.rows > n || x.rows * x.cols != n)
+        // rows * cols == n without forming the product (no overflow)
+        if (x.rows < 1 || x.cols < 1 || x.cols % 4 != 0 || n % x.rows != 0 || n / x.rows != x.cols)
             return fail(MP_E_ARG, "loras[%d]: %lld x %lld does not shape tensor %d (%lld elements; cols a multiple of 4)",
                         r, (long long)x.rows, (long long)x.cols, x.tensor, (long long)n);
         if (n >= ((int64_t)1 << 32))
             return fail(MP_E_UNSUPPORTED, "loras[%d]: tensor %d has 2^32 or more elements", r, x.tensor);
-        if (x.a_off < 0 || x.b_off < 0 || !std::isfinite(x.scale))
-            return fail(MP_E_ARG, "loras[%d]: negative offset or non-finite scale", r);
+        if (x.a_off < 0 || x.b_off < 0 || x.a_off > ((int64_t)1 << 48) || x.b_off > ((int64_t)1 << 48) ||
+            !std::isfinite(x.scale))
+            return fail(MP_E_ARG, "loras[%d]: offset outside [0, 2^48] or non-finite scale", r);
         *need = std::max(*need, std::max(x.a_off + (int64_t)x.rank * x.cols, x.b_off + x.rows * (int64_t)x.rank));
     }
     return MP_OK;
@@ -915,7 +917,13 @@ static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lor
     for (int32_t r = 0; r < n_lora; ++r)
         adapted[(size_t)loras[r].tensor] = 1;
     std::string key = layout_key(bt.device, L);
-    key.append(reinterpret_cast<const char*>(loras), sizeof(mp_lora_tensor) * (size_t)n_lora);
+    for (int32_t r = 0; r < n_lora; ++r) {  // field by field: the struct's padding bytes are not part of it
+        const mp_lora_tensor& x = loras[r];
+        uint32_t sc = 0;
+        std::memcpy(&sc, &x.scale, sizeof sc);
+        const int64_t f[7] = {x.tensor, x.rank, x.rows, x.cols, x.a_off, x.b_off, (int64_t)sc};
+        key.append(reinterpret_cast<const char*>(f), sizeof f);
+    }
     auto it = g_loras.find(key);
     if (it != g_loras.end()) {
         *out = &it->second->t;

@@ -66,6 +66,8 @@ def test_lora_records_rejected_before_any_device_work(mp):
         [(1, 4, 128, 4, 0, 0, 1.0), (0, 4, 64, 96, -1, 0, 1.0)],  # negative offset
         [(0, 4, 64, 96, 0, 0, float("inf"))],    # non-finite scale
         [(1, 4, 256, 2, 0, 0, 1.0)],             # cols not a multiple of 4
+        [(0, 4, 1 << 40, 1 << 40, 0, 0, 1.0)],   # a product that overflows int64
+        [(0, 4, 64, 96, 1 << 50, 0, 1.0)],       # offset beyond 2^48
     ]
     for recs in bad:
         assert rc(recs) == mp.MP_E_ARG, recs
