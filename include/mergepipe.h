@@ -269,7 +269,9 @@ int mp_merge_dare(const mp_layout* layout, const void* base,
  * rows x cols row-major matrix (rows * cols = its numel), has the delta
  * scale * B A, with A (rank x cols) and B (rows x rank) row-major in the
  * layout's dtype at element offsets a_off and b_off of each expert's
- * adapter buffer.  1 <= rank <= 64; cols a multiple of 4; numel < 2^32. */
+ * adapter buffer.  1 <= rank <= 64; cols a multiple of 4; numel < 2^32;
+ * 0 <= a_off, b_off <= 2^48; scale finite; each tensor at most once.
+ * Zero-initialise the struct (its tail padding is ignored either way). */
 typedef struct mp_lora_tensor {
     int32_t tensor;
     int32_t rank;
@@ -291,10 +293,16 @@ typedef struct mp_lora_tensor {
  * Tensors without a record get zeros.  Elements of unselected units are not
  * written.  adapters: HOST array of K device pointers (each at least the
  * largest a_off + rank*cols, b_off + rows*rank elements; the array may be
- * NULL when n_lora = 0); deltas: HOST array of K device checkpoints, disjoint from
- * each other and from the adapters; mask: device uint32[G] or NULL.
- * Records are validated and their device table is cached per (device,
- * layout, records).  Asynchronous on `stream`. */
+ * NULL when n_lora = 0); deltas: HOST array of K device checkpoints,
+ * disjoint from each other and from the adapters; mask: device uint32[G]
+ * or NULL.  The caller owns every buffer; the library reads the adapters
+ * and the mask and writes only the named elements of deltas.  Errors:
+ * MP_E_ARG for an invalid layout, K, record, NULL array, undersized or
+ * non-device buffer, or overlap (checked before anything is enqueued);
+ * MP_E_UNSUPPORTED for tensors of 2^32 or more elements; MP_E_NOMEM or
+ * MP_E_HIP from the table upload or the launch.  Records are validated and
+ * their device table is cached per (device, layout, records) until
+ * mp_release.  Asynchronous on `stream`. */
 int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, int32_t n_lora,
                         const void* const* adapters, int32_t K, const uint32_t* mask,
                         void* const* deltas, void* stream);
