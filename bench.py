@@ -327,6 +327,64 @@ def run_lora(args):
     print(json.dumps(result), flush=True)
 
 
+def cpu_baseline_sweep(spec, base, exps, cfg, flags, dl, target_elems=100_000_000):
+    """Time the oracle on a sweep workload: index, then per budget plan and
+    merge, over every n-th block (a bounded sample of about target_elems
+    expert elements in all).  None for ops the sample cannot express
+    (tensor-scope thresholds need whole tensors)."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    op = cfg["op"]
+    if op not in ("avg", "avg_renorm", "ties", "dare"):
+        return None
+    lay = spec.layout
+    blk = oracle.Blocks(lay.numel, lay.block_elems)
+    stride = max(1, lay.n_params * len(exps) // target_elems)
+    ids = np.arange(0, blk.G, stride)
+    idx = torch.from_numpy(np.concatenate([np.arange(blk.off[g], blk.off[g] + blk.len[g]) for g in ids]))
+
+    def host(t):
+        x = t[idx.to(t.device)]
+        return x.view(torch.int16).cpu().numpy().view(np.uint16) if x.dtype == torch.bfloat16 else x.cpu().numpy()
+
+    b_np = host(base)
+    e_np = [host(e) for e in exps]
+    doff = np.concatenate([[0], np.cumsum(blk.len[ids])[:-1]]).astype(np.int64)
+    sub = oracle.Blocks([int(n) for n in blk.len[ids]], lay.block_elems)
+    K = len(exps)
+    nparams = int(blk.len[ids].sum())
+    full = nparams * lay.elem_bytes * K
+    w = [1.0 / K] * K if op in ("avg", "avg_renorm") else [1.0] * K
+    dt_name = lay.dtype
+    t0 = time.perf_counter()
+    S = oracle.index(blk, dt_name, b_np, e_np, doff=doff, ids=ids, delta=dl).reshape(-1)
+    for f in cfg["budgets"]:
+        mask, _ = oracle.plan(sub, dt_name, K, S, w, int(f * full), flags=flags)
+        kw = dict(ids=ids, doff=doff, delta=dl)
+        if op == "avg":
+            oracle.merge_avg(blk, dt_name, b_np, e_np, mask, w, **kw)
+        elif op == "avg_renorm":
+            oracle.merge_avg_renorm(blk, dt_name, b_np, e_np, mask, w, **kw)
+        elif op == "ties":
+            oracle.merge_ties(blk, dt_name, b_np, e_np, mask, cfg["density"], cfg["lam"], **kw)
+        else:
+            comb = 1 if cfg["combine"] == "sign_elect" else 0
+            oracle.merge_dare(blk, dt_name, b_np, e_np, mask, cfg["p"], cfg["seed"], comb, [1.0] * K, cfg["lam"], **kw)
+    dt = time.perf_counter() - t0
+    return {
+        "value": len(cfg["budgets"]) * nparams / dt,
+        "unit": "params/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"every n-th block, n = {stride} ({len(ids)} blocks, {nparams} params, all {K} experts): "
+                  f"index + plan + "
+                  f"{op} at each budget of the sweep (fractions of the sample's expert bytes); {dt:.2f} s",
+    }
+
+
 def run_sweep(args):
     """One of the other workload shapes: index once, then plan + merge at each
     budget of its sweep.  Experts are device-resident, stay in pinned host
@@ -493,6 +551,11 @@ def run_sweep(args):
                      "measured_file_read_GBps": None if fread is None else fread / 1e9},
         "breakdown": {"index_ms": round(idx_ms, 4), "per_budget": rows},
     }
+    if not args.no_cpu_baseline and not files:
+        log("timing the CPU oracle on a sample")
+        cb = cpu_baseline_sweep(spec, base, exps, cfg, flags, dl)
+        if cb is not None:
+            result["cpu_baseline"] = cb
     print(json.dumps(result), flush=True)
 
 
