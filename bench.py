@@ -60,6 +60,37 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+LORA_SOURCES = ("paper_2605_29489_amd/csrc/k_lora.hip", "paper_2605_29489_amd/csrc/device_common.h")
+LORA_TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "lora_pull_qwen2.5-1.5b_kernel_trace.md")
+
+
+def lora_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in LORA_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_lora_traffic():
+    """HBM bytes of one pull of every unit (k_lora_band + k_lora_zero) from
+    the committed counter profile, or None if it is missing or was taken on a
+    different kernel source."""
+    if not os.path.exists(LORA_TRAFFIC_PROFILE):
+        return None
+    kv = {}
+    for line in open(LORA_TRAFFIC_PROFILE):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            kv[k.strip()] = v.strip().strip("`")
+    if kv.get("kernel_source_sha256_16") != lora_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_pull_all"])
+    except (KeyError, ValueError):
+        return None
+
+
 def stored_traffic(route):
     """HBM bytes per merge launch of the route from the committed counter
     profile, or None if it is missing or was taken on a different kernel
@@ -317,8 +348,9 @@ def run_lora(args):
         "config": {"workload": f"{spec.description}; {cfg}", "storage_dtype": lay.dtype, "params": P,
                    "adapted_params": adapted, "adapter_elems_per_expert": n_ad, "blocks": G, "K": K,
                    "experts": "device (adapters)", "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "k_lora_tile (+ k_lora_zero), all units", "achieved": achieved / 1e9,
-                     "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": None},
+        "roofline": {"bound": "hbm", "kernel": "k_lora_band (+ k_lora_zero), all units", "achieved": achieved / 1e9,
+                     "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": achieved / HBM_PEAK,
+                     "traffic": stored_lora_traffic() if lay.dtype == "bf16" and args.layers is None else None},
         "breakdown": {"pull_all_ms": round(pull_all_ms, 4), "index_ms": round(idx_ms, 4), "per_budget": rows},
     }
     if not args.no_cpu_baseline and lay.dtype == "bf16":
