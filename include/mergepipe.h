@@ -214,9 +214,11 @@ int mp_merge_avg_renorm(const mp_layout* layout, const void* base,
  * kept iff |d| >= tau and |d| > 0.  Per element, over the selected experts
  * in increasing order: P = sum of the positive kept d, N = sum of the
  * negative kept d (fp32 adds from +0), with their counts; the elected sign
- * is + if P > -N, - if P < -N, none if equal (the sign of the total kept
- * mass; the paper fixes no summation order); mean = P / count(+), N /
- * count(-) or 0; out = round(fma(lambda, mean, x_0)).  0 <= density <= 1.
+ * compares the two rounded sums: + if fl32(P) > -fl32(N), - if
+ * fl32(P) < -fl32(N), none if equal (the paper fixes no summation order;
+ * this can differ from the sign of the exact sum: kept deltas
+ * (1, -1, 2^-25) elect none); mean = P / count(+), N / count(-) or 0;
+ * out = round(fma(lambda, mean, x_0)).  0 <= density <= 1.
  * block_elems must be <= 4096 (MP_E_UNSUPPORTED otherwise). */
 int mp_merge_ties(const mp_layout* layout, const void* base,
                   const void* const* experts, int32_t K, int32_t residency,

@@ -386,10 +386,11 @@ int orc_merge_avg_renorm(int64_t nb, const int64_t* doff, const int64_t* len, in
 /* r-th selected expert, experts in increasing index order.            */
 /*   P_j = sum of the positive t_rj, N_j = sum of the negative t_rj     */
 /*   (each in fp32, adds from +0, increasing r), with their counts;     */
-/*   gamma_j = sign of the total signed mass, i.e. +1 if P_j > -N_j,    */
-/*   -1 if P_j < -N_j, 0 if equal (the sign of the sum of the t_rj,     */
-/*   with positive and negative contributions summed separately --     */
-/*   the paper fixes no summation order);                              */
+/*   gamma_j = +1 if fl32(P_j) > -fl32(N_j), -1 if fl32(P_j) <          */
+/*   -fl32(N_j), 0 if they are equal.  The paper fixes no summation     */
+/*   order; this compares the two rounded one-signed masses, which can  */
+/*   differ from the sign of the exact sum: (1, -1, 2^-25) gives        */
+/*   P = fl32(1 + 2^-25) = 1 = -N, so no sign, in every expert order;   */
 /*   mean_j = P_j / count(+) if gamma = +1, N_j / count(-) if -1, else 0 */
 /*   (the sum over the agreeing entries divided by their number);      */
 /*   out_j = round(fma(lambda, mean_j, x0_j)).                          */

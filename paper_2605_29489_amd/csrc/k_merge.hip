@@ -261,8 +261,8 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
             rank += cnt;
         }
         if (MODE == M_TIES_TAU) {
-            // elect the sign of the larger signed mass; mean of the agreeing
-            // entries: with at most four experts by the divisor table and one
+            // elect by comparing the rounded masses P and -N; mean of the
+            // agreeing entries: with at most four experts by the divisor table and one
             // residual step (correctly rounded for a finite mass, as in
             // ties_store_small; a wave with an infinite mass divides),
             // otherwise as below
@@ -308,8 +308,8 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
                 }
             }
         } else if (SIGN) {
-            // elect the sign of the larger signed mass; mean of the agreeing
-            // entries (a count that is a power of two divides by exact scaling,
+            // elect by comparing the rounded masses P and -N; mean of the
+            // agreeing entries (a count that is a power of two divides by exact scaling,
             // correctly rounded as the quotient; otherwise IEEE division)
             bool odd = false;
 #pragma unroll
@@ -368,9 +368,10 @@ __global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src
 //     or the list overflows, an exact 3-level radix select over all
 //     elements runs instead.
 // Then one pass over the elements keeps |d| >= tau (tau is at least the
-// smallest positive pattern, so a kept delta is not zero), elects the sign
-// of the larger of the positive and negative kept masses and takes the mean
-// of the agreeing entries.
+// smallest positive pattern, so a kept delta is not zero), elects a sign by
+// comparing the fp32 sums P of the positive and N of the negative kept
+// deltas (+ if P > -N, - if P < -N, none if equal) and takes the mean of
+// the agreeing entries.
 namespace ties {
 using namespace ::mp::ties;  // window constants of ties_select.h
 #ifndef MP_TIES_NT
@@ -679,8 +680,8 @@ __device__ inline void ties_accumulate(const float (&d)[ties::GS][ties::EPT], co
     }
 }
 
-// Sign election (the sign of the larger of the positive and negative kept
-// masses) and the mean of the agreeing entries, for the V elements of one
+// Sign election (+ if the fp32 positive kept mass P exceeds -N, the negated
+// negative mass, - if it is below, none if equal) and the mean of the agreeing entries, for the V elements of one
 // chunk of a block with NS (2..4) selected experts; then y = lambda * mean
 // + x0, rounded once, is stored.  With at most two agreeing entries the mean
 // is the entry or an exact halving.  Otherwise q = mean * fl32(1/den) and one

@@ -637,6 +637,67 @@ def test_ties_infinite_masses(mp):
     _run_all(mp, spec, base, exps, "ties_tau", [1.0], density=0.0, lam=1.0)
 
 
+def _near_cancellation_deltas(rng, P, K, dt):
+    """Explicit deltas where most elements hold, over three of the experts,
+    an order of (a, -a, +-a * 2^-25), (a, -a, a * 2^-23) or (a, -a, a * 2^-24)
+    (a with a 3-bit mantissa, so every value is exact in bf16); the rest are
+    normal.  With K = 5 the triple sits on experts 0-2 for even elements and
+    on experts 2-4 for odd ones; the other experts hold zeros there."""
+    a = np.ldexp(1.0 + rng.integers(0, 8, P) / 8.0, rng.integers(-12, -4, P)) * rng.choice([-1.0, 1.0], P)
+    small = a * np.ldexp(1.0, rng.choice([-25, -25, -25, -23, -24], P)) * rng.choice([-1.0, 1.0], P)
+    trip = np.stack([a, -a, small])  # [3, P]
+    order = np.argsort(rng.random((3, P)), axis=0)
+    trip = np.take_along_axis(trip, order, axis=0)
+    D = np.zeros((K, P))
+    first = np.where((np.arange(P) % 2 == 1) & (K >= 5), 2, 0)
+    for r in range(3):
+        D[first + r, np.arange(P)] = trip[r]
+    normal = rng.random(P) < 0.3
+    D[:, normal] = rng.normal(0.0, 1e-3, (K, int(normal.sum())))
+    if dt == "bf16":
+        return [oracle.round_bf16(d.astype(np.float32)) for d in D]
+    return [d.astype(np.float32) for d in D]
+
+
+@pytest.mark.parametrize("dt,K", [("bf16", 3), ("f32", 5)])
+def test_ties_election_near_cancellation(mp, dt, K):
+    # The election compares the rounded one-signed masses fl32(P) and
+    # -fl32(N): for kept (a, -a, a * 2^-25) it elects nothing, although the
+    # exact mass is nonzero.  Both TIES routes and DARE's sign-elect combine
+    # match the oracle bit for bit on families built from such triples (the
+    # deltas are explicit, so they reach the kernels exactly).
+    spec = _mini_qwen(n_layers=1, K=K) if dt == "bf16" else _ragged_f32(K=K)
+    P = sum(int(np.prod(s)) for _, s in spec.tensors)
+    rng = np.random.default_rng(29)
+    base = rng.normal(0.0, 0.02, P).astype(np.float32)
+    base = oracle.round_bf16(base) if dt == "bf16" else base
+    deltas = _near_cancellation_deltas(rng, P, K, dt)
+    # the data reach the discriminating case: at density 1 and a full mask,
+    # elements whose exact kept mass is nonzero but elect no sign
+    lay = spec.layout
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    full = np.full(blocks.G, (1 << K) - 1, np.uint32)
+    zero_base = np.zeros_like(base)
+    out0 = oracle.merge_ties(blocks, dt, zero_base, deltas, full, 1.0, 1.0, delta=True)
+    D = np.stack([oracle_f32(d, dt) for d in deltas]).astype(np.float64)
+    hidden = (oracle_f32(out0, dt) == 0) & (D.sum(0) != 0)
+    _say(f"case election near cancellation {dt} K={K}: {int(hidden.sum())} of {P} elements elect none "
+         f"with a nonzero exact mass")
+    assert hidden.sum() > P // 10
+    for dens in (1.0, 0.5):
+        _run_all(mp, spec, base, deltas, "ties", [1.0, 0.5], density=dens, lam=1.0, delta=True)
+        _run_all(mp, spec, base, deltas, "ties_tau", [1.0, 0.5], density=dens, lam=1.0, delta=True)
+    for p in (0.0, 0.3):
+        _run_all(mp, spec, base, deltas, "dare_sign", [1.0, 0.5], p=p, seed=7, lam=1.0, delta=True)
+
+
+def oracle_f32(a, dt):
+    """fp32 values of a checkpoint array (bf16 patterns widened exactly)."""
+    if dt == "bf16":
+        return (np.asarray(a, np.uint16).astype(np.uint32) << 16).view(np.float32)
+    return np.asarray(a, np.float32)
+
+
 def test_skip_zero_full_budget_merges_equal_full_merges(mp):
     # With the skip-zero option, units whose block equals the base (S = 0:
     # the family's untouched blocks) are never selected; at full budget every

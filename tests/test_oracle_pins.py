@@ -878,9 +878,59 @@ def test_ties_worked_example():
         for run in case["runs"]:
             base = np.full(8, run["base"], np.float32)
             exps = [base + d for d in deltas]
-            out = oracle.merge_ties(b, "f32", base, exps, np.array(case["mask"], np.uint32),
-                                    case["density"], run["lambda"])
-            assert np.array_equal(out, np.array(run["out"], np.float32)), case["name"]
+            mask = np.array(case["mask"], np.uint32)
+            want = np.array(run["out"], np.float32)
+            out = oracle.merge_ties(b, "f32", base, exps, mask, case["density"], run["lambda"])
+            assert np.array_equal(out, want), case["name"]
+            # the catalog route (thresholds, then the merge) gives the same bits
+            tau = oracle.ties_thresholds(b, "f32", base, exps, case["density"])
+            out = oracle.merge_ties_tau(b, "f32", base, exps, mask, tau, run["lambda"])
+            assert np.array_equal(out, want), case["name"]
+            if case["density"] == 1.0:
+                # DARE's sign-elect combine with nothing dropped (p = 0) elects
+                # and averages the same way
+                out = oracle.merge_dare(b, "f32", base, exps, mask, 0.0, 7, 1, [0.0] * len(exps), run["lambda"])
+                assert np.array_equal(out, want), case["name"]
+
+
+def _sign_elect_running_sum(ts):
+    # the rejected reading: the sign of a running fp32 sum in expert order
+    s = np.float32(0)
+    for v in ts:
+        s = np.float32(s + np.float32(v))
+    agree = [np.float32(v) for v in ts if v != 0 and np.sign(v) == np.sign(s)]
+    if s == 0 or not agree:
+        return np.float32(0)
+    m = np.float32(0)
+    for v in agree:
+        m = np.float32(m + v)
+    return np.float32(m / np.float32(len(agree)))
+
+
+def test_ties_election_compares_rounded_masses():
+    # Every order of (1, -1, 2^-25) over three experts: fl32(P) = fl32(1 + 2^-25)
+    # = 1 = -N, so nothing is elected for any order, although the exact kept
+    # mass is +2^-25.  A running fp32 sum in expert order (planted below)
+    # elects + for two of the six orders, and fails.
+    import itertools
+    b = oracle.Blocks([8], 8)
+    base = np.zeros(8, np.float32)
+    trip = (1.0, -1.0, 2.0 ** -25)
+    perms = list(itertools.permutations(range(3)))
+    ds = np.zeros((3, 8), np.float32)
+    for j, pm in enumerate(perms):
+        ds[:, j] = [trip[r] for r in pm]
+    ds[:, 6] = (2.0 ** -23, -1.0, 1.0)  # P = 1 + 2^-23 > 1: +, mean 0.5 + 2^-24
+    ds[:, 7] = (-1.0, 2.0 ** -24, 1.0)  # P = fl32(1 + 2^-24) = 1 (tie to even): none
+    out = oracle.merge_ties(b, "f32", base, list(ds), np.full(1, 7, np.uint32), 1.0, 1.0)
+    want = np.zeros(8, np.float32)
+    want[6] = 0.5 + 2.0 ** -24
+    assert np.array_equal(out, want)
+    planted = np.array([_sign_elect_running_sum(ds[:, j]) for j in range(8)], np.float32)
+    assert not np.array_equal(planted, want)
+    # mirrored: all signs flipped flips the result
+    out = oracle.merge_ties(b, "f32", base, list(-ds), np.full(1, 7, np.uint32), 1.0, 1.0)
+    assert np.array_equal(out, -want)
 
 
 def test_ties_trim_keeps_exactly_top_k():
