@@ -13,6 +13,8 @@
 //
 // Addressing: expert i's block sits at its layout offset in expert i's
 // buffer, which is device memory or pinned host memory read over PCIe.
+#include <type_traits>
+
 #include "device_common.h"
 #include "mp_internal.h"
 #include "ties_select.h"
@@ -32,7 +34,38 @@ struct DevSrc {
     {
         return chunk_ptr(ex.p[i], off, es);
     }
+    // With at most four experts the pointer is picked from the first four
+    // by constant indices: the kernel loads them with its arguments, and an
+    // expert read does not wait for a pointer fetched once the mask is known.
+    template <bool SMALLK>
+    __device__ const void* expert_block(int i, int r, int64_t b, uint64_t off, uint32_t n, int es) const
+    {
+        const void* p = SMALLK ? ((i == 0) ? ex.p[0] : (i == 1) ? ex.p[1] : (i == 2) ? ex.p[2] : ex.p[3]) : ex.p[i];
+        return static_cast<const char*>(p) + off * (uint64_t)es;
+    }
 };
+
+// A block of one checkpoint as a buffer resource: a wave-uniform base
+// address and the block's byte length.  Loads then take one 32-bit offset
+// register, which the base, every expert and the output of a block share;
+// a load past the length returns zeros without touching memory and a store
+// past it is dropped, so lanes beyond the end of a short block need no
+// branch.  Third descriptor word: raw 32-bit data (the gfx9 encoding).
+__device__ inline __amdgpu_buffer_rsrc_t block_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ inline uint4 bld16(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ inline void bst16(__amdgpu_buffer_rsrc_t r, uint32_t off, uint4 v)
+{
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, 0);
+}
 
 // Selected expert blocks staged in device memory (host experts): the
 // launch covers blocks b0 .. b0 + grid - 1; block b0 + j's selected experts
@@ -46,16 +79,30 @@ struct StagedSrc {
     {
         return reinterpret_cast<const uint4*>(stage + soff[b] + (uint64_t)r * n * (uint64_t)es);
     }
+    template <bool SMALLK>
+    __device__ const void* expert_block(int i, int r, int64_t b, uint64_t off, uint32_t n, int es) const
+    {
+        return stage + soff[b] + (uint64_t)r * n * (uint64_t)es;
+    }
 };
 
-// Realized expert reads (Prop. 1's N^run): thread i adds the block's bytes
-// of expert i when it is selected, into slot (block mod 8) * 32 + i, so the
-// 256 counters sum per expert and spread the atomics over 8 words each.
-__device__ inline void count_expert_bytes(unsigned long long* ctr, uint32_t m, uint32_t n, int es)
+// Realized expert reads (Prop. 1's N^run), counted where the loads are
+// issued: after loading expert i's chunks q * NT + t (q < CPT) of a block of
+// nch chunks, each wave adds the bytes its lanes loaded into slot
+// ((workgroup * 4 + wave) mod 8) * 32 + i, so the 256 counters sum per
+// expert and the atomics spread over 8 words each.  No-op when ctr is null.
+template <int NT, int CPT>
+__device__ inline void count_loaded(unsigned long long* ctr, int i, uint32_t nch)
 {
-    const uint32_t i = threadIdx.x;
-    if (ctr != nullptr && i < 32u && ((m >> i) & 1u))
-        atomicAdd(&ctr[((blockIdx.x & 7u) << 5) | i], (unsigned long long)n * (unsigned long long)es);
+    if (ctr == nullptr)
+        return;
+    const uint32_t t = threadIdx.x;
+    uint32_t nl = 0;
+#pragma unroll
+    for (int q = 0; q < CPT; ++q)
+        nl += (uint32_t)__popcll(__ballot(q * NT + t < nch));
+    if ((t & 63u) == 0u)
+        atomicAdd(&ctr[(((blockIdx.x * 4u) + (t >> 6)) & 7u) << 5 | (uint32_t)i], (unsigned long long)nl * 16ull);
 }
 
 // Divisors for the mean of at most four agreeing entries: {den, fl32(1/den)}
@@ -69,283 +116,278 @@ __device__ inline float2 ties_divisor(int i)
 // ------------------------------------------------------------ elementwise family
 enum { M_AVG = 0, M_DARE_LIN = 1, M_DARE_SIGN = 2, M_TIES_TAU = 3, M_AVG_RENORM = 4 };
 
-// Occupancy of the elementwise kernels: DARE (either combination) and TIES
-// from thresholds keep their per-element state for half a block per pass
-// (two passes per 4096-element block), which leaves room for 8 waves per
-// SIMD with bf16 (6 with fp32) to hide memory latency; AVG (either
-// coefficient rule) holds a whole block per pass (measured faster than
-// halves at 8 waves).
 template <int MODE>
 constexpr bool is_avg() { return MODE == M_AVG || MODE == M_AVG_RENORM; }
-template <int DT, int MODE>
-constexpr int elem_waves() { return is_avg<MODE>() ? 1 : (DT == 1 ? 8 : 6); }
-template <int MODE>
-constexpr int elem_div() { return is_avg<MODE>() ? 1 : 2; }
 
-template <int DT, int MODE, class Src>
-__global__ __launch_bounds__(kT, (elem_waves<DT, MODE>())) void k_merge_elem(Src src, const void* __restrict__ base,
-                                                   const uint32_t* __restrict__ mask,
-                                                   const uint64_t* __restrict__ boff,
-                                                   const uint32_t* __restrict__ blen,
-                                                   const uint32_t* __restrict__ btensor,
-                                                   const uint64_t* __restrict__ belem0, Coeffs alpha,
-                                                   float lambda, uint32_t drop_T, float scale,
-                                                   uint32_t seed, uint32_t kmask, void* __restrict__ out,
-                                                   unsigned long long* __restrict__ ctr,
-                                                   const uint32_t* __restrict__ tau, int K, float bsub)
+// Shape of the elementwise kernels (AVG, selected-only AVG, DARE, TIES from
+// thresholds), chosen by measurement on MI355X.  A workgroup is one wave;
+// each lane owns one 16-byte chunk (bf16) or two (fp32), eight elements, so
+// a workgroup covers 512 elements and a 4096-element block takes eight
+// (2^sub_log2 workgroups per block; those past the end of a shorter block
+// return at once).  No kernel loops over a block: a loop made the compiler
+// hoist per-expert addresses out of it and spill them.
+//   * Loads are buffer loads with the block as the resource: one 32-bit
+//     offset register serves the base, every expert and the output, a load
+//     past the block's end returns zeros and a store past it is dropped, so
+//     no lane branches.  (Loads under a per-lane condition made the compiler
+//     wait for each load before issuing the next.)
+//   * The selected experts are read one at a time, in increasing order, each
+//     consumed before the next is loaded.  Issuing every stream's load at
+//     once measured slower: on this HBM a merge of five streams into one
+//     moves 0.67 of peak when each wave keeps all five reads in flight and
+//     0.73-0.75 when it reads them in turn, and so did the merges.
+//   * AVG (either coefficient rule) does little arithmetic per byte: it
+//     reads the block's length, offset and mask together, overlaps the base
+//     read with the first expert's, and runs at most 6 waves per SIMD (LDS
+//     reserved per workgroup caps the workgroups per CU); fewer requests in
+//     flight measured faster for it (2.86 against 3.12 ms at B = 100% on the
+//     Qwen2.5-1.5B-shaped family).  The sign-elect and DARE modes, with more
+//     arithmetic per element, run 8 waves per SIMD, read the length first
+//     (the exit test needs it) and the base before the first expert.
+//   * One-wave workgroups measured best among 64 to 512 threads, one or two
+//     chunks per lane and one or two passes per workgroup.
+constexpr int kTE = 64;
+// LDS reserved by each AVG workgroup: 25 of them exceed the CU's 160 KiB,
+// so at most 24 (6 waves per SIMD) are resident
+constexpr unsigned kAvgLds = 6656;
+
+template <int DT, int MODE, bool COUNT, bool SMALLK, class Src>
+__global__ __launch_bounds__(kTE, 8) void k_merge_elem(Src src, const void* __restrict__ base,
+                                                      const uint32_t* __restrict__ mask,
+                                                      const uint64_t* __restrict__ boff,
+                                                      const uint32_t* __restrict__ blen,
+                                                      const uint32_t* __restrict__ btensor,
+                                                      const uint64_t* __restrict__ belem0, Coeffs alpha,
+                                                      float lambda, uint32_t drop_T, float scale, uint32_t seed,
+                                                      uint32_t kmask, void* __restrict__ out,
+                                                      unsigned long long* __restrict__ ctr,
+                                                      const uint32_t* __restrict__ tau, int K, float bsub,
+                                                      uint32_t sub_log2)
 {
     constexpr int V = Fmt<DT>::V;
     constexpr int ES = Fmt<DT>::esize;
-    // chunks per thread per tile (4096-element blocks: 1 tile for AVG, 2
-    // for the others)
-    constexpr int CPT = ((DT == 1) ? 2 : 4) / elem_div<MODE>();
+    constexpr int CPT = (DT == 1) ? 1 : 2;  // chunks per lane
+    constexpr int E = CPT * V;              // elements per lane (8)
     constexpr bool DARE = MODE == M_DARE_LIN || MODE == M_DARE_SIGN;
     constexpr bool SIGN = MODE == M_DARE_SIGN || MODE == M_TIES_TAU;
-    constexpr int E = CPT * V;
-    // experts loaded together: the sign-elect state leaves room for the raw
-    // chunks of two experts only with fp32 data or with DARE's generator
-    constexpr int EG = (SIGN && (DT == 0 || MODE == M_DARE_SIGN)) ? 2 : 4;
-    const int64_t b = blockIdx.x;
+    const int64_t b = blockIdx.x >> sub_log2;
+    // this workgroup's first chunk of the block
+    const uint32_t tile = (blockIdx.x & ((1u << sub_log2) - 1u)) * (uint32_t)(CPT * kTE);
     const int t = threadIdx.x;
-    // TIES with at most four experts: divisors {den, 1/den} of the mean
-    __shared__ float2 rd[8];
-    if (MODE == M_TIES_TAU) {
-        if (t < 8)
-            rd[t] = ties_divisor(t);
-        __syncthreads();
-    }
     const uint32_t g = src.block(b);
-    const uint64_t off = boff[g];
-    const uint32_t n = blen[g];
-    const uint32_t m = mask[g] & kmask;  // bits of experts >= K are ignored
+    uint64_t off;
+    uint32_t n, mraw;
+    if (is_avg<MODE>()) {
+        // the block's metadata fetched together (one memory latency)
+        off = boff[g];
+        n = blen[g];
+        mraw = mask[g];
+        __asm__ volatile("" : : "s"(off), "s"(n), "s"(mraw), "s"(base), "s"(out));
+    }
+    else {
+        n = blen[g];
+    }
     const uint32_t nch = n / V;
-    const uint4* pb = chunk_ptr(base, off, ES);
-    uint4* po = reinterpret_cast<uint4*>(static_cast<char*>(out) + off * ES);
-    count_expert_bytes(ctr, m, n, ES);
+    if (tile >= nch)
+        return;  // past the end of a shorter block
+    if (!is_avg<MODE>()) {
+        off = boff[g];
+        mraw = mask[g];
+    }
+    const uint32_t m = mraw & kmask;  // bits of experts >= K are ignored
+    const uint32_t nbytes = n * (uint32_t)ES;  // < 2^30 (checked by the host)
+    const __amdgpu_buffer_rsrc_t rb = block_rsrc(chunk_ptr(base, off, ES), nbytes);
+    const __amdgpu_buffer_rsrc_t ro = block_rsrc(static_cast<char*>(out) + off * ES, nbytes);
     uint32_t tens = 0;
     uint64_t e0 = 0;
     if (DARE) {
         tens = btensor[g];
         e0 = belem0[g];
     }
-    // selected-only AVG: the coefficients are alpha_i / s, s = the sum of
-    // the selected alpha_i in increasing i (no coefficient when s = 0); s
-    // is formed at its first use, once the first expert reads are issued
+    uint32_t bo[CPT];  // byte offset of the lane's chunks in the block
+    uint32_t nl = 0;   // realized reads: chunks of the block this wave loads per expert
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+        const uint32_t c = tile + q * kTE + t;
+        bo[q] = c * 16u;
+        if (COUNT)
+            nl += (uint32_t)__popcll(__ballot(c < nch));
+    }
+    uint4 xb[CPT];
+#pragma unroll
+    for (int q = 0; q < CPT; ++q)
+        xb[q] = bld16(rb, bo[q]);
+    float x0[E];
+    auto unpack_base = [&]() {
+#pragma unroll
+        for (int q = 0; q < CPT; ++q)
+            Fmt<DT>::unpack(xb[q], &x0[q * V]);
+    };
+    float acc[E], ps[E], ns[E];
+    uint32_t cpn[E];  // sign-elect counts: positive in the low, negative in the high half
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        acc[e] = 0.0f;
+        ps[e] = 0.0f;
+        ns[e] = 0.0f;
+        cpn[e] = 0u;
+    }
+    // selected-only AVG: the coefficients are alpha_i / s, s = the sum of the
+    // selected alpha_i in increasing i (no coefficient when s = 0)
     float s_sel = 0.0f;
-
-    for (uint32_t tile = 0; tile < nch; tile += CPT * kT) {
-        float x0[E];
-        bool ok[CPT];
+    if (MODE == M_AVG_RENORM) {
+        uint32_t ms = m;
+        __asm__ volatile("" : "+s"(ms) : : "memory");  // constant indices: a few wide scalar loads
+#pragma unroll
+        for (int q = 0; q < 32; ++q)
+            if ((ms >> q) & 1u)
+                s_sel = s_sel + alpha.v[q];
+    }
+    // expert i (the r-th selected) read and folded into the state
+    auto expert = [&](int i, int r, bool first) {
+        const __amdgpu_buffer_rsrc_t re =
+            block_rsrc(src.template expert_block<SMALLK>(i, r, b, off, n, ES), nbytes);
+        if (first && !is_avg<MODE>())  // the base arrives before the first expert is read
+            __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        uint4 raw[CPT];
+#pragma unroll
+        for (int q = 0; q < CPT; ++q)
+            raw[q] = bld16(re, bo[q]);
+        if (COUNT && t == 0)
+            atomicAdd(&ctr[((blockIdx.x & 7u) << 5) | (uint32_t)i], (unsigned long long)nl * 16ull);
+        if (first)
+            unpack_base();
+        // TIES from catalog thresholds: keep |d| >= tau (at least the
+        // smallest positive pattern, so a kept delta is not zero)
+        float tauf = 0.0f;
+        if (MODE == M_TIES_TAU)
+            tauf = __uint_as_float(max(tau[(uint64_t)g * (uint32_t)K + (uint32_t)i], 1u));
+        float coef = alpha.v[i];
+        if (MODE == M_AVG_RENORM)
+            coef = (s_sel != 0.0f) ? coef / s_sel : 0.0f;
 #pragma unroll
         for (int q = 0; q < CPT; ++q) {
-            const uint32_t c = tile + q * kT + t;
-            ok[q] = c < nch;
-            uint4 raw = make_uint4(0, 0, 0, 0);
-            if (ok[q])
-                raw = pb[c];
-            Fmt<DT>::unpack(raw, &x0[q * V]);
-        }
-        float acc[E], ps[E], ns[E];
-        // sign-elect counts: DARE packs positive (low) and negative (high
-        // half) in cpn; TIES keeps them apart in cpn and cng
-        uint32_t cpn[E], cng[E];
+            float x[V];
+            Fmt<DT>::unpack(raw[q], x);
+            uint32_t word[V];
+            if (DARE) {
+                // Philox words for elements e .. e+V-1 of tensor `tens` (V is 4 or 8)
+                const uint64_t e = e0 + (uint64_t)(tile + q * kTE + t) * V;
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-            acc[e] = 0.0f;
-            ps[e] = 0.0f;
-            ns[e] = 0.0f;
-            cpn[e] = 0u;
-            cng[e] = 0u;
-        }
-        uint32_t mm = m;
-        int rank = 0;
-        while (mm) {
-            int idx[EG];
-            int cnt = 0;
-#pragma unroll
-            for (int j = 0; j < EG; ++j) {
-                idx[j] = -1;
-                if (mm) {
-                    idx[j] = __builtin_ctz(mm);
-                    mm &= mm - 1u;
-                    ++cnt;
+                for (int h = 0; h < V / 4; ++h) {
+                    const uint64_t qq = (e >> 2) + h;
+                    const uint4 r4 = philox4x32_10(make_uint4((uint32_t)qq, (uint32_t)(qq >> 32), tens, 0u), seed,
+                                                   (uint32_t)i);
+                    word[h * 4 + 0] = r4.x;
+                    word[h * 4 + 1] = r4.y;
+                    word[h * 4 + 2] = r4.z;
+                    word[h * 4 + 3] = r4.w;
                 }
             }
-            uint4 raw[EG][CPT];
-#pragma unroll
-            for (int j = 0; j < EG; ++j) {
-                if (j < cnt) {
-                    const uint4* pe = src.expert(idx[j], rank + j, b, off, n, ES);
-#pragma unroll
-                    for (int q = 0; q < CPT; ++q)
-                        if (ok[q])
-                            raw[j][q] = pe[tile + q * kT + t];
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < EG; ++j) {
-                if (j >= cnt)
-                    break;
-                const int i = idx[j];
-                // TIES from catalog thresholds: keep |d| >= tau (at least the
-                // smallest positive pattern, so a kept delta is not zero)
-                float tauf = 0.0f;
-                if (MODE == M_TIES_TAU)
-                    tauf = __uint_as_float(max(tau[(uint64_t)g * (uint32_t)K + (uint32_t)i], 1u));
-                float coef = alpha.v[i];
-                if (MODE == M_AVG_RENORM) {
-                    if (rank == 0 && j == 0) {
-                        // constant indices: a few wide scalar loads rather
-                        // than one dependent load per selected expert; kept
-                        // behind the expert reads already issued
-                        uint32_t ms = m;
-                        __asm__ volatile("" : "+s"(ms) : : "memory");
-                        s_sel = 0.0f;
-#pragma unroll
-                        for (int q = 0; q < 32; ++q)
-                            if ((ms >> q) & 1u)
-                                s_sel = s_sel + alpha.v[q];
-                    }
-                    coef = (s_sel != 0.0f) ? coef / s_sel : 0.0f;
-                }
-#pragma unroll
-                for (int q = 0; q < CPT; ++q) {
-                    if (!ok[q])
-                        continue;
-                    float x[V];
-                    Fmt<DT>::unpack(raw[j][q], x);
-                    uint32_t word[V];
-                    if (DARE) {
-                        // Philox words for elements e .. e+V-1 of tensor `tens` (V is 4 or 8)
-                        const uint64_t e = e0 + (uint64_t)(tile + q * kT + t) * V;
-#pragma unroll
-                        for (int h = 0; h < V / 4; ++h) {
-                            const uint64_t qq = (e >> 2) + h;
-                            const uint4 r4 = philox4x32_10(
-                                make_uint4((uint32_t)qq, (uint32_t)(qq >> 32), tens, 0u), seed, (uint32_t)i);
-                            word[h * 4 + 0] = r4.x;
-                            word[h * 4 + 1] = r4.y;
-                            word[h * 4 + 2] = r4.z;
-                            word[h * 4 + 3] = r4.w;
-                        }
-                    }
-#pragma unroll
-                    for (int v = 0; v < V; ++v) {
-                        const int e = q * V + v;
-                        // x - x0 (bsub = 1: exactly the difference), or the stored
-                        // delta itself (bsub = 0: explicit deltas)
-                        const float d = fmaf(-bsub, x0[e], x[v]);
-                        if (is_avg<MODE>()) {
-                            acc[e] = fmaf(coef, d, acc[e]);
-                        } else if (MODE == M_TIES_TAU) {
-                            // d >= tau keeps a positive delta, -d >= tau a negative one
-                            const bool kp = d >= tauf, kn = -d >= tauf;
-                            ps[e] = ps[e] + (kp ? d : 0.0f);
-                            ns[e] = ns[e] + (kn ? d : 0.0f);
-                            cpn[e] += kp ? 1u : 0u;
-                            cng[e] += kn ? 1u : 0u;
-                        } else {
-                            const float tv = (word[v] < drop_T) ? 0.0f : d * scale;
-                            if (MODE == M_DARE_LIN) {
-                                acc[e] = fmaf(alpha.v[i], tv, acc[e]);
-                            } else {
-                                const bool pos = tv > 0.0f, neg = tv < 0.0f;
-                                ps[e] = ps[e] + (pos ? tv : 0.0f);
-                                ns[e] = ns[e] + (neg ? tv : 0.0f);
-                                cpn[e] += pos ? 1u : (neg ? 0x10000u : 0u);
-                            }
-                        }
-                    }
-                }
-            }
-            rank += cnt;
-        }
-        if (MODE == M_TIES_TAU) {
-            // elect by comparing the rounded masses P and -N; mean of the
-            // agreeing entries: with at most four experts by the divisor table and one
-            // residual step (correctly rounded for a finite mass, as in
-            // ties_store_small; a wave with an infinite mass divides),
-            // otherwise as below
-            uint32_t den[E];
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const bool up = ps[e] > -ns[e];
-                const bool dn = ps[e] < -ns[e];
-                acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);
-                den[e] = up ? cpn[e] : (dn ? cng[e] : 1u);
-            }
-            if (K <= 4) {
-                bool bad = false;
-                float q[E];
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const float2 c = rd[den[e]];
-                    const float q0 = acc[e] * c.y;
-                    q[e] = fmaf(fmaf(-c.x, q0, acc[e]), c.y, q0);
-                    bad |= q[e] != q[e];
-                }
-                if (__any(bad)) {
-#pragma unroll
-                    for (int e = 0; e < E; ++e)
-                        q[e] = acc[e] / (float)den[e];
-                }
-#pragma unroll
-                for (int e = 0; e < E; ++e)
-                    acc[e] = q[e];
-            } else {
-                bool odd = false;
-#pragma unroll
-                for (int e = 0; e < E; ++e)
-                    odd |= (den[e] & (den[e] - 1u)) != 0u;
-                if (__any(odd)) {
-#pragma unroll
-                    for (int e = 0; e < E; ++e)
-                        acc[e] = acc[e] / (float)den[e];
-                } else {
-#pragma unroll
-                    for (int e = 0; e < E; ++e)
-                        acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
-                }
-            }
-        } else if (SIGN) {
-            // elect by comparing the rounded masses P and -N; mean of the
-            // agreeing entries (a count that is a power of two divides by exact scaling,
-            // correctly rounded as the quotient; otherwise IEEE division)
-            bool odd = false;
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const bool up = ps[e] > -ns[e];
-                const bool dn = ps[e] < -ns[e];
-                acc[e] = dn ? ns[e] : (up ? ps[e] : 0.0f);
-                // with no elected sign acc is 0 and any count >= 1 gives 0
-                cpn[e] = max(__builtin_amdgcn_ubfe(cpn[e], dn ? 16u : 0u, 16u), 1u);
-                odd |= (cpn[e] & (cpn[e] - 1u)) != 0u;
-            }
-            if (__any(odd)) {
-#pragma unroll
-                for (int e = 0; e < E; ++e)
-                    acc[e] = acc[e] / (float)cpn[e];
-            } else {
-#pragma unroll
-                for (int e = 0; e < E; ++e)
-                    acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(cpn[e])) << 23);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < CPT; ++q) {
-            if (!ok[q])
-                continue;
-            float y[V];
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 const int e = q * V + v;
-                if (is_avg<MODE>())
-                    y[v] = x0[e] + acc[e];
-                else
-                    y[v] = fmaf(lambda, acc[e], x0[e]);
+                // x - x0 (bsub = 1: exactly the difference), or the stored
+                // delta itself (bsub = 0: explicit deltas)
+                const float d = fmaf(-bsub, x0[e], x[v]);
+                if (is_avg<MODE>()) {
+                    acc[e] = fmaf(coef, d, acc[e]);
+                } else if (MODE == M_TIES_TAU) {
+                    // d >= tau keeps a positive delta, -d >= tau a negative one
+                    const bool kp = d >= tauf, kn = -d >= tauf;
+                    ps[e] = ps[e] + (kp ? d : 0.0f);
+                    ns[e] = ns[e] + (kn ? d : 0.0f);
+                    cpn[e] += kp ? 1u : (kn ? 0x10000u : 0u);
+                } else {
+                    const float tv = (word[v] < drop_T) ? 0.0f : d * scale;
+                    if (MODE == M_DARE_LIN) {
+                        acc[e] = fmaf(alpha.v[i], tv, acc[e]);
+                    } else {
+                        const bool pos = tv > 0.0f, neg = tv < 0.0f;
+                        ps[e] = ps[e] + (pos ? tv : 0.0f);
+                        ns[e] = ns[e] + (neg ? tv : 0.0f);
+                        cpn[e] += pos ? 1u : (neg ? 0x10000u : 0u);
+                    }
+                }
             }
-            po[tile + q * kT + t] = Fmt<DT>::pack(y);
         }
+    };
+    uint32_t mm = m;
+    if (mm == 0u) {
+        unpack_base();  // no expert selected
+    } else {
+        expert(__builtin_ctz(mm), 0, true);
+        mm &= mm - 1u;
+        for (int r = 1; mm != 0u; ++r) {
+            expert(__builtin_ctz(mm), r, false);
+            mm &= mm - 1u;
+        }
+    }
+    if (SIGN) {
+        // elect by comparing the rounded masses P and -N; mean of the
+        // agreeing entries
+        uint32_t den[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const bool up = ps[e] > -ns[e];
+            const bool dn = ps[e] < -ns[e];
+            acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);
+            // with no elected sign acc is 0 and any count >= 1 gives 0
+            den[e] = up ? (cpn[e] & 0xffffu) : (dn ? (cpn[e] >> 16) : 1u);
+        }
+        if (MODE == M_TIES_TAU && K <= 4) {
+            // den is 1..4: q = mass * fl32(1/den) and one residual step, the
+            // correctly rounded quotient of a finite mass (as in
+            // ties_store_small); a wave with an infinite mass divides
+            bool bad = false;
+            float q[E];
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const float cx = (float)den[e];
+                const float cy = (den[e] == 3u) ? 0x1.555556p-2f
+                                                : __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
+                const float q0 = acc[e] * cy;
+                q[e] = fmaf(fmaf(-cx, q0, acc[e]), cy, q0);
+                bad |= q[e] != q[e];
+            }
+            if (__any(bad)) {
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    q[e] = acc[e] / (float)den[e];
+            }
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                acc[e] = q[e];
+        } else {
+            // a count that is a power of two divides by exact scaling,
+            // correctly rounded as the quotient; otherwise IEEE division
+            bool odd = false;
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                odd |= (den[e] & (den[e] - 1u)) != 0u;
+            if (__any(odd)) {
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    acc[e] = acc[e] / (float)den[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
+            }
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+        float y[V];
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            const int e = q * V + v;
+            if (is_avg<MODE>())
+                y[v] = x0[e] + acc[e];
+            else
+                y[v] = fmaf(lambda, acc[e], x0[e]);
+        }
+        bst16(ro, bo[q], Fmt<DT>::pack(y));  // dropped past the block's end
     }
 }
 
@@ -444,7 +486,7 @@ __device__ inline uint32_t block_radix_select(TiesSmem& sm, int j, const float (
 // block's selected experts) into raw.
 template <int DT, int CPT, class Src>
 __device__ inline void ties_load_group(const Src& src, int64_t b, uint64_t off, uint32_t n, uint32_t gm, int rank0,
-                                       uint4 (&raw)[ties::GS][CPT])
+                                       uint4 (&raw)[ties::GS][CPT], unsigned long long* ctr)
 {
     constexpr int ES = Fmt<DT>::esize;
     const int ns = __popc(gm);
@@ -456,6 +498,7 @@ __device__ inline void ties_load_group(const Src& src, int64_t b, uint64_t off, 
             const int i = __builtin_ctz(mm);
             mm &= mm - 1u;
             load_chunks<DT, ties::NT, CPT>(src.expert(i, rank0 + j, b, off, n, ES), nch, raw[j]);
+            count_loaded<ties::NT, CPT>(ctr, i, nch);
         }
     }
 }
@@ -641,10 +684,10 @@ template <int DT, int CPT, class Src>
 __device__ inline uint32_t ties_trim_group(TiesSmem& sm, const Src& src, int64_t b, uint64_t off, uint32_t n,
                                        uint32_t k, uint32_t gm, int rank0, const float (&x0)[CPT * Fmt<DT>::V],
                                        float (&d)[ties::GS][CPT * Fmt<DT>::V], uint32_t (&tau)[ties::GS],
-                                       float bsub)
+                                       float bsub, unsigned long long* ctr)
 {
     uint4 raw[ties::GS][CPT];
-    ties_load_group<DT, CPT>(src, b, off, n, gm, rank0, raw);
+    ties_load_group<DT, CPT>(src, b, off, n, gm, rank0, raw, ctr);
     const int ns = __popc(gm);
     ties_deltas<DT, CPT>(sm, raw, ns, x0, d, bsub);
     return ties_select_group<CPT * Fmt<DT>::V>(sm, n, k, ns, d, tau);
@@ -848,7 +891,6 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
     }
     const uint32_t m = (k != 0u) ? (mask[g] & kmask) : 0u;  // density 0 keeps nothing: no expert is read
     const uint32_t nch = n / V;
-    count_expert_bytes(ctr, m, n, ES);
     uint4 x0raw[CPT];
     load_chunks<DT, NT, CPT>(chunk_ptr(base, off, ES), nch, x0raw);
     float x0[E];
@@ -860,7 +902,7 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
         const int ns = __popc(m);
         // every load of the block is issued before the base is unpacked
         uint4 raw[GS][CPT];
-        ties_load_group<DT, CPT>(src, b, off, n, m, 0, raw);
+        ties_load_group<DT, CPT>(src, b, off, n, m, 0, raw, ctr);
 #pragma unroll
         for (int q = 0; q < CPT; ++q)
             Fmt<DT>::unpack(x0raw[q], &x0[q * V]);
@@ -907,7 +949,7 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
                 gm |= mm & (0u - mm);
                 mm &= mm - 1u;
             }
-            ties_trim_group<DT, CPT>(sm, src, b, off, n, k, gm, rank0, x0, d, tau, bsub);
+            ties_trim_group<DT, CPT>(sm, src, b, off, n, k, gm, rank0, x0, d, tau, bsub, ctr);
             const int ns = __popc(gm);
             switch (ns) {
             case 1: ties_accumulate_all<1>(d, tau, P, N, cnt); break;
@@ -933,6 +975,29 @@ __global__ __launch_bounds__(ties::NT, MULTI ? ties::NT / 128 : MP_TIES_WAVES) v
     }
 }
 
+// The elementwise kernel with or without the read counters; AVG with the
+// expert pointers picked by constant indices when K <= 4.
+template <int DT, int MODE, bool COUNT, class Src, class... A>
+void launch_elem_k(int K, dim3 grid, hipStream_t s, const Src& src, A... a)
+{
+    if constexpr (is_avg<MODE>()) {
+        if (K <= 4)
+            hipLaunchKernelGGL((k_merge_elem<DT, MODE, COUNT, true, Src>), grid, dim3(kTE), kAvgLds, s, src, a...);
+        else
+            hipLaunchKernelGGL((k_merge_elem<DT, MODE, COUNT, false, Src>), grid, dim3(kTE), kAvgLds, s, src, a...);
+    } else {
+        hipLaunchKernelGGL((k_merge_elem<DT, MODE, COUNT, false, Src>), grid, dim3(kTE), 0, s, src, a...);
+    }
+}
+template <int DT, int MODE, class Src, class... A>
+void launch_elem(bool count, int K, dim3 grid, hipStream_t s, const Src& src, A... a)
+{
+    if (count)
+        launch_elem_k<DT, MODE, true>(K, grid, s, src, a...);
+    else
+        launch_elem_k<DT, MODE, false>(K, grid, s, src, a...);
+}
+
 template <int DT, class Src>
 hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src, const void* base,
                         int K, const uint32_t* mask, int64_t nb, void* out, unsigned long long* ctr,
@@ -941,34 +1006,40 @@ hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src
     const uint32_t kmask = (K >= 32) ? 0xffffffffu : ((1u << K) - 1u);
     if (nb == 0)
         return hipSuccess;
-    const dim3 grid((unsigned)nb), block(kT);
+    // workgroups per block for the elementwise kernels: a power of two
+    // covering the longest block
+    const int64_t per_wg = 8 * (int64_t)kTE;  // elements of one elementwise workgroup (8 per lane)
+    uint32_t sub_log2 = 0;
+    while ((per_wg << sub_log2) < (int64_t)bt.max_len)
+        ++sub_log2;
+    const dim3 grid((unsigned)nb), egrid((unsigned)(nb << sub_log2));
     const uint32_t T = (uint32_t)floor(a.p * 4294967296.0);
     const float scale = (float)(1.0 / (1.0 - a.p));
     switch (a.op) {
     case Op::AVG:
-        hipLaunchKernelGGL((k_merge_elem<DT, M_AVG, Src>), grid, block, 0, s, src, base, mask, bt.d_off,
+        launch_elem<DT, M_AVG>(ctr != nullptr, K, egrid, s, src, base, mask, bt.d_off,
                            bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask, out, ctr,
-                           nullptr, K, a.bsub);
+                           nullptr, K, a.bsub, sub_log2);
         break;
     case Op::AVG_RENORM:
-        hipLaunchKernelGGL((k_merge_elem<DT, M_AVG_RENORM, Src>), grid, block, 0, s, src, base, mask, bt.d_off,
+        launch_elem<DT, M_AVG_RENORM>(ctr != nullptr, K, egrid, s, src, base, mask, bt.d_off,
                            bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask, out, ctr,
-                           nullptr, K, a.bsub);
+                           nullptr, K, a.bsub, sub_log2);
         break;
     case Op::DARE_LINEAR:
-        hipLaunchKernelGGL((k_merge_elem<DT, M_DARE_LIN, Src>), grid, block, 0, s, src, base, mask,
+        launch_elem<DT, M_DARE_LIN>(ctr != nullptr, K, egrid, s, src, base, mask,
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, T, scale,
-                           a.seed, kmask, out, ctr, nullptr, K, a.bsub);
+                           a.seed, kmask, out, ctr, nullptr, K, a.bsub, sub_log2);
         break;
     case Op::DARE_SIGN:
-        hipLaunchKernelGGL((k_merge_elem<DT, M_DARE_SIGN, Src>), grid, block, 0, s, src, base, mask,
+        launch_elem<DT, M_DARE_SIGN>(ctr != nullptr, K, egrid, s, src, base, mask,
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, T, scale,
-                           a.seed, kmask, out, ctr, nullptr, K, a.bsub);
+                           a.seed, kmask, out, ctr, nullptr, K, a.bsub, sub_log2);
         break;
     case Op::TIES_TAU:
-        hipLaunchKernelGGL((k_merge_elem<DT, M_TIES_TAU, Src>), grid, block, 0, s, src, base, mask,
+        launch_elem<DT, M_TIES_TAU>(ctr != nullptr, K, egrid, s, src, base, mask,
                            bt.d_off, bt.d_len, bt.d_tensor, bt.d_elem0, a.alpha, a.lambda, 0u, 1.0f, 0u, kmask,
-                           out, ctr, a.tau, K, a.bsub);
+                           out, ctr, a.tau, K, a.bsub, sub_log2);
         break;
     case Op::TIES: {
         // k for full-length blocks, as the kernel computes it for short ones
