@@ -173,6 +173,29 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq,
             const float* w, uint64_t budget_bytes, uint32_t flags,
             uint32_t* mask, mp_plan_stats* stats, void* stream);
 
+/* mp_plan without allocation, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Arguments, results, errors and the final
+ * synchronisation are those of mp_plan, and it runs the same kernels: mask
+ * and stats are equal bit for bit.  It calls no hipMalloc, hipFree or
+ * other allocation routine and keeps no per-layout cache.  Instead, the
+ * control block, the layout's tensor sizes, the first block of each
+ * tensor, the block lengths and the two candidate lists live in one fixed
+ * device array of 16 MiB (16,777,216 bytes), which each device the library
+ * runs on holds until the process ends.  A layout needs the sum of these
+ * sizes, each rounded up to 256 bytes: about 19 KB for the control block,
+ * 8 * n_tensors, 4 * (n_tensors + 1), 4 * G, and twice 4 * K * max(1, number
+ * of short blocks) -- 1.6 MB for a 1.5B-parameter layout cut into 4096-
+ * element blocks, so up to about four million blocks fit.  A larger layout
+ * gets MP_E_UNSUPPORTED (with the sizes in mp_last_error) before anything
+ * is enqueued.  The array keeps the last call's contents; each call
+ * rebuilds everything it reads from it.  Calls hold the library's lock
+ * until their stream has finished, so calls from several threads are
+ * serialised and never use the array at the same time. */
+int mp_plan_noalloc(const mp_layout* layout, int32_t K, const float* sumsq,
+                    const float* w, uint64_t budget_bytes, uint32_t flags,
+                    uint32_t* mask, mp_plan_stats* stats, void* stream);
+
 /* Coverage of an access mask for the run's manifest (Section 3: the
  * executor records touched blocks and contributing experts).
  * cov: HOST uint64[n_tensors * K]; cov[t*K + i] = number of elements of

@@ -34,7 +34,7 @@ MP_COMBINE_LINEAR, MP_COMBINE_SIGN_ELECT = 0, 1
 MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 
 EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
-           "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
+           "mp_plan_noalloc", "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
            "mp_merge_ties",
            "mp_merge_ties_tau", "mp_merge_dare", "mp_lora_materialize", "mp_set_stage_bytes", "mp_last_error",
            "mp_release")
@@ -91,6 +91,7 @@ def _load():
     L.mp_index_blocks.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, vp]
     L.mp_index_ties.argtypes = [lp, vp, C.POINTER(vp), i32, i32, C.c_double, vp, vp, vp]
     L.mp_plan.argtypes = [lp, i32, vp, C.POINTER(C.c_float), u64, u32, vp, C.POINTER(mp_plan_stats), vp]
+    L.mp_plan_noalloc.argtypes = L.mp_plan.argtypes
     L.mp_merge_avg.argtypes = [lp, vp, C.POINTER(vp), i32, i32, vp, C.POINTER(C.c_float), vp,
                                C.POINTER(mp_io_stats), vp]
     L.mp_merge_avg_renorm.argtypes = L.mp_merge_avg.argtypes
@@ -110,7 +111,7 @@ def _load():
     L.mp_last_error.argtypes = []
     L.mp_release.argtypes = []
     for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
-                 "mp_coverage", "mp_merge_avg",
+                 "mp_plan_noalloc", "mp_coverage", "mp_merge_avg",
                  "mp_merge_avg_renorm", "mp_merge_ties",
                  "mp_merge_ties_tau",
                  "mp_merge_dare", "mp_lora_materialize"):
@@ -214,6 +215,15 @@ def mp_plan(layout: Layout, K: int, sumsq, w, budget_bytes: int, mask, flags: in
     st = mp_plan_stats()
     _check(lib.mp_plan(layout.ref, K, _ptr(sumsq), _floats(w, K), int(budget_bytes), flags, _ptr(mask),
                        C.byref(st), _stream(stream)))
+    return st.as_dict()
+
+
+def mp_plan_noalloc(layout: Layout, K: int, sumsq, w, budget_bytes: int, mask, flags: int = 0,
+                    stream=None) -> dict:
+    """mp_plan on the library's fixed device array (allocates nothing)."""
+    st = mp_plan_stats()
+    _check(lib.mp_plan_noalloc(layout.ref, K, _ptr(sumsq), _floats(w, K), int(budget_bytes), flags, _ptr(mask),
+                               C.byref(st), _stream(stream)))
     return st.as_dict()
 
 

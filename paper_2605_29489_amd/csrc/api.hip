@@ -781,6 +781,71 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float*
     return MP_OK;
 }
 
+int mp_plan_noalloc(const mp_layout* layout, int32_t K, const float* sumsq, const float* w,
+                    uint64_t budget_bytes, uint32_t flags, uint32_t* mask, mp_plan_stats* stats, void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    int es = 0;
+    int rc = validate_layout(layout, &es);
+    if (rc)
+        return rc;
+    if (K < 1 || K > kMaxK)
+        return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
+    if ((flags & ~(uint32_t)(MP_PLAN_PER_BYTE | MP_PLAN_SKIP_ZERO)) != 0u)
+        return fail(MP_E_UNSUPPORTED, "plan flags 0x%x not supported", flags);
+    if (w == nullptr || stats == nullptr)
+        return fail(MP_E_ARG, "w and stats must not be NULL");
+    // the block partition's counts, on the host without allocating
+    int64_t G = 0, n_short = 0, P = 0;
+    for (int32_t t = 0; t < layout->n_tensors; ++t) {
+        const int64_t n = layout->numel[t];
+        G += (n + layout->block_elems - 1) / layout->block_elems;
+        n_short += (n % layout->block_elems) != 0 ? 1 : 0;
+        P += n;
+    }
+    if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
+        return fail(MP_E_ARG, "K * G does not fit 32-bit unit ids");
+    const int64_t need = static_plan_bytes(layout->n_tensors, G, n_short, K);
+    if (need > static_plan_limit())
+        return fail(MP_E_UNSUPPORTED,
+                    "the layout (%d tensors, %lld blocks, K = %d) needs %lld bytes of the fixed plan scratch, "
+                    "whose size is %lld bytes; use mp_plan", layout->n_tensors, (long long)G, K,
+                    (long long)need, (long long)static_plan_limit());
+    Coeffs cw{};
+    for (int i = 0; i < K; ++i) {
+        if (!std::isfinite(w[i]))
+            return fail(MP_E_ARG, "w[%d] is not finite", i);
+        cw.v[i] = w[i];
+    }
+    if (sumsq != nullptr && (rc = check_device_buffer(sumsq, sizeof(float) * (size_t)(G * K), "sumsq")))
+        return rc;
+    if ((rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)G, "mask")))
+        return rc;
+    void* ws = nullptr;
+    hipError_t e = static_plan_scratch(&ws);
+    if (e != hipSuccess)
+        return hip_fail(e, "address of the fixed plan scratch");
+    const uint64_t full = (uint64_t)P * (uint64_t)es * (uint64_t)K;
+    uint64_t h[7] = {0, 0, 0, 0, 0, 0, 0};
+    e = launch_plan_static(ws, layout->numel, layout->n_tensors, layout->block_elems, (uint32_t)es, G, n_short, K,
+                           sumsq, cw, flags, budget_bytes, full, mask, h, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return hip_fail(e, "plan (fixed scratch)");
+    stats->budget_bytes = h[0];
+    stats->cost_bytes = h[1];
+    stats->full_bytes = h[2];
+    stats->n_selected = h[3];
+    stats->n_units = h[4];
+    stats->digest = h[5];
+    if (h[6] != 0)
+        return fail(MP_E_HIP, "plan kernels reported internal error %llu", (unsigned long long)h[6]);
+    if (stats->cost_bytes > budget_bytes)
+        return fail(MP_E_HIP, "plan cost %llu exceeds the budget %llu", (unsigned long long)stats->cost_bytes,
+                    (unsigned long long)budget_bytes);
+    return MP_OK;
+}
+
 static int merge_additive(Op op, const mp_layout* layout, const void* base, const void* const* experts,
                           int32_t K, int32_t residency, const uint32_t* mask, const float* alpha, void* out,
                           mp_io_stats* io, void* stream)

@@ -583,54 +583,196 @@ __global__ __launch_bounds__(kT) void k_plan_final(PlanCtl* ctl, unsigned long l
 
 }  // namespace
 
+namespace {
+
+// The plan's kernel sequence over G blocks with lengths blen[G] (elements),
+// control block ctl and two candidate lists of cap uids each; `rounds`
+// bounds the number of rounds (the distinct block lengths, or any larger
+// number: the later rounds stop once the plan is done).
+hipError_t enqueue_plan(PlanCtl* ctl, uint32_t* list0, uint32_t* list1, unsigned cap, const uint32_t* blen,
+                        uint32_t es, int64_t G, int rounds, int K, const float* sumsq, const Coeffs& w,
+                        uint32_t flags, uint64_t budget, uint64_t full_bytes, uint32_t* mask, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_plan_init, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget);
+    if (G > 0) {
+        const int64_t want = (G + kT - 1) / kT;
+        const unsigned grid0 = (unsigned)std::min<int64_t>(want, kPlanGrid);
+        // round 0 over every unit; its candidates for round 1 go to list1
+        const CandSrc src{nullptr, nullptr, 0u};
+        for (int d = 0; d < 8; ++d)
+            hipLaunchKernelGGL(k_plan_hist, dim3(grid0), dim3(kT), 0, s, ctl, d, sumsq, w, flags, K, blen, es, G,
+                               src);
+        hipLaunchKernelGGL(k_plan_mark, dim3(grid0), dim3(kT), 0, s, ctl, sumsq, w, flags, K, blen, es, G, src,
+                           mask, list1, &ctl->list_n[1], cap);
+        hipLaunchKernelGGL(k_plan_advance, dim3(1), dim3(kT), 0, s, ctl, 1, 0, (int)grid0);
+        if (rounds > 1)
+            hipLaunchKernelGGL(k_plan_rest, dim3(1), dim3(kT), 0, s, ctl, sumsq, w, flags, K, blen, es, G, list0,
+                               list1, cap, mask, 1, rounds);
+        hipLaunchKernelGGL(k_plan_digest, dim3(grid0), dim3(kT), 0, s, ctl, mask, G);
+    }
+    const int n_digest = G > 0 ? (int)std::min<int64_t>((G + kT - 1) / kT, kPlanGrid) : 0;
+    hipLaunchKernelGGL(k_plan_final, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget,
+                       (unsigned long long)full_bytes, (unsigned long long)(G * K), n_digest);
+    return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
                        const Coeffs& w, uint32_t flags, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
                        hipStream_t s)
 {
     PlanCtl* ctl = ps.ctl;
-    const uint32_t es = (uint32_t)bt.esize;
-    hipLaunchKernelGGL(k_plan_init, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget);
-    if (bt.G > 0) {
-        const int64_t want = (bt.G + kT - 1) / kT;
-        const unsigned grid0 = (unsigned)std::min<int64_t>(want, kPlanGrid);
-        const unsigned gridL = 64;
-        const int rounds = bt.n_distinct_len;
-        for (int r = 0; r < std::min(rounds, 1); ++r) {
-            CandSrc src;
-            unsigned grid;
-            if (r == 0) {
-                src.list = nullptr;
-                src.list_n = nullptr;
-                src.cap = 0u;
-                grid = grid0;
-            } else {
-                src.list = ps.list[r & 1];
-                src.list_n = &ctl->list_n[r & 1];
-                src.cap = (unsigned)ps.list_cap;
-                grid = gridL;
-            }
-            const int nxt = (r + 1) & 1;
-            for (int d = 0; d < 8; ++d)
-                hipLaunchKernelGGL(k_plan_hist, dim3(grid), dim3(kT), 0, s, ctl, d, sumsq, w, flags, K,
-                                   bt.d_len, es, bt.G, src);
-            hipLaunchKernelGGL(k_plan_mark, dim3(grid), dim3(kT), 0, s, ctl, sumsq, w, flags, K, bt.d_len,
-                               es, bt.G, src, mask, ps.list[nxt], &ctl->list_n[nxt],
-                               (unsigned)ps.list_cap);
-            hipLaunchKernelGGL(k_plan_advance, dim3(1), dim3(kT), 0, s, ctl, nxt, r & 1, (int)grid);
-        }
-        if (rounds > 1)
-            hipLaunchKernelGGL(k_plan_rest, dim3(1), dim3(kT), 0, s, ctl, sumsq, w, flags, K, bt.d_len, es, bt.G,
-                               ps.list[0], ps.list[1], (unsigned)ps.list_cap, mask, 1, rounds);
-        const unsigned gridD = grid0;
-        hipLaunchKernelGGL(k_plan_digest, dim3(gridD), dim3(kT), 0, s, ctl, mask, bt.G);
-    }
-    const int n_digest = bt.G > 0 ? (int)std::min<int64_t>((bt.G + kT - 1) / kT, kPlanGrid) : 0;
-    hipLaunchKernelGGL(k_plan_final, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget,
-                       (unsigned long long)full_bytes, (unsigned long long)(bt.G * K), n_digest);
-    hipError_t e = hipGetLastError();
+    hipError_t e = enqueue_plan(ctl, ps.list[0], ps.list[1], (unsigned)ps.list_cap, bt.d_len, (uint32_t)bt.esize,
+                                bt.G, bt.n_distinct_len, K, sumsq, w, flags, budget, full_bytes, mask, s);
     if (e != hipSuccess)
         return e;
     return hipMemcpyAsync(ps.h_stats, ctl->stats, sizeof(ctl->stats), hipMemcpyDeviceToHost, s);
+}
+
+// ---------------------------------------------------------------- plan without allocation
+// The plan on a fixed device array instead of the cached workspace and
+// block table: for callers that cannot allocate device memory.  The array
+// holds, each at a 256-byte boundary: the control block, the layout's
+// tensor sizes, the first block of every tensor, the block lengths and the
+// two candidate lists.  Every call on a device shares that device's copy,
+// and each call rebuilds everything it reads from it.
+namespace {
+
+constexpr size_t kStaticPlanBytes = size_t(16) << 20;
+
+static __device__ __align__(256) unsigned char scratch[kStaticPlanBytes];
+
+// The address of `scratch` on each device (0 until the first call there).
+constexpr int kMaxDevices = 64;
+void* g_scratch_dev[kMaxDevices] = {};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// One workgroup: g0[t] = first block of tensor t (blocks of the tensors
+// before it), g0[T] = G.
+__global__ __launch_bounds__(kT) void k_static_g0(const int64_t* __restrict__ numel, int T, int64_t be,
+                                                  uint32_t* __restrict__ g0)
+{
+    __shared__ unsigned long long s_w[kT / 64];
+    __shared__ unsigned long long s_run;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    if (t == 0)
+        s_run = 0ull;
+    for (int base = 0; base < T; base += kT) {
+        const int q = base + t;
+        const unsigned long long nb = (q < T) ? (unsigned long long)((numel[q] + be - 1) / be) : 0ull;
+        unsigned long long incl = nb;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const unsigned long long y = __shfl_up(incl, (unsigned)off);
+            if (lane >= off)
+                incl += y;
+        }
+        __syncthreads();  // s_run of the previous chunk is final; s_w is free
+        if (lane == 63)
+            s_w[wave] = incl;
+        __syncthreads();
+        unsigned long long before = s_run;
+        for (int v = 0; v < wave; ++v)
+            before += s_w[v];
+        if (q < T)
+            g0[q] = (uint32_t)(before + incl - nb);
+        __syncthreads();
+        if (t == kT - 1)
+            s_run = before + incl;
+    }
+    __syncthreads();
+    if (t == 0)
+        g0[T] = (uint32_t)s_run;
+}
+
+// blen[g] = elements of block g: the tensor t holding g is the last one
+// with g0[t] <= g (tensors without elements have no blocks).
+__global__ __launch_bounds__(kT) void k_static_blen(const int64_t* __restrict__ numel, const uint32_t* __restrict__ g0,
+                                                    int T, int64_t be, int64_t G, uint32_t* __restrict__ blen)
+{
+    const int64_t g = (int64_t)blockIdx.x * kT + threadIdx.x;
+    if (g >= G)
+        return;
+    int lo = 0, hi = T - 1;  // g0[lo] <= g holds for lo = 0
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if ((int64_t)g0[mid] <= g)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    const int64_t left = numel[lo] - (g - (int64_t)g0[lo]) * be;
+    blen[g] = (uint32_t)(left < be ? left : be);
+}
+
+}  // namespace
+
+int64_t static_plan_bytes(int64_t n_tensors, int64_t G, int64_t n_short, int K)
+{
+    const int64_t cap = (int64_t)K * std::max<int64_t>(n_short, 1);
+    return (int64_t)(align256(sizeof(PlanCtl)) + align256(sizeof(int64_t) * (size_t)n_tensors) +
+                     align256(sizeof(uint32_t) * (size_t)(n_tensors + 1)) + align256(sizeof(uint32_t) * (size_t)G) +
+                     2 * align256(sizeof(uint32_t) * (size_t)cap));
+}
+
+int64_t static_plan_limit() { return (int64_t)kStaticPlanBytes; }
+
+hipError_t static_plan_scratch(void** ptr)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= kMaxDevices)
+        return hipErrorInvalidDevice;
+    if (g_scratch_dev[dev] == nullptr) {
+        void* p = nullptr;
+        if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess)
+            return e;
+        if (p == nullptr)
+            return hipErrorInvalidSymbol;
+        g_scratch_dev[dev] = p;
+    }
+    *ptr = g_scratch_dev[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_plan_static(void* ws, const int64_t* numel, int32_t n_tensors, int64_t block_elems, uint32_t es,
+                              int64_t G, int64_t n_short, int K, const float* sumsq, const Coeffs& w, uint32_t flags,
+                              uint64_t budget, uint64_t full_bytes, uint32_t* mask, uint64_t* stats,
+                              hipStream_t s)
+{
+    const int64_t cap = (int64_t)K * std::max<int64_t>(n_short, 1);
+    char* p = static_cast<char*>(ws);
+    PlanCtl* ctl = reinterpret_cast<PlanCtl*>(p);
+    p += align256(sizeof(PlanCtl));
+    int64_t* d_numel = reinterpret_cast<int64_t*>(p);
+    p += align256(sizeof(int64_t) * (size_t)n_tensors);
+    uint32_t* g0 = reinterpret_cast<uint32_t*>(p);
+    p += align256(sizeof(uint32_t) * (size_t)(n_tensors + 1));
+    uint32_t* blen = reinterpret_cast<uint32_t*>(p);
+    p += align256(sizeof(uint32_t) * (size_t)G);
+    uint32_t* list0 = reinterpret_cast<uint32_t*>(p);
+    p += align256(sizeof(uint32_t) * (size_t)cap);
+    uint32_t* list1 = reinterpret_cast<uint32_t*>(p);
+    hipError_t e;
+    if (G > 0) {
+        if ((e = hipMemcpyAsync(d_numel, numel, sizeof(int64_t) * (size_t)n_tensors, hipMemcpyHostToDevice, s)) !=
+            hipSuccess)
+            return e;
+        hipLaunchKernelGGL(k_static_g0, dim3(1), dim3(kT), 0, s, d_numel, (int)n_tensors, block_elems, g0);
+        hipLaunchKernelGGL(k_static_blen, dim3((unsigned)((G + kT - 1) / kT)), dim3(kT), 0, s, d_numel, g0,
+                           (int)n_tensors, block_elems, G, blen);
+    }
+    // n_short + 1 bounds the distinct block lengths, hence the rounds
+    if ((e = enqueue_plan(ctl, list0, list1, (unsigned)cap, blen, es, G, (int)std::min<int64_t>(n_short + 1, 1 << 30),
+                          K, sumsq, w, flags, budget, full_bytes, mask, s)) != hipSuccess)
+        return e;
+    if ((e = hipMemcpyAsync(stats, ctl->stats, sizeof(ctl->stats), hipMemcpyDeviceToHost, s)) != hipSuccess)
+        return e;
+    return hipStreamSynchronize(s);
 }
 
 hipError_t plan_ctl_alloc(PlanCtl** ctl) { return hipMalloc((void**)ctl, sizeof(PlanCtl)); }

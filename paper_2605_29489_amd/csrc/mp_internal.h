@@ -80,6 +80,20 @@ hipError_t launch_index(const BlockTable& bt, const void* base, const ExpertPtrs
 hipError_t launch_index_ties(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
                              double density, float* sumsq, uint32_t* tau, hipStream_t s, bool delta = false);
 
+// Algorithm 1 without allocation (k_plan.hip): everything the kernels need
+// beyond the caller's buffers lives in a fixed device array of
+// static_plan_limit() bytes.  static_plan_bytes() is what a layout needs;
+// static_plan_scratch() returns the array's address on the current device
+// (looked up once per device); launch_plan_static() enqueues the plan on it,
+// reads the seven stats words back into `stats` and synchronises `s`.
+int64_t static_plan_bytes(int64_t n_tensors, int64_t G, int64_t n_short, int K);
+int64_t static_plan_limit();
+hipError_t static_plan_scratch(void** ptr);
+hipError_t launch_plan_static(void* ws, const int64_t* numel, int32_t n_tensors, int64_t block_elems, uint32_t es,
+                              int64_t G, int64_t n_short, int K, const float* sumsq, const Coeffs& w, uint32_t flags,
+                              uint64_t budget, uint64_t full_bytes, uint32_t* mask, uint64_t* stats,
+                              hipStream_t s);
+
 // Touched elements per (tensor, expert) of a mask: cov[t * K + i] (device;
 // k_plan.hip).
 hipError_t launch_coverage(const BlockTable& bt, int K, const uint32_t* mask, unsigned long long* cov,

@@ -142,3 +142,21 @@ def test_argument_errors_before_any_device_call(mp):
     big = mp.Layout([4096 * (1 << 28)], 4096, mp.MP_BF16)
     assert lib.mp_index_blocks(big.ref, None, ptrs, 32, 0, None, None) == mp.MP_E_ARG
     assert "32-bit" in mp.mp_last_error()
+
+
+def test_plan_noalloc_rejects_a_layout_beyond_its_fixed_array(mp):
+    # 5 million blocks need 20 MB of block lengths, more than the plan's
+    # fixed 16 MiB device array: refused on the host, before any device work,
+    # with the sizes in the message (no GPU is touched)
+    lib = mp.lib
+    st = mp.mp_plan_stats()
+    w = (C.c_float * 1)(1.0)
+    L = mp.Layout([4096 * 5_000_000], 4096, mp.MP_BF16)
+    rc = lib.mp_plan_noalloc(L.ref, 1, None, w, 0, 0, None, C.byref(st), None)
+    assert rc == mp.MP_E_UNSUPPORTED
+    msg = lib.mp_last_error().decode()
+    assert "16777216" in msg and "20019712" in msg
+    # argument errors come first, as in mp_plan
+    assert lib.mp_plan_noalloc(L.ref, 40, None, w, 0, 0, None, C.byref(st), None) == mp.MP_E_ARG
+    assert lib.mp_plan_noalloc(L.ref, 1, None, w, 0, 8, None, C.byref(st), None) == mp.MP_E_UNSUPPORTED
+
