@@ -36,6 +36,8 @@ def lib():
                                 C.c_int32, C.c_void_p]
         L.orc_plan.argtypes = [C.c_int64, i64p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
                                C.c_uint64, C.c_uint32, C.c_void_p, C.c_void_p]
+        L.orc_plan_tensors.argtypes = [C.c_int32, i64p, C.c_int64, C.c_int32, C.c_int32, C.c_void_p,
+                                       C.c_uint64, C.c_uint32, C.c_void_p, C.c_void_p]
         L.orc_merge_avg.argtypes = [C.c_int64, i64p, i64p, C.c_int32, C.c_void_p, C.POINTER(C.c_void_p),
                                     C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p]
         L.orc_merge_avg_renorm.argtypes = L.orc_merge_avg.argtypes
@@ -110,6 +112,8 @@ class Blocks:
                             self.tensor.ctypes.data_as(C.POINTER(C.c_int32)),
                             self.elem0.ctypes.data_as(C.POINTER(C.c_int64))), "blocks")
         self.G = int(G)
+        self.numel = np.ascontiguousarray(numel, np.int64)
+        self.block_elems = int(block_elems)
 
 
 def index(blocks: Blocks, dtype, base, experts, doff=None, ids=None, delta=False):
@@ -131,17 +135,22 @@ def index(blocks: Blocks, dtype, base, experts, doff=None, ids=None, delta=False
 
 def plan(blocks: Blocks, dtype, K: int, sumsq, w, budget: int, flags: int = 0):
     """Algorithm 1; returns (mask uint32[G], stats dict).  sumsq None: no
-    catalog, the deterministic fallback (every unit's statistic 1)."""
+    block catalog, the deterministic tensor-level fallback (orc_plan_tensors)."""
     L = lib()
-    if sumsq is not None:
-        sumsq = np.ascontiguousarray(sumsq, np.float32).reshape(-1)
-        assert sumsq.size == blocks.G * K
     w = np.ascontiguousarray(w, np.float32)
     assert w.size == K
-    l_a, l_p = _i64(blocks.len)
     mask = np.zeros(blocks.G, np.uint32)
     st = np.zeros(5, np.uint64)
-    _check(L.orc_plan(blocks.G, l_p, _dt(dtype), K, None if sumsq is None else sumsq.ctypes.data, w.ctypes.data,
+    if sumsq is None:
+        n_a, n_p = _i64(blocks.numel)
+        _check(L.orc_plan_tensors(len(blocks.numel), n_p, blocks.block_elems, _dt(dtype), K, w.ctypes.data,
+                                  int(budget), flags, mask.ctypes.data, st.ctypes.data), "plan (tensor level)")
+        return mask, dict(cost=int(st[0]), n_selected=int(st[1]), full_bytes=int(st[2]),
+                          digest=int(st[3]), n_units=int(st[4]))
+    sumsq = np.ascontiguousarray(sumsq, np.float32).reshape(-1)
+    assert sumsq.size == blocks.G * K
+    l_a, l_p = _i64(blocks.len)
+    _check(L.orc_plan(blocks.G, l_p, _dt(dtype), K, sumsq.ctypes.data, w.ctypes.data,
                       int(budget), flags, mask.ctypes.data, st.ctypes.data), "plan")
     return mask, dict(cost=int(st[0]), n_selected=int(st[1]), full_bytes=int(st[2]),
                       digest=int(st[3]), n_units=int(st[4]))

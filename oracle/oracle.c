@@ -248,7 +248,7 @@ int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
              uint32_t* mask, uint64_t* stats)
 {
     int s = elem_bytes(dtype);
-    if (s == 0 || K < 1 || K > 32 || G < 0 || (flags & ~3u) != 0)
+    if (s == 0 || K < 1 || K > 32 || G < 0 || (flags & ~3u) != 0 || sumsq == NULL)
         return -1;
     if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
         return -1;
@@ -262,9 +262,7 @@ int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
         int32_t i = (int32_t)(u % K);
         uint64_t c = (uint64_t)len[u / K] * (uint64_t)s;
         full += c;
-        /* no catalog (sumsq NULL): the planner's deterministic fallback
-           gives every unit the same statistic, 1 */
-        const float S = sumsq ? sumsq[u] : 1.0f;
+        const float S = sumsq[u];
         if ((flags & 2u) && S == 0.0f)
             continue;
         float w2 = w[i] * w[i];
@@ -299,6 +297,89 @@ int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
     stats[2] = full;
     stats[3] = orc_mix64(D ^ C);
     stats[4] = (uint64_t)nu;
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Planning without block metadata (Section 3, Planner: a deterministic */
+/* tensor-level fallback when block metadata are missing; Algorithm 1   */
+/* with fallback scores).  Reading: a unit is (expert i, tensor t) with */
+/* uid t*K + i; its cost is the tensor's stored bytes, numel_t * s; no   */
+/* statistic is known, so every unit's statistic is 1 and its score is  */
+/* fl32(w_i * w_i) (per byte: fl32(score / cost) in fp64); tensors       */
+/* without elements are not candidates.  Algorithm 1 then runs over     */
+/* these units unchanged: decreasing score, ties by uid (tensor, then    */
+/* expert), take a unit iff C + c <= B, continue past the ones that do   */
+/* not fit.  A selected unit sets expert i's bit in every block of      */
+/* tensor t, so a tensor is never split.  Stats and digest are those of */
+/* the resulting block mask (n_selected counts block units).  The skip-  */
+/* zero option has nothing to skip (no statistic is zero).              */
+/* ------------------------------------------------------------------ */
+int orc_plan_tensors(int32_t n_tensors, const int64_t* numel, int64_t block_elems, int32_t dtype,
+                     int32_t K, const float* w, uint64_t budget, uint32_t flags, uint32_t* mask,
+                     uint64_t* stats)
+{
+    int s = elem_bytes(dtype);
+    int64_t G = orc_num_blocks(n_tensors, numel, block_elems);
+    if (s == 0 || K < 1 || K > 32 || G < 0 || (flags & ~3u) != 0)
+        return -1;
+    if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
+        return -1;
+    int64_t nu = (int64_t)n_tensors * K;
+    cand_t* q = (cand_t*)malloc(sizeof(cand_t) * (size_t)(nu > 0 ? nu : 1));
+    if (!q)
+        return -2;
+    uint64_t full = 0;
+    int64_t nq = 0;
+    for (int32_t t = 0; t < n_tensors; ++t) {
+        const uint64_t c = (uint64_t)numel[t] * (uint64_t)s;
+        full += c * (uint64_t)K;
+        if (numel[t] == 0)
+            continue;
+        for (int32_t i = 0; i < K; ++i) {
+            float sc = (w[i] * w[i]) * 1.0f;
+            if (flags & 1u)
+                sc = (float)((double)sc / (double)c);
+            q[nq].score = sc;
+            q[nq].uid = (uint32_t)((int64_t)t * K + i);
+            ++nq;
+        }
+    }
+    qsort(q, (size_t)nq, sizeof(cand_t), cand_cmp);
+    /* per-tensor selection words, then the greedy of Algorithm 1 */
+    uint32_t* tsel = (uint32_t*)calloc((size_t)(n_tensors > 0 ? n_tensors : 1), sizeof(uint32_t));
+    if (!tsel) {
+        free(q);
+        return -2;
+    }
+    uint64_t C = 0;
+    for (int64_t r = 0; r < nq; ++r) {
+        const uint32_t u = q[r].uid;
+        const int32_t t = (int32_t)(u / (uint32_t)K), i = (int32_t)(u % (uint32_t)K);
+        const uint64_t c = (uint64_t)numel[t] * (uint64_t)s;
+        if (C + c <= budget) {
+            tsel[t] |= 1u << i;
+            C += c;
+        }
+    }
+    free(q);
+    /* every block of tensor t takes the tensor's selection word */
+    uint64_t nsel = 0, D = 0;
+    int64_t g = 0;
+    for (int32_t t = 0; t < n_tensors; ++t) {
+        const int64_t nb = (numel[t] + block_elems - 1) / block_elems;
+        for (int64_t j = 0; j < nb; ++j, ++g) {
+            mask[g] = tsel[t];
+            nsel += (uint64_t)__builtin_popcount(tsel[t]);
+            D += orc_mix64(((uint64_t)g << 32) | (uint64_t)mask[g]);
+        }
+    }
+    free(tsel);
+    stats[0] = C;
+    stats[1] = nsel;
+    stats[2] = full;
+    stats[3] = orc_mix64(D ^ C);
+    stats[4] = (uint64_t)(G * K);
     return 0;
 }
 

@@ -37,16 +37,23 @@ int orc_blocks(int32_t n_tensors, const int64_t* numel, int64_t block_elems,
 int orc_index(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,
               const void* base, const void* const* experts, int32_t K, float* sumsq);
 
-/* Algorithm 1 (PlanGen), literal: score, sort, skip-and-continue greedy.
- * sumsq NULL (no block catalog): every unit's statistic is 1, so units rank
- * by w_i^2 and then by uid, i.e. blocks in layout order (Section 3's
- * deterministic fallback when block metadata are missing).
+/* Algorithm 1 (PlanGen), literal: score, sort, skip-and-continue greedy
+ * over the (expert, block) units of a block catalog (sumsq, not NULL).
  * flags: 1 = score per byte of cost, 2 = units with a zero sum of squares
  * are not candidates.  stats[0]=selected cost, [1]=selected units, [2]=full
  * cost, [3]=digest, [4]=number of units. */
 int orc_plan(int64_t G, const int64_t* len, int32_t dtype, int32_t K,
              const float* sumsq, const float* w, uint64_t budget, uint32_t flags,
              uint32_t* mask, uint64_t* stats);
+
+/* Section 3's deterministic tensor-level fallback when block metadata are
+ * missing: Algorithm 1 over (expert, tensor) units with statistic 1 (score
+ * w_i^2, ties by tensor then expert), cost = the tensor's bytes; a selected
+ * unit sets the expert's bit in every block of the tensor.  mask: [G]
+ * block words; stats as orc_plan's, for the block mask. */
+int orc_plan_tensors(int32_t n_tensors, const int64_t* numel, int64_t block_elems, int32_t dtype,
+                     int32_t K, const float* w, uint64_t budget, uint32_t flags, uint32_t* mask,
+                     uint64_t* stats);
 
 /* Mask-aware merge operators (Eq. 4 with Appendix A.1's operators). */
 int orc_merge_avg(int64_t nb, const int64_t* doff, const int64_t* len, int32_t dtype,

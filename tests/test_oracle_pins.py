@@ -289,21 +289,85 @@ def test_plan_skip_zero_drops_exactly_the_zero_units():
     assert int(m[0]) == 0 and st["cost"] == 0 and st["n_selected"] == 0
 
 
-def test_plan_without_catalog_takes_units_by_weight_then_layout_order():
-    # Section 3's fallback when block metadata are missing: with equal block
-    # costs and equal weights the plan is the longest prefix of units in uid
-    # (layout) order that fits; a heavier expert's units all come first.
-    numel = [4096 * 5, 4096 * 3]
-    b = oracle.Blocks(numel, 4096)
-    K = 3
-    c = 4096 * 2
-    for n_fit in (0, 1, 7, 10, 24):
-        m, st = oracle.plan(b, "bf16", K, None, [1.0] * K, n_fit * c + c // 2)
-        sel = [u for u in range(b.G * K) if (m[u // K] >> (u % K)) & 1]
-        assert sel == list(range(n_fit)) and st["cost"] == n_fit * c
-    m, st = oracle.plan(b, "bf16", K, None, [1.0, 2.0, 1.0], 9 * c)
-    sel = [u for u in range(b.G * K) if (m[u // K] >> (u % K)) & 1]
-    assert sel == sorted([g * K + 1 for g in range(8)] + [0])  # expert 1's units, then uid 0
+def test_plan_tensor_fallback_worked_examples():
+    # Section 3's tensor-level fallback, hand-worked cases
+    ex = json.load(open(os.path.join(GOLD, "plan_tensor_fallback.json")))
+    b = oracle.Blocks(ex["numel"], ex["block_elems"])
+    for c in ex["cases"]:
+        m, st = oracle.plan(b, ex["dtype"], c["K"], None, c["w"], c["budget"], flags=c["flags"])
+        assert [int(x) for x in m] == c["mask"], c["name"]
+        assert st["cost"] == c["cost"] and st["n_selected"] == c["n_selected"], c["name"]
+        assert st["full_bytes"] == c["full_bytes"] and st["n_units"] == b.G * c["K"]
+        D = sum(oracle.mix64((g << 32) | int(m[g])) for g in range(b.G)) % (1 << 64)
+        assert st["digest"] == oracle.mix64(D ^ st["cost"])
+
+
+def _block_units_fallback(b, K, w, budget, s):
+    # planted mistake: the greedy over (expert, block) units with statistic 1
+    order = sorted(range(b.G * K), key=lambda u: (-(np.float32(w[u % K]) * np.float32(w[u % K])), u))
+    m = np.zeros(b.G, np.uint32)
+    C = 0
+    for u in order:
+        c = int(b.len[u // K]) * s
+        if C + c <= budget:
+            m[u // K] |= np.uint32(1 << (u % K))
+            C += c
+    return m
+
+
+def test_plan_tensor_fallback_never_splits_a_tensor_and_is_sound():
+    # At every budget: each tensor's blocks carry one selection word (no
+    # tensor is split), C(A) <= B (Prop. 1), and every unselected (expert,
+    # tensor) unit overflows the final cost (skip-and-continue).  Ranking:
+    # a heavier expert's tensor before a lighter one's; equal weights in
+    # tensor order.  The block-unit greedy fails the first property.
+    rng = np.random.default_rng(71)
+    split_seen = False
+    for trial in range(60):
+        T = int(rng.integers(1, 7))
+        numel = [int(x) * 4 for x in rng.integers(0, 9, T)]
+        be = 8
+        b = oracle.Blocks(numel, be)
+        K = int(rng.integers(1, 5))
+        w = [float(x) for x in rng.choice([0.5, 1.0, 1.0, 2.0], K)]
+        flags = int(rng.integers(0, 4))
+        full = sum(numel) * 4 * K
+        for B in sorted(set([0, full, full + 1] + [int(x) for x in rng.integers(0, full + 1, 8)])):
+            m, st = oracle.plan(b, "f32", K, None, w, B, flags=flags)
+            assert st["cost"] <= B
+            words = {}
+            for g in range(b.G):
+                words.setdefault(int(b.tensor[g]), set()).add(int(m[g]))
+            assert all(len(v) == 1 for v in words.values())
+            tsel = {t: v.pop() for t, v in words.items()}
+            cost = sum(numel[t] * 4 * bin(x).count("1") for t, x in tsel.items())
+            assert cost == st["cost"]
+            for t, x in tsel.items():
+                for i in range(K):
+                    if not (x >> i) & 1:
+                        assert st["cost"] + numel[t] * 4 > B
+            bad = _block_units_fallback(b, K, w, B, 4)
+            for t in range(T):
+                gs = [g for g in range(b.G) if b.tensor[g] == t]
+                if len(set(int(bad[g]) for g in gs)) > 1:
+                    split_seen = True
+    assert split_seen  # the planted block-unit greedy does split tensors
+
+
+def test_plan_tensor_fallback_weight_order():
+    # Equal tensor sizes: with weights (1, 2) every tensor of expert 1 comes
+    # before any tensor of expert 0, and within an expert tensors go in
+    # layout order, so a budget of n tensors selects expert 1's first n.
+    numel = [32] * 5
+    b = oracle.Blocks(numel, 8)
+    c = 32 * 2
+    for n in range(0, 11):
+        m, st = oracle.plan(b, "bf16", 2, None, [1.0, 2.0], n * c + c // 2)
+        t_e1 = [t for t in range(5) if (int(m[4 * t]) >> 1) & 1]
+        t_e0 = [t for t in range(5) if int(m[4 * t]) & 1]
+        assert t_e1 == list(range(min(n, 5)))
+        assert t_e0 == list(range(max(0, n - 5)))
+        assert st["cost"] == n * c
 
 
 def _random_plan_case(rng, G, K, uniform, ties=False):
