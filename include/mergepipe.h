@@ -166,9 +166,15 @@ int mp_index_ties(const mp_layout* layout, const void* base,
  *   mix64((g << 32) | mask[g]) mod 2^64 and mix64 the SplitMix64 output
  *   function.  B >= full_bytes yields the all-ones mask.
  * Synchronises `stream` before returning (the one blocking point). */
-/* sumsq may be NULL when no block catalog exists: the planner then falls back
- * (Section 3) to a deterministic order, every unit's statistic being 1 --
- * units by w_i^2, ties by uid, i.e. whole blocks in layout order. */
+/* sumsq may be NULL when no block catalog exists: the planner then falls
+ * back to Section 3's deterministic tensor-level plan.  A unit is (expert
+ * i, tensor t), with uid t*K + i and cost the tensor's bytes; every unit's
+ * statistic is 1, so the score is float(w_i * w_i) (per byte: divided by
+ * the cost as above); tensors without elements are not candidates; the
+ * order and the skip-and-continue greedy are those above.  A selected unit
+ * sets bit i in the mask word of every block of tensor t: no tensor is
+ * split.  The stats describe the block mask (n_selected counts (expert,
+ * block) units).  MP_E_UNSUPPORTED if a tensor has 2^32 or more elements. */
 int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq,
             const float* w, uint64_t budget_bytes, uint32_t flags,
             uint32_t* mask, mp_plan_stats* stats, void* stream);
@@ -179,14 +185,15 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq,
  * synchronisation are those of mp_plan, and it runs the same kernels: mask
  * and stats are equal bit for bit.  It calls no hipMalloc, hipFree or
  * other allocation routine and keeps no per-layout cache.  Instead, the
- * control block, the layout's tensor sizes, the first block of each
- * tensor, the block lengths and the two candidate lists live in one fixed
- * device array of 16 MiB (16,777,216 bytes), which each device the library
- * runs on holds until the process ends.  A layout needs the sum of these
- * sizes, each rounded up to 256 bytes: about 19 KB for the control block,
- * 8 * n_tensors, 4 * (n_tensors + 1), 4 * G, and twice 4 * K * max(1, number
- * of short blocks) -- 1.6 MB for a 1.5B-parameter layout cut into 4096-
- * element blocks, so up to about four million blocks fit.  A larger layout
+ * control block, the layout's tensor sizes (twice), the first block of
+ * each tensor, the tensors' selection words, the block lengths and the two
+ * candidate lists live in one fixed device array of 16 MiB (16,777,216
+ * bytes), which each device the library runs on holds until the process
+ * ends.  A layout needs the sum of these sizes, each rounded up to 256
+ * bytes: about 19 KB for the control block, 8 * n_tensors, 4 * (n_tensors +
+ * 1), twice 4 * n_tensors, 4 * G, and twice 4 * K * max(1, n_tensors) --
+ * 1.6 MB for a 1.5B-parameter layout cut into 4096-element blocks, so up
+ * to about four million blocks fit.  A larger layout
  * gets MP_E_UNSUPPORTED (with the sizes in mp_last_error) before anything
  * is enqueued.  The array keeps the last call's contents; each call
  * rebuilds everything it reads from it.  Calls hold the library's lock

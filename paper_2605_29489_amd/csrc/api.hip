@@ -89,6 +89,8 @@ void free_table(BlockTable& bt)
     (void)hipFree(bt.d_elem0);
     (void)hipFree(bt.d_chunk);
     (void)hipFree(bt.d_tnumel);
+    (void)hipFree(bt.d_tlen);
+    (void)hipFree(bt.d_g0);
     (void)hipSetDevice(cur);
 }
 
@@ -100,6 +102,7 @@ void free_ws(int dev, DeviceWs& w)
     (void)hipFree(w.plan.ctl);
     (void)hipFree(w.plan.list[0]);
     (void)hipFree(w.plan.list[1]);
+    (void)hipFree(w.plan.tmask);
     (void)hipHostFree(w.plan.h_stats);
     (void)hipFree(w.counters);
     (void)hipHostFree(w.h_counters);
@@ -211,13 +214,26 @@ int get_table(const mp_layout* L, int esize, BlockTable** out)
         a = z;
     }
     bt->n_chunks = (int64_t)chunks.size();
+    // the tensor-level plan's table
+    std::vector<uint32_t> tlen((size_t)L->n_tensors), tg0((size_t)L->n_tensors + 1, 0);
+    std::set<uint32_t> tl;
+    for (int32_t t = 0; t < L->n_tensors; ++t) {
+        if (L->numel[t] >= ((int64_t)1 << 32))
+            bt->tlen_fits = false;
+        tlen[(size_t)t] = (uint32_t)L->numel[t];
+        tl.insert(tlen[(size_t)t]);
+        tg0[(size_t)t + 1] = tg0[(size_t)t] + (uint32_t)((L->numel[t] + L->block_elems - 1) / L->block_elems);
+    }
+    bt->n_distinct_tlen = (int)tl.size();
     if (G > 0) {
         if ((e = hipMalloc((void**)&bt->d_off, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
             (e = hipMalloc((void**)&bt->d_len, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
             (e = hipMalloc((void**)&bt->d_tensor, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
             (e = hipMalloc((void**)&bt->d_elem0, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
             (e = hipMalloc((void**)&bt->d_chunk, sizeof(uint4) * chunks.size())) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_tnumel, sizeof(uint64_t) * tnumel.size())) != hipSuccess) {
+            (e = hipMalloc((void**)&bt->d_tnumel, sizeof(uint64_t) * tnumel.size())) != hipSuccess ||
+            (e = hipMalloc((void**)&bt->d_tlen, sizeof(uint32_t) * tlen.size())) != hipSuccess ||
+            (e = hipMalloc((void**)&bt->d_g0, sizeof(uint32_t) * tg0.size())) != hipSuccess) {
             free_table(*bt);
             return fail(MP_E_NOMEM, "block table allocation failed: %s", hipGetErrorString(e));
         }
@@ -226,7 +242,9 @@ int get_table(const mp_layout* L, int esize, BlockTable** out)
             (e = hipMemcpy(bt->d_tensor, tens.data(), sizeof(uint32_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
             (e = hipMemcpy(bt->d_elem0, e0.data(), sizeof(uint64_t) * (size_t)G, hipMemcpyHostToDevice)) != hipSuccess ||
             (e = hipMemcpy(bt->d_chunk, chunks.data(), sizeof(uint4) * chunks.size(), hipMemcpyHostToDevice)) != hipSuccess ||
-            (e = hipMemcpy(bt->d_tnumel, tnumel.data(), sizeof(uint64_t) * tnumel.size(), hipMemcpyHostToDevice)) != hipSuccess) {
+            (e = hipMemcpy(bt->d_tnumel, tnumel.data(), sizeof(uint64_t) * tnumel.size(), hipMemcpyHostToDevice)) != hipSuccess ||
+            (e = hipMemcpy(bt->d_tlen, tlen.data(), sizeof(uint32_t) * tlen.size(), hipMemcpyHostToDevice)) != hipSuccess ||
+            (e = hipMemcpy(bt->d_g0, tg0.data(), sizeof(uint32_t) * tg0.size(), hipMemcpyHostToDevice)) != hipSuccess) {
             free_table(*bt);
             return hip_fail(e, "block table upload");
         }
@@ -756,7 +774,22 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float*
     DeviceWs* ws = nullptr;
     if ((rc = get_table(layout, es, &bt)) || (rc = get_ws(&ws)))
         return rc;
-    if ((rc = ensure_lists(ws->plan, (int64_t)K * std::max<int64_t>(bt->n_short, 1))))
+    if (sumsq == nullptr) {
+        // tensor-level plan: a selection word per tensor, K units per tensor
+        if (!bt->tlen_fits)
+            return fail(MP_E_UNSUPPORTED, "the tensor-level plan needs tensors of fewer than 2^32 elements");
+        if (bt->n_tensors > ws->plan.tmask_cap) {
+            (void)hipFree(ws->plan.tmask);
+            ws->plan.tmask = nullptr;
+            ws->plan.tmask_cap = 0;
+            hipError_t he = hipMalloc((void**)&ws->plan.tmask, sizeof(uint32_t) * (size_t)bt->n_tensors);
+            if (he != hipSuccess)
+                return fail(MP_E_NOMEM, "tensor selection words: %s", hipGetErrorString(he));
+            ws->plan.tmask_cap = bt->n_tensors;
+        }
+    }
+    const int64_t per_k = sumsq != nullptr ? bt->n_short : bt->n_tensors;
+    if ((rc = ensure_lists(ws->plan, (int64_t)K * std::max<int64_t>(per_k, 1))))
         return rc;
     // the blocks partition the checkpoint: their lengths sum to P
     const uint64_t full = (uint64_t)bt->P * (uint64_t)es * (uint64_t)K;
@@ -806,6 +839,10 @@ int mp_plan_noalloc(const mp_layout* layout, int32_t K, const float* sumsq, cons
     }
     if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
         return fail(MP_E_ARG, "K * G does not fit 32-bit unit ids");
+    if (sumsq == nullptr)
+        for (int32_t t = 0; t < layout->n_tensors; ++t)
+            if (layout->numel[t] >= ((int64_t)1 << 32))
+                return fail(MP_E_UNSUPPORTED, "the tensor-level plan needs tensors of fewer than 2^32 elements");
     const int64_t need = static_plan_bytes(layout->n_tensors, G, n_short, K);
     if (need > static_plan_limit())
         return fail(MP_E_UNSUPPORTED,

@@ -75,10 +75,17 @@ __device__ inline unsigned long long unit_key(float S, float w, uint32_t uid, un
     return ((unsigned long long)(~__float_as_uint(sc)) << 32) | uid;
 }
 
-__device__ inline bool plan_skips(float S, uint32_t flags) { return (flags & kPlanSkipZero) && S == 0.0f; }
+// Units that are not candidates: a zero statistic under the skip-zero
+// option, and (tensor-level plans) tensors without elements, which have no
+// block to select.
+__device__ inline bool plan_skips(float S, unsigned long long c, uint32_t flags)
+{
+    return ((flags & kPlanSkipZero) && S == 0.0f) || c == 0ull;
+}
 
-// A unit's catalog statistic; without a catalog (sumsq null) the fallback
-// gives every unit 1, so the plan takes units by weight, then in uid order.
+// A unit's catalog statistic; the tensor-level plan (no block catalog,
+// sumsq null) gives every unit 1, so it takes units by weight, then in uid
+// order.
 __device__ inline float plan_stat(const float* __restrict__ sumsq, uint32_t uid)
 {
     return sumsq != nullptr ? sumsq[uid] : 1.0f;
@@ -221,7 +228,7 @@ __global__ __launch_bounds__(kT) void k_plan_hist(PlanCtl* ctl, int d, const flo
             for (int i = 0; i < K; ++i) {
                 const uint32_t uid = (uint32_t)(g * K + i);
                 const float S = plan_stat(sumsq, uid);
-                if (plan_skips(S, flags))
+                if (plan_skips(S, c, flags))
                     continue;
                 const unsigned long long key = unit_key(S, w.v[i], uid, c, flags);
                 if (d == 0 || ((key ^ prefix) >> hi_shift) == 0)
@@ -300,7 +307,7 @@ __global__ __launch_bounds__(kT) void k_plan_mark(PlanCtl* ctl, const float* __r
             for (int i = 0; i < K; ++i) {
                 const uint32_t uid = (uint32_t)(g * K + i);
                 const float S = plan_stat(sumsq, uid);
-                if (plan_skips(S, flags))
+                if (plan_skips(S, c, flags))
                     continue;
                 const unsigned long long key = unit_key(S, w.v[i], uid, c, flags);
                 if (all || key < keyp) {
@@ -589,9 +596,14 @@ namespace {
 // control block ctl and two candidate lists of cap uids each; `rounds`
 // bounds the number of rounds (the distinct block lengths, or any larger
 // number: the later rounds stop once the plan is done).
-hipError_t enqueue_plan(PlanCtl* ctl, uint32_t* list0, uint32_t* list1, unsigned cap, const uint32_t* blen,
-                        uint32_t es, int64_t G, int rounds, int K, const float* sumsq, const Coeffs& w,
-                        uint32_t flags, uint64_t budget, uint64_t full_bytes, uint32_t* mask, hipStream_t s)
+// Algorithm 1's selection over G "blocks" with lengths blen[G] (elements):
+// control block ctl, two candidate lists of cap uids each; `rounds` bounds
+// the number of rounds (the distinct lengths, or any larger number: the
+// later rounds stop once the plan is done).  Writes mask[G] and the
+// selected cost into ctl; stats come from one of the finals below.
+void enqueue_select(PlanCtl* ctl, uint32_t* list0, uint32_t* list1, unsigned cap, const uint32_t* blen,
+                    uint32_t es, int64_t G, int rounds, int K, const float* sumsq, const Coeffs& w,
+                    uint32_t flags, uint64_t budget, uint32_t* mask, hipStream_t s)
 {
     hipLaunchKernelGGL(k_plan_init, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget);
     if (G > 0) {
@@ -608,11 +620,88 @@ hipError_t enqueue_plan(PlanCtl* ctl, uint32_t* list0, uint32_t* list1, unsigned
         if (rounds > 1)
             hipLaunchKernelGGL(k_plan_rest, dim3(1), dim3(kT), 0, s, ctl, sumsq, w, flags, K, blen, es, G, list0,
                                list1, cap, mask, 1, rounds);
-        hipLaunchKernelGGL(k_plan_digest, dim3(grid0), dim3(kT), 0, s, ctl, mask, G);
     }
+}
+
+// Stats of a block-level plan: digest over mask[G], the units selected.
+hipError_t enqueue_block_final(PlanCtl* ctl, const uint32_t* mask, int64_t G, int K, uint64_t budget,
+                               uint64_t full_bytes, hipStream_t s)
+{
     const int n_digest = G > 0 ? (int)std::min<int64_t>((G + kT - 1) / kT, kPlanGrid) : 0;
+    if (G > 0)
+        hipLaunchKernelGGL(k_plan_digest, dim3((unsigned)n_digest), dim3(kT), 0, s, ctl, mask, G);
     hipLaunchKernelGGL(k_plan_final, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget,
                        (unsigned long long)full_bytes, (unsigned long long)(G * K), n_digest);
+    return hipGetLastError();
+}
+
+// Tensor-level plan: block g takes the selection word of its tensor t, the
+// last one with g0[t] <= g (tensors without elements have no blocks); per
+// workgroup, the selected block units and the digest terms.
+__global__ __launch_bounds__(kT) void k_plan_expand(PlanCtl* ctl, const uint32_t* __restrict__ tmask,
+                                                    const uint32_t* __restrict__ g0, int T, int64_t G,
+                                                    uint32_t* __restrict__ mask)
+{
+    __shared__ unsigned long long s_c[4], s_d[4];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    unsigned long long cnt = 0ull, dg = 0ull;
+    for (int64_t g = (int64_t)blockIdx.x * kT + t; g < G; g += (int64_t)gridDim.x * kT) {
+        int lo = 0, hi = T - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((int64_t)g0[mid] <= g)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        const uint32_t m = tmask[lo];
+        mask[g] = m;
+        cnt += (unsigned long long)__popc(m);
+        dg += mix64(((unsigned long long)g << 32) | m);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        cnt += __shfl_xor(cnt, off);
+        dg += __shfl_xor(dg, off);
+    }
+    if (lane == 0) {
+        s_c[wave] = cnt;
+        s_d[wave] = dg;
+    }
+    __syncthreads();
+    if (t == 0) {
+        ctl->part[1][blockIdx.x] = s_c[0] + s_c[1] + s_c[2] + s_c[3];
+        ctl->part[2][blockIdx.x] = s_d[0] + s_d[1] + s_d[2] + s_d[3];
+    }
+}
+
+__global__ __launch_bounds__(kT) void k_plan_final_tensors(PlanCtl* ctl, unsigned long long budget,
+                                                           unsigned long long full, unsigned long long n_units,
+                                                           int n_part)
+{
+    const unsigned long long cn = block_sum_parts(ctl, 1, n_part);
+    const unsigned long long dg = block_sum_parts(ctl, 2, n_part);
+    if (threadIdx.x != 0)
+        return;
+    ctl->stats[0] = budget;
+    ctl->stats[1] = ctl->sel_cost;
+    ctl->stats[2] = full;
+    ctl->stats[3] = cn;
+    ctl->stats[4] = n_units;
+    ctl->stats[5] = mix64(dg ^ ctl->sel_cost);
+    ctl->stats[6] = ctl->error;
+}
+
+// Stats of a tensor-level plan: expand tmask[T] to mask[G], then count and
+// digest the block mask.
+hipError_t enqueue_tensor_final(PlanCtl* ctl, const uint32_t* tmask, const uint32_t* g0, int T, int64_t G, int K,
+                                uint64_t budget, uint64_t full_bytes, uint32_t* mask, hipStream_t s)
+{
+    const int n_part = G > 0 ? (int)std::min<int64_t>((G + kT - 1) / kT, kPlanGrid) : 0;
+    if (G > 0)
+        hipLaunchKernelGGL(k_plan_expand, dim3((unsigned)n_part), dim3(kT), 0, s, ctl, tmask, g0, T, G, mask);
+    hipLaunchKernelGGL(k_plan_final_tensors, dim3(1), dim3(kT), 0, s, ctl, (unsigned long long)budget,
+                       (unsigned long long)full_bytes, (unsigned long long)(G * K), n_part);
     return hipGetLastError();
 }
 
@@ -623,8 +712,19 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
                        hipStream_t s)
 {
     PlanCtl* ctl = ps.ctl;
-    hipError_t e = enqueue_plan(ctl, ps.list[0], ps.list[1], (unsigned)ps.list_cap, bt.d_len, (uint32_t)bt.esize,
-                                bt.G, bt.n_distinct_len, K, sumsq, w, flags, budget, full_bytes, mask, s);
+    const uint32_t es = (uint32_t)bt.esize;
+    hipError_t e;
+    if (sumsq != nullptr) {
+        enqueue_select(ctl, ps.list[0], ps.list[1], (unsigned)ps.list_cap, bt.d_len, es, bt.G, bt.n_distinct_len, K,
+                       sumsq, w, flags, budget, mask, s);
+        e = enqueue_block_final(ctl, mask, bt.G, K, budget, full_bytes, s);
+    } else {
+        // no block catalog: the tensor-level plan, each tensor one unit per expert
+        const int64_t T = bt.n_tensors;
+        enqueue_select(ctl, ps.list[0], ps.list[1], (unsigned)ps.list_cap, bt.d_tlen, es, T, bt.n_distinct_tlen, K,
+                       nullptr, w, flags, budget, ps.tmask, s);
+        e = enqueue_tensor_final(ctl, ps.tmask, bt.d_g0, (int)T, bt.G, K, budget, full_bytes, mask, s);
+    }
     if (e != hipSuccess)
         return e;
     return hipMemcpyAsync(ps.h_stats, ctl->stats, sizeof(ctl->stats), hipMemcpyDeviceToHost, s);
@@ -650,9 +750,10 @@ void* g_scratch_dev[kMaxDevices] = {};
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // One workgroup: g0[t] = first block of tensor t (blocks of the tensors
-// before it), g0[T] = G.
+// before it), g0[T] = G; tlen[t] = elements of tensor t (below 2^32, checked
+// by the host when the tensor-level plan needs them).
 __global__ __launch_bounds__(kT) void k_static_g0(const int64_t* __restrict__ numel, int T, int64_t be,
-                                                  uint32_t* __restrict__ g0)
+                                                  uint32_t* __restrict__ g0, uint32_t* __restrict__ tlen)
 {
     __shared__ unsigned long long s_w[kT / 64];
     __shared__ unsigned long long s_run;
@@ -676,8 +777,10 @@ __global__ __launch_bounds__(kT) void k_static_g0(const int64_t* __restrict__ nu
         unsigned long long before = s_run;
         for (int v = 0; v < wave; ++v)
             before += s_w[v];
-        if (q < T)
+        if (q < T) {
             g0[q] = (uint32_t)(before + incl - nb);
+            tlen[q] = (uint32_t)numel[q];
+        }
         __syncthreads();
         if (t == kT - 1)
             s_run = before + incl;
@@ -709,12 +812,27 @@ __global__ __launch_bounds__(kT) void k_static_blen(const int64_t* __restrict__ 
 
 }  // namespace
 
+// Sizes of the parts of the fixed array a layout needs; the candidate lists
+// hold K units per tensor, which covers both plans (a block-level plan's
+// later rounds list only units of short blocks, at most one per tensor).
+namespace {
+struct StaticParts {
+    size_t ctl, numel, g0, tlen, tmask, blen, list;
+};
+StaticParts static_parts(int64_t n_tensors, int64_t G, int K)
+{
+    const int64_t cap = (int64_t)K * std::max<int64_t>(n_tensors, 1);
+    return {align256(sizeof(PlanCtl)), align256(sizeof(int64_t) * (size_t)n_tensors),
+            align256(sizeof(uint32_t) * (size_t)(n_tensors + 1)), align256(sizeof(uint32_t) * (size_t)n_tensors),
+            align256(sizeof(uint32_t) * (size_t)n_tensors), align256(sizeof(uint32_t) * (size_t)G),
+            align256(sizeof(uint32_t) * (size_t)cap)};
+}
+}  // namespace
+
 int64_t static_plan_bytes(int64_t n_tensors, int64_t G, int64_t n_short, int K)
 {
-    const int64_t cap = (int64_t)K * std::max<int64_t>(n_short, 1);
-    return (int64_t)(align256(sizeof(PlanCtl)) + align256(sizeof(int64_t) * (size_t)n_tensors) +
-                     align256(sizeof(uint32_t) * (size_t)(n_tensors + 1)) + align256(sizeof(uint32_t) * (size_t)G) +
-                     2 * align256(sizeof(uint32_t) * (size_t)cap));
+    const StaticParts a = static_parts(n_tensors, G, K);
+    return (int64_t)(a.ctl + a.numel + a.g0 + a.tlen + a.tmask + a.blen + 2 * a.list);
 }
 
 int64_t static_plan_limit() { return (int64_t)kStaticPlanBytes; }
@@ -744,31 +862,47 @@ hipError_t launch_plan_static(void* ws, const int64_t* numel, int32_t n_tensors,
                               uint64_t budget, uint64_t full_bytes, uint32_t* mask, uint64_t* stats,
                               hipStream_t s)
 {
-    const int64_t cap = (int64_t)K * std::max<int64_t>(n_short, 1);
+    const StaticParts a = static_parts(n_tensors, G, K);
+    const int64_t cap = (int64_t)K * std::max<int64_t>(n_tensors, 1);
     char* p = static_cast<char*>(ws);
     PlanCtl* ctl = reinterpret_cast<PlanCtl*>(p);
-    p += align256(sizeof(PlanCtl));
+    p += a.ctl;
     int64_t* d_numel = reinterpret_cast<int64_t*>(p);
-    p += align256(sizeof(int64_t) * (size_t)n_tensors);
+    p += a.numel;
     uint32_t* g0 = reinterpret_cast<uint32_t*>(p);
-    p += align256(sizeof(uint32_t) * (size_t)(n_tensors + 1));
+    p += a.g0;
+    uint32_t* tlen = reinterpret_cast<uint32_t*>(p);
+    p += a.tlen;
+    uint32_t* tmask = reinterpret_cast<uint32_t*>(p);
+    p += a.tmask;
     uint32_t* blen = reinterpret_cast<uint32_t*>(p);
-    p += align256(sizeof(uint32_t) * (size_t)G);
+    p += a.blen;
     uint32_t* list0 = reinterpret_cast<uint32_t*>(p);
-    p += align256(sizeof(uint32_t) * (size_t)cap);
+    p += a.list;
     uint32_t* list1 = reinterpret_cast<uint32_t*>(p);
     hipError_t e;
     if (G > 0) {
         if ((e = hipMemcpyAsync(d_numel, numel, sizeof(int64_t) * (size_t)n_tensors, hipMemcpyHostToDevice, s)) !=
             hipSuccess)
             return e;
-        hipLaunchKernelGGL(k_static_g0, dim3(1), dim3(kT), 0, s, d_numel, (int)n_tensors, block_elems, g0);
-        hipLaunchKernelGGL(k_static_blen, dim3((unsigned)((G + kT - 1) / kT)), dim3(kT), 0, s, d_numel, g0,
-                           (int)n_tensors, block_elems, G, blen);
+        hipLaunchKernelGGL(k_static_g0, dim3(1), dim3(kT), 0, s, d_numel, (int)n_tensors, block_elems, g0, tlen);
+        if (sumsq != nullptr)
+            hipLaunchKernelGGL(k_static_blen, dim3((unsigned)((G + kT - 1) / kT)), dim3(kT), 0, s, d_numel, g0,
+                               (int)n_tensors, block_elems, G, blen);
     }
-    // n_short + 1 bounds the distinct block lengths, hence the rounds
-    if ((e = enqueue_plan(ctl, list0, list1, (unsigned)cap, blen, es, G, (int)std::min<int64_t>(n_short + 1, 1 << 30),
-                          K, sumsq, w, flags, budget, full_bytes, mask, s)) != hipSuccess)
+    if (sumsq != nullptr) {
+        // n_short + 1 bounds the distinct block lengths, hence the rounds
+        enqueue_select(ctl, list0, list1, (unsigned)cap, blen, es, G, (int)std::min<int64_t>(n_short + 1, 1 << 30), K,
+                       sumsq, w, flags, budget, mask, s);
+        e = enqueue_block_final(ctl, mask, G, K, budget, full_bytes, s);
+    } else {
+        // tensor-level plan; the number of tensors bounds its rounds
+        const int64_t T = G > 0 ? n_tensors : 0;
+        enqueue_select(ctl, list0, list1, (unsigned)cap, tlen, es, T, (int)std::max<int64_t>(T, 1), K, nullptr, w,
+                       flags, budget, tmask, s);
+        e = enqueue_tensor_final(ctl, tmask, g0, (int)n_tensors, G, K, budget, full_bytes, mask, s);
+    }
+    if (e != hipSuccess)
         return e;
     if ((e = hipMemcpyAsync(stats, ctl->stats, sizeof(ctl->stats), hipMemcpyDeviceToHost, s)) != hipSuccess)
         return e;

@@ -52,6 +52,13 @@ struct BlockTable {
     int64_t n_chunks = 0;
     uint4* d_chunk = nullptr;
     uint64_t* d_tnumel = nullptr;  // elements per tensor [n_tensors]
+    // the tensor-level plan (no block catalog): elements per tensor as u32
+    // (valid when every tensor has fewer than 2^32), their distinct values,
+    // and the first block of every tensor [n_tensors + 1]
+    uint32_t* d_tlen = nullptr;
+    uint32_t* d_g0 = nullptr;
+    int n_distinct_tlen = 0;
+    bool tlen_fits = true;
 };
 
 constexpr int kChunkBlocks = 16;
@@ -64,6 +71,8 @@ struct PlanScratch {
     PlanCtl* ctl = nullptr;
     uint32_t* list[2] = {nullptr, nullptr};  // candidate uid lists for the later rounds
     int64_t list_cap = 0;
+    uint32_t* tmask = nullptr;  // tensor-level plan: selection word per tensor
+    int64_t tmask_cap = 0;
     uint64_t* h_stats = nullptr;  // pinned host mirror of the stats
 };
 
@@ -99,7 +108,9 @@ hipError_t launch_plan_static(void* ws, const int64_t* numel, int32_t n_tensors,
 hipError_t launch_coverage(const BlockTable& bt, int K, const uint32_t* mask, unsigned long long* cov,
                            hipStream_t s);
 
-// Algorithm 1 on the device (k_plan.hip).
+// Algorithm 1 on the device (k_plan.hip).  sumsq null: the tensor-level
+// plan of Section 3's fallback (units (expert, tensor), statistic 1), which
+// needs ps.tmask for n_tensors words and lists of K * n_tensors uids.
 hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float* sumsq,
                        const Coeffs& w, uint32_t flags, uint64_t budget, uint64_t full_bytes, uint32_t* mask,
                        hipStream_t s);

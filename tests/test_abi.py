@@ -151,11 +151,16 @@ def test_plan_noalloc_rejects_a_layout_beyond_its_fixed_array(mp):
     lib = mp.lib
     st = mp.mp_plan_stats()
     w = (C.c_float * 1)(1.0)
-    L = mp.Layout([4096 * 5_000_000], 4096, mp.MP_BF16)
+    L = mp.Layout([4096 * 1000] * 5000, 4096, mp.MP_BF16)
     rc = lib.mp_plan_noalloc(L.ref, 1, None, w, 0, 0, None, C.byref(st), None)
     assert rc == mp.MP_E_UNSUPPORTED
     msg = lib.mp_last_error().decode()
-    assert "16777216" in msg and "20019712" in msg
+    need = int(msg.split(" needs ")[1].split()[0])
+    assert "16777216" in msg and need > 16777216 and "5000000 blocks" in msg
+    # the tensor-level plan (no catalog) refuses tensors of 2^32 or more elements
+    L = mp.Layout([4096 * 2_000_000], 4096, mp.MP_BF16)
+    assert lib.mp_plan_noalloc(L.ref, 1, None, w, 0, 0, None, C.byref(st), None) == mp.MP_E_UNSUPPORTED
+    assert "2^32" in lib.mp_last_error().decode()
     # argument errors come first, as in mp_plan
     assert lib.mp_plan_noalloc(L.ref, 40, None, w, 0, 0, None, C.byref(st), None) == mp.MP_E_ARG
     assert lib.mp_plan_noalloc(L.ref, 1, None, w, 0, 8, None, C.byref(st), None) == mp.MP_E_UNSUPPORTED

@@ -778,29 +778,69 @@ def test_plan_many_rounds(mp):
                 assert st["full_bytes"] == st_orc["full_bytes"] and st["n_units"] == G * K
 
 
+def _assert_tensor_plan(mp, L, blocks, dtype, K, w, B, flags, mask):
+    st = mp.mp_plan(L, K, None, w, B, mask, flags=flags)
+    m = mask.cpu().numpy().view(np.uint32)
+    m_orc, st_orc = oracle.plan(blocks, dtype, K, None, w, B, flags=flags)
+    assert np.array_equal(m, m_orc), f"tensor-level mask differs at B={B} w={w} flags={flags}"
+    assert st["cost_bytes"] == st_orc["cost"] <= B and st["n_selected"] == st_orc["n_selected"]
+    assert st["digest"] == st_orc["digest"] and st["full_bytes"] == st_orc["full_bytes"]
+    assert st["n_units"] == blocks.G * K
+    # no tensor is split: every block of a tensor carries the same word
+    first = np.concatenate([[True], blocks.tensor[1:] != blocks.tensor[:-1]])
+    starts = np.nonzero(first)[0]
+    word = np.repeat(m[starts], np.diff(np.concatenate([starts, [blocks.G]])))
+    assert np.array_equal(m, word)
+    return st
+
+
 def test_plan_without_catalog(mp):
-    # no block catalog (sumsq NULL): the deterministic fallback ranking,
-    # bit-exact against the oracle, then a merge over that mask
+    # no block catalog (sumsq NULL): Section 3's tensor-level plan, bit-exact
+    # against the oracle at every budget, weight vector and flag, no tensor
+    # split; then a merge over that mask
     import torch
-    spec = _mini_qwen(n_layers=1)
+    spec = _mini_qwen(n_layers=2)
     base_np, exps_np = make_family(spec, seed=35)
     L, lay = _lay(mp, spec)
     K = len(exps_np)
     blocks = oracle.Blocks(lay.numel, lay.block_elems)
     mask = torch.empty(blocks.G, dtype=torch.int32, device="cuda")
     full = int(blocks.len.sum()) * lay.elem_bytes * K
-    for w in ([1.0] * K, [0.5, 2.0, 1.0, 1.5]):
-        for f in (0.0, 0.33, 0.8, 1.0):
-            st = mp.mp_plan(L, K, None, w, int(f * full), mask)
-            m_orc, st_orc = oracle.plan(blocks, lay.dtype, K, None, w, int(f * full))
-            assert np.array_equal(mask.cpu().numpy().view(np.uint32), m_orc)
-            assert st["cost_bytes"] == st_orc["cost"] and st["digest"] == st_orc["digest"]
+    rng = np.random.default_rng(36)
+    budgets = sorted(set([0, 1, full // 3, full // 2, full - 1, full, full + 7] +
+                         [int(x) for x in rng.integers(0, full, 12)]))
+    for flags in (0, mp.MP_PLAN_PER_BYTE, mp.MP_PLAN_SKIP_ZERO):
+        for w in ([1.0] * K, [0.5, 2.0, 1.0, 1.5]):
+            for B in budgets:
+                _assert_tensor_plan(mp, L, blocks, lay.dtype, K, w, B, flags, mask)
+    _say(f"  tensor-level plans: {len(budgets)} budgets x 2 weights x 3 flags equal")
+    B = int(0.4 * full)
+    _assert_tensor_plan(mp, L, blocks, lay.dtype, K, [1.0] * K, B, 0, mask)
+    m_orc, _ = oracle.plan(blocks, lay.dtype, K, None, [1.0] * K, B)
     base = to_dev(base_np, lay.dtype)
     exps = [to_dev(e, lay.dtype) for e in exps_np]
     out = torch.empty_like(base)
     mp.mp_merge_ties(L, base, exps, mask, 0.2, 1.0, out)
     want = oracle.merge_ties(blocks, lay.dtype, base_np, exps_np, m_orc, 0.2, 1.0)
     assert assert_merge_equal(to_host(out), want, base_np, lay.dtype, "ties without catalog") == 0
+
+
+@pytest.mark.parametrize("name,K", [("qwen2.5-1.5b", 4), ("llama3-8b", 16)])
+def test_plan_without_catalog_full_layouts(mp, name, K):
+    # the tensor-level plan on the full tensor lists (338 and 291 tensors,
+    # many distinct sizes, hence many plan rounds), against the oracle
+    import torch
+    lay = family_spec(name).layout
+    L = mp.Layout(lay.numel, lay.block_elems, mp.MP_BF16)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    mask = torch.empty(blocks.G, dtype=torch.int32, device="cuda")
+    full = lay.n_params * 2 * K
+    rng = np.random.default_rng(37)
+    w = [float(x) for x in rng.choice([0.25, 0.5, 1.0], K)]
+    for flags in (0, mp.MP_PLAN_PER_BYTE):
+        for f in (1.0 / K, 0.1, 0.25, 0.5, 0.77, 1.0):
+            _assert_tensor_plan(mp, L, blocks, "bf16", K, w, int(f * full), flags, mask)
+    _say(f"  {name} K={K}: tensor-level plans equal")
 
 
 def test_budget_boundaries_exact(mp):
