@@ -157,6 +157,37 @@ def cpu_baseline(spec, base, exps, route, blocks_stride=8):
 PCIE_PEAK = 64.0e9  # PCIe Gen5 x16, one direction, nominal bytes/s
 
 
+def host_cpu():
+    """The host the CPU baseline ran on: model name and socket count from
+    /proc/cpuinfo, and the CPUs this process may use."""
+    model, sockets = None, set()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name") and model is None:
+                    model = line.split(":", 1)[1].strip()
+                elif line.startswith("physical id"):
+                    sockets.add(line.split(":", 1)[1].strip())
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count()
+    return {"cpu_model": model, "sockets": len(sockets) or None, "nproc": nproc}
+
+
+def one_thread(fn):
+    """Run fn with the oracle on one thread, then restore its thread count."""
+    import oracle
+    n = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        return fn()
+    finally:
+        oracle.set_num_threads(n)
+
+
 def fidelity(out, m_full, blen, n_sel, n_units):
     """Fidelity of a budgeted merge against the full-read one (reporting only,
     outside every timed region): Rel. l2 = ||M_A - M_full|| / ||M_full|| over
@@ -389,7 +420,8 @@ def cpu_baseline_sweep(spec, base, exps, cfg, flags, dl, target_elems=100_000_00
     K = len(exps)
     nparams = int(blk.len[ids].sum())
     full = nparams * lay.elem_bytes * K
-    w = [1.0 / K] * K if op in ("avg", "avg_renorm") else [1.0] * K
+    linear = op in ("avg", "avg_renorm") or (op == "dare" and cfg.get("combine") == "linear")
+    w = [1.0 / K] * K if linear else [1.0] * K
     dt_name = lay.dtype
     t0 = time.perf_counter()
     S = oracle.index(blk, dt_name, b_np, e_np, doff=doff, ids=ids, delta=dl).reshape(-1)
@@ -404,7 +436,7 @@ def cpu_baseline_sweep(spec, base, exps, cfg, flags, dl, target_elems=100_000_00
             oracle.merge_ties(blk, dt_name, b_np, e_np, mask, cfg["density"], cfg["lam"], **kw)
         else:
             comb = 1 if cfg["combine"] == "sign_elect" else 0
-            oracle.merge_dare(blk, dt_name, b_np, e_np, mask, cfg["p"], cfg["seed"], comb, [1.0] * K, cfg["lam"], **kw)
+            oracle.merge_dare(blk, dt_name, b_np, e_np, mask, cfg["p"], cfg["seed"], comb, w, cfg["lam"], **kw)
     dt = time.perf_counter() - t0
     return {
         "value": len(cfg["budgets"]) * nparams / dt,
@@ -468,7 +500,8 @@ def run_sweep(args):
     es = lay.elem_bytes
     full = P * es * K
     op = cfg["op"]
-    w = [1.0 / K] * K if op in ("avg", "avg_renorm") else [1.0] * K
+    linear = op in ("avg", "avg_renorm") or (op == "dare" and cfg.get("combine") == "linear")
+    w = [1.0 / K] * K if linear else [1.0] * K  # the plan weighs units by the merge coefficients
     stream = torch.cuda.current_stream()
     tau_t = torch.empty(G * K, dtype=torch.int32, device="cuda") if op == "ties_tensor" else None
 
@@ -488,7 +521,8 @@ def run_sweep(args):
             return mp.mp_merge_ties_tau(L, base, exps, mask, tau_t, cfg["lam"], out, residency=res, io=io,
                                         stream=stream, delta=dl)
         comb = mp.MP_COMBINE_SIGN_ELECT if cfg["combine"] == "sign_elect" else mp.MP_COMBINE_LINEAR
-        return mp.mp_merge_dare(L, base, exps, mask, cfg["p"], cfg["seed"], comb, None, cfg["lam"], out,
+        alpha = None if comb == mp.MP_COMBINE_SIGN_ELECT else [1.0 / K] * K
+        return mp.mp_merge_dare(L, base, exps, mask, cfg["p"], cfg["seed"], comb, alpha, cfg["lam"], out,
                                 residency=res, io=io, stream=stream, delta=dl)
 
     def timed(fn):
@@ -587,6 +621,11 @@ def run_sweep(args):
         log("timing the CPU oracle on a sample")
         cb = cpu_baseline_sweep(spec, base, exps, cfg, flags, dl)
         if cb is not None:
+            cb["host"] = host_cpu()
+            if P * K <= 100_000_000:  # the whole family fits the sample: time it on one thread too
+                cb1 = one_thread(lambda: cpu_baseline_sweep(spec, base, exps, cfg, flags, dl))
+                cb["one_thread"] = {"value": cb1["value"], "unit": cb1["unit"], "cores": cb1["cores"],
+                                    "sample": cb1["sample"]}
             result["cpu_baseline"] = cb
     print(json.dumps(result), flush=True)
 
@@ -730,8 +769,32 @@ def main():
         alt.append((a, b))
     torch.cuda.synchronize()
     alt_ms = [a.elapsed_time(b) for a, b in alt]
-    if args.calibration_copy:
-        empty = torch.zeros(G, dtype=torch.int32, device="cuda")
+    # measured copy rate: the AVG kernel with an empty mask copies the base to
+    # the output (reads 2P + 4G bytes, writes 2P); median of five launches
+    empty = torch.zeros(G, dtype=torch.int32, device="cuda")
+    copy_ms = []
+    for _ in range(6):
+        a, b = ev(), ev()
+        a.record(stream)
+        mp.mp_merge_avg(L, base, exps, empty, [0.25] * K, out, stream=stream)
+        b.record(stream)
+        copy_ms.append((a, b))
+    torch.cuda.synchronize()
+    copy_ms = float(np.median([a.elapsed_time(b) for a, b in copy_ms[1:]]))
+    copy_GBps = (4 * P + 4 * G) / (copy_ms * 1e-3) / 1e9
+    # and the HIP runtime's own device-to-device copy of the base (reads and
+    # writes 2P bytes), median of five
+    rt_ms = []
+    for _ in range(6):
+        a, b = ev(), ev()
+        a.record(stream)
+        out.copy_(base)
+        b.record(stream)
+        rt_ms.append((a, b))
+    torch.cuda.synchronize()
+    rt_ms = float(np.median([a.elapsed_time(b) for a, b in rt_ms[1:]]))
+    rt_GBps = 4 * P / (rt_ms * 1e-3) / 1e9
+    if args.calibration_copy:  # one more, for the byte counters of a profiling run
         mp.mp_merge_avg(L, base, exps, empty, [0.25] * K, out, stream=stream)
         torch.cuda.synchronize()
 
@@ -779,6 +842,14 @@ def main():
             "traffic": traffic,
             "kernel": ("k_merge_elem<bf16, TIES from catalog thresholds>" if catalog else "k_merge_ties<bf16>")
                       + " (device-resident experts)",
+            "measured_copy": {"GBps": copy_GBps, "frac_of_peak": copy_GBps * 1e9 / HBM_PEAK,
+                              "ms": round(copy_ms, 4),
+                              "kernel": "k_merge_elem<bf16, AVG> with an empty mask: copies the base "
+                                        "(reads 2P + 4G bytes, writes 2P)"},
+            "measured_runtime_copy": {"GBps": rt_GBps, "frac_of_peak": rt_GBps * 1e9 / HBM_PEAK,
+                                      "ms": round(rt_ms, 4),
+                                      "kernel": "the HIP runtime's device-to-device copy of the base "
+                                                "(reads and writes 2P bytes)"},
         },
         "breakdown": {
             "index_ms": round(float(idx_ms), 4),
@@ -793,7 +864,13 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(spec, base, exps, args.ties, args.cpu_stride)
+        cb = cpu_baseline(spec, base, exps, args.ties, args.cpu_stride)
+        log("timing the CPU oracle on one thread (a smaller sample)")
+        cb1 = one_thread(lambda: cpu_baseline(spec, base, exps, args.ties, 16 * args.cpu_stride))
+        cb["host"] = host_cpu()
+        cb["one_thread"] = {"value": cb1["value"], "unit": cb1["unit"], "cores": cb1["cores"],
+                            "sample": cb1["sample"]}
+        result["cpu_baseline"] = cb
     print(json.dumps(result), flush=True)
 
 

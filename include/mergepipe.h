@@ -42,10 +42,11 @@
  *   enqueued on it; calls return once enqueued unless stated otherwise.
  *   Calls that fill a host-side stats struct synchronise the stream first.
  * Errors.  Every call returns MP_OK (0) or a negative MP_E_* code;
- *   mp_last_error() gives a message (thread-local).  On an argument error
- *   nothing is enqueued and no output is written.  Asynchronous device
- *   errors surface at the next synchronising call.  No C++ exception crosses
- *   the ABI.
+ *   mp_last_error() gives a message (thread-local).  On an argument error,
+ *   and on MP_E_NOMEM, nothing is enqueued and no output is written.  On
+ *   MP_E_IO (staged residencies) the chunks before the failing one may have
+ *   been merged.  Asynchronous device errors surface at the next
+ *   synchronising call.  No C++ exception crosses the ABI.
  * Validation (all calls): 1 <= K <= 32; block_elems > 0 and a multiple of
  *   16 / (bytes per element); every tensor numel >= 0 and a multiple of
  *   16 / (bytes per element) (each tensor starts 16-byte aligned);
@@ -345,6 +346,24 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
  * Takes effect at the next host-pageable call (buffers are reallocated).
  * MP_E_ARG outside [1 MiB, 4 GiB]. */
 int mp_set_stage_bytes(uint64_t bytes);
+
+/* Cap on the library's cached workspace (block tables, plan scratch, byte
+ * counters, staging buffers: the device and pinned host memory it keeps
+ * between calls), in bytes; 0 (the default) means no cap.  A call whose
+ * workspace allocation would pass the cap returns MP_E_NOMEM before it
+ * enqueues anything, writing no output; memory already held is kept (free
+ * it with mp_release).  Takes effect at the next allocation. */
+int mp_set_workspace_limit(uint64_t bytes);
+
+/* Bytes of workspace the library holds now (all devices). */
+uint64_t mp_workspace_bytes(void);
+
+/* Fault injection for tests of the staged residencies (MP_HOST_PAGEABLE,
+ * MP_HOST_FILE): with the environment variable MP_FAULT_PACK_CHUNK=n set
+ * when a staged call runs, the pack of its chunk n (0-based; a chunk that
+ * packs at least one block) reports a failed read, as an unreadable expert
+ * file does: the call returns MP_E_IO after the kernels of chunks 0..n-1
+ * were enqueued, so outputs may be partly written. */
 
 /* Message for the last failing call on this thread ("" if none). */
 const char* mp_last_error(void);

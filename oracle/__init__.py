@@ -62,6 +62,7 @@ def lib():
         L.orc_ties_k.restype = C.c_int64
         L.orc_ties_k.argtypes = [C.c_int64, C.c_double]
         L.orc_num_threads.restype = C.c_int
+        L.orc_set_num_threads.argtypes = [C.c_int]
         _lib = L
     return _lib
 
@@ -340,6 +341,12 @@ def ties_k(n: int, density: float) -> int:
 
 def num_threads() -> int:
     return int(lib().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (results do not
+    depend on it)."""
+    lib().orc_set_num_threads(int(n))
 
 
 def full_bytes(blocks: Blocks, dtype, K: int) -> int:

@@ -102,6 +102,18 @@ int orc_num_threads(void)
 #endif
 }
 
+/* Threads of the parallel loops that follow (n >= 1).  Every per-block
+ * computation is sequential, so results do not depend on it. */
+void orc_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------ */
 /* Section 2: the tensor set and its deterministic blocks.             */
 /* Reading: each tensor is flattened row-major and cut into            */

@@ -106,6 +106,8 @@ uint64_t orc_mix64(uint64_t x);
 void orc_round_bf16(const float* x, uint16_t* y, int64_t n);
 int64_t orc_ties_k(int64_t n, double density);
 int orc_num_threads(void);
+/* Threads of the following parallel loops (results do not depend on it). */
+void orc_set_num_threads(int n);
 
 #ifdef __cplusplus
 }

@@ -36,8 +36,8 @@ MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
            "mp_plan_noalloc", "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
            "mp_merge_ties",
-           "mp_merge_ties_tau", "mp_merge_dare", "mp_lora_materialize", "mp_set_stage_bytes", "mp_last_error",
-           "mp_release")
+           "mp_merge_ties_tau", "mp_merge_dare", "mp_lora_materialize", "mp_set_stage_bytes",
+           "mp_set_workspace_limit", "mp_workspace_bytes", "mp_last_error", "mp_release")
 
 
 class mp_layout(C.Structure):
@@ -108,6 +108,10 @@ def _load():
     L.mp_last_error.restype = C.c_char_p
     L.mp_set_stage_bytes.argtypes = [u64]
     L.mp_set_stage_bytes.restype = i32
+    L.mp_set_workspace_limit.argtypes = [u64]
+    L.mp_set_workspace_limit.restype = i32
+    L.mp_workspace_bytes.argtypes = []
+    L.mp_workspace_bytes.restype = u64
     L.mp_last_error.argtypes = []
     L.mp_release.argtypes = []
     for name in ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
@@ -317,6 +321,15 @@ def mp_last_error() -> str:
 
 def mp_set_stage_bytes(nbytes: int):
     _check(lib.mp_set_stage_bytes(int(nbytes)))
+
+
+def mp_set_workspace_limit(nbytes: int):
+    """Cap on the library's cached workspace in bytes (0: none)."""
+    _check(lib.mp_set_workspace_limit(int(nbytes)))
+
+
+def mp_workspace_bytes() -> int:
+    return int(lib.mp_workspace_bytes())
 
 
 def mp_release():

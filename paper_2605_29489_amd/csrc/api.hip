@@ -44,10 +44,26 @@ int fail(int code, const char* fmt, ...)
 
 int hip_fail(hipError_t e, const char* what)
 {
-    return fail(MP_E_HIP, "%s: %s", what, hipGetErrorString(e));
+    // an allocation that failed (or passed the workspace limit) is MP_E_NOMEM
+    return fail(e == hipErrorOutOfMemory ? MP_E_NOMEM : MP_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
 // ------------------------------------------------------------ workspaces
+uint64_t g_ws_limit = 0;  // bytes; 0 = no limit
+uint64_t g_ws_held = 0;
+std::map<const void*, size_t> g_ws_sizes;
+
+int ws_free_r(void* p)
+{
+    ws_free(p);
+    return 0;
+}
+int ws_host_free_r(void* p)
+{
+    ws_host_free(p);
+    return 0;
+}
+
 struct DeviceWs {
     PlanScratch plan;
     unsigned long long* counters = nullptr;  // [256]
@@ -73,8 +89,8 @@ void free_lora(LoraEntry& e)
     int cur = 0;
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(e.device);
-    (void)hipFree(e.t.d_desc);
-    (void)hipFree(e.t.d_zero);
+    (void)ws_free_r(e.t.d_desc);
+    (void)ws_free_r(e.t.d_zero);
     (void)hipSetDevice(cur);
 }
 
@@ -83,14 +99,14 @@ void free_table(BlockTable& bt)
     int cur = 0;
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(bt.device);
-    (void)hipFree(bt.d_off);
-    (void)hipFree(bt.d_len);
-    (void)hipFree(bt.d_tensor);
-    (void)hipFree(bt.d_elem0);
-    (void)hipFree(bt.d_chunk);
-    (void)hipFree(bt.d_tnumel);
-    (void)hipFree(bt.d_tlen);
-    (void)hipFree(bt.d_g0);
+    (void)ws_free_r(bt.d_off);
+    (void)ws_free_r(bt.d_len);
+    (void)ws_free_r(bt.d_tensor);
+    (void)ws_free_r(bt.d_elem0);
+    (void)ws_free_r(bt.d_chunk);
+    (void)ws_free_r(bt.d_tnumel);
+    (void)ws_free_r(bt.d_tlen);
+    (void)ws_free_r(bt.d_g0);
     (void)hipSetDevice(cur);
 }
 
@@ -99,16 +115,16 @@ void free_ws(int dev, DeviceWs& w)
     int cur = 0;
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(dev);
-    (void)hipFree(w.plan.ctl);
-    (void)hipFree(w.plan.list[0]);
-    (void)hipFree(w.plan.list[1]);
-    (void)hipFree(w.plan.tmask);
-    (void)hipHostFree(w.plan.h_stats);
-    (void)hipFree(w.counters);
-    (void)hipHostFree(w.h_counters);
-    (void)hipFree(w.cov);
-    (void)hipFree(w.tt_hist);
-    (void)hipFree(w.tt_state);
+    (void)ws_free_r(w.plan.ctl);
+    (void)ws_free_r(w.plan.list[0]);
+    (void)ws_free_r(w.plan.list[1]);
+    (void)ws_free_r(w.plan.tmask);
+    (void)ws_host_free_r(w.plan.h_stats);
+    (void)ws_free_r(w.counters);
+    (void)ws_host_free_r(w.h_counters);
+    (void)ws_free_r(w.cov);
+    (void)ws_free_r(w.tt_hist);
+    (void)ws_free_r(w.tt_state);
     (void)hipSetDevice(cur);
 }
 
@@ -226,14 +242,14 @@ int get_table(const mp_layout* L, int esize, BlockTable** out)
     }
     bt->n_distinct_tlen = (int)tl.size();
     if (G > 0) {
-        if ((e = hipMalloc((void**)&bt->d_off, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_len, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_tensor, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_elem0, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_chunk, sizeof(uint4) * chunks.size())) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_tnumel, sizeof(uint64_t) * tnumel.size())) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_tlen, sizeof(uint32_t) * tlen.size())) != hipSuccess ||
-            (e = hipMalloc((void**)&bt->d_g0, sizeof(uint32_t) * tg0.size())) != hipSuccess) {
+        if ((e = ws_malloc((void**)&bt->d_off, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
+            (e = ws_malloc((void**)&bt->d_len, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
+            (e = ws_malloc((void**)&bt->d_tensor, sizeof(uint32_t) * (size_t)G)) != hipSuccess ||
+            (e = ws_malloc((void**)&bt->d_elem0, sizeof(uint64_t) * (size_t)G)) != hipSuccess ||
+            (e = ws_malloc((void**)&bt->d_chunk, sizeof(uint4) * chunks.size())) != hipSuccess ||
+            (e = ws_malloc((void**)&bt->d_tnumel, sizeof(uint64_t) * tnumel.size())) != hipSuccess ||
+            (e = ws_malloc((void**)&bt->d_tlen, sizeof(uint32_t) * tlen.size())) != hipSuccess ||
+            (e = ws_malloc((void**)&bt->d_g0, sizeof(uint32_t) * tg0.size())) != hipSuccess) {
             free_table(*bt);
             return fail(MP_E_NOMEM, "block table allocation failed: %s", hipGetErrorString(e));
         }
@@ -267,9 +283,9 @@ int get_ws(DeviceWs** out)
     }
     auto w = std::make_unique<DeviceWs>();
     if ((e = plan_ctl_alloc(&w->plan.ctl)) != hipSuccess ||
-        (e = hipHostMalloc((void**)&w->plan.h_stats, sizeof(uint64_t) * 8, hipHostMallocDefault)) != hipSuccess ||
-        (e = hipMalloc((void**)&w->counters, sizeof(unsigned long long) * 256)) != hipSuccess ||
-        (e = hipHostMalloc((void**)&w->h_counters, sizeof(unsigned long long) * 256, hipHostMallocDefault)) != hipSuccess) {
+        (e = ws_host_malloc((void**)&w->plan.h_stats, sizeof(uint64_t) * 8)) != hipSuccess ||
+        (e = ws_malloc((void**)&w->counters, sizeof(unsigned long long) * 256)) != hipSuccess ||
+        (e = ws_host_malloc((void**)&w->h_counters, sizeof(unsigned long long) * 256)) != hipSuccess) {
         free_ws(dev, *w);
         return fail(MP_E_NOMEM, "workspace allocation failed: %s", hipGetErrorString(e));
     }
@@ -285,14 +301,14 @@ int ensure_lists(PlanScratch& ps, int64_t need)
 {
     if (ps.list_cap >= need)
         return MP_OK;
-    (void)hipFree(ps.list[0]);
-    (void)hipFree(ps.list[1]);
+    (void)ws_free_r(ps.list[0]);
+    (void)ws_free_r(ps.list[1]);
     ps.list[0] = ps.list[1] = nullptr;
     ps.list_cap = 0;
     const size_t bytes = sizeof(uint32_t) * (size_t)std::max<int64_t>(need, 1);
     hipError_t e;
-    if ((e = hipMalloc((void**)&ps.list[0], bytes)) != hipSuccess ||
-        (e = hipMalloc((void**)&ps.list[1], bytes)) != hipSuccess)
+    if ((e = ws_malloc((void**)&ps.list[0], bytes)) != hipSuccess ||
+        (e = ws_malloc((void**)&ps.list[1], bytes)) != hipSuccess)
         return fail(MP_E_NOMEM, "plan list allocation failed: %s", hipGetErrorString(e));
     ps.list_cap = std::max<int64_t>(need, 1);
     return MP_OK;
@@ -547,7 +563,7 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
         host_experts(c, experts, &hx);
         e = stage_merge(bt, a, base, hx, K, mask, out, ctr, s, &staged_bytes);
         if (hx.failed.load())
-            return fail(MP_E_IO, "reading an expert file failed");
+            return fail(MP_E_IO, "packing expert blocks failed (a failed file read, or MP_FAULT_PACK_CHUNK)");
         if (e != hipSuccess)
             return hip_fail(e, "staged merge");
     } else if ((e = launch_merge(bt, a, base, c.ex, K, mask, out, ctr, s)) != hipSuccess) {
@@ -577,6 +593,40 @@ int run_merge(const mp_layout* L, const void* base, const void* const* experts, 
 }
 
 }  // namespace
+
+namespace {
+hipError_t ws_take(void** p, size_t bytes, bool host)
+{
+    *p = nullptr;
+    if (g_ws_limit != 0 && g_ws_held + bytes > g_ws_limit)
+        return hipErrorOutOfMemory;
+    const hipError_t e = host ? hipHostMalloc(p, bytes, hipHostMallocDefault) : hipMalloc(p, bytes);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        return e;
+    }
+    g_ws_sizes[*p] = bytes;
+    g_ws_held += bytes;
+    return hipSuccess;
+}
+void ws_give(void* p, bool host)
+{
+    if (p == nullptr)
+        return;
+    auto it = g_ws_sizes.find(p);
+    if (it != g_ws_sizes.end()) {
+        g_ws_held -= it->second;
+        g_ws_sizes.erase(it);
+    }
+    (void)(host ? hipHostFree(p) : hipFree(p));
+}
+}  // namespace
+
+hipError_t ws_malloc(void** p, size_t bytes) { return ws_take(p, bytes, false); }
+hipError_t ws_host_malloc(void** p, size_t bytes) { return ws_take(p, bytes, true); }
+void ws_free(void* p) { ws_give(p, false); }
+void ws_host_free(void* p) { ws_give(p, true); }
+
 }  // namespace mp
 
 using namespace mp;
@@ -617,7 +667,7 @@ int mp_index_blocks(const mp_layout* layout, const void* base, const void* const
         host_experts(c, experts, &hx);
         e = stage_index(bt, base, hx, K, false, 0.0, sumsq, nullptr, s, &staged_bytes, delta);
         if (hx.failed.load())
-            return fail(MP_E_IO, "reading an expert file failed");
+            return fail(MP_E_IO, "packing expert blocks failed (a failed file read, or MP_FAULT_PACK_CHUNK)");
     } else {
         e = launch_index(bt, base, c.ex, K, sumsq, s, delta);
     }
@@ -653,7 +703,7 @@ int mp_index_ties(const mp_layout* layout, const void* base, const void* const* 
         host_experts(c, experts, &hx);
         e = stage_index(bt, base, hx, K, true, density, sumsq, tau, s, &staged_bytes, delta);
         if (hx.failed.load())
-            return fail(MP_E_IO, "reading an expert file failed");
+            return fail(MP_E_IO, "packing expert blocks failed (a failed file read, or MP_FAULT_PACK_CHUNK)");
     } else {
         e = launch_index_ties(bt, base, c.ex, K, density, sumsq, tau, s, delta);
     }
@@ -683,10 +733,10 @@ int mp_coverage(const mp_layout* layout, int32_t K, const uint32_t* mask, uint64
     const int64_t n = bt->n_tensors * K;
     hipError_t e;
     if (n > ws->cov_cap) {
-        (void)hipFree(ws->cov);
+        (void)ws_free_r(ws->cov);
         ws->cov = nullptr;
         ws->cov_cap = 0;
-        if ((e = hipMalloc((void**)&ws->cov, sizeof(unsigned long long) * (size_t)n)) != hipSuccess)
+        if ((e = ws_malloc((void**)&ws->cov, sizeof(unsigned long long) * (size_t)n)) != hipSuccess)
             return fail(MP_E_NOMEM, "coverage buffer: %s", hipGetErrorString(e));
         ws->cov_cap = n;
     }
@@ -725,13 +775,13 @@ int mp_ties_tensor_thresholds(const mp_layout* layout, const void* base, const v
     hipError_t e;
     DeviceWs& ws = *c.ws;
     if (pairs > ws.tt_pairs) {
-        (void)hipFree(ws.tt_hist);
-        (void)hipFree(ws.tt_state);
+        (void)ws_free_r(ws.tt_hist);
+        (void)ws_free_r(ws.tt_state);
         ws.tt_hist = nullptr;
         ws.tt_state = nullptr;
         ws.tt_pairs = 0;
-        if ((e = hipMalloc((void**)&ws.tt_hist, sizeof(uint32_t) * 2048 * (size_t)pairs)) != hipSuccess ||
-            (e = hipMalloc((void**)&ws.tt_state, sizeof(uint4) * (size_t)pairs)) != hipSuccess)
+        if ((e = ws_malloc((void**)&ws.tt_hist, sizeof(uint32_t) * 2048 * (size_t)pairs)) != hipSuccess ||
+            (e = ws_malloc((void**)&ws.tt_state, sizeof(uint4) * (size_t)pairs)) != hipSuccess)
             return fail(MP_E_NOMEM, "tensor-scope TIES buffers: %s", hipGetErrorString(e));
         ws.tt_pairs = pairs;
     }
@@ -779,10 +829,10 @@ int mp_plan(const mp_layout* layout, int32_t K, const float* sumsq, const float*
         if (!bt->tlen_fits)
             return fail(MP_E_UNSUPPORTED, "the tensor-level plan needs tensors of fewer than 2^32 elements");
         if (bt->n_tensors > ws->plan.tmask_cap) {
-            (void)hipFree(ws->plan.tmask);
+            (void)ws_free_r(ws->plan.tmask);
             ws->plan.tmask = nullptr;
             ws->plan.tmask_cap = 0;
-            hipError_t he = hipMalloc((void**)&ws->plan.tmask, sizeof(uint32_t) * (size_t)bt->n_tensors);
+            hipError_t he = ws_malloc((void**)&ws->plan.tmask, sizeof(uint32_t) * (size_t)bt->n_tensors);
             if (he != hipSuccess)
                 return fail(MP_E_NOMEM, "tensor selection words: %s", hipGetErrorString(he));
             ws->plan.tmask_cap = bt->n_tensors;
@@ -1066,10 +1116,10 @@ static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lor
     e->t.n_tiles = (uint32_t)tiles;
     e->t.n_zero = (uint32_t)zero.size();
     hipError_t he = hipSuccess;
-    if ((!desc.empty() && ((he = hipMalloc((void**)&e->t.d_desc, sizeof(LoraDesc) * desc.size())) != hipSuccess ||
+    if ((!desc.empty() && ((he = ws_malloc((void**)&e->t.d_desc, sizeof(LoraDesc) * desc.size())) != hipSuccess ||
                            (he = hipMemcpy(e->t.d_desc, desc.data(), sizeof(LoraDesc) * desc.size(),
                                            hipMemcpyHostToDevice)) != hipSuccess)) ||
-        (!zero.empty() && ((he = hipMalloc((void**)&e->t.d_zero, sizeof(uint32_t) * zero.size())) != hipSuccess ||
+        (!zero.empty() && ((he = ws_malloc((void**)&e->t.d_zero, sizeof(uint32_t) * zero.size())) != hipSuccess ||
                            (he = hipMemcpy(e->t.d_zero, zero.data(), sizeof(uint32_t) * zero.size(),
                                            hipMemcpyHostToDevice)) != hipSuccess))) {
         free_lora(*e);
@@ -1143,6 +1193,20 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
 }
 
 const char* mp_last_error(void) { return g_err.c_str(); }
+
+int mp_set_workspace_limit(uint64_t bytes)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    g_ws_limit = bytes;
+    return MP_OK;
+}
+
+uint64_t mp_workspace_bytes(void)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    return g_ws_held;
+}
 
 int mp_set_stage_bytes(uint64_t bytes)
 {

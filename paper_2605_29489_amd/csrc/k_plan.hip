@@ -909,7 +909,7 @@ hipError_t launch_plan_static(void* ws, const int64_t* numel, int32_t n_tensors,
     return hipStreamSynchronize(s);
 }
 
-hipError_t plan_ctl_alloc(PlanCtl** ctl) { return hipMalloc((void**)ctl, sizeof(PlanCtl)); }
+hipError_t plan_ctl_alloc(PlanCtl** ctl) { return ws_malloc((void**)ctl, sizeof(PlanCtl)); }
 
 // ---------------------------------------------------------------- coverage
 // Touched elements per (tensor, expert) of an access mask, for the run's

@@ -76,6 +76,16 @@ struct PlanScratch {
     uint64_t* h_stats = nullptr;  // pinned host mirror of the stats
 };
 
+// ---------------------------------------------------------------- workspace memory
+// Every cached device or pinned-host allocation of the library goes through
+// these, which count the bytes held and refuse (hipErrorOutOfMemory) an
+// allocation that would pass the limit set by mp_set_workspace_limit
+// (0: none).  Callers hold the library's lock.
+hipError_t ws_malloc(void** p, size_t bytes);
+hipError_t ws_host_malloc(void** p, size_t bytes);
+void ws_free(void* p);
+void ws_host_free(void* p);
+
 // ---------------------------------------------------------------- launchers
 // All launchers enqueue on `s` and return the launch status.
 

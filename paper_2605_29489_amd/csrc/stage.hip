@@ -15,6 +15,7 @@
 
 #include <algorithm>
 #include <cerrno>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -97,9 +98,9 @@ void free_stager(int dev, Stager& st)
             (void)hipEventSynchronize(st.copied[k]);
     }
     for (int k = 0; k < 2; ++k) {
-        (void)hipHostFree(st.h[k]);
-        (void)hipFree(st.d[k]);
-        (void)hipFree(st.soff[k]);
+        ws_host_free(st.h[k]);
+        ws_free(st.d[k]);
+        ws_free(st.soff[k]);
         if (st.copied[k])
             (void)hipEventDestroy(st.copied[k]);
         if (st.consumed[k])
@@ -129,9 +130,9 @@ hipError_t get_stager(Stager** out)
     auto st = std::make_unique<Stager>();
     st->bytes = g_stage_bytes;
     for (int k = 0; k < 2 && e == hipSuccess; ++k) {
-        if ((e = hipHostMalloc((void**)&st->h[k], st->bytes, hipHostMallocDefault)) != hipSuccess ||
-            (e = hipMalloc((void**)&st->d[k], st->bytes)) != hipSuccess ||
-            (e = hipMalloc((void**)&st->soff[k], sizeof(uint64_t) * kStageMaxBlocks)) != hipSuccess ||
+        if ((e = ws_host_malloc((void**)&st->h[k], st->bytes)) != hipSuccess ||
+            (e = ws_malloc((void**)&st->d[k], st->bytes)) != hipSuccess ||
+            (e = ws_malloc((void**)&st->soff[k], sizeof(uint64_t) * kStageMaxBlocks)) != hipSuccess ||
             (e = hipEventCreateWithFlags(&st->copied[k], hipEventDisableTiming)) != hipSuccess ||
             (e = hipEventCreateWithFlags(&st->consumed[k], hipEventDisableTiming)) != hipSuccess)
             break;
@@ -188,6 +189,21 @@ BlockTable view_of(const BlockTable& bt, int64_t b0, int64_t nb)
 }  // namespace
 
 void set_stage_bytes(size_t bytes) { g_stage_bytes = bytes; }
+
+namespace {
+// Fault injection for tests: with MP_FAULT_PACK_CHUNK=n in the environment,
+// the pack of chunk n of every staged call reports a failed read, as an
+// unreadable expert file does.  -1 (unset): no fault.
+int64_t fault_chunk()
+{
+    const char* v = std::getenv("MP_FAULT_PACK_CHUNK");
+    if (v == nullptr || *v == '\0')
+        return -1;
+    char* end = nullptr;
+    const long long n = std::strtoll(v, &end, 10);
+    return (end != v && n >= 0) ? (int64_t)n : -1;
+}
+}  // namespace
 
 void release_stagers()
 {
@@ -258,6 +274,7 @@ hipError_t stage_index(const BlockTable& bt, const void* base, const HostExperts
         return e;
     const size_t es = (size_t)bt.esize;
     const size_t cap_elems = st->bytes / (es * (size_t)K);  // chunk elements per expert
+    const int64_t fault = fault_chunk();
     int64_t g = 0;
     for (int c = 0; g < bt.G; ++c) {
         const int k = c & 1;
@@ -280,6 +297,8 @@ hipError_t stage_index(const BlockTable& bt, const void* base, const HostExperts
                 experts.read(i, st->h[k] + (size_t)i * chunk + a, e0 * es + a, z - a);
             }
         }, experts.fd != nullptr);
+        if (c == fault)
+            experts.failed.store(1);
         if (experts.failed.load())
             return hipErrorInvalidValue;
         const size_t bytes = chunk * (size_t)K;
@@ -325,6 +344,7 @@ hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* bas
         return (size_t)__builtin_popcount(hm[(size_t)g] & kmask) * bt.h_len[(size_t)g] * es;
     };
     std::vector<size_t> off;
+    const int64_t fault = fault_chunk();
     int64_t g = 0;
     for (int c = 0; g < bt.G; ++c) {
         const int k = c & 1;
@@ -395,6 +415,8 @@ hipError_t stage_merge(const BlockTable& bt, const MergeArgs& a, const void* bas
                     }
                 }, true);
             }
+            if (c == fault)
+                experts.failed.store(1);
             if (experts.failed.load())
                 return hipErrorInvalidValue;
             if ((e = hipMemcpyAsync(st->d[k], st->h[k], bytes, hipMemcpyHostToDevice, st->side)) != hipSuccess ||

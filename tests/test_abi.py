@@ -165,3 +165,36 @@ def test_plan_noalloc_rejects_a_layout_beyond_its_fixed_array(mp):
     assert lib.mp_plan_noalloc(L.ref, 40, None, w, 0, 0, None, C.byref(st), None) == mp.MP_E_ARG
     assert lib.mp_plan_noalloc(L.ref, 1, None, w, 0, 8, None, C.byref(st), None) == mp.MP_E_UNSUPPORTED
 
+
+
+def test_argument_errors_leave_host_outputs_untouched(mp):
+    # On an argument error nothing is written: the host-side stats, coverage
+    # and io records keep their contents (checked on the CPU, where the
+    # errors are caught before any device call).
+    lib = mp.lib
+    L = mp.Layout([4096, 4096], 4096, mp.MP_BF16)
+    ptrs = (C.c_void_p * 4)()
+    sentinel = 0x5A5A5A5A5A5A5A5A
+    st = mp.mp_plan_stats(*([sentinel] * 6))
+    w = (C.c_float * 4)(*([1.0] * 4))
+    wn = (C.c_float * 4)(*([float("nan")] * 4))
+    for call in (lambda: lib.mp_plan(L.ref, 0, None, w, 0, 0, None, C.byref(st), None),
+                 lambda: lib.mp_plan(L.ref, 4, None, wn, 0, 0, None, C.byref(st), None),
+                 lambda: lib.mp_plan(L.ref, 4, None, w, 0, 16, None, C.byref(st), None),
+                 lambda: lib.mp_plan_noalloc(L.ref, 4, None, wn, 0, 0, None, C.byref(st), None)):
+        assert call() in (mp.MP_E_ARG, mp.MP_E_UNSUPPORTED)
+        assert all(getattr(st, f) == sentinel for f, _ in st._fields_)
+    cov = (C.c_uint64 * 8)(*([sentinel] * 8))
+    assert lib.mp_coverage(L.ref, 0, None, cov, None) == mp.MP_E_ARG
+    assert lib.mp_coverage(L.ref, 4, None, None, None) == mp.MP_E_ARG
+    assert all(x == sentinel for x in cov)
+    io = mp.mp_io_stats()
+    io.expert_bytes = io.base_bytes = io.out_bytes = io.h2d_bytes = sentinel
+    a = (C.c_float * 4)(*([float("inf")] * 4))
+    assert lib.mp_merge_avg(L.ref, None, ptrs, 4, 0, None, a, None, C.byref(io), None) == mp.MP_E_ARG
+    assert lib.mp_merge_ties(L.ref, None, ptrs, 4, 0, None, 2.0, 1.0, None, C.byref(io), None) == mp.MP_E_ARG
+    assert lib.mp_merge_dare(L.ref, None, ptrs, 4, 0, None, 1.5, 0, 0, w, 1.0, None, C.byref(io), None) == mp.MP_E_ARG
+    assert (io.expert_bytes, io.base_bytes, io.out_bytes, io.h2d_bytes) == (sentinel,) * 4
+    # the workspace cap takes any value; its byte count reads without a GPU
+    assert lib.mp_set_workspace_limit(0) == mp.MP_OK
+    assert lib.mp_workspace_bytes() == 0

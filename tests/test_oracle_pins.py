@@ -1258,3 +1258,42 @@ def test_dare_non_anticipatory_drop_mask():
     zeroed = [base.copy(), base.copy(), exps[2]]  # experts 0,1 have zero delta
     all3 = oracle.merge_dare(b, "f32", base, zeroed, np.full(b.G, 7, np.uint32), 0.9, 7, 0, alpha, 1.0)
     assert np.array_equal(only2, all3)
+
+
+def test_oracle_results_do_not_depend_on_the_thread_count():
+    # Each per-block computation is sequential, so the oracle's results are
+    # bitwise the same on one thread and on several (the parallel loops only
+    # split the blocks among threads).
+    rng = np.random.default_rng(81)
+    numel = [4096 * 9 + 512, 4096 * 4, 1536, 256, 4096 * 7 + 64]
+    b = oracle.Blocks(numel, 4096)
+    K = 4
+    base, exps = _tiny_family(rng, numel, K, "bf16", scale=1e-3)
+    full = sum(numel) * 2 * K
+    w = [0.25] * K
+
+    def run():
+        S = oracle.index(b, "bf16", base, exps)
+        tau = oracle.ties_thresholds(b, "bf16", base, exps, 0.2)
+        m, st = oracle.plan(b, "bf16", K, S, [1.0] * K, full // 2)
+        mt, stt = oracle.plan(b, "bf16", K, None, w, full // 3)
+        return [S, tau, m, mt, np.array([st["digest"], stt["digest"]], np.uint64),
+                oracle.merge_avg(b, "bf16", base, exps, m, w),
+                oracle.merge_avg_renorm(b, "bf16", base, exps, m, w),
+                oracle.merge_ties(b, "bf16", base, exps, m, 0.2, 1.0),
+                oracle.merge_ties_tau(b, "bf16", base, exps, m, tau, 1.0),
+                oracle.merge_dare(b, "bf16", base, exps, m, 0.9, 7, 0, w, 1.0),
+                oracle.merge_dare(b, "bf16", base, exps, m, 0.9, 7, 1, w, 1.0),
+                oracle.ties_tensor_thresholds(b, "bf16", base, exps, m, 0.2)]
+
+    n = oracle.num_threads()
+    try:
+        oracle.set_num_threads(1)
+        assert oracle.num_threads() == 1
+        one = run()
+        oracle.set_num_threads(max(n, 8))
+        many = run()
+    finally:
+        oracle.set_num_threads(n)
+    for a, c in zip(one, many):
+        assert np.array_equal(np.asarray(a).view(np.uint8), np.asarray(c).view(np.uint8))

@@ -186,6 +186,11 @@ CONFIGS = {
                       residency="host_pinned"),
     "qwen2.5-7b": dict(family="qwen2.5-7b", op="dare", p=0.9, seed=7, combine="sign_elect", lam=1.0,
                        budgets=(0.3,), residency="device"),
+    "qwen2.5-7b-dare-sweep": dict(family="qwen2.5-7b", op="dare", p=0.9, seed=7, combine="sign_elect", lam=1.0,
+                                  budgets=(0.1, 0.3, 0.6), residency="device"),
+    "qwen2.5-1.5b-avg": dict(family="qwen2.5-1.5b", op="avg", budgets=(0.25, 0.5, 1.0), residency="device"),
+    "qwen2.5-1.5b-dare-lin": dict(family="qwen2.5-1.5b", op="dare", p=0.9, seed=7, combine="linear", lam=1.0,
+                                  budgets=(0.25, 0.5, 1.0), residency="device"),
     "llama3-8b-k16": dict(family="llama3-8b-k16", op="ties", density=0.1, lam=1.0,
                           budgets=(1 / 16, 0.1, 0.25, 0.5, 0.75, 1.0), residency="host_pinned"),
 }
