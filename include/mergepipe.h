@@ -283,10 +283,11 @@ int mp_merge_ties_tau(const mp_layout* layout, const void* base,
                       void* out, mp_io_stats* io, void* stream);
 
 /* Budgeted DARE (Appendix A.1: random drop and rescale with a fixed seed).
- * Element e of tensor t of expert i is dropped iff u < floor(p * 2^32),
- * u = word (e mod 4) of Philox4x32-10 (Salmon et al., SC 2011) with key
- * (seed, i) and counter (low32(e/4), high32(e/4), t, 0); the decision never
- * depends on the mask.  Kept deltas become float(d * s), s = float(1/(1-p)).
+ * Element e of tensor t of expert i is dropped iff u < floor(p * 2^16),
+ * u = the 16-bit draw h = e mod 8 of Philox4x32-10 (Salmon et al., SC 2011)
+ * with key (seed, i) and counter (low32(e/8), high32(e/8), t, 0): bits
+ * 16 (h mod 2) .. 16 (h mod 2) + 15 of output word h / 2.  The decision
+ * never depends on the mask.  Kept deltas become float(d * s), s = float(1/(1-p)).
  * combine MP_COMBINE_LINEAR: acc = fma(alpha_i, t_i, acc) over selected i
  * increasing, out = round(fma(lambda, acc, x_0)).  MP_COMBINE_SIGN_ELECT:
  * TIES's sign election and disjoint mean (no trim); alpha is ignored and

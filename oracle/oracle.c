@@ -810,9 +810,11 @@ void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t ou
 /* rescale whose randomness is fixed by a seed or a given mask omega). */
 /* Reading: the drop decision for expert i, tensor t, element e of     */
 /* that tensor comes from Philox4x32-10 with key (seed, i) and counter  */
-/* (low32(e/4), high32(e/4), t, 0); output word e mod 4 is u; the       */
-/* element is dropped iff u < T with T = floor(p * 2^32) (fp64).  It    */
-/* depends only on (seed, i, t, e), never on the access mask.  Kept    */
+/* (low32(e/8), high32(e/8), t, 0).  The four output words hold eight   */
+/* 16-bit draws, the low half of a word before its high half: with      */
+/* h = e mod 8, u = bits 16*(h mod 2) .. 16*(h mod 2)+15 of word h/2.   */
+/* The element is dropped iff u < T with T = floor(p * 2^16) (fp64).    */
+/* It depends only on (seed, i, t, e), never on the access mask.  Kept  */
 /* deltas are rescaled: t = float(d * s) with s = float(1 / (1 - p))    */
 /* (fp64 quotient).  Combine: linear -- acc = fma(alpha_i, t_i, acc)    */
 /* over selected i increasing, out = round(fma(lambda, acc, x0)); or    */
@@ -827,7 +829,7 @@ int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
 {
     if (check_common(dtype, K, nb) || !(p >= 0.0 && p < 1.0) || (combine != 0 && combine != 1))
         return -1;
-    const uint32_t T = (uint32_t)floor(p * 4294967296.0);
+    const uint32_t T = (uint32_t)floor(p * 65536.0);
     const float scale = (float)(1.0 / (1.0 - p));
     int bad = 0;
 #pragma omp parallel for schedule(dynamic, 16)
@@ -848,12 +850,13 @@ int orc_merge_dare(int64_t nb, const int64_t* doff, const int64_t* len,
                 continue;
             for (int64_t j = 0; j < n; ++j) {
                 uint64_t e = (uint64_t)elem0[b] + (uint64_t)j;
-                uint64_t q = e >> 2;
+                uint64_t q = e >> 3;
                 uint32_t ctr[4] = {(uint32_t)q, (uint32_t)(q >> 32), (uint32_t)tensor[b], 0u};
                 uint32_t key[2] = {seed, (uint32_t)i};
                 uint32_t word[4];
                 orc_philox4x32_10(ctr, key, word);
-                uint32_t u = word[e & 3u];
+                uint32_t h = (uint32_t)(e & 7u);
+                uint32_t u = (word[h >> 1] >> (16u * (h & 1u))) & 0xFFFFu;
                 float d = delta_vs_base(experts[i], base, dtype, o + j);
                 t[(int64_t)r * n + j] = (u < T) ? 0.0f : d * scale;
             }

@@ -72,6 +72,28 @@ __device__ static inline const uint4* chunk_ptr(const void* base, uint64_t elem_
     return reinterpret_cast<const uint4*>(static_cast<const char*>(base) + elem_off * (uint64_t)esize);
 }
 
+// A block of one checkpoint as a buffer resource: a wave-uniform base
+// address and the block's byte length.  Loads then take one 32-bit offset
+// register, which the base, every expert and the output of a block share;
+// a load past the length returns zeros without touching memory and a store
+// past it is dropped, so lanes beyond the end of a short block need no
+// branch.  Third descriptor word: raw 32-bit data (the gfx9 encoding).
+__device__ inline __amdgpu_buffer_rsrc_t block_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ inline uint4 bld16(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ inline void bst16(__amdgpu_buffer_rsrc_t r, uint32_t off, uint4 v)
+{
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, 0);
+}
+
 // ---------------------------------------------------------------- Philox4x32-10
 // Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3"
 // (SC 2011): ten rounds of two 32x32->64 multiplies with the Weyl-bumped key.

@@ -148,33 +148,40 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
             tau[g * K + i] = th;
         }
     };
-    auto load_expert = [&](int i, uint4 (&xe)[R]) {
-        const uint4* e = chunk_ptr(ex.p[i], off, Fmt<DT>::esize);
+    // Loads are buffer loads over the block's byte range: lanes past a short
+    // block's end read zeros without a branch, so every load of a lane is
+    // issued back to back and the waits count them exactly.
+    const uint32_t nbytes = nch * 16u;
+    auto load_expert = [&](int i, uint32_t bytes, uint4 (&xe)[R]) {
+        const __amdgpu_buffer_rsrc_t re = block_rsrc(chunk_ptr(ex.p[i], off, Fmt<DT>::esize), bytes);
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const uint32_t c = (uint32_t)(r * 64 + lane);
-            xe[r] = (c < nch) ? e[c] : make_uint4(0u, 0u, 0u, 0u);
-        }
+        for (int r = 0; r < R; ++r)
+            xe[r] = bld16(re, (uint32_t)(r * 64 + lane) * 16u);
     };
-    // the wave's first expert is read before the base is staged, so that the
-    // two reads overlap; further experts (K > 4) are read one at a time
-    uint4 xf[R];
-    if (wave < K)
-        load_expert(wave, xf);
+    // The base's chunks are requested first, then the wave's first expert
+    // (a wave without one reads an empty range), so the base arrives first
+    // and is staged while the expert is still in flight; further experts
+    // (K > 4) are read one at a time.
+    uint4 xbr[R / 4];
     if (!DELTA) {  // explicit deltas need no base
-        const uint4* b = chunk_ptr(base, off, Fmt<DT>::esize);
+        const __amdgpu_buffer_rsrc_t rb = block_rsrc(chunk_ptr(base, off, Fmt<DT>::esize), nbytes);
 #pragma unroll
-        for (int q = 0; q < R / 4; ++q) {
-            const uint32_t c = (uint32_t)(q * 256 + t);
-            xb[c] = (c < nch) ? b[c] : make_uint4(0u, 0u, 0u, 0u);
-        }
+        for (int q = 0; q < R / 4; ++q)
+            xbr[q] = bld16(rb, (uint32_t)(q * 256 + t) * 16u);
+    }
+    uint4 xf[R];
+    load_expert(wave < K ? wave : 0, wave < K ? nbytes : 0u, xf);
+    if (!DELTA) {
+#pragma unroll
+        for (int q = 0; q < R / 4; ++q)
+            xb[q * 256 + t] = xbr[q];  // zeros past the block's end
         __syncthreads();
     }
     if (wave < K)
         unit(wave, xf);
     for (int i = wave + 4; i < K; i += 4) {
         uint4 xe[R];
-        load_expert(i, xe);
+        load_expert(i, nbytes, xe);
         unit(i, xe);
     }
 }

@@ -45,28 +45,6 @@ struct DevSrc {
     }
 };
 
-// A block of one checkpoint as a buffer resource: a wave-uniform base
-// address and the block's byte length.  Loads then take one 32-bit offset
-// register, which the base, every expert and the output of a block share;
-// a load past the length returns zeros without touching memory and a store
-// past it is dropped, so lanes beyond the end of a short block need no
-// branch.  Third descriptor word: raw 32-bit data (the gfx9 encoding).
-__device__ inline __amdgpu_buffer_rsrc_t block_rsrc(const void* p, uint32_t bytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
-}
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-__device__ inline uint4 bld16(__amdgpu_buffer_rsrc_t r, uint32_t off)
-{
-    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-    return make_uint4(v.x, v.y, v.z, v.w);
-}
-__device__ inline void bst16(__amdgpu_buffer_rsrc_t r, uint32_t off, uint4 v)
-{
-    const u32x4_t w = {v.x, v.y, v.z, v.w};
-    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, 0);
-}
-
 // Selected expert blocks staged in device memory (host experts): the
 // launch covers blocks b0 .. b0 + grid - 1; block b0 + j's selected experts
 // lie back to back, in increasing expert order (rank r), from stage + soff[j].
@@ -269,20 +247,29 @@ __global__ __launch_bounds__(kTE, 8) void k_merge_elem(Src src, const void* __re
         for (int q = 0; q < CPT; ++q) {
             float x[V];
             Fmt<DT>::unpack(raw[q], x);
-            uint32_t word[V];
+            bool keep[V];  // DARE: the element survives the drop
             if (DARE) {
-                // Philox words for elements e .. e+V-1 of tensor `tens` (V is 4 or 8)
+                // One Philox4x32-10 draw per eight elements of tensor
+                // `tens`: element e takes the 16-bit half (e mod 8) of draw
+                // e/8, the low half of a word first, and is dropped iff that
+                // half is below drop_T >> 16.  A high half is compared in
+                // place (w < drop_T), a low half as the word's low 16 bits.
                 const uint64_t e = e0 + (uint64_t)(tile + q * kTE + t) * V;
-#pragma unroll
-                for (int h = 0; h < V / 4; ++h) {
-                    const uint64_t qq = (e >> 2) + h;
-                    const uint4 r4 = philox4x32_10(make_uint4((uint32_t)qq, (uint32_t)(qq >> 32), tens, 0u), seed,
-                                                   (uint32_t)i);
-                    word[h * 4 + 0] = r4.x;
-                    word[h * 4 + 1] = r4.y;
-                    word[h * 4 + 2] = r4.z;
-                    word[h * 4 + 3] = r4.w;
+                const uint64_t qq = e >> 3;
+                const uint4 r4 = philox4x32_10(make_uint4((uint32_t)qq, (uint32_t)(qq >> 32), tens, 0u), seed,
+                                               (uint32_t)i);
+                uint32_t w[V / 2];  // the draw's words for this chunk's elements
+                if (V == 8) {
+                    w[0] = r4.x; w[1 % (V / 2)] = r4.y; w[2 % (V / 2)] = r4.z; w[3 % (V / 2)] = r4.w;
+                } else {  // fp32: a chunk is the first or the second half of a draw
+                    const bool second = (e & 4u) != 0u;
+                    w[0] = second ? r4.z : r4.x;
+                    w[1] = second ? r4.w : r4.y;
                 }
+                const uint32_t t16 = drop_T >> 16;
+#pragma unroll
+                for (int v = 0; v < V; ++v)
+                    keep[v] = (v & 1) ? !(w[v >> 1] < drop_T) : !((w[v >> 1] & 0xffffu) < t16);
             }
 #pragma unroll
             for (int v = 0; v < V; ++v) {
@@ -299,11 +286,13 @@ __global__ __launch_bounds__(kTE, 8) void k_merge_elem(Src src, const void* __re
                     ns[e] = ns[e] + (kn ? d : 0.0f);
                     cpn[e] += kp ? 1u : (kn ? 0x10000u : 0u);
                 } else {
-                    const float tv = (word[v] < drop_T) ? 0.0f : d * scale;
                     if (MODE == M_DARE_LIN) {
-                        acc[e] = fmaf(alpha.v[i], tv, acc[e]);
+                        acc[e] = fmaf(alpha.v[i], keep[v] ? d * scale : 0.0f, acc[e]);
                     } else {
-                        const bool pos = tv > 0.0f, neg = tv < 0.0f;
+                        // scale >= 1 is finite, so a kept d * scale has the
+                        // sign of d and is zero only when d is
+                        const float tv = d * scale;
+                        const bool pos = keep[v] && d > 0.0f, neg = keep[v] && d < 0.0f;
                         ps[e] = ps[e] + (pos ? tv : 0.0f);
                         ns[e] = ns[e] + (neg ? tv : 0.0f);
                         cpn[e] += pos ? 1u : (neg ? 0x10000u : 0u);
@@ -327,53 +316,60 @@ __global__ __launch_bounds__(kTE, 8) void k_merge_elem(Src src, const void* __re
         // elect by comparing the rounded masses P and -N; mean of the
         // agreeing entries
         uint32_t den[E];
+        bool odd = false;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const bool up = ps[e] > -ns[e];
             const bool dn = ps[e] < -ns[e];
-            acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);
+            acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);  // never NaN: a NaN mass elects nothing
             // with no elected sign acc is 0 and any count >= 1 gives 0
             den[e] = up ? (cpn[e] & 0xffffu) : (dn ? (cpn[e] >> 16) : 1u);
+            odd |= (den[e] & (den[e] - 1u)) != 0u;
         }
-        if (MODE == M_TIES_TAU && K <= 4) {
-            // den is 1..4: q = mass * fl32(1/den) and one residual step, the
-            // correctly rounded quotient of a finite mass (as in
-            // ties_store_small); a wave with an infinite mass divides
-            bool bad = false;
-            float q[E];
+        bool tiny = false;
+        if (__any(odd)) {
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                tiny |= (fabsf(acc[e]) < 0x1p-100f) & (acc[e] != 0.0f);
+        }
+        if (!__any(odd)) {
+            // counts that are powers of two divide by exact scaling, one
+            // rounding of the quotient
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+                acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
+        } else if (!__any(tiny)) {
+            // The correctly rounded quotient acc / den (1 <= den <= 32)
+            // without a division.  Lane j holds h + l, two terms of 1/j:
+            // h <= 1/j within an ulp, l = max(fl32((1 - j h) h), 2^-126) > 0
+            // (the residual 1 - j h is exact), |h + l - 1/j| < 2^-44 / j.  Then
+            // fma(a, h, a l) lies within 2^-43 of a / den (relative).  When
+            // a / den is a normal number, every rounding boundary (a midpoint
+            // between neighbouring floats, which a / den never equals) lies
+            // at least 2^-25 / den >= 2^-30 (relative) away from it, so both
+            // round to the same value.  |a| >= 2^-100 keeps a / den and a l
+            // clear of the subnormal range (smaller masses divide); l > 0,
+            // so an infinite mass gives a l of its own sign and stays
+            // infinite.
+            const float fj = (float)(t > 0 ? t : 1);
+            float h = __builtin_amdgcn_rcpf(fj);
+            float r = fmaf(-fj, h, 1.0f);
+            if (r < 0.0f) {  // the hardware reciprocal rounded up: one ulp down
+                h = __uint_as_float(__float_as_uint(h) - 1u);
+                r = fmaf(-fj, h, 1.0f);
+            }
+            const float l = fmaxf(r * h, 0x1p-126f);
 #pragma unroll
             for (int e = 0; e < E; ++e) {
-                const float cx = (float)den[e];
-                const float cy = (den[e] == 3u) ? 0x1.555556p-2f
-                                                : __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
-                const float q0 = acc[e] * cy;
-                q[e] = fmaf(fmaf(-cx, q0, acc[e]), cy, q0);
-                bad |= q[e] != q[e];
+                const int src = (int)(den[e] << 2);
+                const float he = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(h)));
+                const float le = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(l)));
+                acc[e] = fmaf(acc[e], he, acc[e] * le);
             }
-            if (__any(bad)) {
-#pragma unroll
-                for (int e = 0; e < E; ++e)
-                    q[e] = acc[e] / (float)den[e];
-            }
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                acc[e] = q[e];
         } else {
-            // a count that is a power of two divides by exact scaling,
-            // correctly rounded as the quotient; otherwise IEEE division
-            bool odd = false;
 #pragma unroll
             for (int e = 0; e < E; ++e)
-                odd |= (den[e] & (den[e] - 1u)) != 0u;
-            if (__any(odd)) {
-#pragma unroll
-                for (int e = 0; e < E; ++e)
-                    acc[e] = acc[e] / (float)den[e];
-            } else {
-#pragma unroll
-                for (int e = 0; e < E; ++e)
-                    acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
-            }
+                acc[e] = acc[e] / (float)den[e];
         }
     }
 #pragma unroll
@@ -1013,7 +1009,7 @@ hipError_t launch_typed(const BlockTable& bt, const MergeArgs& a, const Src& src
     while ((per_wg << sub_log2) < (int64_t)bt.max_len)
         ++sub_log2;
     const dim3 grid((unsigned)nb), egrid((unsigned)(nb << sub_log2));
-    const uint32_t T = (uint32_t)floor(a.p * 4294967296.0);
+    const uint32_t T = (uint32_t)floor(a.p * 65536.0) << 16;  // the 16-bit drop threshold, in the top half
     const float scale = (float)(1.0 / (1.0 - a.p));
     switch (a.op) {
     case Op::AVG:

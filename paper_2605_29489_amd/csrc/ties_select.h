@@ -146,10 +146,25 @@ __device__ inline uint32_t wave_sum_u32(uint32_t v)
 
 // Wave-level: the r-th largest of the n patterns in `list`, all of which
 // share the key (pattern >> KS); the low bits are fixed from the top down.
+// Up to 64 patterns sit one per lane in a register, and each bit then
+// costs one compare: the count is the popcount of its lane mask.
 __device__ inline uint32_t wave_select_list(const uint32_t* __restrict__ list, uint32_t n, uint32_t key,
                                             uint32_t r, int lane)
 {
     uint32_t pref = key << ties::KS;
+    if (n <= 64u) {
+        const uint32_t v = ((uint32_t)lane < n) ? list[lane] : 0u;  // 0 lies below every candidate
+        // wave-uniform values, kept in scalar registers
+        uint32_t sp = (uint32_t)__builtin_amdgcn_readfirstlane((int)pref);
+        const uint32_t sr = (uint32_t)__builtin_amdgcn_readfirstlane((int)r);
+#pragma unroll
+        for (int bit = ties::KS - 1; bit >= 0; --bit) {
+            const uint32_t cand = sp | (1u << bit);
+            if ((uint32_t)__popcll(__ballot(v >= cand)) >= sr)
+                sp = cand;
+        }
+        return sp;
+    }
 #pragma unroll 1
     for (int bit = ties::KS - 1; bit >= 0; --bit) {
         const uint32_t cand = pref | (1u << bit);
@@ -309,11 +324,13 @@ __device__ inline uint32_t wave_kth_largest(char* base, int row_off, const float
             const uint32_t mg = mag_bits(d[e]);
             const bool in = (mg >> KS) == key;
             const unsigned long long bal = __ballot(in);
+            // position: n plus the lanes below this one that list a value
             const uint32_t pos =
-                n + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-            if (in && pos < (uint32_t)NB)
+                __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, n));
+            const uint32_t nn = n + (uint32_t)__popcll(bal);  // wave-uniform: one bound test for all lanes
+            if (in && nn <= (uint32_t)NB)
                 h[pos] = mg;
-            n += (uint32_t)__popcll(bal);
+            n = nn;
         }
         wave_lds_sync();
         if (n <= (uint32_t)NB)

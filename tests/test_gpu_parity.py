@@ -355,6 +355,19 @@ def test_block_sizes(mp, be):
     _run_all(mp, spec, base, exps, "dare_lin", [0.5], alpha=[0.3, 0.2, 0.4, 0.1], p=0.3, seed=11, lam=1.0)
 
 
+@pytest.mark.parametrize("be", [1028, 4100])
+def test_dare_fp32_blocks_starting_mid_draw(mp, be):
+    # fp32 blocks of be = 4 (mod 8) elements: every other block of a tensor
+    # starts in the middle of a Philox draw (eight elements per draw), so its
+    # chunks take the draw's upper two words
+    t = (("a", (3 * 4100 + 8,)), ("b", (12,)), ("c", (5000,)), ("d", (4, 1025)))
+    spec = FamilySpec("fp32-mid-draw", t, "f32", be, 3, ())
+    base, exps = make_family(spec, seed=5)
+    _say(f"case fp32 DARE block_elems={be}")
+    for op in ("dare_lin", "dare_sign"):
+        _run_all(mp, spec, base, exps, op, [0.4, 1.0], alpha=[0.5, 0.25, 0.25], p=0.7, seed=13, lam=0.9)
+
+
 def _as_deltas(base_np, exps_np, dtype):
     """Explicit-delta experts of a family: fl32(W_i - W_0) in the checkpoint
     dtype (any arrays of that dtype are valid deltas)."""

@@ -719,6 +719,24 @@ def test_ties_tensor_scope_on_single_block_tensors_is_the_block_scope():
                               oracle.merge_ties(b, "bf16", base, exps, full, dens, 1.0))
 
 
+def test_ties_from_catalog_thresholds_equals_ties_on_any_mask():
+    # the per-unit threshold depends on the unit's own block only, so TIES
+    # from thresholds computed over the whole checkpoint equals TIES that
+    # trims the selected units itself, whatever the mask (the in-merge route
+    # recomputes exactly the catalog value)
+    rng = np.random.default_rng(44)
+    numel = [4096 * 3 + 100, 1536, 256, 4096 * 2]
+    b = oracle.Blocks(numel, 4096)
+    for dtype in ("f32", "bf16"):
+        base, exps = _tiny_family(rng, numel, 5, dtype, scale=1e-3)
+        for dens in (0.1, 0.2, 0.7):
+            tau = oracle.ties_thresholds(b, dtype, base, exps, dens)
+            for _ in range(4):
+                m = rng.integers(0, 32, b.G).astype(np.uint32)
+                assert np.array_equal(oracle.merge_ties_tau(b, dtype, base, exps, m, tau, 1.0),
+                                      oracle.merge_ties(b, dtype, base, exps, m, dens, 1.0)), (dtype, dens)
+
+
 def test_ties_tensor_thresholds_non_anticipatory():
     rng = np.random.default_rng(43)
     numel = [4096 * 3, 1536]
@@ -1219,31 +1237,40 @@ def test_dare_masks_independent_across_experts_tensors_and_lanes():
     assert abs((k0 & k1).mean() - 0.25) < 6 * sd  # experts draw independent masks
     half = numel[0]
     assert abs((k0[:half] == k0[half:]).mean() - 0.5) < 6 * math.sqrt(0.25 / half)  # tensors differ
-    g4 = k0.reshape(-1, 4)
-    all_eq = (g4.all(1) | (~g4).all(1)).mean()
-    assert abs(all_eq - 0.125) < 6 * math.sqrt(0.125 * 0.875 / g4.shape[0])  # the 4 words of a draw differ
+    g8 = k0.reshape(-1, 8)
+    all_eq = (g8.all(1) | (~g8).all(1)).mean()
+    assert abs(all_eq - 1 / 128) < 6 * math.sqrt(1 / 128 * 127 / 128 / g8.shape[0])  # the 8 draws of a call differ
+    lo = k0.reshape(-1, 2)
+    assert abs((lo[:, 0] == lo[:, 1]).mean() - 0.5) < 6 * math.sqrt(0.25 / lo.shape[0])  # a word's two halves differ
     # a different seed gives a different mask
     k0b = oracle.merge_dare(b, "f32", base, exps, np.full(b.G, 1, np.uint32), p, 4, 0, [1.0, 1.0], 1.0) != 0
     assert abs((k0 == k0b).mean() - 0.5) < 6 * math.sqrt(0.25 / n)
 
 
 def test_dare_drop_decision_follows_counter_mapping():
-    # element e of tensor t of expert i uses Philox word e%4 of counter
-    # (e//4, 0, t, 0) under key (seed, i); dropped iff word < floor(p*2^32).
-    numel = [64, 4096 + 64]
-    b = oracle.Blocks(numel, 4096)
-    base, exps = _const_delta_family(numel, 3)
-    p, seed = 0.5, 0xDEADBEEF
-    out = oracle.merge_dare(b, "f32", base, exps, np.full(b.G, 4, np.uint32), p, seed, 0,
-                            [0.0, 0.0, 1.0], 1.0)
-    T = math.floor(p * 2**32)
-    starts = [0, 64]
-    for t, n in enumerate(numel):
-        for e in list(range(0, 12)) + [n - 1, n - 5, 4096 + 3] if n > 4096 else range(n):
-            if e >= n:
-                continue
-            w = oracle.philox4x32_10([e // 4, 0, t, 0], [seed, 2])[e % 4]
-            assert (out[starts[t] + e] == 0) == (int(w) < T)
+    # element e of tensor t of expert i uses the 16-bit half e%8 of the
+    # Philox output for counter (e//8, 0, t, 0) under key (seed, i): word
+    # (e%8)//2, its low half for even e; dropped iff half < floor(p*2^16).
+    # Tensors of 64, 4096+64 and 4100 elements: fp32 blocks of 4100 start
+    # at element 0 only, so every block starts a draw; the 4100-element
+    # block size below puts a second block of tensor 2 at element 4100,
+    # the middle of draw 512.
+    for numel, be in (([64, 4096 + 64], 4096), ([8200, 20], 4100)):
+        b = oracle.Blocks(numel, be)
+        base, exps = _const_delta_family(numel, 3)
+        for p, seed in ((0.5, 0xDEADBEEF), (0.9, 7), (0.3, 0)):
+            out = oracle.merge_dare(b, "f32", base, exps, np.full(b.G, 4, np.uint32), p, seed, 0,
+                                    [0.0, 0.0, 1.0], 1.0)
+            T = math.floor(p * 2**16)
+            start = 0
+            for t, n in enumerate(numel):
+                probe = sorted({e for e in list(range(0, 20)) + [n - 1, n - 5, n - 8, 4096 + 3, 4100, 4101, 4103,
+                                                                 4104] if 0 <= e < n})
+                for e in probe:
+                    w = int(oracle.philox4x32_10([e // 8, 0, t, 0], [seed, 2])[(e % 8) // 2])
+                    u = (w >> 16) if e % 2 else (w & 0xFFFF)
+                    assert (out[start + e] == 0) == (u < T), (numel, p, t, e)
+                start += n
 
 
 def test_dare_non_anticipatory_drop_mask():
