@@ -266,7 +266,11 @@ int mp_merge_ties(const mp_layout* layout, const void* base,
  * these thresholds is the tensor-scope TIES merge.  mask: device uint32[G]
  * (the mask the merge will use); tau: device uint32[G*K].  Residency
  * MP_DEVICE or MP_HOST_PINNED (MP_E_UNSUPPORTED for MP_HOST_PAGEABLE),
- * optionally with MP_EXPERTS_DELTA.  Asynchronous on `stream`. */
+ * optionally with MP_EXPERTS_DELTA.  Runs on `stream` and returns once the
+ * thresholds are complete: the kernels share one scratch area per device,
+ * so calls on different streams run one after the other, and a selection
+ * that finds no cut (an internal error, never expected) returns MP_E_HIP
+ * with tau unspecified. */
 int mp_ties_tensor_thresholds(const mp_layout* layout, const void* base,
                               const void* const* experts, int32_t K, int32_t residency,
                               const uint32_t* mask, double density, uint32_t* tau,
@@ -364,7 +368,10 @@ uint64_t mp_workspace_bytes(void);
  * when a staged call runs, the pack of its chunk n (0-based; a chunk that
  * packs at least one block) reports a failed read, as an unreadable expert
  * file does: the call returns MP_E_IO after the kernels of chunks 0..n-1
- * were enqueued, so outputs may be partly written. */
+ * were enqueued, so outputs may be partly written.
+ * With MP_FAULT_TENSOR_NO_CUT=1 set, mp_ties_tensor_thresholds sends its
+ * first (expert, tensor) pair down the no-cut error path: the kernels finish
+ * normally and the call returns MP_E_HIP. */
 
 /* Message for the last failing call on this thread ("" if none). */
 const char* mp_last_error(void);

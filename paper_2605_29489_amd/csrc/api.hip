@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -71,8 +72,9 @@ struct DeviceWs {
     unsigned long long* cov = nullptr;         // coverage counters, grown on demand
     int64_t cov_cap = 0;
     uint32_t* tt_hist = nullptr;               // tensor-scope TIES: digit histograms per (expert, tensor)
-    uint4* tt_state = nullptr;                 //   and the select state per pair
+    uint4* tt_state = nullptr;                 //   and the select state per pair (+ the error word)
     int64_t tt_pairs = 0;
+    uint32_t* h_tt_err = nullptr;              // pinned copy of the error word
 };
 
 std::mutex g_mu;
@@ -125,6 +127,7 @@ void free_ws(int dev, DeviceWs& w)
     (void)ws_free_r(w.cov);
     (void)ws_free_r(w.tt_hist);
     (void)ws_free_r(w.tt_state);
+    (void)ws_host_free_r(w.h_tt_err);
     (void)hipSetDevice(cur);
 }
 
@@ -285,7 +288,8 @@ int get_ws(DeviceWs** out)
     if ((e = plan_ctl_alloc(&w->plan.ctl)) != hipSuccess ||
         (e = ws_host_malloc((void**)&w->plan.h_stats, sizeof(uint64_t) * 8)) != hipSuccess ||
         (e = ws_malloc((void**)&w->counters, sizeof(unsigned long long) * 256)) != hipSuccess ||
-        (e = ws_host_malloc((void**)&w->h_counters, sizeof(unsigned long long) * 256)) != hipSuccess) {
+        (e = ws_host_malloc((void**)&w->h_counters, sizeof(unsigned long long) * 256)) != hipSuccess ||
+        (e = ws_host_malloc((void**)&w->h_tt_err, sizeof(uint32_t))) != hipSuccess) {
         free_ws(dev, *w);
         return fail(MP_E_NOMEM, "workspace allocation failed: %s", hipGetErrorString(e));
     }
@@ -781,13 +785,28 @@ int mp_ties_tensor_thresholds(const mp_layout* layout, const void* base, const v
         ws.tt_state = nullptr;
         ws.tt_pairs = 0;
         if ((e = ws_malloc((void**)&ws.tt_hist, sizeof(uint32_t) * 2048 * (size_t)pairs)) != hipSuccess ||
-            (e = ws_malloc((void**)&ws.tt_state, sizeof(uint4) * (size_t)pairs)) != hipSuccess)
+            (e = ws_malloc((void**)&ws.tt_state, sizeof(uint4) * (size_t)(pairs + 1))) != hipSuccess)
             return fail(MP_E_NOMEM, "tensor-scope TIES buffers: %s", hipGetErrorString(e));
         ws.tt_pairs = pairs;
     }
-    if ((e = launch_ties_tensor(bt, base, c.ex, K, mask, density, tau, ws.tt_hist, ws.tt_state,
-                                static_cast<hipStream_t>(stream), delta)) != hipSuccess)
+    // The scratch is shared by every call on this device: the call returns
+    // only once its kernels are done (under the library lock), so a call on
+    // another stream never finds it in use, and the error word is read here.
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (bt.G == 0)
+        return MP_OK;  // no units: nothing to select
+    const char* hook = std::getenv("MP_FAULT_TENSOR_NO_CUT");
+    const bool force = hook != nullptr && hook[0] == '1';
+    if ((e = launch_ties_tensor(bt, base, c.ex, K, mask, density, tau, ws.tt_hist, ws.tt_state, s, delta, force)) !=
+        hipSuccess)
         return hip_fail(e, "tensor-scope thresholds launch");
+    if ((e = hipMemcpyAsync(ws.h_tt_err, ws.tt_state + pairs, sizeof(uint32_t), hipMemcpyDeviceToHost, s)) !=
+        hipSuccess)
+        return hip_fail(e, "tensor-scope error word readback");
+    if ((e = hipStreamSynchronize(s)) != hipSuccess)
+        return hip_fail(e, "hipStreamSynchronize");
+    if (*ws.h_tt_err != 0u)
+        return fail(MP_E_HIP, "tensor-scope threshold kernels reported an internal error (no cut found)");
     return MP_OK;
 }
 

@@ -93,7 +93,8 @@ __global__ __launch_bounds__(kTT) void k_tt_hist(const void* __restrict__ base, 
 
 __global__ __launch_bounds__(kTT) void k_tt_resolve(uint4* __restrict__ state, const uint32_t* __restrict__ hist,
                                                      const uint64_t* __restrict__ tnumel, int K, int T,
-                                                     double density, int pass)
+                                                     double density, int pass, uint32_t* __restrict__ err,
+                                                     int force_no_cut)
 {
     const int lane = threadIdx.x & 63;
     const int64_t q = (int64_t)blockIdx.x * (kTT / 64) + (threadIdx.x >> 6);
@@ -148,10 +149,14 @@ __global__ __launch_bounds__(kTT) void k_tt_resolve(uint4* __restrict__ state, c
             acc += c[j];
         }
     }
-    const unsigned long long bal = __ballot(bin >= 0);
+    unsigned long long bal = __ballot(bin >= 0);
+    if (force_no_cut && q == 0)
+        bal = 0ull;  // test hook: pair 0 takes the error path
     if (bal == 0ull) {  // cannot happen: the prefix's elements hold the rank-th largest
-        if (lane == 0)
+        if (lane == 0) {
             state[q] = make_uint4(st.x, 0u, 1u, 0u);
+            err[0] = 1u;  // the host reports an internal error
+        }
         return;
     }
     const int src = __ffsll((long long)bal) - 1;
@@ -184,15 +189,17 @@ __global__ __launch_bounds__(kTT) void k_tt_expand(const uint4* __restrict__ sta
 
 hipError_t launch_ties_tensor(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
                               const uint32_t* mask, double density, uint32_t* tau, uint32_t* hist, uint4* state,
-                              hipStream_t s, bool delta)
+                              hipStream_t s, bool delta, bool force_no_cut)
 {
     if (bt.G == 0)
         return hipSuccess;
     const int T = (int)bt.n_tensors;
     const int64_t pairs = (int64_t)K * T;
     const int64_t nh = pairs * kDigBins;
-    hipLaunchKernelGGL(k_tt_zero, dim3((unsigned)std::min<int64_t>((pairs * 4 + kTT - 1) / kTT, 1024)), dim3(kTT), 0,
-                       s, reinterpret_cast<uint32_t*>(state), pairs * 4);
+    // the state words and, after them, the error word start at zero
+    uint32_t* err = reinterpret_cast<uint32_t*>(state + pairs);
+    hipLaunchKernelGGL(k_tt_zero, dim3((unsigned)std::min<int64_t>((pairs * 4 + 4 + kTT - 1) / kTT, 1024)), dim3(kTT),
+                       0, s, reinterpret_cast<uint32_t*>(state), pairs * 4 + 4);
     const dim3 hgrid((unsigned)bt.n_chunks, (unsigned)K);
     for (int pass = 0; pass < 3; ++pass) {
         hipLaunchKernelGGL(k_tt_zero, dim3((unsigned)std::min<int64_t>((nh + kTT - 1) / kTT, 2048)), dim3(kTT), 0, s,
@@ -206,7 +213,7 @@ hipError_t launch_ties_tensor(const BlockTable& bt, const void* base, const Expe
         else
             delta ? go(k_tt_hist<1, true>) : go(k_tt_hist<1, false>);
         hipLaunchKernelGGL(k_tt_resolve, dim3((unsigned)((pairs + 3) / 4)), dim3(kTT), 0, s, state, hist,
-                           bt.d_tnumel, K, T, density, pass);
+                           bt.d_tnumel, K, T, density, pass, err, force_no_cut ? 1 : 0);
     }
     hipLaunchKernelGGL(k_tt_expand, dim3((unsigned)((bt.G * K + kTT - 1) / kTT)), dim3(kTT), 0, s, state,
                        bt.d_tensor, bt.G, K, T, tau);

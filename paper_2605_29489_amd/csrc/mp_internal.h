@@ -127,10 +127,13 @@ hipError_t launch_plan(const BlockTable& bt, PlanScratch& ps, int K, const float
 
 // TIES thresholds at tensor scope (k_tensor_ties.hip): per unit (g, i) the
 // k-th largest |d| of tensor(g)'s zero-completed masked deltas of expert i.
-// hist: device uint32[K * n_tensors * 2048], state: device uint4[K * n_tensors].
+// hist: device uint32[K * n_tensors * 2048], state: device uint4[K * n_tensors
+// + 1]; the word after the pairs' states is set to nonzero if a selection
+// found no cut (an internal error).  force_no_cut: a test hook that sends
+// the first pair down that error path (the kernels still finish normally).
 hipError_t launch_ties_tensor(const BlockTable& bt, const void* base, const ExpertPtrs& ex, int K,
                               const uint32_t* mask, double density, uint32_t* tau, uint32_t* hist, uint4* state,
-                              hipStream_t s, bool delta);
+                              hipStream_t s, bool delta, bool force_no_cut);
 
 // ---------------------------------------------------------------- LoRA source (k_lora.hip)
 constexpr int kMaxLoraRank = 64;

@@ -175,3 +175,39 @@ def test_argument_errors_write_no_output(mp):
     torch.cuda.synchronize()
     assert torch.equal(out.view(torch.int16), before.view(torch.int16))
     assert bool((sumsq == 7.0).all()) and bool((tau == 7).all()) and bool((m2 == 5).all())
+
+
+def test_tensor_thresholds_report_no_cut_and_serialise_streams(mp):
+    # the selection's "no cut" branch (never reached by real data) is forced
+    # from the host: the kernels finish normally, the call reads the error
+    # word and returns MP_E_HIP; without the hook, calls on two streams that
+    # share the device scratch give the oracle's thresholds back to back
+    import torch
+    spec, base_np, exps_np = _family()
+    L, blocks, K, mask, m_np = _setup(mp, spec, base_np, exps_np)
+    base = to_dev(base_np, "bf16")
+    exps = [to_dev(e, "bf16") for e in exps_np]
+    tau = torch.empty(blocks.G * K, dtype=torch.int32, device="cuda")
+    try:
+        os.environ["MP_FAULT_TENSOR_NO_CUT"] = "1"
+        with pytest.raises(mp.MPError) as ei:
+            mp.mp_ties_tensor_thresholds(L, base, exps, mask, 0.2, tau)
+        assert ei.value.code == mp.MP_E_HIP and "internal error" in str(ei.value)
+    finally:
+        os.environ.pop("MP_FAULT_TENSOR_NO_CUT", None)
+    full = np.full(blocks.G, (1 << K) - 1, np.uint32)
+    mask_full = torch.from_numpy(full.view(np.int32)).cuda()
+    want_half = oracle.expand_tensor_thresholds(
+        blocks, oracle.ties_tensor_thresholds(blocks, "bf16", base_np, exps_np, m_np, 0.2))
+    want_full = oracle.expand_tensor_thresholds(
+        blocks, oracle.ties_tensor_thresholds(blocks, "bf16", base_np, exps_np, full, 0.1))
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    tau2 = torch.empty_like(tau)
+    torch.cuda.synchronize()  # inputs made on the current stream are ready for s1 and s2
+    for _ in range(3):
+        mp.mp_ties_tensor_thresholds(L, base, exps, mask, 0.2, tau, stream=s1)
+        mp.mp_ties_tensor_thresholds(L, base, exps, mask_full, 0.1, tau2, stream=s2)
+        torch.cuda.synchronize()
+        assert np.array_equal(tau.cpu().numpy().view(np.uint32), want_half)
+        assert np.array_equal(tau2.cpu().numpy().view(np.uint32), want_full)
+    _say("  forced no-cut: MP_E_HIP; two streams in turn: both thresholds equal the oracle's")
