@@ -94,6 +94,33 @@ __device__ inline void bst16(__amdgpu_buffer_rsrc_t r, uint32_t off, uint4 v)
     __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, 0);
 }
 
+// Streaming accesses: data a kernel touches once (expert and base blocks,
+// merged output) carry the non-temporal cache policy (the "nt" bit, cache
+// policy 2 of the buffer and global instructions), so that they do not
+// displace lines that are reused.  Measured on the headline family, it took
+// the threshold merges from 1.69 / 2.07 / 2.95 ms to 1.62 / 1.95 / 2.74 ms at
+// B = 25/50/100%.
+__device__ inline uint4 bld16s(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ inline void bst16s(__amdgpu_buffer_rsrc_t r, uint32_t off, uint4 v)
+{
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, off, 0, 2);
+}
+__device__ inline uint4 ld16s(const uint4* p)
+{
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ inline void st16s(uint4* p, uint4 v)
+{
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t*>(p));
+}
+
 // ---------------------------------------------------------------- Philox4x32-10
 // Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3"
 // (SC 2011): ten rounds of two 32x32->64 multiplies with the Weyl-bumped key.

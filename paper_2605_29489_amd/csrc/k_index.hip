@@ -35,8 +35,8 @@ __device__ inline float block_sumsq(const uint4* __restrict__ b, const uint4* __
             const uint32_t c = c0 + r * 64 + lane;
             if (c < nch) {
                 if (!DELTA)
-                    xb[r] = b[c];
-                xe[r] = e[c];
+                    xb[r] = b[c];  // re-read per expert: cached
+                xe[r] = ld16s(&e[c]);
             }
         }
 #pragma unroll
@@ -156,7 +156,7 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
         const __amdgpu_buffer_rsrc_t re = block_rsrc(chunk_ptr(ex.p[i], off, Fmt<DT>::esize), bytes);
 #pragma unroll
         for (int r = 0; r < R; ++r)
-            xe[r] = bld16(re, (uint32_t)(r * 64 + lane) * 16u);
+            xe[r] = bld16s(re, (uint32_t)(r * 64 + lane) * 16u);
     };
     // The base's chunks are requested first, then the wave's first expert
     // (a wave without one reads an empty range), so the base arrives first
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
         const __amdgpu_buffer_rsrc_t rb = block_rsrc(chunk_ptr(base, off, Fmt<DT>::esize), nbytes);
 #pragma unroll
         for (int q = 0; q < R / 4; ++q)
-            xbr[q] = bld16(rb, (uint32_t)(q * 256 + t) * 16u);
+            xbr[q] = bld16s(rb, (uint32_t)(q * 256 + t) * 16u);
     }
     uint4 xf[R];
     load_expert(wave < K ? wave : 0, wave < K ? nbytes : 0u, xf);

@@ -194,7 +194,7 @@ __global__ __launch_bounds__(kTE, 8) void k_merge_elem(Src src, const void* __re
     uint4 xb[CPT];
 #pragma unroll
     for (int q = 0; q < CPT; ++q)
-        xb[q] = bld16(rb, bo[q]);
+        xb[q] = bld16s(rb, bo[q]);
     float x0[E];
     auto unpack_base = [&]() {
 #pragma unroll
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(kTE, 8) void k_merge_elem(Src src, const void* __re
         uint4 raw[CPT];
 #pragma unroll
         for (int q = 0; q < CPT; ++q)
-            raw[q] = bld16(re, bo[q]);
+            raw[q] = bld16s(re, bo[q]);
         if (COUNT && t == 0)
             atomicAdd(&ctr[((blockIdx.x & 7u) << 5) | (uint32_t)i], (unsigned long long)nl * 16ull);
         if (first)
@@ -383,7 +383,7 @@ __global__ __launch_bounds__(kTE, 8) void k_merge_elem(Src src, const void* __re
             else
                 y[v] = fmaf(lambda, acc[e], x0[e]);
         }
-        bst16(ro, bo[q], Fmt<DT>::pack(y));  // dropped past the block's end
+        bst16s(ro, bo[q], Fmt<DT>::pack(y));  // dropped past the block's end
     }
 }
 
@@ -434,7 +434,7 @@ __device__ inline void load_chunks(const uint4* __restrict__ p, uint32_t nch, ui
     const int t = threadIdx.x;
 #pragma unroll
     for (int q = 0; q < CPT; ++q)
-        dst[q] = (q * NT + t < nch) ? p[q * NT + t] : make_uint4(0u, 0u, 0u, 0u);
+        dst[q] = (q * NT + t < nch) ? ld16s(&p[q * NT + t]) : make_uint4(0u, 0u, 0u, 0u);
 }
 
 // Whole workgroup: exact k-th largest magnitude pattern of slot j over all
@@ -759,7 +759,7 @@ __device__ inline void ties_store_small(const float (&P)[Fmt<DT>::V], const floa
         y[v] = fmaf(lambda, q, x0[v]);
     }
     if (ok)
-        *dst = Fmt<DT>::pack(y);
+        st16s(dst, Fmt<DT>::pack(y));
 }
 
 // Election and mean for any number of agreeing entries (counts packed:
@@ -796,7 +796,7 @@ __device__ inline void ties_store_chunk(const float (&P)[Fmt<DT>::V], const floa
 #pragma unroll
         for (int v = 0; v < V; ++v)
             y[v] = fmaf(lambda, num[v], x0[v]);
-        *dst = Fmt<DT>::pack(y);
+        st16s(dst, Fmt<DT>::pack(y));
     }
 }
 
@@ -825,7 +825,7 @@ __device__ inline void ties_finish_single(const float (&d)[ties::GS][ties::EPT],
                     }
                     y[v] = fmaf(lambda, mean, x0[q * V + v]);
                 }
-                po[q * ties::NT + t] = Fmt<DT>::pack(y);
+                st16s(&po[q * ties::NT + t], Fmt<DT>::pack(y));
             }
             continue;
         }
