@@ -44,17 +44,24 @@ TRAFFIC_PROFILES = {
     "catalog": os.path.join(ROOT, "profiles", "ties_threshold_merge_qwen2.5-1.5b_counters.md"),
     "in-merge": os.path.join(ROOT, "profiles", "ties_merge_qwen2.5-1.5b_counters.md"),
 }
-KERNEL_SOURCES = ("paper_2605_29489_amd/csrc/k_merge.hip", "paper_2605_29489_amd/csrc/device_common.h",
-                  "paper_2605_29489_amd/csrc/ties_select.h")
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+_CSRC = "paper_2605_29489_amd/csrc/"
+# the sources each route's merge kernel is built from: a committed counter
+# profile is used only while their hash matches the one it records
+KERNEL_SOURCES = {
+    "catalog": tuple(_CSRC + f for f in ("k_merge.hip", "merge_src.h", "device_common.h")),
+    "in-merge": tuple(_CSRC + f for f in ("k_merge_ties.hip", "merge_src.h", "device_common.h", "ties_select.h")),
+}
+
+
+def kernel_source_hash(route="catalog") -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in KERNEL_SOURCES[route]:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -103,7 +110,7 @@ def stored_traffic(route):
         if ":" in line and line.startswith("- "):
             k, v = line[2:].split(":", 1)
             kv[k.strip()] = v.strip().strip("`")
-    if kv.get("kernel_source_sha256_16") != kernel_source_hash():
+    if kv.get("kernel_source_sha256_16") != kernel_source_hash(route):
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])

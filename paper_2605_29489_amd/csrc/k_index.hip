@@ -189,7 +189,7 @@ __global__ __launch_bounds__(256, DT == 1 ? MP_CAT_WAVES : 3) void k_index_ties(
 }  // namespace
 
 // z with P(|Z| > z) = rho for a standard normal Z (bisection on erfc).
-static double normal_two_sided_quantile(double rho)
+double normal_two_sided_quantile(double rho)
 {
     if (!(rho > 0.0) || rho >= 1.0)
         return 0.0;

@@ -199,6 +199,18 @@ hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const v
                                const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s,
                                const void* stage, const uint64_t* soff, int64_t b0, int64_t nb);
 
+// z with P(|Z| > z) = rho for a standard normal Z (0 unless 0 < rho < 1);
+// scales the TIES kernels' first guess at a trim threshold (k_index.hip).
+double normal_two_sided_quantile(double rho);
+
+// The TIES merge that selects its trim thresholds itself (k_merge_ties.hip);
+// launch_merge and launch_merge_staged forward Op::TIES here.
+hipError_t launch_merge_ties(const BlockTable& bt, const MergeArgs& a, const void* base, const ExpertPtrs& ex, int K,
+                             const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s);
+hipError_t launch_merge_ties_staged(const BlockTable& bt, const MergeArgs& a, const void* base, int K,
+                                    const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s,
+                                    const void* stage, const uint64_t* soff, int64_t b0, int64_t nb);
+
 // ---------------------------------------------------------------- host experts (stage.hip)
 // Expert checkpoints on the host: memory (ptr[i]) or files (fd[i], read
 // with pread).  read() copies bytes [pos, pos + n) of expert i; a failed

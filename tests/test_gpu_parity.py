@@ -599,11 +599,12 @@ def test_ties_threshold_search_paths(mp):
 
 
 def test_ties_threshold_guess_above_tau(mp):
-    # The catalog's selector first counts only values above a guess taken
-    # from the deltas' RMS.  Bimodal deltas (a tenth near 1.0, the rest in
-    # [0.13, 0.2]) put that guess above the k-th largest at density 0.2
-    # while the k-th largest still lies in the window below the maximum: the
-    # full-window pass must find it.  A normal expert takes the first pass.
+    # Both TIES selectors (the catalog's and the one inside the merge) first
+    # count only values above a guess taken from the deltas' RMS.  Bimodal
+    # deltas (a tenth near 1.0, the rest in [0.13, 0.2]) put that guess above
+    # the k-th largest at density 0.2 while the k-th largest still lies in
+    # the window below the maximum: the rest of the window must be counted
+    # and the cut found there.  A normal expert takes the first pass.
     spec = _mini_qwen(n_layers=1, K=2)
     P = sum(int(np.prod(s)) for _, s in spec.tensors)
     rng = np.random.default_rng(19)
@@ -615,6 +616,7 @@ def test_ties_threshold_guess_above_tau(mp):
     for dens in (0.2, 0.12, 0.5):
         _say(f"case guess above tau density={dens}")
         _run_all(mp, spec, base, exps, "ties_tau", [1.0], density=dens, lam=1.0)
+        _run_all(mp, spec, base, exps, "ties", [0.5, 1.0], density=dens, lam=1.0)
 
 
 def test_ties_subnormal_deltas(mp):
