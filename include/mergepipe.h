@@ -345,6 +345,17 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
                         const void* const* adapters, int32_t K, const uint32_t* mask,
                         void* const* deltas, void* stream);
 
+/* Measurement aid, not part of the method: a plain stream copy of `bytes`
+ * bytes (a multiple of 16, at most 2^40) from device memory src to device
+ * memory dst, which must not overlap, with the merge kernels' access pattern
+ * (16-byte non-temporal loads and stores, one chunk per lane) and none of
+ * their arithmetic.  Timing it gives the HBM rate the device reaches on a
+ * read-once, write-once stream, the practical ceiling beside the published
+ * peak.  MP_E_ARG for a null, non-device or too small buffer, a size that is
+ * not a multiple of 16, or overlapping buffers; MP_E_HIP if the launch fails.
+ * Asynchronous on `stream`. */
+int mp_stream_copy(const void* src, void* dst, uint64_t bytes, void* stream);
+
 /* Staging for MP_HOST_PAGEABLE: the bytes of each of the two pinned host
  * buffers (and of their two device counterparts) that chunks of packed
  * expert blocks pass through; default 256 MiB, rounded down to 256 bytes.

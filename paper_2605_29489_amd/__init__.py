@@ -36,7 +36,7 @@ MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
            "mp_plan_noalloc", "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
            "mp_merge_ties",
-           "mp_merge_ties_tau", "mp_merge_dare", "mp_lora_materialize", "mp_set_stage_bytes",
+           "mp_merge_ties_tau", "mp_merge_dare", "mp_lora_materialize", "mp_stream_copy", "mp_set_stage_bytes",
            "mp_set_workspace_limit", "mp_workspace_bytes", "mp_last_error", "mp_release")
 
 
@@ -106,6 +106,7 @@ def _load():
     L.mp_lora_materialize.argtypes = [lp, C.POINTER(mp_lora_tensor), i32, C.POINTER(vp), i32, vp, C.POINTER(vp),
                                       vp]
     L.mp_last_error.restype = C.c_char_p
+    L.mp_stream_copy.argtypes = [vp, vp, u64, vp]
     L.mp_set_stage_bytes.argtypes = [u64]
     L.mp_set_stage_bytes.restype = i32
     L.mp_set_workspace_limit.argtypes = [u64]
@@ -118,7 +119,7 @@ def _load():
                  "mp_plan_noalloc", "mp_coverage", "mp_merge_avg",
                  "mp_merge_avg_renorm", "mp_merge_ties",
                  "mp_merge_ties_tau",
-                 "mp_merge_dare", "mp_lora_materialize"):
+                 "mp_merge_dare", "mp_lora_materialize", "mp_stream_copy"):
         getattr(L, name).restype = C.c_int
     return L
 
@@ -317,6 +318,15 @@ def mp_lora_materialize(layout: Layout, loras, adapters, deltas, mask=None, stre
 
 def mp_last_error() -> str:
     return lib.mp_last_error().decode()
+
+
+def mp_stream_copy(src, dst, stream=None):
+    """Plain stream copy of src's bytes into dst (device tensors of equal
+    byte size, a multiple of 16): a measurement aid for the HBM rate."""
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != n:
+        raise ValueError("src and dst differ in size")
+    _check(lib.mp_stream_copy(_ptr(src), _ptr(dst), n, _stream(stream)))
 
 
 def mp_set_stage_bytes(nbytes: int):

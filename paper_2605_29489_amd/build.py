@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmergepipe.so")
 OBJ = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "k_index.hip", "k_plan.hip", "k_merge.hip", "k_merge_ties.hip", "k_tensor_ties.hip", "k_lora.hip", "stage.hip"]
+SOURCES = ["api.hip", "k_index.hip", "k_plan.hip", "k_merge.hip", "k_merge_ties.hip", "k_tensor_ties.hip", "k_lora.hip", "k_copy.hip", "stage.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

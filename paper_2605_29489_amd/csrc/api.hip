@@ -1227,6 +1227,27 @@ uint64_t mp_workspace_bytes(void)
     return g_ws_held;
 }
 
+int mp_stream_copy(const void* src, void* dst, uint64_t bytes, void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    if (bytes % 16 != 0)
+        return fail(MP_E_ARG, "bytes = %llu must be a multiple of 16", (unsigned long long)bytes);
+    if (bytes > (uint64_t(1) << 40))
+        return fail(MP_E_ARG, "bytes = %llu exceeds 2^40", (unsigned long long)bytes);
+    int rc;
+    if ((rc = check_device_buffer(src, (size_t)bytes, "src")) || (rc = check_device_buffer(dst, (size_t)bytes, "dst")))
+        return rc;
+    const char* a = static_cast<const char*>(src);
+    const char* b = static_cast<const char*>(dst);
+    if (bytes != 0 && a < b + bytes && b < a + bytes)
+        return fail(MP_E_ARG, "src and dst overlap");
+    hipError_t e = launch_stream_copy(src, dst, bytes, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return hip_fail(e, "stream copy launch");
+    return MP_OK;
+}
+
 int mp_set_stage_bytes(uint64_t bytes)
 {
     std::lock_guard<std::mutex> lock(g_mu);

@@ -59,6 +59,26 @@ constexpr int GS = 4;                    // experts trimmed together (one scanni
 constexpr uint32_t RETRY = 4u;           // state: the cut lies below the first pass's floor
 }  // namespace ties
 
+// Sum over the 64 lanes of a wave, returned wave-uniform: the butterfly of
+// wave_max_u32 (quad permutes, row mirrors, row broadcasts) with adds.  The
+// order of the adds differs from a sequential sum; the result only guides
+// the threshold guess.
+template <int CTRL, int ROW_MASK, int BANK_MASK, bool BOUND_CTRL>
+__device__ inline float dpp_f32(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, BANK_MASK, BOUND_CTRL));
+}
+__device__ inline float wave_sum_f32(float v)
+{
+    v = v + dpp_f32<0xb1, 0xf, 0xf, true>(v);    // quad_perm [1,0,3,2]
+    v = v + dpp_f32<0x4e, 0xf, 0xf, true>(v);    // quad_perm [2,3,0,1]
+    v = v + dpp_f32<0x141, 0xf, 0xf, true>(v);   // row_half_mirror
+    v = v + dpp_f32<0x140, 0xf, 0xf, true>(v);   // row_mirror
+    v = v + dpp_f32<0x142, 0xa, 0xf, false>(v);  // row_bcast:15
+    v = v + dpp_f32<0x143, 0xc, 0xf, false>(v);  // row_bcast:31
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
 // The window histogram's update for the values with lo <= |d| < hi
 // (magnitude patterns): the part of the window below a first pass's floor.
 __device__ inline void window_add_range(char* base, uint32_t bits, uint32_t lo, uint32_t hi, uint32_t koff)
@@ -188,9 +208,7 @@ __device__ inline void ties_deltas(TiesSmem& sm, const uint4 (&raw)[ties::GS][CP
                     mx = fmaxf(mx, fmaxf(fabsf(d[j][q * V + v]), fabsf(d[j][q * V + v + 1])));
             }
             const uint32_t w = wave_max_u32(__float_as_uint(mx));
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1)
-                ss = ss + __shfl_xor(ss, o);
+            ss = wave_sum_f32(ss);
             if (lane == 0) {
                 sm.wmax[j][wave] = w;
                 sm.wss[j][wave] = ss;

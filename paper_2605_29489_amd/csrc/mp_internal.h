@@ -199,6 +199,10 @@ hipError_t launch_merge_staged(const BlockTable& bt, const MergeArgs& a, const v
                                const uint32_t* mask, void* out, unsigned long long* counters, hipStream_t s,
                                const void* stage, const uint64_t* soff, int64_t b0, int64_t nb);
 
+// Stream copy of nbytes (a multiple of 16, at most 2^40) of device
+// memory (k_copy.hip).
+hipError_t launch_stream_copy(const void* src, void* dst, uint64_t nbytes, hipStream_t s);
+
 // z with P(|Z| > z) = rho for a standard normal Z (0 unless 0 < rho < 1);
 // scales the TIES kernels' first guess at a trim threshold (k_index.hip).
 double normal_two_sided_quantile(double rho);

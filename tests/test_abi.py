@@ -138,6 +138,10 @@ def test_argument_errors_before_any_device_call(mp):
     assert lib.mp_merge_avg(L.ref, None, ptrs, 1, 0, None, an, None, None, None) == mp.MP_E_ARG
     assert lib.mp_merge_avg_renorm(L.ref, None, ptrs, 1, 0, None, None, None, None, None) == mp.MP_E_ARG
     assert lib.mp_merge_avg_renorm(L.ref, None, ptrs, 1, 0, None, an, None, None, None) == mp.MP_E_ARG
+    # stream copy: sizes that are not a multiple of 16, or beyond 2^40
+    assert lib.mp_stream_copy(None, None, 17, None) == mp.MP_E_ARG
+    assert "multiple of 16" in mp.mp_last_error()
+    assert lib.mp_stream_copy(None, None, 1 << 41, None) == mp.MP_E_ARG
     # unit ids must fit 32 bits: 2^28 blocks x 32 experts
     big = mp.Layout([4096 * (1 << 28)], 4096, mp.MP_BF16)
     assert lib.mp_index_blocks(big.ref, None, ptrs, 32, 0, None, None) == mp.MP_E_ARG

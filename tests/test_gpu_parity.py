@@ -987,3 +987,23 @@ def test_invalid_device_arguments_rejected(mp):
         torch.cuda.synchronize()
         for b in (small_out, small_mask, small_sumsq):
             b.free()
+
+
+def test_stream_copy(mp):
+    # the measurement aid copies every byte, ragged sizes included, writes
+    # nothing past the end, and refuses overlapping or non-device buffers
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(5)
+    for n in (16, 1008, 1024, 1040, (1 << 20) + 48, 3 * (1 << 24) + 16):
+        src = torch.randint(-2**31, 2**31 - 1, (n // 4,), dtype=torch.int32, device="cuda", generator=g)
+        dst = torch.full((n // 4 + 64,), -1, dtype=torch.int32, device="cuda")
+        mp.mp_stream_copy(src, dst[:n // 4])
+        torch.cuda.synchronize()
+        assert torch.equal(src, dst[:n // 4]), n
+        assert bool((dst[n // 4:] == -1).all()), n
+    buf = torch.zeros(4096, dtype=torch.int32, device="cuda")
+    with pytest.raises(mp.MPError):
+        mp._check(mp.lib.mp_stream_copy(mp._ptr(buf), mp._ptr(buf[16:]), 4096, None))
+    host = torch.zeros(4096, dtype=torch.int32)  # ordinary host memory: not a device buffer
+    with pytest.raises(mp.MPError):
+        mp._check(mp.lib.mp_stream_copy(mp._ptr(buf), host.data_ptr(), 4096, None))
