@@ -128,28 +128,51 @@ __global__ __launch_bounds__(256, DT == 1 ? 4 : 2) void k_lora_band(const LoraDe
             }
         }
     };
+    // The lane's column groups of a tile: c0 + 16 ct (ct < kCT), c0 = n0 + cg.
+    // Element row * cols + c0 lies in block lb of the tensor, lr elements in;
+    // tiles are selected in order, so (lb, lr) advances by kTN elements per
+    // tile instead of being divided out again.  With blocks of at least 116
+    // elements the lane's groups (within 116 elements) lie in block lb or
+    // lb + 1; shorter blocks take the division per group.
+    const bool two = block_elems >= 116u;
+    uint32_t lb = 0u, lr = 0u;
+    if (row < rows && two) {
+        const uint32_t e = row * cols + cg;  // < numel < 2^32
+        lb = e / block_elems;
+        lr = e - lb * block_elems;
+    }
     auto selection = [&](uint32_t n0) {
         uint32_t sel = 0u;
         const uint32_t c0 = n0 + cg;
         if (row < rows && c0 < cols) {
-            // the lane's groups lie in one row, within 116 columns: at most two
-            // blocks when blocks are at least that long (one or two mask words)
-            const uint32_t last = min(n0 + (kCT - 1) * 16 + cg, (cols - 1) & ~3u);
-            const uint32_t e0 = row * cols + c0;  // < numel < 2^32
-            const uint32_t b0 = e0 / block_elems, b1 = (row * cols + last) / block_elems;
-            const bool two = block_elems >= 116u;
-            const uint32_t w0 = mask != nullptr && two ? mask[D.g0 + b0] : 0u;
-            const uint32_t w1 = mask != nullptr && two && b1 != b0 ? mask[D.g0 + b1] : w0;
+            if (mask == nullptr) {
 #pragma unroll
-            for (int ct = 0; ct < kCT; ++ct) {
-                const uint32_t col = c0 + ct * 16;
-                if (col < cols) {
-                    const uint32_t b = (row * cols + col) / block_elems;
-                    const uint32_t w = mask == nullptr ? 0xffffffffu
-                                       : two          ? (b == b0 ? w0 : w1)
-                                                      : mask[D.g0 + b];
-                    sel |= ((w >> i) & 1u) << ct;
+                for (int ct = 0; ct < kCT; ++ct)
+                    sel |= (c0 + ct * 16 < cols ? 1u : 0u) << ct;
+            } else if (two) {
+                // the lane's last group; a second mask word only if it crosses
+                const uint32_t span = min((uint32_t)((kCT - 1) * 16), ((cols - 1) & ~3u) - c0);
+                const uint32_t w0 = mask[D.g0 + lb];
+                const uint32_t w1 = (lr + span >= block_elems) ? mask[D.g0 + lb + 1] : w0;
+#pragma unroll
+                for (int ct = 0; ct < kCT; ++ct) {
+                    const uint32_t w = (lr + ct * 16 >= block_elems) ? w1 : w0;
+                    sel |= (c0 + ct * 16 < cols ? ((w >> i) & 1u) : 0u) << ct;
                 }
+            } else {
+#pragma unroll
+                for (int ct = 0; ct < kCT; ++ct) {
+                    const uint32_t col = c0 + ct * 16;
+                    if (col < cols)
+                        sel |= ((mask[D.g0 + (row * cols + col) / block_elems] >> i) & 1u) << ct;
+                }
+            }
+        }
+        if (two) {  // the next tile's first group
+            lr += kTN;
+            while (lr >= block_elems) {
+                lr -= block_elems;
+                ++lb;
             }
         }
         return sel;
