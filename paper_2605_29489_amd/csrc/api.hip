@@ -93,6 +93,10 @@ void free_lora(LoraEntry& e)
     (void)hipSetDevice(e.device);
     (void)ws_free_r(e.t.d_desc);
     (void)ws_free_r(e.t.d_zero);
+    (void)ws_free_r(e.t.d_rl);
+    (void)ws_free_r(e.t.d_rc);
+    if (e.t.ev != nullptr)
+        (void)hipEventDestroy(e.t.ev);
     (void)hipSetDevice(cur);
 }
 
@@ -1118,7 +1122,12 @@ static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lor
         desc.push_back(d);
     }
     std::sort(desc.begin(), desc.end(), [](const LoraDesc& a, const LoraDesc& b) { return a.toff < b.toff; });
+    uint64_t rows_total = 0;
     for (LoraDesc& d : desc) {
+        d.r0 = (uint32_t)rows_total;
+        rows_total += d.rows;
+        if (rows_total >= ((uint64_t)1 << 31))
+            return fail(MP_E_UNSUPPORTED, "adapted tensors hold 2^31 or more rows");
         d.tile0 = (uint32_t)tiles;
         tiles += lora_bands(d.rows, d.cols, &d.tiles_n);
         if (tiles >= ((uint64_t)1 << 31))
@@ -1133,6 +1142,7 @@ static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lor
                 zero.push_back((uint32_t)g);
     e->t.n_desc = (int)desc.size();
     e->t.n_tiles = (uint32_t)tiles;
+    e->t.rows_total = (uint32_t)rows_total;
     e->t.n_zero = (uint32_t)zero.size();
     hipError_t he = hipSuccess;
     if ((!desc.empty() && ((he = ws_malloc((void**)&e->t.d_desc, sizeof(LoraDesc) * desc.size())) != hipSuccess ||
@@ -1205,7 +1215,34 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
                 return fail(MP_E_ARG, "a delta buffer overlaps %s", r.name);
     if (mask != nullptr && (rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)G, "mask")))
         return rc;
-    hipError_t e = launch_lora(*bt, *lt, ad, dl, K, mask, static_cast<hipStream_t>(stream));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    const bool listed = mask != nullptr && lt->n_tiles > 0;
+    if (listed) {
+        // the row lists of a masked pull; calls with the same layout and
+        // records share them, so each call's stream first waits for the
+        // previous masked pull's kernels (on any stream)
+        if (lt->ev == nullptr && (e = hipEventCreateWithFlags(&lt->ev, hipEventDisableTiming)) != hipSuccess)
+            return hip_fail(e, "hipEventCreateWithFlags");
+        if (lt->rl_k < K) {
+            if (lt->d_rl != nullptr && (e = hipEventSynchronize(lt->ev)) != hipSuccess)  // its last reader is done
+                return hip_fail(e, "hipEventSynchronize");
+            (void)ws_free_r(lt->d_rl);
+            (void)ws_free_r(lt->d_rc);
+            lt->d_rl = nullptr;
+            lt->d_rc = nullptr;
+            lt->rl_k = 0;
+            if ((e = ws_malloc((void**)&lt->d_rl, sizeof(uint32_t) * (size_t)K * lt->rows_total)) != hipSuccess ||
+                (e = ws_malloc((void**)&lt->d_rc, sizeof(uint32_t) * (size_t)K * (size_t)lt->n_desc)) != hipSuccess)
+                return hip_fail(e, "adapter row lists");
+            lt->rl_k = K;
+        }
+        if ((e = hipStreamWaitEvent(s, lt->ev, 0)) != hipSuccess)
+            return hip_fail(e, "hipStreamWaitEvent");
+    }
+    e = launch_lora(*bt, *lt, ad, dl, K, mask, s);
+    if (e == hipSuccess && listed)
+        e = hipEventRecord(lt->ev, s);
     if (e != hipSuccess)
         return hip_fail(e, "adapter delta launch");
     return MP_OK;

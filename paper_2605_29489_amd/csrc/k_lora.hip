@@ -19,6 +19,12 @@
 // zero-padded to the MFMA depth (16 for bf16, 4 for fp32).  Column tiles
 // with no selected element are neither loaded nor computed.
 //
+// A masked pull computes only the rows that hold a selected element:
+// k_lora_rows lists, per tensor and expert, the rows that meet a selected
+// block, and the bands then take 64 listed rows each (bands past the list's
+// end return at once).  Selected blocks are spread over a tensor's rows, so
+// at a low budget most rows are skipped whole.
+//
 // Blocks of tensors without an adapter get zeros (k_lora_zero).
 #include <type_traits>
 
@@ -59,10 +65,53 @@ __device__ inline void lds_barrier()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// The rows of each adapted tensor that meet a selected block of expert i
+// (blockIdx.y): workgroup d lists tensor d's in increasing order at
+// rl[i * rows_total + r0 ..] and their count at rc[i * n_desc + d].
+__global__ __launch_bounds__(256) void k_lora_rows(const LoraDesc* __restrict__ desc, int n_desc,
+                                                   const uint32_t* __restrict__ mask, uint32_t block_elems,
+                                                   uint32_t* __restrict__ rl, uint32_t* __restrict__ rc,
+                                                   uint32_t rows_total)
+{
+    __shared__ uint32_t wcount[4];
+    const int d = blockIdx.x, i = blockIdx.y;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const LoraDesc D = desc[d];
+    uint32_t* out = rl + (uint64_t)i * rows_total + D.r0;
+    uint32_t total = 0u;
+    for (uint32_t r0 = 0; r0 < D.rows; r0 += 256) {
+        const uint32_t r = r0 + (uint32_t)t;
+        bool need = false;
+        if (r < D.rows) {
+            const uint32_t b0 = r * D.cols / block_elems;  // < numel < 2^32
+            const uint32_t b1 = (r * D.cols + D.cols - 1) / block_elems;
+            for (uint32_t b = b0; b <= b1 && !need; ++b)
+                need = ((mask[D.g0 + b] >> i) & 1u) != 0u;
+        }
+        const unsigned long long bal = __ballot(need);
+        if (lane == 0)
+            wcount[wave] = (uint32_t)__popcll(bal);
+        __syncthreads();
+        uint32_t before = total;
+        for (int w = 0; w < wave; ++w)
+            before += wcount[w];
+        const uint32_t pos =
+            __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, before));
+        if (need)
+            out[pos] = r;
+        total += wcount[0] + wcount[1] + wcount[2] + wcount[3];
+        __syncthreads();  // wcount is rewritten by the next chunk
+    }
+    if (t == 0)
+        rc[(uint64_t)i * n_desc + d] = total;
+}
+
 template <int DT>
 __global__ __launch_bounds__(256, DT == 1 ? 4 : 2) void k_lora_band(const LoraDesc* __restrict__ desc, int n_desc,
                                                    ExpertPtrs ad, OutPtrs dl, const uint32_t* __restrict__ mask,
-                                                   uint32_t block_elems, int aligned)
+                                                   uint32_t block_elems, int aligned,
+                                                   const uint32_t* __restrict__ rl, const uint32_t* __restrict__ rc,
+                                                   uint32_t rows_total)
 {
     using E = typename std::conditional<DT == 0, float, uint16_t>::type;
     constexpr int KS = DT == 0 ? 4 : 16;    // MFMA depth
@@ -70,28 +119,40 @@ __global__ __launch_bounds__(256, DT == 1 ? 4 : 2) void k_lora_band(const LoraDe
     constexpr int RS = kMaxLoraRank + 4;    // LDS row stride in elements (breaks bank aliasing, keeps 8 B alignment)
     constexpr int APT = kMaxLoraRank * kTN / CV / 256;  // A chunks per thread at the largest rank
     __shared__ __align__(16) E As[kTN * RS];  // As[n * RS + k] = A[k][n0 + n]
-    __shared__ __align__(16) E Bs[kTM * RS];  // Bs[m * RS + k] = B[m0 + m][k]
+    __shared__ __align__(16) E Bs[kTM * RS];  // Bs[m * RS + k] = B[rix[m]][k]
     constexpr int OS = kTN / 2 + 8;  // bf16 output strip row stride (16-byte aligned rows)
     __shared__ __align__(16) uint16_t Os[DT == 1 ? kTM * OS : 8];  // vector reads and writes
     __shared__ uint32_t flags[2][4];
+    __shared__ uint32_t rix[kTM];  // the band's rows (rows: none)
     const int i = blockIdx.y;
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
     const int d = __builtin_amdgcn_readfirstlane(find_desc(desc, n_desc, blockIdx.x));
     const LoraDesc D = desc[d];
-    const uint32_t m0 = (blockIdx.x - D.tile0) * kTM;
+    const uint32_t m0 = (blockIdx.x - D.tile0) * kTM;  // the band's first (listed) row
     const uint32_t rows = D.rows, cols = D.cols, rank = D.rank;
     const uint32_t rp = (rank + KS - 1) / KS * KS;
-    const uint32_t row = m0 + wave * 16 + (lane & 15);
+    // a masked pull walks the listed rows; a full pull every row
+    const uint32_t nrow = mask != nullptr ? rc[(uint64_t)i * n_desc + d] : rows;
+    if (m0 >= nrow)
+        return;  // past the list's end (workgroup-uniform, before any barrier)
+    if (t < kTM) {
+        // the list holds rows in increasing order, so a full list is the identity
+        const uint32_t j = m0 + (uint32_t)t;
+        rix[t] = (j >= nrow) ? rows : (nrow != rows ? rl[(uint64_t)i * rows_total + D.r0 + j] : j);
+    }
+    __syncthreads();
+    const uint32_t row = rix[wave * 16 + (lane & 15)];
     const uint32_t cg = 4u * (uint32_t)(lane >> 4);  // the lane's first column inside each 16-column tile
     const E* __restrict__ A = static_cast<const E*>(ad.p[i]) + D.a_off;
     const E* __restrict__ B = static_cast<const E*>(ad.p[i]) + D.b_off;
     E* __restrict__ out = static_cast<E*>(dl.p[i]) + D.toff;
     const bool vec = D.vec != 0u && aligned != 0;  // A's rows are 16-byte aligned: chunked loads
     // the band's B rows, once
-    for (uint32_t x = t; x < rp * kTM; x += 256) {  // B's rows m0.. are contiguous
+    for (uint32_t x = t; x < rp * kTM; x += 256) {
         const uint32_t m = x / rp, k = x % rp;
-        Bs[m * RS + k] = (k < rank && m0 + m < rows) ? B[(uint64_t)(m0 + m) * rank + k] : E(0);
+        const uint32_t rm = rix[m];
+        Bs[m * RS + k] = (k < rank && rm < rows) ? B[(uint64_t)rm * rank + k] : E(0);
     }
     // A chunk c of a column tile: depth k = c / (kTN / CV), columns n = (c % (kTN / CV)) * CV ..
     auto load_a = [&](uint32_t n0, uint4 (&ra)[APT]) {
@@ -272,7 +333,7 @@ __global__ __launch_bounds__(256, DT == 1 ? 4 : 2) void k_lora_band(const LoraDe
                             // never straddles a block or the row end)
                             const uint32_t so = (uint32_t)__shfl((int)sel, r + 16 * ((cc & 15) >> 2));
                             if ((so >> (h * (kCT / 2) + (cc >> 4))) & 1u) {
-                                const uint32_t e = (m0 + wave * 16 + r) * cols + n0 + h * 64 + cc;
+                                const uint32_t e = rix[wave * 16 + r] * cols + n0 + h * 64 + cc;
                                 *reinterpret_cast<uint4*>(out + e) = *reinterpret_cast<const uint4*>(&ow[r * OS + cc]);
                             }
                         }
@@ -326,12 +387,15 @@ hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPt
         for (int i = 0; i < K; ++i)
             if (reinterpret_cast<uintptr_t>(ad.p[i]) % 16 != 0)
                 aligned = 0;
+        if (mask != nullptr)
+            hipLaunchKernelGGL(k_lora_rows, dim3((unsigned)lt.n_desc, (unsigned)K), dim3(256), 0, s, lt.d_desc,
+                               lt.n_desc, mask, be, lt.d_rl, lt.d_rc, lt.rows_total);
         if (bt.dtype == 0)
             hipLaunchKernelGGL(k_lora_band<0>, grid, dim3(256), 0, s, lt.d_desc, lt.n_desc, ad, dl, mask, be,
-                               aligned);
+                               aligned, lt.d_rl, lt.d_rc, lt.rows_total);
         else
             hipLaunchKernelGGL(k_lora_band<1>, grid, dim3(256), 0, s, lt.d_desc, lt.n_desc, ad, dl, mask, be,
-                               aligned);
+                               aligned, lt.d_rl, lt.d_rc, lt.rows_total);
     }
     if (lt.n_zero > 0)
         hipLaunchKernelGGL(k_lora_zero, dim3((unsigned)lt.n_zero, (unsigned)K), dim3(256), 0, s, lt.d_zero,

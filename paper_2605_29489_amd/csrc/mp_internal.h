@@ -154,6 +154,7 @@ struct LoraDesc {
     uint32_t tiles_n;  // 128-column tiles per band
     uint32_t tile0;
     uint32_t vec;  // every row of A starts 16-byte aligned (relative to the adapter buffer)
+    uint32_t r0;   // the tensor's first entry in a row list (rows of the earlier tensors)
 };
 
 // A validated set of adapter records for a layout, cached per device.
@@ -163,12 +164,18 @@ struct LoraTable {
     uint32_t n_tiles = 0;  // row bands (workgroups per expert)
     uint32_t* d_zero = nullptr;  // blocks of tensors without an adapter
     uint32_t n_zero = 0;
+    uint32_t rows_total = 0;     // rows of all adapted tensors
+    uint32_t* d_rl = nullptr;    // masked pulls: the listed rows, K x rows_total (grown on demand)
+    uint32_t* d_rc = nullptr;    //   and their counts, K x n_desc
+    int rl_k = 0;                // experts the two arrays hold
+    hipEvent_t ev = nullptr;     // recorded after each masked pull: the next one (any stream) waits for it
 };
 
 // Row bands of a rows x cols tensor; *tiles_n receives the column tiles per band.
 uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n);
 
-// Writes the selected units' deltas (all units when mask is null).
+// Writes the selected units' deltas (all units when mask is null).  A masked
+// pull needs lt.d_rl and lt.d_rc for at least K experts.
 hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& dl, int K,
                        const uint32_t* mask, hipStream_t s);
 
