@@ -340,7 +340,10 @@ typedef struct mp_lora_tensor {
  * MP_E_UNSUPPORTED for tensors of 2^32 or more elements; MP_E_NOMEM or
  * MP_E_HIP from the table upload or the launch.  Records are validated and
  * their device table is cached per (device, layout, records) until
- * mp_release.  Asynchronous on `stream`. */
+ * mp_release; with a mask the call also fills that table's row lists (the
+ * rows meeting a selected block), so a masked call's stream first waits for
+ * the previous masked call with the same layout and records, on whatever
+ * stream it ran.  Asynchronous on `stream`. */
 int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, int32_t n_lora,
                         const void* const* adapters, int32_t K, const uint32_t* mask,
                         void* const* deltas, void* stream);
