@@ -282,10 +282,11 @@ def cpu_baseline_lora(spec, recs, ads_np, base, cfg, n_layers=5):
     t0 = time.perf_counter()
     d_all = oracle.lora_materialize(sub, lay.dtype, numel, sub_recs, ads_np)
     S = oracle.index(sub, lay.dtype, b_np, d_all, delta=True).reshape(-1)
+    tau = oracle.ties_thresholds(sub, lay.dtype, b_np, d_all, cfg["density"], delta=True)
     for f in cfg["budgets"]:
         mask, _ = oracle.plan(sub, lay.dtype, K, S, [1.0] * K, int(f * full), flags=2)
         d = oracle.lora_materialize(sub, lay.dtype, numel, sub_recs, ads_np, mask=mask)
-        oracle.merge_ties(sub, lay.dtype, b_np, d, mask, cfg["density"], cfg["lam"], delta=True)
+        oracle.merge_ties_tau(sub, lay.dtype, b_np, d, mask, tau, cfg["lam"], delta=True)
     dt = time.perf_counter() - t0
     return {
         "value": len(cfg["budgets"]) * nparams / dt,
@@ -294,16 +295,17 @@ def cpu_baseline_lora(spec, recs, ads_np, base, cfg, n_layers=5):
         "kind": "oracle",
         "sample": f"the {len(pick)} adapted tensors of layers 0-{n_layers - 1} ({nparams} params, all {K} experts): "
                   f"pull of every unit + "
-                  f"index + per budget (B=25/50/100% of the sample's expert bytes) plan, pull of the selected "
-                  f"units and TIES; {dt:.2f} s",
+                  f"index and thresholds + per budget (B=25/50/100% of the sample's expert bytes) plan, pull of "
+                  f"the selected units and TIES from the thresholds; {dt:.2f} s",
     }
 
 
 def run_lora(args):
     """Experts given as low-rank adapters: the catalog materialises every
-    expert's deltas once and indexes them; each budget then plans, pulls only
-    the selected units' deltas from the adapters (matrix-core contraction) and
-    merges them as explicit deltas."""
+    expert's deltas once and indexes them (sums of squares and every unit's
+    TIES trim threshold); each budget then plans, pulls only the selected
+    units' deltas from the adapters (matrix-core contraction) and merges them
+    as explicit deltas with the stored thresholds."""
     import numpy as np
     import torch
 
@@ -354,7 +356,11 @@ def run_lora(args):
         return float(np.median([timed(fn)[0] for _ in range(max(1, args.steps))]))
 
     pull_all_ms = med(lambda: mp.mp_lora_materialize(L, recs, ads, deltas, stream=stream))
-    idx_ms = med(lambda: mp.mp_index_blocks(L, base, deltas, sumsq, stream=stream, delta=True))
+    # the catalog of the pulled deltas: sums of squares and every unit's TIES
+    # trim threshold (the headline's route: thresholds depend on the unit only)
+    tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
+    idx_ms = med(lambda: mp.mp_index_ties(L, base, deltas, cfg["density"], tau, sumsq=sumsq, stream=stream,
+                                          delta=True))
     flags = mp.MP_PLAN_SKIP_ZERO  # tensors without an adapter have zero deltas: never worth a read
     mp.mp_plan(L, K, sumsq, w, full, mask, flags=flags, stream=stream)
     rows = []
@@ -362,7 +368,7 @@ def run_lora(args):
         B = int(f * full)
         plan_ms, st = timed(lambda: mp.mp_plan(L, K, sumsq, w, B, mask, flags=flags, stream=stream))
         pull_ms = med(lambda: mp.mp_lora_materialize(L, recs, ads, deltas, mask=mask, stream=stream))
-        merge = lambda io=False: mp.mp_merge_ties(L, base, deltas, mask, cfg["density"], cfg["lam"], out, io=io,
+        merge = lambda io=False: mp.mp_merge_ties_tau(L, base, deltas, mask, tau, cfg["lam"], out, io=io,
                                                   stream=stream, delta=True)
         io = merge(io=True)
         assert io["expert_bytes"] == st["cost_bytes"]
@@ -371,7 +377,8 @@ def run_lora(args):
                      "n_selected": st["n_selected"], "plan_ms": round(plan_ms, 4), "pull_ms": round(pull_ms, 4),
                      "merge_ms": round(ms, 4),
                      "pull_effective_GBps": (st["cost_bytes"] + K * n_ad * es) / (pull_ms * 1e-3) / 1e9,
-                     "merge_effective_GBps": (2 * P * es + st["cost_bytes"] + 4 * G) / (ms * 1e-3) / 1e9})
+                     "merge_effective_GBps": (2 * P * es + st["cost_bytes"] + 4 * G + 4 * st["n_selected"])
+                     / (ms * 1e-3) / 1e9})
     step_ms = pull_all_ms + idx_ms + sum(r["plan_ms"] + r["pull_ms"] + r["merge_ms"] for r in rows)
     if args.calibration_copy:  # an empty-mask AVG launch copies the base: a copy of known size for byte counters
         mask.zero_()
