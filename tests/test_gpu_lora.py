@@ -103,6 +103,49 @@ def test_lora_materialize_exact_grid_bitwise(mp, dtype, rank):
             assert np.array_equal(got, want[i]), f"expert {i}: {int((got != want[i]).sum())} elements differ"
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_lora_masked_pull_row_lists(mp, dtype):
+    # Masked pulls compute only the rows that meet a selected block: sparse
+    # masks (most rows of most tensors unlisted), a mask selecting every
+    # block (every list full: read as the identity), and two masked pulls
+    # with one layout and record set issued on two streams without a
+    # synchronisation between them (they share the cached row lists).
+    import torch
+    spec = _awkward(dtype)
+    lay = spec.layout
+    recs, n = lora_records(spec, 16, 0.5, targets=("w0", "w1", "w2", "w3", "w4", "w5"))
+    ads = make_lora_adapters(n, 3, dtype, seed=41, grid=True)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    rng = np.random.default_rng(41)
+    fill = [_sentinel(lay.n_params, dtype, i) for i in range(3)]
+    sparse = np.where(rng.random((blocks.G, 3)) < 0.05, 1, 0).astype(np.uint32)
+    sparse = (sparse << np.arange(3, dtype=np.uint32)).sum(1).astype(np.uint32)
+    full = np.full(blocks.G, 7, np.uint32)
+    for name, mask in (("sparse", sparse), ("full", full)):
+        _say(f"case lora row lists {dtype} {name}")
+        _, outs = _materialize(mp, spec, recs, ads, mask)
+        want = oracle.lora_materialize(blocks, dtype, lay.numel, recs, ads, mask=mask, fill=fill)
+        for i in range(3):
+            got = to_host(outs[i])
+            assert np.array_equal(got, want[i]), f"{name} expert {i}: {int((got != want[i]).sum())} differ"
+    _say(f"case lora row lists {dtype} two streams")
+    L = mp.Layout(lay.numel, lay.block_elems, lay.dtype_code)
+    ads_d = [to_dev(a, dtype) for a in ads]
+    masks = [sparse, rng.integers(0, 8, blocks.G).astype(np.uint32)]
+    outs = [[to_dev(_sentinel(lay.n_params, dtype, i), dtype) for i in range(3)] for _ in masks]
+    mdev = [torch.from_numpy(m.view(np.int32)).cuda() for m in masks]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for o, m, st in zip(outs, mdev, streams):
+        mp.mp_lora_materialize(L, recs, ads_d, o, mask=m, stream=st)
+    torch.cuda.synchronize()
+    for o, m in zip(outs, masks):
+        want = oracle.lora_materialize(blocks, dtype, lay.numel, recs, ads, mask=m, fill=fill)
+        for i in range(3):
+            got = to_host(o[i])
+            assert np.array_equal(got, want[i]), f"two streams expert {i}: {int((got != want[i]).sum())} differ"
+
+
 @pytest.mark.parametrize("rank", [8, 16, 64])
 def test_lora_materialize_exact_grid_bitwise_aligned_rows(mp, rank):
     # bf16 with every row of A 16-byte aligned: the 16-byte loads of A
