@@ -348,6 +348,27 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
                         const void* const* adapters, int32_t K, const uint32_t* mask,
                         void* const* deltas, void* stream);
 
+/* Budgeted TIES from catalog thresholds with the experts given as adapters
+ * (Section 3's delta iterator feeding the executor, Algorithm 2 with the
+ * merge operator of Appendix A.1): the result of mp_lora_materialize(mask)
+ * followed by mp_merge_ties_tau(MP_DEVICE | MP_EXPERTS_DELTA, mask, tau,
+ * lambda) on those deltas, bit for bit wherever the base is finite (the
+ * explicit-delta merge forms x - 0 * x0, which is NaN where x0 is not), but
+ * with no delta checkpoint: each selected unit's deltas are computed by the
+ * same matrix-core tiles, rounded to the dtype as the pull stores them, and
+ * trimmed, elected and averaged in registers.  Writes every element of out.
+ * base, out: device checkpoints (layout order and dtype); out must not
+ * overlap base, an adapter, mask or tau.  adapters, loras, n_lora and K as
+ * for mp_lora_materialize; mask: device uint32[G]; tau: device uint32[G*K]
+ * (from mp_index_ties on the deltas, or mp_ties_tensor_thresholds).
+ * MP_E_UNSUPPORTED when an adapted bf16 tensor's columns are not a multiple
+ * of 8 (then use the two calls); MP_E_ARG as for the two calls, or for a
+ * non-finite lambda.  Asynchronous on `stream`. */
+int mp_lora_merge_ties_tau(const mp_layout* layout, const void* base, const mp_lora_tensor* loras,
+                           int32_t n_lora, const void* const* adapters, int32_t K,
+                           const uint32_t* mask, const uint32_t* tau, float lambda, void* out,
+                           void* stream);
+
 /* Measurement aid, not part of the method: a plain stream copy of `bytes`
  * bytes (a multiple of 16, at most 2^40) from device memory src to device
  * memory dst, which must not overlap, with the merge kernels' access pattern

@@ -36,7 +36,8 @@ MP_PLAN_PER_BYTE, MP_PLAN_SKIP_ZERO = 1, 2
 EXPORTS = ("mp_layout_blocks", "mp_index_blocks", "mp_index_ties", "mp_ties_tensor_thresholds", "mp_plan",
            "mp_plan_noalloc", "mp_coverage", "mp_merge_avg", "mp_merge_avg_renorm",
            "mp_merge_ties",
-           "mp_merge_ties_tau", "mp_merge_dare", "mp_lora_materialize", "mp_stream_copy", "mp_set_stage_bytes",
+           "mp_merge_ties_tau", "mp_merge_dare", "mp_lora_materialize", "mp_lora_merge_ties_tau", "mp_stream_copy",
+           "mp_set_stage_bytes",
            "mp_set_workspace_limit", "mp_workspace_bytes", "mp_last_error", "mp_release")
 
 
@@ -105,6 +106,8 @@ def _load():
                                 C.POINTER(C.c_float), C.c_float, vp, C.POINTER(mp_io_stats), vp]
     L.mp_lora_materialize.argtypes = [lp, C.POINTER(mp_lora_tensor), i32, C.POINTER(vp), i32, vp, C.POINTER(vp),
                                       vp]
+    L.mp_lora_merge_ties_tau.argtypes = [lp, vp, C.POINTER(mp_lora_tensor), i32, C.POINTER(vp), i32, vp, vp,
+                                         C.c_float, vp, vp]
     L.mp_last_error.restype = C.c_char_p
     L.mp_stream_copy.argtypes = [vp, vp, u64, vp]
     L.mp_set_stage_bytes.argtypes = [u64]
@@ -119,7 +122,7 @@ def _load():
                  "mp_plan_noalloc", "mp_coverage", "mp_merge_avg",
                  "mp_merge_avg_renorm", "mp_merge_ties",
                  "mp_merge_ties_tau",
-                 "mp_merge_dare", "mp_lora_materialize", "mp_stream_copy"):
+                 "mp_merge_dare", "mp_lora_materialize", "mp_lora_merge_ties_tau", "mp_stream_copy"):
         getattr(L, name).restype = C.c_int
     return L
 
@@ -314,6 +317,23 @@ def mp_lora_materialize(layout: Layout, loras, adapters, deltas, mask=None, stre
     K = len(deltas)
     _check(lib.mp_lora_materialize(layout.ref, recs, len(loras), _ptrs(adapters) if loras else None, K, _ptr(mask),
                                    _ptrs(deltas), _stream(stream)))
+
+
+def mp_lora_merge_ties_tau(layout: Layout, base, loras, adapters, mask, tau, lam, out, stream=None):
+    """Budgeted TIES from catalog thresholds with every selected delta drawn
+    from the adapters inside the merge (no delta checkpoint): equal to
+    ``mp_lora_materialize(mask)`` then ``mp_merge_ties_tau(delta=True)``.
+
+    ``loras`` as for mp_lora_materialize; ``adapters``: K device tensors
+    (K entries of None when there are no records); ``mask``: device
+    int32[G]; ``tau``: device int32[G*K]."""
+    recs = (mp_lora_tensor * max(len(loras), 1))(
+        *[mp_lora_tensor(int(t), int(rank), int(rows), int(cols), int(a), int(b), float(sc))
+          for (t, rows, cols, rank, a, b, sc) in loras])
+    K = len(adapters)
+    _check(lib.mp_lora_merge_ties_tau(layout.ref, _ptr(base), recs, len(loras), _ptrs(adapters) if loras else None,
+                                      K, _ptr(mask),
+                                      _ptr(tau), float(lam), _ptr(out), _stream(stream)))
 
 
 def mp_last_error() -> str:

@@ -95,6 +95,7 @@ void free_lora(LoraEntry& e)
     (void)ws_free_r(e.t.d_zero);
     (void)ws_free_r(e.t.d_rl);
     (void)ws_free_r(e.t.d_rc);
+    (void)ws_free_r(e.t.d_prep);
     if (e.t.ev != nullptr)
         (void)hipEventDestroy(e.t.ev);
     (void)hipSetDevice(cur);
@@ -1134,7 +1135,22 @@ static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lor
             return fail(MP_E_UNSUPPORTED, "adapted tensors need 2^31 or more row bands");
         const uint64_t cv = 16 / (uint64_t)bt.esize;  // elements per 16 bytes
         d.vec = (d.a_off % cv == 0 && d.cols % cv == 0) ? 1u : 0u;
+        e->t.max_rank = std::max(e->t.max_rank, d.rank);
+        e->t.max_cols = std::max(e->t.max_cols, d.cols);
+        if (d.cols % cv != 0)
+            e->t.rows_chunked = false;
     }
+    // the fused merge's operand-order copy of one expert: per tensor A^T
+    // (columns padded to 64) then B (rows padded to 16), prep_rank values each
+    e->t.prep_rank = e->t.max_rank <= 16 ? 16u : (uint32_t)kMaxLoraRank;
+    uint64_t prep = 0;
+    for (LoraDesc& d : desc) {
+        d.at_off = prep;
+        prep += (uint64_t)(d.cols + 63) / 64 * 64 * e->t.prep_rank;
+        d.bp_off = prep;
+        prep += (uint64_t)(d.rows + 15) / 16 * 16 * e->t.prep_rank;
+    }
+    e->t.prep_elems = prep;
     std::vector<uint32_t> zero;
     for (int32_t t = 0; t < L->n_tensors; ++t)
         if (!adapted[(size_t)t])
@@ -1245,6 +1261,93 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
         e = hipEventRecord(lt->ev, s);
     if (e != hipSuccess)
         return hip_fail(e, "adapter delta launch");
+    return MP_OK;
+}
+
+int mp_lora_merge_ties_tau(const mp_layout* layout, const void* base, const mp_lora_tensor* loras, int32_t n_lora,
+                           const void* const* adapters, int32_t K, const uint32_t* mask, const uint32_t* tau,
+                           float lambda, void* out, void* stream)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    g_err.clear();
+    int es = 0;
+    int rc = validate_layout(layout, &es);
+    if (rc)
+        return rc;
+    if (K < 1 || K > kMaxK)
+        return fail(MP_E_ARG, "K = %d must be in [1, 32]", K);
+    if (!std::isfinite(lambda))
+        return fail(MP_E_ARG, "lambda is not finite");
+    if (n_lora > 0 && adapters == nullptr)
+        return fail(MP_E_ARG, "adapters is NULL");
+    const int64_t G = count_blocks(layout);
+    if ((uint64_t)G * (uint64_t)K >= (1ull << 32))
+        return fail(MP_E_ARG, "K * G = %lld does not fit 32-bit unit ids", (long long)(G * K));
+    int64_t need = 0;
+    if ((rc = validate_loras(layout, loras, n_lora, &need)))
+        return rc;
+    BlockTable* bt = nullptr;
+    LoraTable* lt = nullptr;
+    if ((rc = get_table(layout, es, &bt)) || (rc = get_lora_table(layout, *bt, loras, n_lora, &lt)))
+        return rc;
+    if (!lt->rows_chunked)
+        return fail(MP_E_UNSUPPORTED, "an adapted tensor's rows are not a whole number of 16-byte chunks "
+                                      "(bf16 needs a multiple of 8 columns)");
+    if ((uint64_t)16 * lt->max_cols * (uint64_t)es >= ((uint64_t)1 << 31))
+        return fail(MP_E_UNSUPPORTED, "an adapted tensor has %u columns: 16 rows exceed 2 GiB", lt->max_cols);
+    const size_t ckpt = (size_t)bt->P * (size_t)es;
+    std::vector<Range> ins;
+    if ((rc = check_device_buffer(base, ckpt, "base")))
+        return rc;
+    ins.push_back({static_cast<const char*>(base), ckpt, "base"});
+    ExpertPtrs ad{};
+    for (int i = 0; i < K && n_lora > 0; ++i) {
+        char nm[32];
+        std::snprintf(nm, sizeof nm, "adapters[%d]", i);
+        if ((rc = check_device_buffer(adapters[i], (size_t)need * (size_t)es, nm)))
+            return rc;
+        ins.push_back({static_cast<const char*>(adapters[i]), (size_t)need * (size_t)es, "an adapter"});
+        ad.p[i] = adapters[i];
+    }
+    if ((rc = check_device_buffer(mask, sizeof(uint32_t) * (size_t)G, "mask")) ||
+        (rc = check_device_buffer(tau, sizeof(uint32_t) * (size_t)(G * K), "tau")) ||
+        (rc = check_device_buffer(out, ckpt, "out")))
+        return rc;
+    ins.push_back({reinterpret_cast<const char*>(mask), sizeof(uint32_t) * (size_t)G, "mask"});
+    ins.push_back({reinterpret_cast<const char*>(tau), sizeof(uint32_t) * (size_t)(G * K), "tau"});
+    const Range o{static_cast<const char*>(out), ckpt, "out"};
+    for (const Range& r : ins)
+        if (overlaps(o, r))
+            return fail(MP_E_ARG, "out overlaps %s", r.name);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    OutPtrs prep{};
+    if (lt->n_tiles > 0) {
+        // the operand-order copies belong to the table: calls with the same
+        // layout and records run one after the other, on whatever streams
+        if (lt->ev == nullptr && (e = hipEventCreateWithFlags(&lt->ev, hipEventDisableTiming)) != hipSuccess)
+            return hip_fail(e, "hipEventCreateWithFlags");
+        if (lt->prep_k < K) {
+            if (lt->d_prep != nullptr && (e = hipEventSynchronize(lt->ev)) != hipSuccess)
+                return hip_fail(e, "hipEventSynchronize");
+            (void)ws_free_r(lt->d_prep);
+            lt->d_prep = nullptr;
+            lt->prep_k = 0;
+            if ((e = ws_malloc(&lt->d_prep, (size_t)K * lt->prep_elems * (size_t)es)) != hipSuccess)
+                return fail(MP_E_NOMEM, "adapter operand copies (%zu bytes): %s",
+                            (size_t)K * lt->prep_elems * (size_t)es, hipGetErrorString(e));
+            lt->prep_k = K;
+        }
+        for (int i = 0; i < K; ++i)
+            prep.p[i] = static_cast<char*>(lt->d_prep) + (size_t)i * lt->prep_elems * (size_t)es;
+        if ((e = hipStreamWaitEvent(s, lt->ev, 0)) != hipSuccess)
+            return hip_fail(e, "hipStreamWaitEvent");
+    }
+    e = launch_lora_ties(*bt, *lt, ad, prep, K, base, mask, tau, lambda, out, s);
+    if (e == hipSuccess && lt->n_tiles > 0)
+        e = hipEventRecord(lt->ev, s);
+    if (e != hipSuccess)
+        return hip_fail(e, "adapter TIES merge launch");
     return MP_OK;
 }
 

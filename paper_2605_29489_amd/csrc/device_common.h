@@ -1,5 +1,6 @@
 // Device helpers shared by the kernel files: element formats, 16-byte chunk
-// access and the counter-based RNG.
+// access, the counter-based RNG, wave reductions and TIES's sign election
+// with the disjoint mean.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -187,9 +188,94 @@ __device__ static inline uint32_t wave_max_u32(uint32_t v)
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// Bitwise OR over the 64 lanes of a wave, returned as a wave-uniform value.
+__device__ static inline uint32_t wave_or_u32(uint32_t v)
+{
+    v |= dpp_u32<0xb1, 0xf, 0xf, true>(v);   // quad_perm [1,0,3,2]
+    v |= dpp_u32<0x4e, 0xf, 0xf, true>(v);   // quad_perm [2,3,0,1]
+    v |= dpp_u32<0x141, 0xf, 0xf, true>(v);  // row_half_mirror
+    v |= dpp_u32<0x140, 0xf, 0xf, true>(v);  // row_mirror
+    v |= dpp_u32<0x142, 0xa, 0xf, false>(v); // row_bcast:15
+    v |= dpp_u32<0x143, 0xc, 0xf, false>(v); // row_bcast:31
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
 __device__ static inline uint32_t uniform_u32(uint32_t v)
 {
     return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+
+// ---------------------------------------------------------------- TIES sign election
+// TIES's sign election and disjoint mean (Appendix A.1) over a lane's E
+// elements: ps and ns hold the sums of the kept positive and negative deltas
+// (added in increasing expert order), cpn their counts (positive in the low,
+// negative in the high half, at most 32 each).  The sign whose rounded mass
+// is larger in magnitude is elected; acc receives the elected sum divided by
+// its count, correctly rounded, or 0 where no sign is elected (equal masses,
+// nothing kept).  Every lane of the wave calls it together (it reads other
+// lanes' registers); lane is the caller's index in the wave.
+template <int E>
+__device__ inline void ties_elect_mean(const float (&ps)[E], const float (&ns)[E], const uint32_t (&cpn)[E],
+                                       float (&acc)[E], int lane)
+{
+    // elect by comparing the rounded masses P and -N; mean of the
+    // agreeing entries
+    uint32_t den[E];
+    bool odd = false;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const bool up = ps[e] > -ns[e];
+        const bool dn = ps[e] < -ns[e];
+        acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);  // never NaN: a NaN mass elects nothing
+        // with no elected sign acc is 0 and any count >= 1 gives 0
+        den[e] = up ? (cpn[e] & 0xffffu) : (dn ? (cpn[e] >> 16) : 1u);
+        odd |= (den[e] & (den[e] - 1u)) != 0u;
+    }
+    bool tiny = false;
+    if (__any(odd)) {
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            tiny |= (fabsf(acc[e]) < 0x1p-100f) & (acc[e] != 0.0f);
+    }
+    if (!__any(odd)) {
+        // counts that are powers of two divide by exact scaling, one
+        // rounding of the quotient
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
+    } else if (!__any(tiny)) {
+        // The correctly rounded quotient acc / den (1 <= den <= 32)
+        // without a division.  Lane j holds h + l, two terms of 1/j:
+        // h <= 1/j within an ulp, l = max(fl32((1 - j h) h), 2^-126) > 0
+        // (the residual 1 - j h is exact), |h + l - 1/j| < 2^-44 / j.  Then
+        // fma(a, h, a l) lies within 2^-43 of a / den (relative).  When
+        // a / den is a normal number, every rounding boundary (a midpoint
+        // between neighbouring floats, which a / den never equals) lies
+        // at least 2^-25 / den >= 2^-30 (relative) away from it, so both
+        // round to the same value.  |a| >= 2^-100 keeps a / den and a l
+        // clear of the subnormal range (smaller masses divide); l > 0,
+        // so an infinite mass gives a l of its own sign and stays
+        // infinite.
+        const float fj = (float)(lane > 0 ? lane : 1);
+        float h = __builtin_amdgcn_rcpf(fj);
+        float r = fmaf(-fj, h, 1.0f);
+        if (r < 0.0f) {  // the hardware reciprocal rounded up: one ulp down
+            h = __uint_as_float(__float_as_uint(h) - 1u);
+            r = fmaf(-fj, h, 1.0f);
+        }
+        const float l = fmaxf(r * h, 0x1p-126f);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int src = (int)(den[e] << 2);
+            const float he = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(h)));
+            const float le = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(l)));
+            acc[e] = fmaf(acc[e], he, acc[e] * le);
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            acc[e] = acc[e] / (float)den[e];
+    }
 }
 
 // SplitMix64 output function: the value SplitMix64 returns when its state

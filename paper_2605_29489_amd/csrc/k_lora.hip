@@ -369,6 +369,325 @@ __global__ __launch_bounds__(256) void k_lora_zero(const uint32_t* __restrict__ 
         p[c] = make_uint4(0u, 0u, 0u, 0u);
 }
 
+// ---------------------------------------------------------------- TIES from thresholds, fused
+// The budgeted TIES merge with stored trim thresholds, drawing each delta
+// from the adapters inside the merge: out = fma(lambda, mean, x0) with the
+// sign election and disjoint mean over the selected units' kept deltas, each
+// delta computed exactly as the pull computes it (the same matrix-core tile
+// arrangement and summation, the same scaling and rounding to the dtype) and
+// never written to memory.
+//
+// First k_lora_prep lays each adapter out in MFMA operand order, zero-padded
+// to the depth RM: A^T (columns padded to a multiple of 64, RM values per
+// column) and B (rows padded to a multiple of 16, RM values per row).  An
+// operand is then one unconditional 8-byte (bf16) or 4-byte (fp32) load per
+// lane, and no staging in LDS is needed.  Zero padding adds exact zero
+// products, so the sums equal the pull's.
+//
+// k_lora_ties: one wave takes 16 rows of an adapted tensor (a quarter of a
+// 64-row band) and walks its 64-column tiles, on its own (no workgroup
+// barrier).  Per tile it issues the next tile's mask words and this tile's
+// base chunks, then for each expert selected in some block the tile meets,
+// in increasing order:
+//   * the expert's operands and thresholds arrive from a load issued while
+//     the previous expert computed;
+//   * it computes the 16 x 64 delta tile as D^T = A^T B^T in four 16 x 16
+//     MFMA tiles, scales and rounds it to the dtype, and passes it through
+//     its LDS strip so that each lane holds whole 16-byte chunks of one row;
+//   * the lane folds its chunks into the TIES state (sums and counts of the
+//     kept positive and negative deltas) with the unit's threshold; a chunk
+//     whose block does not select the expert gets a NaN threshold, which
+//     keeps nothing.
+// Then the sign election and mean, and the output chunks are stored.  A
+// chunk never straddles a block or a row: rows are a whole number of chunks
+// (bf16 tensors need a multiple of 8 columns) and blocks a whole number of
+// chunks.  The band's four waves run on one XCD and the bands are split
+// into eight contiguous ranges, one per XCD, so that a tensor's operands are
+// read into few L2s.
+constexpr int kFN = 64;  // fused tile columns (four MFMA tiles of 16)
+
+template <int DT, int RM>
+__global__ __launch_bounds__(256) void k_lora_prep(const LoraDesc* __restrict__ desc, ExpertPtrs ad, OutPtrs prep)
+{
+    using E = typename std::conditional<DT == 0, float, uint16_t>::type;
+    constexpr int CV = 16 / sizeof(E);
+    const LoraDesc D = desc[blockIdx.x];
+    const int i = blockIdx.y;
+    const E* __restrict__ A = static_cast<const E*>(ad.p[i]) + D.a_off;
+    const E* __restrict__ B = static_cast<const E*>(ad.p[i]) + D.b_off;
+    E* __restrict__ at = static_cast<E*>(prep.p[i]) + D.at_off;
+    E* __restrict__ bp = static_cast<E*>(prep.p[i]) + D.bp_off;
+    const uint32_t colsp = (D.cols + kFN - 1) / kFN * kFN, rowsp = (D.rows + 15u) / 16u * 16u;
+    const uint32_t step = gridDim.z * 256u;
+    for (uint32_t c = blockIdx.z * 256u + threadIdx.x; c < colsp; c += step) {
+        E v[RM];
+#pragma unroll
+        for (int k = 0; k < RM; ++k)
+            v[k] = ((uint32_t)k < D.rank && c < D.cols) ? A[(uint64_t)k * D.cols + c] : E(0);
+#pragma unroll
+        for (int q = 0; q < RM / CV; ++q)
+            reinterpret_cast<uint4*>(at + (uint64_t)c * RM)[q] = *reinterpret_cast<const uint4*>(&v[q * CV]);
+    }
+    for (uint32_t r = blockIdx.z * 256u + threadIdx.x; r < rowsp; r += step) {
+        E v[RM];
+#pragma unroll
+        for (int k = 0; k < RM; ++k)
+            v[k] = ((uint32_t)k < D.rank && r < D.rows) ? B[(uint64_t)r * D.rank + k] : E(0);
+#pragma unroll
+        for (int q = 0; q < RM / CV; ++q)
+            reinterpret_cast<uint4*>(bp + (uint64_t)r * RM)[q] = *reinterpret_cast<const uint4*>(&v[q * CV]);
+    }
+}
+
+template <int DT, int RM>
+__global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 64) ? 1 : 2) void k_lora_ties(const LoraDesc* __restrict__ desc, int n_desc, uint32_t n_bands,
+                                                  uint32_t bpx, ExpertPtrs prep, const void* __restrict__ base,
+                                                  const uint32_t* __restrict__ mask,
+                                                  const uint32_t* __restrict__ tau, int K, uint32_t kmask,
+                                                  float lambda, uint32_t block_elems, void* __restrict__ out)
+{
+    using E = typename std::conditional<DT == 0, float, uint16_t>::type;
+    constexpr int KS = DT == 0 ? 4 : 16;  // MFMA depth
+    constexpr int CV = 16 / sizeof(E);    // elements per 16-byte chunk
+    constexpr int NKS = RM / KS;          // MFMA depth steps
+    constexpr int CPR = kFN / CV;         // chunks per strip row
+    constexpr int NS = 16 * CPR / 64;     // chunk slots per lane
+    constexpr int EL = NS * CV;           // elements per lane (16)
+    constexpr int OSR = kFN + CV;         // strip row stride (elements; rows stay 16-byte aligned)
+    constexpr int FC = kFN / 16;          // MFMA tiles per tile
+    using AOp = typename std::conditional<DT == 0, float, short4_t>::type;
+    __shared__ __align__(16) E ow[16 * OSR];
+    // workgroup -> (band, quarter): XCD x = id mod 8 takes bands x*bpx ..
+    const uint32_t id = blockIdx.x, xcd = id & 7u, j = id >> 3;
+    const uint32_t band = xcd * bpx + (j >> 2);
+    if (band >= n_bands)
+        return;
+    const int lane = threadIdx.x;
+    const int d = __builtin_amdgcn_readfirstlane(find_desc(desc, n_desc, band));
+    const LoraDesc D = desc[d];
+    const uint32_t r0 = (band - D.tile0) * kTM + (j & 3u) * 16u;  // the wave's first row
+    const uint32_t rows = D.rows, cols = D.cols;
+    if (r0 >= rows)
+        return;
+    const uint32_t nrow = min(16u, rows - r0);
+    const uint32_t tiles = (cols + kFN - 1) / kFN;
+    const uint32_t nblk = (uint32_t)(((uint64_t)rows * cols + block_elems - 1) / block_elems);
+    const float scale = D.scale;
+    // the wave's rows of the base as a buffer: a load at an offset past them
+    // returns zeros without reading (16 * cols * esize < 2^31, checked by
+    // the host, so 2^31 is past them)
+    const uint32_t wbytes = nrow * cols * (uint32_t)sizeof(E);
+    const __amdgpu_buffer_rsrc_t rbase =
+        block_rsrc(static_cast<const E*>(base) + D.toff + (uint64_t)r0 * cols, wbytes);
+    E* __restrict__ xo = static_cast<E*>(out) + D.toff + (uint64_t)r0 * cols;
+    const uint32_t* __restrict__ mk = mask + D.g0;
+    const uint32_t* __restrict__ tk = tau + (uint64_t)D.g0 * (uint32_t)K;
+    // operands: A^T column n0 + ct*16 + lane%16, depth k0 + (bf16) 4*(lane/16) .. +3
+    // or (fp32) lane/16; B row r0 + lane%16, the same depths
+    const uint32_t dk = DT == 1 ? 4u * (uint32_t)(lane >> 4) : (uint32_t)(lane >> 4);
+    const uint64_t aoff = D.at_off + (uint64_t)(lane & 15) * RM + dk;
+    const uint64_t boff = D.bp_off + (uint64_t)(r0 + (uint32_t)(lane & 15)) * RM + dk;
+    // the lane's chunk slots: strip row srow, column scol; element e of the
+    // tensor in block lb, lr elements in
+    uint32_t srow[NS], scol[NS], lb[NS], lr[NS];
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+        const int c = q * 64 + lane;
+        srow[q] = (uint32_t)(c / CPR);
+        scol[q] = (uint32_t)((c % CPR) * CV);
+        const uint32_t e = (r0 + srow[q] < rows) ? (r0 + srow[q]) * cols + scol[q] : 0u;  // < numel < 2^32
+        lb[q] = e / block_elems;
+        lr[q] = e - lb[q] * block_elems;
+    }
+    auto chunk_ok = [&](int q, uint32_t n0) { return srow[q] < nrow && n0 + scol[q] < cols; };
+    // mask words of a tile's chunks (zero for chunks outside the tensor)
+    auto words = [&](uint32_t n0, const uint32_t (&b)[NS], uint32_t (&w)[NS]) {
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+            const uint32_t v = mk[min(b[q], nblk - 1u)];
+            w[q] = chunk_ok(q, n0) ? (v & kmask) : 0u;
+        }
+    };
+    auto tile_set = [&](const uint32_t (&w)[NS]) {
+        uint32_t o = 0u;
+#pragma unroll
+        for (int q = 0; q < NS; ++q)
+            o |= w[q];
+        return wave_or_u32(o);
+    };
+    struct Ops {
+        AOp a[NKS][FC];
+        AOp b[NKS];
+        uint32_t t[NS];
+    };
+    // expert i's operands for the tile at column n0, and its thresholds for
+    // the tile's blocks b
+    auto load_ops = [&](int i, uint32_t n0, const uint32_t (&b)[NS], Ops& o) {
+        const E* __restrict__ pa = static_cast<const E*>(prep.p[i]) + aoff + (uint64_t)n0 * RM;
+        const E* __restrict__ pb = static_cast<const E*>(prep.p[i]) + boff;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+#pragma unroll
+            for (int ct = 0; ct < FC; ++ct)
+                o.a[ks][ct] = *reinterpret_cast<const AOp*>(pa + ct * 16 * RM + ks * KS);
+            o.b[ks] = *reinterpret_cast<const AOp*>(pb + ks * KS);
+        }
+#pragma unroll
+        for (int q = 0; q < NS; ++q)
+            o.t[q] = tk[(uint64_t)min(b[q], nblk - 1u) * (uint32_t)K + (uint32_t)i];
+    };
+    uint32_t w[NS];
+    words(0u, lb, w);
+    uint32_t sel = tile_set(w);
+    Ops pre;
+    int pre_i = -1;       // the expert whose operands pre holds
+    uint32_t pre_t = 0u;  // and their tile
+    if (sel != 0u) {
+        pre_i = __builtin_ctz(sel);
+        load_ops(pre_i, 0u, lb, pre);
+    }
+    for (uint32_t tn = 0; tn < tiles; ++tn) {
+        const uint32_t n0 = tn * kFN;
+        const bool more = tn + 1 < tiles;
+        // the next tile's blocks and mask words, then this tile's base chunks
+        uint32_t lbn[NS], lrn[NS], wn[NS];
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+            lbn[q] = lb[q];
+            lrn[q] = lr[q] + kFN;
+            while (lrn[q] >= block_elems) {
+                lrn[q] -= block_elems;
+                ++lbn[q];
+            }
+        }
+        words(n0 + kFN, lbn, wn);  // all zero past the last tile (no chunk is inside)
+        uint4 xr[NS];
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+            const uint32_t off = chunk_ok(q, n0) ? (srow[q] * cols + n0 + scol[q]) * (uint32_t)sizeof(E) : 0x80000000u;
+            xr[q] = bld16s(rbase, off);
+        }
+        float ps[EL], ns[EL];
+        uint32_t cpn[EL];
+#pragma unroll
+        for (int e = 0; e < EL; ++e) {
+            ps[e] = 0.0f;
+            ns[e] = 0.0f;
+            cpn[e] = 0u;
+        }
+        uint32_t mm = sel;
+        while (mm != 0u) {
+            const int i = __builtin_ctz(mm);
+            mm &= mm - 1u;
+            if (pre_i != i || pre_t != tn)  // not prefetched (wave-uniform; not expected)
+                load_ops(i, n0, lb, pre);
+            const Ops cur = pre;
+            // the following expert's operands, in flight while this one computes
+            if (mm != 0u) {
+                pre_i = __builtin_ctz(mm);
+                pre_t = tn;
+                load_ops(pre_i, n0, lb, pre);
+            } else if (more) {
+                const uint32_t sn = tile_set(wn);
+                if (sn != 0u) {
+                    pre_i = __builtin_ctz(sn);
+                    pre_t = tn + 1;
+                    load_ops(pre_i, n0 + kFN, lbn, pre);
+                }
+            }
+            float4_t acc[FC];
+#pragma unroll
+            for (int ct = 0; ct < FC; ++ct)
+                acc[ct] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+#pragma unroll
+                for (int ct = 0; ct < FC; ++ct) {
+                    if constexpr (DT == 1)
+                        acc[ct] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(cur.a[ks][ct], cur.b[ks], acc[ct], 0, 0, 0);
+                    else
+                        acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.a[ks][ct], cur.b[ks], acc[ct], 0, 0, 0);
+                }
+            }
+            // the deltas as the pull stores them: scale * acc rounded to the
+            // dtype; accumulator j of tile ct is column ct*16 + 4*(lane/16) + j
+            // of strip row lane % 16 (the wave's LDS operations run in order)
+            const uint32_t cg = 4u * (uint32_t)(lane >> 4);
+#pragma unroll
+            for (int ct = 0; ct < FC; ++ct) {
+                const float y0 = scale * acc[ct][0], y1 = scale * acc[ct][1];
+                const float y2 = scale * acc[ct][2], y3 = scale * acc[ct][3];
+                E* p = &ow[(lane & 15) * OSR + ct * 16 + cg];
+                if constexpr (DT == 1)
+                    *reinterpret_cast<uint2*>(p) = make_uint2(Fmt<1>::pack2(y0, y1), Fmt<1>::pack2(y2, y3));
+                else
+                    *reinterpret_cast<float4*>(p) = make_float4(y0, y1, y2, y3);
+            }
+#pragma unroll
+            for (int q = 0; q < NS; ++q) {
+                const uint4 raw = *reinterpret_cast<const uint4*>(&ow[srow[q] * OSR + scol[q]]);
+                float x[CV];
+                Fmt<DT>::unpack(raw, x);
+                // keep |d| >= tau (at least the smallest positive pattern); a
+                // NaN threshold where the block does not select expert i
+                const float tauf = __uint_as_float(((w[q] >> i) & 1u) ? max(cur.t[q], 1u) : 0x7fc00000u);
+#pragma unroll
+                for (int v = 0; v < CV; ++v) {
+                    const int e = q * CV + v;
+                    const bool kp = x[v] >= tauf, kn = -x[v] >= tauf;
+                    ps[e] = ps[e] + (kp ? x[v] : 0.0f);
+                    ns[e] = ns[e] + (kn ? x[v] : 0.0f);
+                    cpn[e] += kp ? 1u : (kn ? 0x10000u : 0u);
+                }
+            }
+        }
+        float mean[EL];
+        ties_elect_mean<EL>(ps, ns, cpn, mean, lane);
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+            float x0[CV], y[CV];
+            Fmt<DT>::unpack(xr[q], x0);
+#pragma unroll
+            for (int v = 0; v < CV; ++v)
+                y[v] = fmaf(lambda, mean[q * CV + v], x0[v]);
+            if (chunk_ok(q, n0))
+                st16s(reinterpret_cast<uint4*>(xo + (uint64_t)srow[q] * cols + n0 + scol[q]), Fmt<DT>::pack(y));
+        }
+        sel = tile_set(wn);
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+            lb[q] = lbn[q];
+            lr[q] = lrn[q];
+            w[q] = wn[q];
+        }
+    }
+}
+
+// The merge where no expert has a delta (tensors without an adapter):
+// nothing is kept, so every element is fma(lambda, 0, x0), as the merge
+// over zero deltas writes it.
+template <int DT>
+__global__ __launch_bounds__(256) void k_lora_ties_rest(const uint32_t* __restrict__ blocks,
+                                                        const uint64_t* __restrict__ boff,
+                                                        const uint32_t* __restrict__ blen,
+                                                        const void* __restrict__ base, float lambda,
+                                                        void* __restrict__ out)
+{
+    constexpr int V = Fmt<DT>::V, ES = Fmt<DT>::esize;
+    const uint32_t g = blocks[blockIdx.x];
+    const uint4* src = chunk_ptr(base, boff[g], ES);
+    uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(out) + boff[g] * (uint64_t)ES);
+    const uint32_t nch = blen[g] / (uint32_t)V;
+    for (uint32_t c = threadIdx.x; c < nch; c += 256) {
+        float x0[V], y[V];
+        Fmt<DT>::unpack(ld16s(src + c), x0);
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+            y[v] = fmaf(lambda, 0.0f, x0[v]);
+        st16s(dst + c, Fmt<DT>::pack(y));
+    }
+}
+
 }  // namespace
 
 uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n)
@@ -400,6 +719,49 @@ hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPt
     if (lt.n_zero > 0)
         hipLaunchKernelGGL(k_lora_zero, dim3((unsigned)lt.n_zero, (unsigned)K), dim3(256), 0, s, lt.d_zero,
                            bt.d_off, bt.d_len, bt.esize, dl, mask);
+    return hipGetLastError();
+}
+
+
+hipError_t launch_lora_ties(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& prep,
+                            int K, const void* base, const uint32_t* mask, const uint32_t* tau, float lambda,
+                            void* out, hipStream_t s)
+{
+    const uint32_t kmask = (K >= 32) ? 0xffffffffu : ((1u << K) - 1u);
+    if (lt.n_tiles > 0) {
+        const uint32_t be = (uint32_t)bt.block_elems;
+        const uint32_t bpx = (lt.n_tiles + 7u) / 8u;  // bands per XCD
+        const dim3 pgrid((unsigned)lt.n_desc, (unsigned)K, 4u), grid(32u * bpx);
+        ExpertPtrs pp{};
+        for (int i = 0; i < K; ++i)
+            pp.p[i] = prep.p[i];
+#define MP_LORA_TIES(DTV, RMV)                                                                                     \
+    do {                                                                                                           \
+        hipLaunchKernelGGL((k_lora_prep<DTV, RMV>), pgrid, dim3(256), 0, s, lt.d_desc, ad, prep);                  \
+        hipLaunchKernelGGL((k_lora_ties<DTV, RMV>), grid, dim3(64), 0, s, lt.d_desc, lt.n_desc, lt.n_tiles, bpx,  \
+                           pp, base, mask, tau, K, kmask, lambda, be, out);                                        \
+    } while (0)
+        if (bt.dtype == 0) {
+            if (lt.prep_rank == 16)
+                MP_LORA_TIES(0, 16);
+            else
+                MP_LORA_TIES(0, kMaxLoraRank);
+        } else {
+            if (lt.prep_rank == 16)
+                MP_LORA_TIES(1, 16);
+            else
+                MP_LORA_TIES(1, kMaxLoraRank);
+        }
+#undef MP_LORA_TIES
+    }
+    if (lt.n_zero > 0) {
+        if (bt.dtype == 0)
+            hipLaunchKernelGGL(k_lora_ties_rest<0>, dim3((unsigned)lt.n_zero), dim3(256), 0, s, lt.d_zero, bt.d_off,
+                               bt.d_len, base, lambda, out);
+        else
+            hipLaunchKernelGGL(k_lora_ties_rest<1>, dim3((unsigned)lt.n_zero), dim3(256), 0, s, lt.d_zero, bt.d_off,
+                               bt.d_len, base, lambda, out);
+    }
     return hipGetLastError();
 }
 

@@ -238,66 +238,8 @@ __global__ __launch_bounds__(kTE, 8) void k_merge_elem(Src src, const void* __re
             mm &= mm - 1u;
         }
     }
-    if (SIGN) {
-        // elect by comparing the rounded masses P and -N; mean of the
-        // agreeing entries
-        uint32_t den[E];
-        bool odd = false;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            const bool up = ps[e] > -ns[e];
-            const bool dn = ps[e] < -ns[e];
-            acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);  // never NaN: a NaN mass elects nothing
-            // with no elected sign acc is 0 and any count >= 1 gives 0
-            den[e] = up ? (cpn[e] & 0xffffu) : (dn ? (cpn[e] >> 16) : 1u);
-            odd |= (den[e] & (den[e] - 1u)) != 0u;
-        }
-        bool tiny = false;
-        if (__any(odd)) {
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                tiny |= (fabsf(acc[e]) < 0x1p-100f) & (acc[e] != 0.0f);
-        }
-        if (!__any(odd)) {
-            // counts that are powers of two divide by exact scaling, one
-            // rounding of the quotient
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
-        } else if (!__any(tiny)) {
-            // The correctly rounded quotient acc / den (1 <= den <= 32)
-            // without a division.  Lane j holds h + l, two terms of 1/j:
-            // h <= 1/j within an ulp, l = max(fl32((1 - j h) h), 2^-126) > 0
-            // (the residual 1 - j h is exact), |h + l - 1/j| < 2^-44 / j.  Then
-            // fma(a, h, a l) lies within 2^-43 of a / den (relative).  When
-            // a / den is a normal number, every rounding boundary (a midpoint
-            // between neighbouring floats, which a / den never equals) lies
-            // at least 2^-25 / den >= 2^-30 (relative) away from it, so both
-            // round to the same value.  |a| >= 2^-100 keeps a / den and a l
-            // clear of the subnormal range (smaller masses divide); l > 0,
-            // so an infinite mass gives a l of its own sign and stays
-            // infinite.
-            const float fj = (float)(t > 0 ? t : 1);
-            float h = __builtin_amdgcn_rcpf(fj);
-            float r = fmaf(-fj, h, 1.0f);
-            if (r < 0.0f) {  // the hardware reciprocal rounded up: one ulp down
-                h = __uint_as_float(__float_as_uint(h) - 1u);
-                r = fmaf(-fj, h, 1.0f);
-            }
-            const float l = fmaxf(r * h, 0x1p-126f);
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int src = (int)(den[e] << 2);
-                const float he = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(h)));
-                const float le = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(l)));
-                acc[e] = fmaf(acc[e], he, acc[e] * le);
-            }
-        } else {
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                acc[e] = acc[e] / (float)den[e];
-        }
-    }
+    if (SIGN)
+        ties_elect_mean<E>(ps, ns, cpn, acc, t);
 #pragma unroll
     for (int q = 0; q < CPT; ++q) {
         float y[V];

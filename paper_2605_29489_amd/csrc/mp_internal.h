@@ -155,6 +155,7 @@ struct LoraDesc {
     uint32_t tile0;
     uint32_t vec;  // every row of A starts 16-byte aligned (relative to the adapter buffer)
     uint32_t r0;   // the tensor's first entry in a row list (rows of the earlier tensors)
+    uint64_t at_off, bp_off;  // element offsets of A^T and B in one expert's operand-order copy
 };
 
 // A validated set of adapter records for a layout, cached per device.
@@ -169,6 +170,13 @@ struct LoraTable {
     uint32_t* d_rc = nullptr;    //   and their counts, K x n_desc
     int rl_k = 0;                // experts the two arrays hold
     hipEvent_t ev = nullptr;     // recorded after each masked pull: the next one (any stream) waits for it
+    uint32_t max_rank = 0;       // the largest adapter rank
+    bool rows_chunked = true;    // every adapted tensor's rows are a whole number of 16-byte chunks
+    uint32_t max_cols = 0;       // the widest adapted tensor
+    uint32_t prep_rank = 16;     // depth of the operand-order copy (16 or kMaxLoraRank)
+    uint64_t prep_elems = 0;     // elements of one expert's operand-order copy
+    void* d_prep = nullptr;      // the fused merge's operand-order copies, prep_k x prep_elems (grown on demand)
+    int prep_k = 0;
 };
 
 // Row bands of a rows x cols tensor; *tiles_n receives the column tiles per band.
@@ -178,6 +186,12 @@ uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n);
 // pull needs lt.d_rl and lt.d_rc for at least K experts.
 hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& dl, int K,
                        const uint32_t* mask, hipStream_t s);
+// The budgeted TIES merge from stored thresholds with every delta drawn from
+// the adapters inside the merge (no delta checkpoint).
+// prep: K device buffers of lt.prep_elems elements each, rewritten by the call.
+hipError_t launch_lora_ties(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& prep,
+                            int K, const void* base, const uint32_t* mask, const uint32_t* tau, float lambda,
+                            void* out, hipStream_t s);
 
 // Merge operators.  `counters` is null or a device array of 256 uint64
 // accumulating the expert bytes the kernels load: slot (block mod 8) * 32 + i

@@ -338,3 +338,143 @@ def test_lora_fullsize_qwen_layout_sampled_tensors(mp):
     # tensors without an adapter: zeros
     for t in (0, len(lay.numel) - 1):
         assert not outs[0][int(toff[t]):int(toff[t + 1])].view(torch.int16).any().item()
+
+
+# ------------------------------------------------------------ fused adapter TIES merge
+def _fused(mp, spec, recs, ads_d, base_d, mask_np, tau_d, lam, K):
+    import torch
+    lay = spec.layout
+    L = mp.Layout(lay.numel, lay.block_elems, lay.dtype_code)
+    mask = torch.from_numpy(np.ascontiguousarray(mask_np, np.uint32).view(np.int32)).cuda()
+    out = torch.empty_like(base_d)
+    mp.mp_lora_merge_ties_tau(L, base_d, recs, ads_d if recs else [None] * K, mask, tau_d, lam, out)
+    torch.cuda.synchronize()
+    return to_host(out)
+
+
+def _fused_targets(dtype):
+    # bf16 needs whole 16-byte chunks per row: w5 (44 columns) only in fp32
+    return ("w0", "w1", "w2", "w3", "w4") + (("w5",) if dtype == "f32" else ())
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("rank", [1, 7, 16, 33, 64])
+def test_lora_fused_ties_exact_grid_bitwise(mp, dtype, rank):
+    # The fused merge against the oracle's pull then TIES from thresholds,
+    # on dyadic adapters (every rank sum exact): bitwise, at random, full and
+    # empty masks, with tensors off the tile grid and without adapters.
+    import torch
+    spec = _awkward(dtype)
+    lay = spec.layout
+    K = 3
+    recs, n = lora_records(spec, rank, 0.5, targets=_fused_targets(dtype))
+    ads = make_lora_adapters(n, K, dtype, seed=200 + rank, grid=True)
+    base_np, _ = make_family(spec, K=1, seed=rank)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    d_full = oracle.lora_materialize(blocks, dtype, lay.numel, recs, ads)
+    tau = oracle.ties_thresholds(blocks, dtype, base_np, d_full, 0.3, delta=True)
+    tau_d = torch.from_numpy(np.ascontiguousarray(tau, np.uint32).reshape(-1).view(np.int32)).cuda()
+    ads_d = [to_dev(a, dtype) for a in ads]
+    base_d = to_dev(base_np, dtype)
+    rng = np.random.default_rng(rank)
+    for name, mask in (("random", rng.integers(0, 8, blocks.G).astype(np.uint32)),
+                       ("full", np.full(blocks.G, 7, np.uint32)), ("empty", np.zeros(blocks.G, np.uint32))):
+        for lam in (1.0, 0.7):
+            _say(f"case lora fused exact {dtype} rank={rank} mask={name} lam={lam}")
+            got = _fused(mp, spec, recs, ads_d, base_d, mask, tau_d, lam, K)
+            want = oracle.merge_ties_tau(blocks, dtype, base_np, d_full, mask, tau, lam, delta=True)
+            assert assert_merge_equal(got, want, base_np, dtype, f"fused {name} lam={lam}") == 0
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("be", [8, 64, 112, 4096])
+def test_lora_fused_ties_block_sizes_bitwise(mp, dtype, be):
+    # blocks shorter than a tile row segment (several blocks per lane and
+    # tile) up to blocks holding many rows
+    import torch
+    spec = _awkward(dtype, be=be)
+    lay = spec.layout
+    K = 3
+    recs, n = lora_records(spec, 16, 0.5, targets=_fused_targets(dtype))
+    ads = make_lora_adapters(n, K, dtype, seed=be, grid=True)
+    base_np, _ = make_family(spec, K=1, seed=be)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    d_full = oracle.lora_materialize(blocks, dtype, lay.numel, recs, ads)
+    tau = oracle.ties_thresholds(blocks, dtype, base_np, d_full, 0.2, delta=True)
+    tau_d = torch.from_numpy(np.ascontiguousarray(tau, np.uint32).reshape(-1).view(np.int32)).cuda()
+    mask = np.random.default_rng(be).integers(0, 8, blocks.G).astype(np.uint32)
+    _say(f"case lora fused blocks {dtype} be={be} G={blocks.G}")
+    got = _fused(mp, spec, recs, [to_dev(a, dtype) for a in ads], to_dev(base_np, dtype), mask, tau_d, 1.0, K)
+    want = oracle.merge_ties_tau(blocks, dtype, base_np, d_full, mask, tau, 1.0, delta=True)
+    assert assert_merge_equal(got, want, base_np, dtype, f"fused be={be}") == 0
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("rank", [16, 64])
+def test_lora_fused_ties_equals_pull_then_merge(mp, dtype, rank):
+    # Normal-distributed adapters (fp32 accumulation not exact): the fused
+    # merge equals the library's own pull of the selected units followed by
+    # the threshold merge, bit for bit, with the thresholds from the
+    # library's catalog pass over the full pull.
+    import torch
+    spec = _awkward(dtype)
+    lay = spec.layout
+    K = 4
+    recs, n = lora_records(spec, rank, 2.0, targets=_fused_targets(dtype))
+    ads = make_lora_adapters(n, K, dtype, seed=300 + rank, std=0.05)
+    base_np, _ = make_family(spec, K=1, seed=300 + rank)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    L, full = _materialize(mp, spec, recs, ads, prefill=False)
+    base_d = to_dev(base_np, dtype)
+    tau_d = torch.empty(blocks.G * K, dtype=torch.int32, device="cuda")
+    mp.mp_index_ties(L, base_d, full, 0.2, tau_d, delta=True)
+    ads_d = [to_dev(a, dtype) for a in ads]
+    rng = np.random.default_rng(rank)
+    out = torch.empty_like(base_d)
+    for f in (0.1, 0.5, 1.0):
+        mask = np.where(rng.random((blocks.G, K)) < f, 1, 0).astype(np.uint32)
+        mask = (mask << np.arange(K, dtype=np.uint32)).sum(1).astype(np.uint32)
+        _say(f"case lora fused vs pull {dtype} rank={rank} f={f}")
+        _, sel = _materialize(mp, spec, recs, ads, mask, prefill=False)
+        mdev = torch.from_numpy(mask.view(np.int32)).cuda()
+        mp.mp_merge_ties_tau(L, base_d, sel, mdev, tau_d, 1.0, out, delta=True)
+        torch.cuda.synchronize()
+        want = to_host(out)
+        got = _fused(mp, spec, recs, ads_d, base_d, mask, tau_d, 1.0, K)
+        assert np.array_equal(got, want), f"f={f}: {int((got != want).sum())} elements differ"
+
+
+def test_lora_fused_ties_without_records_and_bad_arguments(mp):
+    import torch
+    spec = _awkward("bf16")
+    lay = spec.layout
+    K = 2
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    base_np, _ = make_family(spec, K=1, seed=7)
+    base_d = to_dev(base_np, "bf16")
+    mask = np.random.default_rng(7).integers(0, 4, blocks.G).astype(np.uint32)
+    tau = np.full(blocks.G * K, 0x3c000000, np.uint32)
+    tau_d = torch.from_numpy(tau.view(np.int32)).cuda()
+    _say("case lora fused no records")
+    got = _fused(mp, spec, [], None, base_d, mask, tau_d, 0.5, K)
+    zeros = [np.zeros(lay.n_params, np.uint16) for _ in range(K)]
+    want = oracle.merge_ties_tau(blocks, "bf16", base_np, zeros, mask, tau.reshape(blocks.G, K), 0.5, delta=True)
+    assert np.array_equal(got, want)
+    L = mp.Layout(lay.numel, lay.block_elems, lay.dtype_code)
+    mdev = torch.from_numpy(mask.view(np.int32)).cuda()
+    recs, n = lora_records(spec, 8, 1.0, targets=("w0", "w5"))
+    ads = [torch.zeros(n, dtype=torch.bfloat16, device="cuda") for _ in range(K)]
+    out = torch.empty_like(base_d)
+    with pytest.raises(mp.MPError) as e:  # w5: 44 bf16 columns, rows not whole 16-byte chunks
+        mp.mp_lora_merge_ties_tau(L, base_d, recs, ads, mdev, tau_d, 1.0, out)
+    assert e.value.code == mp.MP_E_UNSUPPORTED
+    recs, n = lora_records(spec, 8, 1.0, targets=("w0",))
+    with pytest.raises(mp.MPError) as e:  # out is the base
+        mp.mp_lora_merge_ties_tau(L, base_d, recs, ads, mdev, tau_d, 1.0, base_d)
+    assert e.value.code == mp.MP_E_ARG
+    with pytest.raises(mp.MPError) as e:  # thresholds in host memory
+        mp.mp_lora_merge_ties_tau(L, base_d, recs, ads, mdev, torch.from_numpy(tau.view(np.int32)), 1.0, out)
+    assert e.value.code == mp.MP_E_ARG
+    with pytest.raises(mp.MPError) as e:
+        mp.mp_lora_merge_ties_tau(L, base_d, recs, ads, mdev, tau_d, float("nan"), out)
+    assert e.value.code == mp.MP_E_ARG
