@@ -1145,6 +1145,8 @@ static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lor
     e->t.prep_rank = e->t.max_rank <= 16 ? 16u : (uint32_t)kMaxLoraRank;
     uint64_t prep = 0;
     for (LoraDesc& d : desc) {
+        const uint64_t z = std::max((uint64_t)(d.cols + 63) / 64 * 64, (uint64_t)(d.rows + 15) / 16 * 16);
+        e->t.prep_z = std::max(e->t.prep_z, (uint32_t)((z + 127) / 128));
         d.at_off = prep;
         prep += (uint64_t)(d.cols + 63) / 64 * 64 * e->t.prep_rank;
         d.bp_off = prep;

@@ -219,18 +219,20 @@ __device__ inline void ties_elect_mean(const float (&ps)[E], const float (&ns)[E
                                        float (&acc)[E], int lane)
 {
     // elect by comparing the rounded masses P and -N; mean of the
-    // agreeing entries
+    // agreeing entries (branch-free: every lane runs the same instructions)
     uint32_t den[E];
-    bool odd = false;
+    uint32_t oddm = 0u;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
         const bool up = ps[e] > -ns[e];
         const bool dn = ps[e] < -ns[e];
         acc[e] = up ? ps[e] : (dn ? ns[e] : 0.0f);  // never NaN: a NaN mass elects nothing
-        // with no elected sign acc is 0 and any count >= 1 gives 0
-        den[e] = up ? (cpn[e] & 0xffffu) : (dn ? (cpn[e] >> 16) : 1u);
-        odd |= (den[e] & (den[e] - 1u)) != 0u;
+        // the elected sign's count (low half: positive, high half:
+        // negative); with no elected sign acc is 0 and any count >= 1 gives 0
+        den[e] = max(__builtin_amdgcn_ubfe(cpn[e], dn ? 16u : 0u, 16u), 1u);
+        oddm |= den[e] & (den[e] - 1u);
     }
+    const bool odd = oddm != 0u;
     bool tiny = false;
     if (__any(odd)) {
 #pragma unroll
@@ -242,7 +244,7 @@ __device__ inline void ties_elect_mean(const float (&ps)[E], const float (&ns)[E
         // rounding of the quotient
 #pragma unroll
         for (int e = 0; e < E; ++e)
-            acc[e] = acc[e] * __uint_as_float((127u - (uint32_t)__builtin_ctz(den[e])) << 23);
+            acc[e] = __builtin_amdgcn_ldexpf(acc[e], -(int)__builtin_ctz(den[e]));
     } else if (!__any(tiny)) {
         // The correctly rounded quotient acc / den (1 <= den <= 32)
         // without a division.  Lane j holds h + l, two terms of 1/j:

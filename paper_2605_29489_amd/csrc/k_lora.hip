@@ -406,36 +406,104 @@ __global__ __launch_bounds__(256) void k_lora_zero(const uint32_t* __restrict__ 
 // read into few L2s.
 constexpr int kFN = 64;  // fused tile columns (four MFMA tiles of 16)
 
+// Two deltas d0, d1 folded into their elements' TIES state with threshold
+// tau: keep d iff d >= tau (positive) or -d >= tau (negative); ps sums the
+// kept positive deltas, ns the kept negative ones, cpn counts them (low half
+// positive, high half negative).  Eight instructions per delta, the positive
+// test being the carry into the count's add (the compiler's own form takes
+// ten).  Every lane mask is read at least three instructions after the
+// compare that writes it (a VALU write of an SGPR needs two wait states
+// before a VALU reads it).  c16 holds 0x10000.
+__device__ inline void ties_fold2(float d0, float d1, float tau, uint32_t c16, float& ps0, float& ns0,
+                                  uint32_t& cpn0, float& ps1, float& ns1, uint32_t& cpn1)
+{
+    uint64_t kp0, kn0, kp1, kn1, co;
+    float t0, t1;
+    asm("v_cmp_le_f32_e64 %[kp0], %[tau], %[d0]\n\t"
+        "v_cmp_le_f32_e64 %[kn0], %[tau], -%[d0]\n\t"
+        "v_cmp_le_f32_e64 %[kp1], %[tau], %[d1]\n\t"
+        "v_cmp_le_f32_e64 %[kn1], %[tau], -%[d1]\n\t"
+        "v_cndmask_b32_e64 %[t0], 0, %[d0], %[kp0]\n\t"
+        "v_cndmask_b32_e64 %[t1], 0, %[d0], %[kn0]\n\t"
+        "v_add_f32_e32 %[ps0], %[ps0], %[t0]\n\t"
+        "v_add_f32_e32 %[ns0], %[ns0], %[t1]\n\t"
+        "v_cndmask_b32_e64 %[t0], 0, %[d1], %[kp1]\n\t"
+        "v_cndmask_b32_e64 %[t1], 0, %[d1], %[kn1]\n\t"
+        "v_add_f32_e32 %[ps1], %[ps1], %[t0]\n\t"
+        "v_add_f32_e32 %[ns1], %[ns1], %[t1]\n\t"
+        "v_cndmask_b32_e64 %[t0], 0, %[c16], %[kn0]\n\t"
+        "v_cndmask_b32_e64 %[t1], 0, %[c16], %[kn1]\n\t"
+        "v_addc_co_u32_e64 %[cpn0], %[co], %[cpn0], %[t0], %[kp0]\n\t"
+        "v_addc_co_u32_e64 %[cpn1], %[co], %[cpn1], %[t1], %[kp1]"
+        : [ps0] "+v"(ps0), [ns0] "+v"(ns0), [cpn0] "+v"(cpn0), [ps1] "+v"(ps1), [ns1] "+v"(ns1),
+          [cpn1] "+v"(cpn1), [kp0] "=&s"(kp0), [kn0] "=&s"(kn0), [kp1] "=&s"(kp1), [kn1] "=&s"(kn1),
+          [co] "=&s"(co), [t0] "=&v"(t0), [t1] "=&v"(t1)
+        : [d0] "v"(d0), [d1] "v"(d1), [tau] "v"(tau), [c16] "v"(c16));
+}
+
+// Workgroup z of (tensor, expert) lays out columns z*128 .. of A^T and rows
+// z*128 .. of B.  A's 128-column slice is read in 16-byte row chunks and
+// transposed through LDS, so that both the loads and the stores are
+// contiguous across lanes.
+constexpr int kPrepCols = 128;
+
 template <int DT, int RM>
-__global__ __launch_bounds__(256) void k_lora_prep(const LoraDesc* __restrict__ desc, ExpertPtrs ad, OutPtrs prep)
+__global__ __launch_bounds__(256) void k_lora_prep(const LoraDesc* __restrict__ desc, ExpertPtrs ad, OutPtrs prep,
+                                                   int aligned)
 {
     using E = typename std::conditional<DT == 0, float, uint16_t>::type;
     constexpr int CV = 16 / sizeof(E);
+    constexpr int RS = RM + CV;  // LDS row stride: rows stay 16-byte aligned
+    constexpr int CPC = RM / CV; // chunks per A^T column (and per B row)
+    __shared__ __align__(16) E T[kPrepCols * RS];
     const LoraDesc D = desc[blockIdx.x];
     const int i = blockIdx.y;
+    const uint32_t t = threadIdx.x;
     const E* __restrict__ A = static_cast<const E*>(ad.p[i]) + D.a_off;
     const E* __restrict__ B = static_cast<const E*>(ad.p[i]) + D.b_off;
     E* __restrict__ at = static_cast<E*>(prep.p[i]) + D.at_off;
     E* __restrict__ bp = static_cast<E*>(prep.p[i]) + D.bp_off;
     const uint32_t colsp = (D.cols + kFN - 1) / kFN * kFN, rowsp = (D.rows + 15u) / 16u * 16u;
-    const uint32_t step = gridDim.z * 256u;
-    for (uint32_t c = blockIdx.z * 256u + threadIdx.x; c < colsp; c += step) {
-        E v[RM];
+    const uint32_t c0 = blockIdx.z * kPrepCols;
+    if (c0 < colsp) {
+        // A[k][c0 + n .. + CV - 1] for k < RM (zeros past the rank and the columns)
+        const bool vec = aligned != 0 && D.vec != 0u;
+        for (uint32_t c = t; c < (uint32_t)(RM * kPrepCols / CV); c += 256) {
+            const uint32_t k = c / (kPrepCols / CV), n = (c % (kPrepCols / CV)) * CV;
+            E v[CV];
+            if (vec && k < D.rank && c0 + n < D.cols) {
+                *reinterpret_cast<uint4*>(v) = *reinterpret_cast<const uint4*>(A + (uint64_t)k * D.cols + c0 + n);
+            } else {
 #pragma unroll
-        for (int k = 0; k < RM; ++k)
-            v[k] = ((uint32_t)k < D.rank && c < D.cols) ? A[(uint64_t)k * D.cols + c] : E(0);
+                for (int q = 0; q < CV; ++q)
+                    v[q] = (k < D.rank && c0 + n + q < D.cols) ? A[(uint64_t)k * D.cols + c0 + n + q] : E(0);
+            }
 #pragma unroll
-        for (int q = 0; q < RM / CV; ++q)
-            reinterpret_cast<uint4*>(at + (uint64_t)c * RM)[q] = *reinterpret_cast<const uint4*>(&v[q * CV]);
+            for (int q = 0; q < CV; ++q)
+                T[(n + q) * RS + k] = v[q];
+        }
+        __syncthreads();
+        const uint32_t ncol = min((uint32_t)kPrepCols, colsp - c0);
+        for (uint32_t c = t; c < ncol * CPC; c += 256) {
+            const uint32_t n = c / CPC, j = c % CPC;
+            reinterpret_cast<uint4*>(at + (uint64_t)(c0 + n) * RM)[j] =
+                *reinterpret_cast<const uint4*>(&T[n * RS + j * CV]);
+        }
     }
-    for (uint32_t r = blockIdx.z * 256u + threadIdx.x; r < rowsp; r += step) {
-        E v[RM];
-#pragma unroll
-        for (int k = 0; k < RM; ++k)
-            v[k] = ((uint32_t)k < D.rank && r < D.rows) ? B[(uint64_t)r * D.rank + k] : E(0);
-#pragma unroll
-        for (int q = 0; q < RM / CV; ++q)
-            reinterpret_cast<uint4*>(bp + (uint64_t)r * RM)[q] = *reinterpret_cast<const uint4*>(&v[q * CV]);
+    if (c0 < rowsp) {
+        // B's rows c0 .. with RM values each (zeros past the rank and the rows)
+        const uint32_t nrow = min((uint32_t)kPrepCols, rowsp - c0);
+        if (aligned != 0 && D.rank == (uint32_t)RM && D.b_off % CV == 0) {
+            const uint4* src = reinterpret_cast<const uint4*>(B + (uint64_t)c0 * RM);
+            uint4* dst = reinterpret_cast<uint4*>(bp + (uint64_t)c0 * RM);
+            for (uint32_t c = t; c < nrow * CPC; c += 256)
+                dst[c] = (c0 + c / CPC < D.rows) ? src[c] : make_uint4(0u, 0u, 0u, 0u);
+        } else {
+            for (uint32_t c = t; c < nrow * RM; c += 256) {
+                const uint32_t r = c0 + c / RM, k = c % RM;
+                bp[(uint64_t)c0 * RM + c] = (k < D.rank && r < D.rows) ? B[(uint64_t)r * D.rank + k] : E(0);
+            }
+        }
     }
 }
 
@@ -444,7 +512,9 @@ __global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 6
                                                   uint32_t bpx, ExpertPtrs prep, const void* __restrict__ base,
                                                   const uint32_t* __restrict__ mask,
                                                   const uint32_t* __restrict__ tau, int K, uint32_t kmask,
-                                                  float lambda, uint32_t block_elems, void* __restrict__ out)
+                                                  float lambda, uint32_t block_elems, void* __restrict__ out,
+                                                  const uint32_t* __restrict__ zero, const uint64_t* __restrict__ zoff,
+                                                  const uint32_t* __restrict__ zlen)
 {
     using E = typename std::conditional<DT == 0, float, uint16_t>::type;
     constexpr int KS = DT == 0 ? 4 : 16;  // MFMA depth
@@ -457,6 +527,36 @@ __global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 6
     constexpr int FC = kFN / 16;          // MFMA tiles per tile
     using AOp = typename std::conditional<DT == 0, float, short4_t>::type;
     __shared__ __align__(16) E ow[16 * OSR];
+    if (blockIdx.x >= 32u * bpx) {
+        // the workgroups past the bands take the blocks of tensors without an
+        // adapter, where nothing is kept: fma(lambda, 0, x0), as the merge
+        // over zero deltas writes it (they run last and fill the tail)
+        constexpr int V = Fmt<DT>::V, ES = Fmt<DT>::esize;
+        const uint32_t g = zero[blockIdx.x - 32u * bpx];
+        const uint4* src = chunk_ptr(base, zoff[g], ES);
+        uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(out) + zoff[g] * (uint64_t)ES);
+        const uint32_t nch = zlen[g] / (uint32_t)V;
+        for (uint32_t c0 = 0; c0 < nch; c0 += 4 * 64) {
+            uint4 v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t c = c0 + (uint32_t)(q * 64) + threadIdx.x;
+                v[q] = c < nch ? ld16s(src + c) : make_uint4(0u, 0u, 0u, 0u);
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t c = c0 + (uint32_t)(q * 64) + threadIdx.x;
+                float x0[V], y[V];
+                Fmt<DT>::unpack(v[q], x0);
+#pragma unroll
+                for (int e = 0; e < V; ++e)
+                    y[e] = fmaf(lambda, 0.0f, x0[e]);
+                if (c < nch)
+                    st16s(dst + c, Fmt<DT>::pack(y));
+            }
+        }
+        return;
+    }
     // workgroup -> (band, quarter): XCD x = id mod 8 takes bands x*bpx ..
     const uint32_t id = blockIdx.x, xcd = id & 7u, j = id >> 3;
     const uint32_t band = xcd * bpx + (j >> 2);
@@ -473,6 +573,7 @@ __global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 6
     const uint32_t tiles = (cols + kFN - 1) / kFN;
     const uint32_t nblk = (uint32_t)(((uint64_t)rows * cols + block_elems - 1) / block_elems);
     const float scale = D.scale;
+    const uint32_t c16 = 0x10000u;  // a negative kept delta's count increment
     // the wave's rows of the base as a buffer: a load at an offset past them
     // returns zeros without reading (16 * cols * esize < 2^31, checked by
     // the host, so 2^31 is past them)
@@ -569,12 +670,17 @@ __global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 6
         }
         float ps[EL], ns[EL];
         uint32_t cpn[EL];
+        if (sel == 0u) {
 #pragma unroll
-        for (int e = 0; e < EL; ++e) {
-            ps[e] = 0.0f;
-            ns[e] = 0.0f;
-            cpn[e] = 0u;
+            for (int e = 0; e < EL; ++e) {
+                ps[e] = 0.0f;
+                ns[e] = 0.0f;
+                cpn[e] = 0u;
+            }
         }
+        // the first selected expert starts the state: 0 + t is t for every
+        // t a kept or dropped delta contributes (kept ones are nonzero)
+        bool first = true;
         uint32_t mm = sel;
         while (mm != 0u) {
             const int i = __builtin_ctz(mm);
@@ -631,15 +737,25 @@ __global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 6
                 // keep |d| >= tau (at least the smallest positive pattern); a
                 // NaN threshold where the block does not select expert i
                 const float tauf = __uint_as_float(((w[q] >> i) & 1u) ? max(cur.t[q], 1u) : 0x7fc00000u);
+                if (first) {
 #pragma unroll
-                for (int v = 0; v < CV; ++v) {
-                    const int e = q * CV + v;
-                    const bool kp = x[v] >= tauf, kn = -x[v] >= tauf;
-                    ps[e] = ps[e] + (kp ? x[v] : 0.0f);
-                    ns[e] = ns[e] + (kn ? x[v] : 0.0f);
-                    cpn[e] += kp ? 1u : (kn ? 0x10000u : 0u);
+                    for (int v = 0; v < CV; ++v) {
+                        const int e = q * CV + v;
+                        const bool kp = x[v] >= tauf, kn = -x[v] >= tauf;
+                        ps[e] = kp ? x[v] : 0.0f;
+                        ns[e] = kn ? x[v] : 0.0f;
+                        cpn[e] = kp ? 1u : (kn ? 0x10000u : 0u);
+                    }
+                } else {
+#pragma unroll
+                    for (int v = 0; v < CV; v += 2) {
+                        const int e = q * CV + v;
+                        ties_fold2(x[v], x[v + 1], tauf, c16, ps[e], ns[e], cpn[e], ps[e + 1], ns[e + 1],
+                                   cpn[e + 1]);
+                    }
                 }
             }
+            first = false;
         }
         float mean[EL];
         ties_elect_mean<EL>(ps, ns, cpn, mean, lane);
@@ -660,31 +776,6 @@ __global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 6
             lr[q] = lrn[q];
             w[q] = wn[q];
         }
-    }
-}
-
-// The merge where no expert has a delta (tensors without an adapter):
-// nothing is kept, so every element is fma(lambda, 0, x0), as the merge
-// over zero deltas writes it.
-template <int DT>
-__global__ __launch_bounds__(256) void k_lora_ties_rest(const uint32_t* __restrict__ blocks,
-                                                        const uint64_t* __restrict__ boff,
-                                                        const uint32_t* __restrict__ blen,
-                                                        const void* __restrict__ base, float lambda,
-                                                        void* __restrict__ out)
-{
-    constexpr int V = Fmt<DT>::V, ES = Fmt<DT>::esize;
-    const uint32_t g = blocks[blockIdx.x];
-    const uint4* src = chunk_ptr(base, boff[g], ES);
-    uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(out) + boff[g] * (uint64_t)ES);
-    const uint32_t nch = blen[g] / (uint32_t)V;
-    for (uint32_t c = threadIdx.x; c < nch; c += 256) {
-        float x0[V], y[V];
-        Fmt<DT>::unpack(ld16s(src + c), x0);
-#pragma unroll
-        for (int v = 0; v < V; ++v)
-            y[v] = fmaf(lambda, 0.0f, x0[v]);
-        st16s(dst + c, Fmt<DT>::pack(y));
     }
 }
 
@@ -728,40 +819,37 @@ hipError_t launch_lora_ties(const BlockTable& bt, const LoraTable& lt, const Exp
                             void* out, hipStream_t s)
 {
     const uint32_t kmask = (K >= 32) ? 0xffffffffu : ((1u << K) - 1u);
-    if (lt.n_tiles > 0) {
-        const uint32_t be = (uint32_t)bt.block_elems;
-        const uint32_t bpx = (lt.n_tiles + 7u) / 8u;  // bands per XCD
-        const dim3 pgrid((unsigned)lt.n_desc, (unsigned)K, 4u), grid(32u * bpx);
-        ExpertPtrs pp{};
-        for (int i = 0; i < K; ++i)
-            pp.p[i] = prep.p[i];
+    const uint32_t be = (uint32_t)bt.block_elems;
+    const uint32_t bpx = (lt.n_tiles + 7u) / 8u;  // bands per XCD
+    if (32u * bpx + lt.n_zero == 0u)
+        return hipSuccess;
+    int aligned = 1;
+    for (int i = 0; i < K && lt.n_tiles > 0; ++i)
+        if (reinterpret_cast<uintptr_t>(ad.p[i]) % 16 != 0)
+            aligned = 0;
+    const dim3 pgrid((unsigned)lt.n_desc, (unsigned)K, lt.prep_z), grid(32u * bpx + lt.n_zero);
+    ExpertPtrs pp{};
+    for (int i = 0; i < K; ++i)
+        pp.p[i] = prep.p[i];
 #define MP_LORA_TIES(DTV, RMV)                                                                                     \
     do {                                                                                                           \
-        hipLaunchKernelGGL((k_lora_prep<DTV, RMV>), pgrid, dim3(256), 0, s, lt.d_desc, ad, prep);                  \
+        if (lt.n_tiles > 0)                                                                                        \
+            hipLaunchKernelGGL((k_lora_prep<DTV, RMV>), pgrid, dim3(256), 0, s, lt.d_desc, ad, prep, aligned);     \
         hipLaunchKernelGGL((k_lora_ties<DTV, RMV>), grid, dim3(64), 0, s, lt.d_desc, lt.n_desc, lt.n_tiles, bpx,  \
-                           pp, base, mask, tau, K, kmask, lambda, be, out);                                        \
+                           pp, base, mask, tau, K, kmask, lambda, be, out, lt.d_zero, bt.d_off, bt.d_len);         \
     } while (0)
-        if (bt.dtype == 0) {
-            if (lt.prep_rank == 16)
-                MP_LORA_TIES(0, 16);
-            else
-                MP_LORA_TIES(0, kMaxLoraRank);
-        } else {
-            if (lt.prep_rank == 16)
-                MP_LORA_TIES(1, 16);
-            else
-                MP_LORA_TIES(1, kMaxLoraRank);
-        }
-#undef MP_LORA_TIES
-    }
-    if (lt.n_zero > 0) {
-        if (bt.dtype == 0)
-            hipLaunchKernelGGL(k_lora_ties_rest<0>, dim3((unsigned)lt.n_zero), dim3(256), 0, s, lt.d_zero, bt.d_off,
-                               bt.d_len, base, lambda, out);
+    if (bt.dtype == 0) {
+        if (lt.prep_rank == 16)
+            MP_LORA_TIES(0, 16);
         else
-            hipLaunchKernelGGL(k_lora_ties_rest<1>, dim3((unsigned)lt.n_zero), dim3(256), 0, s, lt.d_zero, bt.d_off,
-                               bt.d_len, base, lambda, out);
+            MP_LORA_TIES(0, kMaxLoraRank);
+    } else {
+        if (lt.prep_rank == 16)
+            MP_LORA_TIES(1, 16);
+        else
+            MP_LORA_TIES(1, kMaxLoraRank);
     }
+#undef MP_LORA_TIES
     return hipGetLastError();
 }
 

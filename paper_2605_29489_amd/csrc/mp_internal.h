@@ -175,6 +175,7 @@ struct LoraTable {
     uint32_t max_cols = 0;       // the widest adapted tensor
     uint32_t prep_rank = 16;     // depth of the operand-order copy (16 or kMaxLoraRank)
     uint64_t prep_elems = 0;     // elements of one expert's operand-order copy
+    uint32_t prep_z = 1;         // 128-column (and 128-row) slices of the widest (tallest) adapted tensor
     void* d_prep = nullptr;      // the fused merge's operand-order copies, prep_k x prep_elems (grown on demand)
     int prep_k = 0;
 };
