@@ -70,7 +70,7 @@ def kernel_source_hash(route="catalog") -> str:
 
 
 LORA_SOURCES = ("paper_2605_29489_amd/csrc/k_lora.hip", "paper_2605_29489_amd/csrc/device_common.h")
-LORA_TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "lora_pull_qwen2.5-1.5b_kernel_trace.md")
+LORA_TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "lora_ties_qwen2.5-1.5b_counters.md")
 
 
 def lora_source_hash() -> str:
@@ -82,9 +82,9 @@ def lora_source_hash() -> str:
 
 
 def stored_lora_traffic():
-    """HBM bytes of one pull of every unit (k_lora_band + k_lora_zero) from
-    the committed counter profile, or None if it is missing or was taken on a
-    different kernel source."""
+    """HBM bytes of one fused adapter TIES merge launch (k_lora_ties, the
+    mean over the three budgets) from the committed counter profile, or None
+    if it is missing or was taken on a different kernel source."""
     if not os.path.exists(LORA_TRAFFIC_PROFILE):
         return None
     kv = {}
@@ -95,7 +95,7 @@ def stored_lora_traffic():
     if kv.get("kernel_source_sha256_16") != lora_source_hash():
         return None
     try:
-        return float(kv["hbm_bytes_pull_all"])
+        return float(kv["hbm_bytes_fused_launch"])
     except (KeyError, ValueError):
         return None
 
@@ -411,9 +411,12 @@ def run_lora(args):
         "config": {"workload": f"{spec.description}; {cfg}", "storage_dtype": lay.dtype, "params": P,
                    "adapted_params": adapted, "adapter_elems_per_expert": n_ad, "blocks": G, "K": K,
                    "experts": "device (adapters)", "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "k_lora_ties (+ k_lora_ties_rest), mean over the budgets",
+        "roofline": {"bound": "hbm", "kernel": "k_lora_ties, mean over the budgets",
                      "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": achieved / HBM_PEAK,
-                     "traffic": stored_lora_traffic() if lay.dtype == "bf16" and args.layers is None else None},
+                     "traffic": stored_lora_traffic() if lay.dtype == "bf16" and args.layers is None else None,
+                     "note": "bytes moved are the base read and the output written once; the kernel is bound by "
+                             "vector-ALU issue (the TIES fold of every element for each selected expert, 8 "
+                             "instructions per delta), not by HBM"},
         "breakdown": {"pull_all_ms": round(pull_all_ms, 4), "index_ms": round(idx_ms, 4),
                       "pull_all_GBps": (K * P * es + K * n_ad * es) / (pull_all_ms * 1e-3) / 1e9,
                       "per_budget": rows},
