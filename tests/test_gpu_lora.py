@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 from tests.gpu_util import assert_merge_equal, to_dev, to_host
-from workloads import FamilySpec, family_spec, lora_records, make_family, make_lora_adapters
+from workloads import FamilySpec, family_spec, lora_records, make_family, make_family_device, make_lora_adapters
 
 pytestmark = pytest.mark.gpu
 
@@ -478,3 +478,66 @@ def test_lora_fused_ties_without_records_and_bad_arguments(mp):
     with pytest.raises(mp.MPError) as e:
         mp.mp_lora_merge_ties_tau(L, base_d, recs, ads, mdev, tau_d, float("nan"), out)
     assert e.value.code == mp.MP_E_ARG
+
+
+def test_lora_fused_fullsize_qwen_layout(mp):
+    # The Qwen2.5-1.5B layout with rank-16 adapters on every projection, four
+    # experts, in the launch configuration the benchmark times: catalog from
+    # the full pull, skip-zero plans at two budgets, then the fused merge.
+    # Dyadic adapters keep every delta exact, so the whole output equals the
+    # two-call route and whole tensors equal the oracle (thresholds included).
+    import torch
+    spec = family_spec("qwen2.5-1.5b")
+    lay = spec.layout
+    K = 4
+    P = lay.n_params
+    recs, n = lora_records(spec, 16, 2.0)
+    ads_np = make_lora_adapters(n, K, "bf16", seed=23, grid=True)
+    L = mp.Layout(lay.numel, lay.block_elems, lay.dtype_code)
+    G = mp.mp_layout_blocks(L)
+    base, ex = make_family_device(spec, K=1, seed=5)
+    del ex
+    ads = [to_dev(a, "bf16") for a in ads_np]
+    deltas = [torch.empty(P, dtype=torch.bfloat16, device="cuda") for _ in range(K)]
+    _say("case lora fused fullsize: catalog")
+    mp.mp_lora_materialize(L, recs, ads, deltas)
+    tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
+    sumsq = torch.empty(G * K, dtype=torch.float32, device="cuda")
+    mp.mp_index_ties(L, base, deltas, 0.2, tau, sumsq=sumsq, delta=True)
+    mask = torch.empty(G, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(base)
+    out2 = torch.empty_like(base)
+    names = [nm for nm, _ in spec.tensors]
+    toff = np.concatenate([[0], np.cumsum(lay.numel)]).astype(np.int64)
+    nblk = [(int(x) + lay.block_elems - 1) // lay.block_elems for x in lay.numel]
+    g0s = np.concatenate([[0], np.cumsum(nblk)]).astype(np.int64)
+    by_t = {r[0]: r for r in recs}
+    picks = [names.index(x) for x in ("layers.0.self_attn.q_proj.weight", "layers.13.mlp.down_proj.weight",
+                                      "layers.27.self_attn.v_proj.weight", "layers.27.mlp.up_proj.weight",
+                                      "norm.weight")]
+    tau_h = tau.cpu().numpy().view(np.uint32).reshape(G, K)
+    for f in (0.25, 1.0):
+        _say(f"case lora fused fullsize B={f}")
+        mp.mp_plan(L, K, sumsq, [1.0] * K, int(f * P * 2 * K), mask, flags=mp.MP_PLAN_SKIP_ZERO)
+        mp.mp_lora_merge_ties_tau(L, base, recs, ads, mask, tau, 1.0, out)
+        mp.mp_lora_materialize(L, recs, ads, deltas, mask=mask)
+        mp.mp_merge_ties_tau(L, base, deltas, mask, tau, 1.0, out2, delta=True)
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), out2.view(torch.int16)), "fused and two-call outputs differ"
+        mask_h = mask.cpu().numpy().view(np.uint32)
+        for t in picks:
+            a, b = int(toff[t]), int(toff[t + 1])
+            sub = oracle.Blocks([b - a], lay.block_elems)
+            b_np = to_host(base[a:b])
+            if t in by_t:
+                _, rows, cols, r, a_off, b_off, sc = by_t[t]
+                d_t = [oracle.lora_delta("bf16", rows, cols, ads_np[i][a_off:a_off + r * cols].reshape(r, cols),
+                                         ads_np[i][b_off:b_off + rows * r].reshape(rows, r), sc) for i in range(K)]
+            else:
+                d_t = [np.zeros(b - a, np.uint16) for _ in range(K)]
+            g0, g1 = int(g0s[t]), int(g0s[t + 1])
+            tau_t = oracle.ties_thresholds(sub, "bf16", b_np, d_t, 0.2, delta=True)
+            assert np.array_equal(tau_h[g0:g1], tau_t), f"{names[t]}: thresholds differ from the oracle's"
+            want = oracle.merge_ties_tau(sub, "bf16", b_np, d_t, mask_h[g0:g1], tau_t, 1.0, delta=True)
+            got = to_host(out[a:b])
+            assert np.array_equal(got, want), f"{names[t]} B={f}: {int((got != want).sum())} elements differ"
