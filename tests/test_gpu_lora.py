@@ -541,3 +541,59 @@ def test_lora_fused_fullsize_qwen_layout(mp):
             want = oracle.merge_ties_tau(sub, "bf16", b_np, d_t, mask_h[g0:g1], tau_t, 1.0, delta=True)
             got = to_host(out[a:b])
             assert np.array_equal(got, want), f"{names[t]} B={f}: {int((got != want).sum())} elements differ"
+
+
+def test_lora_fused_two_streams_and_workspace_cap(mp):
+    # Two fused merges with one layout and record set but different adapters,
+    # issued on two streams with no synchronisation between them: they share
+    # the table's operand-order copies, so the second call's copy must wait
+    # for the first call's merge.  Then a workspace cap: MP_E_NOMEM before
+    # anything is enqueued, the output untouched.
+    import torch
+    spec = _awkward("bf16")
+    lay = spec.layout
+    K = 3
+    recs, n = lora_records(spec, 16, 0.5, targets=_fused_targets("bf16"))
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    L = mp.Layout(lay.numel, lay.block_elems, lay.dtype_code)
+    base_np, _ = make_family(spec, K=1, seed=51)
+    base_d = to_dev(base_np, "bf16")
+    rng = np.random.default_rng(51)
+    cases = []
+    for j in range(2):
+        ads = make_lora_adapters(n, K, "bf16", seed=60 + j, grid=True)
+        d_full = oracle.lora_materialize(blocks, "bf16", lay.numel, recs, ads)
+        tau = oracle.ties_thresholds(blocks, "bf16", base_np, d_full, 0.2, delta=True)
+        mask = rng.integers(0, 8, blocks.G).astype(np.uint32)
+        want = oracle.merge_ties_tau(blocks, "bf16", base_np, d_full, mask, tau, 1.0, delta=True)
+        cases.append(([to_dev(a, "bf16") for a in ads],
+                      torch.from_numpy(mask.view(np.int32)).cuda(),
+                      torch.from_numpy(np.ascontiguousarray(tau, np.uint32).reshape(-1).view(np.int32)).cuda(),
+                      torch.empty_like(base_d), want))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    _say("case lora fused two streams")
+    for (ads_d, m_d, t_d, out, _), st in zip(cases, streams):
+        mp.mp_lora_merge_ties_tau(L, base_d, recs, ads_d, m_d, t_d, 1.0, out, stream=st)
+    torch.cuda.synchronize()
+    for j, (_, _, _, out, want) in enumerate(cases):
+        got = to_host(out)
+        assert np.array_equal(got, want), f"stream {j}: {int((got != want).sum())} elements differ"
+    _say("case lora fused workspace cap")
+    ads_d, m_d, t_d, _, want = cases[0]
+    try:
+        mp.mp_release()
+        mp.mp_set_workspace_limit(1)
+        out = torch.full_like(base_d, 3.0)
+        before = out.clone()
+        with pytest.raises(mp.MPError) as ei:
+            mp.mp_lora_merge_ties_tau(L, base_d, recs, ads_d, m_d, t_d, 1.0, out)
+        assert ei.value.code == mp.MP_E_NOMEM
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), before.view(torch.int16))
+        mp.mp_set_workspace_limit(0)
+        mp.mp_lora_merge_ties_tau(L, base_d, recs, ads_d, m_d, t_d, 1.0, out)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(out), want)
+    finally:
+        mp.mp_set_workspace_limit(0)
