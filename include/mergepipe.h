@@ -338,12 +338,15 @@ typedef struct mp_lora_tensor {
  * MP_E_ARG for an invalid layout, K, record, NULL array, undersized or
  * non-device buffer, or overlap (checked before anything is enqueued);
  * MP_E_UNSUPPORTED for tensors of 2^32 or more elements; MP_E_NOMEM or
- * MP_E_HIP from the table upload or the launch.  Records are validated and
- * their device table is cached per (device, layout, records) until
- * mp_release; with a mask the call also fills that table's row lists (the
- * rows meeting a selected block), so a masked call's stream first waits for
- * the previous masked call with the same layout and records, on whatever
- * stream it ran.  Asynchronous on `stream`. */
+ * MP_E_HIP from the table upload, the table's scratch or the launch.
+ * Records are validated and their device table is cached per (device,
+ * layout, records) until mp_release.  The table also holds scratch: with a
+ * mask, the row lists (the rows meeting a selected block); without one, when
+ * every adapted tensor's rows are whole 16-byte chunks, an operand-order copy
+ * of the adapters (K x about 2 x the adapter elements) that the pull runs
+ * on.  So a call's stream first waits for the previous call that used the
+ * same table's scratch (this entry point or mp_lora_merge_ties_tau), on
+ * whatever stream it ran.  Asynchronous on `stream`. */
 int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, int32_t n_lora,
                         const void* const* adapters, int32_t K, const uint32_t* mask,
                         void* const* deltas, void* stream);
@@ -363,7 +366,10 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
  * (from mp_index_ties on the deltas, or mp_ties_tensor_thresholds).
  * MP_E_UNSUPPORTED when an adapted bf16 tensor's columns are not a multiple
  * of 8 (then use the two calls); MP_E_ARG as for the two calls, or for a
- * non-finite lambda.  Asynchronous on `stream`. */
+ * non-finite lambda; MP_E_NOMEM if the operand-order copy of the adapters
+ * (kept with the record table, as for mp_lora_materialize's full pull, whose
+ * ordering across streams applies here too) does not fit the workspace cap.
+ * Asynchronous on `stream`. */
 int mp_lora_merge_ties_tau(const mp_layout* layout, const void* base, const mp_lora_tensor* loras,
                            int32_t n_lora, const void* const* adapters, int32_t K,
                            const uint32_t* mask, const uint32_t* tau, float lambda, void* out,

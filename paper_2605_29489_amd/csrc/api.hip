@@ -1177,6 +1177,32 @@ static int get_lora_table(const mp_layout* L, const BlockTable& bt, const mp_lor
     return MP_OK;
 }
 
+// The operand-order copies of a record table for K experts (grown on
+// demand), with `s` ordered after the previous call that used the table's
+// scratch (on any stream); the caller records lt->ev after its launches.
+static int lora_prep(LoraTable* lt, int K, int es, hipStream_t s, OutPtrs* prep)
+{
+    hipError_t e;
+    if (lt->ev == nullptr && (e = hipEventCreateWithFlags(&lt->ev, hipEventDisableTiming)) != hipSuccess)
+        return hip_fail(e, "hipEventCreateWithFlags");
+    if (lt->prep_k < K) {
+        if (lt->d_prep != nullptr && (e = hipEventSynchronize(lt->ev)) != hipSuccess)
+            return hip_fail(e, "hipEventSynchronize");
+        (void)ws_free_r(lt->d_prep);
+        lt->d_prep = nullptr;
+        lt->prep_k = 0;
+        if ((e = ws_malloc(&lt->d_prep, (size_t)K * lt->prep_elems * (size_t)es)) != hipSuccess)
+            return fail(MP_E_NOMEM, "adapter operand copies (%zu bytes): %s",
+                        (size_t)K * lt->prep_elems * (size_t)es, hipGetErrorString(e));
+        lt->prep_k = K;
+    }
+    for (int i = 0; i < K; ++i)
+        prep->p[i] = static_cast<char*>(lt->d_prep) + (size_t)i * lt->prep_elems * (size_t)es;
+    if ((e = hipStreamWaitEvent(s, lt->ev, 0)) != hipSuccess)
+        return hip_fail(e, "hipStreamWaitEvent");
+    return MP_OK;
+}
+
 int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, int32_t n_lora,
                         const void* const* adapters, int32_t K, const uint32_t* mask, void* const* deltas,
                         void* stream)
@@ -1258,8 +1284,14 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
         if ((e = hipStreamWaitEvent(s, lt->ev, 0)) != hipSuccess)
             return hip_fail(e, "hipStreamWaitEvent");
     }
-    e = launch_lora(*bt, *lt, ad, dl, K, mask, s);
-    if (e == hipSuccess && listed)
+    // a pull of every unit runs on the operand-order copy (the table's
+    // scratch too, ordered the same way) when rows are whole 16-byte chunks
+    const bool prepped = mask == nullptr && lt->n_tiles > 0 && lt->rows_chunked;
+    OutPtrs prep{};
+    if (prepped && (rc = lora_prep(lt, K, es, s, &prep)))
+        return rc;
+    e = launch_lora(*bt, *lt, ad, dl, K, mask, s, prepped ? &prep : nullptr);
+    if (e == hipSuccess && (listed || prepped))
         e = hipEventRecord(lt->ev, s);
     if (e != hipSuccess)
         return hip_fail(e, "adapter delta launch");
@@ -1324,27 +1356,10 @@ int mp_lora_merge_ties_tau(const mp_layout* layout, const void* base, const mp_l
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
     OutPtrs prep{};
-    if (lt->n_tiles > 0) {
-        // the operand-order copies belong to the table: calls with the same
-        // layout and records run one after the other, on whatever streams
-        if (lt->ev == nullptr && (e = hipEventCreateWithFlags(&lt->ev, hipEventDisableTiming)) != hipSuccess)
-            return hip_fail(e, "hipEventCreateWithFlags");
-        if (lt->prep_k < K) {
-            if (lt->d_prep != nullptr && (e = hipEventSynchronize(lt->ev)) != hipSuccess)
-                return hip_fail(e, "hipEventSynchronize");
-            (void)ws_free_r(lt->d_prep);
-            lt->d_prep = nullptr;
-            lt->prep_k = 0;
-            if ((e = ws_malloc(&lt->d_prep, (size_t)K * lt->prep_elems * (size_t)es)) != hipSuccess)
-                return fail(MP_E_NOMEM, "adapter operand copies (%zu bytes): %s",
-                            (size_t)K * lt->prep_elems * (size_t)es, hipGetErrorString(e));
-            lt->prep_k = K;
-        }
-        for (int i = 0; i < K; ++i)
-            prep.p[i] = static_cast<char*>(lt->d_prep) + (size_t)i * lt->prep_elems * (size_t)es;
-        if ((e = hipStreamWaitEvent(s, lt->ev, 0)) != hipSuccess)
-            return hip_fail(e, "hipStreamWaitEvent");
-    }
+    // the operand-order copies belong to the table: calls with the same
+    // layout and records run one after the other, on whatever streams
+    if (lt->n_tiles > 0 && (rc = lora_prep(lt, K, es, s, &prep)))
+        return rc;
     e = launch_lora_ties(*bt, *lt, ad, prep, K, base, mask, tau, lambda, out, s);
     if (e == hipSuccess && lt->n_tiles > 0)
         e = hipEventRecord(lt->ev, s);

@@ -779,6 +779,115 @@ __global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 6
     }
 }
 
+// The pull of every unit on the operand-order copy (the full pull the
+// catalog reads): one wave per 16 rows of a band and expert (blockIdx.y),
+// 64-column tiles with the next tile's A operands in flight, the B operands
+// held for the whole band, and the deltas stored as whole 16-byte chunks
+// through the wave's LDS strip.  The same MFMA tiles as k_lora_band, so the
+// same bits.  Workgroups past the bands write the zeros of tensors without
+// an adapter.
+template <int DT, int RM>
+__global__ __launch_bounds__(64) void k_lora_pull(const LoraDesc* __restrict__ desc, int n_desc, uint32_t n_bands,
+                                                  uint32_t bpx, ExpertPtrs prep, OutPtrs dl,
+                                                  const uint32_t* __restrict__ zero, const uint64_t* __restrict__ zoff,
+                                                  const uint32_t* __restrict__ zlen)
+{
+    using E = typename std::conditional<DT == 0, float, uint16_t>::type;
+    constexpr int KS = DT == 0 ? 4 : 16;
+    constexpr int CV = 16 / sizeof(E);
+    constexpr int NKS = RM / KS;
+    constexpr int CPR = kFN / CV;
+    constexpr int NS = 16 * CPR / 64;
+    constexpr int OSR = kFN + CV;
+    constexpr int FC = kFN / 16;
+    using AOp = typename std::conditional<DT == 0, float, short4_t>::type;
+    __shared__ __align__(16) E ow[16 * OSR];
+    const int i = blockIdx.y;
+    const int lane = threadIdx.x;
+    if (blockIdx.x >= 32u * bpx) {
+        const uint32_t g = zero[blockIdx.x - 32u * bpx];
+        uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(dl.p[i]) + zoff[g] * (uint64_t)sizeof(E));
+        const uint32_t nch = zlen[g] / (uint32_t)CV;
+        for (uint32_t c = (uint32_t)lane; c < nch; c += 64)
+            st16s(dst + c, make_uint4(0u, 0u, 0u, 0u));
+        return;
+    }
+    const uint32_t id = blockIdx.x, xcd = id & 7u, j = id >> 3;
+    const uint32_t band = xcd * bpx + (j >> 2);
+    if (band >= n_bands)
+        return;
+    const int d = __builtin_amdgcn_readfirstlane(find_desc(desc, n_desc, band));
+    const LoraDesc D = desc[d];
+    const uint32_t r0 = (band - D.tile0) * kTM + (j & 3u) * 16u;
+    const uint32_t rows = D.rows, cols = D.cols;
+    if (r0 >= rows)
+        return;
+    const uint32_t nrow = min(16u, rows - r0);
+    const uint32_t tiles = (cols + kFN - 1) / kFN;
+    const float scale = D.scale;
+    E* __restrict__ xo = static_cast<E*>(dl.p[i]) + D.toff + (uint64_t)r0 * cols;
+    const uint32_t dk = DT == 1 ? 4u * (uint32_t)(lane >> 4) : (uint32_t)(lane >> 4);
+    const E* __restrict__ pa = static_cast<const E*>(prep.p[i]) + D.at_off + (uint64_t)(lane & 15) * RM + dk;
+    const E* __restrict__ pb = static_cast<const E*>(prep.p[i]) + D.bp_off + (uint64_t)(r0 + (uint32_t)(lane & 15)) * RM + dk;
+    AOp b[NKS];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+        b[ks] = *reinterpret_cast<const AOp*>(pb + ks * KS);
+    auto load_a = [&](uint32_t n0, AOp (&a)[NKS][FC]) {
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+            for (int ct = 0; ct < FC; ++ct)
+                a[ks][ct] = *reinterpret_cast<const AOp*>(pa + (uint64_t)(n0 + ct * 16) * RM + ks * KS);
+    };
+    AOp pre[NKS][FC];
+    load_a(0u, pre);
+    const uint32_t cg = 4u * (uint32_t)(lane >> 4);
+    for (uint32_t tn = 0; tn < tiles; ++tn) {
+        const uint32_t n0 = tn * kFN;
+        AOp cur[NKS][FC];
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+            for (int ct = 0; ct < FC; ++ct)
+                cur[ks][ct] = pre[ks][ct];
+        if (tn + 1 < tiles)
+            load_a(n0 + kFN, pre);
+        float4_t acc[FC];
+#pragma unroll
+        for (int ct = 0; ct < FC; ++ct)
+            acc[ct] = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+#pragma unroll
+            for (int ct = 0; ct < FC; ++ct) {
+                if constexpr (DT == 1)
+                    acc[ct] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(cur[ks][ct], b[ks], acc[ct], 0, 0, 0);
+                else
+                    acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur[ks][ct], b[ks], acc[ct], 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int ct = 0; ct < FC; ++ct) {
+            const float y0 = scale * acc[ct][0], y1 = scale * acc[ct][1];
+            const float y2 = scale * acc[ct][2], y3 = scale * acc[ct][3];
+            E* p = &ow[(lane & 15) * OSR + ct * 16 + cg];
+            if constexpr (DT == 1)
+                *reinterpret_cast<uint2*>(p) = make_uint2(Fmt<1>::pack2(y0, y1), Fmt<1>::pack2(y2, y3));
+            else
+                *reinterpret_cast<float4*>(p) = make_float4(y0, y1, y2, y3);
+        }
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+            const int c = q * 64 + lane;
+            const uint32_t sr = (uint32_t)(c / CPR), sc = (uint32_t)((c % CPR) * CV);
+            const uint4 v = *reinterpret_cast<const uint4*>(&ow[sr * OSR + sc]);
+            if (sr < nrow && n0 + sc < cols)
+                st16s(reinterpret_cast<uint4*>(xo + (uint64_t)sr * cols + n0 + sc), v);
+        }
+    }
+}
+
 }  // namespace
 
 uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n)
@@ -788,8 +897,42 @@ uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n)
 }
 
 hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& dl, int K,
-                       const uint32_t* mask, hipStream_t s)
+                       const uint32_t* mask, hipStream_t s, const OutPtrs* prep)
 {
+    if (mask == nullptr && prep != nullptr) {
+        // the full pull on the operand-order copy
+        const uint32_t bpx = (lt.n_tiles + 7u) / 8u;
+        if (32u * bpx + lt.n_zero == 0u)
+            return hipSuccess;
+        int aligned = 1;
+        for (int i = 0; i < K && lt.n_tiles > 0; ++i)
+            if (reinterpret_cast<uintptr_t>(ad.p[i]) % 16 != 0)
+                aligned = 0;
+        const dim3 pgrid((unsigned)lt.n_desc, (unsigned)K, lt.prep_z), grid(32u * bpx + lt.n_zero, (unsigned)K);
+        ExpertPtrs pp{};
+        for (int i = 0; i < K; ++i)
+            pp.p[i] = prep->p[i];
+#define MP_LORA_PULL(DTV, RMV)                                                                                     \
+    do {                                                                                                           \
+        if (lt.n_tiles > 0)                                                                                        \
+            hipLaunchKernelGGL((k_lora_prep<DTV, RMV>), pgrid, dim3(256), 0, s, lt.d_desc, ad, *prep, aligned);    \
+        hipLaunchKernelGGL((k_lora_pull<DTV, RMV>), grid, dim3(64), 0, s, lt.d_desc, lt.n_desc, lt.n_tiles, bpx,  \
+                           pp, dl, lt.d_zero, bt.d_off, bt.d_len);                                                 \
+    } while (0)
+        if (bt.dtype == 0) {
+            if (lt.prep_rank == 16)
+                MP_LORA_PULL(0, 16);
+            else
+                MP_LORA_PULL(0, kMaxLoraRank);
+        } else {
+            if (lt.prep_rank == 16)
+                MP_LORA_PULL(1, 16);
+            else
+                MP_LORA_PULL(1, kMaxLoraRank);
+        }
+#undef MP_LORA_PULL
+        return hipGetLastError();
+    }
     if (lt.n_tiles > 0) {
         const dim3 grid((unsigned)lt.n_tiles, (unsigned)K);
         const uint32_t be = (uint32_t)bt.block_elems;

@@ -184,9 +184,11 @@ struct LoraTable {
 uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n);
 
 // Writes the selected units' deltas (all units when mask is null).  A masked
-// pull needs lt.d_rl and lt.d_rc for at least K experts.
+// pull needs lt.d_rl and lt.d_rc for at least K experts; a full pull with
+// prep (K buffers of lt.prep_elems elements, rewritten) runs on the
+// operand-order copy.
 hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& dl, int K,
-                       const uint32_t* mask, hipStream_t s);
+                       const uint32_t* mask, hipStream_t s, const OutPtrs* prep = nullptr);
 // The budgeted TIES merge from stored thresholds with every delta drawn from
 // the adapters inside the merge (no delta checkpoint).
 // prep: K device buffers of lt.prep_elems elements each, rewritten by the call.
