@@ -1261,7 +1261,11 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
         return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
-    const bool listed = mask != nullptr && lt->n_tiles > 0;
+    // with every adapted tensor's rows whole 16-byte chunks the pull runs on
+    // the operand-order copy (the table's scratch); otherwise masked pulls
+    // use row lists (scratch too); either way ordered across streams
+    const bool prepped = lt->n_tiles > 0 && lt->rows_chunked;
+    const bool listed = mask != nullptr && lt->n_tiles > 0 && !prepped;
     if (listed) {
         // the row lists of a masked pull; calls with the same layout and
         // records share them, so each call's stream first waits for the
@@ -1278,15 +1282,12 @@ int mp_lora_materialize(const mp_layout* layout, const mp_lora_tensor* loras, in
             lt->rl_k = 0;
             if ((e = ws_malloc((void**)&lt->d_rl, sizeof(uint32_t) * (size_t)K * lt->rows_total)) != hipSuccess ||
                 (e = ws_malloc((void**)&lt->d_rc, sizeof(uint32_t) * (size_t)K * (size_t)lt->n_desc)) != hipSuccess)
-                return hip_fail(e, "adapter row lists");
+                return fail(MP_E_NOMEM, "adapter row lists: %s", hipGetErrorString(e));
             lt->rl_k = K;
         }
         if ((e = hipStreamWaitEvent(s, lt->ev, 0)) != hipSuccess)
             return hip_fail(e, "hipStreamWaitEvent");
     }
-    // a pull of every unit runs on the operand-order copy (the table's
-    // scratch too, ordered the same way) when rows are whole 16-byte chunks
-    const bool prepped = mask == nullptr && lt->n_tiles > 0 && lt->rows_chunked;
     OutPtrs prep{};
     if (prepped && (rc = lora_prep(lt, K, es, s, &prep)))
         return rc;

@@ -786,11 +786,12 @@ __global__ __launch_bounds__(64, (DT == 1 && RM == 16) ? 4 : (DT == 0 && RM == 6
 // through the wave's LDS strip.  The same MFMA tiles as k_lora_band, so the
 // same bits.  Workgroups past the bands write the zeros of tensors without
 // an adapter.
-template <int DT, int RM>
+template <int DT, int RM, bool MASKED>
 __global__ __launch_bounds__(64) void k_lora_pull(const LoraDesc* __restrict__ desc, int n_desc, uint32_t n_bands,
                                                   uint32_t bpx, ExpertPtrs prep, OutPtrs dl,
                                                   const uint32_t* __restrict__ zero, const uint64_t* __restrict__ zoff,
-                                                  const uint32_t* __restrict__ zlen)
+                                                  const uint32_t* __restrict__ zlen,
+                                                  const uint32_t* __restrict__ mask, uint32_t block_elems)
 {
     using E = typename std::conditional<DT == 0, float, uint16_t>::type;
     constexpr int KS = DT == 0 ? 4 : 16;
@@ -806,6 +807,8 @@ __global__ __launch_bounds__(64) void k_lora_pull(const LoraDesc* __restrict__ d
     const int lane = threadIdx.x;
     if (blockIdx.x >= 32u * bpx) {
         const uint32_t g = zero[blockIdx.x - 32u * bpx];
+        if (MASKED && !((mask[g] >> i) & 1u))
+            return;
         uint4* dst = reinterpret_cast<uint4*>(static_cast<char*>(dl.p[i]) + zoff[g] * (uint64_t)sizeof(E));
         const uint32_t nch = zlen[g] / (uint32_t)CV;
         for (uint32_t c = (uint32_t)lane; c < nch; c += 64)
@@ -843,8 +846,48 @@ __global__ __launch_bounds__(64) void k_lora_pull(const LoraDesc* __restrict__ d
     AOp pre[NKS][FC];
     load_a(0u, pre);
     const uint32_t cg = 4u * (uint32_t)(lane >> 4);
+    // masked: the lane's chunk slots' blocks (tracked across tiles) and
+    // whether expert i is selected there
+    uint32_t lb[NS], lr[NS];
+    const uint32_t nblk = (uint32_t)(((uint64_t)rows * cols + block_elems - 1) / block_elems);
+    if (MASKED) {
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+            const int c = q * 64 + lane;
+            const uint32_t sr = (uint32_t)(c / CPR), sc = (uint32_t)((c % CPR) * CV);
+            const uint32_t e = (sr < nrow) ? (r0 + sr) * cols + sc : 0u;  // < numel < 2^32
+            lb[q] = e / block_elems;
+            lr[q] = e - lb[q] * block_elems;
+        }
+    }
     for (uint32_t tn = 0; tn < tiles; ++tn) {
         const uint32_t n0 = tn * kFN;
+        bool selq[NS];
+        if (MASKED) {
+            uint32_t any = 0u;
+#pragma unroll
+            for (int q = 0; q < NS; ++q) {
+                const int c = q * 64 + lane;
+                const uint32_t sr = (uint32_t)(c / CPR), sc = (uint32_t)((c % CPR) * CV);
+                const uint32_t w = mask[D.g0 + min(lb[q], nblk - 1u)];  // clamped into the tensor
+                selq[q] = sr < nrow && n0 + sc < cols && ((w >> i) & 1u);
+                any |= selq[q] ? 1u : 0u;
+            }
+            // the next tile's blocks
+#pragma unroll
+            for (int q = 0; q < NS; ++q) {
+                lr[q] += kFN;
+                while (lr[q] >= block_elems) {
+                    lr[q] -= block_elems;
+                    ++lb[q];
+                }
+            }
+            if (wave_or_u32(any) == 0u) {  // nothing selected in the wave's tile: no compute, no store
+                if (tn + 1 < tiles)
+                    load_a(n0 + kFN, pre);
+                continue;
+            }
+        }
         AOp cur[NKS][FC];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
@@ -882,7 +925,7 @@ __global__ __launch_bounds__(64) void k_lora_pull(const LoraDesc* __restrict__ d
             const int c = q * 64 + lane;
             const uint32_t sr = (uint32_t)(c / CPR), sc = (uint32_t)((c % CPR) * CV);
             const uint4 v = *reinterpret_cast<const uint4*>(&ow[sr * OSR + sc]);
-            if (sr < nrow && n0 + sc < cols)
+            if (MASKED ? selq[q] : (sr < nrow && n0 + sc < cols))
                 st16s(reinterpret_cast<uint4*>(xo + (uint64_t)sr * cols + n0 + sc), v);
         }
     }
@@ -899,8 +942,8 @@ uint32_t lora_bands(uint32_t rows, uint32_t cols, uint32_t* tiles_n)
 hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPtrs& ad, const OutPtrs& dl, int K,
                        const uint32_t* mask, hipStream_t s, const OutPtrs* prep)
 {
-    if (mask == nullptr && prep != nullptr) {
-        // the full pull on the operand-order copy
+    if (prep != nullptr) {
+        // the pull on the operand-order copy
         const uint32_t bpx = (lt.n_tiles + 7u) / 8u;
         if (32u * bpx + lt.n_zero == 0u)
             return hipSuccess;
@@ -909,6 +952,7 @@ hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPt
             if (reinterpret_cast<uintptr_t>(ad.p[i]) % 16 != 0)
                 aligned = 0;
         const dim3 pgrid((unsigned)lt.n_desc, (unsigned)K, lt.prep_z), grid(32u * bpx + lt.n_zero, (unsigned)K);
+        const uint32_t be = (uint32_t)bt.block_elems;
         ExpertPtrs pp{};
         for (int i = 0; i < K; ++i)
             pp.p[i] = prep->p[i];
@@ -916,8 +960,12 @@ hipError_t launch_lora(const BlockTable& bt, const LoraTable& lt, const ExpertPt
     do {                                                                                                           \
         if (lt.n_tiles > 0)                                                                                        \
             hipLaunchKernelGGL((k_lora_prep<DTV, RMV>), pgrid, dim3(256), 0, s, lt.d_desc, ad, *prep, aligned);    \
-        hipLaunchKernelGGL((k_lora_pull<DTV, RMV>), grid, dim3(64), 0, s, lt.d_desc, lt.n_desc, lt.n_tiles, bpx,  \
-                           pp, dl, lt.d_zero, bt.d_off, bt.d_len);                                                 \
+        if (mask != nullptr)                                                                                       \
+            hipLaunchKernelGGL((k_lora_pull<DTV, RMV, true>), grid, dim3(64), 0, s, lt.d_desc, lt.n_desc,          \
+                               lt.n_tiles, bpx, pp, dl, lt.d_zero, bt.d_off, bt.d_len, mask, be);                   \
+        else                                                                                                       \
+            hipLaunchKernelGGL((k_lora_pull<DTV, RMV, false>), grid, dim3(64), 0, s, lt.d_desc, lt.n_desc,         \
+                               lt.n_tiles, bpx, pp, dl, lt.d_zero, bt.d_off, bt.d_len, mask, be);                   \
     } while (0)
         if (bt.dtype == 0) {
             if (lt.prep_rank == 16)
