@@ -1,13 +1,20 @@
 // Deltas drawn from low-rank adapters (the LoRA source of Section 3's delta
 // iterator): for an adapted tensor viewed as a rows x cols row-major matrix,
-// d = scale * (B A) with A (rank x cols) and B (rows x rank), written into
-// an explicit-delta checkpoint for the selected units only.
+// d = scale * (B A) with A (rank x cols) and B (rows x rank).  Two uses:
+//   * the pull writes them into an explicit-delta checkpoint for the
+//     selected units only (k_lora_pull on an operand-order copy of the
+//     adapters made by k_lora_prep; the band kernel k_lora_band below when
+//     a bf16 tensor's rows are not whole 16-byte chunks);
+//   * the fused TIES merge (k_lora_ties, further down) folds them into the
+//     merge without writing them.
+// All compute the same 16 x 16 MFMA tiles in the same arrangement, so they
+// give the same bits.
 //
-// The contraction runs on the matrix cores.  One 256-thread workgroup takes
-// a band of 64 rows of one tensor for one expert: it stages the band's B
-// rows in LDS once, then walks the band's 128-column tiles, staging each
-// tile's A columns transposed in LDS (16-byte loads of the next tile are in
-// flight while the current one computes and stores).  Wave w owns rows
+// The band kernel.  The contraction runs on the matrix cores.  One
+// 256-thread workgroup takes a band of 64 rows of one tensor for one expert:
+// it stages the band's B rows in LDS once, then walks the band's 128-column
+// tiles, staging each tile's A columns transposed in LDS (16-byte loads of
+// the next tile are in flight while the current one computes and stores).  Wave w owns rows
 // w*16 .. w*16+15 and computes the tile transposed, D^T = A^T B^T, in eight
 // 16 x 16 MFMA tiles along the columns:
 //   MFMA rows    = output columns (operand from A)
@@ -19,7 +26,7 @@
 // zero-padded to the MFMA depth (16 for bf16, 4 for fp32).  Column tiles
 // with no selected element are neither loaded nor computed.
 //
-// A masked pull computes only the rows that hold a selected element:
+// A masked band pull computes only the rows that hold a selected element:
 // k_lora_rows lists, per tensor and expert, the rows that meet a selected
 // block, and the bands then take 64 listed rows each (bands past the list's
 // end return at once).  Selected blocks are spread over a tensor's rows, so
@@ -387,8 +394,9 @@ __global__ __launch_bounds__(256) void k_lora_zero(const uint32_t* __restrict__ 
 // k_lora_ties: one wave takes 16 rows of an adapted tensor (a quarter of a
 // 64-row band) and walks its 64-column tiles, on its own (no workgroup
 // barrier).  Per tile it issues the next tile's mask words and this tile's
-// base chunks, then for each expert selected in some block the tile meets,
-// in increasing order:
+// base chunks, then for each expert selected in some block the tile meets
+// (a wave skips the experts none of its chunks selects), in increasing
+// order:
 //   * the expert's operands and thresholds arrive from a load issued while
 //     the previous expert computed;
 //   * it computes the 16 x 64 delta tile as D^T = A^T B^T in four 16 x 16
