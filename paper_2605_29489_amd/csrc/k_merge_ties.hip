@@ -113,6 +113,7 @@ __device__ inline void load_chunks(const uint4* __restrict__ p, uint32_t nch, ui
 // of its elements (padding elements are zeros, which cannot change the k
 // largest), by levels on bits 30..20, 19..9 and 8..0.  Returns the pattern
 // (at least 1: a zero threshold keeps every nonzero delta).
+static_assert(ties::NB >= 2048, "the radix levels use 11-bit digits: a row must hold 2048 counters");
 template <int E>
 __device__ inline uint32_t block_radix_select(TiesSmem& sm, int j, const float (&dj)[E], uint32_t k, int t,
                                               int lane, int wave)

@@ -31,7 +31,7 @@ constexpr int MB = MP_TIES_MB;  // mantissa bits in a window key
 constexpr int NC = MP_TIES_NC;  // copies of each window bin (lanes spread over them)
 constexpr int KS = 23 - MB;     // pattern bits below a key
 constexpr int NBIN = 4 << MB;   // window bins: four binades
-constexpr int NB = 2048;        // words per histogram row
+constexpr int NB = NBIN * NC;    // words per histogram row
 static_assert(NBIN * NC == NB, "a histogram row holds every copy of every bin");
 static_assert(NC == 1 || NC == 2 || NC == 4 || NC == 8 || NC == 16, "bins are 16-byte aligned or fill one");
 constexpr int LG = (NC == 1) ? 2 : (NC == 2) ? 3 : (NC == 4) ? 4 : (NC == 8) ? 5 : 6;  // log2(4 NC)
@@ -336,12 +336,17 @@ __device__ inline uint32_t wave_kth_largest(char* base, int row_off, const float
         if (n <= (uint32_t)NB)
             return wave_select_list(h, n, key, c.rank, lane);
     }
-    // exact radix select over all values: bits 30..20, 19..9, 8..0
+    // exact radix select over all values, from bit 30 down in digits of WD
+    // bits (the row holds 2^WD counters): 30..20, 19..9, 8..0 for a row of
+    // 2048 words
+    constexpr int WD = (NB >= 2048) ? 11 : (NB >= 1024) ? 10 : 9;
+    constexpr int NL = (31 + WD - 1) / WD;
     uint32_t pref = 0u, r = k;
 #pragma unroll 1
-    for (int lv = 0; lv < 3; ++lv) {
-        const int sh = (lv == 0) ? 20 : ((lv == 1) ? 9 : 0);
-        const int wd = (lv == 2) ? 9 : 11;
+    for (int lv = 0; lv < NL; ++lv) {
+        const int top_bit = 31 - lv * WD;  // one past the digit's highest bit
+        const int sh = (top_bit - WD > 0) ? top_bit - WD : 0;
+        const int wd = top_bit - sh;
         wave_lds_sync();
 #pragma unroll
         for (int q = 0; q < NB / 256; ++q)
