@@ -111,19 +111,22 @@ __device__ inline void load_chunks(const uint4* __restrict__ p, uint32_t nch, ui
 
 // Whole workgroup: exact k-th largest magnitude pattern of slot j over all
 // of its elements (padding elements are zeros, which cannot change the k
-// largest), by levels on bits 30..20, 19..9 and 8..0.  Returns the pattern
-// (at least 1: a zero threshold keeps every nonzero delta).
-static_assert(ties::NB >= 2048, "the radix levels use 11-bit digits: a row must hold 2048 counters");
+// largest), by levels from bit 30 down in digits that fit the histogram row
+// (30..20, 19..9, 8..0 for 2048 counters).  Returns the pattern (at least 1:
+// a zero threshold keeps every nonzero delta).
 template <int E>
 __device__ inline uint32_t block_radix_select(TiesSmem& sm, int j, const float (&dj)[E], uint32_t k, int t,
                                               int lane, int wave)
 {
+    constexpr int WD = (ties::NB >= 2048) ? 11 : (ties::NB >= 1024) ? 10 : 9;
+    constexpr int NL = (31 + WD - 1) / WD;
     uint32_t* h = sm.h[j];
     uint32_t pref = 0u, r = k;
 #pragma unroll 1
-    for (int lv = 0; lv < 3; ++lv) {
-        const int sh = (lv == 0) ? 20 : ((lv == 1) ? 9 : 0);
-        const int wd = (lv == 2) ? 9 : 11;
+    for (int lv = 0; lv < NL; ++lv) {
+        const int top_bit = 31 - lv * WD;  // one past the digit's highest bit
+        const int sh = (top_bit - WD > 0) ? top_bit - WD : 0;
+        const int wd = top_bit - sh;
         __syncthreads();  // earlier readers of h and st are done
         for (int q = t; q < ties::NB; q += ties::NT)
             h[q] = 0u;
