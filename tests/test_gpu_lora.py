@@ -603,3 +603,39 @@ def test_lora_fused_two_streams_and_workspace_cap(mp):
         assert np.array_equal(to_host(out), want)
     finally:
         mp.mp_set_workspace_limit(0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_lora_fused_and_pulls_with_32_experts(mp, dtype):
+    # The widest expert set (K = 32: every bit of a mask word is an expert):
+    # the full and masked pulls on the operand-order copy and the fused
+    # merge, against the oracle on the dyadic grid.
+    import torch
+    spec = _awkward(dtype)
+    lay = spec.layout
+    K = 32
+    recs, n = lora_records(spec, 8, 0.5, targets=_fused_targets(dtype))
+    ads = make_lora_adapters(n, K, dtype, seed=320, grid=True)
+    base_np, _ = make_family(spec, K=1, seed=320)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    rng = np.random.default_rng(320)
+    mask = rng.integers(0, 1 << 32, blocks.G, dtype=np.uint64).astype(np.uint32)
+    mask[::7] = 0xFFFFFFFF
+    mask[3::7] = 0
+    _say(f"case lora K=32 {dtype} pulls")
+    d_full = oracle.lora_materialize(blocks, dtype, lay.numel, recs, ads)
+    _, outs = _materialize(mp, spec, recs, ads)
+    for i in (0, 17, 31):
+        assert np.array_equal(to_host(outs[i]), d_full[i]), f"full pull, expert {i}"
+    fill = [_sentinel(lay.n_params, dtype, i) for i in range(K)]
+    _, outs = _materialize(mp, spec, recs, ads, mask)
+    want = oracle.lora_materialize(blocks, dtype, lay.numel, recs, ads, mask=mask, fill=fill)
+    for i in (0, 5, 17, 31):
+        assert np.array_equal(to_host(outs[i]), want[i]), f"masked pull, expert {i}"
+    del outs
+    _say(f"case lora K=32 {dtype} fused")
+    tau = oracle.ties_thresholds(blocks, dtype, base_np, d_full, 0.3, delta=True)
+    tau_d = torch.from_numpy(np.ascontiguousarray(tau, np.uint32).reshape(-1).view(np.int32)).cuda()
+    got = _fused(mp, spec, recs, [to_dev(a, dtype) for a in ads], to_dev(base_np, dtype), mask, tau_d, 0.9, K)
+    want = oracle.merge_ties_tau(blocks, dtype, base_np, d_full, mask, tau, 0.9, delta=True)
+    assert assert_merge_equal(got, want, base_np, dtype, "fused K=32") == 0
