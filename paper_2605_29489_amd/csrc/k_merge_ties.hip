@@ -1,6 +1,13 @@
 // The TIES merge operator with the trim inside the merge (Appendix A.1:
 // trim, elect signs, average the sign-consistent entries, over the masked
 // deltas), one workgroup per block.
+//
+// Two copies of each window bin: registers (about 120 per lane: the K
+// experts' 16 deltas each) hold the kernel at four waves per SIMD either
+// way, and halving the histogram rows (33 to 17 KiB per workgroup) took the
+// merges on the Qwen2.5-1.5B-shaped family at B = 25/50/100% from 1.90 /
+// 2.71 / 4.03 ms to 1.82 / 2.61 / 3.97 ms.  A fifth wave spills the deltas.
+#define MP_TIES_NC 2
 #include "device_common.h"
 #include "merge_src.h"
 #include "mp_internal.h"
