@@ -197,8 +197,11 @@ __device__ inline void ties_deltas(TiesSmem& sm, const uint4 (&raw)[ties::GS][CP
     for (int j = 0; j < GS; ++j) {
         if (j < ns) {
 #pragma unroll
-            for (int q = 0; q < NB / (4 * NT); ++q)
-                *reinterpret_cast<uint4*>(&sm.h[j][4 * (q * NT + t)]) = make_uint4(0u, 0u, 0u, 0u);
+            for (int q = 0; q < (NB + 4 * NT - 1) / (4 * NT); ++q) {
+                const int w = 4 * (q * NT + t);
+                if (NB % (4 * NT) == 0 || w < NB)
+                    *reinterpret_cast<uint4*>(&sm.h[j][w]) = make_uint4(0u, 0u, 0u, 0u);
+            }
         }
     }
 #pragma unroll
