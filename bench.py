@@ -541,6 +541,7 @@ def run_sweep(args):
     w = [1.0 / K] * K if linear else [1.0] * K  # the plan weighs units by the merge coefficients
     stream = torch.cuda.current_stream()
     tau_t = torch.empty(G * K, dtype=torch.int32, device="cuda") if op == "ties_tensor" else None
+    blen_np = np.asarray(lay.block_lengths(), np.int64)
 
     def merge(io=False):
         if op == "avg":
@@ -596,12 +597,17 @@ def run_sweep(args):
         ms = float(np.median([timed(merge)[0] for _ in range(reps)]))
         fid = fidelity(out, m_full, blen, st["n_selected"], K * G) if args.fidelity else None
         alg = 2 * P * es + st["cost_bytes"] + 4 * G if not host else st["cost_bytes"]
-        if op == "ties_tensor":  # three digit passes, each reading every selected unit's expert and base block
-            alg += 3 * st["cost_bytes"] * (1 if dl else 2)
+        pass_bytes = 0
+        if op == "ties_tensor":  # three digit passes, each reading every selected expert block and, once, the base under it
+            m_np = mask.cpu().numpy()
+            pass_bytes = 3 * (st["cost_bytes"] + (0 if dl else int(blen_np[m_np != 0].sum()) * es))
+            alg += pass_bytes
         rows.append({"budget_frac": round(f, 4), "budget_bytes": B, "cost_bytes": st["cost_bytes"],
                      "h2d_bytes": io["h2d_bytes"], "n_selected": st["n_selected"], "plan_ms": round(plan_ms, 4),
                      "merge_ms": round(ms, 4), "merge_params_per_s": P / (ms * 1e-3),
                      ("h2d_GBps" if host else "merge_effective_GBps"): alg / (ms * 1e-3) / 1e9})
+        if op == "ties_tensor":
+            rows[-1]["threshold_pass_bytes"] = pass_bytes
         if fid is not None:
             rows[-1]["fidelity"] = fid
     step_ms = idx_ms + sum(r["plan_ms"] + r["merge_ms"] for r in rows)
@@ -631,7 +637,7 @@ def run_sweep(args):
         del dst, src
     tot_bytes = sum(r["cost_bytes"] if host else 2 * P * es + r["cost_bytes"] + 4 * G for r in rows)
     if op == "ties_tensor":
-        tot_bytes += sum(3 * r["cost_bytes"] * (1 if dl else 2) for r in rows)
+        tot_bytes += sum(r["threshold_pass_bytes"] for r in rows)
     tot_ms = sum(r["merge_ms"] for r in rows)
     achieved = tot_bytes / (tot_ms * 1e-3)
     peak = PCIE_PEAK if host else HBM_PEAK

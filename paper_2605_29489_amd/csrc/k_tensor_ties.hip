@@ -9,7 +9,10 @@
 //   k_tt_hist     one workgroup per (run of <= 16 consecutive blocks of one
 //                 tensor, expert): LDS histogram of the digit of the
 //                 elements that match the prefix fixed so far, nonzero bins
-//                 added to the pair's global histogram;
+//                 added to the pair's global histogram.  Each XCD takes a
+//                 contiguous range of (run, expert) pairs with the expert
+//                 fastest, so the K workgroups of a run read its base
+//                 blocks through one L2;
 //   k_tt_resolve  one wave per (expert, tensor) pair: the bin holding the
 //                 k-th largest fixes the digit and the remaining rank.  In
 //                 the first pass, k = 0 gives all ones (nothing kept) and
@@ -28,6 +31,10 @@ namespace {
 
 constexpr int kTT = 256;
 constexpr int kDigBins = 2048;  // 11-bit digits (the last pass uses 9 bits)
+#ifndef MP_TT_COPIES
+#define MP_TT_COPIES 2
+#endif
+constexpr int kCopies = MP_TT_COPIES;  // LDS copies of each bin: lane l adds to copy l mod kCopies
 
 __host__ __device__ inline int tt_shift(int pass) { return pass == 0 ? 20 : (pass == 1 ? 9 : 0); }
 __host__ __device__ inline int tt_width(int pass) { return pass == 2 ? 9 : 11; }
@@ -45,20 +52,26 @@ __global__ __launch_bounds__(kTT) void k_tt_hist(const void* __restrict__ base, 
                                                   const uint32_t* __restrict__ blen,
                                                   const uint32_t* __restrict__ mask,
                                                   const uint4* __restrict__ state, int T, int pass,
-                                                  uint32_t* __restrict__ hist)
+                                                  uint32_t* __restrict__ hist, uint32_t n_pairs, uint32_t per_xcd)
 {
     constexpr int V = Fmt<DT>::V;
-    __shared__ uint32_t h[kDigBins];
-    const uint4 ch = chunks[blockIdx.x];
-    const int i = blockIdx.y;
+    __shared__ uint32_t h[kDigBins * kCopies];  // h[bin * kCopies + copy]
+    // workgroup id -> (run, expert): XCD x = id mod 8 takes pairs
+    // x*per_xcd .. in order
+    const uint32_t pr = (blockIdx.x & 7u) * per_xcd + (blockIdx.x >> 3);
+    if (pr >= n_pairs)
+        return;
+    const uint4 ch = chunks[pr / (uint32_t)K];
+    const int i = (int)(pr % (uint32_t)K);
     const uint32_t t = ch.z;
     const uint4 st = state[(size_t)i * T + t];
     if (st.z != 0u)  // this pair's threshold is already known
         return;
     const int tid = threadIdx.x;
-    for (int q = tid; q < kDigBins; q += kTT)
+    for (int q = tid; q < kDigBins * kCopies; q += kTT)
         h[q] = 0u;
     __syncthreads();
+    const uint32_t cp = (uint32_t)(tid % kCopies);
     const int sh = tt_shift(pass), wd = tt_width(pass);
     const uint32_t dmask = (1u << wd) - 1u;
     const int hsh = sh + wd;  // the bits above the digit must match the prefix
@@ -70,25 +83,44 @@ __global__ __launch_bounds__(kTT) void k_tt_hist(const void* __restrict__ base, 
         const uint32_t nch = blen[g] / V;
         const uint4* pe = chunk_ptr(ex.p[i], off, Fmt<DT>::esize);
         const uint4* pb = chunk_ptr(base, off, Fmt<DT>::esize);
-        for (uint32_t c = tid; c < nch; c += kTT) {
-            float fe[V], fb[V];
-            Fmt<DT>::unpack(pe[c], fe);
-            if (!DELTA)
-                Fmt<DT>::unpack(pb[c], fb);
+        // two chunks per thread in flight (a 4096-element bf16 block is
+        // exactly two)
+        for (uint32_t c0 = tid; c0 < nch; c0 += 2 * kTT) {
+            uint4 re[2], rb[2];
 #pragma unroll
-            for (int v = 0; v < V; ++v) {
-                const float d = DELTA ? fe[v] : fe[v] - fb[v];
-                const uint32_t mg = __float_as_uint(d) & 0x7fffffffu;
-                if (pass == 0 || (mg >> hsh) == prefix)
-                    atomicAdd(&h[(mg >> sh) & dmask], 1u);
+            for (int u = 0; u < 2; ++u) {
+                const uint32_t c = c0 + (uint32_t)(u * kTT);
+                re[u] = c < nch ? ld16s(pe + c) : make_uint4(0u, 0u, 0u, 0u);
+                rb[u] = (!DELTA && c < nch) ? pb[c] : make_uint4(0u, 0u, 0u, 0u);  // cached: the run's other experts read it too
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                if (c0 + (uint32_t)(u * kTT) >= nch)
+                    continue;
+                float fe[V], fb[V];
+                Fmt<DT>::unpack(re[u], fe);
+                if (!DELTA)
+                    Fmt<DT>::unpack(rb[u], fb);
+#pragma unroll
+                for (int v = 0; v < V; ++v) {
+                    const float d = DELTA ? fe[v] : fe[v] - fb[v];
+                    const uint32_t mg = __float_as_uint(d) & 0x7fffffffu;
+                    if (pass == 0 || (mg >> hsh) == prefix)
+                        atomicAdd(&h[((mg >> sh) & dmask) * kCopies + cp], 1u);
+                }
             }
         }
     }
     __syncthreads();
     uint32_t* out = hist + ((size_t)i * T + t) * kDigBins;
-    for (int q = tid; q < kDigBins; q += kTT)
-        if (h[q] != 0u)
-            atomicAdd(&out[q], h[q]);
+    for (int q = tid; q < kDigBins; q += kTT) {
+        uint32_t v = 0u;
+#pragma unroll
+        for (int c = 0; c < kCopies; ++c)
+            v += h[q * kCopies + c];
+        if (v != 0u)
+            atomicAdd(&out[q], v);
+    }
 }
 
 __global__ __launch_bounds__(kTT) void k_tt_resolve(uint4* __restrict__ state, const uint32_t* __restrict__ hist,
@@ -200,13 +232,14 @@ hipError_t launch_ties_tensor(const BlockTable& bt, const void* base, const Expe
     uint32_t* err = reinterpret_cast<uint32_t*>(state + pairs);
     hipLaunchKernelGGL(k_tt_zero, dim3((unsigned)std::min<int64_t>((pairs * 4 + 4 + kTT - 1) / kTT, 1024)), dim3(kTT),
                        0, s, reinterpret_cast<uint32_t*>(state), pairs * 4 + 4);
-    const dim3 hgrid((unsigned)bt.n_chunks, (unsigned)K);
+    const uint32_t n_pairs = (uint32_t)(bt.n_chunks * K), per_xcd = (n_pairs + 7u) / 8u;
+    const dim3 hgrid(8u * per_xcd);
     for (int pass = 0; pass < 3; ++pass) {
         hipLaunchKernelGGL(k_tt_zero, dim3((unsigned)std::min<int64_t>((nh + kTT - 1) / kTT, 2048)), dim3(kTT), 0, s,
                            hist, nh);
         auto go = [&](auto kern) {
             hipLaunchKernelGGL(kern, hgrid, dim3(kTT), 0, s, base, ex, K, bt.d_chunk, bt.d_off, bt.d_len, mask, state,
-                               T, pass, hist);
+                               T, pass, hist, n_pairs, per_xcd);
         };
         if (bt.dtype == 0)
             delta ? go(k_tt_hist<0, true>) : go(k_tt_hist<0, false>);
