@@ -31,10 +31,16 @@ namespace {
 
 constexpr int kTT = 256;
 constexpr int kDigBins = 2048;  // 11-bit digits (the last pass uses 9 bits)
-#ifndef MP_TT_COPIES
-#define MP_TT_COPIES 2
-#endif
-constexpr int kCopies = MP_TT_COPIES;  // LDS copies of each bin: lane l adds to copy l mod kCopies
+// Digit-pass workgroups: the first pass counts every element, and equal
+// top digits are common, so its histogram has four copies of each bin
+// (lane l adds to copy l mod 4) in 512-thread workgroups (32 KiB of LDS, 32
+// waves per CU); later passes count only the prefix's elements, with two
+// copies in 256-thread workgroups.  On the Qwen2.5-1.5B-shaped family at
+// B = 25/50/100%, thresholds and merge: 4.29-4.34 / 6.51-6.55 / 11.07-11.22
+// ms; 4.14 / 6.42 / 12.32 ms with the later passes' form throughout, 4.39 /
+// 6.52 / 10.92 ms with the first's.
+constexpr int kTH0 = 512, kCop0 = 4;
+constexpr int kTH = 256, kCop = 2;
 
 __host__ __device__ inline int tt_shift(int pass) { return pass == 0 ? 20 : (pass == 1 ? 9 : 0); }
 __host__ __device__ inline int tt_width(int pass) { return pass == 2 ? 9 : 11; }
@@ -45,8 +51,8 @@ __global__ __launch_bounds__(kTT) void k_tt_zero(uint32_t* __restrict__ p, int64
         p[q] = 0u;
 }
 
-template <int DT, bool DELTA>
-__global__ __launch_bounds__(kTT) void k_tt_hist(const void* __restrict__ base, ExpertPtrs ex, int K,
+template <int DT, bool DELTA, int kTH, int kCopies>
+__global__ __launch_bounds__(kTH) void k_tt_hist(const void* __restrict__ base, ExpertPtrs ex, int K,
                                                   const uint4* __restrict__ chunks,
                                                   const uint64_t* __restrict__ boff,
                                                   const uint32_t* __restrict__ blen,
@@ -55,7 +61,8 @@ __global__ __launch_bounds__(kTT) void k_tt_hist(const void* __restrict__ base, 
                                                   uint32_t* __restrict__ hist, uint32_t n_pairs, uint32_t per_xcd)
 {
     constexpr int V = Fmt<DT>::V;
-    __shared__ uint32_t h[kDigBins * kCopies];  // h[bin * kCopies + copy]
+    __shared__ __align__(16) uint32_t h[kDigBins * kCopies];  // h[bin * kCopies + copy]
+    static_assert(kCopies == 1 || kCopies == 2 || kCopies == 4, "a bin's copies are one LDS read");
     // workgroup id -> (run, expert): XCD x = id mod 8 takes pairs
     // x*per_xcd .. in order
     const uint32_t pr = (blockIdx.x & 7u) * per_xcd + (blockIdx.x >> 3);
@@ -68,8 +75,12 @@ __global__ __launch_bounds__(kTT) void k_tt_hist(const void* __restrict__ base, 
     if (st.z != 0u)  // this pair's threshold is already known
         return;
     const int tid = threadIdx.x;
-    for (int q = tid; q < kDigBins * kCopies; q += kTT)
-        h[q] = 0u;
+    // nothing to count when the expert has no selected block in the run
+    static_assert(kChunkBlocks <= kTH, "a thread per block of a run");
+    if (!__syncthreads_or(tid < (int)(ch.y - ch.x) && ((mask[ch.x + (uint32_t)tid] >> i) & 1u)))
+        return;
+    for (int q = tid; q < kDigBins * kCopies / 4; q += kTH)
+        reinterpret_cast<uint4*>(h)[q] = make_uint4(0u, 0u, 0u, 0u);
     __syncthreads();
     const uint32_t cp = (uint32_t)(tid % kCopies);
     const int sh = tt_shift(pass), wd = tt_width(pass);
@@ -85,17 +96,17 @@ __global__ __launch_bounds__(kTT) void k_tt_hist(const void* __restrict__ base, 
         const uint4* pb = chunk_ptr(base, off, Fmt<DT>::esize);
         // two chunks per thread in flight (a 4096-element bf16 block is
         // exactly two)
-        for (uint32_t c0 = tid; c0 < nch; c0 += 2 * kTT) {
+        for (uint32_t c0 = tid; c0 < nch; c0 += 2 * kTH) {
             uint4 re[2], rb[2];
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
-                const uint32_t c = c0 + (uint32_t)(u * kTT);
+                const uint32_t c = c0 + (uint32_t)(u * kTH);
                 re[u] = c < nch ? ld16s(pe + c) : make_uint4(0u, 0u, 0u, 0u);
                 rb[u] = (!DELTA && c < nch) ? pb[c] : make_uint4(0u, 0u, 0u, 0u);  // cached: the run's other experts read it too
             }
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
-                if (c0 + (uint32_t)(u * kTT) >= nch)
+                if (c0 + (uint32_t)(u * kTH) >= nch)
                     continue;
                 float fe[V], fb[V];
                 Fmt<DT>::unpack(re[u], fe);
@@ -113,11 +124,17 @@ __global__ __launch_bounds__(kTT) void k_tt_hist(const void* __restrict__ base, 
     }
     __syncthreads();
     uint32_t* out = hist + ((size_t)i * T + t) * kDigBins;
-    for (int q = tid; q < kDigBins; q += kTT) {
-        uint32_t v = 0u;
-#pragma unroll
-        for (int c = 0; c < kCopies; ++c)
-            v += h[q * kCopies + c];
+    for (int q = tid; q < kDigBins; q += kTH) {
+        uint32_t v;
+        if constexpr (kCopies == 4) {
+            const uint4 w = reinterpret_cast<const uint4*>(h)[q];
+            v = w.x + w.y + w.z + w.w;
+        } else if constexpr (kCopies == 2) {
+            const uint2 w = reinterpret_cast<const uint2*>(h)[q];
+            v = w.x + w.y;
+        } else {
+            v = h[q];
+        }
         if (v != 0u)
             atomicAdd(&out[q], v);
     }
@@ -237,14 +254,21 @@ hipError_t launch_ties_tensor(const BlockTable& bt, const void* base, const Expe
     for (int pass = 0; pass < 3; ++pass) {
         hipLaunchKernelGGL(k_tt_zero, dim3((unsigned)std::min<int64_t>((nh + kTT - 1) / kTT, 2048)), dim3(kTT), 0, s,
                            hist, nh);
-        auto go = [&](auto kern) {
-            hipLaunchKernelGGL(kern, hgrid, dim3(kTT), 0, s, base, ex, K, bt.d_chunk, bt.d_off, bt.d_len, mask, state,
+        auto go = [&](auto kern, int nth) {
+            hipLaunchKernelGGL(kern, hgrid, dim3(nth), 0, s, base, ex, K, bt.d_chunk, bt.d_off, bt.d_len, mask, state,
                                T, pass, hist, n_pairs, per_xcd);
         };
-        if (bt.dtype == 0)
-            delta ? go(k_tt_hist<0, true>) : go(k_tt_hist<0, false>);
-        else
-            delta ? go(k_tt_hist<1, true>) : go(k_tt_hist<1, false>);
+        if (pass == 0) {
+            if (bt.dtype == 0)
+                delta ? go(k_tt_hist<0, true, kTH0, kCop0>, kTH0) : go(k_tt_hist<0, false, kTH0, kCop0>, kTH0);
+            else
+                delta ? go(k_tt_hist<1, true, kTH0, kCop0>, kTH0) : go(k_tt_hist<1, false, kTH0, kCop0>, kTH0);
+        } else {
+            if (bt.dtype == 0)
+                delta ? go(k_tt_hist<0, true, kTH, kCop>, kTH) : go(k_tt_hist<0, false, kTH, kCop>, kTH);
+            else
+                delta ? go(k_tt_hist<1, true, kTH, kCop>, kTH) : go(k_tt_hist<1, false, kTH, kCop>, kTH);
+        }
         hipLaunchKernelGGL(k_tt_resolve, dim3((unsigned)((pairs + 3) / 4)), dim3(kTT), 0, s, state, hist,
                            bt.d_tnumel, K, T, density, pass, err, force_no_cut ? 1 : 0);
     }
