@@ -5,7 +5,8 @@ times.
   oracle runs on host copies of the whole family.  The index, the catalog
   thresholds, the mask and plan statistics at every budget, and the merged
   checkpoint of both TIES routes are compared bit for bit in full; the oracle
-  plans from its own index.
+  plans from its own index.  The tensor-scope thresholds are compared on
+  every (tensor, expert) pair for a seeded mask.
 * Llama-3-8B-shaped families cut to two layers (real hidden, FFN and vocab:
   the embedding and output head, the largest tensors, are whole):
   K = 8 AVG with experts in pinned host memory at ten budgets (merged
@@ -143,6 +144,40 @@ def test_headline_qwen15b_ties_full_compare(mp):
         _say(f"  B={f}: cost={st['cost_bytes']} selected={st['n_selected']}: both TIES routes equal in full")
         del want
     del base, exps, out, b_h, e_h
+    _free()
+
+
+def test_headline_qwen15b_tensor_ties_thresholds(mp):
+    """Tensor-scope TIES thresholds at the headline shape, in the launch
+    configuration the tensor-scope benchmark times (runs of 16 blocks, every
+    XCD's range of (run, expert) pairs): a seeded mask holding about half of
+    the units, with expert t mod K taking no block of every third tensor t;
+    every (tensor, expert) threshold compared with the oracle's."""
+    import torch
+    spec = family_spec("qwen2.5-1.5b")
+    lay = spec.layout
+    K, dens = 4, 0.2
+    L = mp.Layout(lay.numel, lay.block_elems, lay.dtype_code)
+    blocks = oracle.Blocks(lay.numel, lay.block_elems)
+    G = blocks.G
+    _say(f"case qwen2.5-1.5b tensor-scope TIES thresholds: G={G} K={K} density {dens}")
+    base, exps = make_family_device(spec, K=K, seed=0, device="cuda")
+    b_h = to_host(base)
+    e_h = [to_host(e) for e in exps]
+    rng = np.random.default_rng(41)
+    m = rng.integers(0, 1 << K, size=G, dtype=np.uint32)
+    t = np.asarray(blocks.tensor, np.int64)
+    left = t % 3 == 0
+    m[left] &= ~(np.uint32(1) << (t[left] % K).astype(np.uint32))
+    mask = torch.from_numpy(m.view(np.int32)).cuda()
+    tau = torch.empty(G * K, dtype=torch.int32, device="cuda")
+    mp.mp_ties_tensor_thresholds(L, base, exps, mask, dens, tau)
+    got = tau.cpu().numpy().view(np.uint32)
+    _say("  GPU thresholds done; oracle")
+    want = oracle.expand_tensor_thresholds(blocks, oracle.ties_tensor_thresholds(blocks, "bf16", b_h, e_h, m, dens))
+    assert np.array_equal(got, want), f"{int(np.count_nonzero(got != want))} unit thresholds differ"
+    _say(f"  thresholds equal on all {G} x {K} units")
+    del base, exps, b_h, e_h
     _free()
 
 
